@@ -1,0 +1,234 @@
+/*
+ * vfl.h - C ABI of the MI355X (gfx950) two-party publisher/subscriber
+ * split-learning training step (PubSub-VFL, arXiv 2510.12494).
+ *
+ * What one step computes (paper, Section 3 "Problem Formulation", Eqs. 1-2;
+ * Section 4.1 "System Design"; Algorithm 1):
+ *   - the passive party B runs its bottom model f_B on its features and
+ *     publishes the embedding z_B of a batch group to the embedding channel
+ *     of that group, optionally clipped per row and with Gaussian noise
+ *     added (Appendix "Differential Privacy Protocol");
+ *   - the active party A (labels + top model g) subscribes to that channel,
+ *     runs f_A, g([z_A | z_B]), the binary cross-entropy of Eq. (1), and
+ *     back-propagates; it publishes the per-row gradient w.r.t. z_B to the
+ *     gradient channel (optionally clipped and noised) and updates its and
+ *     the top model's parameters with SGD (Eq. 2);
+ *   - B fetches the gradient, back-propagates it through f_B at the
+ *     parameters that produced the embedding (the delayed parameter of
+ *     Assumption 4 and the Theorem's update rule) and updates its current
+ *     parameters with SGD.
+ * With staleness s, B may publish up to s groups ahead of the group A
+ * consumes; each party's k worker replicas process k consecutive batches of
+ * a group with the same parameters and their gradients are averaged with row
+ * weights (parameter-server step), giving one update per party per group.
+ *
+ * Memory and ownership.  The caller allocates one device workspace of
+ * vfl_workspace_size() bytes and every input buffer; the library never
+ * allocates or frees device memory.  The context owns only HIP events and
+ * host metadata.  All pointers in vfl_batch are device pointers; they must
+ * stay valid until the enqueued work that reads them has completed (for B:
+ * until vfl_bottom_backward of that group has completed, because the
+ * backward re-reads B's inputs).
+ *
+ * Streams.  Party A's work (A's bottom, top model, A's update) runs on
+ * stream_a, party B's on stream_b; the two are ordered only through the
+ * channel events (an embedding slot's "published" event and a gradient
+ * slot's "published" event).  No call blocks the host except
+ * vfl_get_param, vfl_get_message, vfl_check, vfl_get_trace and vfl_destroy.
+ *
+ * Errors.  Every call returns a vfl_status; nothing else crosses the ABI.
+ * vfl_last_error() gives a text for the last failure on a context.
+ */
+#ifndef VFL_H
+#define VFL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  VFL_OK = 0,
+  VFL_E_INVALID = 1,    /* bad argument, shape, alignment or option */
+  VFL_E_NOMEM = 2,      /* workspace smaller than vfl_workspace_size() */
+  VFL_E_HIP = 3,        /* a HIP runtime call failed (text in vfl_last_error) */
+  VFL_E_NOT_READY = 4,  /* subscribing to a group not yet published */
+  VFL_E_STALE = 5,      /* publishing would exceed the staleness bound s */
+  VFL_E_STATE = 6       /* call out of order (wrong group for this phase) */
+} vfl_status;
+
+typedef enum { VFL_F32 = 0, VFL_BF16 = 1 } vfl_dtype;
+
+typedef enum {
+  VFL_PARTY_A = 0,      /* active party: labels + top model */
+  VFL_PARTY_B = 1,      /* passive party: publishes its embeddings */
+  VFL_TOP = 2           /* the top model (held by A) */
+} vfl_party;
+
+enum { VFL_PARAM_W = 0, VFL_PARAM_B = 1, VFL_PARAM_TABLE = 2 };
+
+/* vfl_opts.flags */
+enum {
+  VFL_NOISE_EMB = 1,    /* add Gaussian noise to the published embedding */
+  VFL_NOISE_GRAD = 2,   /* add Gaussian noise to the returned gradient */
+  VFL_CLIP_EMB = 4,     /* clip each embedding row to L2 norm clip_c */
+  VFL_CLIP_GRAD = 8     /* clip each gradient row to L2 norm clip_c */
+};
+
+#define VFL_MAX_LAYERS 8
+#define VFL_MAX_REPLICAS 8
+#define VFL_MAX_STALENESS 4   /* channel capacity p = q = 5 slots */
+
+/* A party's bottom model: input = [embeddings of n_cat fields | dense].
+ * Field f's table occupies rows [f*vocab, (f+1)*vocab) of one table of
+ * n_cat*vocab rows x emb_dim float32 columns.  Layer l maps widths[l-1]
+ * (the input width for l = 0) to widths[l]; bit l of relu_mask puts a ReLU
+ * after layer l. */
+typedef struct {
+  int32_t dense_in, n_cat, vocab, emb_dim, n_layers;
+  int32_t widths[VFL_MAX_LAYERS];
+  uint32_t relu_mask;
+} vfl_bottom_spec;
+
+/* The top model on [z_A | z_B]: n_layers >= 2 fully connected layers, the
+ * last of width 1 (the logit, linear); bit j of relu_mask puts a ReLU after
+ * hidden layer j. */
+typedef struct {
+  int32_t n_layers;
+  int32_t widths[VFL_MAX_LAYERS];
+  uint32_t relu_mask;
+} vfl_top_spec;
+
+/* dtype: storage and matrix-product operand type of activations, messages
+ * and weight copies (VFL_BF16: bf16 operands, float32 accumulation, float32
+ * master parameters and updates; VFL_F32: float32 throughout).  batch: rows
+ * per replica; staleness s in [0, VFL_MAX_STALENESS]; replicas k in
+ * [1, VFL_MAX_REPLICAS]; lr: SGD step; clip_c: L2 bound C; sigma: noise
+ * multiplier (noise std = sigma * C, C = 1 when clipping is off); seed:
+ * Philox4x32-10 key (low word, high word). */
+typedef struct {
+  vfl_dtype dtype;
+  int32_t batch, staleness, replicas;
+  float lr, clip_c, sigma;
+  uint64_t seed;
+  uint32_t flags;
+} vfl_opts;
+
+/* One replica's batch.  dense: [rows x ld] row-major, dtype elements (NULL
+ * when dense_in == 0; ld == 0 means dense_in; ld * element size must be a
+ * multiple of 16 bytes and dense 16-byte aligned).  ids: int32 [rows x n_cat]
+ * (per-field id in [0, vocab)).  labels: float32 [rows] in {0, 1}, party A
+ * only.  row0: global sample id of row 0 (keys the noise).  The k replicas
+ * of one call must lie back to back (replica r starts where r-1 ends, in
+ * every array and in row0), each of `batch` rows except the last. */
+typedef struct {
+  const void* dense;
+  int64_t ld;
+  const int32_t* ids;
+  const float* labels;
+  int32_t rows;
+  int64_t row0;
+} vfl_batch;
+
+typedef struct vfl_ctx vfl_ctx;
+
+/* Bytes of device workspace the configuration needs (host-only call). */
+vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                              const vfl_top_spec* top, const vfl_opts* o, size_t* bytes);
+
+/* Create a context over a caller-owned device workspace (16-byte aligned) of
+ * at least vfl_workspace_size() bytes; stream_a / stream_b are hipStream_t
+ * (NULL: the null stream).  Parameters start at zero: set them with
+ * vfl_set_param before the first step. */
+vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                      const vfl_top_spec* top, const vfl_opts* o, void* workspace,
+                      size_t bytes, void* stream_a, void* stream_b, vfl_ctx** out);
+
+/* Copy one parameter tensor in or out (float32 master copy).  party
+ * VFL_PARTY_A / VFL_PARTY_B / VFL_TOP; kind VFL_PARAM_W ([out x in]
+ * row-major), VFL_PARAM_B ([out]) or VFL_PARAM_TABLE (layer ignored).
+ * bytes must equal the tensor size.  *_on_device selects a device or host
+ * pointer.  Both calls complete (synchronise both streams) before returning. */
+vfl_status vfl_set_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kind,
+                         const void* src, size_t bytes, int32_t src_on_device);
+vfl_status vfl_get_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kind,
+                         void* dst, size_t bytes, int32_t dst_on_device);
+
+/* Bottom forward of batch group `group` for one party (enqueue only).
+ * Party B: uses B's current parameters (the version is recorded), stashes
+ * the weights and activations in the group's slot (group mod (s+1)); at most
+ * s+1 groups may be in flight (published and not yet back-propagated), else
+ * VFL_E_STALE.  Party A: group must be the next group A consumes.
+ * per_replica: n_replicas (1..k) back-to-back batches. */
+vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group,
+                              const vfl_batch* per_replica, int32_t n_replicas);
+
+/* Party B: clip + noise (when enabled) of the group's embedding into the
+ * embedding channel slot, write the slot header {group, tick, version} and
+ * record the slot's event.  Must follow vfl_bottom_forward(B, group). */
+vfl_status vfl_publish(vfl_ctx* c, int64_t group);
+
+/* Party A, after vfl_bottom_forward(A, group): wait for the group's
+ * embedding (VFL_E_NOT_READY if vfl_publish(group) was not enqueued), run the
+ * top model, the loss (mean BCE of the group's rows written to *loss_dev when
+ * loss_dev is not NULL, a device float), the top backward and the top SGD
+ * step; publish the gradient message to the group's gradient slot and
+ * record its event. */
+vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev);
+
+/* Backward + SGD of one party for `group` (after vfl_top_step(group)).
+ * Party B waits for the gradient slot's event and back-propagates with the
+ * weights and activations stashed by its forward of that group; the update
+ * goes to B's current parameters and increments B's version. */
+vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group);
+
+/* One tick t of the deterministic schedule: when n_b > 0, B's forward and
+ * publish of group t; when n_a > 0, A's forward, top step and backward of
+ * group u = t - s, then B's backward of u.  (b: group t's batches, a: group
+ * u's batches with labels.)  With this schedule B's forward of group g uses
+ * version max(0, g - s) and the update from group u is delayed by min(u, s). */
+vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a,
+                    const vfl_batch* b, int32_t n_b, float* loss_dev);
+
+/* Copy a channel slot to host memory after synchronising: which 0 = the
+ * embedding of `group`, 1 = its gradient message; [rows x width] of the
+ * context dtype (float32 or bf16 bits).  header (may be NULL) receives the
+ * slot header {group, tick, version}.  VFL_E_STATE if the slot no longer
+ * holds that group. */
+vfl_status vfl_get_message(vfl_ctx* c, int32_t which, int64_t group, void* dst,
+                           size_t bytes, int32_t header[3]);
+
+/* Integer schedule trace, one row of 7 int64 per enqueued tick/phase:
+ * {tick, group published or -1, its slot or -1, B version used by that
+ * forward or -1, group consumed or -1, its slot or -1, B version after the
+ * update or -1}.  Writes min(cap_rows, rows) rows; *rows = total. */
+vfl_status vfl_get_trace(vfl_ctx* c, int64_t* buf, size_t cap_rows, size_t* rows);
+
+/* Pure host function: the trace row of tick t of vfl_step's schedule for
+ * staleness s and n_groups groups (no context, no GPU). */
+vfl_status vfl_schedule_tick(int64_t t, int32_t s, int64_t n_groups, int64_t out[7]);
+
+/* Synchronise both streams and report the device-side channel checks: the
+ * number of times a consumer found a slot header whose group differs from
+ * the one it expected (0 when the channel is race-free). */
+vfl_status vfl_check(vfl_ctx* c, uint32_t* header_mismatches);
+
+/* Raw Philox4x32-10 words of the noise generator (enqueued on `stream`,
+ * a hipStream_t): out_dev[(r * groups + q) * 4 + i] = word i for counter
+ * (step, row0 + r, q, tag) and key (seed low word, seed high word), for
+ * r < rows, q < groups.  out_dev: device uint32 [rows * groups * 4]. */
+vfl_status vfl_philox(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0, int32_t rows,
+                      int32_t groups, uint32_t* out_dev, void* stream);
+
+const char* vfl_last_error(const vfl_ctx* c);
+
+/* Synchronise both streams and release the context's events and host state.
+ * The workspace stays the caller's. */
+vfl_status vfl_destroy(vfl_ctx* c);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VFL_H */

@@ -1,0 +1,856 @@
+// C ABI of the publisher/subscriber split-learning step (include/vfl.h).
+//
+// Host side only: it validates shapes, lays the caller's workspace out,
+// keeps the channel state machine (which group each slot holds, B's
+// parameter version, how many groups are in flight) and enqueues the
+// kernels of kernels.h on the two party streams.  Party A's work goes to
+// stream_a, party B's to stream_b; the only cross-stream edges are the
+// per-slot "embedding published" and "gradient published" events.
+//
+// Slot reuse needs no further edges: B rewrites embedding slot g mod (s+1)
+// with group g + s + 1 only after its backward of group g, which waited for
+// g's gradient event, recorded by A after A read embedding g; A rewrites
+// gradient slot u mod (s+1) with group u + s + 1 only after waiting for that
+// group's embedding event, recorded by B after its backward of group u.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/vfl.h"
+#include "kernels.h"
+
+using namespace vfl;
+
+namespace {
+
+constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
+constexpr int kLogitBlocks = 256;
+
+int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
+
+struct Layout {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    off = (off + 255) / 256 * 256;
+    size_t o = off;
+    off += bytes;
+    return o;
+  }
+};
+
+struct DwPlan { int rps = 0, splits = 1; };
+
+DwPlan dw_plan(Elt e, int R, int N, int K) {
+  DwPlan p;
+  const int RE = dw_stage_rows(e), T = dw_tile(e);
+  const int tiles = ((N + T - 1) / T) * ((K + T - 1) / T);
+  const int max_splits = std::max(1, (R + RE - 1) / RE);
+  int s = std::min(max_splits, std::max(1, (512 + tiles - 1) / tiles));
+  int rps = (R + s - 1) / s;
+  rps = (rps + RE - 1) / RE * RE;
+  p.rps = rps;
+  p.splits = (R + rps - 1) / rps;
+  return p;
+}
+
+struct Party {
+  vfl_bottom_spec spec{};
+  int L = 0, din = 0, nslots = 1;
+  int in[VFL_MAX_LAYERS]{}, out[VFL_MAX_LAYERS]{};
+  bool relu[VFL_MAX_LAYERS]{};
+  int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
+  size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{}, T = 0;
+  size_t Wq[kMaxSlots][VFL_MAX_LAYERS]{}, Wtq[kMaxSlots][VFL_MAX_LAYERS]{};
+  size_t x0[kMaxSlots]{};
+  int64_t ldx0 = 0;
+  size_t act[kMaxSlots][VFL_MAX_LAYERS]{};
+  size_t zhat[kMaxSlots]{};          // published embedding (party B)
+  size_t norm[kMaxSlots]{}, cfac[kMaxSlots]{};
+  size_t dbuf[2]{};
+  int64_t ld_delta = 0;
+  size_t gx = 0;
+  int64_t ldgx = 0;
+  DwPlan dw[VFL_MAX_LAYERS];
+  size_t part = 0, partb = 0;
+};
+
+struct Top {
+  vfl_top_spec spec{};
+  int H = 0;                          // hidden layers (n_layers - 1)
+  int in[VFL_MAX_LAYERS]{}, out[VFL_MAX_LAYERS]{};
+  bool relu[VFL_MAX_LAYERS]{};
+  int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
+  size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{};
+  size_t Wq[VFL_MAX_LAYERS]{}, Wtq[VFL_MAX_LAYERS]{};
+  size_t act[VFL_MAX_LAYERS]{};
+  DwPlan dw[VFL_MAX_LAYERS];
+  size_t logit_part = 0;
+};
+
+struct Plan {
+  Elt e = F32;
+  int s = 0, k = 1, B = 1, R = 1, dA = 0, dB = 0;
+  Party A, P;                         // P: party B (passive)
+  Top T;
+  size_t ring_g[kMaxSlots]{};
+  size_t gpre = 0;                    // float32 gradient message before clip/noise
+  size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
+  size_t part_a = 0, partb_a = 0;     // dW partials, stream A
+  size_t total = 0;
+};
+
+struct SlotState {
+  int64_t group = -1;
+  int64_t version = -1;
+  bool published = false;
+  int rows = 0;
+  const void* dense = nullptr;
+  int64_t ld = 0;
+  const int32_t* ids = nullptr;
+  RowMap rmap;
+};
+
+}  // namespace
+
+struct vfl_ctx {
+  Plan p;
+  vfl_opts o{};
+  char* ws = nullptr;
+  hipStream_t sa = nullptr, sb = nullptr;
+  hipEvent_t ev_emb[kMaxSlots]{}, ev_grad[kMaxSlots]{};
+  // B
+  int64_t b_next_fwd = 0, b_next_bwd = 0, b_version = 0, b_pub_next = 0;
+  SlotState bslot[kMaxSlots];
+  int64_t grad_group[kMaxSlots];
+  int grad_rows[kMaxSlots]{};
+  // A
+  int64_t a_next = 0;
+  int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
+  SlotState aslot;
+  const float* a_labels = nullptr;
+  std::vector<int64_t> trace;
+  std::string err;
+};
+
+namespace {
+
+template <typename T>
+T* at(vfl_ctx* c, size_t off) { return (T*)(c->ws + off); }
+
+vfl_status fail(vfl_ctx* c, vfl_status st, const std::string& msg) {
+  if (c) c->err = msg;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(c, VFL_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
+  } while (0)
+
+bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
+  if (!s) { why = "null bottom spec"; return false; }
+  if (s->n_layers < 1 || s->n_layers > VFL_MAX_LAYERS) { why = "bottom n_layers out of range"; return false; }
+  if (s->dense_in < 0 || s->n_cat < 0) { why = "negative bottom input width"; return false; }
+  if (s->n_cat > 0 && (s->vocab < 1 || s->vocab > (1 << 19) || s->emb_dim < 4 || s->emb_dim % 4 ||
+                       s->emb_dim > kMaxEmbDim)) {
+    why = "embedding dims: vocab in [1, 2^19], emb_dim a multiple of 4 in [4, 16]"; return false;
+  }
+  if (s->n_cat * (int64_t)std::max(s->emb_dim, 0) + s->dense_in < 1) { why = "empty bottom input"; return false; }
+  for (int l = 0; l < s->n_layers; ++l)
+    if (s->widths[l] < 1 || s->widths[l] > 65536) { why = "bad bottom width"; return false; }
+  return true;
+}
+
+std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* t,
+                       const vfl_opts* o, Plan& p) {
+  std::string why;
+  if (!o) return "null opts";
+  if (o->dtype != VFL_F32 && o->dtype != VFL_BF16) return "dtype must be VFL_F32 or VFL_BF16";
+  if (o->batch < 1) return "batch must be >= 1";
+  if (o->staleness < 0 || o->staleness > VFL_MAX_STALENESS) return "staleness out of [0, 4]";
+  if (o->replicas < 1 || o->replicas > VFL_MAX_REPLICAS) return "replicas out of [1, 8]";
+  if (!std::isfinite(o->lr)) return "lr not finite";
+  if ((o->flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) && !(o->clip_c > 0.f)) return "clip needs clip_c > 0";
+  if ((o->flags & (VFL_NOISE_EMB | VFL_NOISE_GRAD)) && !(o->sigma >= 0.f)) return "sigma must be >= 0";
+  if (!check_bottom(a, why) || !check_bottom(b, why)) return why;
+  if (!t || t->n_layers < 2 || t->n_layers > VFL_MAX_LAYERS) return "top needs 2..8 layers (>= 1 hidden + logit)";
+  if (t->widths[t->n_layers - 1] != 1) return "last top layer must have width 1";
+  for (int j = 0; j + 1 < t->n_layers; ++j)
+    if (t->widths[j] < 1 || t->widths[j] > 65536) return "bad top width";
+  if (t->widths[t->n_layers - 2] > 512) return "last hidden top width must be <= 512";
+  if (a->widths[a->n_layers - 1] % 8) return "party A's embedding width must be a multiple of 8";
+  if (b->widths[b->n_layers - 1] > 65536) return "bad party B width";
+  if ((int64_t)o->batch * o->replicas > (1 << 28)) return "rows per tick too large";
+
+  p.e = o->dtype == VFL_BF16 ? BF16 : F32;
+  p.s = o->staleness;
+  p.k = o->replicas;
+  p.B = o->batch;
+  p.R = o->batch * o->replicas;
+  const int es = elt_size(p.e);
+  const int64_t R = p.R;
+  Layout ly;
+
+  auto party = [&](Party& P, const vfl_bottom_spec* s, int nslots, bool passive) {
+    P.spec = *s;
+    P.L = s->n_layers;
+    P.din = s->n_cat * s->emb_dim + s->dense_in;
+    P.nslots = nslots;
+    int in = P.din, maxw = P.din;
+    for (int l = 0; l < P.L; ++l) {
+      P.in[l] = in;
+      P.out[l] = s->widths[l];
+      P.relu[l] = (s->relu_mask >> l) & 1u;
+      P.ldq[l] = ld_of(in);
+      P.ldt[l] = ld_of(P.out[l]);
+      P.W[l] = ly.take(sizeof(float) * (size_t)P.out[l] * in);
+      P.b[l] = ly.take(sizeof(float) * (size_t)P.out[l]);
+      maxw = std::max(maxw, P.out[l]);
+      in = P.out[l];
+    }
+    if (s->n_cat) P.T = ly.take(sizeof(float) * (size_t)s->n_cat * s->vocab * s->emb_dim);
+    P.ldx0 = ld_of(P.din);
+    for (int q = 0; q < nslots; ++q) {
+      for (int l = 0; l < P.L; ++l) {
+        P.Wq[q][l] = ly.take((size_t)es * P.out[l] * P.ldq[l]);
+        P.Wtq[q][l] = ly.take((size_t)es * P.in[l] * P.ldt[l]);
+        P.act[q][l] = ly.take((size_t)es * R * ld_of(P.out[l]));
+      }
+      if (s->n_cat) P.x0[q] = ly.take((size_t)es * R * P.ldx0);
+      if (passive) {
+        const bool extra = o->flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
+        P.zhat[q] = extra ? ly.take((size_t)es * R * ld_of(P.out[P.L - 1])) : P.act[q][P.L - 1];
+        if (o->flags & VFL_CLIP_EMB) {
+          P.norm[q] = ly.take(sizeof(float) * R);
+          P.cfac[q] = ly.take(sizeof(float) * R);
+        }
+      }
+    }
+    return maxw;
+  };
+
+  int maxwA = party(p.A, a, 1, false);
+  party(p.P, b, p.s + 1, true);
+  p.dA = p.A.out[p.A.L - 1];
+  p.dB = p.P.out[p.P.L - 1];
+
+  Top& T = p.T;
+  T.spec = *t;
+  T.H = t->n_layers - 1;
+  int in = p.dA + p.dB;
+  for (int j = 0; j < t->n_layers; ++j) {
+    T.in[j] = in;
+    T.out[j] = t->widths[j];
+    T.relu[j] = j < T.H && ((t->relu_mask >> j) & 1u);
+    T.ldq[j] = ld_of(in);
+    T.ldt[j] = ld_of(T.out[j]);
+    T.W[j] = ly.take(sizeof(float) * (size_t)T.out[j] * in);
+    T.b[j] = ly.take(sizeof(float) * (size_t)T.out[j]);
+    if (j < T.H) {
+      T.Wq[j] = ly.take((size_t)es * T.out[j] * T.ldq[j]);
+      T.Wtq[j] = ly.take((size_t)es * T.in[j] * T.ldt[j]);
+      T.act[j] = ly.take((size_t)es * R * ld_of(T.out[j]));
+      maxwA = std::max(maxwA, T.out[j]);
+    }
+    in = T.out[j];
+  }
+  maxwA = std::max(maxwA, p.dA + p.dB);
+  T.logit_part = ly.take(sizeof(float) * kLogitBlocks * (T.out[T.H - 1] + 2));
+
+  // delta ping-pong buffers and embedding-gradient scratch
+  p.A.ld_delta = ld_of(maxwA);
+  int maxwB = 0;
+  for (int l = 0; l < p.P.L; ++l) maxwB = std::max(maxwB, std::max(p.P.out[l], p.P.in[l]));
+  p.P.ld_delta = ld_of(maxwB);
+  for (int i = 0; i < 2; ++i) {
+    p.A.dbuf[i] = ly.take((size_t)es * R * p.A.ld_delta);
+    p.P.dbuf[i] = ly.take((size_t)es * R * p.P.ld_delta);
+  }
+  for (Party* P : {&p.A, &p.P}) {
+    if (P->spec.n_cat) {
+      P->ldgx = ld_of(P->spec.n_cat * P->spec.emb_dim);
+      P->gx = ly.take(sizeof(float) * R * P->ldgx);
+    }
+  }
+  // messages
+  for (int q = 0; q <= p.s; ++q) p.ring_g[q] = ly.take((size_t)es * R * ld_of(p.dB));
+  if (o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD)) p.gpre = ly.take(sizeof(float) * R * ld_of(p.dB));
+  p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
+
+  // weight-gradient partials (one scratch per stream, sized for its largest layer)
+  size_t need_a = 0, needb_a = 0, need_b = 0, needb_b = 0;
+  for (int l = 0; l < p.A.L; ++l) {
+    p.A.dw[l] = dw_plan(p.e, p.R, p.A.out[l], p.A.in[l]);
+    need_a = std::max(need_a, (size_t)p.A.dw[l].splits * p.A.out[l] * p.A.in[l]);
+    needb_a = std::max(needb_a, (size_t)p.A.dw[l].splits * p.A.out[l]);
+  }
+  for (int j = 0; j < T.H; ++j) {
+    T.dw[j] = dw_plan(p.e, p.R, T.out[j], T.in[j]);
+    need_a = std::max(need_a, (size_t)T.dw[j].splits * T.out[j] * T.in[j]);
+    needb_a = std::max(needb_a, (size_t)T.dw[j].splits * T.out[j]);
+  }
+  for (int l = 0; l < p.P.L; ++l) {
+    p.P.dw[l] = dw_plan(p.e, p.R, p.P.out[l], p.P.in[l]);
+    need_b = std::max(need_b, (size_t)p.P.dw[l].splits * p.P.out[l] * p.P.in[l]);
+    needb_b = std::max(needb_b, (size_t)p.P.dw[l].splits * p.P.out[l]);
+  }
+  p.part_a = ly.take(sizeof(float) * need_a);
+  p.partb_a = ly.take(sizeof(float) * needb_a);
+  p.P.part = ly.take(sizeof(float) * need_b);
+  p.P.partb = ly.take(sizeof(float) * needb_b);
+  p.total = (ly.off + 255) / 256 * 256;
+  return "";
+}
+
+// Validate k back-to-back replica batches; fills the slot description.
+vfl_status take_batches(vfl_ctx* c, const Party& P, const vfl_batch* br, int n, bool need_labels,
+                        SlotState& st) {
+  const Plan& p = c->p;
+  if (!br || n < 1 || n > p.k) return fail(c, VFL_E_INVALID, "need 1..k replica batches");
+  const int es = elt_size(p.e);
+  const int64_t ld = br[0].ld ? br[0].ld : P.spec.dense_in;
+  if (P.spec.dense_in) {
+    if (!br[0].dense) return fail(c, VFL_E_INVALID, "dense input missing");
+    if (ld < P.spec.dense_in || (!P.spec.n_cat && ((ld * es) % 16 || ((uintptr_t)br[0].dense) % 16)))
+      return fail(c, VFL_E_INVALID, "dense rows must be 16-byte aligned (ld * element size % 16 == 0)");
+  }
+  if (P.spec.n_cat && !br[0].ids) return fail(c, VFL_E_INVALID, "ids missing");
+  if (need_labels && !br[0].labels) return fail(c, VFL_E_INVALID, "labels missing");
+  int64_t off = 0;
+  st.rmap = RowMap();
+  st.rmap.n = n;
+  for (int r = 0; r < n; ++r) {
+    const vfl_batch& x = br[r];
+    if (x.rows < 1 || x.rows > p.B || (r + 1 < n && x.rows != p.B))
+      return fail(c, VFL_E_INVALID, "each replica holds `batch` rows (the last may hold fewer)");
+    if ((x.ld ? x.ld : P.spec.dense_in) != ld) return fail(c, VFL_E_INVALID, "replicas differ in ld");
+    if (r > 0) {
+      bool ok = x.row0 == br[0].row0 + off;
+      if (P.spec.dense_in) ok = ok && (const char*)x.dense == (const char*)br[0].dense + off * ld * es;
+      if (P.spec.n_cat) ok = ok && x.ids == br[0].ids + off * P.spec.n_cat;
+      if (need_labels) ok = ok && x.labels == br[0].labels + off;
+      if (!ok) return fail(c, VFL_E_INVALID, "replica batches must lie back to back");
+    }
+    st.rmap.start[r] = (int32_t)off;
+    st.rmap.row0[r] = x.row0;
+    off += x.rows;
+  }
+  st.rows = (int)off;
+  st.dense = br[0].dense;
+  st.ld = ld;
+  st.ids = br[0].ids;
+  return VFL_OK;
+}
+
+vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipStream_t st) {
+  CastJob jobs[2 * VFL_MAX_LAYERS + 2];
+  int n = 0;
+  for (int l = 0; l < P.L; ++l)
+    jobs[n++] = CastJob{at<float>(c, P.W[l]), c->ws + P.Wq[slot][l], c->ws + P.Wtq[slot][l],
+                        P.out[l], P.in[l], P.ldq[l], P.ldt[l]};
+  if (T)
+    for (int j = 0; j < T->H; ++j)
+      jobs[n++] = CastJob{at<float>(c, T->W[j]), c->ws + T->Wq[j], c->ws + T->Wtq[j],
+                          T->out[j], T->in[j], T->ldq[j], T->ldt[j]};
+  HIPCHK(launch_cast(c->p.e, jobs, n, st));
+  return VFL_OK;
+}
+
+// Party bottom forward (gather + layers) into slot `slot`.
+vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const SlotState& in,
+                                  hipStream_t st, int32_t* hdr_out, const int32_t hdr[3]) {
+  const Plan& p = c->p;
+  const int R = in.rows;
+  const void* x = in.dense;
+  int64_t ldx = in.ld;
+  if (P.spec.n_cat) {
+    GatherJob gj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
+                 in.dense, in.ld, P.spec.dense_in, c->ws + P.x0[slot], P.ldx0, R};
+    HIPCHK(launch_gather(p.e, gj, st));
+    x = c->ws + P.x0[slot];
+    ldx = P.ldx0;
+  }
+  for (int l = 0; l < P.L; ++l) {
+    GemmNT g;
+    g.A1 = l == 0 ? x : c->ws + P.act[slot][l - 1];
+    g.lda1 = l == 0 ? ldx : ld_of(P.out[l - 1]);
+    g.B = c->ws + P.Wq[slot][l];
+    g.ldb = P.ldq[l];
+    g.C1 = c->ws + P.act[slot][l];
+    g.ldc1 = ld_of(P.out[l]);
+    g.bias = at<float>(c, P.b[l]);
+    g.relu = P.relu[l];
+    g.M = R; g.N = P.out[l]; g.K = P.in[l];
+    if (l == P.L - 1 && hdr_out) {
+      g.hdr_out = hdr_out;
+      g.hdr[0] = hdr[0]; g.hdr[1] = hdr[1]; g.hdr[2] = hdr[2];
+    }
+    HIPCHK(launch_gemm_nt(p.e, g, st));
+  }
+  return VFL_OK;
+}
+
+// Backward of a party's bottom layers from delta (gradient w.r.t. the last
+// layer's pre-activation) in dbuf[cur]; SGD on the master parameters.
+vfl_status enqueue_bottom_backward(vfl_ctx* c, const Party& P, int slot, const SlotState& in,
+                                   int cur, float* part, float* partb, hipStream_t st) {
+  const Plan& p = c->p;
+  const int R = in.rows;
+  const float scale = c->o.lr / (float)R;
+  const void* x = P.spec.n_cat ? (const void*)(c->ws + P.x0[slot]) : in.dense;
+  const int64_t ldx = P.spec.n_cat ? P.ldx0 : in.ld;
+  for (int l = P.L - 1; l >= 0; --l) {
+    const void* D = c->ws + P.dbuf[cur];
+    GemmDW d;
+    d.D = D; d.ldd = P.ld_delta;
+    d.X1 = l == 0 ? x : c->ws + P.act[slot][l - 1];
+    d.ldx1 = l == 0 ? ldx : ld_of(P.out[l - 1]);
+    d.part = part; d.partb = partb;
+    d.R = R; d.N = P.out[l]; d.K = P.in[l];
+    d.rows_per_split = P.dw[l].rps;
+    d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
+    HIPCHK(launch_gemm_dw(p.e, d, st));
+    HIPCHK(launch_sgd_reduce(at<float>(c, P.W[l]), part, (int64_t)P.out[l] * P.in[l],
+                             at<float>(c, P.b[l]), partb, P.out[l], d.splits, scale, st));
+    if (l > 0) {
+      GemmNT g;
+      g.A1 = D; g.lda1 = P.ld_delta;
+      g.B = c->ws + P.Wtq[slot][l]; g.ldb = P.ldt[l];
+      g.C1 = c->ws + P.dbuf[cur ^ 1]; g.ldc1 = P.ld_delta;
+      if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
+      g.M = R; g.N = P.in[l]; g.K = P.out[l];
+      HIPCHK(launch_gemm_nt(p.e, g, st));
+      cur ^= 1;
+    } else if (P.spec.n_cat) {
+      GemmNT g;
+      g.A1 = D; g.lda1 = P.ld_delta;
+      g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
+      g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
+      g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
+      HIPCHK(launch_gemm_nt(p.e, g, st));
+      ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
+                    at<float>(c, P.gx), P.ldgx, R, scale};
+      HIPCHK(launch_scatter_sgd(sj, st));
+    }
+  }
+  return VFL_OK;
+}
+
+int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
+int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
+
+vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
+  const Plan& p = c->p;
+  if (party == VFL_PARTY_A || party == VFL_PARTY_B) {
+    const Party& P = party == VFL_PARTY_A ? p.A : p.P;
+    if (kind == VFL_PARAM_TABLE) {
+      if (!P.spec.n_cat) return fail(c, VFL_E_INVALID, "party has no embedding table");
+      off = P.T; bytes = sizeof(float) * (size_t)P.spec.n_cat * P.spec.vocab * P.spec.emb_dim;
+      return VFL_OK;
+    }
+    if (layer < 0 || layer >= P.L) return fail(c, VFL_E_INVALID, "layer out of range");
+    if (kind == VFL_PARAM_W) { off = P.W[layer]; bytes = sizeof(float) * (size_t)P.out[layer] * P.in[layer]; }
+    else if (kind == VFL_PARAM_B) { off = P.b[layer]; bytes = sizeof(float) * P.out[layer]; }
+    else return fail(c, VFL_E_INVALID, "bad parameter kind");
+    return VFL_OK;
+  }
+  if (party == VFL_TOP) {
+    const Top& T = p.T;
+    if (layer < 0 || layer > T.H) return fail(c, VFL_E_INVALID, "layer out of range");
+    if (kind == VFL_PARAM_W) { off = T.W[layer]; bytes = sizeof(float) * (size_t)T.out[layer] * T.in[layer]; }
+    else if (kind == VFL_PARAM_B) { off = T.b[layer]; bytes = sizeof(float) * T.out[layer]; }
+    else return fail(c, VFL_E_INVALID, "bad parameter kind");
+    return VFL_OK;
+  }
+  return fail(c, VFL_E_INVALID, "bad party");
+}
+
+}  // namespace
+
+extern "C" {
+
+vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                              const vfl_top_spec* top, const vfl_opts* o, size_t* bytes) {
+  if (!bytes) return VFL_E_INVALID;
+  Plan p;
+  if (!build_plan(a, b, top, o, p).empty()) return VFL_E_INVALID;
+  *bytes = p.total;
+  return VFL_OK;
+}
+
+vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* top,
+                      const vfl_opts* o, void* workspace, size_t bytes, void* stream_a,
+                      void* stream_b, vfl_ctx** out) {
+  if (!out) return VFL_E_INVALID;
+  *out = nullptr;
+  vfl_ctx* c = new vfl_ctx();
+  std::string why = build_plan(a, b, top, o, c->p);
+  if (!why.empty()) { delete c; return VFL_E_INVALID; }
+  if (!workspace || ((uintptr_t)workspace) % 256) { delete c; return VFL_E_INVALID; }
+  if (bytes < c->p.total) { delete c; return VFL_E_NOMEM; }
+  c->o = *o;
+  c->ws = (char*)workspace;
+  c->sa = (hipStream_t)stream_a;
+  c->sb = (hipStream_t)stream_b;
+  for (int q = 0; q < kMaxSlots; ++q) c->grad_group[q] = -1;
+  hipError_t e = hipSuccess;
+  for (int q = 0; q <= c->p.s && e == hipSuccess; ++q) {
+    e = hipEventCreateWithFlags(&c->ev_emb[q], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_grad[q], hipEventDisableTiming);
+  }
+  // parameters, headers and the error counter start at zero
+  if (e == hipSuccess) e = hipMemsetAsync(c->ws, 0, c->p.total, c->sa);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->sa);
+  if (e != hipSuccess) {
+    vfl_destroy(c);
+    return VFL_E_HIP;
+  }
+  *out = c;
+  return VFL_OK;
+}
+
+vfl_status vfl_set_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kind, const void* src,
+                         size_t bytes, int32_t src_on_device) {
+  if (!c || !src) return VFL_E_INVALID;
+  size_t off = 0, nb = 0;
+  vfl_status st = param_loc(c, party, layer, kind, off, nb);
+  if (st) return st;
+  if (bytes != nb) return fail(c, VFL_E_INVALID, "parameter size mismatch");
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  HIPCHK(hipMemcpy(c->ws + off, src, nb, src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice));
+  return VFL_OK;
+}
+
+vfl_status vfl_get_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kind, void* dst,
+                         size_t bytes, int32_t dst_on_device) {
+  if (!c || !dst) return VFL_E_INVALID;
+  size_t off = 0, nb = 0;
+  vfl_status st = param_loc(c, party, layer, kind, off, nb);
+  if (st) return st;
+  if (bytes != nb) return fail(c, VFL_E_INVALID, "parameter size mismatch");
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  HIPCHK(hipMemcpy(dst, c->ws + off, nb, dst_on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost));
+  return VFL_OK;
+}
+
+vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const vfl_batch* br,
+                              int32_t n) {
+  if (!c) return VFL_E_INVALID;
+  Plan& p = c->p;
+  if (party == VFL_PARTY_B) {
+    if (group != c->b_next_fwd || c->b_pub_next != group)
+      return fail(c, VFL_E_STATE, "B's forward must take the next group after publishing the last");
+    if (group - c->b_next_bwd > p.s)
+      return fail(c, VFL_E_STALE, "more than s+1 groups in flight");
+    const int slot = (int)(group % (p.s + 1));
+    SlotState st;
+    vfl_status r = take_batches(c, p.P, br, n, false, st);
+    if (r) return r;
+    st.group = group;
+    st.version = c->b_version;
+    st.published = false;
+    if ((r = enqueue_cast(c, p.P, slot, nullptr, c->sb))) return r;
+    const bool extra = c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
+    const int32_t hdr[3] = {(int32_t)group, (int32_t)(group), (int32_t)c->b_version};
+    if ((r = enqueue_bottom_forward(c, p.P, slot, st, c->sb, extra ? nullptr : hdr_ptr(c, 0, slot), hdr)))
+      return r;
+    c->bslot[slot] = st;
+    c->b_next_fwd = group + 1;
+    return VFL_OK;
+  }
+  if (party == VFL_PARTY_A) {
+    if (group != c->a_next || c->a_phase != 0)
+      return fail(c, VFL_E_STATE, "A's forward must take the next group A consumes");
+    SlotState st;
+    vfl_status r = take_batches(c, p.A, br, n, true, st);
+    if (r) return r;
+    st.group = group;
+    if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+    if ((r = enqueue_bottom_forward(c, p.A, 0, st, c->sa, nullptr, nullptr))) return r;
+    c->aslot = st;
+    c->a_labels = br[0].labels;
+    c->a_phase = 1;
+    return VFL_OK;
+  }
+  return fail(c, VFL_E_INVALID, "bad party");
+}
+
+vfl_status vfl_publish(vfl_ctx* c, int64_t group) {
+  if (!c) return VFL_E_INVALID;
+  Plan& p = c->p;
+  const int slot = (int)(group % (p.s + 1));
+  if (group != c->b_pub_next || c->b_next_fwd != group + 1 || c->bslot[slot].group != group)
+    return fail(c, VFL_E_STATE, "publish must follow B's forward of the same group");
+  SlotState& st = c->bslot[slot];
+  if (c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB)) {
+    ClipNoiseJob j{};
+    j.v = c->ws + p.P.act[slot][p.P.L - 1]; j.ldv = ld_of(p.dB); j.v_f32 = p.e == F32;
+    j.out = c->ws + p.P.zhat[slot]; j.ldo = ld_of(p.dB);
+    j.norm = p.P.norm[slot] ? at<float>(c, p.P.norm[slot]) : nullptr;
+    j.cfac = p.P.cfac[slot] ? at<float>(c, p.P.cfac[slot]) : nullptr;
+    j.R = st.rows; j.D = p.dB;
+    j.clip = (c->o.flags & VFL_CLIP_EMB) != 0; j.C = c->o.clip_c;
+    j.noise = (c->o.flags & VFL_NOISE_EMB) != 0;
+    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
+    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 0; j.rows = st.rmap;
+    j.hdr_out = hdr_ptr(c, 0, slot);
+    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)group; j.hdr[2] = (int32_t)st.version;
+    HIPCHK(launch_clip_noise(p.e, j, c->sb));
+  }
+  HIPCHK(hipEventRecord(c->ev_emb[slot], c->sb));
+  st.published = true;
+  c->b_pub_next = group + 1;
+  return VFL_OK;
+}
+
+vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
+  if (!c) return VFL_E_INVALID;
+  Plan& p = c->p;
+  if (group != c->a_next || c->a_phase != 1)
+    return fail(c, VFL_E_STATE, "top step must follow A's forward of the same group");
+  const int slot = (int)(group % (p.s + 1));
+  SlotState& bs = c->bslot[slot];
+  if (bs.group != group || !bs.published)
+    return fail(c, VFL_E_NOT_READY, "embedding of this group not published");
+  if (bs.rows != c->aslot.rows) return fail(c, VFL_E_INVALID, "A and B batches differ in rows");
+  const int R = c->aslot.rows;
+  const float scale = c->o.lr / (float)R;
+  hipStream_t st = c->sa;
+  HIPCHK(hipStreamWaitEvent(st, c->ev_emb[slot], 0));
+  const Top& T = p.T;
+  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
+  const void* zB = c->ws + p.P.zhat[slot];
+  // hidden layers
+  for (int j = 0; j < T.H; ++j) {
+    GemmNT g;
+    if (j == 0) {
+      g.A1 = zA; g.lda1 = ld_of(p.dA);
+      g.A2 = zB; g.lda2 = ld_of(p.dB); g.ksplit = p.dA;
+      g.hdr_chk = hdr_ptr(c, 0, slot); g.chk_seq = (int32_t)group; g.err = err_ptr(c);
+    } else {
+      g.A1 = c->ws + T.act[j - 1]; g.lda1 = ld_of(T.out[j - 1]);
+    }
+    g.B = c->ws + T.Wq[j]; g.ldb = T.ldq[j];
+    g.C1 = c->ws + T.act[j]; g.ldc1 = ld_of(T.out[j]);
+    g.bias = at<float>(c, T.b[j]); g.relu = T.relu[j];
+    g.M = R; g.N = T.out[j]; g.K = T.in[j];
+    HIPCHK(launch_gemm_nt(p.e, g, st));
+  }
+  // logit + BCE, logit-layer SGD
+  int cur = 0;
+  LogitJob lj{};
+  lj.H = c->ws + T.act[T.H - 1]; lj.ldh = ld_of(T.out[T.H - 1]); lj.Hd = T.out[T.H - 1]; lj.R = R;
+  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = c->a_labels;
+  lj.delta = c->ws + p.A.dbuf[cur]; lj.ldd = p.A.ld_delta; lj.relu = T.relu[T.H - 1];
+  lj.part = at<float>(c, T.logit_part);
+  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 15) / 16));
+  HIPCHK(launch_logit_bce(p.e, lj, st));
+  HIPCHK(launch_logit_sgd(lj, scale, loss_dev, st));
+  // hidden layers backward
+  float* part = at<float>(c, p.part_a);
+  float* partb = at<float>(c, p.partb_a);
+  const bool gextra = c->o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
+  for (int j = T.H - 1; j >= 0; --j) {
+    const void* D = c->ws + p.A.dbuf[cur];
+    GemmDW d;
+    d.D = D; d.ldd = p.A.ld_delta;
+    if (j == 0) {
+      d.X1 = zA; d.ldx1 = ld_of(p.dA); d.X2 = zB; d.ldx2 = ld_of(p.dB); d.ksplit = p.dA;
+    } else {
+      d.X1 = c->ws + T.act[j - 1]; d.ldx1 = ld_of(T.out[j - 1]);
+    }
+    d.part = part; d.partb = partb;
+    d.R = R; d.N = T.out[j]; d.K = T.in[j];
+    d.rows_per_split = T.dw[j].rps;
+    d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
+    HIPCHK(launch_gemm_dw(p.e, d, st));
+    HIPCHK(launch_sgd_reduce(at<float>(c, T.W[j]), part, (int64_t)T.out[j] * T.in[j],
+                             at<float>(c, T.b[j]), partb, T.out[j], d.splits, scale, st));
+    GemmNT g;
+    g.A1 = D; g.lda1 = p.A.ld_delta;
+    g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
+    g.C1 = c->ws + p.A.dbuf[cur ^ 1]; g.ldc1 = p.A.ld_delta;
+    g.M = R; g.N = T.in[j]; g.K = T.out[j];
+    if (j > 0) {
+      if (T.relu[j - 1]) { g.mask = c->ws + T.act[j - 1]; g.ldm = ld_of(T.out[j - 1]); }
+    } else {
+      if (p.A.relu[p.A.L - 1]) { g.mask = zA; g.ldm = ld_of(p.dA); }
+      g.nsplit = p.dA;
+      if (gextra) { g.C2 = c->ws + p.gpre; g.ldc2 = ld_of(p.dB); g.c2_f32 = 1; }
+      else {
+        g.C2 = c->ws + p.ring_g[slot]; g.ldc2 = ld_of(p.dB);
+        g.hdr_out = hdr_ptr(c, 1, slot);
+        g.hdr[0] = (int32_t)group; g.hdr[1] = (int32_t)(group + p.s); g.hdr[2] = (int32_t)bs.version;
+      }
+    }
+    HIPCHK(launch_gemm_nt(p.e, g, st));
+    cur ^= 1;
+  }
+  if (gextra) {
+    ClipNoiseJob j{};
+    j.v = c->ws + p.gpre; j.ldv = ld_of(p.dB); j.v_f32 = 1;
+    j.out = c->ws + p.ring_g[slot]; j.ldo = ld_of(p.dB);
+    j.R = R; j.D = p.dB;
+    j.clip = (c->o.flags & VFL_CLIP_GRAD) != 0; j.C = c->o.clip_c;
+    j.noise = (c->o.flags & VFL_NOISE_GRAD) != 0;
+    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
+    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 1; j.rows = c->aslot.rmap;
+    j.hdr_out = hdr_ptr(c, 1, slot);
+    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)(group + p.s); j.hdr[2] = (int32_t)bs.version;
+    HIPCHK(launch_clip_noise(p.e, j, st));
+  }
+  HIPCHK(hipEventRecord(c->ev_grad[slot], st));
+  c->grad_group[slot] = group;
+  c->grad_rows[slot] = R;
+  c->a_phase = 2;
+  return VFL_OK;
+}
+
+vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
+  if (!c) return VFL_E_INVALID;
+  Plan& p = c->p;
+  if (party == VFL_PARTY_A) {
+    if (group != c->a_next || c->a_phase != 2)
+      return fail(c, VFL_E_STATE, "A's backward must follow its top step");
+    // the top backward left A's cut-layer delta in dbuf[T.H & 1]
+    vfl_status r = enqueue_bottom_backward(c, p.A, 0, c->aslot, p.T.H & 1, at<float>(c, p.part_a),
+                                           at<float>(c, p.partb_a), c->sa);
+    if (r) return r;
+    c->a_next = group + 1;
+    c->a_phase = 0;
+    return VFL_OK;
+  }
+  if (party == VFL_PARTY_B) {
+    if (group != c->b_next_bwd) return fail(c, VFL_E_STATE, "B back-propagates groups in order");
+    const int slot = (int)(group % (p.s + 1));
+    if (c->grad_group[slot] != group || c->bslot[slot].group != group)
+      return fail(c, VFL_E_NOT_READY, "gradient of this group not published");
+    SlotState& st = c->bslot[slot];
+    HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
+    CutBwdJob cj{};
+    cj.g = c->ws + p.ring_g[slot]; cj.ldg = ld_of(p.dB);
+    cj.z = c->ws + p.P.act[slot][p.P.L - 1]; cj.ldz = ld_of(p.dB);
+    cj.clip = (c->o.flags & VFL_CLIP_EMB) != 0;
+    cj.norm = cj.clip ? at<float>(c, p.P.norm[slot]) : nullptr;
+    cj.cfac = cj.clip ? at<float>(c, p.P.cfac[slot]) : nullptr;
+    cj.C = c->o.clip_c; cj.relu = p.P.relu[p.P.L - 1];
+    cj.delta = c->ws + p.P.dbuf[0]; cj.ldd = p.P.ld_delta;
+    cj.R = st.rows; cj.D = p.dB;
+    cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
+    HIPCHK(launch_cut_backward(p.e, cj, c->sb));
+    vfl_status r = enqueue_bottom_backward(c, p.P, slot, st, 0, at<float>(c, p.P.part),
+                                           at<float>(c, p.P.partb), c->sb);
+    if (r) return r;
+    c->b_next_bwd = group + 1;
+    c->b_version += 1;
+    return VFL_OK;
+  }
+  return fail(c, VFL_E_INVALID, "bad party");
+}
+
+vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a, const vfl_batch* b,
+                    int32_t n_b, float* loss_dev) {
+  if (!c) return VFL_E_INVALID;
+  const int s = c->p.s;
+  int64_t row[7] = {t, -1, -1, -1, -1, -1, -1};
+  vfl_status r;
+  if (n_b > 0) {
+    row[1] = t; row[2] = t % (s + 1); row[3] = c->b_version;
+    if ((r = vfl_bottom_forward(c, VFL_PARTY_B, t, b, n_b))) return r;
+    if ((r = vfl_publish(c, t))) return r;
+  }
+  if (n_a > 0) {
+    const int64_t u = t - s;
+    if (u < 0) return fail(c, VFL_E_STATE, "no group to consume before tick s");
+    if ((r = vfl_bottom_forward(c, VFL_PARTY_A, u, a, n_a))) return r;
+    if ((r = vfl_top_step(c, u, loss_dev))) return r;
+    if ((r = vfl_bottom_backward(c, VFL_PARTY_A, u))) return r;
+    if ((r = vfl_bottom_backward(c, VFL_PARTY_B, u))) return r;
+    row[4] = u; row[5] = u % (s + 1); row[6] = c->b_version;
+  }
+  c->trace.insert(c->trace.end(), row, row + 7);
+  return VFL_OK;
+}
+
+vfl_status vfl_get_message(vfl_ctx* c, int32_t which, int64_t group, void* dst, size_t bytes,
+                           int32_t header[3]) {
+  if (!c || !dst) return VFL_E_INVALID;
+  Plan& p = c->p;
+  const int slot = (int)(group % (p.s + 1));
+  int rows = 0;
+  size_t off = 0;
+  if (which == 0) {
+    if (c->bslot[slot].group != group || !c->bslot[slot].published)
+      return fail(c, VFL_E_STATE, "embedding slot does not hold this group");
+    rows = c->bslot[slot].rows;
+    off = p.P.zhat[slot];
+  } else if (which == 1) {
+    if (c->grad_group[slot] != group) return fail(c, VFL_E_STATE, "gradient slot does not hold this group");
+    rows = c->grad_rows[slot];
+    off = p.ring_g[slot];
+  } else {
+    return fail(c, VFL_E_INVALID, "which must be 0 or 1");
+  }
+  const int es = elt_size(p.e);
+  if (bytes != (size_t)rows * p.dB * es) return fail(c, VFL_E_INVALID, "message size mismatch");
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  HIPCHK(hipMemcpy2D(dst, (size_t)p.dB * es, c->ws + off, (size_t)ld_of(p.dB) * es, (size_t)p.dB * es,
+                     rows, hipMemcpyDeviceToHost));
+  if (header) HIPCHK(hipMemcpy(header, hdr_ptr(c, which, slot), 3 * sizeof(int32_t), hipMemcpyDeviceToHost));
+  return VFL_OK;
+}
+
+vfl_status vfl_get_trace(vfl_ctx* c, int64_t* buf, size_t cap_rows, size_t* rows) {
+  if (!c) return VFL_E_INVALID;
+  const size_t n = c->trace.size() / 7;
+  if (rows) *rows = n;
+  if (buf) std::memcpy(buf, c->trace.data(), sizeof(int64_t) * 7 * std::min(n, cap_rows));
+  return VFL_OK;
+}
+
+vfl_status vfl_check(vfl_ctx* c, uint32_t* mismatches) {
+  if (!c || !mismatches) return VFL_E_INVALID;
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  int32_t v = 0;
+  HIPCHK(hipMemcpy(&v, err_ptr(c), sizeof(v), hipMemcpyDeviceToHost));
+  *mismatches = (uint32_t)v;
+  return VFL_OK;
+}
+
+vfl_status vfl_philox(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0, int32_t rows,
+                      int32_t groups, uint32_t* out_dev, void* stream) {
+  if (!out_dev || rows < 0 || groups < 0) return VFL_E_INVALID;
+  if (hipSuccess != launch_philox_words(seed, step, tag, row0, rows, groups, out_dev, (hipStream_t)stream))
+    return VFL_E_HIP;
+  return VFL_OK;
+}
+
+const char* vfl_last_error(const vfl_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+vfl_status vfl_destroy(vfl_ctx* c) {
+  if (!c) return VFL_E_INVALID;
+  vfl_status r = VFL_OK;
+  if (c->ws) {
+    if (hipStreamSynchronize(c->sa) != hipSuccess) r = VFL_E_HIP;
+    if (hipStreamSynchronize(c->sb) != hipSuccess) r = VFL_E_HIP;
+  }
+  for (int q = 0; q < kMaxSlots; ++q) {
+    if (c->ev_emb[q]) (void)hipEventDestroy(c->ev_emb[q]);
+    if (c->ev_grad[q]) (void)hipEventDestroy(c->ev_grad[q]);
+  }
+  delete c;
+  return r;
+}
+
+}  // extern "C"

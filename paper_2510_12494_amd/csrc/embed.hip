@@ -1,0 +1,182 @@
+// Embedding tables of the categorical bottoms on gfx950: the gather that
+// builds a bottom model's input [tables of n_cat fields | dense], and the
+// sparse SGD step on the tables.
+//
+// The sparse step sums, for every table row a batch touches, the gradient
+// rows of all samples that looked it up, and applies SGD once per touched
+// row.  One workgroup owns one field: it sorts the (id, row) keys of up to
+// 8192 samples in LDS (bitonic network over unique 32-bit keys, so the order
+// is deterministic), walks the sorted keys in 16-key pieces per thread,
+// and combines the pieces of each id in sample order; the table row is then
+// updated with a single rounding.  Fields own disjoint table rows, so the
+// workgroups never write the same address.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace vfl {
+namespace {
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void st1(T* p, float v) {
+  if constexpr (sizeof(T) == 4) *p = v;
+  else *p = f2bf(v);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather(GatherJob j) {
+  const int ne4 = j.E >> 2;                    // float4 chunks per field row
+  const int64_t n_emb = (int64_t)j.R * j.n_cat * ne4;
+  const int64_t total = n_emb + (int64_t)j.R * j.dense_in;
+  T* X = (T*)j.X;
+  const T* Dn = (const T*)j.dense;
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    if (i < n_emb) {
+      const int q = (int)(i % ne4);
+      const int64_t rf = i / ne4;
+      const int f = (int)(rf % j.n_cat);
+      const int r = (int)(rf / j.n_cat);
+      const int id = j.ids[(int64_t)r * j.n_cat + f];
+      const f32x4 v = *(const f32x4*)(j.T + ((int64_t)f * j.V + id) * j.E + 4 * q);
+      T* dst = X + (int64_t)r * j.ldx + f * j.E + 4 * q;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) st1<T>(dst + e, v[e]);
+    } else {
+      const int64_t k = i - n_emb;
+      const int c = (int)(k % j.dense_in);
+      const int r = (int)(k / j.dense_in);
+      X[(int64_t)r * j.ldx + j.n_cat * j.E + c] = Dn[(int64_t)r * j.ldx_in + c];
+    }
+  }
+}
+
+constexpr int kSortN = 8192;               // samples sorted per pass
+constexpr int kThreads = 512;
+constexpr int kPer = kSortN / kThreads;    // sorted keys walked per thread
+constexpr int kRowBits = 13;               // kSortN == 1 << kRowBits
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+__global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
+  __shared__ uint32_t keys[kSortN];
+  __shared__ float facc[kThreads][kMaxEmbDim], lacc[kThreads][kMaxEmbDim];
+  __shared__ uint32_t fid[kThreads], lid[kThreads];
+  __shared__ uint8_t single[kThreads];
+  const int tid = threadIdx.x;
+  const int f = blockIdx.x;
+  const int E = j.E;
+  float* table = j.T + (int64_t)f * j.V * E;
+
+  auto apply = [&](uint32_t id, const float (&s)[kMaxEmbDim]) {
+    float* row = table + (int64_t)id * E;
+    for (int e = 0; e < E; ++e) row[e] -= j.scale * s[e];
+  };
+
+  for (int c0 = 0; c0 < j.R; c0 += kSortN) {
+    const int n = min(kSortN, j.R - c0);
+    for (int i = tid; i < kSortN; i += kThreads)
+      keys[i] = i < n ? ((uint32_t)j.ids[(int64_t)(c0 + i) * j.n_cat + f] << kRowBits) | (uint32_t)i
+                      : kNone;
+    __syncthreads();
+    for (int k = 2; k <= kSortN; k <<= 1) {
+      for (int h = k >> 1; h > 0; h >>= 1) {
+        for (int i = tid; i < kSortN; i += kThreads) {
+          const int l = i ^ h;
+          if (l > i) {
+            const uint32_t a = keys[i], b = keys[l];
+            const bool up = (i & k) == 0;
+            if (up ? (a > b) : (a < b)) { keys[i] = b; keys[l] = a; }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // walk this thread's sorted keys; pieces strictly inside are complete ids
+    uint32_t cur = kNone, first = kNone;
+    float acc[kMaxEmbDim];
+    for (int e = 0; e < kMaxEmbDim; ++e) acc[e] = 0.f;
+    int pieces = 0;
+    for (int p = 0; p < kPer; ++p) {
+      const uint32_t key = keys[tid * kPer + p];
+      if (key == kNone) break;
+      const uint32_t id = key >> kRowBits;
+      const int r = (int)(key & (kSortN - 1));
+      if (id != cur) {
+        if (cur != kNone) {
+          if (pieces == 1) {
+            for (int e = 0; e < E; ++e) facc[tid][e] = acc[e];
+          } else {
+            apply(cur, acc);
+          }
+        }
+        if (pieces == 0) first = id;
+        cur = id;
+        ++pieces;
+        for (int e = 0; e < E; ++e) acc[e] = 0.f;
+      }
+      const float* g = j.G + (int64_t)(c0 + r) * j.ldg + f * E;
+      for (int e = 0; e < E; ++e) acc[e] += g[e];
+    }
+    fid[tid] = first;
+    lid[tid] = cur;
+    single[tid] = pieces == 1;
+    if (pieces >= 1) {
+      if (pieces == 1) {
+        for (int e = 0; e < E; ++e) facc[tid][e] = acc[e];
+      } else {
+        for (int e = 0; e < E; ++e) lacc[tid][e] = acc[e];
+      }
+    }
+    __syncthreads();
+    // an id's pieces lie in consecutive threads; its first piece's owner sums
+    // them in thread (= sample) order and applies the update once
+    float tot[kMaxEmbDim];
+    auto gather_from = [&](uint32_t id, int t0) {
+      for (int t = t0; t < kThreads && fid[t] == id; ++t) {
+        for (int e = 0; e < E; ++e) tot[e] += facc[t][e];
+        if (!single[t]) break;
+      }
+    };
+    if (fid[tid] != kNone && (tid == 0 || lid[tid - 1] != fid[tid])) {
+      for (int e = 0; e < E; ++e) tot[e] = facc[tid][e];
+      if (single[tid]) gather_from(fid[tid], tid + 1);
+      apply(fid[tid], tot);
+    }
+    if (lid[tid] != kNone && !single[tid]) {
+      for (int e = 0; e < E; ++e) tot[e] = lacc[tid][e];
+      gather_from(lid[tid], tid + 1);
+      apply(lid[tid], tot);
+    }
+    __syncthreads();
+  }
+}
+
+int grid_for(int64_t work, int per_block, int cap) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>((work + per_block - 1) / per_block, cap));
+}
+
+}  // namespace
+
+hipError_t launch_gather(Elt e, const GatherJob& j, hipStream_t st) {
+  const int64_t total = (int64_t)j.R * (j.n_cat * (j.E / 4) + j.dense_in);
+  const int blocks = grid_for(total, 256, 8192);
+  if (e == BF16) hipLaunchKernelGGL(k_gather<uint16_t>, dim3(blocks), dim3(256), 0, st, j);
+  else hipLaunchKernelGGL(k_gather<float>, dim3(blocks), dim3(256), 0, st, j);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st) {
+  if (j.E > kMaxEmbDim || j.V > (1 << (32 - kRowBits))) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed_sgd, dim3(j.n_cat), dim3(kThreads), 0, st, j);
+  return hipGetLastError();
+}
+
+}  // namespace vfl

@@ -1,0 +1,136 @@
+// Internal launch interface of the gfx950 kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vfl {
+
+// Element type of activations, messages and weight copies.
+enum Elt { F32 = 0, BF16 = 1 };
+
+inline int elt_size(Elt e) { return e == F32 ? 4 : 2; }
+
+// C[m][n] = epilogue( sum_k A[m][k] * B[n][k] ), A = [A1 | A2] split at
+// column ksplit (A2 may be null when ksplit >= K).  Epilogue: + bias[n],
+// optional ReLU, then columns n < nsplit go to C1 (multiplied by
+// (mask[m][n] > 0) when mask is set), columns n >= nsplit to C2 at column
+// n - nsplit (float32 when c2_f32).  All matrices row-major with leading
+// dimensions in elements; rows must be 16-byte aligned.
+struct GemmNT {
+  const void* A1 = nullptr; int64_t lda1 = 0;
+  const void* A2 = nullptr; int64_t lda2 = 0; int ksplit = 1 << 30;
+  const void* B = nullptr; int64_t ldb = 0;
+  void* C1 = nullptr; int64_t ldc1 = 0;
+  void* C2 = nullptr; int64_t ldc2 = 0; int nsplit = 1 << 30; int c2_f32 = 0;
+  const float* bias = nullptr;
+  const void* mask = nullptr; int64_t ldm = 0;
+  int relu = 0;
+  int M = 0, N = 0, K = 0;
+  // channel slot header written by block 0 (hdr_out != null) / checked by
+  // block 0 against chk_seq (mismatch -> atomic increment of *err)
+  int32_t* hdr_out = nullptr; int32_t hdr[3] = {0, 0, 0};
+  const int32_t* hdr_chk = nullptr; int32_t chk_seq = 0; int32_t* err = nullptr;
+};
+
+// Split-row weight gradient: part[s][n][k] = sum over rows r of split s of
+// D[r][n] * X[r][k] and partb[s][n] = sum of D[r][n]; X = [X1 | X2] split at
+// column ksplit.  rows_per_split is a multiple of the stage depth.
+struct GemmDW {
+  const void* D = nullptr; int64_t ldd = 0;
+  const void* X1 = nullptr; int64_t ldx1 = 0;
+  const void* X2 = nullptr; int64_t ldx2 = 0; int ksplit = 1 << 30;
+  float* part = nullptr; float* partb = nullptr;
+  int R = 0, N = 0, K = 0, rows_per_split = 0, splits = 1;
+};
+
+hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st);
+hipError_t launch_gemm_dw(Elt e, const GemmDW& g, hipStream_t st);
+int dw_stage_rows(Elt e);   // rows per pipeline stage of the dW kernel
+int dw_tile(Elt e);         // output tile edge of the dW kernel
+
+// W[i] -= scale * sum_s part[s][i]   (i < n), b likewise with partb.
+hipError_t launch_sgd_reduce(float* W, const float* part, int64_t nW, float* b,
+                             const float* partb, int nb, int splits, float scale,
+                             hipStream_t st);
+
+// Operand copies of one layer's float32 weight W [out x in]:
+// Wq [out x ldq] and Wtq [in x ldt] of element type e (ldq, ldt padded).
+struct CastJob {
+  const float* W; void* Wq; void* Wtq; int out, in; int64_t ldq, ldt;
+};
+hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
+
+// Logit layer + BCE on the last hidden activation H [R x ldh] (width Hd):
+// l = H w + b, loss_i = BCE(l, y), dl = sigmoid(l) - y; writes
+// delta [R x ldd] = dl * w * (H > 0) (element type e), and per-block partial
+// sums part[blk] = {loss, sum dl, sum_r dl * H[r][0..Hd)} (Hd + 2 floats).
+struct LogitJob {
+  const void* H; int64_t ldh; int Hd, R;
+  float* w; float* b; const float* y;
+  void* delta; int64_t ldd; int relu;
+  float* part; int blocks;
+};
+hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st);
+// Reduce the partials: w -= scale * sum dl*H, b -= scale * sum dl,
+// *loss_out = sum loss / R (loss_out may be null).
+hipError_t launch_logit_sgd(const LogitJob& j, float scale, float* loss_out, hipStream_t st);
+
+// Segments mapping a row of a tick to its global sample id (<= 8 replicas).
+struct RowMap {
+  int n = 1;
+  int32_t start[8] = {0};
+  int64_t row0[8] = {0};
+};
+
+// Per-row clip + Gaussian noise: out[r] = c_r * v[r] + std * xi(seed, step,
+// global row, col, tag), c_r = min(1, C / ||v[r]||) when clip (else 1).
+// v is element type e (or float32 when v_f32); out is element type e.
+// norm/cfac (nullable) receive ||v[r]|| and c_r.  Block 0 writes the slot
+// header.
+struct ClipNoiseJob {
+  const void* v; int64_t ldv; int v_f32;
+  void* out; int64_t ldo;
+  float* norm; float* cfac;
+  int R, D; int clip; float C; int noise; float stdv;
+  uint64_t seed; uint32_t step; uint32_t tag; RowMap rows;
+  int32_t* hdr_out; int32_t hdr[3];
+};
+hipError_t launch_clip_noise(Elt e, const ClipNoiseJob& j, hipStream_t st);
+
+// Cut-layer backward of party B: g = message row; if clipped (n_r > C):
+// g = c_r (g - u (u . g)), u = z_r / n_r; delta = g * (z > 0 when relu).
+// Block 0 checks the slot header.
+struct CutBwdJob {
+  const void* g; int64_t ldg; const void* z; int64_t ldz;
+  const float* norm; const float* cfac; int clip; float C; int relu;
+  void* delta; int64_t ldd; int R, D;
+  const int32_t* hdr_chk; int32_t chk_seq; int32_t* err;
+};
+hipError_t launch_cut_backward(Elt e, const CutBwdJob& j, hipStream_t st);
+
+// Embedding gather + concat: X[r] = [T[f*V + ids[r][f]] for f | dense[r]]
+// (float32 tables; X and dense of element type e).
+struct GatherJob {
+  const float* T; const int32_t* ids; int n_cat, V, E;
+  const void* dense; int64_t ldx_in; int dense_in;
+  void* X; int64_t ldx; int R;
+};
+hipError_t launch_gather(Elt e, const GatherJob& j, hipStream_t st);
+
+// Sparse SGD on the tables: for every row f*V + id touched by field f,
+// T[row][c] -= scale * sum over samples r with ids[r][f] == id of G[r][f*E + c]
+// (one rounding per touched row; deterministic).  E <= kMaxEmbDim,
+// V <= 2^19.
+constexpr int kMaxEmbDim = 16;
+struct ScatterJob {
+  float* T; const int32_t* ids; int n_cat, V, E;
+  const float* G; int64_t ldg; int R; float scale;
+};
+hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st);
+
+// Raw Philox4x32-10 words: out[(r * groups + q) * 4 + i] = word i of the
+// counter (step, row0 + r, q, tag) under key (seed low, seed high).
+hipError_t launch_philox_words(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0,
+                               int rows, int groups, uint32_t* out, hipStream_t st);
+
+}  // namespace vfl

@@ -1,0 +1,317 @@
+// Row-wise kernels of the split-learning step on gfx950: the logit layer +
+// binary cross-entropy (Eq. 1) with its gradient, per-row clip + Philox
+// Gaussian noise of the exchanged messages, the cut-layer backward of the
+// passive party and the weight operand copies.
+// One 64-lane wavefront owns one row at a time; row reductions (dot
+// products, norms) use cross-lane shuffles.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace vfl {
+namespace {
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float ld1(const T* p) {
+  if constexpr (sizeof(T) == 4) return *p;
+  else return bf2f(*p);
+}
+
+template <typename T>
+__device__ __forceinline__ void st1(T* p, float v) {
+  if constexpr (sizeof(T) == 4) *p = v;
+  else *p = f2bf(v);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------- logit + BCE
+constexpr int kMaxLogitCols = 512;   // hidden width handled by the logit kernel
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_logit_bce(LogitJob j) {
+  constexpr int Q = kMaxLogitCols / 64;
+  __shared__ float red[4][kMaxLogitCols + 2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const T* H = (const T*)j.H;
+  T* Dl = (T*)j.delta;
+  float wv[Q], gw[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int c = lane + 64 * q;
+    wv[q] = c < j.Hd ? j.w[c] : 0.f;
+    gw[q] = 0.f;
+  }
+  const float bias = j.b[0];
+  float gb = 0.f, lsum = 0.f;
+  const int per = (j.R + gridDim.x - 1) / gridDim.x;
+  const int rb = blockIdx.x * per, re = min(j.R, rb + per);
+  for (int r = rb + wave; r < re; r += 4) {
+    float h[Q];
+    float dot = 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int c = lane + 64 * q;
+      h[q] = c < j.Hd ? ld1<T>(H + (int64_t)r * j.ldh + c) : 0.f;
+      dot += h[q] * wv[q];
+    }
+    const float l = wave_sum(dot) + bias;
+    const float y = j.y[r];
+    const float e = expf(-fabsf(l));
+    const float loss = fmaxf(l, 0.f) - y * l + log1pf(e);
+    const float sig = l >= 0.f ? 1.f / (1.f + e) : e / (1.f + e);
+    const float dl = sig - y;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int c = lane + 64 * q;
+      if (c < j.Hd) {
+        float d = dl * wv[q];
+        if (j.relu && !(h[q] > 0.f)) d = 0.f;
+        st1<T>(Dl + (int64_t)r * j.ldd + c, d);
+        gw[q] += dl * h[q];
+      }
+    }
+    if (lane == 0) { gb += dl; lsum += loss; }
+  }
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int c = lane + 64 * q;
+    if (c < j.Hd) red[wave][2 + c] = gw[q];
+  }
+  if (lane == 0) { red[wave][0] = lsum; red[wave][1] = gb; }
+  __syncthreads();
+  for (int c = threadIdx.x; c < j.Hd + 2; c += 256)
+    j.part[(int64_t)blockIdx.x * (j.Hd + 2) + c] = red[0][c] + red[1][c] + red[2][c] + red[3][c];
+}
+
+__global__ __launch_bounds__(256) void k_logit_sgd(LogitJob j, float scale, float* loss_out) {
+  const int W = j.Hd + 2;
+  for (int c = threadIdx.x; c < W; c += blockDim.x) {
+    float s = 0.f;
+    for (int b = 0; b < j.blocks; ++b) s += j.part[(int64_t)b * W + c];
+    if (c == 0) {
+      if (loss_out) *loss_out = s / (float)j.R;
+    } else if (c == 1) {
+      j.b[0] -= scale * s;
+    } else {
+      j.w[c - 2] -= scale * s;
+    }
+  }
+}
+
+// ---------------------------------------------------- Philox4x32-10 + noise
+__device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]), lo0 = 0xD2511F53u * c[0];
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]), lo1 = 0xCD9E8D57u * c[2];
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+  }
+}
+
+__device__ __forceinline__ float word_uniform(uint32_t w) {  // (0, 1], exact
+  return (float)((w >> 8) + 1u) * 5.9604644775390625e-8f;
+}
+
+// four standard normals for columns 4q .. 4q+3 of (step, row, tag)
+__device__ __forceinline__ void gauss4(uint64_t seed, uint32_t step, uint32_t row, uint32_t q,
+                                       uint32_t tag, float (&n)[4]) {
+  uint32_t c[4] = {step, row, q, tag};
+  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const float ua = word_uniform(c[2 * p]), ub = word_uniform(c[2 * p + 1]);
+    const float rad = sqrtf(-2.f * logf(ua));
+    float s, co;
+    sincospif(2.f * ub, &s, &co);
+    n[2 * p] = rad * co;
+    n[2 * p + 1] = rad * s;
+  }
+}
+
+__device__ __forceinline__ uint32_t global_row(const RowMap& m, int r) {
+  int s = 0;
+#pragma unroll
+  for (int i = 1; i < 8; ++i)
+    if (i < m.n && r >= m.start[i]) s = i;
+  return (uint32_t)(m.row0[s] + (r - m.start[s]));
+}
+
+template <typename T, typename V>
+__global__ __launch_bounds__(256) void k_clip_noise(ClipNoiseJob j) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_out) {
+    j.hdr_out[0] = j.hdr[0]; j.hdr_out[1] = j.hdr[1]; j.hdr_out[2] = j.hdr[2];
+  }
+  const V* v = (const V*)j.v;
+  T* out = (T*)j.out;
+  const int ngrp = (j.D + 3) >> 2;
+  for (int r = blockIdx.x * 4 + wave; r < j.R; r += gridDim.x * 4) {
+    float ss = 0.f;
+    for (int g = lane; g < ngrp; g += 64) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * g + e;
+        if (c < j.D) { const float x = ld1<V>(v + (int64_t)r * j.ldv + c); ss += x * x; }
+      }
+    }
+    const float n = sqrtf(wave_sum(ss));
+    const float cf = (j.clip && n > j.C) ? j.C / n : 1.f;
+    if (lane == 0) {
+      if (j.norm) j.norm[r] = n;
+      if (j.cfac) j.cfac[r] = cf;
+    }
+    const uint32_t grow = j.noise ? global_row(j.rows, r) : 0u;
+    for (int g = lane; g < ngrp; g += 64) {
+      float xi[4] = {0.f, 0.f, 0.f, 0.f};
+      if (j.noise) gauss4(j.seed, j.step, grow, (uint32_t)g, j.tag, xi);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * g + e;
+        if (c < j.D) {
+          const float x = ld1<V>(v + (int64_t)r * j.ldv + c);
+          st1<T>(out + (int64_t)r * j.ldo + c, cf * x + j.stdv * xi[e]);
+        }
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t step, uint32_t tag,
+                                                      uint32_t row0, int rows, int groups,
+                                                      uint32_t* out) {
+  const int64_t total = (int64_t)rows * groups;
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int q = (int)(i % groups);
+    const uint32_t row = row0 + (uint32_t)(i / groups);
+    uint32_t c[4] = {step, row, (uint32_t)q, tag};
+    philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[4 * i + k] = c[k];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_cut_backward(CutBwdJob j) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_chk && j.hdr_chk[0] != j.chk_seq)
+    atomicAdd(j.err, 1);
+  const T* G = (const T*)j.g;
+  const T* Z = (const T*)j.z;
+  T* Dl = (T*)j.delta;
+  for (int r = blockIdx.x * 4 + wave; r < j.R; r += gridDim.x * 4) {
+    const bool clipped = j.clip && j.norm[r] > j.C;
+    float dot = 0.f, inv = 0.f, cf = 1.f;
+    if (clipped) {
+      inv = 1.f / j.norm[r];
+      cf = j.cfac[r];
+      for (int c = lane; c < j.D; c += 64)
+        dot += ld1<T>(Z + (int64_t)r * j.ldz + c) * inv * ld1<T>(G + (int64_t)r * j.ldg + c);
+      dot = wave_sum(dot);
+    }
+    for (int c = lane; c < j.D; c += 64) {
+      const float z = ld1<T>(Z + (int64_t)r * j.ldz + c);
+      float g = ld1<T>(G + (int64_t)r * j.ldg + c);
+      if (clipped) g = cf * (g - z * inv * dot);
+      if (j.relu && !(z > 0.f)) g = 0.f;
+      st1<T>(Dl + (int64_t)r * j.ldd + c, g);
+    }
+  }
+}
+
+// ------------------------------------------------------------ weight copies
+struct CastJobs { CastJob j[2 * 8 + 2]; int n; };
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_cast(CastJobs js) {
+  const CastJob& j = js.j[blockIdx.y];
+  const int64_t total = (int64_t)j.out * j.in;
+  T* Wq = (T*)j.Wq;
+  T* Wt = (T*)j.Wtq;
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int o = (int)(i / j.in), k = (int)(i % j.in);
+    const float w = j.W[i];
+    st1<T>(Wq + (int64_t)o * j.ldq + k, w);
+    st1<T>(Wt + (int64_t)k * j.ldt + o, w);
+  }
+}
+
+int grid_for(int64_t work, int per_block, int cap) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>((work + per_block - 1) / per_block, cap));
+}
+
+}  // namespace
+
+hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st) {
+  if (j.Hd > kMaxLogitCols) return hipErrorInvalidValue;
+  if (e == BF16) hipLaunchKernelGGL(k_logit_bce<uint16_t>, dim3(j.blocks), dim3(256), 0, st, j);
+  else hipLaunchKernelGGL(k_logit_bce<float>, dim3(j.blocks), dim3(256), 0, st, j);
+  return hipGetLastError();
+}
+
+hipError_t launch_philox_words(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0,
+                               int rows, int groups, uint32_t* out, hipStream_t st) {
+  const int64_t total = (int64_t)rows * groups;
+  hipLaunchKernelGGL(k_philox_words, dim3(grid_for(total, 256, 4096)), dim3(256), 0, st, seed,
+                     step, tag, row0, rows, groups, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_logit_sgd(const LogitJob& j, float scale, float* loss_out, hipStream_t st) {
+  hipLaunchKernelGGL(k_logit_sgd, dim3(1), dim3(256), 0, st, j, scale, loss_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_clip_noise(Elt e, const ClipNoiseJob& j, hipStream_t st) {
+  const int blocks = grid_for(j.R, 4, 4096);
+  if (e == BF16) {
+    if (j.v_f32) hipLaunchKernelGGL((k_clip_noise<uint16_t, float>), dim3(blocks), dim3(256), 0, st, j);
+    else hipLaunchKernelGGL((k_clip_noise<uint16_t, uint16_t>), dim3(blocks), dim3(256), 0, st, j);
+  } else {
+    hipLaunchKernelGGL((k_clip_noise<float, float>), dim3(blocks), dim3(256), 0, st, j);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_cut_backward(Elt e, const CutBwdJob& j, hipStream_t st) {
+  const int blocks = grid_for(j.R, 4, 4096);
+  if (e == BF16) hipLaunchKernelGGL(k_cut_backward<uint16_t>, dim3(blocks), dim3(256), 0, st, j);
+  else hipLaunchKernelGGL(k_cut_backward<float>, dim3(blocks), dim3(256), 0, st, j);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st) {
+  if (n_jobs <= 0) return hipSuccess;
+  CastJobs js;
+  if (n_jobs > (int)(sizeof(js.j) / sizeof(js.j[0]))) return hipErrorInvalidValue;
+  int64_t maxw = 0;
+  for (int i = 0; i < n_jobs; ++i) {
+    js.j[i] = jobs[i];
+    maxw = std::max<int64_t>(maxw, (int64_t)jobs[i].out * jobs[i].in);
+  }
+  js.n = n_jobs;
+  dim3 grid(grid_for(maxw, 256, 1024), n_jobs);
+  if (e == BF16) hipLaunchKernelGGL(k_cast<uint16_t>, grid, dim3(256), 0, st, js);
+  else hipLaunchKernelGGL(k_cast<float>, grid, dim3(256), 0, st, js);
+  return hipGetLastError();
+}
+
+}  // namespace vfl

@@ -1,0 +1,103 @@
+"""Shared driver of the GPU parity tests: runs the HIP path through the C ABI
+and the oracle on the same seeded inputs, and the comparison metrics.
+
+Tolerances (written in the tests that use them):
+* float32 workloads: max relative error <= 1e-4 per tick on every parameter
+  tensor (||gpu - ref||_inf / ||ref||_inf);
+* bf16 workloads: <= 2e-2 on parameters after the run;
+* parameter *changes* d = theta_t - theta_0 are compared too, with the
+  allowance that float32 master storage imposes: each update rounds the
+  stored parameter to float32, so |d_gpu - d_ref| may exceed the relative
+  bound by up to one unit in the last place of the tensor's largest
+  magnitude per update;
+* exchanged messages: each side decides every ReLU by the sign of its own
+  accumulated pre-activation (float32 on the GPU, float64 in the oracle); a
+  pre-activation within rounding of zero can flip, which changes whole rows
+  of the downstream gradient message.  Messages are therefore compared
+  element-wise on all but a bounded fraction of elements, plus a global
+  relative L2 error bound;
+* integers (schedule trace, slot headers, Philox words): equality.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import vfl_synth as S
+from oracle import PubSubOracle
+
+F32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+def rel_inf(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    den = np.max(np.abs(b)) if b.size else 0.0
+    num = np.max(np.abs(a - b)) if b.size else 0.0
+    return 0.0 if num == 0.0 else num / max(den, 1e-300)
+
+
+def ulp32(x):
+    m = float(np.max(np.abs(x)))
+    return 0.0 if m == 0.0 else 2.0 ** (np.floor(np.log2(m)) - 23)
+
+
+def delta_ok(g, o, p0, tol, n_updates):
+    """|(g - p0) - (o - p0)| <= tol * max|o - p0| + n_updates * ulp(max|theta|)."""
+    d_g = np.asarray(g, np.float64) - p0
+    d_o = np.asarray(o, np.float64) - p0
+    bound = tol * np.max(np.abs(d_o)) + n_updates * max(ulp32(o), ulp32(p0))
+    err = np.max(np.abs(d_g - d_o))
+    return err <= bound, err, bound
+
+
+def message_ok(g, o, tol_elem, max_bad_frac, tol_l2):
+    g = np.asarray(g, np.float64)
+    o = np.asarray(o, np.float64)
+    scale = max(np.max(np.abs(o)), 1e-30)
+    bad = np.abs(g - o) > tol_elem * scale
+    frac = bad.mean() if bad.size else 0.0
+    l2 = np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-30)
+    return (frac <= max_bad_frac and l2 <= tol_l2), frac, l2
+
+
+class Run:
+    """GPU run of ``n_groups`` batch groups over ``n_rows`` rows; group g of
+    the run covers the dataset rows of group ``g + g0`` (g0 selects a window
+    of the epoch, e.g. its ragged tail)."""
+
+    def __init__(self, w, n_rows, n_groups, g0=0, data=None, params=None, snap=None,
+                 messages=True):
+        from paper_2510_12494_amd.session import Session
+        from paper_2510_12494_amd import vfl as V
+        self.w, self.n_rows, self.n_groups, self.g0 = w, n_rows, n_groups, g0
+        self.data = S.generate(w, n_rows) if data is None else data
+        self.p0 = S.init_params(w) if params is None else params
+        self.rows_of = lambda g: S.group_rows(w, g + g0, n_rows)
+        sess = Session(w, self.data, self.p0, self.rows_of)
+        shapes = {k: v.shape for k, v in self.p0.items()}
+        self.snaps, self.msgs = {}, {}
+        s = w.staleness
+        try:
+            for t in range(n_groups + s):
+                sess.step(t, n_groups)
+                if messages:
+                    if t < n_groups:
+                        self.msgs[("e", t)] = sess.message(0, t)
+                    u = t - s
+                    if 0 <= u < n_groups:
+                        self.msgs[("g", u)] = sess.message(1, u)
+                if snap is None or snap(t):
+                    self.snaps[t] = sess.params(shapes)
+            self.final = sess.params(shapes)
+            self.losses = sess.losses(range(n_groups))
+            self.mismatches = V.vfl_check(sess.ctx)
+            self.trace = V.vfl_get_trace(sess.ctx)
+        finally:
+            sess.close()
+
+    def oracle(self, precision, snap=None):
+        o = PubSubOracle(self.w, self.p0, precision)
+        recs = o.run(self.data, self.n_groups, self.rows_of,
+                     snapshot=(lambda t: True) if snap is None else snap)
+        return o, recs

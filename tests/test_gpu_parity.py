@@ -1,0 +1,200 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle on the same
+seeded inputs, for the five workloads at their real tick shapes, their
+full-size ragged epoch tails, odd shapes and the schedule's integer state.
+Metrics and tolerances: tests/gpu_harness.py."""
+import numpy as np
+import pytest
+
+import vfl_synth as S
+from vfl_synth.workloads import Workload, PartySpec, TopSpec
+from oracle.philox import philox4x32_10
+import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs an MI355X")
+
+
+def _prec(w):
+    return "bf16" if w.dtype == "bf16" else "f64"
+
+
+def _tol(w):
+    return H.BF16_TOL if w.dtype == "bf16" else H.F32_TOL
+
+
+def _check_ints(run, o, recs):
+    assert run.mismatches == 0
+    assert run.trace == [tuple(r) for r in o.trace]
+    for r in recs:
+        if "emb_header" in r:
+            assert run.msgs[("e", r["fwd_group"])][1] == r["emb_header"]
+        if "grad_header" in r:
+            assert run.msgs[("g", r["bwd_group"])][1] == r["grad_header"]
+
+
+def _check_messages(run, recs, w):
+    if w.dtype == "bf16":
+        tol_elem, frac, l2 = 2.0 ** -6, 2e-3, 2e-2
+    else:
+        tol_elem, frac, l2 = 1e-4, 2e-3, 1e-4
+    for r in recs:
+        for key, tag, grp in (("zhat", "e", "fwd_group"), ("gtilde", "g", "bwd_group")):
+            if key in r:
+                ok, f, e = H.message_ok(run.msgs[(tag, r[grp])][0], r[key], tol_elem, frac, l2)
+                assert ok, (key, r["tick"], f, e)
+
+
+def _check_losses(run, recs, tol):
+    ref = np.array([r["loss"] for r in recs if "loss" in r])
+    np.testing.assert_allclose(run.losses, ref, rtol=tol)
+
+
+def _check_params(run, recs, w, per_tick):
+    tol = _tol(w)
+    s = w.staleness
+    ticks = sorted(run.snaps) if per_tick else [max(run.snaps)]
+    by_tick = {r["tick"]: r for r in recs}
+    for t in ticks:
+        ref = by_tick[t]["params"]
+        n_upd = max(0, t - s + 1)
+        for k, v in ref.items():
+            g = run.snaps[t][k]
+            assert H.rel_inf(g, v) <= tol, (k, t, H.rel_inf(g, v))
+            ok, err, bound = H.delta_ok(g, v, run.p0[k].astype(np.float64), tol, n_upd)
+            assert ok, (k, t, err, bound)
+
+
+# ------------------------------------------------------------- Philox words
+@pytest.mark.parametrize("step,tag,row0", [(0, 0, 0), (305, 1, 9_990_000), (7, 0, 123_456)])
+def test_philox_words_bit_exact(step, tag, row0):
+    import torch
+    from paper_2510_12494_amd import vfl as V
+    rows, groups, seed = 4096, 32, 0x5EED0005
+    out = torch.zeros(rows * groups * 4, dtype=torch.int32, device="cuda")
+    V.vfl_philox(seed, step, tag, row0, rows, groups, out.data_ptr(), 0)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32).reshape(rows, groups, 4)
+    r = (np.arange(rows, dtype=np.uint64) + row0)[:, None]
+    q = np.arange(groups, dtype=np.uint64)[None, :]
+    ref = philox4x32_10(step, r, q, tag, seed & 0xFFFFFFFF, seed >> 32)
+    for i in range(4):
+        assert np.array_equal(got[:, :, i], ref[i])
+
+
+# ------------------------------------------------------------ the workloads
+def test_tiny_sync_full_epoch():
+    """4096 rows, 16 ticks, fp32, s=0: every tick against the float64 oracle."""
+    w = S.get("tiny_sync")
+    run = H.Run(w, w.n_rows, 16)
+    o, recs = run.oracle("f64")
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
+
+
+def test_dense_tabular_100_ticks():
+    """bf16, s=2: 100 batch groups (102 ticks) against the bf16-emulating
+    oracle; parameters after the run within 2e-2."""
+    w = S.get("dense_tabular")
+    n = 100 * w.rows_per_tick
+    last = 100 + w.staleness - 1
+    snap = lambda t: t in (10, 50, last)
+    run = H.Run(w, n, 100, snap=snap)
+    o, recs = run.oracle("bf16", snap=snap)
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
+
+
+def test_ctr_per_tick():
+    """fp32 with 13 + 13 embedding fields (Zipf ids), s=2: every tick."""
+    w = S.get("ctr")
+    n = 6 * w.rows_per_tick
+    run = H.Run(w, n, 6)
+    o, recs = run.oracle("f64")
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
+
+
+@pytest.mark.parametrize("name", ["hetero", "private"])
+def test_large_tick_workloads(name):
+    """hetero (s=4, k=4) and private (s=2, k=2, clip + noise on both
+    messages) at R = 32768 rows per tick."""
+    w = S.get(name)
+    n = 6 * w.rows_per_tick
+    run = H.Run(w, n, 6)
+    o, recs = run.oracle("bf16")
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
+
+
+@pytest.mark.parametrize("name", list(S.ALL))
+def test_gradient_probe(name):
+    """One update per party at lr = 1, so that every parameter change is far
+    above float32 resolution: the change equals -grad, compared at the
+    workload's tolerance (float32 1e-4, bf16 2e-2)."""
+    w = S.get(name).replace(lr=1.0)
+    run = H.Run(w, w.rows_per_tick, 1)
+    o, recs = run.oracle(_prec(w))
+    _check_ints(run, o, recs)
+    tol = _tol(w)
+    for k, v in o.p.items():
+        ok, err, bound = H.delta_ok(run.final[k], v, run.p0[k].astype(np.float64), tol, 1)
+        assert ok, (k, err, bound)
+
+
+@pytest.mark.parametrize("name", list(S.ALL))
+def test_full_size_epoch_tail(name):
+    """The workload's full dataset; the last two groups of its epoch (the
+    last one ragged), so row ids, noise counters and tails are those of the
+    full size."""
+    w = S.get(name)
+    T = w.ticks_per_epoch()
+    g0 = T - 2
+    run = H.Run(w, w.n_rows, 2, g0=g0)
+    if w.n_rows % w.rows_per_tick:
+        assert sum(c for _, c in run.rows_of(1)) < w.rows_per_tick
+    o, recs = run.oracle(_prec(w))
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3 if w.dtype == "bf16" else 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
+
+
+# ------------------------------------------------------------- odd shapes
+def _odd(dtype, s, k, clip):
+    return Workload(name="odd", n_rows=1101, dtype=dtype,
+                    A=PartySpec(dense=13, widths=[40, 24]),
+                    B=PartySpec(dense=21, n_cat=3, vocab=37, emb_dim=4, widths=[33, 17]),
+                    top=TopSpec(widths=[19, 1]), batch=100, staleness=s, replicas=k, lr=0.5,
+                    clip=1.0 if clip else 0.0, sigma=0.5 if clip else 0.0, clip_emb=clip,
+                    clip_grad=clip, noise_emb=clip, noise_grad=clip, labels="bernoulli",
+                    label_p=0.4, zipf_a=1.1, data_seed=77, init_seed=78, noise_seed=79)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("s,k,clip", [(0, 1, False), (1, 3, True), (3, 2, False)])
+def test_odd_shapes(dtype, s, k, clip):
+    """Widths that are not multiples of any tile, 3 embedding fields with an
+    input width not a multiple of 16, row counts not multiples of 64 and an
+    epoch whose last group holds a single row (1101 = 11 * 100 + 1)."""
+    w = _odd(dtype, s, k, clip)
+    n_groups = (w.n_rows + w.rows_per_tick - 1) // w.rows_per_tick
+    run = H.Run(w, w.n_rows, n_groups)
+    o, recs = run.oracle(_prec(w))
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3 if dtype == "bf16" else 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
