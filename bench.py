@@ -1,0 +1,195 @@
+"""Throughput of the two-party publisher/subscriber split-learning step on one
+MI355X.
+
+One step = one tick of the deterministic schedule: party B's bottom forward
+and publish of group t, party A's bottom forward, top model, BCE, backward
+and SGD of group t - s, and B's delayed backward + SGD of that group (both
+parties' forward, backward and update).  Inputs are seeded synthetic data of
+the workload's shape, resident in HBM before timing starts.
+
+Prints one JSON line: samples/s (rows per tick / tick time), the MFMA
+utilisation of the algorithmic matrix-product FLOPs, the roofline of the
+dominant kernel class (its algorithmic FLOPs or bytes per launch over its
+average duration, timed with HIP events on its own stream during the timed
+region) and the oracle's CPU throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"bf16": 2.5e15, "f32": 157.3e12}     # dense MFMA FLOP/s (MI355X spec)
+HBM_PEAK = 8.0e12                            # bytes/s
+METRIC = "training samples/sec (both parties fwd+bwd+update) on 1 MI355X; MFMA util %"
+GEMM_CLASSES = ("gemm_fwd", "gemm_dx", "gemm_dw")
+
+
+def gemm_flops_per_tick(w) -> float:
+    """Algorithmic matrix-product FLOPs of one tick (no padding): every layer's
+    forward and weight gradient, and the input gradient of every layer but
+    the first layer of a bottom model without embedding tables; the logit
+    layer counted as a product of width 1."""
+    R = w.rows_per_tick
+    f = 0.0
+    for spec in (w.A, w.B):
+        for l, (fi, fo) in enumerate(spec.layer_dims()):
+            f += 2 * 2.0 * R * fi * fo
+            if l > 0:
+                f += 2.0 * R * fi * fo
+            elif spec.n_cat:
+                f += 2.0 * R * (spec.n_cat * spec.emb_dim) * fo
+    fi = w.top_in
+    for fo in w.top.widths:
+        f += 3 * 2.0 * R * fi * fo
+        fi = fo
+    return f
+
+
+def source_sha(path: str) -> str:
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def traffic_for(kernel: str, per_launch_work: float):
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    or None when there is none or the kernel source changed since."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as fh:
+        t = json.load(fh)
+    src = os.path.join(ROOT, t.get("source", ""))
+    if not os.path.exists(src) or source_sha(src) != t.get("source_sha"):
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, data, params, seconds: float) -> dict:
+    """The oracle (float64 numpy) on this host over the same resident dataset,
+    for about ``seconds`` of CPU work: one probe group sizes the sample."""
+    import vfl_synth as S
+    from oracle import PubSubOracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    R = w.rows_per_tick
+    rows_of = lambda g: S.group_rows(w, g)
+    t0 = time.perf_counter()
+    PubSubOracle(w, params, "f64").run(data, 1, rows_of, keep_messages=False)
+    per_group = time.perf_counter() - t0
+    groups = int(max(1, min(4096, seconds / max(per_group, 1e-6))))
+    o = PubSubOracle(w, params, "f64")
+    t0 = time.perf_counter()
+    o.run(data, groups, rows_of, keep_messages=False)
+    dt = time.perf_counter() - t0
+    return {"value": groups * R / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {groups} batch groups of {R} rows of the same dataset "
+                      f"({groups + w.staleness} ticks incl. the s={w.staleness} lead-in), "
+                      f"float64 numpy, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="dense_tabular")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: both parties share a single MI355X as two HIP "
+              f"streams; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import vfl_synth as S
+    from paper_2510_12494_amd import vfl as V
+    from paper_2510_12494_amd.session import Session
+
+    w = S.get(args.workload)
+    data = S.generate(w)
+    params = S.init_params(w)
+    epoch = w.ticks_per_epoch()
+    sess = Session(w, data, params, lambda g: S.group_rows(w, g))
+    warm = max(args.warmup, 2 * (w.staleness + 1))
+    t = 0
+    for _ in range(warm):
+        sess.step(t, epoch=epoch)
+        t += 1
+    # pick the dominant kernel class on a short profiled pass
+    V.vfl_timing_enable(sess.ctx, (1 << len(V.KERNEL_CLASSES)) - 1)
+    for _ in range(50):
+        sess.step(t, epoch=epoch)
+        t += 1
+    probe = {name: V.vfl_timing_read(sess.ctx, i) for i, name in enumerate(V.KERNEL_CLASSES)}
+    dom = max(probe, key=lambda k: probe[k][0])
+    dom_i = V.KERNEL_CLASSES.index(dom)
+    V.vfl_timing_enable(sess.ctx, 1 << dom_i)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        sess.step(t, epoch=epoch)
+        t += 1
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms, launches, work = V.vfl_timing_read(sess.ctx, dom_i)
+    V.vfl_timing_enable(sess.ctx, 0)
+    losses = sess.losses([t - w.staleness - 1])
+    sess.close()
+
+    R = w.rows_per_tick
+    value = args.steps * R / dt
+    tick_s = dt / args.steps
+    flops = gemm_flops_per_tick(w)
+    mfma = flops / tick_s / PEAK[w.dtype]
+    is_gemm = dom in GEMM_CLASSES
+    avg_s = ms / 1e3 / max(launches, 1)
+    per_launch = work / max(launches, 1)
+    achieved = per_launch / avg_s if avg_s > 0 else 0.0
+    if is_gemm:
+        roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK[w.dtype] / 1e12,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_for(dom, per_launch)
+    roof["kernel"] = dom
+    roof["launches"] = launches
+    roof["avg_us"] = avg_s * 1e6
+    roof["work_per_launch"] = per_launch
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": warm, "ms_per_step": tick_s * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic (seeded, resident in HBM)",
+        "mfma_util_pct": 100.0 * mfma, "gemm_gflop_per_step": flops / 1e9,
+        "config": {"workload": w.name, "rows": w.n_rows, "rows_per_tick": R, "batch": w.batch,
+                   "replicas": w.replicas, "staleness": w.staleness,
+                   "bottom_A": "-".join(map(str, [w.A.d_in] + w.A.widths)),
+                   "bottom_B": "-".join(map(str, [w.B.d_in] + w.B.widths)),
+                   "top": "-".join(map(str, [w.top_in] + w.top.widths)), "lr": w.lr},
+        "roofline": roof,
+        "kernel_classes_ms_per_step_probe": {k: v[0] / 50 for k, v in probe.items() if v[1]},
+        "last_loss": float(losses[0]),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, data, params, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

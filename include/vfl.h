@@ -222,6 +222,33 @@ vfl_status vfl_check(vfl_ctx* c, uint32_t* header_mismatches);
 vfl_status vfl_philox(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0, int32_t rows,
                       int32_t groups, uint32_t* out_dev, void* stream);
 
+/* Kernel classes for vfl_timing_* (bit i of a mask selects class i). */
+typedef enum {
+  VFL_K_GEMM_FWD = 0,   /* layer forward products (+ bias, ReLU) */
+  VFL_K_GEMM_DX = 1,    /* input-gradient products (+ ReLU mask, split) */
+  VFL_K_GEMM_DW = 2,    /* weight-gradient products (SGD fused when unsplit) */
+  VFL_K_REDUCE = 3,     /* split-partial reductions + SGD (weights, logit) */
+  VFL_K_LOGIT = 4,      /* logit + BCE + its gradient */
+  VFL_K_CLIP_NOISE = 5, /* per-row clip + Philox noise of a message */
+  VFL_K_CUT_BWD = 6,    /* passive party's cut-layer backward */
+  VFL_K_CAST = 7,       /* weight operand copies */
+  VFL_K_GATHER = 8,     /* embedding gather */
+  VFL_K_EMB_SGD = 9,    /* sorted sparse SGD of the tables */
+  VFL_K_COUNT = 10
+} vfl_kernel_class;
+
+/* Measurement hook: while class_mask is non-zero, every launch of a
+ * selected class is bracketed by two HIP events on its own stream (this adds
+ * two event records per launch and nothing else).  vfl_timing_read
+ * synchronises both streams and returns, for one class, the summed kernel
+ * durations in milliseconds, the number of launches and the summed
+ * algorithmic work (FLOPs for the three product classes, bytes that the
+ * kernel must move at minimum for the others); then it resets that class.
+ * Enabling with mask 0 stops recording. */
+vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t class_mask);
+vfl_status vfl_timing_read(vfl_ctx* c, int32_t kernel_class, double* ms, int64_t* launches,
+                           double* work);
+
 const char* vfl_last_error(const vfl_ctx* c);
 
 /* Synchronise both streams and release the context's events and host state.

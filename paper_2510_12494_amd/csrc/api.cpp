@@ -50,7 +50,7 @@ DwPlan dw_plan(Elt e, int R, int N, int K) {
   const int RE = dw_stage_rows(e), T = dw_tile(e);
   const int tiles = ((N + T - 1) / T) * ((K + T - 1) / T);
   const int max_splits = std::max(1, (R + RE - 1) / RE);
-  int s = std::min(max_splits, std::max(1, (512 + tiles - 1) / tiles));
+  int s = std::min(max_splits, std::max(1, (256 + tiles - 1) / tiles));
   int rps = (R + s - 1) / s;
   rps = (rps + RE - 1) / RE * RE;
   p.rps = rps;
@@ -117,8 +117,25 @@ struct SlotState {
 
 }  // namespace
 
+namespace {
+// Event pairs bracketing the launches of the selected kernel classes.
+struct Timing {
+  static constexpr int kPool = 4096;
+  uint32_t mask = 0;
+  bool created = false;
+  hipEvent_t ev0[kPool]{}, ev1[kPool]{};
+  int cls[kPool]{};
+  double work[kPool]{};
+  bool used[kPool]{};
+  int next = 0;
+  double ms[VFL_K_COUNT]{}, wk[VFL_K_COUNT]{};
+  int64_t n[VFL_K_COUNT]{};
+};
+}  // namespace
+
 struct vfl_ctx {
   Plan p;
+  Timing tm;
   vfl_opts o{};
   char* ws = nullptr;
   hipStream_t sa = nullptr, sb = nullptr;
@@ -349,6 +366,45 @@ vfl_status take_batches(vfl_ctx* c, const Party& P, const vfl_batch* br, int n, 
   return VFL_OK;
 }
 
+// harvest one finished event pair into its class totals
+void harvest(vfl_ctx* c, int i) {
+  Timing& T = c->tm;
+  if (!T.used[i]) return;
+  float ms = 0.f;
+  if (hipEventSynchronize(T.ev1[i]) == hipSuccess && hipEventElapsedTime(&ms, T.ev0[i], T.ev1[i]) == hipSuccess) {
+    T.ms[T.cls[i]] += ms;
+    T.wk[T.cls[i]] += T.work[i];
+    T.n[T.cls[i]] += 1;
+  }
+  T.used[i] = false;
+}
+
+int tbegin(vfl_ctx* c, int cls, double work, hipStream_t st) {
+  Timing& T = c->tm;
+  if (!((T.mask >> cls) & 1u)) return -1;
+  const int i = T.next;
+  T.next = (T.next + 1) % Timing::kPool;
+  harvest(c, i);
+  T.cls[i] = cls;
+  T.work[i] = work;
+  if (hipEventRecord(T.ev0[i], st) != hipSuccess) return -1;
+  return i;
+}
+
+void tend(vfl_ctx* c, int i, hipStream_t st) {
+  if (i < 0) return;
+  if (hipEventRecord(c->tm.ev1[i], st) == hipSuccess) c->tm.used[i] = true;
+}
+
+#define TIMED(cls, work, st, call)                      \
+  do {                                                  \
+    const int ts_ = tbegin(c, (cls), (work), (st));     \
+    HIPCHK(call);                                       \
+    tend(c, ts_, (st));                                 \
+  } while (0)
+
+double gemm_flops(int M, int N, int K) { return 2.0 * M * (double)N * K; }
+
 vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipStream_t st) {
   CastJob jobs[2 * VFL_MAX_LAYERS + 2];
   int n = 0;
@@ -359,7 +415,9 @@ vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipS
     for (int j = 0; j < T->H; ++j)
       jobs[n++] = CastJob{at<float>(c, T->W[j]), c->ws + T->Wq[j], c->ws + T->Wtq[j],
                           T->out[j], T->in[j], T->ldq[j], T->ldt[j]};
-  HIPCHK(launch_cast(c->p.e, jobs, n, st));
+  double bytes = 0;
+  for (int i = 0; i < n; ++i) bytes += (double)jobs[i].out * jobs[i].in * (4 + 2 * elt_size(c->p.e));
+  TIMED(VFL_K_CAST, bytes, st, launch_cast(c->p.e, jobs, n, st));
   return VFL_OK;
 }
 
@@ -373,7 +431,9 @@ vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const Sl
   if (P.spec.n_cat) {
     GatherJob gj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
                  in.dense, in.ld, P.spec.dense_in, c->ws + P.x0[slot], P.ldx0, R};
-    HIPCHK(launch_gather(p.e, gj, st));
+    const double gb = (double)R * P.spec.n_cat * (4 + P.spec.emb_dim * (4.0 + elt_size(p.e))) +
+                      2.0 * R * P.spec.dense_in * elt_size(p.e);
+    TIMED(VFL_K_GATHER, gb, st, launch_gather(p.e, gj, st));
     x = c->ws + P.x0[slot];
     ldx = P.ldx0;
   }
@@ -392,7 +452,7 @@ vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const Sl
       g.hdr_out = hdr_out;
       g.hdr[0] = hdr[0]; g.hdr[1] = hdr[1]; g.hdr[2] = hdr[2];
     }
-    HIPCHK(launch_gemm_nt(p.e, g, st));
+    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
   return VFL_OK;
 }
@@ -413,12 +473,13 @@ vfl_status enqueue_bottom_backward(vfl_ctx* c, const Party& P, int slot, const S
     d.X1 = l == 0 ? x : c->ws + P.act[slot][l - 1];
     d.ldx1 = l == 0 ? ldx : ld_of(P.out[l - 1]);
     d.part = part; d.partb = partb;
+    d.W = at<float>(c, P.W[l]); d.bias = at<float>(c, P.b[l]); d.scale = scale;
     d.R = R; d.N = P.out[l]; d.K = P.in[l];
     d.rows_per_split = P.dw[l].rps;
     d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
-    HIPCHK(launch_gemm_dw(p.e, d, st));
-    HIPCHK(launch_sgd_reduce(at<float>(c, P.W[l]), part, (int64_t)P.out[l] * P.in[l],
-                             at<float>(c, P.b[l]), partb, P.out[l], d.splits, scale, st));
+    TIMED(VFL_K_GEMM_DW, gemm_flops(R, d.N, d.K), st, launch_gemm_dw(p.e, d, st));
+    if (d.splits > 1)
+      TIMED(VFL_K_REDUCE, 4.0 * ((double)d.N * d.K + d.N) * (d.splits + 2), st, launch_dw_reduce(d, st));
     if (l > 0) {
       GemmNT g;
       g.A1 = D; g.lda1 = P.ld_delta;
@@ -426,7 +487,7 @@ vfl_status enqueue_bottom_backward(vfl_ctx* c, const Party& P, int slot, const S
       g.C1 = c->ws + P.dbuf[cur ^ 1]; g.ldc1 = P.ld_delta;
       if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
       g.M = R; g.N = P.in[l]; g.K = P.out[l];
-      HIPCHK(launch_gemm_nt(p.e, g, st));
+      TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
       cur ^= 1;
     } else if (P.spec.n_cat) {
       GemmNT g;
@@ -434,10 +495,11 @@ vfl_status enqueue_bottom_backward(vfl_ctx* c, const Party& P, int slot, const S
       g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
       g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
       g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
-      HIPCHK(launch_gemm_nt(p.e, g, st));
+      TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
       ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
                     at<float>(c, P.gx), P.ldgx, R, scale};
-      HIPCHK(launch_scatter_sgd(sj, st));
+      TIMED(VFL_K_EMB_SGD, (double)R * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
+            launch_scatter_sgd(sj, st));
     }
   }
   return VFL_OK;
@@ -604,7 +666,8 @@ vfl_status vfl_publish(vfl_ctx* c, int64_t group) {
     j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 0; j.rows = st.rmap;
     j.hdr_out = hdr_ptr(c, 0, slot);
     j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)group; j.hdr[2] = (int32_t)st.version;
-    HIPCHK(launch_clip_noise(p.e, j, c->sb));
+    TIMED(VFL_K_CLIP_NOISE, (double)st.rows * p.dB * (elt_size(p.e) * 2.0) + 8.0 * st.rows, c->sb,
+          launch_clip_noise(p.e, j, c->sb));
   }
   HIPCHK(hipEventRecord(c->ev_emb[slot], c->sb));
   st.published = true;
@@ -643,7 +706,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
     g.C1 = c->ws + T.act[j]; g.ldc1 = ld_of(T.out[j]);
     g.bias = at<float>(c, T.b[j]); g.relu = T.relu[j];
     g.M = R; g.N = T.out[j]; g.K = T.in[j];
-    HIPCHK(launch_gemm_nt(p.e, g, st));
+    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
   // logit + BCE, logit-layer SGD
   int cur = 0;
@@ -652,9 +715,10 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
   lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = c->a_labels;
   lj.delta = c->ws + p.A.dbuf[cur]; lj.ldd = p.A.ld_delta; lj.relu = T.relu[T.H - 1];
   lj.part = at<float>(c, T.logit_part);
-  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 15) / 16));
-  HIPCHK(launch_logit_bce(p.e, lj, st));
-  HIPCHK(launch_logit_sgd(lj, scale, loss_dev, st));
+  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 63) / 64));
+  lj.scale = scale; lj.loss_out = loss_dev;
+  TIMED(VFL_K_LOGIT, (double)R * lj.Hd * 2.0 * elt_size(p.e) + 4.0 * R, st, launch_logit_bce(p.e, lj, st));
+  TIMED(VFL_K_REDUCE, 4.0 * lj.blocks * (lj.Hd + 2) + 8.0 * lj.Hd, st, launch_logit_reduce(lj, st));
   // hidden layers backward
   float* part = at<float>(c, p.part_a);
   float* partb = at<float>(c, p.partb_a);
@@ -669,12 +733,13 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
       d.X1 = c->ws + T.act[j - 1]; d.ldx1 = ld_of(T.out[j - 1]);
     }
     d.part = part; d.partb = partb;
+    d.W = at<float>(c, T.W[j]); d.bias = at<float>(c, T.b[j]); d.scale = scale;
     d.R = R; d.N = T.out[j]; d.K = T.in[j];
     d.rows_per_split = T.dw[j].rps;
     d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
-    HIPCHK(launch_gemm_dw(p.e, d, st));
-    HIPCHK(launch_sgd_reduce(at<float>(c, T.W[j]), part, (int64_t)T.out[j] * T.in[j],
-                             at<float>(c, T.b[j]), partb, T.out[j], d.splits, scale, st));
+    TIMED(VFL_K_GEMM_DW, gemm_flops(R, d.N, d.K), st, launch_gemm_dw(p.e, d, st));
+    if (d.splits > 1)
+      TIMED(VFL_K_REDUCE, 4.0 * ((double)d.N * d.K + d.N) * (d.splits + 2), st, launch_dw_reduce(d, st));
     GemmNT g;
     g.A1 = D; g.lda1 = p.A.ld_delta;
     g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
@@ -692,7 +757,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
         g.hdr[0] = (int32_t)group; g.hdr[1] = (int32_t)(group + p.s); g.hdr[2] = (int32_t)bs.version;
       }
     }
-    HIPCHK(launch_gemm_nt(p.e, g, st));
+    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
     cur ^= 1;
   }
   if (gextra) {
@@ -706,7 +771,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
     j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 1; j.rows = c->aslot.rmap;
     j.hdr_out = hdr_ptr(c, 1, slot);
     j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)(group + p.s); j.hdr[2] = (int32_t)bs.version;
-    HIPCHK(launch_clip_noise(p.e, j, st));
+    TIMED(VFL_K_CLIP_NOISE, (double)R * p.dB * (4.0 + elt_size(p.e)), st, launch_clip_noise(p.e, j, st));
   }
   HIPCHK(hipEventRecord(c->ev_grad[slot], st));
   c->grad_group[slot] = group;
@@ -746,7 +811,8 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     cj.delta = c->ws + p.P.dbuf[0]; cj.ldd = p.P.ld_delta;
     cj.R = st.rows; cj.D = p.dB;
     cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
-    HIPCHK(launch_cut_backward(p.e, cj, c->sb));
+    TIMED(VFL_K_CUT_BWD, (double)st.rows * p.dB * 3.0 * elt_size(p.e) + (cj.clip ? 8.0 * st.rows : 0.0),
+          c->sb, launch_cut_backward(p.e, cj, c->sb));
     vfl_status r = enqueue_bottom_backward(c, p.P, slot, st, 0, at<float>(c, p.P.part),
                                            at<float>(c, p.P.partb), c->sb);
     if (r) return r;
@@ -836,6 +902,36 @@ vfl_status vfl_philox(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0,
   return VFL_OK;
 }
 
+vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t mask) {
+  if (!c) return VFL_E_INVALID;
+  Timing& T = c->tm;
+  if (mask && !T.created) {
+    for (int i = 0; i < Timing::kPool; ++i) {
+      HIPCHK(hipEventCreate(&T.ev0[i]));
+      HIPCHK(hipEventCreate(&T.ev1[i]));
+    }
+    T.created = true;
+  }
+  T.mask = mask;
+  return VFL_OK;
+}
+
+vfl_status vfl_timing_read(vfl_ctx* c, int32_t cls, double* ms, int64_t* launches, double* work) {
+  if (!c || cls < 0 || cls >= VFL_K_COUNT) return VFL_E_INVALID;
+  Timing& T = c->tm;
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  if (T.created)
+    for (int i = 0; i < Timing::kPool; ++i) harvest(c, i);
+  if (ms) *ms = T.ms[cls];
+  if (launches) *launches = T.n[cls];
+  if (work) *work = T.wk[cls];
+  T.ms[cls] = 0.0;
+  T.wk[cls] = 0.0;
+  T.n[cls] = 0;
+  return VFL_OK;
+}
+
 const char* vfl_last_error(const vfl_ctx* c) { return c ? c->err.c_str() : "null context"; }
 
 vfl_status vfl_destroy(vfl_ctx* c) {
@@ -845,6 +941,11 @@ vfl_status vfl_destroy(vfl_ctx* c) {
     if (hipStreamSynchronize(c->sa) != hipSuccess) r = VFL_E_HIP;
     if (hipStreamSynchronize(c->sb) != hipSuccess) r = VFL_E_HIP;
   }
+  if (c->tm.created)
+    for (int i = 0; i < Timing::kPool; ++i) {
+      (void)hipEventDestroy(c->tm.ev0[i]);
+      (void)hipEventDestroy(c->tm.ev1[i]);
+    }
   for (int q = 0; q < kMaxSlots; ++q) {
     if (c->ev_emb[q]) (void)hipEventDestroy(c->ev_emb[q]);
     if (c->ev_grad[q]) (void)hipEventDestroy(c->ev_grad[q]);

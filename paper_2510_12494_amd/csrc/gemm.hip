@@ -8,7 +8,8 @@
 //                                              weight copy W^T [in x out]
 //   weight   dW = dY^T X, db = colsum(dY)      reduction over rows: both
 //                                              operands are transposed while
-//                                              staged through LDS
+//                                              staged through LDS; the SGD
+//                                              step is fused into it
 // Tiles: 256 threads = 4 wavefronts in a 2 x 2 grid, each wavefront owning a
 // (BM/2) x (BN/2) block of 16 x 16 MFMA tiles (v_mfma_f32_16x16x32_bf16 for
 // bf16 operands, v_mfma_f32_16x16x4_f32 for float32), float32 accumulation.
@@ -343,6 +344,23 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
     __syncthreads();
   }
 
+  if (g.splits == 1) {
+    // the block holds the whole row sum: SGD straight from the accumulators
+#pragma unroll
+    for (int j = 0; j < BN / 32; ++j) {
+#pragma unroll
+      for (int i = 0; i < BK / 32; ++i) {
+        const int k = k0 + wm * (BK / 2) + i * 16 + (lane & 15);
+        const int nb = n0 + wn * (BN / 2) + j * 16 + (lane >> 4) * 4;
+        if (k >= g.K) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (nb + r < g.N) g.W[(int64_t)(nb + r) * g.K + k] -= g.scale * acc[j][i][r];
+      }
+    }
+    if (do_bias && tid < BN && n0 + tid < g.N) g.bias[n0 + tid] -= g.scale * accb;
+    return;
+  }
   float* part = g.part + (int64_t)split * g.N * g.K;
 #pragma unroll
   for (int j = 0; j < BN / 32; ++j) {
@@ -359,21 +377,39 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
   if (do_bias && tid < BN && n0 + tid < g.N) g.partb[(int64_t)split * g.N + n0 + tid] = accb;
 }
 
-__global__ void k_sgd_reduce(float* W, const float* part, int64_t nW, float* b,
-                             const float* partb, int nb, int splits, float scale) {
-  const int64_t total = nW + nb;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    float s = 0.f;
-    if (i < nW) {
-      for (int q = 0; q < splits; ++q) s += part[(int64_t)q * nW + i];
-      W[i] -= scale * s;
-    } else {
-      const int64_t j = i - nW;
-      for (int q = 0; q < splits; ++q) s += partb[(int64_t)q * nb + j];
-      b[j] -= scale * s;
-    }
+// Sum of the split partials in split order + SGD: four consecutive
+// elements per thread (weights first, then bias), eight splits' loads in
+// flight at a time.
+__global__ __launch_bounds__(256) void k_dw_reduce(GemmDW g) {
+  const int64_t NK = (int64_t)g.N * g.K;
+  const int64_t qw = (NK + 3) / 4, qb = (g.N + 3) / 4;
+  const int64_t t = blockIdx.x * (int64_t)256 + threadIdx.x;
+  if (t >= qw + qb) return;
+  const bool is_w = t < qw;
+  const float* src = is_w ? g.part : g.partb;
+  const int64_t stride = is_w ? NK : g.N;
+  const int64_t base = 4 * (is_w ? t : t - qw);
+  float* dst = (is_w ? g.W : g.bias) + base;
+  const int n = (int)std::min<int64_t>(4, stride - base);
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+  int q = 0;
+  for (; q + 8 <= g.splits; q += 8) {
+    float v[8][4];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[u][e] = e < n ? src[(q + u) * stride + base + e] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum[e] += v[u][e];
   }
+  for (; q < g.splits; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sum[e] += e < n ? src[q * stride + base + e] : 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (e < n) dst[e] -= g.scale * sum[e];
 }
 
 template <typename T, int BM, int BN>
@@ -394,6 +430,7 @@ hipError_t dw_launch(const GemmDW& g, hipStream_t st) {
 
 int dw_stage_rows(Elt e) { return 128 / elt_size(e); }
 int dw_tile(Elt) { return 64; }
+int dw_tiles(int N, int K) { return ((N + 63) / 64) * ((K + 63) / 64); }
 
 hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
@@ -406,20 +443,17 @@ hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st) {
   return nt_launch<float, 64, 64>(g, st);
 }
 
+hipError_t launch_dw_reduce(const GemmDW& g, hipStream_t st) {
+  if (g.splits <= 1 || g.N <= 0 || g.K <= 0) return hipSuccess;
+  const int64_t quads = ((int64_t)g.N * g.K + 3) / 4 + (g.N + 3) / 4;
+  hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_dw(Elt e, const GemmDW& g, hipStream_t st) {
   if (g.N <= 0 || g.K <= 0 || g.splits <= 0) return hipSuccess;
   if (e == BF16) return dw_launch<uint16_t, 64, 64>(g, st);
   return dw_launch<float, 64, 64>(g, st);
-}
-
-hipError_t launch_sgd_reduce(float* W, const float* part, int64_t nW, float* b,
-                             const float* partb, int nb, int splits, float scale,
-                             hipStream_t st) {
-  const int64_t total = nW + nb;
-  int blocks = (int)std::min<int64_t>((total + 255) / 256, 2048);
-  hipLaunchKernelGGL(k_sgd_reduce, dim3(blocks), dim3(256), 0, st, W, part, nW, b, partb,
-                     nb, splits, scale);
-  return hipGetLastError();
 }
 
 }  // namespace vfl

@@ -32,26 +32,27 @@ struct GemmNT {
   const int32_t* hdr_chk = nullptr; int32_t chk_seq = 0; int32_t* err = nullptr;
 };
 
-// Split-row weight gradient: part[s][n][k] = sum over rows r of split s of
-// D[r][n] * X[r][k] and partb[s][n] = sum of D[r][n]; X = [X1 | X2] split at
-// column ksplit.  rows_per_split is a multiple of the stage depth.
+// Weight gradient + SGD: G[n][k] = sum over rows r of D[r][n] * X[r][k],
+// g_b[n] = sum_r D[r][n]; W -= scale * G, bias -= scale * g_b.  X = [X1 | X2]
+// split at column ksplit.  The rows are cut into `splits` chunks of
+// rows_per_split (a multiple of the stage depth); with more than one chunk
+// each block writes a float32 partial part[s][n][k] (partb[s][n]) and a
+// second kernel sums the partials in chunk order and applies the update.
 struct GemmDW {
   const void* D = nullptr; int64_t ldd = 0;
   const void* X1 = nullptr; int64_t ldx1 = 0;
   const void* X2 = nullptr; int64_t ldx2 = 0; int ksplit = 1 << 30;
   float* part = nullptr; float* partb = nullptr;
+  float* W = nullptr; float* bias = nullptr; float scale = 0.f;
   int R = 0, N = 0, K = 0, rows_per_split = 0, splits = 1;
 };
 
 hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st);
 hipError_t launch_gemm_dw(Elt e, const GemmDW& g, hipStream_t st);
+// second stage of a split weight gradient (no-op when splits == 1)
+hipError_t launch_dw_reduce(const GemmDW& g, hipStream_t st);
 int dw_stage_rows(Elt e);   // rows per pipeline stage of the dW kernel
 int dw_tile(Elt e);         // output tile edge of the dW kernel
-
-// W[i] -= scale * sum_s part[s][i]   (i < n), b likewise with partb.
-hipError_t launch_sgd_reduce(float* W, const float* part, int64_t nW, float* b,
-                             const float* partb, int nb, int splits, float scale,
-                             hipStream_t st);
 
 // Operand copies of one layer's float32 weight W [out x in]:
 // Wq [out x ldq] and Wtq [in x ldt] of element type e (ldq, ldt padded).
@@ -62,18 +63,19 @@ hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
 
 // Logit layer + BCE on the last hidden activation H [R x ldh] (width Hd):
 // l = H w + b, loss_i = BCE(l, y), dl = sigmoid(l) - y; writes
-// delta [R x ldd] = dl * w * (H > 0) (element type e), and per-block partial
-// sums part[blk] = {loss, sum dl, sum_r dl * H[r][0..Hd)} (Hd + 2 floats).
+// delta [R x ldd] = dl * w * (H > 0) (element type e).  Each block writes
+// partial sums part[blk] = {loss, sum dl, sum_r dl * H[r][0..Hd)} (Hd + 2
+// floats); a second kernel reduces them in block order:
+// *loss_out = sum loss / R (loss_out may be null), w -= scale * sum dl*H,
+// b -= scale * sum dl.
 struct LogitJob {
   const void* H; int64_t ldh; int Hd, R;
   float* w; float* b; const float* y;
   void* delta; int64_t ldd; int relu;
-  float* part; int blocks;
+  float* part; int blocks; float scale; float* loss_out;
 };
 hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st);
-// Reduce the partials: w -= scale * sum dl*H, b -= scale * sum dl,
-// *loss_out = sum loss / R (loss_out may be null).
-hipError_t launch_logit_sgd(const LogitJob& j, float scale, float* loss_out, hipStream_t st);
+hipError_t launch_logit_reduce(const LogitJob& j, hipStream_t st);
 
 // Segments mapping a row of a tick to its global sample id (<= 8 replicas).
 struct RowMap {

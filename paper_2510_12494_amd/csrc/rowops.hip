@@ -96,21 +96,32 @@ __global__ __launch_bounds__(256) void k_logit_bce(LogitJob j) {
   }
   if (lane == 0) { red[wave][0] = lsum; red[wave][1] = gb; }
   __syncthreads();
-  for (int c = threadIdx.x; c < j.Hd + 2; c += 256)
-    j.part[(int64_t)blockIdx.x * (j.Hd + 2) + c] = red[0][c] + red[1][c] + red[2][c] + red[3][c];
+  const int W = j.Hd + 2;
+  for (int c = threadIdx.x; c < W; c += 256)
+    j.part[(int64_t)blockIdx.x * W + c] = red[0][c] + red[1][c] + red[2][c] + red[3][c];
 }
 
-__global__ __launch_bounds__(256) void k_logit_sgd(LogitJob j, float scale, float* loss_out) {
+// Sum of the logit kernel's block partials in block order + the logit
+// layer's SGD step and the mean loss.
+__global__ __launch_bounds__(256) void k_logit_reduce(LogitJob j) {
   const int W = j.Hd + 2;
-  for (int c = threadIdx.x; c < W; c += blockDim.x) {
+  for (int c = threadIdx.x; c < W; c += 256) {
     float s = 0.f;
-    for (int b = 0; b < j.blocks; ++b) s += j.part[(int64_t)b * W + c];
+    int b = 0;
+    for (; b + 8 <= j.blocks; b += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = j.part[(int64_t)(b + u) * W + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; b < j.blocks; ++b) s += j.part[(int64_t)b * W + c];
     if (c == 0) {
-      if (loss_out) *loss_out = s / (float)j.R;
+      if (j.loss_out) *j.loss_out = s / (float)j.R;
     } else if (c == 1) {
-      j.b[0] -= scale * s;
+      j.b[0] -= j.scale * s;
     } else {
-      j.w[c - 2] -= scale * s;
+      j.w[c - 2] -= j.scale * s;
     }
   }
 }
@@ -267,16 +278,16 @@ hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st) {
   return hipGetLastError();
 }
 
+hipError_t launch_logit_reduce(const LogitJob& j, hipStream_t st) {
+  hipLaunchKernelGGL(k_logit_reduce, dim3(1), dim3(256), 0, st, j);
+  return hipGetLastError();
+}
+
 hipError_t launch_philox_words(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0,
                                int rows, int groups, uint32_t* out, hipStream_t st) {
   const int64_t total = (int64_t)rows * groups;
   hipLaunchKernelGGL(k_philox_words, dim3(grid_for(total, 256, 4096)), dim3(256), 0, st, seed,
                      step, tag, row0, rows, groups, out);
-  return hipGetLastError();
-}
-
-hipError_t launch_logit_sgd(const LogitJob& j, float scale, float* loss_out, hipStream_t st) {
-  hipLaunchKernelGGL(k_logit_sgd, dim3(1), dim3(256), 0, st, j, scale, loss_out);
   return hipGetLastError();
 }
 

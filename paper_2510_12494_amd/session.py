@@ -85,6 +85,7 @@ class Session:
         torch.cuda.synchronize(self.dev)
         self.set_params(params)
         self.loss = torch.zeros(1 << 16, dtype=torch.float32, device=self.dev)
+        self._cache = {}
 
     # ------------------------------------------------------------ params
     @staticmethod
@@ -132,14 +133,33 @@ class Session:
             out.append(b)
         return out
 
-    def step(self, t: int, n_groups: int | None = None):
-        """Tick t of the deterministic schedule (n_groups None: unbounded)."""
+    def _cached(self, party: str, g: int):
+        """ctypes array of group g's replica batches (cached per group)."""
+        key = (party, g)
+        hit = self._cache.get(key)
+        if hit is None:
+            bs = self.batches(party, g)
+            hit = ((V.vfl_batch * len(bs))(*bs), len(bs))
+            if len(self._cache) < 4096:
+                self._cache[key] = hit
+        return hit
+
+    def step(self, t: int, n_groups: int | None = None, epoch: int | None = None):
+        """Tick t of the deterministic schedule (n_groups None: unbounded).
+        ``epoch``: groups per epoch, so that batch descriptors are reused."""
         s = self.w.staleness
-        bb = self.batches("B", t) if (n_groups is None or t < n_groups) else []
+        lib = V.library()
+        nb = na = 0
+        bb = aa = None
+        if n_groups is None or t < n_groups:
+            bb, nb = self._cached("B", t if epoch is None else t % epoch)
         u = t - s
-        aa = self.batches("A", u) if (u >= 0 and (n_groups is None or u < n_groups)) else []
-        lp = self.loss.data_ptr() + 4 * (u % self.loss.numel()) if aa else 0
-        V.vfl_step(self.ctx, t, aa, bb, lp)
+        if u >= 0 and (n_groups is None or u < n_groups):
+            aa, na = self._cached("A", u if epoch is None else u % epoch)
+        lp = self.loss.data_ptr() + 4 * (u % self.loss.numel()) if na else None
+        st = lib.vfl_step(self.ctx, t, aa, na, bb, nb, lp)
+        if st != V.VFL_OK:
+            V._chk(st, "vfl_step", self.ctx)
 
     def message(self, which: int, g: int) -> tuple[np.ndarray, tuple]:
         rows = sum(c for _, c in self.rows_of(g))

@@ -23,7 +23,10 @@ STATUS_NAMES = {0: "VFL_OK", 1: "VFL_E_INVALID", 2: "VFL_E_NOMEM", 3: "VFL_E_HIP
 EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
-           "vfl_philox", "vfl_last_error", "vfl_destroy")
+           "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_last_error",
+           "vfl_destroy")
+KERNEL_CLASSES = ("gemm_fwd", "gemm_dx", "gemm_dw", "reduce", "logit", "clip_noise", "cut_bwd",
+                  "cast", "gather", "emb_sgd")
 
 
 class vfl_bottom_spec(C.Structure):
@@ -77,6 +80,8 @@ def _load():
         "vfl_schedule_tick": [I64, I32, I64, C.POINTER(I64)],
         "vfl_check": [P, C.POINTER(U32)],
         "vfl_philox": [U64, U32, U32, U32, I32, I32, P, P],
+        "vfl_timing_enable": [P, U32],
+        "vfl_timing_read": [P, I32, C.POINTER(C.c_double), C.POINTER(I64), C.POINTER(C.c_double)],
         "vfl_destroy": [P],
     }
     for name, args in sig.items():
@@ -188,6 +193,17 @@ def vfl_philox(seed: int, step: int, tag: int, row0: int, rows: int, groups: int
                stream: int = 0):
     _chk(_lib.vfl_philox(seed, step, tag, row0, rows, groups, C.c_void_p(out_ptr),
                          C.c_void_p(stream or None)), "vfl_philox")
+
+
+def vfl_timing_enable(ctx, mask: int):
+    _chk(_lib.vfl_timing_enable(ctx, mask), "vfl_timing_enable", ctx)
+
+
+def vfl_timing_read(ctx, cls: int):
+    """(milliseconds, launches, algorithmic work) summed over the class."""
+    ms, n, wk = C.c_double(0), C.c_int64(0), C.c_double(0)
+    _chk(_lib.vfl_timing_read(ctx, cls, C.byref(ms), C.byref(n), C.byref(wk)), "vfl_timing_read", ctx)
+    return ms.value, n.value, wk.value
 
 
 def vfl_last_error(ctx) -> str:
