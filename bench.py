@@ -143,6 +143,7 @@ def main():
     for _ in range(args.steps):
         sess.step(t, epoch=epoch)
         t += 1
+    t_host = time.perf_counter() - t0
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms, launches, work = V.vfl_timing_read(sess.ctx, dom_i)
@@ -177,6 +178,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.dtype, "data": "synthetic (seeded, resident in HBM)",
         "mfma_util_pct": 100.0 * mfma, "gemm_gflop_per_step": flops / 1e9,
+        "host_enqueue_us_per_step": t_host / args.steps * 1e6,
         "config": {"workload": w.name, "rows": w.n_rows, "rows_per_tick": R, "batch": w.batch,
                    "replicas": w.replicas, "staleness": w.staleness,
                    "bottom_A": "-".join(map(str, [w.A.d_in] + w.A.widths)),

@@ -12,6 +12,14 @@
 // g's gradient event, recorded by A after A read embedding g; A rewrites
 // gradient slot u mod (s+1) with group u + s + 1 only after waiting for that
 // group's embedding event, recorded by B after its backward of group u.
+//
+// Backward order per party: the input-gradient chain first (every layer's
+// delta kept in its own buffer), then one launch for all layers' weight
+// gradients (SGD fused, operand copies of the new weights refreshed) and one
+// reduction launch for the layers whose rows were split across blocks.  The
+// refreshed copies of party B land in the slot of the group just
+// back-propagated, which is the slot B's next forward uses; a forward casts
+// the master weights only when its slot's copies hold another version.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -29,7 +37,7 @@ using namespace vfl;
 namespace {
 
 constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
-constexpr int kLogitBlocks = 256;
+constexpr int kLogitBlocks = 512;
 
 int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
 
@@ -42,21 +50,6 @@ struct Layout {
     return o;
   }
 };
-
-struct DwPlan { int rps = 0, splits = 1; };
-
-DwPlan dw_plan(Elt e, int R, int N, int K) {
-  DwPlan p;
-  const int RE = dw_stage_rows(e), T = dw_tile(e);
-  const int tiles = ((N + T - 1) / T) * ((K + T - 1) / T);
-  const int max_splits = std::max(1, (R + RE - 1) / RE);
-  int s = std::min(max_splits, std::max(1, (256 + tiles - 1) / tiles));
-  int rps = (R + s - 1) / s;
-  rps = (rps + RE - 1) / RE * RE;
-  p.rps = rps;
-  p.splits = (R + rps - 1) / rps;
-  return p;
-}
 
 struct Party {
   vfl_bottom_spec spec{};
@@ -71,12 +64,10 @@ struct Party {
   size_t act[kMaxSlots][VFL_MAX_LAYERS]{};
   size_t zhat[kMaxSlots]{};          // published embedding (party B)
   size_t norm[kMaxSlots]{}, cfac[kMaxSlots]{};
-  size_t dbuf[2]{};
-  int64_t ld_delta = 0;
+  size_t dlt[VFL_MAX_LAYERS]{};      // gradient w.r.t. each layer's pre-activation
   size_t gx = 0;
   int64_t ldgx = 0;
-  DwPlan dw[VFL_MAX_LAYERS];
-  size_t part = 0, partb = 0;
+  size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
 };
 
 struct Top {
@@ -88,7 +79,8 @@ struct Top {
   size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{};
   size_t Wq[VFL_MAX_LAYERS]{}, Wtq[VFL_MAX_LAYERS]{};
   size_t act[VFL_MAX_LAYERS]{};
-  DwPlan dw[VFL_MAX_LAYERS];
+  size_t dlt[VFL_MAX_LAYERS]{};
+  size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
   size_t logit_part = 0;
 };
 
@@ -97,10 +89,10 @@ struct Plan {
   int s = 0, k = 1, B = 1, R = 1, dA = 0, dB = 0;
   Party A, P;                         // P: party B (passive)
   Top T;
+  int splits_a = 1, rps_a = 0, splits_b = 1, rps_b = 0;   // weight-gradient row chunks
   size_t ring_g[kMaxSlots]{};
   size_t gpre = 0;                    // float32 gradient message before clip/noise
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
-  size_t part_a = 0, partb_a = 0;     // dW partials, stream A
   size_t total = 0;
 };
 
@@ -115,9 +107,6 @@ struct SlotState {
   RowMap rmap;
 };
 
-}  // namespace
-
-namespace {
 // Event pairs bracketing the launches of the selected kernel classes.
 struct Timing {
   static constexpr int kPool = 4096;
@@ -131,6 +120,7 @@ struct Timing {
   double ms[VFL_K_COUNT]{}, wk[VFL_K_COUNT]{};
   int64_t n[VFL_K_COUNT]{};
 };
+
 }  // namespace
 
 struct vfl_ctx {
@@ -143,13 +133,15 @@ struct vfl_ctx {
   // B
   int64_t b_next_fwd = 0, b_next_bwd = 0, b_version = 0, b_pub_next = 0;
   SlotState bslot[kMaxSlots];
+  int64_t b_copy_version[kMaxSlots];  // version held by each slot's operand copies (-1: none)
   int64_t grad_group[kMaxSlots];
   int grad_rows[kMaxSlots]{};
-  // A
-  int64_t a_next = 0;
+  // A (and the top model)
+  int64_t a_next = 0, a_version = 0, a_copy_version = -1;
   int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
   SlotState aslot;
   const float* a_labels = nullptr;
+  float* a_loss = nullptr;
   std::vector<int64_t> trace;
   std::string err;
 };
@@ -185,6 +177,17 @@ bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
   return true;
 }
 
+// rows per weight-gradient chunk for a launch over `tiles` output tiles:
+// aim at >= 256 blocks, chunks a multiple of the kernel's stage depth
+void dw_chunks(Elt e, int R, int tiles, int& splits, int& rps) {
+  const int RE = dw_stage_rows(e);
+  const int max_splits = std::max(1, (R + RE - 1) / RE);
+  int s = std::min(max_splits, std::max(1, (256 + tiles - 1) / tiles));
+  rps = (R + s - 1) / s;
+  rps = (rps + RE - 1) / RE * RE;
+  splits = (R + rps - 1) / rps;
+}
+
 std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* t,
                        const vfl_opts* o, Plan& p) {
   std::string why;
@@ -201,9 +204,9 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   if (t->widths[t->n_layers - 1] != 1) return "last top layer must have width 1";
   for (int j = 0; j + 1 < t->n_layers; ++j)
     if (t->widths[j] < 1 || t->widths[j] > 65536) return "bad top width";
-  if (t->widths[t->n_layers - 2] > 512) return "last hidden top width must be <= 512";
+  if (t->widths[t->n_layers - 2] > kMaxLogitCols) return "last hidden top width must be <= 512";
   if (a->widths[a->n_layers - 1] % 8) return "party A's embedding width must be a multiple of 8";
-  if (b->widths[b->n_layers - 1] > 65536) return "bad party B width";
+  if (a->n_layers + t->n_layers - 1 > kMaxDw) return "party A + top hidden layers must be <= 8";
   if ((int64_t)o->batch * o->replicas > (1 << 28)) return "rows per tick too large";
 
   p.e = o->dtype == VFL_BF16 ? BF16 : F32;
@@ -220,7 +223,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     P.L = s->n_layers;
     P.din = s->n_cat * s->emb_dim + s->dense_in;
     P.nslots = nslots;
-    int in = P.din, maxw = P.din;
+    int in = P.din;
     for (int l = 0; l < P.L; ++l) {
       P.in[l] = in;
       P.out[l] = s->widths[l];
@@ -229,7 +232,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       P.ldt[l] = ld_of(P.out[l]);
       P.W[l] = ly.take(sizeof(float) * (size_t)P.out[l] * in);
       P.b[l] = ly.take(sizeof(float) * (size_t)P.out[l]);
-      maxw = std::max(maxw, P.out[l]);
+      P.dlt[l] = ly.take((size_t)es * R * ld_of(P.out[l]));
       in = P.out[l];
     }
     if (s->n_cat) P.T = ly.take(sizeof(float) * (size_t)s->n_cat * s->vocab * s->emb_dim);
@@ -250,10 +253,13 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
         }
       }
     }
-    return maxw;
+    if (s->n_cat) {
+      P.ldgx = ld_of(s->n_cat * s->emb_dim);
+      P.gx = ly.take(sizeof(float) * R * P.ldgx);
+    }
   };
 
-  int maxwA = party(p.A, a, 1, false);
+  party(p.A, a, 1, false);
   party(p.P, b, p.s + 1, true);
   p.dA = p.A.out[p.A.L - 1];
   p.dB = p.P.out[p.P.L - 1];
@@ -274,54 +280,33 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       T.Wq[j] = ly.take((size_t)es * T.out[j] * T.ldq[j]);
       T.Wtq[j] = ly.take((size_t)es * T.in[j] * T.ldt[j]);
       T.act[j] = ly.take((size_t)es * R * ld_of(T.out[j]));
-      maxwA = std::max(maxwA, T.out[j]);
+      T.dlt[j] = ly.take((size_t)es * R * ld_of(T.out[j]));
     }
     in = T.out[j];
   }
-  maxwA = std::max(maxwA, p.dA + p.dB);
   T.logit_part = ly.take(sizeof(float) * kLogitBlocks * (T.out[T.H - 1] + 2));
 
-  // delta ping-pong buffers and embedding-gradient scratch
-  p.A.ld_delta = ld_of(maxwA);
-  int maxwB = 0;
-  for (int l = 0; l < p.P.L; ++l) maxwB = std::max(maxwB, std::max(p.P.out[l], p.P.in[l]));
-  p.P.ld_delta = ld_of(maxwB);
-  for (int i = 0; i < 2; ++i) {
-    p.A.dbuf[i] = ly.take((size_t)es * R * p.A.ld_delta);
-    p.P.dbuf[i] = ly.take((size_t)es * R * p.P.ld_delta);
-  }
-  for (Party* P : {&p.A, &p.P}) {
-    if (P->spec.n_cat) {
-      P->ldgx = ld_of(P->spec.n_cat * P->spec.emb_dim);
-      P->gx = ly.take(sizeof(float) * R * P->ldgx);
-    }
-  }
   // messages
   for (int q = 0; q <= p.s; ++q) p.ring_g[q] = ly.take((size_t)es * R * ld_of(p.dB));
   if (o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD)) p.gpre = ly.take(sizeof(float) * R * ld_of(p.dB));
   p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
 
-  // weight-gradient partials (one scratch per stream, sized for its largest layer)
-  size_t need_a = 0, needb_a = 0, need_b = 0, needb_b = 0;
-  for (int l = 0; l < p.A.L; ++l) {
-    p.A.dw[l] = dw_plan(p.e, p.R, p.A.out[l], p.A.in[l]);
-    need_a = std::max(need_a, (size_t)p.A.dw[l].splits * p.A.out[l] * p.A.in[l]);
-    needb_a = std::max(needb_a, (size_t)p.A.dw[l].splits * p.A.out[l]);
-  }
-  for (int j = 0; j < T.H; ++j) {
-    T.dw[j] = dw_plan(p.e, p.R, T.out[j], T.in[j]);
-    need_a = std::max(need_a, (size_t)T.dw[j].splits * T.out[j] * T.in[j]);
-    needb_a = std::max(needb_a, (size_t)T.dw[j].splits * T.out[j]);
-  }
-  for (int l = 0; l < p.P.L; ++l) {
-    p.P.dw[l] = dw_plan(p.e, p.R, p.P.out[l], p.P.in[l]);
-    need_b = std::max(need_b, (size_t)p.P.dw[l].splits * p.P.out[l] * p.P.in[l]);
-    needb_b = std::max(needb_b, (size_t)p.P.dw[l].splits * p.P.out[l]);
-  }
-  p.part_a = ly.take(sizeof(float) * need_a);
-  p.partb_a = ly.take(sizeof(float) * needb_a);
-  p.P.part = ly.take(sizeof(float) * need_b);
-  p.P.partb = ly.take(sizeof(float) * needb_b);
+  // weight-gradient row chunks and partials (one region per layer: all
+  // layers of a party are in flight in the same launch)
+  int tiles_a = 0, tiles_b = 0;
+  for (int l = 0; l < p.A.L; ++l) tiles_a += dw_tiles(p.A.out[l], p.A.in[l]);
+  for (int j = 0; j < T.H; ++j) tiles_a += dw_tiles(T.out[j], T.in[j]);
+  for (int l = 0; l < p.P.L; ++l) tiles_b += dw_tiles(p.P.out[l], p.P.in[l]);
+  dw_chunks(p.e, p.R, tiles_a, p.splits_a, p.rps_a);
+  dw_chunks(p.e, p.R, tiles_b, p.splits_b, p.rps_b);
+  auto parts = [&](int splits, int N, int K, size_t& pw, size_t& pb) {
+    if (splits <= 1) return;
+    pw = ly.take(sizeof(float) * (size_t)splits * N * K);
+    pb = ly.take(sizeof(float) * (size_t)splits * N);
+  };
+  for (int l = 0; l < p.A.L; ++l) parts(p.splits_a, p.A.out[l], p.A.in[l], p.A.part[l], p.A.partb[l]);
+  for (int j = 0; j < T.H; ++j) parts(p.splits_a, T.out[j], T.in[j], T.part[j], T.partb[j]);
+  for (int l = 0; l < p.P.L; ++l) parts(p.splits_b, p.P.out[l], p.P.in[l], p.P.part[l], p.P.partb[l]);
   p.total = (ly.off + 255) / 256 * 256;
   return "";
 }
@@ -366,7 +351,7 @@ vfl_status take_batches(vfl_ctx* c, const Party& P, const vfl_batch* br, int n, 
   return VFL_OK;
 }
 
-// harvest one finished event pair into its class totals
+// ------------------------------------------------------------- timing hook
 void harvest(vfl_ctx* c, int i) {
   Timing& T = c->tm;
   if (!T.used[i]) return;
@@ -405,6 +390,10 @@ void tend(vfl_ctx* c, int i, hipStream_t st) {
 
 double gemm_flops(int M, int N, int K) { return 2.0 * M * (double)N * K; }
 
+int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
+int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
+
+// ------------------------------------------------------------ enqueue steps
 vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipStream_t st) {
   CastJob jobs[2 * VFL_MAX_LAYERS + 2];
   int n = 0;
@@ -457,56 +446,97 @@ vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const Sl
   return VFL_OK;
 }
 
-// Backward of a party's bottom layers from delta (gradient w.r.t. the last
-// layer's pre-activation) in dbuf[cur]; SGD on the master parameters.
-vfl_status enqueue_bottom_backward(vfl_ctx* c, const Party& P, int slot, const SlotState& in,
-                                   int cur, float* part, float* partb, hipStream_t st) {
+// Input-gradient chain of a bottom model: from dlt[L-1] down to dlt[0], and
+// for tables the float32 gradient of the gathered input columns.
+vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStream_t st) {
   const Plan& p = c->p;
-  const int R = in.rows;
-  const float scale = c->o.lr / (float)R;
-  const void* x = P.spec.n_cat ? (const void*)(c->ws + P.x0[slot]) : in.dense;
-  const int64_t ldx = P.spec.n_cat ? P.ldx0 : in.ld;
-  for (int l = P.L - 1; l >= 0; --l) {
-    const void* D = c->ws + P.dbuf[cur];
-    GemmDW d;
-    d.D = D; d.ldd = P.ld_delta;
-    d.X1 = l == 0 ? x : c->ws + P.act[slot][l - 1];
-    d.ldx1 = l == 0 ? ldx : ld_of(P.out[l - 1]);
-    d.part = part; d.partb = partb;
-    d.W = at<float>(c, P.W[l]); d.bias = at<float>(c, P.b[l]); d.scale = scale;
-    d.R = R; d.N = P.out[l]; d.K = P.in[l];
-    d.rows_per_split = P.dw[l].rps;
-    d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
-    TIMED(VFL_K_GEMM_DW, gemm_flops(R, d.N, d.K), st, launch_gemm_dw(p.e, d, st));
-    if (d.splits > 1)
-      TIMED(VFL_K_REDUCE, 4.0 * ((double)d.N * d.K + d.N) * (d.splits + 2), st, launch_dw_reduce(d, st));
-    if (l > 0) {
-      GemmNT g;
-      g.A1 = D; g.lda1 = P.ld_delta;
-      g.B = c->ws + P.Wtq[slot][l]; g.ldb = P.ldt[l];
-      g.C1 = c->ws + P.dbuf[cur ^ 1]; g.ldc1 = P.ld_delta;
-      if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
-      g.M = R; g.N = P.in[l]; g.K = P.out[l];
-      TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-      cur ^= 1;
-    } else if (P.spec.n_cat) {
-      GemmNT g;
-      g.A1 = D; g.lda1 = P.ld_delta;
-      g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
-      g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
-      g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
-      TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-      ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                    at<float>(c, P.gx), P.ldgx, R, scale};
-      TIMED(VFL_K_EMB_SGD, (double)R * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
-            launch_scatter_sgd(sj, st));
-    }
+  for (int l = P.L - 1; l >= 1; --l) {
+    GemmNT g;
+    g.A1 = c->ws + P.dlt[l]; g.lda1 = ld_of(P.out[l]);
+    g.B = c->ws + P.Wtq[slot][l]; g.ldb = P.ldt[l];
+    g.C1 = c->ws + P.dlt[l - 1]; g.ldc1 = ld_of(P.out[l - 1]);
+    if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
+    g.M = R; g.N = P.in[l]; g.K = P.out[l];
+    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
+  }
+  if (P.spec.n_cat) {
+    GemmNT g;
+    g.A1 = c->ws + P.dlt[0]; g.lda1 = ld_of(P.out[0]);
+    g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
+    g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
+    g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
+    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
   return VFL_OK;
 }
 
-int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
-int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
+void add_dw(MultiDW& m, const void* D, int N, const void* X1, int64_t ldx1, const void* X2,
+            int64_t ldx2, int ksplit, int K, float* W, float* bias, void* Wq, int64_t ldq,
+            void* Wtq, int64_t ldt, float* part, float* partb, int splits, int rps) {
+  GemmDW& d = m.p[m.n++];
+  d.D = D; d.ldd = ld_of(N);
+  d.X1 = X1; d.ldx1 = ldx1; d.X2 = X2; d.ldx2 = ldx2; d.ksplit = ksplit;
+  d.W = W; d.bias = bias; d.Wq = Wq; d.ldq = ldq; d.Wtq = Wtq; d.ldt = ldt;
+  d.part = part; d.partb = partb;
+  d.N = N; d.K = K;
+  d.splits = splits; d.rows_per_split = rps;
+}
+
+// Bottom layers' weight gradients of one party appended to m.
+void add_party_dw(vfl_ctx* c, MultiDW& m, const Party& P, int slot, const SlotState& in,
+                  int splits, int rps) {
+  const void* x = P.spec.n_cat ? (const void*)(c->ws + P.x0[slot]) : in.dense;
+  const int64_t ldx = P.spec.n_cat ? P.ldx0 : in.ld;
+  for (int l = 0; l < P.L; ++l)
+    add_dw(m, c->ws + P.dlt[l], P.out[l], l == 0 ? x : c->ws + P.act[slot][l - 1],
+           l == 0 ? ldx : ld_of(P.out[l - 1]), nullptr, 0, 1 << 30, P.in[l], at<float>(c, P.W[l]),
+           at<float>(c, P.b[l]), c->ws + P.Wq[slot][l], P.ldq[l], c->ws + P.Wtq[slot][l], P.ldt[l],
+           P.part[l] ? at<float>(c, P.part[l]) : nullptr, P.partb[l] ? at<float>(c, P.partb[l]) : nullptr,
+           splits, rps);
+}
+
+vfl_status enqueue_weight_update(vfl_ctx* c, MultiDW& m, const LogitJob* lj, hipStream_t st) {
+  const Plan& p = c->p;
+  double flops = 0, rbytes = 0;
+  bool split = false;
+  for (int q = 0; q < m.n; ++q) {
+    flops += gemm_flops(m.R, m.p[q].N, m.p[q].K);
+    if (m.p[q].splits > 1) {
+      split = true;
+      rbytes += 4.0 * ((double)m.p[q].N * m.p[q].K + m.p[q].N) * (m.p[q].splits + 2);
+    }
+  }
+  TIMED(VFL_K_GEMM_DW, flops, st, launch_multi_dw(p.e, m, st));
+  if (split || lj) {
+    if (lj) rbytes += 4.0 * lj->blocks * (lj->Hd + 2) + 8.0 * lj->Hd;
+    TIMED(VFL_K_REDUCE, rbytes, st, launch_multi_reduce(p.e, m, lj, st));
+  }
+  return VFL_OK;
+}
+
+vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const SlotState& in, float scale,
+                             hipStream_t st) {
+  if (!P.spec.n_cat) return VFL_OK;
+  ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
+                at<float>(c, P.gx), P.ldgx, in.rows, scale};
+  TIMED(VFL_K_EMB_SGD, (double)in.rows * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
+        launch_scatter_sgd(sj, st));
+  return VFL_OK;
+}
+
+LogitJob logit_job(vfl_ctx* c, int R, float* loss_dev) {
+  const Plan& p = c->p;
+  const Top& T = p.T;
+  LogitJob lj{};
+  lj.H = c->ws + T.act[T.H - 1]; lj.ldh = ld_of(T.out[T.H - 1]); lj.Hd = T.out[T.H - 1]; lj.R = R;
+  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = c->a_labels;
+  lj.delta = c->ws + T.dlt[T.H - 1]; lj.ldd = ld_of(T.out[T.H - 1]); lj.relu = T.relu[T.H - 1];
+  lj.part = at<float>(c, T.logit_part);
+  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 15) / 16));
+  lj.scale = c->o.lr / (float)R;
+  lj.loss_out = loss_dev;
+  return lj;
+}
 
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
   const Plan& p = c->p;
@@ -561,7 +591,10 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
   c->ws = (char*)workspace;
   c->sa = (hipStream_t)stream_a;
   c->sb = (hipStream_t)stream_b;
-  for (int q = 0; q < kMaxSlots; ++q) c->grad_group[q] = -1;
+  for (int q = 0; q < kMaxSlots; ++q) {
+    c->grad_group[q] = -1;
+    c->b_copy_version[q] = -1;
+  }
   hipError_t e = hipSuccess;
   for (int q = 0; q <= c->p.s && e == hipSuccess; ++q) {
     e = hipEventCreateWithFlags(&c->ev_emb[q], hipEventDisableTiming);
@@ -588,6 +621,11 @@ vfl_status vfl_set_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kin
   HIPCHK(hipStreamSynchronize(c->sa));
   HIPCHK(hipStreamSynchronize(c->sb));
   HIPCHK(hipMemcpy(c->ws + off, src, nb, src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice));
+  // operand copies of the changed party no longer hold its weights
+  if (party == VFL_PARTY_B)
+    for (int q = 0; q < kMaxSlots; ++q) c->b_copy_version[q] = -1;
+  else
+    c->a_copy_version = -1;
   return VFL_OK;
 }
 
@@ -620,9 +658,12 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
     st.group = group;
     st.version = c->b_version;
     st.published = false;
-    if ((r = enqueue_cast(c, p.P, slot, nullptr, c->sb))) return r;
+    if (c->b_copy_version[slot] != c->b_version) {
+      if ((r = enqueue_cast(c, p.P, slot, nullptr, c->sb))) return r;
+      c->b_copy_version[slot] = c->b_version;
+    }
     const bool extra = c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
-    const int32_t hdr[3] = {(int32_t)group, (int32_t)(group), (int32_t)c->b_version};
+    const int32_t hdr[3] = {(int32_t)group, (int32_t)group, (int32_t)c->b_version};
     if ((r = enqueue_bottom_forward(c, p.P, slot, st, c->sb, extra ? nullptr : hdr_ptr(c, 0, slot), hdr)))
       return r;
     c->bslot[slot] = st;
@@ -636,7 +677,10 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
     vfl_status r = take_batches(c, p.A, br, n, true, st);
     if (r) return r;
     st.group = group;
-    if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+    if (c->a_copy_version != c->a_version) {
+      if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+      c->a_copy_version = c->a_version;
+    }
     if ((r = enqueue_bottom_forward(c, p.A, 0, st, c->sa, nullptr, nullptr))) return r;
     c->aslot = st;
     c->a_labels = br[0].labels;
@@ -686,7 +730,6 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
     return fail(c, VFL_E_NOT_READY, "embedding of this group not published");
   if (bs.rows != c->aslot.rows) return fail(c, VFL_E_INVALID, "A and B batches differ in rows");
   const int R = c->aslot.rows;
-  const float scale = c->o.lr / (float)R;
   hipStream_t st = c->sa;
   HIPCHK(hipStreamWaitEvent(st, c->ev_emb[slot], 0));
   const Top& T = p.T;
@@ -708,46 +751,22 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
     g.M = R; g.N = T.out[j]; g.K = T.in[j];
     TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
-  // logit + BCE, logit-layer SGD
-  int cur = 0;
-  LogitJob lj{};
-  lj.H = c->ws + T.act[T.H - 1]; lj.ldh = ld_of(T.out[T.H - 1]); lj.Hd = T.out[T.H - 1]; lj.R = R;
-  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = c->a_labels;
-  lj.delta = c->ws + p.A.dbuf[cur]; lj.ldd = p.A.ld_delta; lj.relu = T.relu[T.H - 1];
-  lj.part = at<float>(c, T.logit_part);
-  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 63) / 64));
-  lj.scale = scale; lj.loss_out = loss_dev;
+  // logit + BCE; its reduction and SGD run with the weight update
+  LogitJob lj = logit_job(c, R, loss_dev);
   TIMED(VFL_K_LOGIT, (double)R * lj.Hd * 2.0 * elt_size(p.e) + 4.0 * R, st, launch_logit_bce(p.e, lj, st));
-  TIMED(VFL_K_REDUCE, 4.0 * lj.blocks * (lj.Hd + 2) + 8.0 * lj.Hd, st, launch_logit_reduce(lj, st));
-  // hidden layers backward
-  float* part = at<float>(c, p.part_a);
-  float* partb = at<float>(c, p.partb_a);
+  // input-gradient chain of the top model; the last product splits into A's
+  // cut-layer delta and the per-row gradient message for B
   const bool gextra = c->o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
   for (int j = T.H - 1; j >= 0; --j) {
-    const void* D = c->ws + p.A.dbuf[cur];
-    GemmDW d;
-    d.D = D; d.ldd = p.A.ld_delta;
-    if (j == 0) {
-      d.X1 = zA; d.ldx1 = ld_of(p.dA); d.X2 = zB; d.ldx2 = ld_of(p.dB); d.ksplit = p.dA;
-    } else {
-      d.X1 = c->ws + T.act[j - 1]; d.ldx1 = ld_of(T.out[j - 1]);
-    }
-    d.part = part; d.partb = partb;
-    d.W = at<float>(c, T.W[j]); d.bias = at<float>(c, T.b[j]); d.scale = scale;
-    d.R = R; d.N = T.out[j]; d.K = T.in[j];
-    d.rows_per_split = T.dw[j].rps;
-    d.splits = (R + d.rows_per_split - 1) / d.rows_per_split;
-    TIMED(VFL_K_GEMM_DW, gemm_flops(R, d.N, d.K), st, launch_gemm_dw(p.e, d, st));
-    if (d.splits > 1)
-      TIMED(VFL_K_REDUCE, 4.0 * ((double)d.N * d.K + d.N) * (d.splits + 2), st, launch_dw_reduce(d, st));
     GemmNT g;
-    g.A1 = D; g.lda1 = p.A.ld_delta;
+    g.A1 = c->ws + T.dlt[j]; g.lda1 = ld_of(T.out[j]);
     g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
-    g.C1 = c->ws + p.A.dbuf[cur ^ 1]; g.ldc1 = p.A.ld_delta;
     g.M = R; g.N = T.in[j]; g.K = T.out[j];
     if (j > 0) {
+      g.C1 = c->ws + T.dlt[j - 1]; g.ldc1 = ld_of(T.out[j - 1]);
       if (T.relu[j - 1]) { g.mask = c->ws + T.act[j - 1]; g.ldm = ld_of(T.out[j - 1]); }
     } else {
+      g.C1 = c->ws + p.A.dlt[p.A.L - 1]; g.ldc1 = ld_of(p.dA);
       if (p.A.relu[p.A.L - 1]) { g.mask = zA; g.ldm = ld_of(p.dA); }
       g.nsplit = p.dA;
       if (gextra) { g.C2 = c->ws + p.gpre; g.ldc2 = ld_of(p.dB); g.c2_f32 = 1; }
@@ -758,7 +777,6 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
       }
     }
     TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-    cur ^= 1;
   }
   if (gextra) {
     ClipNoiseJob j{};
@@ -776,6 +794,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
   HIPCHK(hipEventRecord(c->ev_grad[slot], st));
   c->grad_group[slot] = group;
   c->grad_rows[slot] = R;
+  c->a_loss = loss_dev;
   c->a_phase = 2;
   return VFL_OK;
 }
@@ -786,10 +805,30 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
   if (party == VFL_PARTY_A) {
     if (group != c->a_next || c->a_phase != 2)
       return fail(c, VFL_E_STATE, "A's backward must follow its top step");
-    // the top backward left A's cut-layer delta in dbuf[T.H & 1]
-    vfl_status r = enqueue_bottom_backward(c, p.A, 0, c->aslot, p.T.H & 1, at<float>(c, p.part_a),
-                                           at<float>(c, p.partb_a), c->sa);
+    const int R = c->aslot.rows;
+    vfl_status r = enqueue_dx_chain(c, p.A, 0, R, c->sa);
     if (r) return r;
+    // one weight update for the top model's hidden layers and A's layers,
+    // with the logit layer's reduction, SGD and loss in the same reduction
+    MultiDW m;
+    m.R = R;
+    m.scale = c->o.lr / (float)R;
+    const Top& T = p.T;
+    const void* zA = c->ws + p.A.act[0][p.A.L - 1];
+    const void* zB = c->ws + p.P.zhat[(int)(group % (p.s + 1))];
+    for (int j = 0; j < T.H; ++j)
+      add_dw(m, c->ws + T.dlt[j], T.out[j], j == 0 ? zA : c->ws + T.act[j - 1],
+             j == 0 ? ld_of(p.dA) : ld_of(T.out[j - 1]), j == 0 ? zB : nullptr,
+             j == 0 ? ld_of(p.dB) : 0, j == 0 ? p.dA : 1 << 30, T.in[j], at<float>(c, T.W[j]),
+             at<float>(c, T.b[j]), c->ws + T.Wq[j], T.ldq[j], c->ws + T.Wtq[j], T.ldt[j],
+             T.part[j] ? at<float>(c, T.part[j]) : nullptr, T.partb[j] ? at<float>(c, T.partb[j]) : nullptr,
+             p.splits_a, p.rps_a);
+    add_party_dw(c, m, p.A, 0, c->aslot, p.splits_a, p.rps_a);
+    LogitJob lj = logit_job(c, R, c->a_loss);
+    if ((r = enqueue_weight_update(c, m, &lj, c->sa))) return r;
+    if ((r = enqueue_table_sgd(c, p.A, c->aslot, c->o.lr / (float)R, c->sa))) return r;
+    c->a_version += 1;
+    c->a_copy_version = c->a_version;
     c->a_next = group + 1;
     c->a_phase = 0;
     return VFL_OK;
@@ -808,16 +847,24 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     cj.norm = cj.clip ? at<float>(c, p.P.norm[slot]) : nullptr;
     cj.cfac = cj.clip ? at<float>(c, p.P.cfac[slot]) : nullptr;
     cj.C = c->o.clip_c; cj.relu = p.P.relu[p.P.L - 1];
-    cj.delta = c->ws + p.P.dbuf[0]; cj.ldd = p.P.ld_delta;
+    cj.delta = c->ws + p.P.dlt[p.P.L - 1]; cj.ldd = ld_of(p.dB);
     cj.R = st.rows; cj.D = p.dB;
     cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
     TIMED(VFL_K_CUT_BWD, (double)st.rows * p.dB * 3.0 * elt_size(p.e) + (cj.clip ? 8.0 * st.rows : 0.0),
           c->sb, launch_cut_backward(p.e, cj, c->sb));
-    vfl_status r = enqueue_bottom_backward(c, p.P, slot, st, 0, at<float>(c, p.P.part),
-                                           at<float>(c, p.P.partb), c->sb);
+    vfl_status r = enqueue_dx_chain(c, p.P, slot, st.rows, c->sb);
     if (r) return r;
+    // SGD on B's current weights; the refreshed operand copies go to this
+    // slot, which B's next forward uses
+    MultiDW m;
+    m.R = st.rows;
+    m.scale = c->o.lr / (float)st.rows;
+    add_party_dw(c, m, p.P, slot, st, p.splits_b, p.rps_b);
+    if ((r = enqueue_weight_update(c, m, nullptr, c->sb))) return r;
+    if ((r = enqueue_table_sgd(c, p.P, st, c->o.lr / (float)st.rows, c->sb))) return r;
     c->b_next_bwd = group + 1;
     c->b_version += 1;
+    c->b_copy_version[slot] = c->b_version;
     return VFL_OK;
   }
   return fail(c, VFL_E_INVALID, "bad party");

@@ -254,10 +254,21 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmNT g) {
   }
 }
 
-// Weight gradient.  LDS rows: sQ row n holds D[r][n] for the stage's rows,
-// sP row k holds X[r][k]; both are written transposed from row-major loads.
+// Weight gradients of several layers in one launch.  Block -> (layer,
+// output tile, row chunk).  LDS rows: sQ row n holds D[r][n] for the stage's
+// rows, sP row k holds X[r][k]; both are written transposed from row-major
+// loads.  An unsplit tile applies SGD in its epilogue and refreshes the
+// layer's operand copies; a split tile writes float32 partials for
+// k_multi_reduce.
+template <typename T>
+__device__ __forceinline__ void copy_out(void* Wq, int64_t ldq, void* Wtq, int64_t ldt, int n,
+                                         int k, float w) {
+  if (Wq) store1<T>((T*)Wq + (int64_t)n * ldq + k, w);
+  if (Wtq) store1<T>((T*)Wtq + (int64_t)k * ldt + n, w);
+}
+
 template <typename T, int BN, int BK>
-__global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
+__global__ __launch_bounds__(256) void k_multi_dw(MultiDW m) {
   constexpr int CE = 16 / (int)sizeof(T);
   constexpr int RE = 128 / (int)sizeof(T);       // rows per stage
   constexpr int RH = RE / 8;
@@ -266,15 +277,20 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
   __shared__ __attribute__((aligned(16))) char sP[BK * 128];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  int q = 0;
+#pragma unroll 1
+  while (q + 1 < m.n && (int)blockIdx.x >= m.first_block[q + 1]) ++q;
+  const GemmDW& g = m.p[q];
+  const int lb = blockIdx.x - m.first_block[q];
   const int tiles_k = (g.K + BK - 1) / BK;
-  const int n0 = (blockIdx.x / tiles_k) * BN, k0 = (blockIdx.x % tiles_k) * BK;
-  const int split = blockIdx.y;
+  const int tile = lb / g.splits, split = lb % g.splits;
+  const int n0 = (tile / tiles_k) * BN, k0 = (tile % tiles_k) * BK;
   const int rb = split * g.rows_per_split;
-  const int re = min(g.R, rb + g.rows_per_split);
+  const int re = min(m.R, rb + g.rows_per_split);
   const T* D = (const T*)g.D;
   const T* X1 = (const T*)g.X1;
   const T* X2 = (const T*)g.X2;
-  const bool do_bias = g.partb && (blockIdx.x % tiles_k) == 0;
+  const bool do_bias = (tile % tiles_k) == 0;
 
   f32x4 acc[BN / 32][BK / 32];
 #pragma unroll
@@ -307,16 +323,16 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
       rp[j] = v;
     }
   };
-  auto tstore = [&](char* s, const u32x4& v, int c) {
+  auto tstore = [&](char* sm, const u32x4& v, int c) {
     const int r = crow(c), col0 = ccol(c) * CE;
     const int off = (r % CE) * (int)sizeof(T);
 #pragma unroll
     for (int e = 0; e < CE; ++e) {
-      char* p = s + swz(col0 + e, r / CE) + off;
+      char* ptr = sm + swz(col0 + e, r / CE) + off;
       if constexpr (sizeof(T) == 4) {
-        *(uint32_t*)p = v[e];
+        *(uint32_t*)ptr = v[e];
       } else {
-        *(uint16_t*)p = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
+        *(uint16_t*)ptr = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
       }
     }
   };
@@ -334,9 +350,9 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
       for (int ch = 0; ch < 8; ++ch) {
         u32x4 v = *(const u32x4*)(sQ + swz(tid, ch));
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if constexpr (sizeof(T) == 4) accb += __uint_as_float(v[q]);
-          else accb += __uint_as_float(v[q] << 16) + __uint_as_float(v[q] & 0xffff0000u);
+        for (int u = 0; u < 4; ++u) {
+          if constexpr (sizeof(T) == 4) accb += __uint_as_float(v[u]);
+          else accb += __uint_as_float(v[u] << 16) + __uint_as_float(v[u] & 0xffff0000u);
         }
       }
     }
@@ -345,7 +361,8 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
   }
 
   if (g.splits == 1) {
-    // the block holds the whole row sum: SGD straight from the accumulators
+    // the block holds the whole row sum: SGD from the accumulators, then the
+    // operand copies of the updated weights
 #pragma unroll
     for (int j = 0; j < BN / 32; ++j) {
 #pragma unroll
@@ -354,11 +371,18 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
         const int nb = n0 + wn * (BN / 2) + j * 16 + (lane >> 4) * 4;
         if (k >= g.K) continue;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (nb + r < g.N) g.W[(int64_t)(nb + r) * g.K + k] -= g.scale * acc[j][i][r];
+        for (int r = 0; r < 4; ++r) {
+          const int n = nb + r;
+          if (n < g.N) {
+            float* wp = g.W + (int64_t)n * g.K + k;
+            const float w = *wp - m.scale * acc[j][i][r];
+            *wp = w;
+            copy_out<T>(g.Wq, g.ldq, g.Wtq, g.ldt, n, k, w);
+          }
+        }
       }
     }
-    if (do_bias && tid < BN && n0 + tid < g.N) g.bias[n0 + tid] -= g.scale * accb;
+    if (do_bias && tid < BN && n0 + tid < g.N) g.bias[n0 + tid] -= m.scale * accb;
     return;
   }
   float* part = g.part + (int64_t)split * g.N * g.K;
@@ -377,39 +401,73 @@ __global__ __launch_bounds__(256) void k_gemm_dw(GemmDW g) {
   if (do_bias && tid < BN && n0 + tid < g.N) g.partb[(int64_t)split * g.N + n0 + tid] = accb;
 }
 
-// Sum of the split partials in split order + SGD: four consecutive
-// elements per thread (weights first, then bias), eight splits' loads in
-// flight at a time.
-__global__ __launch_bounds__(256) void k_dw_reduce(GemmDW g) {
-  const int64_t NK = (int64_t)g.N * g.K;
-  const int64_t qw = (NK + 3) / 4, qb = (g.N + 3) / 4;
-  const int64_t t = blockIdx.x * (int64_t)256 + threadIdx.x;
-  if (t >= qw + qb) return;
-  const bool is_w = t < qw;
-  const float* src = is_w ? g.part : g.partb;
-  const int64_t stride = is_w ? NK : g.N;
-  const int64_t base = 4 * (is_w ? t : t - qw);
-  float* dst = (is_w ? g.W : g.bias) + base;
-  const int n = (int)std::min<int64_t>(4, stride - base);
-  float sum[4] = {0.f, 0.f, 0.f, 0.f};
-  int q = 0;
-  for (; q + 8 <= g.splits; q += 8) {
-    float v[8][4];
+// Second stage: sum the split partials of every split layer in split order,
+// apply SGD and refresh the operand copies; optionally the logit kernel's
+// block partials (loss, logit weight and bias gradients).  Thread ranges:
+// [layers' weight quads | layers' bias quads | logit columns].
+template <typename T>
+__global__ __launch_bounds__(256) void k_multi_reduce(MultiDW m, LogitJob lj, int with_logit) {
+  int64_t t = blockIdx.x * (int64_t)256 + threadIdx.x;
+  for (int q = 0; q < m.n; ++q) {
+    const GemmDW& g = m.p[q];
+    if (g.splits <= 1) continue;
+    const int64_t NK = (int64_t)g.N * g.K;
+    const int64_t qw = (NK + 3) / 4, qb = (g.N + 3) / 4;
+    if (t >= qw + qb) { t -= qw + qb; continue; }
+    const bool is_w = t < qw;
+    const float* src = is_w ? g.part : g.partb;
+    const int64_t stride = is_w ? NK : g.N;
+    const int64_t base = 4 * (is_w ? t : t - qw);
+    const int n_el = (int)min((int64_t)4, stride - base);
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+    int s = 0;
+    for (; s + 8 <= g.splits; s += 8) {
+      float v[8][4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[u][e] = e < n ? src[(q + u) * stride + base + e] : 0.f;
+        for (int e = 0; e < 4; ++e) v[u][e] = e < n_el ? src[(s + u) * stride + base + e] : 0.f;
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sum[e] += v[u][e];
+        for (int e = 0; e < 4; ++e) sum[e] += v[u][e];
+    }
+    for (; s < g.splits; ++s)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum[e] += e < n_el ? src[s * stride + base + e] : 0.f;
+    for (int e = 0; e < n_el; ++e) {
+      const int64_t idx = base + e;
+      if (is_w) {
+        const float w = g.W[idx] - m.scale * sum[e];
+        g.W[idx] = w;
+        copy_out<T>(g.Wq, g.ldq, g.Wtq, g.ldt, (int)(idx / g.K), (int)(idx % g.K), w);
+      } else {
+        g.bias[idx] -= m.scale * sum[e];
+      }
+    }
+    return;
   }
-  for (; q < g.splits; ++q)
+  if (!with_logit) return;
+  const int W = lj.Hd + 2;
+  if (t >= W) return;
+  const int c = (int)t;
+  float sum = 0.f;
+  int b = 0;
+  for (; b + 8 <= lj.blocks; b += 8) {
+    float v[8];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sum[e] += e < n ? src[q * stride + base + e] : 0.f;
+    for (int u = 0; u < 8; ++u) v[u] = lj.part[(int64_t)(b + u) * W + c];
 #pragma unroll
-  for (int e = 0; e < 4; ++e)
-    if (e < n) dst[e] -= g.scale * sum[e];
+    for (int u = 0; u < 8; ++u) sum += v[u];
+  }
+  for (; b < lj.blocks; ++b) sum += lj.part[(int64_t)b * W + c];
+  if (c == 0) {
+    if (lj.loss_out) *lj.loss_out = sum / (float)lj.R;
+  } else if (c == 1) {
+    lj.b[0] -= lj.scale * sum;
+  } else {
+    lj.w[c - 2] -= lj.scale * sum;
+  }
 }
 
 template <typename T, int BM, int BN>
@@ -419,17 +477,9 @@ hipError_t nt_launch(const GemmNT& g, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, int BN, int BK>
-hipError_t dw_launch(const GemmDW& g, hipStream_t st) {
-  dim3 grid(((g.N + BN - 1) / BN) * ((g.K + BK - 1) / BK), g.splits);
-  hipLaunchKernelGGL((k_gemm_dw<T, BN, BK>), grid, dim3(256), 0, st, g);
-  return hipGetLastError();
-}
-
 }  // namespace
 
 int dw_stage_rows(Elt e) { return 128 / elt_size(e); }
-int dw_tile(Elt) { return 64; }
 int dw_tiles(int N, int K) { return ((N + 63) / 64) * ((K + 63) / 64); }
 
 hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st) {
@@ -443,17 +493,33 @@ hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st) {
   return nt_launch<float, 64, 64>(g, st);
 }
 
-hipError_t launch_dw_reduce(const GemmDW& g, hipStream_t st) {
-  if (g.splits <= 1 || g.N <= 0 || g.K <= 0) return hipSuccess;
-  const int64_t quads = ((int64_t)g.N * g.K + 3) / 4 + (g.N + 3) / 4;
-  hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st, g);
+hipError_t launch_multi_dw(Elt e, MultiDW& m, hipStream_t st) {
+  if (m.n <= 0 || m.n > kMaxDw || m.R <= 0) return m.n == 0 ? hipSuccess : hipErrorInvalidValue;
+  int blocks = 0;
+  for (int q = 0; q < m.n; ++q) {
+    m.first_block[q] = blocks;
+    blocks += dw_tiles(m.p[q].N, m.p[q].K) * m.p[q].splits;
+  }
+  m.first_block[m.n] = blocks;
+  if (e == BF16) hipLaunchKernelGGL((k_multi_dw<uint16_t, 64, 64>), dim3(blocks), dim3(256), 0, st, m);
+  else hipLaunchKernelGGL((k_multi_dw<float, 64, 64>), dim3(blocks), dim3(256), 0, st, m);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_dw(Elt e, const GemmDW& g, hipStream_t st) {
-  if (g.N <= 0 || g.K <= 0 || g.splits <= 0) return hipSuccess;
-  if (e == BF16) return dw_launch<uint16_t, 64, 64>(g, st);
-  return dw_launch<float, 64, 64>(g, st);
+hipError_t launch_multi_reduce(Elt e, const MultiDW& m, const LogitJob* lj, hipStream_t st) {
+  int64_t threads = 0;
+  for (int q = 0; q < m.n; ++q)
+    if (m.p[q].splits > 1)
+      threads += ((int64_t)m.p[q].N * m.p[q].K + 3) / 4 + (m.p[q].N + 3) / 4;
+  if (lj) threads += lj->Hd + 2;
+  if (threads == 0) return hipSuccess;
+  LogitJob none{};
+  const int blocks = (int)((threads + 255) / 256);
+  if (e == BF16)
+    hipLaunchKernelGGL(k_multi_reduce<uint16_t>, dim3(blocks), dim3(256), 0, st, m, lj ? *lj : none, lj ? 1 : 0);
+  else
+    hipLaunchKernelGGL(k_multi_reduce<float>, dim3(blocks), dim3(256), 0, st, m, lj ? *lj : none, lj ? 1 : 0);
+  return hipGetLastError();
 }
 
 }  // namespace vfl

@@ -32,27 +32,35 @@ struct GemmNT {
   const int32_t* hdr_chk = nullptr; int32_t chk_seq = 0; int32_t* err = nullptr;
 };
 
-// Weight gradient + SGD: G[n][k] = sum over rows r of D[r][n] * X[r][k],
-// g_b[n] = sum_r D[r][n]; W -= scale * G, bias -= scale * g_b.  X = [X1 | X2]
-// split at column ksplit.  The rows are cut into `splits` chunks of
-// rows_per_split (a multiple of the stage depth); with more than one chunk
-// each block writes a float32 partial part[s][n][k] (partb[s][n]) and a
-// second kernel sums the partials in chunk order and applies the update.
+// One layer's weight gradient + SGD: G[n][k] = sum over rows r of
+// D[r][n] * X[r][k], g_b[n] = sum_r D[r][n]; W -= scale * G, bias -= scale *
+// g_b, then the operand copies Wq [N x ldq] and Wtq [K x ldt] (nullable) are
+// rewritten from the new W.  X = [X1 | X2] split at column ksplit.  The rows
+// are cut into `splits` chunks of rows_per_split (a multiple of the stage
+// depth); with more than one chunk each block writes float32 partials
+// part[s][n][k] (partb[s][n]) and k_multi_reduce finishes the layer.
 struct GemmDW {
   const void* D = nullptr; int64_t ldd = 0;
   const void* X1 = nullptr; int64_t ldx1 = 0;
   const void* X2 = nullptr; int64_t ldx2 = 0; int ksplit = 1 << 30;
+  float* W = nullptr; float* bias = nullptr;
+  void* Wq = nullptr; int64_t ldq = 0; void* Wtq = nullptr; int64_t ldt = 0;
   float* part = nullptr; float* partb = nullptr;
-  float* W = nullptr; float* bias = nullptr; float scale = 0.f;
-  int R = 0, N = 0, K = 0, rows_per_split = 0, splits = 1;
+  int N = 0, K = 0, splits = 1, rows_per_split = 0;
+};
+constexpr int kMaxDw = 8;
+// Several layers' weight gradients over the same R rows (one launch).
+struct MultiDW {
+  GemmDW p[kMaxDw];
+  int n = 0, R = 0;
+  float scale = 0.f;
+  int first_block[kMaxDw + 1] = {0};   // filled by launch_multi_dw
 };
 
 hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st);
-hipError_t launch_gemm_dw(Elt e, const GemmDW& g, hipStream_t st);
-// second stage of a split weight gradient (no-op when splits == 1)
-hipError_t launch_dw_reduce(const GemmDW& g, hipStream_t st);
+hipError_t launch_multi_dw(Elt e, MultiDW& m, hipStream_t st);
 int dw_stage_rows(Elt e);   // rows per pipeline stage of the dW kernel
-int dw_tile(Elt e);         // output tile edge of the dW kernel
+int dw_tiles(int N, int K); // 64 x 64 output tiles of one layer
 
 // Operand copies of one layer's float32 weight W [out x in]:
 // Wq [out x ldq] and Wtq [in x ldt] of element type e (ldq, ldt padded).
@@ -61,11 +69,13 @@ struct CastJob {
 };
 hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
 
+constexpr int kMaxLogitCols = 512;   // widest last hidden layer of the top model
+
 // Logit layer + BCE on the last hidden activation H [R x ldh] (width Hd):
 // l = H w + b, loss_i = BCE(l, y), dl = sigmoid(l) - y; writes
 // delta [R x ldd] = dl * w * (H > 0) (element type e).  Each block writes
 // partial sums part[blk] = {loss, sum dl, sum_r dl * H[r][0..Hd)} (Hd + 2
-// floats); a second kernel reduces them in block order:
+// floats); k_multi_reduce reduces them in block order:
 // *loss_out = sum loss / R (loss_out may be null), w -= scale * sum dl*H,
 // b -= scale * sum dl.
 struct LogitJob {
@@ -75,7 +85,9 @@ struct LogitJob {
   float* part; int blocks; float scale; float* loss_out;
 };
 hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st);
-hipError_t launch_logit_reduce(const LogitJob& j, hipStream_t st);
+// Second stage of the split layers of m and (lj != null) of the logit
+// kernel's partials, in one launch.
+hipError_t launch_multi_reduce(Elt e, const MultiDW& m, const LogitJob* lj, hipStream_t st);
 
 // Segments mapping a row of a tick to its global sample id (<= 8 replicas).
 struct RowMap {

@@ -35,6 +35,37 @@ __device__ __forceinline__ void st1(T* p, float v) {
   else *p = f2bf(v);
 }
 
+// one 16-byte chunk <-> CE floats
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&v)[16 / sizeof(T)]) {
+  typedef __attribute__((ext_vector_type(4))) uint32_t u4;
+  const u4 x = *(const u4*)p;
+  if constexpr (sizeof(T) == 4) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __uint_as_float(x[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(x[i] << 16);
+      v[2 * i + 1] = __uint_as_float(x[i] & 0xffff0000u);
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float (&v)[16 / sizeof(T)]) {
+  typedef __attribute__((ext_vector_type(4))) uint32_t u4;
+  u4 x;
+  if constexpr (sizeof(T) == 4) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __float_as_uint(v[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  }
+  *(u4*)p = x;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -42,87 +73,98 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------- logit + BCE
-constexpr int kMaxLogitCols = 512;   // hidden width handled by the logit kernel
-
+// A row is owned by a group of lpr lanes (a power of two <= 64), each lane
+// holding up to two 16-byte chunks of the row, so a wavefront works on
+// 64 / lpr rows at once; the dot product is a shuffle reduction inside the
+// group.  Block partials are summed by k_multi_reduce.
 template <typename T>
 __global__ __launch_bounds__(256) void k_logit_bce(LogitJob j) {
-  constexpr int Q = kMaxLogitCols / 64;
-  __shared__ float red[4][kMaxLogitCols + 2];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int CE = 16 / (int)sizeof(T);
+  constexpr int MAXC = 2;
+  __shared__ float red[256 * CE * MAXC];
+  __shared__ float redl[256], redb[256];
+  const int nch = (j.Hd + CE - 1) / CE;
+  int lpr = 1;
+  while (lpr < nch && lpr < 64) lpr <<= 1;
+  const int cpl = (nch + lpr - 1) / lpr;
+  const int G = 256 / lpr;
+  const int grp = threadIdx.x / lpr, li = threadIdx.x % lpr;
   const T* H = (const T*)j.H;
   T* Dl = (T*)j.delta;
-  float wv[Q], gw[Q];
+  float wv[MAXC][CE], gw[MAXC][CE];
 #pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int c = lane + 64 * q;
-    wv[q] = c < j.Hd ? j.w[c] : 0.f;
-    gw[q] = 0.f;
-  }
+  for (int c = 0; c < MAXC; ++c)
+#pragma unroll
+    for (int e = 0; e < CE; ++e) {
+      const int col = (li + c * lpr) * CE + e;
+      wv[c][e] = (c < cpl && col < j.Hd) ? j.w[col] : 0.f;
+      gw[c][e] = 0.f;
+    }
   const float bias = j.b[0];
   float gb = 0.f, lsum = 0.f;
   const int per = (j.R + gridDim.x - 1) / gridDim.x;
   const int rb = blockIdx.x * per, re = min(j.R, rb + per);
-  for (int r = rb + wave; r < re; r += 4) {
-    float h[Q];
+  for (int r = rb + grp; r < re; r += G) {
+    float h[MAXC][CE];
     float dot = 0.f;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int c = lane + 64 * q;
-      h[q] = c < j.Hd ? ld1<T>(H + (int64_t)r * j.ldh + c) : 0.f;
-      dot += h[q] * wv[q];
+    for (int c = 0; c < MAXC; ++c) {
+      const int col0 = (li + c * lpr) * CE;
+      if (c < cpl && col0 < j.Hd) {
+        load8<T>(H + (int64_t)r * j.ldh + col0, h[c]);
+#pragma unroll
+        for (int e = 0; e < CE; ++e)
+          if (col0 + e >= j.Hd) h[c][e] = 0.f;
+      } else {
+#pragma unroll
+        for (int e = 0; e < CE; ++e) h[c][e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < CE; ++e) dot += h[c][e] * wv[c][e];
     }
-    const float l = wave_sum(dot) + bias;
+    for (int o = lpr >> 1; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
+    const float l = dot + bias;
     const float y = j.y[r];
-    const float e = expf(-fabsf(l));
-    const float loss = fmaxf(l, 0.f) - y * l + log1pf(e);
-    const float sig = l >= 0.f ? 1.f / (1.f + e) : e / (1.f + e);
+    const float ex = expf(-fabsf(l));
+    const float loss = fmaxf(l, 0.f) - y * l + log1pf(ex);
+    const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
     const float dl = sig - y;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int c = lane + 64 * q;
-      if (c < j.Hd) {
-        float d = dl * wv[q];
-        if (j.relu && !(h[q] > 0.f)) d = 0.f;
-        st1<T>(Dl + (int64_t)r * j.ldd + c, d);
-        gw[q] += dl * h[q];
+    for (int c = 0; c < MAXC; ++c) {
+      const int col0 = (li + c * lpr) * CE;
+      if (c < cpl && col0 < j.Hd) {
+        float d[CE];
+#pragma unroll
+        for (int e = 0; e < CE; ++e) {
+          d[e] = dl * wv[c][e];
+          if (j.relu && !(h[c][e] > 0.f)) d[e] = 0.f;
+          gw[c][e] += dl * h[c][e];
+        }
+        store8<T>(Dl + (int64_t)r * j.ldd + col0, d);
       }
     }
-    if (lane == 0) { gb += dl; lsum += loss; }
+    if (li == 0) { gb += dl; lsum += loss; }
   }
 #pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int c = lane + 64 * q;
-    if (c < j.Hd) red[wave][2 + c] = gw[q];
-  }
-  if (lane == 0) { red[wave][0] = lsum; red[wave][1] = gb; }
+  for (int c = 0; c < MAXC; ++c)
+#pragma unroll
+    for (int e = 0; e < CE; ++e) {
+      const int col = (li + c * lpr) * CE + e;
+      if (c < cpl && col < j.Hd) red[grp * j.Hd + col] = gw[c][e];
+    }
+  if (li == 0) { redl[grp] = lsum; redb[grp] = gb; }
   __syncthreads();
   const int W = j.Hd + 2;
-  for (int c = threadIdx.x; c < W; c += 256)
-    j.part[(int64_t)blockIdx.x * W + c] = red[0][c] + red[1][c] + red[2][c] + red[3][c];
-}
-
-// Sum of the logit kernel's block partials in block order + the logit
-// layer's SGD step and the mean loss.
-__global__ __launch_bounds__(256) void k_logit_reduce(LogitJob j) {
-  const int W = j.Hd + 2;
-  for (int c = threadIdx.x; c < W; c += 256) {
-    float s = 0.f;
-    int b = 0;
-    for (; b + 8 <= j.blocks; b += 8) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = j.part[(int64_t)(b + u) * W + c];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
-    }
-    for (; b < j.blocks; ++b) s += j.part[(int64_t)b * W + c];
-    if (c == 0) {
-      if (j.loss_out) *j.loss_out = s / (float)j.R;
-    } else if (c == 1) {
-      j.b[0] -= j.scale * s;
-    } else {
-      j.w[c - 2] -= j.scale * s;
-    }
+  for (int col = threadIdx.x; col < j.Hd; col += 256) {
+    float acc = 0.f;
+    for (int g = 0; g < G; ++g) acc += red[g * j.Hd + col];
+    j.part[(int64_t)blockIdx.x * W + 2 + col] = acc;
+  }
+  if (threadIdx.x == 0) {
+    float a = 0.f, b2 = 0.f;
+    for (int g = 0; g < G; ++g) { a += redl[g]; b2 += redb[g]; }
+    j.part[(int64_t)blockIdx.x * W] = a;
+    j.part[(int64_t)blockIdx.x * W + 1] = b2;
   }
 }
 
@@ -275,11 +317,6 @@ hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st) {
   if (j.Hd > kMaxLogitCols) return hipErrorInvalidValue;
   if (e == BF16) hipLaunchKernelGGL(k_logit_bce<uint16_t>, dim3(j.blocks), dim3(256), 0, st, j);
   else hipLaunchKernelGGL(k_logit_bce<float>, dim3(j.blocks), dim3(256), 0, st, j);
-  return hipGetLastError();
-}
-
-hipError_t launch_logit_reduce(const LogitJob& j, hipStream_t st) {
-  hipLaunchKernelGGL(k_logit_reduce, dim3(1), dim3(256), 0, st, j);
   return hipGetLastError();
 }
 
