@@ -192,6 +192,35 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group);
 vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a,
                     const vfl_batch* b, int32_t n_b, float* loss_dev);
 
+/* A party's resident dataset for vfl_run: row r of every array belongs to
+ * sample r.  dense [n_rows x ld] (alignment as for vfl_batch), ids [n_rows x
+ * n_cat], labels [n_rows] (party A).  Device pointers, owned by the caller,
+ * valid while the binding is used. */
+typedef struct {
+  const void* dense;
+  int64_t ld;
+  const int32_t* ids;
+  const float* labels;
+} vfl_dataset;
+
+/* Bind both parties' resident datasets of n_rows rows for vfl_run. */
+vfl_status vfl_bind_dataset(vfl_ctx* c, const vfl_dataset* a, const vfl_dataset* b, int64_t n_rows);
+
+/* Run ticks t0 .. t0+n-1 of vfl_step's schedule over the bound dataset.
+ * Group g covers rows [(g mod E) * R, ...) with E = ceil(n_rows / R) groups
+ * per epoch (the last group of an epoch is short; its rows are split into
+ * replicas of `batch` rows like any group), which are exactly the batches a
+ * caller of vfl_step would pass.  The ticks replay a captured HIP graph of
+ * several ticks per phase t mod (s+1); a small kernel at the start of each
+ * party's part of a tick derives the tick's rows, noise step and channel
+ * headers from a device-side tick counter, so the host launches one graph
+ * per graph length (VFL_GRAPH_CYCLES * (s+1) ticks; the remainder runs as
+ * vfl_step).  Steady state only: t0 >= s+1 and ticks 0 .. t0-1 already run
+ * (VFL_E_STATE otherwise).  loss_ring (device float [loss_len], nullable)
+ * receives group u's mean loss at index u mod loss_len. */
+#define VFL_GRAPH_CYCLES 4
+vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t loss_len);
+
 /* Copy a channel slot to host memory after synchronising: which 0 = the
  * embedding of `group`, 1 = its gradient message; [rows x width] of the
  * context dtype (float32 or bf16 bits).  header (may be NULL) receives the

@@ -12,7 +12,7 @@ SOURCES = ["gemm.hip", "rowops.hip", "embed.hip", "api.cpp", "schedule.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-Wall", "-Wno-unused-function"]
+         "-Wall", "-Wno-unused-function", "-Werror=uninitialized", "-Werror=unused-variable"]
 
 
 def build(verbose: bool = False) -> str:

@@ -93,6 +93,8 @@ struct Plan {
   size_t ring_g[kMaxSlots]{};
   size_t gpre = 0;                    // float32 gradient message before clip/noise
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
+  size_t ta_a = 0, ta_bf = 0, ta_bb = 0;   // tick records (graph replay)
+  size_t ctr = 0;                     // int64 tick counters of streams A and B
   size_t total = 0;
 };
 
@@ -144,6 +146,23 @@ struct vfl_ctx {
   float* a_loss = nullptr;
   std::vector<int64_t> trace;
   std::string err;
+  // resident dataset + captured graphs (one per phase t mod (s+1))
+  bool bound = false;
+  vfl_dataset ds_a{}, ds_b{};
+  int64_t n_rows = 0;
+  hipGraph_t graph[kMaxSlots]{};
+  hipGraphExec_t gexec[kMaxSlots]{};
+  float* graph_loss[kMaxSlots]{};
+  int64_t graph_loss_len[kMaxSlots]{};
+  uint32_t graph_mask[kMaxSlots]{};
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  int capture_phase = -1;             // >= 0 while capturing that phase's graph
+  struct GPair { hipEvent_t e0, e1; int cls; double work; };
+  std::vector<GPair> gpairs[kMaxSlots];   // created before capture
+  int gused[kMaxSlots]{};                 // pairs used by the captured graph
+  hipError_t tm_err = hipSuccess;         // first failed event record in a capture
+  std::string tm_err_what;
+  int last_phase = -1;                // phase of the graph replayed last
 };
 
 namespace {
@@ -290,6 +309,10 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   for (int q = 0; q <= p.s; ++q) p.ring_g[q] = ly.take((size_t)es * R * ld_of(p.dB));
   if (o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD)) p.gpre = ly.take(sizeof(float) * R * ld_of(p.dB));
   p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
+  p.ta_a = ly.take(sizeof(TickArgs));
+  p.ta_bf = ly.take(sizeof(TickArgs));
+  p.ta_bb = ly.take(sizeof(TickArgs));
+  p.ctr = ly.take(2 * sizeof(int64_t));
 
   // weight-gradient row chunks and partials (one region per layer: all
   // layers of a party are in flight in the same launch)
@@ -364,9 +387,48 @@ void harvest(vfl_ctx* c, int i) {
   T.used[i] = false;
 }
 
+// An event-record node appended to the stream's captured work: it depends on
+// the stream's current capture dependencies and becomes the only one, so the
+// next captured launch on the stream starts after it.
+bool capture_record(vfl_ctx* c, hipEvent_t ev, hipStream_t st, int cls, int end) {
+  hipStreamCaptureStatus cs;
+  unsigned long long id = 0;
+  hipGraph_t g = nullptr;
+  const hipGraphNode_t* deps = nullptr;
+  size_t nd = 0;
+  hipGraphNode_t node;
+  const char* what = "hipStreamGetCaptureInfo_v2";
+  hipError_t he = hipStreamGetCaptureInfo_v2(st, &cs, &id, &g, &deps, &nd);
+  if (he == hipSuccess) { what = "hipGraphAddEventRecordNode"; he = hipGraphAddEventRecordNode(&node, g, deps, nd, ev); }
+  if (he == hipSuccess) {
+    what = "hipStreamUpdateCaptureDependencies";
+    he = hipStreamUpdateCaptureDependencies(st, &node, 1, hipStreamSetCaptureDependencies);
+  }
+  if (he == hipSuccess) return true;
+  (void)hipGetLastError();   // do not leave it to the next launch's check
+  if (c->tm_err == hipSuccess) {
+    c->tm_err = he;
+    c->tm_err_what = std::string(what) + (end ? " (end" : " (begin") + ", class " + std::to_string(cls) +
+                     ", stream " + (st == c->sa ? "A" : st == c->sb ? "B" : "?") + ", deps " +
+                     std::to_string(nd) + ", pair " + std::to_string(c->gused[c->capture_phase]) + ")";
+  }
+  return false;
+}
+
 int tbegin(vfl_ctx* c, int cls, double work, hipStream_t st) {
   Timing& T = c->tm;
   if (!((T.mask >> cls) & 1u)) return -1;
+  if (c->capture_phase >= 0) {
+    // inside a captured graph: an event pair of its own (created before the
+    // capture), recorded as graph nodes, read after the graph's last replay
+    const int ph = c->capture_phase;
+    if (c->gused[ph] >= (int)c->gpairs[ph].size()) return -1;
+    vfl_ctx::GPair& gp = c->gpairs[ph][c->gused[ph]];
+    gp.cls = cls;
+    gp.work = work;
+    if (!capture_record(c, gp.e0, st, cls, 0)) return -1;
+    return c->gused[ph]++ + (1 << 20);
+  }
   const int i = T.next;
   T.next = (T.next + 1) % Timing::kPool;
   harvest(c, i);
@@ -378,6 +440,10 @@ int tbegin(vfl_ctx* c, int cls, double work, hipStream_t st) {
 
 void tend(vfl_ctx* c, int i, hipStream_t st) {
   if (i < 0) return;
+  if (i >= (1 << 20)) {
+    (void)capture_record(c, c->gpairs[c->capture_phase][i - (1 << 20)].e1, st, -1, 1);
+    return;
+  }
   if (hipEventRecord(c->tm.ev1[i], st) == hipSuccess) c->tm.used[i] = true;
 }
 
@@ -394,6 +460,9 @@ int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.h
 int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
 
 // ------------------------------------------------------------ enqueue steps
+// Every enqueue function below takes an optional tick record `ta`: null when
+// the call's values are known on the host (the per-call API), the device
+// record of the stream when the work is captured into a replayed graph.
 vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipStream_t st) {
   CastJob jobs[2 * VFL_MAX_LAYERS + 2];
   int n = 0;
@@ -410,16 +479,18 @@ vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipS
   return VFL_OK;
 }
 
-// Party bottom forward (gather + layers) into slot `slot`.
+// Party bottom forward (gather + layers) into slot `slot`.  With a tick
+// record the input pointers in `in` are dataset bases.
 vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const SlotState& in,
-                                  hipStream_t st, int32_t* hdr_out, const int32_t hdr[3]) {
+                                  hipStream_t st, int32_t* hdr_out, const int32_t hdr[3],
+                                  const TickArgs* ta) {
   const Plan& p = c->p;
   const int R = in.rows;
   const void* x = in.dense;
   int64_t ldx = in.ld;
   if (P.spec.n_cat) {
     GatherJob gj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                 in.dense, in.ld, P.spec.dense_in, c->ws + P.x0[slot], P.ldx0, R};
+                 in.dense, in.ld, P.spec.dense_in, c->ws + P.x0[slot], P.ldx0, R, ta};
     const double gb = (double)R * P.spec.n_cat * (4 + P.spec.emb_dim * (4.0 + elt_size(p.e))) +
                       2.0 * R * P.spec.dense_in * elt_size(p.e);
     TIMED(VFL_K_GATHER, gb, st, launch_gather(p.e, gj, st));
@@ -437,9 +508,11 @@ vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const Sl
     g.bias = at<float>(c, P.b[l]);
     g.relu = P.relu[l];
     g.M = R; g.N = P.out[l]; g.K = P.in[l];
+    g.ta = ta;
+    g.ta_in = (ta && l == 0 && !P.spec.n_cat) ? 1 : 0;
     if (l == P.L - 1 && hdr_out) {
       g.hdr_out = hdr_out;
-      g.hdr[0] = hdr[0]; g.hdr[1] = hdr[1]; g.hdr[2] = hdr[2];
+      if (hdr) { g.hdr[0] = hdr[0]; g.hdr[1] = hdr[1]; g.hdr[2] = hdr[2]; }
     }
     TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
@@ -448,7 +521,8 @@ vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const Sl
 
 // Input-gradient chain of a bottom model: from dlt[L-1] down to dlt[0], and
 // for tables the float32 gradient of the gathered input columns.
-vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStream_t st) {
+vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStream_t st,
+                            const TickArgs* ta) {
   const Plan& p = c->p;
   for (int l = P.L - 1; l >= 1; --l) {
     GemmNT g;
@@ -457,6 +531,7 @@ vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStre
     g.C1 = c->ws + P.dlt[l - 1]; g.ldc1 = ld_of(P.out[l - 1]);
     if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
     g.M = R; g.N = P.in[l]; g.K = P.out[l];
+    g.ta = ta;
     TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
   if (P.spec.n_cat) {
@@ -465,6 +540,7 @@ vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStre
     g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
     g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
     g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
+    g.ta = ta;
     TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
   }
   return VFL_OK;
@@ -482,17 +558,20 @@ void add_dw(MultiDW& m, const void* D, int N, const void* X1, int64_t ldx1, cons
   d.splits = splits; d.rows_per_split = rps;
 }
 
-// Bottom layers' weight gradients of one party appended to m.
+// Bottom layers' weight gradients of one party appended to m.  With a tick
+// record the dense input in `in` is a dataset base.
 void add_party_dw(vfl_ctx* c, MultiDW& m, const Party& P, int slot, const SlotState& in,
-                  int splits, int rps) {
+                  int splits, int rps, bool dataset_in) {
   const void* x = P.spec.n_cat ? (const void*)(c->ws + P.x0[slot]) : in.dense;
   const int64_t ldx = P.spec.n_cat ? P.ldx0 : in.ld;
-  for (int l = 0; l < P.L; ++l)
+  for (int l = 0; l < P.L; ++l) {
     add_dw(m, c->ws + P.dlt[l], P.out[l], l == 0 ? x : c->ws + P.act[slot][l - 1],
            l == 0 ? ldx : ld_of(P.out[l - 1]), nullptr, 0, 1 << 30, P.in[l], at<float>(c, P.W[l]),
            at<float>(c, P.b[l]), c->ws + P.Wq[slot][l], P.ldq[l], c->ws + P.Wtq[slot][l], P.ldt[l],
            P.part[l] ? at<float>(c, P.part[l]) : nullptr, P.partb[l] ? at<float>(c, P.partb[l]) : nullptr,
            splits, rps);
+    if (l == 0 && dataset_in && !P.spec.n_cat) m.p[m.n - 1].x_ta = 1;
+  }
 }
 
 vfl_status enqueue_weight_update(vfl_ctx* c, MultiDW& m, const LogitJob* lj, hipStream_t st) {
@@ -515,27 +594,203 @@ vfl_status enqueue_weight_update(vfl_ctx* c, MultiDW& m, const LogitJob* lj, hip
 }
 
 vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const SlotState& in, float scale,
-                             hipStream_t st) {
+                             hipStream_t st, const TickArgs* ta) {
   if (!P.spec.n_cat) return VFL_OK;
   ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                at<float>(c, P.gx), P.ldgx, in.rows, scale};
+                at<float>(c, P.gx), P.ldgx, in.rows, scale, ta};
   TIMED(VFL_K_EMB_SGD, (double)in.rows * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
         launch_scatter_sgd(sj, st));
   return VFL_OK;
 }
 
-LogitJob logit_job(vfl_ctx* c, int R, float* loss_dev) {
+LogitJob logit_job(vfl_ctx* c, int R, const float* labels, float* loss_dev, const TickArgs* ta) {
   const Plan& p = c->p;
   const Top& T = p.T;
   LogitJob lj{};
   lj.H = c->ws + T.act[T.H - 1]; lj.ldh = ld_of(T.out[T.H - 1]); lj.Hd = T.out[T.H - 1]; lj.R = R;
-  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = c->a_labels;
+  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = labels;
   lj.delta = c->ws + T.dlt[T.H - 1]; lj.ldd = ld_of(T.out[T.H - 1]); lj.relu = T.relu[T.H - 1];
   lj.part = at<float>(c, T.logit_part);
-  lj.blocks = std::max(1, std::min(kLogitBlocks, (R + 15) / 16));
+  // blocking from the configured rows per tick, so that a short group is
+  // cut the same way whether its row count is known on the host or read
+  // from a tick record
+  lj.blocks = std::max(1, std::min(kLogitBlocks, (p.R + 15) / 16));
   lj.scale = c->o.lr / (float)R;
-  lj.loss_out = loss_dev;
+  lj.loss_out = ta ? nullptr : loss_dev;
+  lj.ta = ta;
+  lj.loss_base = ta ? loss_dev : nullptr;
   return lj;
+}
+
+// ---- the phases of a tick (enqueue only; the callers keep the host state)
+
+// B's forward of group `group` into `slot`; the embedding slot header is
+// written by the last layer unless clip/noise publish it.
+vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, const TickArgs* ta) {
+  const Plan& p = c->p;
+  const bool extra = c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
+  const int32_t hdr[3] = {(int32_t)st.group, (int32_t)st.group, (int32_t)st.version};
+  return enqueue_bottom_forward(c, p.P, slot, st, c->sb, extra ? nullptr : hdr_ptr(c, 0, slot),
+                                ta ? nullptr : hdr, ta);
+}
+
+vfl_status b_publish(vfl_ctx* c, int slot, const SlotState& st, const TickArgs* ta) {
+  const Plan& p = c->p;
+  if (c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB)) {
+    ClipNoiseJob j{};
+    j.v = c->ws + p.P.act[slot][p.P.L - 1]; j.ldv = ld_of(p.dB); j.v_f32 = p.e == F32;
+    j.out = c->ws + p.P.zhat[slot]; j.ldo = ld_of(p.dB);
+    j.norm = p.P.norm[slot] ? at<float>(c, p.P.norm[slot]) : nullptr;
+    j.cfac = p.P.cfac[slot] ? at<float>(c, p.P.cfac[slot]) : nullptr;
+    j.R = st.rows; j.D = p.dB;
+    j.clip = (c->o.flags & VFL_CLIP_EMB) != 0; j.C = c->o.clip_c;
+    j.noise = (c->o.flags & VFL_NOISE_EMB) != 0;
+    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
+    j.seed = c->o.seed; j.step = (uint32_t)st.group; j.tag = 0; j.rows = st.rmap;
+    j.hdr_out = hdr_ptr(c, 0, slot);
+    j.hdr[0] = (int32_t)st.group; j.hdr[1] = (int32_t)st.group; j.hdr[2] = (int32_t)st.version;
+    j.ta = ta;
+    TIMED(VFL_K_CLIP_NOISE, (double)st.rows * p.dB * (elt_size(p.e) * 2.0) + 8.0 * st.rows, c->sb,
+          launch_clip_noise(p.e, j, c->sb));
+  }
+  HIPCHK(hipEventRecord(c->ev_emb[slot], c->sb));
+  return VFL_OK;
+}
+
+vfl_status a_forward(vfl_ctx* c, const SlotState& st, const TickArgs* ta) {
+  return enqueue_bottom_forward(c, c->p.A, 0, st, c->sa, nullptr, nullptr, ta);
+}
+
+// Top model step of A's group (rows R) against embedding slot `slot`:
+// forward, logit + BCE, input-gradient chain, gradient message + event.
+vfl_status a_top(vfl_ctx* c, int64_t group, int slot, int R, const float* labels,
+                 int32_t b_version, float* loss_dev, const TickArgs* ta, bool wait_emb = true) {
+  const Plan& p = c->p;
+  hipStream_t st = c->sa;
+  if (wait_emb) HIPCHK(hipStreamWaitEvent(st, c->ev_emb[slot], 0));
+  const Top& T = p.T;
+  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
+  const void* zB = c->ws + p.P.zhat[slot];
+  for (int j = 0; j < T.H; ++j) {
+    GemmNT g;
+    if (j == 0) {
+      g.A1 = zA; g.lda1 = ld_of(p.dA);
+      g.A2 = zB; g.lda2 = ld_of(p.dB); g.ksplit = p.dA;
+      g.hdr_chk = hdr_ptr(c, 0, slot); g.chk_seq = (int32_t)group; g.err = err_ptr(c);
+    } else {
+      g.A1 = c->ws + T.act[j - 1]; g.lda1 = ld_of(T.out[j - 1]);
+    }
+    g.B = c->ws + T.Wq[j]; g.ldb = T.ldq[j];
+    g.C1 = c->ws + T.act[j]; g.ldc1 = ld_of(T.out[j]);
+    g.bias = at<float>(c, T.b[j]); g.relu = T.relu[j];
+    g.M = R; g.N = T.out[j]; g.K = T.in[j];
+    g.ta = ta;
+    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
+  }
+  // logit + BCE; its reduction and SGD run with the weight update
+  LogitJob lj = logit_job(c, R, labels, loss_dev, ta);
+  TIMED(VFL_K_LOGIT, (double)R * lj.Hd * 2.0 * elt_size(p.e) + 4.0 * R, st, launch_logit_bce(p.e, lj, st));
+  // input-gradient chain of the top model; the last product splits into A's
+  // cut-layer delta and the per-row gradient message for B
+  const bool gextra = c->o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
+  for (int j = T.H - 1; j >= 0; --j) {
+    GemmNT g;
+    g.A1 = c->ws + T.dlt[j]; g.lda1 = ld_of(T.out[j]);
+    g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
+    g.M = R; g.N = T.in[j]; g.K = T.out[j];
+    g.ta = ta;
+    if (j > 0) {
+      g.C1 = c->ws + T.dlt[j - 1]; g.ldc1 = ld_of(T.out[j - 1]);
+      if (T.relu[j - 1]) { g.mask = c->ws + T.act[j - 1]; g.ldm = ld_of(T.out[j - 1]); }
+    } else {
+      g.C1 = c->ws + p.A.dlt[p.A.L - 1]; g.ldc1 = ld_of(p.dA);
+      if (p.A.relu[p.A.L - 1]) { g.mask = zA; g.ldm = ld_of(p.dA); }
+      g.nsplit = p.dA;
+      if (gextra) { g.C2 = c->ws + p.gpre; g.ldc2 = ld_of(p.dB); g.c2_f32 = 1; }
+      else {
+        g.C2 = c->ws + p.ring_g[slot]; g.ldc2 = ld_of(p.dB);
+        g.hdr_out = hdr_ptr(c, 1, slot);
+        g.hdr[0] = (int32_t)group; g.hdr[1] = (int32_t)(group + p.s); g.hdr[2] = b_version;
+      }
+    }
+    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
+  }
+  if (gextra) {
+    ClipNoiseJob j{};
+    j.v = c->ws + p.gpre; j.ldv = ld_of(p.dB); j.v_f32 = 1;
+    j.out = c->ws + p.ring_g[slot]; j.ldo = ld_of(p.dB);
+    j.R = R; j.D = p.dB;
+    j.clip = (c->o.flags & VFL_CLIP_GRAD) != 0; j.C = c->o.clip_c;
+    j.noise = (c->o.flags & VFL_NOISE_GRAD) != 0;
+    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
+    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 1; j.rows = c->aslot.rmap;
+    j.hdr_out = hdr_ptr(c, 1, slot);
+    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)(group + p.s); j.hdr[2] = b_version;
+    j.ta = ta;
+    TIMED(VFL_K_CLIP_NOISE, (double)R * p.dB * (4.0 + elt_size(p.e)), st, launch_clip_noise(p.e, j, st));
+  }
+  HIPCHK(hipEventRecord(c->ev_grad[slot], st));
+  return VFL_OK;
+}
+
+// A's and the top model's backward + SGD for A's group in `st` (rows R);
+// `slot` is the embedding slot the top model read.
+vfl_status a_backward(vfl_ctx* c, int slot, const SlotState& st, const float* labels,
+                      float* loss_dev, const TickArgs* ta) {
+  const Plan& p = c->p;
+  const int R = st.rows;
+  vfl_status r = enqueue_dx_chain(c, p.A, 0, R, c->sa, ta);
+  if (r) return r;
+  // one weight update for the top model's hidden layers and A's layers,
+  // with the logit layer's reduction, SGD and loss in the same reduction
+  MultiDW m;
+  m.R = R;
+  m.scale = c->o.lr / (float)R;
+  m.ta = ta;
+  const Top& T = p.T;
+  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
+  const void* zB = c->ws + p.P.zhat[slot];
+  for (int j = 0; j < T.H; ++j)
+    add_dw(m, c->ws + T.dlt[j], T.out[j], j == 0 ? zA : c->ws + T.act[j - 1],
+           j == 0 ? ld_of(p.dA) : ld_of(T.out[j - 1]), j == 0 ? zB : nullptr,
+           j == 0 ? ld_of(p.dB) : 0, j == 0 ? p.dA : 1 << 30, T.in[j], at<float>(c, T.W[j]),
+           at<float>(c, T.b[j]), c->ws + T.Wq[j], T.ldq[j], c->ws + T.Wtq[j], T.ldt[j],
+           T.part[j] ? at<float>(c, T.part[j]) : nullptr, T.partb[j] ? at<float>(c, T.partb[j]) : nullptr,
+           p.splits_a, p.rps_a);
+  add_party_dw(c, m, p.A, 0, st, p.splits_a, p.rps_a, ta != nullptr);
+  LogitJob lj = logit_job(c, R, labels, loss_dev, ta);
+  if ((r = enqueue_weight_update(c, m, &lj, c->sa))) return r;
+  return enqueue_table_sgd(c, p.A, st, c->o.lr / (float)R, c->sa, ta);
+}
+
+// B's delayed backward of the group stashed in `slot` + SGD on B's current
+// weights; the refreshed operand copies go to this slot, which B's next
+// forward uses.
+vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, const TickArgs* ta) {
+  const Plan& p = c->p;
+  HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
+  CutBwdJob cj{};
+  cj.g = c->ws + p.ring_g[slot]; cj.ldg = ld_of(p.dB);
+  cj.z = c->ws + p.P.act[slot][p.P.L - 1]; cj.ldz = ld_of(p.dB);
+  cj.clip = (c->o.flags & VFL_CLIP_EMB) != 0;
+  cj.norm = cj.clip ? at<float>(c, p.P.norm[slot]) : nullptr;
+  cj.cfac = cj.clip ? at<float>(c, p.P.cfac[slot]) : nullptr;
+  cj.C = c->o.clip_c; cj.relu = p.P.relu[p.P.L - 1];
+  cj.delta = c->ws + p.P.dlt[p.P.L - 1]; cj.ldd = ld_of(p.dB);
+  cj.R = st.rows; cj.D = p.dB;
+  cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
+  cj.ta = ta;
+  TIMED(VFL_K_CUT_BWD, (double)st.rows * p.dB * 3.0 * elt_size(p.e) + (cj.clip ? 8.0 * st.rows : 0.0),
+        c->sb, launch_cut_backward(p.e, cj, c->sb));
+  vfl_status r = enqueue_dx_chain(c, p.P, slot, st.rows, c->sb, ta);
+  if (r) return r;
+  MultiDW m;
+  m.R = st.rows;
+  m.scale = c->o.lr / (float)st.rows;
+  m.ta = ta;
+  add_party_dw(c, m, p.P, slot, st, p.splits_b, p.rps_b, ta != nullptr);
+  if ((r = enqueue_weight_update(c, m, nullptr, c->sb))) return r;
+  return enqueue_table_sgd(c, p.P, st, c->o.lr / (float)st.rows, c->sb, ta);
 }
 
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
@@ -562,6 +817,31 @@ vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& o
     return VFL_OK;
   }
   return fail(c, VFL_E_INVALID, "bad party");
+}
+
+// Replica batches of group g of the bound dataset (consecutive chunks of at
+// most `batch` rows of the group's rows).
+int dataset_batches(vfl_ctx* c, int party, int64_t g, vfl_batch* out) {
+  const Plan& p = c->p;
+  const int64_t E = (c->n_rows + p.R - 1) / p.R;
+  const int64_t start = (g % E) * p.R;
+  const int64_t rows = std::min<int64_t>(p.R, c->n_rows - start);
+  const vfl_dataset& d = party == 0 ? c->ds_a : c->ds_b;
+  const Party& P = party == 0 ? p.A : p.P;
+  const int es = elt_size(p.e);
+  const int64_t ld = d.ld ? d.ld : P.spec.dense_in;
+  int n = 0;
+  for (int64_t o = 0; o < rows; o += p.B, ++n) {
+    vfl_batch& b = out[n];
+    b = vfl_batch{};
+    const int64_t r0 = start + o;
+    if (d.dense) { b.dense = (const char*)d.dense + r0 * ld * es; b.ld = ld; }
+    if (d.ids) b.ids = d.ids + r0 * P.spec.n_cat;
+    if (d.labels) b.labels = d.labels + r0;
+    b.rows = (int32_t)std::min<int64_t>(p.B, rows - o);
+    b.row0 = r0;
+  }
+  return n;
 }
 
 }  // namespace
@@ -600,6 +880,8 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
     e = hipEventCreateWithFlags(&c->ev_emb[q], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_grad[q], hipEventDisableTiming);
   }
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming);
   // parameters, headers and the error counter start at zero
   if (e == hipSuccess) e = hipMemsetAsync(c->ws, 0, c->p.total, c->sa);
   if (e == hipSuccess) e = hipStreamSynchronize(c->sa);
@@ -662,10 +944,7 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
       if ((r = enqueue_cast(c, p.P, slot, nullptr, c->sb))) return r;
       c->b_copy_version[slot] = c->b_version;
     }
-    const bool extra = c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
-    const int32_t hdr[3] = {(int32_t)group, (int32_t)group, (int32_t)c->b_version};
-    if ((r = enqueue_bottom_forward(c, p.P, slot, st, c->sb, extra ? nullptr : hdr_ptr(c, 0, slot), hdr)))
-      return r;
+    if ((r = b_forward(c, slot, st, nullptr))) return r;
     c->bslot[slot] = st;
     c->b_next_fwd = group + 1;
     return VFL_OK;
@@ -681,7 +960,7 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
       if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
       c->a_copy_version = c->a_version;
     }
-    if ((r = enqueue_bottom_forward(c, p.A, 0, st, c->sa, nullptr, nullptr))) return r;
+    if ((r = a_forward(c, st, nullptr))) return r;
     c->aslot = st;
     c->a_labels = br[0].labels;
     c->a_phase = 1;
@@ -696,25 +975,9 @@ vfl_status vfl_publish(vfl_ctx* c, int64_t group) {
   const int slot = (int)(group % (p.s + 1));
   if (group != c->b_pub_next || c->b_next_fwd != group + 1 || c->bslot[slot].group != group)
     return fail(c, VFL_E_STATE, "publish must follow B's forward of the same group");
-  SlotState& st = c->bslot[slot];
-  if (c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB)) {
-    ClipNoiseJob j{};
-    j.v = c->ws + p.P.act[slot][p.P.L - 1]; j.ldv = ld_of(p.dB); j.v_f32 = p.e == F32;
-    j.out = c->ws + p.P.zhat[slot]; j.ldo = ld_of(p.dB);
-    j.norm = p.P.norm[slot] ? at<float>(c, p.P.norm[slot]) : nullptr;
-    j.cfac = p.P.cfac[slot] ? at<float>(c, p.P.cfac[slot]) : nullptr;
-    j.R = st.rows; j.D = p.dB;
-    j.clip = (c->o.flags & VFL_CLIP_EMB) != 0; j.C = c->o.clip_c;
-    j.noise = (c->o.flags & VFL_NOISE_EMB) != 0;
-    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
-    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 0; j.rows = st.rmap;
-    j.hdr_out = hdr_ptr(c, 0, slot);
-    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)group; j.hdr[2] = (int32_t)st.version;
-    TIMED(VFL_K_CLIP_NOISE, (double)st.rows * p.dB * (elt_size(p.e) * 2.0) + 8.0 * st.rows, c->sb,
-          launch_clip_noise(p.e, j, c->sb));
-  }
-  HIPCHK(hipEventRecord(c->ev_emb[slot], c->sb));
-  st.published = true;
+  vfl_status r = b_publish(c, slot, c->bslot[slot], nullptr);
+  if (r) return r;
+  c->bslot[slot].published = true;
   c->b_pub_next = group + 1;
   return VFL_OK;
 }
@@ -729,71 +992,10 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
   if (bs.group != group || !bs.published)
     return fail(c, VFL_E_NOT_READY, "embedding of this group not published");
   if (bs.rows != c->aslot.rows) return fail(c, VFL_E_INVALID, "A and B batches differ in rows");
-  const int R = c->aslot.rows;
-  hipStream_t st = c->sa;
-  HIPCHK(hipStreamWaitEvent(st, c->ev_emb[slot], 0));
-  const Top& T = p.T;
-  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
-  const void* zB = c->ws + p.P.zhat[slot];
-  // hidden layers
-  for (int j = 0; j < T.H; ++j) {
-    GemmNT g;
-    if (j == 0) {
-      g.A1 = zA; g.lda1 = ld_of(p.dA);
-      g.A2 = zB; g.lda2 = ld_of(p.dB); g.ksplit = p.dA;
-      g.hdr_chk = hdr_ptr(c, 0, slot); g.chk_seq = (int32_t)group; g.err = err_ptr(c);
-    } else {
-      g.A1 = c->ws + T.act[j - 1]; g.lda1 = ld_of(T.out[j - 1]);
-    }
-    g.B = c->ws + T.Wq[j]; g.ldb = T.ldq[j];
-    g.C1 = c->ws + T.act[j]; g.ldc1 = ld_of(T.out[j]);
-    g.bias = at<float>(c, T.b[j]); g.relu = T.relu[j];
-    g.M = R; g.N = T.out[j]; g.K = T.in[j];
-    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  // logit + BCE; its reduction and SGD run with the weight update
-  LogitJob lj = logit_job(c, R, loss_dev);
-  TIMED(VFL_K_LOGIT, (double)R * lj.Hd * 2.0 * elt_size(p.e) + 4.0 * R, st, launch_logit_bce(p.e, lj, st));
-  // input-gradient chain of the top model; the last product splits into A's
-  // cut-layer delta and the per-row gradient message for B
-  const bool gextra = c->o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
-  for (int j = T.H - 1; j >= 0; --j) {
-    GemmNT g;
-    g.A1 = c->ws + T.dlt[j]; g.lda1 = ld_of(T.out[j]);
-    g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
-    g.M = R; g.N = T.in[j]; g.K = T.out[j];
-    if (j > 0) {
-      g.C1 = c->ws + T.dlt[j - 1]; g.ldc1 = ld_of(T.out[j - 1]);
-      if (T.relu[j - 1]) { g.mask = c->ws + T.act[j - 1]; g.ldm = ld_of(T.out[j - 1]); }
-    } else {
-      g.C1 = c->ws + p.A.dlt[p.A.L - 1]; g.ldc1 = ld_of(p.dA);
-      if (p.A.relu[p.A.L - 1]) { g.mask = zA; g.ldm = ld_of(p.dA); }
-      g.nsplit = p.dA;
-      if (gextra) { g.C2 = c->ws + p.gpre; g.ldc2 = ld_of(p.dB); g.c2_f32 = 1; }
-      else {
-        g.C2 = c->ws + p.ring_g[slot]; g.ldc2 = ld_of(p.dB);
-        g.hdr_out = hdr_ptr(c, 1, slot);
-        g.hdr[0] = (int32_t)group; g.hdr[1] = (int32_t)(group + p.s); g.hdr[2] = (int32_t)bs.version;
-      }
-    }
-    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  if (gextra) {
-    ClipNoiseJob j{};
-    j.v = c->ws + p.gpre; j.ldv = ld_of(p.dB); j.v_f32 = 1;
-    j.out = c->ws + p.ring_g[slot]; j.ldo = ld_of(p.dB);
-    j.R = R; j.D = p.dB;
-    j.clip = (c->o.flags & VFL_CLIP_GRAD) != 0; j.C = c->o.clip_c;
-    j.noise = (c->o.flags & VFL_NOISE_GRAD) != 0;
-    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
-    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 1; j.rows = c->aslot.rmap;
-    j.hdr_out = hdr_ptr(c, 1, slot);
-    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)(group + p.s); j.hdr[2] = (int32_t)bs.version;
-    TIMED(VFL_K_CLIP_NOISE, (double)R * p.dB * (4.0 + elt_size(p.e)), st, launch_clip_noise(p.e, j, st));
-  }
-  HIPCHK(hipEventRecord(c->ev_grad[slot], st));
+  vfl_status r = a_top(c, group, slot, c->aslot.rows, c->a_labels, (int32_t)bs.version, loss_dev, nullptr);
+  if (r) return r;
   c->grad_group[slot] = group;
-  c->grad_rows[slot] = R;
+  c->grad_rows[slot] = c->aslot.rows;
   c->a_loss = loss_dev;
   c->a_phase = 2;
   return VFL_OK;
@@ -805,28 +1007,8 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
   if (party == VFL_PARTY_A) {
     if (group != c->a_next || c->a_phase != 2)
       return fail(c, VFL_E_STATE, "A's backward must follow its top step");
-    const int R = c->aslot.rows;
-    vfl_status r = enqueue_dx_chain(c, p.A, 0, R, c->sa);
+    vfl_status r = a_backward(c, (int)(group % (p.s + 1)), c->aslot, c->a_labels, c->a_loss, nullptr);
     if (r) return r;
-    // one weight update for the top model's hidden layers and A's layers,
-    // with the logit layer's reduction, SGD and loss in the same reduction
-    MultiDW m;
-    m.R = R;
-    m.scale = c->o.lr / (float)R;
-    const Top& T = p.T;
-    const void* zA = c->ws + p.A.act[0][p.A.L - 1];
-    const void* zB = c->ws + p.P.zhat[(int)(group % (p.s + 1))];
-    for (int j = 0; j < T.H; ++j)
-      add_dw(m, c->ws + T.dlt[j], T.out[j], j == 0 ? zA : c->ws + T.act[j - 1],
-             j == 0 ? ld_of(p.dA) : ld_of(T.out[j - 1]), j == 0 ? zB : nullptr,
-             j == 0 ? ld_of(p.dB) : 0, j == 0 ? p.dA : 1 << 30, T.in[j], at<float>(c, T.W[j]),
-             at<float>(c, T.b[j]), c->ws + T.Wq[j], T.ldq[j], c->ws + T.Wtq[j], T.ldt[j],
-             T.part[j] ? at<float>(c, T.part[j]) : nullptr, T.partb[j] ? at<float>(c, T.partb[j]) : nullptr,
-             p.splits_a, p.rps_a);
-    add_party_dw(c, m, p.A, 0, c->aslot, p.splits_a, p.rps_a);
-    LogitJob lj = logit_job(c, R, c->a_loss);
-    if ((r = enqueue_weight_update(c, m, &lj, c->sa))) return r;
-    if ((r = enqueue_table_sgd(c, p.A, c->aslot, c->o.lr / (float)R, c->sa))) return r;
     c->a_version += 1;
     c->a_copy_version = c->a_version;
     c->a_next = group + 1;
@@ -838,30 +1020,8 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     const int slot = (int)(group % (p.s + 1));
     if (c->grad_group[slot] != group || c->bslot[slot].group != group)
       return fail(c, VFL_E_NOT_READY, "gradient of this group not published");
-    SlotState& st = c->bslot[slot];
-    HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
-    CutBwdJob cj{};
-    cj.g = c->ws + p.ring_g[slot]; cj.ldg = ld_of(p.dB);
-    cj.z = c->ws + p.P.act[slot][p.P.L - 1]; cj.ldz = ld_of(p.dB);
-    cj.clip = (c->o.flags & VFL_CLIP_EMB) != 0;
-    cj.norm = cj.clip ? at<float>(c, p.P.norm[slot]) : nullptr;
-    cj.cfac = cj.clip ? at<float>(c, p.P.cfac[slot]) : nullptr;
-    cj.C = c->o.clip_c; cj.relu = p.P.relu[p.P.L - 1];
-    cj.delta = c->ws + p.P.dlt[p.P.L - 1]; cj.ldd = ld_of(p.dB);
-    cj.R = st.rows; cj.D = p.dB;
-    cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
-    TIMED(VFL_K_CUT_BWD, (double)st.rows * p.dB * 3.0 * elt_size(p.e) + (cj.clip ? 8.0 * st.rows : 0.0),
-          c->sb, launch_cut_backward(p.e, cj, c->sb));
-    vfl_status r = enqueue_dx_chain(c, p.P, slot, st.rows, c->sb);
+    vfl_status r = b_backward(c, slot, c->bslot[slot], group, nullptr);
     if (r) return r;
-    // SGD on B's current weights; the refreshed operand copies go to this
-    // slot, which B's next forward uses
-    MultiDW m;
-    m.R = st.rows;
-    m.scale = c->o.lr / (float)st.rows;
-    add_party_dw(c, m, p.P, slot, st, p.splits_b, p.rps_b);
-    if ((r = enqueue_weight_update(c, m, nullptr, c->sb))) return r;
-    if ((r = enqueue_table_sgd(c, p.P, st, c->o.lr / (float)st.rows, c->sb))) return r;
     c->b_next_bwd = group + 1;
     c->b_version += 1;
     c->b_copy_version[slot] = c->b_version;
@@ -891,6 +1051,190 @@ vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a, cons
     row[4] = u; row[5] = u % (s + 1); row[6] = c->b_version;
   }
   c->trace.insert(c->trace.end(), row, row + 7);
+  return VFL_OK;
+}
+
+vfl_status vfl_bind_dataset(vfl_ctx* c, const vfl_dataset* a, const vfl_dataset* b, int64_t n_rows) {
+  if (!c || !a || !b || n_rows < 1) return VFL_E_INVALID;
+  const Plan& p = c->p;
+  const int es = elt_size(p.e);
+  const vfl_dataset* ds[2] = {a, b};
+  const Party* P[2] = {&p.A, &p.P};
+  for (int i = 0; i < 2; ++i) {
+    const int64_t ld = ds[i]->ld ? ds[i]->ld : P[i]->spec.dense_in;
+    if (P[i]->spec.dense_in) {
+      if (!ds[i]->dense || ld < P[i]->spec.dense_in)
+        return fail(c, VFL_E_INVALID, "dataset dense input missing or ld too small");
+      if (!P[i]->spec.n_cat && ((ld * es) % 16 || ((uintptr_t)ds[i]->dense) % 16))
+        return fail(c, VFL_E_INVALID, "dataset dense rows must be 16-byte aligned");
+    }
+    if (P[i]->spec.n_cat && !ds[i]->ids) return fail(c, VFL_E_INVALID, "dataset ids missing");
+  }
+  if (!a->labels) return fail(c, VFL_E_INVALID, "dataset labels missing");
+  // captured graphs point at the previous binding
+  for (int q = 0; q < kMaxSlots; ++q) {
+    if (c->gexec[q]) (void)hipGraphExecDestroy(c->gexec[q]);
+    if (c->graph[q]) (void)hipGraphDestroy(c->graph[q]);
+    c->gexec[q] = nullptr;
+    c->graph[q] = nullptr;
+  }
+  c->ds_a = *a;
+  c->ds_b = *b;
+  if (!c->ds_a.ld) c->ds_a.ld = p.A.spec.dense_in;
+  if (!c->ds_b.ld) c->ds_b.ld = p.P.spec.dense_in;
+  c->n_rows = n_rows;
+  c->bound = true;
+  return VFL_OK;
+}
+
+vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t loss_len) {
+  if (!c || n < 0) return VFL_E_INVALID;
+  if (!c->bound) return fail(c, VFL_E_STATE, "no dataset bound");
+  Plan& p = c->p;
+  const int s = p.s, S1 = s + 1;
+  if (loss_ring && loss_len < 1) return fail(c, VFL_E_INVALID, "loss_len must be >= 1");
+  if (t0 < S1 || c->b_next_fwd != t0 || c->b_pub_next != t0 || c->b_next_bwd != t0 - s ||
+      c->a_next != t0 - s || c->a_phase != 0)
+    return fail(c, VFL_E_STATE, "vfl_run continues a run of ticks 0 .. t0-1 with t0 >= s+1");
+  if (c->b_copy_version[t0 % S1] != c->b_version || c->a_copy_version != c->a_version)
+    return fail(c, VFL_E_STATE, "operand copies not current; run vfl_step first");
+  const int cyc = VFL_GRAPH_CYCLES * S1;
+  const int64_t reps = n / cyc;
+  if (reps > 0) {
+    const int phase = (int)(t0 % S1);
+    const uint32_t mask = c->tm.mask;
+    const bool stale = c->gexec[phase] &&
+        (c->graph_loss[phase] != loss_ring || c->graph_loss_len[phase] != loss_len ||
+         c->graph_mask[phase] != mask);
+    if (stale) {
+      (void)hipGraphExecDestroy(c->gexec[phase]);
+      (void)hipGraphDestroy(c->graph[phase]);
+      c->gexec[phase] = nullptr;
+      c->graph[phase] = nullptr;
+    }
+    if (!c->gexec[phase]) {
+      c->gused[phase] = 0;
+      if (mask && c->gpairs[phase].empty()) {
+        constexpr int kGraphPairs = 1024;
+        c->gpairs[phase].resize(kGraphPairs);
+        for (auto& gp : c->gpairs[phase]) {
+          HIPCHK(hipEventCreate(&gp.e0));
+          HIPCHK(hipEventCreate(&gp.e1));
+        }
+      }
+      // capture cyc ticks starting at this phase; the tick records and
+      // counters make the graph independent of the absolute tick
+      TickArgs* ta_a = at<TickArgs>(c, p.ta_a);
+      TickArgs* ta_bf = at<TickArgs>(c, p.ta_bf);
+      TickArgs* ta_bb = at<TickArgs>(c, p.ta_bb);
+      int64_t* ctr = at<int64_t>(c, p.ctr);
+      AdvanceJob adv_a, adv_b;
+      adv_a.counter = ctr; adv_a.out[0] = ta_a; adv_a.kind = 0;
+      adv_b.counter = ctr + 1; adv_b.out[0] = ta_bf; adv_b.out[1] = ta_bb; adv_b.kind = 1;
+      for (AdvanceJob* aj : {&adv_a, &adv_b}) {
+        aj->n_rows = c->n_rows; aj->R = p.R; aj->s = s; aj->lr = c->o.lr;
+        aj->loss_len = loss_ring ? loss_len : 1;
+      }
+      SlotState sa_in, sb_in;
+      sa_in.rows = p.R; sa_in.dense = c->ds_a.dense; sa_in.ld = c->ds_a.ld; sa_in.ids = c->ds_a.ids;
+      sb_in.rows = p.R; sb_in.dense = c->ds_b.dense; sb_in.ld = c->ds_b.ld; sb_in.ids = c->ds_b.ids;
+      c->tm_err = hipSuccess;
+      HIPCHK(hipStreamBeginCapture(c->sa, hipStreamCaptureModeThreadLocal));
+      c->capture_phase = phase;
+      vfl_status r = VFL_OK;
+      hipError_t he = hipEventRecord(c->ev_fork, c->sa);
+      if (he == hipSuccess) he = hipStreamWaitEvent(c->sb, c->ev_fork, 0);
+      for (int i = 0; i < cyc && he == hipSuccess && r == VFL_OK; ++i) {
+        const int fs = (phase + i) % S1;             // slot of group t
+        const int us = ((phase + i - s) % S1 + S1) % S1;   // slot of group t - s
+        he = launch_advance(adv_b, c->sb);
+        if (he == hipSuccess) he = launch_advance(adv_a, c->sa);
+        if (he != hipSuccess) break;
+        if ((r = b_forward(c, fs, sb_in, ta_bf))) break;
+        if ((r = b_publish(c, fs, sb_in, ta_bf))) break;
+        if ((r = a_forward(c, sa_in, ta_a))) break;
+        // the first s ticks consume groups published before this graph;
+        // replays of a graph on one stream never overlap, so the publish
+        // of those groups is already complete
+        if ((r = a_top(c, 0, us, p.R, c->ds_a.labels, 0, loss_ring, ta_a, i >= s))) break;
+        if ((r = a_backward(c, us, sa_in, c->ds_a.labels, loss_ring, ta_a))) break;
+        if ((r = b_backward(c, us, sb_in, 0, ta_bb))) break;
+      }
+      if (he == hipSuccess && r == VFL_OK) he = hipEventRecord(c->ev_join, c->sb);
+      if (he == hipSuccess && r == VFL_OK) he = hipStreamWaitEvent(c->sa, c->ev_join, 0);
+      hipGraph_t g = nullptr;
+      const hipError_t he2 = hipStreamEndCapture(c->sa, &g);
+      c->capture_phase = -1;
+      if (r) { if (g) (void)hipGraphDestroy(g); return r; }
+      if (he != hipSuccess || he2 != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        return fail(c, VFL_E_HIP, std::string("graph capture: ") + hipGetErrorString(he != hipSuccess ? he : he2));
+      }
+      if (c->tm_err != hipSuccess) {
+        const hipError_t te = c->tm_err;
+        c->tm_err = hipSuccess;
+        (void)hipGraphDestroy(g);
+        return fail(c, VFL_E_HIP, std::string("timing event record in graph capture: ") + c->tm_err_what +
+                               ": " + hipGetErrorString(te));
+      }
+      c->graph[phase] = g;
+      HIPCHK(hipGraphInstantiate(&c->gexec[phase], g, nullptr, nullptr, 0));
+      c->graph_loss[phase] = loss_ring;
+      c->graph_loss_len[phase] = loss_len;
+      c->graph_mask[phase] = mask;
+    }
+    // both counters start at t0; the graph's advance kernels read them
+    const int64_t ctr_h[2] = {t0, t0};
+    HIPCHK(hipMemcpyAsync(at<int64_t>(c, p.ctr), ctr_h, sizeof(ctr_h), hipMemcpyHostToDevice, c->sa));
+    // the graph runs both parties' work from stream A: it must follow the
+    // work already enqueued on stream B
+    HIPCHK(hipEventRecord(c->ev_fork, c->sb));
+    HIPCHK(hipStreamWaitEvent(c->sa, c->ev_fork, 0));
+    for (int64_t k = 0; k < reps; ++k) HIPCHK(hipGraphLaunch(c->gexec[phase], c->sa));
+    // later work on stream B must follow the graph
+    HIPCHK(hipEventRecord(c->ev_join, c->sa));
+    HIPCHK(hipStreamWaitEvent(c->sb, c->ev_join, 0));
+    c->last_phase = phase;
+    // host state as if the ticks had been enqueued one by one
+    for (int64_t t = t0; t < t0 + reps * cyc; ++t) {
+      const int64_t u = t - s;
+      const int fs = (int)(t % S1), us = (int)(u % S1);
+      int64_t row[7] = {t, t, fs, c->b_version, u, us, -1};
+      SlotState st;
+      vfl_batch bb[VFL_MAX_REPLICAS];
+      const int nb = dataset_batches(c, 1, t, bb);
+      st.rows = 0;
+      st.rmap = RowMap();
+      st.rmap.n = nb;
+      for (int i = 0; i < nb; ++i) {
+        st.rmap.start[i] = st.rows;
+        st.rmap.row0[i] = bb[i].row0;
+        st.rows += bb[i].rows;
+      }
+      st.dense = bb[0].dense; st.ld = bb[0].ld; st.ids = bb[0].ids;
+      st.group = t; st.version = c->b_version; st.published = true;
+      c->bslot[fs] = st;
+      c->grad_group[us] = u;
+      c->grad_rows[us] = c->bslot[us].rows;
+      c->a_version += 1;
+      c->b_version += 1;
+      c->b_copy_version[us] = c->b_version;
+      row[6] = c->b_version;
+      c->trace.insert(c->trace.end(), row, row + 7);
+    }
+    c->a_copy_version = c->a_version;
+    c->b_next_fwd = c->b_pub_next = t0 + reps * cyc;
+    c->b_next_bwd = c->a_next = t0 + reps * cyc - s;
+  }
+  // the remainder tick by tick
+  for (int64_t t = t0 + reps * cyc; t < t0 + n; ++t) {
+    vfl_batch ab[VFL_MAX_REPLICAS], bb[VFL_MAX_REPLICAS];
+    const int na = dataset_batches(c, 0, t - s, ab);
+    const int nb = dataset_batches(c, 1, t, bb);
+    float* lp = loss_ring ? loss_ring + ((t - s) % loss_len) : nullptr;
+    vfl_status r = vfl_step(c, t, ab, na, bb, nb, lp);
+    if (r) return r;
+  }
   return VFL_OK;
 }
 
@@ -970,6 +1314,17 @@ vfl_status vfl_timing_read(vfl_ctx* c, int32_t cls, double* ms, int64_t* launche
   HIPCHK(hipStreamSynchronize(c->sb));
   if (T.created)
     for (int i = 0; i < Timing::kPool; ++i) harvest(c, i);
+  // event pairs inside the last replayed graph: its last replay's launches
+  if (c->last_phase >= 0)
+    for (int i = 0; i < c->gused[c->last_phase]; ++i) {
+      const vfl_ctx::GPair& gp = c->gpairs[c->last_phase][i];
+      float ms_ = 0.f;
+      if (gp.cls == cls && hipEventElapsedTime(&ms_, gp.e0, gp.e1) == hipSuccess) {
+        T.ms[cls] += ms_;
+        T.wk[cls] += gp.work;
+        T.n[cls] += 1;
+      }
+    }
   if (ms) *ms = T.ms[cls];
   if (launches) *launches = T.n[cls];
   if (work) *work = T.wk[cls];
@@ -996,7 +1351,15 @@ vfl_status vfl_destroy(vfl_ctx* c) {
   for (int q = 0; q < kMaxSlots; ++q) {
     if (c->ev_emb[q]) (void)hipEventDestroy(c->ev_emb[q]);
     if (c->ev_grad[q]) (void)hipEventDestroy(c->ev_grad[q]);
+    if (c->gexec[q]) (void)hipGraphExecDestroy(c->gexec[q]);
+    if (c->graph[q]) (void)hipGraphDestroy(c->graph[q]);
+    for (auto& gp : c->gpairs[q]) {
+      (void)hipEventDestroy(gp.e0);
+      (void)hipEventDestroy(gp.e1);
+    }
   }
+  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+  if (c->ev_join) (void)hipEventDestroy(c->ev_join);
   delete c;
   return r;
 }

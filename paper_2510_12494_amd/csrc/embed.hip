@@ -35,6 +35,11 @@ __device__ __forceinline__ void st1(T* p, float v) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_gather(GatherJob j) {
   const int ne4 = j.E >> 2;                    // float4 chunks per field row
+  if (j.ta) {
+    j.R = j.ta->rows;
+    j.ids += j.ta->row0 * j.n_cat;
+    if (j.dense) j.dense = (const T*)j.dense + j.ta->row0 * j.ldx_in;
+  }
   const int64_t n_emb = (int64_t)j.R * j.n_cat * ne4;
   const int64_t total = n_emb + (int64_t)j.R * j.dense_in;
   T* X = (T*)j.X;
@@ -73,6 +78,11 @@ __global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
   const int tid = threadIdx.x;
   const int f = blockIdx.x;
   const int E = j.E;
+  if (j.ta) {
+    j.R = j.ta->rows;
+    j.scale = j.ta->scale;
+    j.ids += j.ta->row0 * j.n_cat;
+  }
   float* table = j.T + (int64_t)f * j.V * E;
 
   auto apply = [&](uint32_t id, const float (&s)[kMaxEmbDim]) {

@@ -141,6 +141,12 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmNT g) {
   const T* A1 = (const T*)g.A1;
   const T* A2 = (const T*)g.A2;
   const T* Bm = (const T*)g.B;
+  int M = g.M;
+  if (g.ta) {
+    M = g.ta->rows;
+    if (g.ta_in) A1 += g.ta->row0 * g.lda1;
+  }
+  if (m0 >= M) return;
 
   f32x4 acc[BN / 32][BM / 32];
 #pragma unroll
@@ -155,7 +161,7 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmNT g) {
       const int c = tid + 256 * j, row = c >> 3, ch = c & 7;
       const int m = m0 + row, k = k0 + ch * CE;
       u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (m < g.M && k < g.K) {
+      if (m < M && k < g.K) {
         const T* src = k < g.ksplit ? A1 + (int64_t)m * g.lda1 + k
                                     : A2 + (int64_t)m * g.lda2 + (k - g.ksplit);
         v = mask_tail<T>(*(const u32x4*)src, g.K - k);
@@ -195,8 +201,9 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmNT g) {
   }
 
   if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
-    if (g.hdr_out) { g.hdr_out[0] = g.hdr[0]; g.hdr_out[1] = g.hdr[1]; g.hdr_out[2] = g.hdr[2]; }
-    if (g.hdr_chk && g.hdr_chk[0] != g.chk_seq) atomicAdd(g.err, 1);
+    const int32_t* hv = g.ta ? g.ta->hdr : g.hdr;
+    if (g.hdr_out) { g.hdr_out[0] = hv[0]; g.hdr_out[1] = hv[1]; g.hdr_out[2] = hv[2]; }
+    if (g.hdr_chk && g.hdr_chk[0] != (g.ta ? g.ta->chk : g.chk_seq)) atomicAdd(g.err, 1);
   }
 
   T* C1 = (T*)g.C1;
@@ -207,7 +214,7 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmNT g) {
     for (int i = 0; i < BM / 32; ++i) {
       const int m = m0 + wm * (BM / 2) + i * 16 + (lane & 15);
       const int nb = n0 + wn * (BN / 2) + j * 16 + (lane >> 4) * 4;
-      if (m >= g.M || nb >= g.N) continue;
+      if (m >= M || nb >= g.N) continue;
       float v[4] = {acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]};
       const bool full = nb + 4 <= g.N && (nb + 4 <= g.nsplit || nb >= g.nsplit);
       if (full) {
@@ -285,10 +292,13 @@ __global__ __launch_bounds__(256) void k_multi_dw(MultiDW m) {
   const int tiles_k = (g.K + BK - 1) / BK;
   const int tile = lb / g.splits, split = lb % g.splits;
   const int n0 = (tile / tiles_k) * BN, k0 = (tile % tiles_k) * BK;
+  const int rows = m.ta ? m.ta->rows : m.R;
+  const float scale = m.ta ? m.ta->scale : m.scale;
   const int rb = split * g.rows_per_split;
-  const int re = min(m.R, rb + g.rows_per_split);
+  const int re = min(rows, rb + g.rows_per_split);
   const T* D = (const T*)g.D;
   const T* X1 = (const T*)g.X1;
+  if (g.x_ta) X1 += m.ta->row0 * g.ldx1;
   const T* X2 = (const T*)g.X2;
   const bool do_bias = (tile % tiles_k) == 0;
 
@@ -375,14 +385,14 @@ __global__ __launch_bounds__(256) void k_multi_dw(MultiDW m) {
           const int n = nb + r;
           if (n < g.N) {
             float* wp = g.W + (int64_t)n * g.K + k;
-            const float w = *wp - m.scale * acc[j][i][r];
+            const float w = *wp - scale * acc[j][i][r];
             *wp = w;
             copy_out<T>(g.Wq, g.ldq, g.Wtq, g.ldt, n, k, w);
           }
         }
       }
     }
-    if (do_bias && tid < BN && n0 + tid < g.N) g.bias[n0 + tid] -= m.scale * accb;
+    if (do_bias && tid < BN && n0 + tid < g.N) g.bias[n0 + tid] -= scale * accb;
     return;
   }
   float* part = g.part + (int64_t)split * g.N * g.K;
@@ -408,6 +418,7 @@ __global__ __launch_bounds__(256) void k_multi_dw(MultiDW m) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_multi_reduce(MultiDW m, LogitJob lj, int with_logit) {
   int64_t t = blockIdx.x * (int64_t)256 + threadIdx.x;
+  const float scale = m.ta ? m.ta->scale : m.scale;
   for (int q = 0; q < m.n; ++q) {
     const GemmDW& g = m.p[q];
     if (g.splits <= 1) continue;
@@ -438,11 +449,11 @@ __global__ __launch_bounds__(256) void k_multi_reduce(MultiDW m, LogitJob lj, in
     for (int e = 0; e < n_el; ++e) {
       const int64_t idx = base + e;
       if (is_w) {
-        const float w = g.W[idx] - m.scale * sum[e];
+        const float w = g.W[idx] - scale * sum[e];
         g.W[idx] = w;
         copy_out<T>(g.Wq, g.ldq, g.Wtq, g.ldt, (int)(idx / g.K), (int)(idx % g.K), w);
       } else {
-        g.bias[idx] -= m.scale * sum[e];
+        g.bias[idx] -= scale * sum[e];
       }
     }
     return;
@@ -461,12 +472,14 @@ __global__ __launch_bounds__(256) void k_multi_reduce(MultiDW m, LogitJob lj, in
     for (int u = 0; u < 8; ++u) sum += v[u];
   }
   for (; b < lj.blocks; ++b) sum += lj.part[(int64_t)b * W + c];
+  const float ls = lj.ta ? lj.ta->scale : lj.scale;
   if (c == 0) {
-    if (lj.loss_out) *lj.loss_out = sum / (float)lj.R;
+    float* lo = lj.ta ? (lj.loss_base ? lj.loss_base + lj.ta->loss_idx : nullptr) : lj.loss_out;
+    if (lo) *lo = sum / (float)(lj.ta ? lj.ta->rows : lj.R);
   } else if (c == 1) {
-    lj.b[0] -= lj.scale * sum;
+    lj.b[0] -= ls * sum;
   } else {
-    lj.w[c - 2] -= lj.scale * sum;
+    lj.w[c - 2] -= ls * sum;
   }
 }
 

@@ -10,6 +10,39 @@ enum Elt { F32 = 0, BF16 = 1 };
 
 inline int elt_size(Elt e) { return e == F32 ? 4 : 2; }
 
+// Per-tick values that a replayed graph reads from device memory; k_advance
+// writes them at the start of each stream's part of a tick.  A job whose
+// `ta` is set takes its row count (and the values listed with each job)
+// from *ta instead of its immediate fields; with ta_in set its dataset
+// input pointers are bases, offset by ta->row0 rows.
+struct TickArgs {
+  int32_t rows;        // rows of the batch group
+  int32_t group;       // batch-group id (noise step, header sequence)
+  int64_t row0;        // dataset row of the group's first row
+  int32_t hdr[3];      // channel header to write {group, tick, version}
+  int32_t chk;         // group expected in the header of the slot read
+  float scale;         // lr / rows
+  int32_t pad;
+  int64_t loss_idx;    // index of the group's loss in the loss ring
+};
+
+// k_advance: one thread reads this stream's tick counter t, writes the
+// records of tick t of the deterministic schedule over a resident dataset
+// of n_rows rows (group g covers rows [(g mod E) * R, ...), E = ceil(n/R),
+// the last group of an epoch short) and increments the counter.
+// Party A (kind 0): out[0] = group t - s.  Party B (kind 1): out[0] =
+// group t (its forward), out[1] = group t - s (its backward).
+struct AdvanceJob {
+  int64_t* counter = nullptr;
+  TickArgs* out[2] = {nullptr, nullptr};
+  int kind = 0;
+  int64_t n_rows = 0;
+  int R = 0, s = 0;
+  float lr = 0.f;
+  int64_t loss_len = 1;
+};
+hipError_t launch_advance(const AdvanceJob& j, hipStream_t st);
+
 // C[m][n] = epilogue( sum_k A[m][k] * B[n][k] ), A = [A1 | A2] split at
 // column ksplit (A2 may be null when ksplit >= K).  Epilogue: + bias[n],
 // optional ReLU, then columns n < nsplit go to C1 (multiplied by
@@ -30,6 +63,9 @@ struct GemmNT {
   // block 0 against chk_seq (mismatch -> atomic increment of *err)
   int32_t* hdr_out = nullptr; int32_t hdr[3] = {0, 0, 0};
   const int32_t* hdr_chk = nullptr; int32_t chk_seq = 0; int32_t* err = nullptr;
+  // tick record: M = ta->rows; ta_in: A1 += ta->row0 rows; header values
+  // and the expected sequence from *ta
+  const TickArgs* ta = nullptr; int ta_in = 0;
 };
 
 // One layer's weight gradient + SGD: G[n][k] = sum over rows r of
@@ -47,6 +83,7 @@ struct GemmDW {
   void* Wq = nullptr; int64_t ldq = 0; void* Wtq = nullptr; int64_t ldt = 0;
   float* part = nullptr; float* partb = nullptr;
   int N = 0, K = 0, splits = 1, rows_per_split = 0;
+  int x_ta = 0;                        // X1 += ta->row0 rows (dataset input)
 };
 constexpr int kMaxDw = 8;
 // Several layers' weight gradients over the same R rows (one launch).
@@ -55,6 +92,7 @@ struct MultiDW {
   int n = 0, R = 0;
   float scale = 0.f;
   int first_block[kMaxDw + 1] = {0};   // filled by launch_multi_dw
+  const TickArgs* ta = nullptr;        // R = ta->rows, scale = ta->scale
 };
 
 hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st);
@@ -83,6 +121,8 @@ struct LogitJob {
   float* w; float* b; const float* y;
   void* delta; int64_t ldd; int relu;
   float* part; int blocks; float scale; float* loss_out;
+  // tick record: R, scale, y += row0, loss_out = loss_base + loss_idx
+  const TickArgs* ta; float* loss_base;
 };
 hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st);
 // Second stage of the split layers of m and (lj != null) of the logit
@@ -108,6 +148,8 @@ struct ClipNoiseJob {
   int R, D; int clip; float C; int noise; float stdv;
   uint64_t seed; uint32_t step; uint32_t tag; RowMap rows;
   int32_t* hdr_out; int32_t hdr[3];
+  // tick record: R, step = group, global rows from row0, header values
+  const TickArgs* ta;
 };
 hipError_t launch_clip_noise(Elt e, const ClipNoiseJob& j, hipStream_t st);
 
@@ -119,6 +161,7 @@ struct CutBwdJob {
   const float* norm; const float* cfac; int clip; float C; int relu;
   void* delta; int64_t ldd; int R, D;
   const int32_t* hdr_chk; int32_t chk_seq; int32_t* err;
+  const TickArgs* ta;                  // R and the expected sequence
 };
 hipError_t launch_cut_backward(Elt e, const CutBwdJob& j, hipStream_t st);
 
@@ -128,6 +171,7 @@ struct GatherJob {
   const float* T; const int32_t* ids; int n_cat, V, E;
   const void* dense; int64_t ldx_in; int dense_in;
   void* X; int64_t ldx; int R;
+  const TickArgs* ta;                  // R; ids and dense offset by row0 rows
 };
 hipError_t launch_gather(Elt e, const GatherJob& j, hipStream_t st);
 
@@ -139,6 +183,7 @@ constexpr int kMaxEmbDim = 16;
 struct ScatterJob {
   float* T; const int32_t* ids; int n_cat, V, E;
   const float* G; int64_t ldg; int R; float scale;
+  const TickArgs* ta;                  // R, scale; ids offset by row0 rows
 };
 hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st);
 

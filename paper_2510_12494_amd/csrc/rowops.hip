@@ -102,8 +102,10 @@ __global__ __launch_bounds__(256) void k_logit_bce(LogitJob j) {
     }
   const float bias = j.b[0];
   float gb = 0.f, lsum = 0.f;
-  const int per = (j.R + gridDim.x - 1) / gridDim.x;
-  const int rb = blockIdx.x * per, re = min(j.R, rb + per);
+  const int R = j.ta ? j.ta->rows : j.R;
+  const float* Y = j.ta ? j.y + j.ta->row0 : j.y;
+  const int per = (R + gridDim.x - 1) / gridDim.x;
+  const int rb = blockIdx.x * per, re = min(R, rb + per);
   for (int r = rb + grp; r < re; r += G) {
     float h[MAXC][CE];
     float dot = 0.f;
@@ -124,7 +126,7 @@ __global__ __launch_bounds__(256) void k_logit_bce(LogitJob j) {
     }
     for (int o = lpr >> 1; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
     const float l = dot + bias;
-    const float y = j.y[r];
+    const float y = Y[r];
     const float ex = expf(-fabsf(l));
     const float loss = fmaxf(l, 0.f) - y * l + log1pf(ex);
     const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
@@ -211,8 +213,16 @@ __device__ __forceinline__ uint32_t global_row(const RowMap& m, int r) {
 template <typename T, typename V>
 __global__ __launch_bounds__(256) void k_clip_noise(ClipNoiseJob j) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (j.ta) {
+    j.R = j.ta->rows;
+    j.step = (uint32_t)j.ta->group;
+    j.rows.n = 1;
+    j.rows.start[0] = 0;
+    j.rows.row0[0] = j.ta->row0;
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_out) {
-    j.hdr_out[0] = j.hdr[0]; j.hdr_out[1] = j.hdr[1]; j.hdr_out[2] = j.hdr[2];
+    const int32_t* hv = j.ta ? j.ta->hdr : j.hdr;
+    j.hdr_out[0] = hv[0]; j.hdr_out[1] = hv[1]; j.hdr_out[2] = hv[2];
   }
   const V* v = (const V*)j.v;
   T* out = (T*)j.out;
@@ -265,6 +275,10 @@ __global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t st
 template <typename T>
 __global__ __launch_bounds__(256) void k_cut_backward(CutBwdJob j) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (j.ta) {
+    j.R = j.ta->rows;
+    j.chk_seq = j.ta->chk;
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_chk && j.hdr_chk[0] != j.chk_seq)
     atomicAdd(j.err, 1);
   const T* G = (const T*)j.g;
@@ -307,6 +321,39 @@ __global__ __launch_bounds__(256) void k_cast(CastJobs js) {
   }
 }
 
+__device__ void fill_tick(const AdvanceJob& j, TickArgs* o, int64_t g) {
+  const int64_t E = (j.n_rows + j.R - 1) / j.R;
+  const int64_t start = (g % E) * j.R;
+  const int64_t rows = j.n_rows - start < j.R ? j.n_rows - start : j.R;
+  o->rows = (int32_t)rows;
+  o->group = (int32_t)g;
+  o->row0 = start;
+  o->scale = j.lr / (float)rows;
+  o->loss_idx = g % j.loss_len;
+  o->chk = (int32_t)g;
+}
+
+__global__ void k_advance(AdvanceJob j) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int64_t t = *j.counter;
+  *j.counter = t + 1;
+  const int64_t u = t - j.s;
+  if (j.kind == 0) {
+    // party A consumes group u and writes the header of its gradient slot
+    fill_tick(j, j.out[0], u);
+    j.out[0]->hdr[0] = (int32_t)u;
+    j.out[0]->hdr[1] = (int32_t)t;
+    j.out[0]->hdr[2] = (int32_t)(u - j.s > 0 ? u - j.s : 0);
+  } else {
+    // party B publishes group t (version max(0, t - s)) and back-propagates u
+    fill_tick(j, j.out[0], t);
+    j.out[0]->hdr[0] = (int32_t)t;
+    j.out[0]->hdr[1] = (int32_t)t;
+    j.out[0]->hdr[2] = (int32_t)(t - j.s > 0 ? t - j.s : 0);
+    fill_tick(j, j.out[1], u);
+  }
+}
+
 int grid_for(int64_t work, int per_block, int cap) {
   return (int)std::max<int64_t>(1, std::min<int64_t>((work + per_block - 1) / per_block, cap));
 }
@@ -317,6 +364,11 @@ hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st) {
   if (j.Hd > kMaxLogitCols) return hipErrorInvalidValue;
   if (e == BF16) hipLaunchKernelGGL(k_logit_bce<uint16_t>, dim3(j.blocks), dim3(256), 0, st, j);
   else hipLaunchKernelGGL(k_logit_bce<float>, dim3(j.blocks), dim3(256), 0, st, j);
+  return hipGetLastError();
+}
+
+hipError_t launch_advance(const AdvanceJob& j, hipStream_t st) {
+  hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, st, j);
   return hipGetLastError();
 }
 

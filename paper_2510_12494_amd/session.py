@@ -161,6 +161,27 @@ class Session:
         if st != V.VFL_OK:
             V._chk(st, "vfl_step", self.ctx)
 
+    def bind(self):
+        """Bind the resident dataset (all rows) for run()."""
+        ds = []
+        for party in ("A", "B"):
+            x = self.data["xa" if party == "A" else "xb"]
+            ids = self.data["ida" if party == "A" else "idb"]
+            d = V.vfl_dataset()
+            if x is not None:
+                d.dense, d.ld = x.data_ptr(), x.shape[1]
+            if ids is not None:
+                d.ids = ids.data_ptr()
+            if party == "A":
+                d.labels = self.data["y"].data_ptr()
+            ds.append(d)
+        V.vfl_bind_dataset(self.ctx, ds[0], ds[1], self.data["y"].shape[0])
+
+    def run(self, t0: int, n: int):
+        """Ticks t0 .. t0+n-1 over the bound dataset by graph replay; group
+        u's loss lands in the loss ring at u mod its length."""
+        V.vfl_run(self.ctx, t0, n, self.loss.data_ptr(), self.loss.numel())
+
     def message(self, which: int, g: int) -> tuple[np.ndarray, tuple]:
         rows = sum(c for _, c in self.rows_of(g))
         d = self.w.B.widths[-1]

@@ -17,14 +17,15 @@ VFL_PARTY_A, VFL_PARTY_B, VFL_TOP = 0, 1, 2
 VFL_PARAM_W, VFL_PARAM_B, VFL_PARAM_TABLE = 0, 1, 2
 VFL_NOISE_EMB, VFL_NOISE_GRAD, VFL_CLIP_EMB, VFL_CLIP_GRAD = 1, 2, 4, 8
 VFL_MAX_LAYERS = 8
+VFL_GRAPH_CYCLES = 4
 STATUS_NAMES = {0: "VFL_OK", 1: "VFL_E_INVALID", 2: "VFL_E_NOMEM", 3: "VFL_E_HIP",
                 4: "VFL_E_NOT_READY", 5: "VFL_E_STALE", 6: "VFL_E_STATE"}
 
 EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
-           "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_last_error",
-           "vfl_destroy")
+           "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
+           "vfl_last_error", "vfl_destroy")
 KERNEL_CLASSES = ("gemm_fwd", "gemm_dx", "gemm_dw", "reduce", "logit", "clip_noise", "cut_bwd",
                   "cast", "gather", "emb_sgd")
 
@@ -49,6 +50,11 @@ class vfl_opts(C.Structure):
 class vfl_batch(C.Structure):
     _fields_ = [("dense", C.c_void_p), ("ld", C.c_int64), ("ids", C.c_void_p),
                 ("labels", C.c_void_p), ("rows", C.c_int32), ("row0", C.c_int64)]
+
+
+class vfl_dataset(C.Structure):
+    _fields_ = [("dense", C.c_void_p), ("ld", C.c_int64), ("ids", C.c_void_p),
+                ("labels", C.c_void_p)]
 
 
 class VflError(RuntimeError):
@@ -82,6 +88,8 @@ def _load():
         "vfl_philox": [U64, U32, U32, U32, I32, I32, P, P],
         "vfl_timing_enable": [P, U32],
         "vfl_timing_read": [P, I32, C.POINTER(C.c_double), C.POINTER(I64), C.POINTER(C.c_double)],
+        "vfl_bind_dataset": [P, C.POINTER(vfl_dataset), C.POINTER(vfl_dataset), I64],
+        "vfl_run": [P, I64, I64, P, I64],
         "vfl_destroy": [P],
     }
     for name, args in sig.items():
@@ -204,6 +212,14 @@ def vfl_timing_read(ctx, cls: int):
     ms, n, wk = C.c_double(0), C.c_int64(0), C.c_double(0)
     _chk(_lib.vfl_timing_read(ctx, cls, C.byref(ms), C.byref(n), C.byref(wk)), "vfl_timing_read", ctx)
     return ms.value, n.value, wk.value
+
+
+def vfl_bind_dataset(ctx, a: vfl_dataset, b: vfl_dataset, n_rows: int):
+    _chk(_lib.vfl_bind_dataset(ctx, C.byref(a), C.byref(b), n_rows), "vfl_bind_dataset", ctx)
+
+
+def vfl_run(ctx, t0: int, n: int, loss_ptr: int = 0, loss_len: int = 0):
+    _chk(_lib.vfl_run(ctx, t0, n, C.c_void_p(loss_ptr or None), loss_len), "vfl_run", ctx)
 
 
 def vfl_last_error(ctx) -> str:
