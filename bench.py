@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 PEAK = {"bf16": 2.5e15, "f32": 157.3e12}     # dense MFMA FLOP/s (MI355X spec)
 HBM_PEAK = 8.0e12                            # bytes/s
 METRIC = "training samples/sec (both parties fwd+bwd+update) on 1 MI355X; MFMA util %"
-GEMM_CLASSES = ("gemm_fwd", "gemm_dx", "gemm_dw")
+GEMM_CLASSES = ("fwd", "active", "bwd", "dw")
 
 
 def gemm_flops_per_tick(w) -> float:

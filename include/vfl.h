@@ -253,17 +253,15 @@ vfl_status vfl_philox(uint64_t seed, uint32_t step, uint32_t tag, uint32_t row0,
 
 /* Kernel classes for vfl_timing_* (bit i of a mask selects class i). */
 typedef enum {
-  VFL_K_GEMM_FWD = 0,   /* layer forward products (+ bias, ReLU) */
-  VFL_K_GEMM_DX = 1,    /* input-gradient products (+ ReLU mask, split) */
-  VFL_K_GEMM_DW = 2,    /* weight-gradient products (SGD fused when unsplit) */
-  VFL_K_REDUCE = 3,     /* split-partial reductions + SGD (weights, logit) */
-  VFL_K_LOGIT = 4,      /* logit + BCE + its gradient */
-  VFL_K_CLIP_NOISE = 5, /* per-row clip + Philox noise of a message */
-  VFL_K_CUT_BWD = 6,    /* passive party's cut-layer backward */
-  VFL_K_CAST = 7,       /* weight operand copies */
-  VFL_K_GATHER = 8,     /* embedding gather */
-  VFL_K_EMB_SGD = 9,    /* sorted sparse SGD of the tables */
-  VFL_K_COUNT = 10
+  VFL_K_FWD = 0,        /* party B: bottom forward + published embedding */
+  VFL_K_ACTIVE = 1,     /* party A: bottom + top forward, loss, input-gradient
+                           chains, gradient message */
+  VFL_K_BWD = 2,        /* party B: cut-layer backward + input-gradient chain */
+  VFL_K_DW = 3,         /* weight-gradient products (SGD fused when unsplit) */
+  VFL_K_REDUCE = 4,     /* split-partial and logit reductions + SGD */
+  VFL_K_CAST = 5,       /* weight operand copies */
+  VFL_K_EMB_SGD = 6,    /* sorted sparse SGD of the tables */
+  VFL_K_COUNT = 7
 } vfl_kernel_class;
 
 /* Measurement hook: while class_mask is non-zero, every launch of a
@@ -271,8 +269,8 @@ typedef enum {
  * two event records per launch and nothing else).  vfl_timing_read
  * synchronises both streams and returns, for one class, the summed kernel
  * durations in milliseconds, the number of launches and the summed
- * algorithmic work (FLOPs for the three product classes, bytes that the
- * kernel must move at minimum for the others); then it resets that class.
+ * algorithmic work (matrix-product FLOPs for the first four classes, bytes
+ * that the kernel must move at minimum for the others); then it resets that class.
  * Enabling with mask 0 stops recording. */
 vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t class_mask);
 vfl_status vfl_timing_read(vfl_ctx* c, int32_t kernel_class, double* ms, int64_t* launches,

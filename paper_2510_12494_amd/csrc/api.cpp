@@ -1,11 +1,13 @@
 // C ABI of the publisher/subscriber split-learning step (include/vfl.h).
 //
 // Host side only: it validates shapes, lays the caller's workspace out,
-// keeps the channel state machine (which group each slot holds, B's
-// parameter version, how many groups are in flight) and enqueues the
-// kernels of kernels.h on the two party streams.  Party A's work goes to
-// stream_a, party B's to stream_b; the only cross-stream edges are the
-// per-slot "embedding published" and "gradient published" events.
+// plans the LDS layout of the fused chain kernels, writes their job
+// descriptors into the workspace once, keeps the channel state machine
+// (which group each slot holds, B's parameter version, how many groups are
+// in flight) and enqueues the kernels of kernels.h on the two party streams.
+// Party A's work goes to stream_a, party B's to stream_b; the only
+// cross-stream edges are the per-slot "embedding published" and "gradient
+// published" events.
 //
 // Slot reuse needs no further edges: B rewrites embedding slot g mod (s+1)
 // with group g + s + 1 only after its backward of group g, which waited for
@@ -13,13 +15,13 @@
 // gradient slot u mod (s+1) with group u + s + 1 only after waiting for that
 // group's embedding event, recorded by B after its backward of group u.
 //
-// Backward order per party: the input-gradient chain first (every layer's
-// delta kept in its own buffer), then one launch for all layers' weight
-// gradients (SGD fused, operand copies of the new weights refreshed) and one
-// reduction launch for the layers whose rows were split across blocks.  The
-// refreshed copies of party B land in the slot of the group just
-// back-propagated, which is the slot B's next forward uses; a forward casts
-// the master weights only when its slot's copies hold another version.
+// Per tick and party: B runs k_fwd (forward + publish) for group t, and for
+// group u = t - s k_bwd, k_dw and k_dw_reduce; A runs k_active, k_dw and
+// k_dw_reduce for group u (plus the sparse table step with embedding
+// tables).  The weight update refreshes the operand copies of party B in the
+// slot of the group just back-propagated, which is the slot B's next
+// forward uses; a forward casts the master weights only when its slot's
+// copies hold another version.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,7 +39,9 @@ using namespace vfl;
 namespace {
 
 constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
-constexpr int kLogitBlocks = 512;
+constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
+constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
+constexpr int kDwRows = 128;          // rows of one k_dw load group (4 MFMA steps of bf16)
 
 int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
 
@@ -59,12 +63,11 @@ struct Party {
   int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
   size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{}, T = 0;
   size_t Wq[kMaxSlots][VFL_MAX_LAYERS]{}, Wtq[kMaxSlots][VFL_MAX_LAYERS]{};
-  size_t x0[kMaxSlots]{};
-  int64_t ldx0 = 0;
-  size_t act[kMaxSlots][VFL_MAX_LAYERS]{};
-  size_t zhat[kMaxSlots]{};          // published embedding (party B)
+  size_t x0rc[kMaxSlots]{};                     // RC copy of the bottom input
+  size_t arc[kMaxSlots][VFL_MAX_LAYERS]{};      // RC outputs of layers 0 .. L-2
+  size_t drc[VFL_MAX_LAYERS]{};                 // RC deltas of every layer
+  size_t z[kMaxSlots]{}, zhat[kMaxSlots]{};     // party B: last layer, published message
   size_t norm[kMaxSlots]{}, cfac[kMaxSlots]{};
-  size_t dlt[VFL_MAX_LAYERS]{};      // gradient w.r.t. each layer's pre-activation
   size_t gx = 0;
   int64_t ldgx = 0;
   size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
@@ -78,23 +81,59 @@ struct Top {
   int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
   size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{};
   size_t Wq[VFL_MAX_LAYERS]{}, Wtq[VFL_MAX_LAYERS]{};
-  size_t act[VFL_MAX_LAYERS]{};
-  size_t dlt[VFL_MAX_LAYERS]{};
+  size_t arc[VFL_MAX_LAYERS]{}, drc[VFL_MAX_LAYERS]{};
   size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
   size_t logit_part = 0;
 };
 
+// LDS layout of one chain kernel at BR rows per block
+struct Lds {
+  int KS = 32, BR = 16, off = 0;
+  LBuf take(int width, int elt_bytes) {
+    const int cols = (width + KS - 1) / KS * KS;
+    LBuf b;
+    b.off = off;
+    b.pitch = (cols * elt_bytes + 127) / 128 * 128 + 16;
+    off += b.pitch * BR;
+    off = (off + 15) / 16 * 16;
+    return b;
+  }
+  LBuf raw(int bytes) {
+    LBuf b;
+    b.off = off;
+    b.pitch = 1;
+    off += (bytes + 15) / 16 * 16;
+    return b;
+  }
+};
+
+struct FwdLds { LBuf buf[2]; int bytes = 0; };
+struct ActLds {
+  LBuf in, fa[VFL_MAX_LAYERS], cat, ft[VFL_MAX_LAYERS], P[2], msg, red;
+  int bytes = 0;
+};
+struct BwdLds { LBuf P[2], mask; int bytes = 0; };
+
+struct KMeta { int rt = 1, blocks = 1, lds = 0; };
+
+struct DwMeta { int splits = 1, rps = 0, blocks = 0, red_blocks = 0, red_threads = 0, logit_blocks = 0; };
+
 struct Plan {
   Elt e = F32;
-  int s = 0, k = 1, B = 1, R = 1, dA = 0, dB = 0;
+  int s = 0, k = 1, B = 1, R = 1, Ra = 64, dA = 0, dB = 0;
   Party A, P;                         // P: party B (passive)
   Top T;
-  int splits_a = 1, rps_a = 0, splits_b = 1, rps_b = 0;   // weight-gradient row chunks
+  size_t cat_rc = 0;
   size_t ring_g[kMaxSlots]{};
-  size_t gpre = 0;                    // float32 gradient message before clip/noise
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
   size_t ta_a = 0, ta_bf = 0, ta_bb = 0;   // tick records (graph replay)
   size_t ctr = 0;                     // int64 tick counters of streams A and B
+  size_t job_fwd = 0, job_act = 0, job_bwd = 0, job_dwa = 0, job_dwb = 0;
+  KMeta kf, ka, kb;
+  FwdLds lf;
+  ActLds la;
+  BwdLds lb;
+  DwMeta da, db;
   size_t total = 0;
 };
 
@@ -103,10 +142,11 @@ struct SlotState {
   int64_t version = -1;
   bool published = false;
   int rows = 0;
+  int64_t row0 = 0;                   // sample id of row 0
   const void* dense = nullptr;
   int64_t ld = 0;
   const int32_t* ids = nullptr;
-  RowMap rmap;
+  const float* labels = nullptr;
 };
 
 // Event pairs bracketing the launches of the selected kernel classes.
@@ -142,7 +182,6 @@ struct vfl_ctx {
   int64_t a_next = 0, a_version = 0, a_copy_version = -1;
   int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
   SlotState aslot;
-  const float* a_labels = nullptr;
   float* a_loss = nullptr;
   std::vector<int64_t> trace;
   std::string err;
@@ -191,20 +230,86 @@ bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
     why = "embedding dims: vocab in [1, 2^19], emb_dim a multiple of 4 in [4, 16]"; return false;
   }
   if (s->n_cat * (int64_t)std::max(s->emb_dim, 0) + s->dense_in < 1) { why = "empty bottom input"; return false; }
+  if (s->n_cat * (int64_t)std::max(s->emb_dim, 0) + s->dense_in > 65536) { why = "bottom input too wide"; return false; }
   for (int l = 0; l < s->n_layers; ++l)
     if (s->widths[l] < 1 || s->widths[l] > 65536) { why = "bad bottom width"; return false; }
   return true;
 }
 
-// rows per weight-gradient chunk for a launch over `tiles` output tiles:
-// aim at >= 256 blocks, chunks a multiple of the kernel's stage depth
-void dw_chunks(Elt e, int R, int tiles, int& splits, int& rps) {
-  const int RE = dw_stage_rows(e);
-  const int max_splits = std::max(1, (R + RE - 1) / RE);
-  int s = std::min(max_splits, std::max(1, (256 + tiles - 1) / tiles));
-  rps = (R + s - 1) / s;
-  rps = (rps + RE - 1) / RE * RE;
-  splits = (R + rps - 1) / rps;
+int dw_tiles(int N, int K) { return ((N + 63) / 64) * ((K + 63) / 64); }
+
+// Row chunks of a weight-gradient launch over `tiles` output tiles: aim at
+// kDwBlocks blocks, chunks a multiple of kDwRows rows (the rows of one load
+// group of the kernel).
+void dw_split(int R, int tiles, DwMeta& m) {
+  const int max_splits = std::max(1, (R + kDwRows - 1) / kDwRows);
+  const int s = std::min(max_splits, std::max(1, (kDwBlocks + tiles - 1) / tiles));
+  m.rps = ((R + s - 1) / s + kDwRows - 1) / kDwRows * kDwRows;
+  m.splits = (R + m.rps - 1) / m.rps;
+}
+
+// LDS layouts at BR rows per block (bytes in .bytes)
+void plan_fwd_lds(const Plan& p, int BR, FwdLds& f) {
+  Lds l;
+  l.KS = p.e == BF16 ? 32 : 16;
+  l.BR = BR;
+  int w = p.P.din;
+  for (int i = 0; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
+  const int es = elt_size(p.e);
+  f.buf[0] = l.take(w, es);
+  f.buf[1] = l.take(w, es);
+  f.bytes = l.off;
+}
+
+void plan_act_lds(const Plan& p, int BR, bool gextra, ActLds& a) {
+  Lds l;
+  l.KS = p.e == BF16 ? 32 : 16;
+  l.BR = BR;
+  const int es = elt_size(p.e);
+  a.in = l.take(p.A.din, es);
+  for (int i = 0; i + 1 < p.A.L; ++i) a.fa[i] = l.take(p.A.out[i], es);
+  a.cat = l.take(p.dA + p.dB, es);
+  for (int j = 0; j < p.T.H; ++j) a.ft[j] = l.take(p.T.out[j], es);
+  int w = 1;
+  for (int j = 0; j < p.T.H; ++j) w = std::max(w, p.T.out[j]);
+  for (int i = 0; i < p.A.L; ++i) w = std::max(w, p.A.out[i]);
+  a.P[0] = l.take(w, es);
+  a.P[1] = l.take(w, es);
+  if (gextra) a.msg = l.take(p.dB, 4);
+  a.red = l.raw(4 * 4 * (p.T.out[p.T.H - 1] + 2));
+  a.bytes = l.off;
+}
+
+void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
+  Lds l;
+  l.KS = p.e == BF16 ? 32 : 16;
+  l.BR = BR;
+  const int es = elt_size(p.e);
+  int w = 1, wm = 0;
+  for (int i = 0; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
+  for (int i = 0; i + 1 < p.P.L; ++i) wm = std::max(wm, p.P.out[i]);
+  b.P[0] = l.take(w, es);
+  b.P[1] = l.take(w, es);
+  if (wm) b.mask = l.take(wm, es);
+  b.bytes = l.off;
+}
+
+// Rows per block: the largest of 64, 32, 16 whose layout fits the LDS and
+// that still gives kMinBlocks blocks (16 when nothing gives that many).
+template <typename F>
+bool pick_rt(int R, KMeta& m, F&& bytes_at) {
+  for (int rt : {4, 2, 1}) {
+    const int BR = 16 * rt;
+    const int blocks = (R + BR - 1) / BR;
+    const int lds = bytes_at(BR);
+    if (lds > kLdsMax) continue;
+    if (rt > 1 && blocks < kMinBlocks) continue;
+    m.rt = rt;
+    m.blocks = blocks;
+    m.lds = lds;
+    return true;
+  }
+  return false;
 }
 
 std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* t,
@@ -233,9 +338,13 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.k = o->replicas;
   p.B = o->batch;
   p.R = o->batch * o->replicas;
+  p.Ra = (p.R + kDwRows - 1) / kDwRows * kDwRows;   // RC rows: whole k_dw load groups
   const int es = elt_size(p.e);
-  const int64_t R = p.R;
+  const int64_t R = p.R, Ra = p.Ra;
+  const bool eextra = o->flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
+  const bool gextra = o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
   Layout ly;
+  auto rc_bytes = [&](int cols) { return (size_t)es * Ra * ld_of(cols); };
 
   auto party = [&](Party& P, const vfl_bottom_spec* s, int nslots, bool passive) {
     P.spec = *s;
@@ -251,21 +360,20 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       P.ldt[l] = ld_of(P.out[l]);
       P.W[l] = ly.take(sizeof(float) * (size_t)P.out[l] * in);
       P.b[l] = ly.take(sizeof(float) * (size_t)P.out[l]);
-      P.dlt[l] = ly.take((size_t)es * R * ld_of(P.out[l]));
+      P.drc[l] = ly.take(rc_bytes(P.out[l]));
       in = P.out[l];
     }
     if (s->n_cat) P.T = ly.take(sizeof(float) * (size_t)s->n_cat * s->vocab * s->emb_dim);
-    P.ldx0 = ld_of(P.din);
     for (int q = 0; q < nslots; ++q) {
       for (int l = 0; l < P.L; ++l) {
         P.Wq[q][l] = ly.take((size_t)es * P.out[l] * P.ldq[l]);
         P.Wtq[q][l] = ly.take((size_t)es * P.in[l] * P.ldt[l]);
-        P.act[q][l] = ly.take((size_t)es * R * ld_of(P.out[l]));
+        if (l + 1 < P.L) P.arc[q][l] = ly.take(rc_bytes(P.out[l]));
       }
-      if (s->n_cat) P.x0[q] = ly.take((size_t)es * R * P.ldx0);
+      P.x0rc[q] = ly.take(rc_bytes(P.din));
       if (passive) {
-        const bool extra = o->flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
-        P.zhat[q] = extra ? ly.take((size_t)es * R * ld_of(P.out[P.L - 1])) : P.act[q][P.L - 1];
+        P.z[q] = ly.take((size_t)es * R * ld_of(P.out[P.L - 1]));
+        P.zhat[q] = eextra ? ly.take((size_t)es * R * ld_of(P.out[P.L - 1])) : P.z[q];
         if (o->flags & VFL_CLIP_EMB) {
           P.norm[q] = ly.take(sizeof(float) * R);
           P.cfac[q] = ly.take(sizeof(float) * R);
@@ -298,40 +406,333 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     if (j < T.H) {
       T.Wq[j] = ly.take((size_t)es * T.out[j] * T.ldq[j]);
       T.Wtq[j] = ly.take((size_t)es * T.in[j] * T.ldt[j]);
-      T.act[j] = ly.take((size_t)es * R * ld_of(T.out[j]));
-      T.dlt[j] = ly.take((size_t)es * R * ld_of(T.out[j]));
+      if (j + 1 < T.H) T.arc[j] = ly.take(rc_bytes(T.out[j]));
+      T.drc[j] = ly.take(rc_bytes(T.out[j]));
     }
     in = T.out[j];
   }
-  T.logit_part = ly.take(sizeof(float) * kLogitBlocks * (T.out[T.H - 1] + 2));
+  p.cat_rc = ly.take(rc_bytes(p.dA + p.dB));
 
-  // messages
+  // chain kernels: rows per block and LDS layouts
+  if (!pick_rt(p.R, p.kf, [&](int BR) { FwdLds f; plan_fwd_lds(p, BR, f); return f.bytes; }))
+    return "party B's widths exceed the LDS of one workgroup";
+  if (!pick_rt(p.R, p.ka, [&](int BR) { ActLds x; plan_act_lds(p, BR, gextra, x); return x.bytes; }))
+    return "party A's and the top model's widths exceed the LDS of one workgroup";
+  if (!pick_rt(p.R, p.kb, [&](int BR) { BwdLds x; plan_bwd_lds(p, BR, x); return x.bytes; }))
+    return "party B's widths exceed the LDS of one workgroup";
+  plan_fwd_lds(p, 16 * p.kf.rt, p.lf);
+  plan_act_lds(p, 16 * p.ka.rt, gextra, p.la);
+  plan_bwd_lds(p, 16 * p.kb.rt, p.lb);
+  T.logit_part = ly.take(sizeof(float) * (size_t)p.ka.blocks * (T.out[T.H - 1] + 2));
+
+  // messages and control
   for (int q = 0; q <= p.s; ++q) p.ring_g[q] = ly.take((size_t)es * R * ld_of(p.dB));
-  if (o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD)) p.gpre = ly.take(sizeof(float) * R * ld_of(p.dB));
   p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
   p.ta_a = ly.take(sizeof(TickArgs));
   p.ta_bf = ly.take(sizeof(TickArgs));
   p.ta_bb = ly.take(sizeof(TickArgs));
   p.ctr = ly.take(2 * sizeof(int64_t));
 
-  // weight-gradient row chunks and partials (one region per layer: all
-  // layers of a party are in flight in the same launch)
+  // weight gradients: row chunks, partials, block counts
   int tiles_a = 0, tiles_b = 0;
   for (int l = 0; l < p.A.L; ++l) tiles_a += dw_tiles(p.A.out[l], p.A.in[l]);
   for (int j = 0; j < T.H; ++j) tiles_a += dw_tiles(T.out[j], T.in[j]);
   for (int l = 0; l < p.P.L; ++l) tiles_b += dw_tiles(p.P.out[l], p.P.in[l]);
-  dw_chunks(p.e, p.R, tiles_a, p.splits_a, p.rps_a);
-  dw_chunks(p.e, p.R, tiles_b, p.splits_b, p.rps_b);
-  auto parts = [&](int splits, int N, int K, size_t& pw, size_t& pb) {
-    if (splits <= 1) return;
-    pw = ly.take(sizeof(float) * (size_t)splits * N * K);
-    pb = ly.take(sizeof(float) * (size_t)splits * N);
+  dw_split(p.R, tiles_a, p.da);
+  dw_split(p.R, tiles_b, p.db);
+  p.da.blocks = tiles_a * p.da.splits;
+  p.db.blocks = tiles_b * p.db.splits;
+  auto parts = [&](const DwMeta& m, int N, int K, size_t& pw, size_t& pb, int& thr) {
+    if (m.splits <= 1) return;
+    const int kp = (K + 3) / 4 * 4;
+    pw = ly.take(sizeof(float) * (size_t)m.splits * N * kp);
+    pb = ly.take(sizeof(float) * (size_t)m.splits * N);
+    thr += N * (kp / 4) + N;
   };
-  for (int l = 0; l < p.A.L; ++l) parts(p.splits_a, p.A.out[l], p.A.in[l], p.A.part[l], p.A.partb[l]);
-  for (int j = 0; j < T.H; ++j) parts(p.splits_a, T.out[j], T.in[j], T.part[j], T.partb[j]);
-  for (int l = 0; l < p.P.L; ++l) parts(p.splits_b, p.P.out[l], p.P.in[l], p.P.part[l], p.P.partb[l]);
+  for (int l = 0; l < p.A.L; ++l) parts(p.da, p.A.out[l], p.A.in[l], p.A.part[l], p.A.partb[l], p.da.red_threads);
+  for (int j = 0; j < T.H; ++j) parts(p.da, T.out[j], T.in[j], T.part[j], T.partb[j], p.da.red_threads);
+  for (int l = 0; l < p.P.L; ++l) parts(p.db, p.P.out[l], p.P.in[l], p.P.part[l], p.P.partb[l], p.db.red_threads);
+  p.da.red_blocks = (p.da.red_threads + 255) / 256;
+  p.db.red_blocks = (p.db.red_threads + 255) / 256;
+  p.da.logit_blocks = (T.out[T.H - 1] + 2 + 3) / 4;
+
+  // device job descriptors
+  p.job_fwd = ly.take(sizeof(FwdJob) * (p.s + 1));
+  p.job_act = ly.take(sizeof(ActiveJob) * (p.s + 1));
+  p.job_bwd = ly.take(sizeof(BwdJob) * (p.s + 1));
+  p.job_dwa = ly.take(sizeof(DwJob));
+  p.job_dwb = ly.take(sizeof(DwJob) * (p.s + 1));
   p.total = (ly.off + 255) / 256 * 256;
   return "";
+}
+
+int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
+int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
+
+ChainLayer layer(const void* W, int64_t ldw, const float* bias, int N, int K, bool relu, LBuf in,
+                 LBuf out) {
+  ChainLayer L;
+  L.W = W; L.ldw = (int32_t)ldw; L.bias = bias;
+  L.N = N; L.K = K; L.relu = relu ? 1 : 0;
+  L.in = in; L.out = out;
+  return L;
+}
+
+MsgOp msg_op(const vfl_opts& o, bool clip, bool noise, uint32_t tag) {
+  MsgOp m;
+  m.clip = clip; m.noise = noise; m.C = o.clip_c;
+  m.stdv = o.sigma * ((o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? o.clip_c : 1.f);
+  m.seed = o.seed; m.tag = tag;
+  return m;
+}
+
+// Host check of what a chain kernel touches in LDS and in a weight operand:
+// the input buffer holds K columns rounded up to the MFMA depth, the output
+// and mask buffers N columns, all inside the block's LDS, and the operand
+// rows hold K elements rounded up to a 16-byte chunk; the RC copy holds
+// rc_cols columns (N unless given).
+bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_out, int rc_cols = -1) {
+  const int es = elt_size(p.e), KS = p.e == BF16 ? 32 : 16, CE = 16 / es;
+  auto inside = [&](const LBuf& b, int cols) {
+    const int need = (cols + KS - 1) / KS * KS * es;
+    return b.pitch >= need && b.off >= 0 && b.off + b.pitch * BR <= lds && b.off % 16 == 0 && b.pitch % 16 == 0;
+  };
+  if (!L.W || L.N < 1 || L.K < 1 || L.ldw < (L.K + CE - 1) / CE * CE) return false;
+  if (!inside(L.in, L.K)) return false;
+  if (lds_out && !inside(L.out, L.N)) return false;
+  if (L.mask.pitch && !inside(L.mask, L.N)) return false;
+  if (L.rc.p && L.rc.cp < ((rc_cols < 0 ? L.N : rc_cols) + 7) / 8 * 8) return false;
+  return true;
+}
+
+struct Jobs {
+  std::vector<FwdJob> fj;
+  std::vector<ActiveJob> aj;
+  std::vector<BwdJob> bj;
+  std::vector<DwJob> dwb;
+  DwJob dwa;
+};
+
+// The job descriptors of every slot for a workspace at `ws` (host only;
+// empty string when every layer's layout checks out).
+std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
+  struct Base { char* ws; } cb{ws};
+  const Base* c = &cb;
+  const Party& A = p.A;
+  const Party& P = p.P;
+  const Top& T = p.T;
+  const int S1 = p.s + 1;
+  const bool eextra = o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
+  const bool gextra = o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
+  J.fj.assign(S1, FwdJob());
+  J.aj.assign(S1, ActiveJob());
+  J.bj.assign(S1, BwdJob());
+  J.dwb.assign(S1, DwJob());
+  J.dwa = DwJob();
+  std::vector<FwdJob>& fj = J.fj;
+  std::vector<ActiveJob>& aj = J.aj;
+  std::vector<BwdJob>& bj = J.bj;
+  std::vector<DwJob>& dwb = J.dwb;
+  DwJob& dwa = J.dwa;
+  auto at_f = [&](size_t off) { return (float*)(ws + off); };
+  auto hdrp = [&](int which, int slot) { return (int32_t*)(ws + p.hdr) + (which * kMaxSlots + slot) * 4; };
+  auto rcm = [&](const Base*, size_t off, int cols) {
+    RCMat m;
+    m.p = ws + off;
+    m.cp = (int32_t)ld_of(cols);
+    return m;
+  };
+  for (int q = 0; q < S1; ++q) {
+    // party B forward + publish
+    FwdJob& f = fj[q];
+    f.in.dense_in = P.spec.dense_in; f.in.n_cat = P.spec.n_cat; f.in.V = P.spec.vocab; f.in.E = P.spec.emb_dim;
+    f.in.dense_vec = P.spec.n_cat == 0;
+    f.in.T = P.spec.n_cat ? at_f(P.T) : nullptr;
+    f.in.buf = p.lf.buf[0];
+    f.in.rc = rcm(c, P.x0rc[q], P.din);
+    f.L = P.L;
+    for (int l = 0; l < P.L; ++l) {
+      f.l[l] = layer(c->ws + P.Wq[q][l], P.ldq[l], at_f(P.b[l]), P.out[l], P.in[l], P.relu[l],
+                     p.lf.buf[l % 2], p.lf.buf[(l + 1) % 2]);
+      if (l + 1 < P.L) f.l[l].rc = rcm(c, P.arc[q][l], P.out[l]);
+    }
+    f.z = c->ws + P.z[q]; f.ldz = (int32_t)ld_of(p.dB);
+    f.publish = eextra;
+    f.m = msg_op(o, o.flags & VFL_CLIP_EMB, o.flags & VFL_NOISE_EMB, 0);
+    f.zhat = c->ws + P.zhat[q]; f.ldzh = (int32_t)ld_of(p.dB);
+    f.norm = P.norm[q] ? at_f(P.norm[q]) : nullptr;
+    f.cfac = P.cfac[q] ? at_f(P.cfac[q]) : nullptr;
+    f.hdr_out = hdrp(0, q);
+
+    // party A's step against embedding slot q
+    ActiveJob& a = aj[q];
+    const ActLds& la = p.la;
+    a.in.dense_in = A.spec.dense_in; a.in.n_cat = A.spec.n_cat; a.in.V = A.spec.vocab; a.in.E = A.spec.emb_dim;
+    a.in.dense_vec = A.spec.n_cat == 0;
+    a.in.T = A.spec.n_cat ? at_f(A.T) : nullptr;
+    a.in.buf = la.in;
+    a.in.rc = rcm(c, A.x0rc[0], A.din);
+    a.LA = A.L;
+    for (int l = 0; l < A.L; ++l) {
+      const LBuf src = l == 0 ? la.in : la.fa[l - 1];
+      const LBuf dst = l + 1 < A.L ? la.fa[l] : la.cat;
+      a.fa[l] = layer(c->ws + A.Wq[0][l], A.ldq[l], at_f(A.b[l]), A.out[l], A.in[l], A.relu[l], src, dst);
+      if (l + 1 < A.L) a.fa[l].rc = rcm(c, A.arc[0][l], A.out[l]);
+    }
+    a.cat = la.cat; a.cat_rc = rcm(c, p.cat_rc, p.dA + p.dB); a.dA = p.dA; a.dB = p.dB;
+    a.zb = c->ws + P.zhat[q]; a.ldzb = (int32_t)ld_of(p.dB);
+    a.hdr_chk = hdrp(0, q); a.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
+    a.H = T.H;
+    for (int j = 0; j < T.H; ++j) {
+      a.ft[j] = layer(c->ws + T.Wq[j], T.ldq[j], at_f(T.b[j]), T.out[j], T.in[j], T.relu[j],
+                      j == 0 ? la.cat : la.ft[j - 1], la.ft[j]);
+      if (j + 1 < T.H) a.ft[j].rc = rcm(c, T.arc[j], T.out[j]);
+    }
+    a.lw = at_f(T.W[T.H]); a.lb = at_f(T.b[T.H]); a.relu_h = T.relu[T.H - 1];
+    a.dh = la.P[0]; a.dh_rc = rcm(c, T.drc[T.H - 1], T.out[T.H - 1]);
+    a.part = at_f(T.logit_part);
+    a.red = la.red;
+    for (int qq = 0; qq + 1 < T.H; ++qq) {
+      const int j = T.H - 1 - qq;           // delta of top layer j -> layer j-1
+      ChainLayer& L = a.dt[qq];
+      L = layer(c->ws + T.Wtq[j], T.ldt[j], nullptr, T.in[j], T.out[j], false, la.P[qq % 2], la.P[(qq + 1) % 2]);
+      if (T.relu[j - 1]) L.mask = la.ft[j - 1];
+      L.rc = rcm(c, T.drc[j - 1], T.out[j - 1]);
+    }
+    {
+      const int h = T.H - 1;
+      ChainLayer& L = a.dc;
+      L = layer(c->ws + T.Wtq[0], T.ldt[0], nullptr, p.dA + p.dB, T.out[0], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      if (A.relu[A.L - 1]) L.mask = la.cat;
+      L.rc = rcm(c, A.drc[A.L - 1], p.dA);
+    }
+    a.gextra = gextra;
+    a.m = msg_op(o, o.flags & VFL_CLIP_GRAD, o.flags & VFL_NOISE_GRAD, 1);
+    a.msg = la.msg;
+    a.ring = c->ws + p.ring_g[q]; a.ldring = (int32_t)ld_of(p.dB);
+    a.hdr_out = hdrp(1, q);
+    a.nda = A.L - 1;
+    for (int qq = 0; qq + 1 < A.L; ++qq) {
+      const int l = A.L - 1 - qq;           // delta of A's layer l -> layer l-1
+      const int h = T.H + qq;
+      ChainLayer& L = a.da[qq];
+      L = layer(c->ws + A.Wtq[0][l], A.ldt[l], nullptr, A.in[l], A.out[l], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      if (A.relu[l - 1]) L.mask = la.fa[l - 1];
+      L.rc = rcm(c, A.drc[l - 1], A.out[l - 1]);
+    }
+    a.has_gx = A.spec.n_cat > 0;
+    if (a.has_gx) {
+      const int h = T.H + A.L - 1;
+      a.gx = layer(c->ws + A.Wtq[0][0], A.ldt[0], nullptr, A.spec.n_cat * A.spec.emb_dim, A.out[0], false,
+                   la.P[h % 2], LBuf());
+      a.gxp = at_f(A.gx); a.ldgx = (int32_t)A.ldgx;
+    }
+
+    // party B's backward of the group stashed in slot q
+    BwdJob& b = bj[q];
+    const BwdLds& lb = p.lb;
+    b.g = c->ws + p.ring_g[q]; b.ldg = (int32_t)ld_of(p.dB);
+    b.z = c->ws + P.z[q]; b.ldz = (int32_t)ld_of(p.dB);
+    b.clip = (o.flags & VFL_CLIP_EMB) != 0;
+    b.norm = b.clip ? at_f(P.norm[q]) : nullptr;
+    b.cfac = b.clip ? at_f(P.cfac[q]) : nullptr;
+    b.C = o.clip_c; b.relu = P.relu[P.L - 1]; b.D = p.dB;
+    b.d = lb.P[0]; b.d_rc = rcm(c, P.drc[P.L - 1], p.dB);
+    b.hdr_chk = hdrp(1, q); b.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
+    b.nd = P.L - 1;
+    for (int qq = 0; qq + 1 < P.L; ++qq) {
+      const int l = P.L - 1 - qq;
+      ChainLayer& L = b.dx[qq];
+      L = layer(c->ws + P.Wtq[q][l], P.ldt[l], nullptr, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
+      if (P.relu[l - 1]) {
+        L.mask = lb.mask;
+        L.mask_src = rcm(c, P.arc[q][l - 1], P.out[l - 1]);
+      }
+      L.rc = rcm(c, P.drc[l - 1], P.out[l - 1]);
+    }
+    b.has_gx = P.spec.n_cat > 0;
+    if (b.has_gx) {
+      b.gx = layer(c->ws + P.Wtq[q][0], P.ldt[0], nullptr, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
+                   lb.P[(P.L - 1) % 2], LBuf());
+      b.gxp = at_f(P.gx); b.ldgx = (int32_t)P.ldgx;
+    }
+  }
+
+  // weight gradients
+  auto add = [&](DwJob& J, const DwMeta& m, size_t D, size_t X, int N, int K, size_t W, size_t bias,
+                 size_t Wq, int64_t ldq, size_t Wtq, int64_t ldt, size_t part, size_t partb) {
+    DwProb& d = J.p[J.n++];
+    d.D = rcm(c, D, N);
+    d.X = rcm(c, X, K);
+    d.W = at_f(W); d.bias = at_f(bias);
+    d.Wq = c->ws + Wq; d.Wtq = c->ws + Wtq; d.ldq = (int32_t)ldq; d.ldt = (int32_t)ldt;
+    d.part = part ? at_f(part) : nullptr;
+    d.partb = partb ? at_f(partb) : nullptr;
+    d.N = N; d.K = K; d.kp = (K + 3) / 4 * 4;
+    d.splits = m.splits; d.rps = m.rps;
+    d.first_block = J.blocks;
+    J.blocks += dw_tiles(N, K) * m.splits;
+  };
+  for (int j = 0; j < T.H; ++j)
+    add(dwa, p.da, T.drc[j], j == 0 ? p.cat_rc : T.arc[j - 1], T.out[j], T.in[j], T.W[j], T.b[j], T.Wq[j],
+        T.ldq[j], T.Wtq[j], T.ldt[j], T.part[j], T.partb[j]);
+  for (int l = 0; l < A.L; ++l)
+    add(dwa, p.da, A.drc[l], l == 0 ? A.x0rc[0] : A.arc[0][l - 1], A.out[l], A.in[l], A.W[l], A.b[l],
+        A.Wq[0][l], A.ldq[l], A.Wtq[0][l], A.ldt[l], A.part[l], A.partb[l]);
+  dwa.red_threads = p.da.red_threads;
+  dwa.red_blocks = p.da.red_blocks;
+  dwa.lpart = at_f(T.logit_part);
+  dwa.Hd = T.out[T.H - 1];
+  dwa.lrows = 16 * p.ka.rt;
+  dwa.lw = at_f(T.W[T.H]);
+  dwa.lb = at_f(T.b[T.H]);
+  for (int q = 0; q < S1; ++q) {
+    DwJob& J = dwb[q];
+    for (int l = 0; l < P.L; ++l)
+      add(J, p.db, P.drc[l], l == 0 ? P.x0rc[q] : P.arc[q][l - 1], P.out[l], P.in[l], P.W[l], P.b[l],
+          P.Wq[q][l], P.ldq[l], P.Wtq[q][l], P.ldt[l], P.part[l], P.partb[l]);
+    J.red_threads = p.db.red_threads;
+    J.red_blocks = p.db.red_blocks;
+  }
+  if (dwa.blocks != p.da.blocks || dwb[0].blocks != p.db.blocks)
+    return "internal: weight-gradient block count mismatch";
+  for (int q = 0; q < S1; ++q) {
+    bool ok = true;
+    const int bf = 16 * p.kf.rt, ba = 16 * p.ka.rt, bb = 16 * p.kb.rt;
+    for (int l = 0; l < fj[q].L; ++l) ok = ok && layer_fits(p, fj[q].l[l], bf, p.kf.lds, true);
+    for (int l = 0; l < aj[q].LA; ++l) ok = ok && layer_fits(p, aj[q].fa[l], ba, p.ka.lds, true);
+    for (int j = 0; j < aj[q].H; ++j) ok = ok && layer_fits(p, aj[q].ft[j], ba, p.ka.lds, true);
+    for (int j = 0; j + 1 < aj[q].H; ++j) ok = ok && layer_fits(p, aj[q].dt[j], ba, p.ka.lds, true);
+    ok = ok && layer_fits(p, aj[q].dc, ba, p.ka.lds, true, p.dA);   // RC copy: A's columns only
+    for (int l = 0; l < aj[q].nda; ++l) ok = ok && layer_fits(p, aj[q].da[l], ba, p.ka.lds, true);
+    if (aj[q].has_gx) ok = ok && layer_fits(p, aj[q].gx, ba, p.ka.lds, false);
+    for (int l = 0; l < bj[q].nd; ++l) ok = ok && layer_fits(p, bj[q].dx[l], bb, p.kb.lds, true);
+    if (bj[q].has_gx) ok = ok && layer_fits(p, bj[q].gx, bb, p.kb.lds, false);
+    ok = ok && p.la.red.off + 16 * (p.T.out[p.T.H - 1] + 2) <= p.ka.lds;
+    if (!ok) return "internal: chain layout does not cover a layer";
+  }
+  return "";
+}
+
+// Write the job descriptors into the workspace (once, at creation).
+vfl_status write_jobs(vfl_ctx* c) {
+  const Plan& p = c->p;
+  const int S1 = p.s + 1;
+  Jobs J;
+  const std::string why = build_jobs(p, c->o, c->ws, J);
+  if (!why.empty()) return fail(c, VFL_E_INVALID, why);
+  const std::vector<FwdJob>& fj = J.fj;
+  const std::vector<ActiveJob>& aj = J.aj;
+  const std::vector<BwdJob>& bj = J.bj;
+  const std::vector<DwJob>& dwb = J.dwb;
+  const DwJob& dwa = J.dwa;
+
+  HIPCHK(hipMemcpy(c->ws + p.job_fwd, fj.data(), sizeof(FwdJob) * S1, hipMemcpyHostToDevice));
+  HIPCHK(hipMemcpy(c->ws + p.job_act, aj.data(), sizeof(ActiveJob) * S1, hipMemcpyHostToDevice));
+  HIPCHK(hipMemcpy(c->ws + p.job_bwd, bj.data(), sizeof(BwdJob) * S1, hipMemcpyHostToDevice));
+  HIPCHK(hipMemcpy(c->ws + p.job_dwa, &dwa, sizeof(DwJob), hipMemcpyHostToDevice));
+  HIPCHK(hipMemcpy(c->ws + p.job_dwb, dwb.data(), sizeof(DwJob) * S1, hipMemcpyHostToDevice));
+  return VFL_OK;
 }
 
 // Validate k back-to-back replica batches; fills the slot description.
@@ -349,8 +750,6 @@ vfl_status take_batches(vfl_ctx* c, const Party& P, const vfl_batch* br, int n, 
   if (P.spec.n_cat && !br[0].ids) return fail(c, VFL_E_INVALID, "ids missing");
   if (need_labels && !br[0].labels) return fail(c, VFL_E_INVALID, "labels missing");
   int64_t off = 0;
-  st.rmap = RowMap();
-  st.rmap.n = n;
   for (int r = 0; r < n; ++r) {
     const vfl_batch& x = br[r];
     if (x.rows < 1 || x.rows > p.B || (r + 1 < n && x.rows != p.B))
@@ -363,14 +762,14 @@ vfl_status take_batches(vfl_ctx* c, const Party& P, const vfl_batch* br, int n, 
       if (need_labels) ok = ok && x.labels == br[0].labels + off;
       if (!ok) return fail(c, VFL_E_INVALID, "replica batches must lie back to back");
     }
-    st.rmap.start[r] = (int32_t)off;
-    st.rmap.row0[r] = x.row0;
     off += x.rows;
   }
   st.rows = (int)off;
+  st.row0 = br[0].row0;
   st.dense = br[0].dense;
   st.ld = ld;
   st.ids = br[0].ids;
+  st.labels = br[0].labels;
   return VFL_OK;
 }
 
@@ -454,10 +853,7 @@ void tend(vfl_ctx* c, int i, hipStream_t st) {
     tend(c, ts_, (st));                                 \
   } while (0)
 
-double gemm_flops(int M, int N, int K) { return 2.0 * M * (double)N * K; }
-
-int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
-int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
+double mm_flops(int R, int N, int K) { return 2.0 * R * (double)N * K; }
 
 // ------------------------------------------------------------ enqueue steps
 // Every enqueue function below takes an optional tick record `ta`: null when
@@ -479,288 +875,114 @@ vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipS
   return VFL_OK;
 }
 
-// Party bottom forward (gather + layers) into slot `slot`.  With a tick
-// record the input pointers in `in` are dataset bases.
-vfl_status enqueue_bottom_forward(vfl_ctx* c, const Party& P, int slot, const SlotState& in,
-                                  hipStream_t st, int32_t* hdr_out, const int32_t hdr[3],
-                                  const TickArgs* ta) {
-  const Plan& p = c->p;
-  const int R = in.rows;
-  const void* x = in.dense;
-  int64_t ldx = in.ld;
-  if (P.spec.n_cat) {
-    GatherJob gj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                 in.dense, in.ld, P.spec.dense_in, c->ws + P.x0[slot], P.ldx0, R, ta};
-    const double gb = (double)R * P.spec.n_cat * (4 + P.spec.emb_dim * (4.0 + elt_size(p.e))) +
-                      2.0 * R * P.spec.dense_in * elt_size(p.e);
-    TIMED(VFL_K_GATHER, gb, st, launch_gather(p.e, gj, st));
-    x = c->ws + P.x0[slot];
-    ldx = P.ldx0;
-  }
-  for (int l = 0; l < P.L; ++l) {
-    GemmNT g;
-    g.A1 = l == 0 ? x : c->ws + P.act[slot][l - 1];
-    g.lda1 = l == 0 ? ldx : ld_of(P.out[l - 1]);
-    g.B = c->ws + P.Wq[slot][l];
-    g.ldb = P.ldq[l];
-    g.C1 = c->ws + P.act[slot][l];
-    g.ldc1 = ld_of(P.out[l]);
-    g.bias = at<float>(c, P.b[l]);
-    g.relu = P.relu[l];
-    g.M = R; g.N = P.out[l]; g.K = P.in[l];
-    g.ta = ta;
-    g.ta_in = (ta && l == 0 && !P.spec.n_cat) ? 1 : 0;
-    if (l == P.L - 1 && hdr_out) {
-      g.hdr_out = hdr_out;
-      if (hdr) { g.hdr[0] = hdr[0]; g.hdr[1] = hdr[1]; g.hdr[2] = hdr[2]; }
-    }
-    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  return VFL_OK;
+ChainCall call_of(const SlotState& st, int64_t group, const int32_t hdr[3], int64_t chk) {
+  ChainCall k;
+  k.dense = st.dense; k.ld = st.ld; k.ids = st.ids; k.labels = st.labels;
+  k.row0 = st.row0; k.rows = st.rows; k.group = (int32_t)group;
+  if (hdr) { k.hdr[0] = hdr[0]; k.hdr[1] = hdr[1]; k.hdr[2] = hdr[2]; }
+  k.chk = (int32_t)chk;
+  return k;
 }
 
-// Input-gradient chain of a bottom model: from dlt[L-1] down to dlt[0], and
-// for tables the float32 gradient of the gathered input columns.
-vfl_status enqueue_dx_chain(vfl_ctx* c, const Party& P, int slot, int R, hipStream_t st,
-                            const TickArgs* ta) {
-  const Plan& p = c->p;
-  for (int l = P.L - 1; l >= 1; --l) {
-    GemmNT g;
-    g.A1 = c->ws + P.dlt[l]; g.lda1 = ld_of(P.out[l]);
-    g.B = c->ws + P.Wtq[slot][l]; g.ldb = P.ldt[l];
-    g.C1 = c->ws + P.dlt[l - 1]; g.ldc1 = ld_of(P.out[l - 1]);
-    if (P.relu[l - 1]) { g.mask = c->ws + P.act[slot][l - 1]; g.ldm = ld_of(P.out[l - 1]); }
-    g.M = R; g.N = P.in[l]; g.K = P.out[l];
-    g.ta = ta;
-    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  if (P.spec.n_cat) {
-    GemmNT g;
-    g.A1 = c->ws + P.dlt[0]; g.lda1 = ld_of(P.out[0]);
-    g.B = c->ws + P.Wtq[slot][0]; g.ldb = P.ldt[0];
-    g.C2 = c->ws + P.gx; g.ldc2 = P.ldgx; g.nsplit = 0; g.c2_f32 = 1;
-    g.M = R; g.N = P.spec.n_cat * P.spec.emb_dim; g.K = P.out[0];
-    g.ta = ta;
-    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  return VFL_OK;
+double party_fwd_flops(const Party& P, int R) {
+  double f = 0;
+  for (int l = 0; l < P.L; ++l) f += mm_flops(R, P.out[l], P.in[l]);
+  return f;
 }
 
-void add_dw(MultiDW& m, const void* D, int N, const void* X1, int64_t ldx1, const void* X2,
-            int64_t ldx2, int ksplit, int K, float* W, float* bias, void* Wq, int64_t ldq,
-            void* Wtq, int64_t ldt, float* part, float* partb, int splits, int rps) {
-  GemmDW& d = m.p[m.n++];
-  d.D = D; d.ldd = ld_of(N);
-  d.X1 = X1; d.ldx1 = ldx1; d.X2 = X2; d.ldx2 = ldx2; d.ksplit = ksplit;
-  d.W = W; d.bias = bias; d.Wq = Wq; d.ldq = ldq; d.Wtq = Wtq; d.ldt = ldt;
-  d.part = part; d.partb = partb;
-  d.N = N; d.K = K;
-  d.splits = splits; d.rows_per_split = rps;
+double party_dx_flops(const Party& P, int R) {
+  double f = 0;
+  for (int l = 1; l < P.L; ++l) f += mm_flops(R, P.in[l], P.out[l]);
+  if (P.spec.n_cat) f += mm_flops(R, P.spec.n_cat * P.spec.emb_dim, P.out[0]);
+  return f;
 }
 
-// Bottom layers' weight gradients of one party appended to m.  With a tick
-// record the dense input in `in` is a dataset base.
-void add_party_dw(vfl_ctx* c, MultiDW& m, const Party& P, int slot, const SlotState& in,
-                  int splits, int rps, bool dataset_in) {
-  const void* x = P.spec.n_cat ? (const void*)(c->ws + P.x0[slot]) : in.dense;
-  const int64_t ldx = P.spec.n_cat ? P.ldx0 : in.ld;
-  for (int l = 0; l < P.L; ++l) {
-    add_dw(m, c->ws + P.dlt[l], P.out[l], l == 0 ? x : c->ws + P.act[slot][l - 1],
-           l == 0 ? ldx : ld_of(P.out[l - 1]), nullptr, 0, 1 << 30, P.in[l], at<float>(c, P.W[l]),
-           at<float>(c, P.b[l]), c->ws + P.Wq[slot][l], P.ldq[l], c->ws + P.Wtq[slot][l], P.ldt[l],
-           P.part[l] ? at<float>(c, P.part[l]) : nullptr, P.partb[l] ? at<float>(c, P.partb[l]) : nullptr,
-           splits, rps);
-    if (l == 0 && dataset_in && !P.spec.n_cat) m.p[m.n - 1].x_ta = 1;
-  }
-}
-
-vfl_status enqueue_weight_update(vfl_ctx* c, MultiDW& m, const LogitJob* lj, hipStream_t st) {
-  const Plan& p = c->p;
-  double flops = 0, rbytes = 0;
-  bool split = false;
-  for (int q = 0; q < m.n; ++q) {
-    flops += gemm_flops(m.R, m.p[q].N, m.p[q].K);
-    if (m.p[q].splits > 1) {
-      split = true;
-      rbytes += 4.0 * ((double)m.p[q].N * m.p[q].K + m.p[q].N) * (m.p[q].splits + 2);
-    }
-  }
-  TIMED(VFL_K_GEMM_DW, flops, st, launch_multi_dw(p.e, m, st));
-  if (split || lj) {
-    if (lj) rbytes += 4.0 * lj->blocks * (lj->Hd + 2) + 8.0 * lj->Hd;
-    TIMED(VFL_K_REDUCE, rbytes, st, launch_multi_reduce(p.e, m, lj, st));
-  }
-  return VFL_OK;
-}
-
-vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const SlotState& in, float scale,
+// sparse SGD of a party's tables from its float32 input gradient gx
+vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const int32_t* ids, int R, float scale,
                              hipStream_t st, const TickArgs* ta) {
   if (!P.spec.n_cat) return VFL_OK;
-  ScatterJob sj{at<float>(c, P.T), in.ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                at<float>(c, P.gx), P.ldgx, in.rows, scale, ta};
-  TIMED(VFL_K_EMB_SGD, (double)in.rows * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
+  ScatterJob sj{at<float>(c, P.T), ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
+                at<float>(c, P.gx), P.ldgx, R, scale, ta};
+  TIMED(VFL_K_EMB_SGD, (double)R * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
         launch_scatter_sgd(sj, st));
   return VFL_OK;
 }
 
-LogitJob logit_job(vfl_ctx* c, int R, const float* labels, float* loss_dev, const TickArgs* ta) {
+// one party's weight gradients + SGD (+ the logit layer and loss for A)
+vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, const TickArgs* ta,
+                      hipStream_t st) {
   const Plan& p = c->p;
-  const Top& T = p.T;
-  LogitJob lj{};
-  lj.H = c->ws + T.act[T.H - 1]; lj.ldh = ld_of(T.out[T.H - 1]); lj.Hd = T.out[T.H - 1]; lj.R = R;
-  lj.w = at<float>(c, T.W[T.H]); lj.b = at<float>(c, T.b[T.H]); lj.y = labels;
-  lj.delta = c->ws + T.dlt[T.H - 1]; lj.ldd = ld_of(T.out[T.H - 1]); lj.relu = T.relu[T.H - 1];
-  lj.part = at<float>(c, T.logit_part);
-  // blocking from the configured rows per tick, so that a short group is
-  // cut the same way whether its row count is known on the host or read
-  // from a tick record
-  lj.blocks = std::max(1, std::min(kLogitBlocks, (p.R + 15) / 16));
-  lj.scale = c->o.lr / (float)R;
-  lj.loss_out = ta ? nullptr : loss_dev;
-  lj.ta = ta;
-  lj.loss_base = ta ? loss_dev : nullptr;
-  return lj;
+  const DwMeta& m = party_a ? p.da : p.db;
+  const DwJob* job = party_a ? (const DwJob*)(c->ws + p.job_dwa) : (const DwJob*)(c->ws + p.job_dwb) + slot;
+  const float scale = c->o.lr / (float)R;
+  double flops = 0;
+  if (party_a) {
+    for (int j = 0; j < p.T.H; ++j) flops += mm_flops(R, p.T.out[j], p.T.in[j]);
+    flops += party_fwd_flops(p.A, R);
+  } else {
+    flops += party_fwd_flops(p.P, R);
+  }
+  TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, ta, st));
+  const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);
+  if (blocks > 0) {
+    double bytes = 0;
+    const Party& P = party_a ? p.A : p.P;
+    auto add = [&](int N, int K) { bytes += 4.0 * ((double)N * K + N) * (m.splits + 2); };
+    if (m.splits > 1) {
+      for (int l = 0; l < P.L; ++l) add(P.out[l], P.in[l]);
+      if (party_a)
+        for (int j = 0; j < p.T.H; ++j) add(p.T.out[j], p.T.in[j]);
+    }
+    if (party_a) bytes += 4.0 * p.ka.blocks * (p.T.out[p.T.H - 1] + 2);
+    TIMED(VFL_K_REDUCE, bytes, st,
+          launch_dw_reduce(p.e, job, blocks, R, scale, ta ? nullptr : loss, ta, ta ? loss : nullptr, st));
+  }
+  return VFL_OK;
 }
 
 // ---- the phases of a tick (enqueue only; the callers keep the host state)
 
-// B's forward of group `group` into `slot`; the embedding slot header is
-// written by the last layer unless clip/noise publish it.
+// B's forward + publish of `st` (group st.group) into `slot`.
 vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, const TickArgs* ta) {
   const Plan& p = c->p;
-  const bool extra = c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
   const int32_t hdr[3] = {(int32_t)st.group, (int32_t)st.group, (int32_t)st.version};
-  return enqueue_bottom_forward(c, p.P, slot, st, c->sb, extra ? nullptr : hdr_ptr(c, 0, slot),
-                                ta ? nullptr : hdr, ta);
+  const ChainCall k = call_of(st, st.group, hdr, 0);
+  TIMED(VFL_K_FWD, party_fwd_flops(p.P, p.R), c->sb,
+        launch_fwd(p.e, p.kf.rt, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k, ta, c->sb));
+  return VFL_OK;
 }
 
-vfl_status b_publish(vfl_ctx* c, int slot, const SlotState& st, const TickArgs* ta) {
-  const Plan& p = c->p;
-  if (c->o.flags & (VFL_CLIP_EMB | VFL_NOISE_EMB)) {
-    ClipNoiseJob j{};
-    j.v = c->ws + p.P.act[slot][p.P.L - 1]; j.ldv = ld_of(p.dB); j.v_f32 = p.e == F32;
-    j.out = c->ws + p.P.zhat[slot]; j.ldo = ld_of(p.dB);
-    j.norm = p.P.norm[slot] ? at<float>(c, p.P.norm[slot]) : nullptr;
-    j.cfac = p.P.cfac[slot] ? at<float>(c, p.P.cfac[slot]) : nullptr;
-    j.R = st.rows; j.D = p.dB;
-    j.clip = (c->o.flags & VFL_CLIP_EMB) != 0; j.C = c->o.clip_c;
-    j.noise = (c->o.flags & VFL_NOISE_EMB) != 0;
-    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
-    j.seed = c->o.seed; j.step = (uint32_t)st.group; j.tag = 0; j.rows = st.rmap;
-    j.hdr_out = hdr_ptr(c, 0, slot);
-    j.hdr[0] = (int32_t)st.group; j.hdr[1] = (int32_t)st.group; j.hdr[2] = (int32_t)st.version;
-    j.ta = ta;
-    TIMED(VFL_K_CLIP_NOISE, (double)st.rows * p.dB * (elt_size(p.e) * 2.0) + 8.0 * st.rows, c->sb,
-          launch_clip_noise(p.e, j, c->sb));
-  }
+vfl_status b_publish(vfl_ctx* c, int slot) {
   HIPCHK(hipEventRecord(c->ev_emb[slot], c->sb));
   return VFL_OK;
 }
 
-vfl_status a_forward(vfl_ctx* c, const SlotState& st, const TickArgs* ta) {
-  return enqueue_bottom_forward(c, c->p.A, 0, st, c->sa, nullptr, nullptr, ta);
-}
-
-// Top model step of A's group (rows R) against embedding slot `slot`:
-// forward, logit + BCE, input-gradient chain, gradient message + event.
-vfl_status a_top(vfl_ctx* c, int64_t group, int slot, int R, const float* labels,
-                 int32_t b_version, float* loss_dev, const TickArgs* ta, bool wait_emb = true) {
+// A's forward, top model, loss and input-gradient chains of group `group`
+// (A's batch in `st`) against embedding slot `slot`; gradient message +
+// event.
+vfl_status a_top(vfl_ctx* c, int64_t group, int slot, const SlotState& st, int32_t b_version,
+                 const TickArgs* ta, bool wait_emb = true) {
   const Plan& p = c->p;
-  hipStream_t st = c->sa;
-  if (wait_emb) HIPCHK(hipStreamWaitEvent(st, c->ev_emb[slot], 0));
-  const Top& T = p.T;
-  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
-  const void* zB = c->ws + p.P.zhat[slot];
-  for (int j = 0; j < T.H; ++j) {
-    GemmNT g;
-    if (j == 0) {
-      g.A1 = zA; g.lda1 = ld_of(p.dA);
-      g.A2 = zB; g.lda2 = ld_of(p.dB); g.ksplit = p.dA;
-      g.hdr_chk = hdr_ptr(c, 0, slot); g.chk_seq = (int32_t)group; g.err = err_ptr(c);
-    } else {
-      g.A1 = c->ws + T.act[j - 1]; g.lda1 = ld_of(T.out[j - 1]);
-    }
-    g.B = c->ws + T.Wq[j]; g.ldb = T.ldq[j];
-    g.C1 = c->ws + T.act[j]; g.ldc1 = ld_of(T.out[j]);
-    g.bias = at<float>(c, T.b[j]); g.relu = T.relu[j];
-    g.M = R; g.N = T.out[j]; g.K = T.in[j];
-    g.ta = ta;
-    TIMED(VFL_K_GEMM_FWD, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  // logit + BCE; its reduction and SGD run with the weight update
-  LogitJob lj = logit_job(c, R, labels, loss_dev, ta);
-  TIMED(VFL_K_LOGIT, (double)R * lj.Hd * 2.0 * elt_size(p.e) + 4.0 * R, st, launch_logit_bce(p.e, lj, st));
-  // input-gradient chain of the top model; the last product splits into A's
-  // cut-layer delta and the per-row gradient message for B
-  const bool gextra = c->o.flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
-  for (int j = T.H - 1; j >= 0; --j) {
-    GemmNT g;
-    g.A1 = c->ws + T.dlt[j]; g.lda1 = ld_of(T.out[j]);
-    g.B = c->ws + T.Wtq[j]; g.ldb = T.ldt[j];
-    g.M = R; g.N = T.in[j]; g.K = T.out[j];
-    g.ta = ta;
-    if (j > 0) {
-      g.C1 = c->ws + T.dlt[j - 1]; g.ldc1 = ld_of(T.out[j - 1]);
-      if (T.relu[j - 1]) { g.mask = c->ws + T.act[j - 1]; g.ldm = ld_of(T.out[j - 1]); }
-    } else {
-      g.C1 = c->ws + p.A.dlt[p.A.L - 1]; g.ldc1 = ld_of(p.dA);
-      if (p.A.relu[p.A.L - 1]) { g.mask = zA; g.ldm = ld_of(p.dA); }
-      g.nsplit = p.dA;
-      if (gextra) { g.C2 = c->ws + p.gpre; g.ldc2 = ld_of(p.dB); g.c2_f32 = 1; }
-      else {
-        g.C2 = c->ws + p.ring_g[slot]; g.ldc2 = ld_of(p.dB);
-        g.hdr_out = hdr_ptr(c, 1, slot);
-        g.hdr[0] = (int32_t)group; g.hdr[1] = (int32_t)(group + p.s); g.hdr[2] = b_version;
-      }
-    }
-    TIMED(VFL_K_GEMM_DX, gemm_flops(g.M, g.N, g.K), st, launch_gemm_nt(p.e, g, st));
-  }
-  if (gextra) {
-    ClipNoiseJob j{};
-    j.v = c->ws + p.gpre; j.ldv = ld_of(p.dB); j.v_f32 = 1;
-    j.out = c->ws + p.ring_g[slot]; j.ldo = ld_of(p.dB);
-    j.R = R; j.D = p.dB;
-    j.clip = (c->o.flags & VFL_CLIP_GRAD) != 0; j.C = c->o.clip_c;
-    j.noise = (c->o.flags & VFL_NOISE_GRAD) != 0;
-    j.stdv = c->o.sigma * ((c->o.flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) ? c->o.clip_c : 1.f);
-    j.seed = c->o.seed; j.step = (uint32_t)group; j.tag = 1; j.rows = c->aslot.rmap;
-    j.hdr_out = hdr_ptr(c, 1, slot);
-    j.hdr[0] = (int32_t)group; j.hdr[1] = (int32_t)(group + p.s); j.hdr[2] = b_version;
-    j.ta = ta;
-    TIMED(VFL_K_CLIP_NOISE, (double)R * p.dB * (4.0 + elt_size(p.e)), st, launch_clip_noise(p.e, j, st));
-  }
-  HIPCHK(hipEventRecord(c->ev_grad[slot], st));
+  if (wait_emb) HIPCHK(hipStreamWaitEvent(c->sa, c->ev_emb[slot], 0));
+  const int32_t hdr[3] = {(int32_t)group, (int32_t)(group + p.s), b_version};
+  const ChainCall k = call_of(st, group, hdr, group);
+  const int R = p.R;
+  double f = party_fwd_flops(p.A, R) + party_dx_flops(p.A, R) + mm_flops(R, p.dA + p.dB, p.T.out[0]);
+  for (int j = 0; j < p.T.H; ++j) f += mm_flops(R, p.T.out[j], p.T.in[j]);
+  for (int j = 1; j < p.T.H; ++j) f += mm_flops(R, p.T.in[j], p.T.out[j]);
+  TIMED(VFL_K_ACTIVE, f, c->sa,
+        launch_active(p.e, p.ka.rt, (const ActiveJob*)(c->ws + p.job_act) + slot, p.ka.lds, p.ka.blocks, k,
+                      ta, c->sa));
+  HIPCHK(hipEventRecord(c->ev_grad[slot], c->sa));
   return VFL_OK;
 }
 
-// A's and the top model's backward + SGD for A's group in `st` (rows R);
-// `slot` is the embedding slot the top model read.
-vfl_status a_backward(vfl_ctx* c, int slot, const SlotState& st, const float* labels,
-                      float* loss_dev, const TickArgs* ta) {
+// A's and the top model's SGD for A's group (rows R).
+vfl_status a_backward(vfl_ctx* c, const SlotState& st, float* loss, const TickArgs* ta) {
   const Plan& p = c->p;
-  const int R = st.rows;
-  vfl_status r = enqueue_dx_chain(c, p.A, 0, R, c->sa, ta);
+  vfl_status r = enqueue_dw(c, true, 0, st.rows, loss, ta, c->sa);
   if (r) return r;
-  // one weight update for the top model's hidden layers and A's layers,
-  // with the logit layer's reduction, SGD and loss in the same reduction
-  MultiDW m;
-  m.R = R;
-  m.scale = c->o.lr / (float)R;
-  m.ta = ta;
-  const Top& T = p.T;
-  const void* zA = c->ws + p.A.act[0][p.A.L - 1];
-  const void* zB = c->ws + p.P.zhat[slot];
-  for (int j = 0; j < T.H; ++j)
-    add_dw(m, c->ws + T.dlt[j], T.out[j], j == 0 ? zA : c->ws + T.act[j - 1],
-           j == 0 ? ld_of(p.dA) : ld_of(T.out[j - 1]), j == 0 ? zB : nullptr,
-           j == 0 ? ld_of(p.dB) : 0, j == 0 ? p.dA : 1 << 30, T.in[j], at<float>(c, T.W[j]),
-           at<float>(c, T.b[j]), c->ws + T.Wq[j], T.ldq[j], c->ws + T.Wtq[j], T.ldt[j],
-           T.part[j] ? at<float>(c, T.part[j]) : nullptr, T.partb[j] ? at<float>(c, T.partb[j]) : nullptr,
-           p.splits_a, p.rps_a);
-  add_party_dw(c, m, p.A, 0, st, p.splits_a, p.rps_a, ta != nullptr);
-  LogitJob lj = logit_job(c, R, labels, loss_dev, ta);
-  if ((r = enqueue_weight_update(c, m, &lj, c->sa))) return r;
-  return enqueue_table_sgd(c, p.A, st, c->o.lr / (float)R, c->sa, ta);
+  return enqueue_table_sgd(c, p.A, st.ids, st.rows, c->o.lr / (float)st.rows, c->sa, ta);
 }
 
 // B's delayed backward of the group stashed in `slot` + SGD on B's current
@@ -769,28 +991,12 @@ vfl_status a_backward(vfl_ctx* c, int slot, const SlotState& st, const float* la
 vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, const TickArgs* ta) {
   const Plan& p = c->p;
   HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
-  CutBwdJob cj{};
-  cj.g = c->ws + p.ring_g[slot]; cj.ldg = ld_of(p.dB);
-  cj.z = c->ws + p.P.act[slot][p.P.L - 1]; cj.ldz = ld_of(p.dB);
-  cj.clip = (c->o.flags & VFL_CLIP_EMB) != 0;
-  cj.norm = cj.clip ? at<float>(c, p.P.norm[slot]) : nullptr;
-  cj.cfac = cj.clip ? at<float>(c, p.P.cfac[slot]) : nullptr;
-  cj.C = c->o.clip_c; cj.relu = p.P.relu[p.P.L - 1];
-  cj.delta = c->ws + p.P.dlt[p.P.L - 1]; cj.ldd = ld_of(p.dB);
-  cj.R = st.rows; cj.D = p.dB;
-  cj.hdr_chk = hdr_ptr(c, 1, slot); cj.chk_seq = (int32_t)group; cj.err = err_ptr(c);
-  cj.ta = ta;
-  TIMED(VFL_K_CUT_BWD, (double)st.rows * p.dB * 3.0 * elt_size(p.e) + (cj.clip ? 8.0 * st.rows : 0.0),
-        c->sb, launch_cut_backward(p.e, cj, c->sb));
-  vfl_status r = enqueue_dx_chain(c, p.P, slot, st.rows, c->sb, ta);
+  const ChainCall k = call_of(st, group, nullptr, group);
+  TIMED(VFL_K_BWD, party_dx_flops(p.P, p.R), c->sb,
+        launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, ta, c->sb));
+  vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, ta, c->sb);
   if (r) return r;
-  MultiDW m;
-  m.R = st.rows;
-  m.scale = c->o.lr / (float)st.rows;
-  m.ta = ta;
-  add_party_dw(c, m, p.P, slot, st, p.splits_b, p.rps_b, ta != nullptr);
-  if ((r = enqueue_weight_update(c, m, nullptr, c->sb))) return r;
-  return enqueue_table_sgd(c, p.P, st, c->o.lr / (float)st.rows, c->sb, ta);
+  return enqueue_table_sgd(c, p.P, st.ids, st.rows, c->o.lr / (float)st.rows, c->sb, ta);
 }
 
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
@@ -819,27 +1025,40 @@ vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& o
   return fail(c, VFL_E_INVALID, "bad party");
 }
 
-// Replica batches of group g of the bound dataset (consecutive chunks of at
-// most `batch` rows of the group's rows).
-int dataset_batches(vfl_ctx* c, int party, int64_t g, vfl_batch* out) {
+// The slot description of group g of the bound dataset for one party.
+SlotState dataset_slot(vfl_ctx* c, int party, int64_t g) {
   const Plan& p = c->p;
   const int64_t E = (c->n_rows + p.R - 1) / p.R;
   const int64_t start = (g % E) * p.R;
-  const int64_t rows = std::min<int64_t>(p.R, c->n_rows - start);
   const vfl_dataset& d = party == 0 ? c->ds_a : c->ds_b;
   const Party& P = party == 0 ? p.A : p.P;
   const int es = elt_size(p.e);
-  const int64_t ld = d.ld ? d.ld : P.spec.dense_in;
+  SlotState st;
+  st.rows = (int)std::min<int64_t>(p.R, c->n_rows - start);
+  st.row0 = start;
+  st.ld = d.ld ? d.ld : P.spec.dense_in;
+  st.dense = d.dense ? (const char*)d.dense + start * st.ld * es : nullptr;
+  st.ids = d.ids ? d.ids + start * P.spec.n_cat : nullptr;
+  st.labels = d.labels ? d.labels + start : nullptr;
+  st.group = g;
+  return st;
+}
+
+// the same group as replica batches (what a caller of vfl_step would pass)
+int dataset_batches(vfl_ctx* c, int party, int64_t g, vfl_batch* out) {
+  const Plan& p = c->p;
+  const SlotState st = dataset_slot(c, party, g);
+  const int es = elt_size(p.e);
+  const Party& P = party == 0 ? p.A : p.P;
   int n = 0;
-  for (int64_t o = 0; o < rows; o += p.B, ++n) {
+  for (int64_t o = 0; o < st.rows; o += p.B, ++n) {
     vfl_batch& b = out[n];
     b = vfl_batch{};
-    const int64_t r0 = start + o;
-    if (d.dense) { b.dense = (const char*)d.dense + r0 * ld * es; b.ld = ld; }
-    if (d.ids) b.ids = d.ids + r0 * P.spec.n_cat;
-    if (d.labels) b.labels = d.labels + r0;
-    b.rows = (int32_t)std::min<int64_t>(p.B, rows - o);
-    b.row0 = r0;
+    if (st.dense) { b.dense = (const char*)st.dense + o * st.ld * es; b.ld = st.ld; }
+    if (st.ids) b.ids = st.ids + o * P.spec.n_cat;
+    if (st.labels) b.labels = st.labels + o;
+    b.rows = (int32_t)std::min<int64_t>(p.B, st.rows - o);
+    b.row0 = st.row0 + o;
   }
   return n;
 }
@@ -853,6 +1072,9 @@ vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b
   if (!bytes) return VFL_E_INVALID;
   Plan p;
   if (!build_plan(a, b, top, o, p).empty()) return VFL_E_INVALID;
+  // the kernels' layouts are checked here already (against a nominal base)
+  Jobs J;
+  if (!build_jobs(p, *o, (char*)(uintptr_t)4096, J).empty()) return VFL_E_INVALID;
   *bytes = p.total;
   return VFL_OK;
 }
@@ -875,7 +1097,7 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
     c->grad_group[q] = -1;
     c->b_copy_version[q] = -1;
   }
-  hipError_t e = hipSuccess;
+  hipError_t e = chain_init();
   for (int q = 0; q <= c->p.s && e == hipSuccess; ++q) {
     e = hipEventCreateWithFlags(&c->ev_emb[q], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_grad[q], hipEventDisableTiming);
@@ -888,6 +1110,11 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
   if (e != hipSuccess) {
     vfl_destroy(c);
     return VFL_E_HIP;
+  }
+  const vfl_status js = write_jobs(c);
+  if (js != VFL_OK) {
+    vfl_destroy(c);
+    return js;
   }
   *out = c;
   return VFL_OK;
@@ -950,19 +1177,14 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
     return VFL_OK;
   }
   if (party == VFL_PARTY_A) {
+    // A's forward runs fused with its top step; this call takes the batch
     if (group != c->a_next || c->a_phase != 0)
       return fail(c, VFL_E_STATE, "A's forward must take the next group A consumes");
     SlotState st;
     vfl_status r = take_batches(c, p.A, br, n, true, st);
     if (r) return r;
     st.group = group;
-    if (c->a_copy_version != c->a_version) {
-      if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
-      c->a_copy_version = c->a_version;
-    }
-    if ((r = a_forward(c, st, nullptr))) return r;
     c->aslot = st;
-    c->a_labels = br[0].labels;
     c->a_phase = 1;
     return VFL_OK;
   }
@@ -975,7 +1197,7 @@ vfl_status vfl_publish(vfl_ctx* c, int64_t group) {
   const int slot = (int)(group % (p.s + 1));
   if (group != c->b_pub_next || c->b_next_fwd != group + 1 || c->bslot[slot].group != group)
     return fail(c, VFL_E_STATE, "publish must follow B's forward of the same group");
-  vfl_status r = b_publish(c, slot, c->bslot[slot], nullptr);
+  vfl_status r = b_publish(c, slot);
   if (r) return r;
   c->bslot[slot].published = true;
   c->b_pub_next = group + 1;
@@ -992,8 +1214,12 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
   if (bs.group != group || !bs.published)
     return fail(c, VFL_E_NOT_READY, "embedding of this group not published");
   if (bs.rows != c->aslot.rows) return fail(c, VFL_E_INVALID, "A and B batches differ in rows");
-  vfl_status r = a_top(c, group, slot, c->aslot.rows, c->a_labels, (int32_t)bs.version, loss_dev, nullptr);
-  if (r) return r;
+  vfl_status r;
+  if (c->a_copy_version != c->a_version) {
+    if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+    c->a_copy_version = c->a_version;
+  }
+  if ((r = a_top(c, group, slot, c->aslot, (int32_t)bs.version, nullptr))) return r;
   c->grad_group[slot] = group;
   c->grad_rows[slot] = c->aslot.rows;
   c->a_loss = loss_dev;
@@ -1007,7 +1233,7 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
   if (party == VFL_PARTY_A) {
     if (group != c->a_next || c->a_phase != 2)
       return fail(c, VFL_E_STATE, "A's backward must follow its top step");
-    vfl_status r = a_backward(c, (int)(group % (p.s + 1)), c->aslot, c->a_labels, c->a_loss, nullptr);
+    vfl_status r = a_backward(c, c->aslot, c->a_loss, nullptr);
     if (r) return r;
     c->a_version += 1;
     c->a_copy_version = c->a_version;
@@ -1135,8 +1361,10 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
         aj->n_rows = c->n_rows; aj->R = p.R; aj->s = s; aj->lr = c->o.lr;
         aj->loss_len = loss_ring ? loss_len : 1;
       }
+      // dataset bases: the tick records supply rows, row0 and the headers
       SlotState sa_in, sb_in;
       sa_in.rows = p.R; sa_in.dense = c->ds_a.dense; sa_in.ld = c->ds_a.ld; sa_in.ids = c->ds_a.ids;
+      sa_in.labels = c->ds_a.labels;
       sb_in.rows = p.R; sb_in.dense = c->ds_b.dense; sb_in.ld = c->ds_b.ld; sb_in.ids = c->ds_b.ids;
       c->tm_err = hipSuccess;
       HIPCHK(hipStreamBeginCapture(c->sa, hipStreamCaptureModeThreadLocal));
@@ -1151,13 +1379,12 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
         if (he == hipSuccess) he = launch_advance(adv_a, c->sa);
         if (he != hipSuccess) break;
         if ((r = b_forward(c, fs, sb_in, ta_bf))) break;
-        if ((r = b_publish(c, fs, sb_in, ta_bf))) break;
-        if ((r = a_forward(c, sa_in, ta_a))) break;
+        if ((r = b_publish(c, fs))) break;
         // the first s ticks consume groups published before this graph;
         // replays of a graph on one stream never overlap, so the publish
         // of those groups is already complete
-        if ((r = a_top(c, 0, us, p.R, c->ds_a.labels, 0, loss_ring, ta_a, i >= s))) break;
-        if ((r = a_backward(c, us, sa_in, c->ds_a.labels, loss_ring, ta_a))) break;
+        if ((r = a_top(c, 0, us, sa_in, 0, ta_a, i >= s))) break;
+        if ((r = a_backward(c, sa_in, loss_ring, ta_a))) break;
         if ((r = b_backward(c, us, sb_in, 0, ta_bb))) break;
       }
       if (he == hipSuccess && r == VFL_OK) he = hipEventRecord(c->ev_join, c->sb);
@@ -1200,19 +1427,9 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
       const int64_t u = t - s;
       const int fs = (int)(t % S1), us = (int)(u % S1);
       int64_t row[7] = {t, t, fs, c->b_version, u, us, -1};
-      SlotState st;
-      vfl_batch bb[VFL_MAX_REPLICAS];
-      const int nb = dataset_batches(c, 1, t, bb);
-      st.rows = 0;
-      st.rmap = RowMap();
-      st.rmap.n = nb;
-      for (int i = 0; i < nb; ++i) {
-        st.rmap.start[i] = st.rows;
-        st.rmap.row0[i] = bb[i].row0;
-        st.rows += bb[i].rows;
-      }
-      st.dense = bb[0].dense; st.ld = bb[0].ld; st.ids = bb[0].ids;
-      st.group = t; st.version = c->b_version; st.published = true;
+      SlotState st = dataset_slot(c, 1, t);
+      st.version = c->b_version;
+      st.published = true;
       c->bslot[fs] = st;
       c->grad_group[us] = u;
       c->grad_rows[us] = c->bslot[us].rows;

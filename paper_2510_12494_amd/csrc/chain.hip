@@ -1,0 +1,748 @@
+// Fused row-block kernels of the split-learning step on gfx950 (k_fwd,
+// k_active, k_bwd; see kernels.h for what each computes).
+//
+// A workgroup of 256 threads (4 wavefronts) owns BR = 16 * RT consecutive
+// rows of the group and runs every layer of its chain on them, the
+// activations and deltas staying in LDS.  Each layer is one MFMA product
+// out[BR x N] = in[BR x K] W^T: wavefront w takes the 16-column output tiles
+// w, w+4, w+8, ... (four at a time), loads the weight fragments of its tiles
+// straight from global memory (L2-resident: every block reads each weight
+// once) four MFMA steps ahead, and the activation fragments from LDS;
+// v_mfma_f32_16x16x32_bf16 for bf16 operands, v_mfma_f32_16x16x4_f32 for
+// float32, float32 accumulation.  The weight fragment is the MFMA's A
+// operand, so a lane ends up with four consecutive output columns of one row.
+//
+// LDS rows are padded to 16 bytes past a multiple of 128, so the 16 rows a
+// fragment read touches fall in distinct banks.  After a layer, the tensors a
+// later kernel needs go to HBM: row-major for messages, the RC layout for
+// the operands of the weight gradients (8 x 8 register transposes of bf16
+// chunks, 4 x 4 of float32).
+//
+// Paper correspondence: bottom models f_A, f_B and the top model g of
+// Section 3, the BCE loss of Eq. (1) and its gradient, the embedding and
+// gradient messages of Section 4.1 with the per-row clip and Gaussian noise
+// of the differential-privacy appendix, and the cut-layer backward through
+// the clip of B's published embedding.
+#include "device.h"
+#include "kernels.h"
+
+namespace vfl {
+namespace {
+using namespace dev;
+
+template <typename T>
+struct Ch {
+  static constexpr int CE = 16 / (int)sizeof(T);   // elements per chunk = rows per RC chunk
+  static constexpr int KS = 4 * CE;                // contraction depth of one MFMA step
+};
+
+// values of this launch, from the call or the tick record
+struct Call {
+  int rows, group, chk;
+  int64_t row0;      // sample id of the group's row 0 (noise counter)
+  int64_t in_off;    // dataset row offset of the inputs
+  int32_t hdr[3];
+};
+
+__device__ __forceinline__ Call resolve(const ChainCall& c, const TickArgs* ta) {
+  Call k;
+  if (ta) {
+    k.rows = ta->rows; k.group = ta->group; k.chk = ta->chk;
+    k.row0 = ta->row0; k.in_off = ta->row0;
+    k.hdr[0] = ta->hdr[0]; k.hdr[1] = ta->hdr[1]; k.hdr[2] = ta->hdr[2];
+  } else {
+    k.rows = c.rows; k.group = c.group; k.chk = c.chk;
+    k.row0 = c.row0; k.in_off = 0;
+    k.hdr[0] = c.hdr[0]; k.hdr[1] = c.hdr[1]; k.hdr[2] = c.hdr[2];
+  }
+  return k;
+}
+
+__device__ __forceinline__ char* lp(char* s, const LBuf& b, int r, int byte_col) {
+  return s + b.off + r * b.pitch + byte_col;
+}
+
+// ------------------------------------------------------------ block product
+// epi(r, n, acc, bias): block row r, output columns n .. n+3 (n a multiple
+// of 4; bias[i] = bias[n + i], zero without a bias or beyond N), called for
+// every row of the block and every column below N rounded up to the MFMA
+// depth.  The weight fragments of PF consecutive MFMA steps are loaded as
+// one group while the previous group is multiplied, so a layer exposes the
+// load latency about once per PF steps.  Loads are unconditional and
+// fragments are used as loaded: a condition or a mask around a load makes
+// the compiler wait for it on the spot.
+template <typename T, int RT, typename Epi>
+__device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Epi&& epi) {
+  constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS, NTW = 4, PF = 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kc = lane >> 4, lr = lane & 15;
+  const int N = L.N, K = L.K;
+  const int ntl = (N + KS - 1) / KS * (KS / 16);
+  const int nks = (K + KS - 1) / KS;
+  const VFL_GLOBAL T* W = glb((const T*)L.W);
+  const VFL_GLOBAL float* bias = L.bias ? glb(L.bias) : nullptr;
+  const int64_t ldw = L.ldw;
+  const LBuf in = L.in;
+#pragma unroll 1
+  for (int pass = 0; wave + 4 * NTW * pass < ntl; ++pass) {
+    int tile[NTW];
+    bool on[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      tile[j] = wave + 4 * (NTW * pass + j);
+      on[j] = tile[j] < ntl;
+    }
+    f32x4 bv[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      const int n = tile[j] * 16 + 4 * kc;
+      bv[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (bias && on[j]) {
+        if (n + 4 <= N) {
+          bv[j] = *(const VFL_GLOBAL f32x4*)(bias + n);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (n + i < N) bv[j][i] = bias[n + i];
+        }
+      }
+    }
+    f32x4 acc[NTW][RT];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int t = 0; t < RT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // branch-free loads from clamped addresses: a lane past N only feeds
+    // output columns the epilogue zeroes, a lane past K multiplies the zero
+    // LDS padding, and steps past the last are never multiplied
+    const VFL_GLOBAL T* wrow[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) wrow[j] = W + (int64_t)min(tile[j] * 16 + lr, N - 1) * ldw;
+    u32x4 wa[PF][NTW], wb[PF][NTW];
+    auto wload = [&](int g, u32x4 (&d)[PF][NTW]) {
+#pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        const int k = (g * PF + q) * KS + kc * CE;
+        const int kk = k < K ? k : 0;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) d[q][j] = *(const VFL_GLOBAL u32x4*)(wrow[j] + kk);
+      }
+    };
+    // one MFMA step: the weight fragments of step ks (held in w) against
+    // the LDS activation fragments of the step
+    auto step = [&](int ks, const u32x4 (&w)[NTW]) {
+      u32x4 xf[RT];
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+        xf[t] = *(const u32x4*)(s + in.off + (t * 16 + lr) * in.pitch + (ks * 4 + kc) * 16);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+          if constexpr (sizeof(T) == 2) {
+            acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, w[j]), __builtin_bit_cast(bf16x8, xf[t]), acc[j][t], 0, 0, 0);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  __uint_as_float(w[j][e]), __uint_as_float(xf[t][e]), acc[j][t], 0, 0, 0);
+          }
+        }
+      }
+    };
+    // full groups pipelined with an unconditional prefetch of the next
+    // group (the remainder group after the last full one), then the
+    // remainder steps; off tiles are multiplied too and never stored
+    // (two groups per iteration, ping-ponging between wa and wb, so that no
+    // register copy waits for a prefetch)
+    const int nfull = nks / PF, rem = nks % PF;
+    auto group = [&](int g, const u32x4 (&w)[PF][NTW]) {
+#pragma unroll
+      for (int q = 0; q < PF; ++q) step(g * PF + q, w[q]);
+    };
+    auto tail = [&](const u32x4 (&w)[PF][NTW]) {
+#pragma unroll
+      for (int q = 0; q < PF - 1; ++q)
+        if (q < rem) step(nfull * PF + q, w[q]);
+    };
+    wload(0, wa);
+    int g = 0;
+#pragma unroll 1
+    for (; g + 2 <= nfull; g += 2) {
+      wload(g + 1, wb);
+      group(g, wa);
+      wload(g + 2, wa);
+      group(g + 1, wb);
+    }
+    if (g < nfull) {
+      wload(g + 1, wb);
+      group(g, wa);
+      tail(wb);
+    } else {
+      tail(wa);
+    }
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      if (!on[j]) continue;
+#pragma unroll
+      for (int t = 0; t < RT; ++t) epi(t * 16 + lr, tile[j] * 16 + 4 * kc, acc[j][t], bv[j]);
+    }
+  }
+}
+
+// Forward or input-gradient layer into LDS (see ChainLayer).
+template <typename T, int RT>
+__device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv) {
+  const int N = L.N;
+  const bool relu = L.relu != 0, msk = L.mask.pitch > 0;
+  const LBuf out = L.out, mk = L.mask;
+  block_mm<T, RT>(s, L, [&](int r, int n, const f32x4& a, const f32x4& b) {
+    float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
+    if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float x = a[i] + b[i];
+      if (relu) x = fmaxf(x, 0.f);
+      if (!(m[i] > 0.f)) x = 0.f;
+      if (n + i >= N || r >= rv) x = 0.f;
+      v[i] = x;
+    }
+    st4<T>(lp(s, out, r, n * (int)sizeof(T)), v);
+  });
+}
+
+// Input gradient of the embedding columns of a bottom input: float32 rows
+// of gx (block rows below rv).
+template <typename T, int RT>
+__device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float* gx, int64_t ldgx,
+                                       int r0, int rv) {
+  const int N = L.N;
+  VFL_GLOBAL float* gxg = glb(gx);
+  block_mm<T, RT>(s, L, [&](int r, int n, const f32x4& a, const f32x4&) {
+    if (r >= rv) return;
+    VFL_GLOBAL float* dst = gxg + (int64_t)(r0 + r) * ldgx + n;
+    if (n + 4 <= N) {
+      *(VFL_GLOBAL f32x4*)dst = a;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (n + i < N) dst[i] = a[i];
+    }
+  });
+}
+
+// ------------------------------------------------------------ data movement
+// LDS rows -> RC global matrix (block rows at tick rows r0 ..)
+template <typename T, int BR>
+__device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+  constexpr int RR = Ch<T>::CE;
+  const int ncc = (cols + RR - 1) / RR;
+  const int units = (BR / RR) * ncc;
+  VFL_GLOBAL char* g = glb((char*)m.p);
+  const int64_t cp = m.cp;
+  for (int u = threadIdx.x; u < units; u += 256) {
+    const int rg = u / ncc, cc = u % ncc;
+    u32x4 in[RR], out[RR];
+#pragma unroll
+    for (int i = 0; i < RR; ++i) in[i] = *(const u32x4*)(s + b.off + (rg * RR + i) * b.pitch + cc * 16);
+    if constexpr (RR == 8) transpose8x8_u16(in, out);
+    else transpose4x4_u32(in, out);
+    const int64_t base = ((int64_t)(r0 / RR + rg) * cp + (int64_t)cc * RR) * 16;
+#pragma unroll
+    for (int j = 0; j < RR; ++j) *(VFL_GLOBAL u32x4*)(g + base + j * 16) = out[j];
+  }
+}
+
+// zero rows r0 .. r0+BR-1 of an RC global matrix (columns below cols)
+template <typename T, int BR>
+__device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
+  constexpr int RR = Ch<T>::CE;
+  if (!m.p) return;
+  const int ncc = (cols + RR - 1) / RR;
+  VFL_GLOBAL char* g = glb((char*)m.p);
+  for (int u = threadIdx.x; u < (BR / RR) * ncc * RR; u += 256) {
+    const int rg = u / (ncc * RR), c = u % (ncc * RR);
+    *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * m.cp + c) * 16) = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// RC global matrix -> LDS rows (columns below cols; zeros up to the MFMA
+// depth)
+template <typename T, int BR>
+__device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+  constexpr int RR = Ch<T>::CE, KS = Ch<T>::KS;
+  const int ncc = (cols + KS - 1) / KS * 4;   // chunks up to the MFMA depth
+  const int units = (BR / RR) * ncc;
+  const VFL_GLOBAL char* g = glb((const char*)m.p);
+  const int64_t cp = m.cp;
+  for (int u = threadIdx.x; u < units; u += 256) {
+    const int rg = u / ncc, cc = u % ncc;
+    u32x4 in[RR], out[RR];
+    if (cc * RR < cols) {
+      const int64_t base = ((int64_t)(r0 / RR + rg) * cp + (int64_t)cc * RR) * 16;
+#pragma unroll
+      for (int j = 0; j < RR; ++j) out[j] = *(const VFL_GLOBAL u32x4*)(g + base + j * 16);
+      if constexpr (RR == 8) transpose8x8_u16(out, in);
+      else transpose4x4_u32(out, in);
+    } else {
+#pragma unroll
+      for (int i = 0; i < RR; ++i) in[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < RR; ++i) *(u32x4*)(s + b.off + (rg * RR + i) * b.pitch + cc * 16) = in[i];
+  }
+}
+
+// LDS rows -> row-major global rows (16-byte chunks; rows below rv)
+template <typename T, int BR>
+__device__ __forceinline__ void lds_to_rows(const char* s, const LBuf& b, int cols, void* dst,
+                                            int64_t ld, int r0, int rv) {
+  constexpr int CE = Ch<T>::CE;
+  const int nch = (cols + CE - 1) / CE;
+  VFL_GLOBAL char* d = glb((char*)dst);
+  for (int u = threadIdx.x; u < rv * nch; u += 256) {
+    const int r = u / nch, ch = u % nch;
+    *(VFL_GLOBAL u32x4*)(d + ((int64_t)(r0 + r) * ld + ch * CE) * sizeof(T)) =
+        *(const u32x4*)(s + b.off + r * b.pitch + ch * 16);
+  }
+}
+
+// Bottom input [embeddings | dense] of the block into LDS (zeros beyond the
+// input width up to the MFMA depth and for rows below the group).
+template <typename T, int BR>
+__device__ __forceinline__ void load_input(char* s, const RowInput& in, const ChainCall& cc,
+                                           const Call& k, int r0, int rv) {
+  constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS;
+  const int ne = in.n_cat * in.E;
+  const int din = ne + in.dense_in;
+  const int nch = (din + KS - 1) / KS * 4;
+  const VFL_GLOBAL T* dense = glb((const T*)cc.dense);
+  const VFL_GLOBAL int32_t* ids = glb(cc.ids);
+  const VFL_GLOBAL float* tab = glb(in.T);
+  for (int u = threadIdx.x; u < BR * nch; u += 256) {
+    const int r = u / nch, ch = u % nch, c0 = ch * CE;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (r < rv && c0 < din) {
+      const int64_t row = k.in_off + r0 + r;
+      if (c0 >= ne && in.dense_vec && (ne % CE) == 0) {
+        v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (c0 - ne)), din - c0);
+      } else if (c0 + CE <= ne && (in.E % CE) == 0) {
+        const int f = c0 / in.E, o = c0 % in.E;
+        const VFL_GLOBAL float* src = tab + ((int64_t)f * in.V + ids[row * in.n_cat + f]) * in.E + o;
+        float x[CE];
+#pragma unroll
+        for (int q = 0; q < CE / 4; ++q) {
+          const f32x4 t = *(const VFL_GLOBAL f32x4*)(src + 4 * q);
+          x[4 * q] = t[0]; x[4 * q + 1] = t[1]; x[4 * q + 2] = t[2]; x[4 * q + 3] = t[3];
+        }
+        if constexpr (sizeof(T) == 4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = __float_as_uint(x[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = (uint32_t)f2bf(x[2 * e]) | ((uint32_t)f2bf(x[2 * e + 1]) << 16);
+        }
+      } else {
+        float x[CE];
+#pragma unroll
+        for (int e = 0; e < CE; ++e) {
+          const int c = c0 + e;
+          float val = 0.f;
+          if (c < ne) {
+            const int f = c / in.E;
+            val = tab[((int64_t)f * in.V + ids[row * in.n_cat + f]) * in.E + (c % in.E)];
+          } else if (c < din) {
+            val = ld1<T>((const T*)(dense + row * cc.ld + (c - ne)));
+          }
+          x[e] = val;
+        }
+        if constexpr (sizeof(T) == 4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = __float_as_uint(x[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = (uint32_t)f2bf(x[2 * e]) | ((uint32_t)f2bf(x[2 * e + 1]) << 16);
+        }
+      }
+    }
+    *(u32x4*)(s + in.buf.off + r * in.buf.pitch + ch * 16) = v;
+  }
+}
+
+// Per-row clip + noise of an LDS message of D columns (element V) into
+// row-major element-T rows; norm/cfac (nullable) receive ||v|| and the clip
+// factor.  One wavefront per row; the noise is keyed by the row's sample id.
+template <typename T, typename V, int BR>
+__device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, const MsgOp& m,
+                                         uint32_t step, int64_t sample0, void* out, int64_t ldo,
+                                         float* norm, float* cfac, int r0, int rv) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ngrp = (D + 3) >> 2;
+  for (int r = wave; r < rv; r += 4) {
+    const char* row = s + src.off + r * src.pitch;
+    float ss = 0.f;
+    for (int g = lane; g < ngrp; g += 64) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * g + e;
+        if (c < D) { const float x = ld1<V>((const V*)row + c); ss += x * x; }
+      }
+    }
+    const float n = sqrtf(wave_sum(ss));
+    const float cf = (m.clip && n > m.C) ? m.C / n : 1.f;
+    if (lane == 0) {
+      if (norm) glb(norm)[r0 + r] = n;
+      if (cfac) glb(cfac)[r0 + r] = cf;
+    }
+    VFL_GLOBAL T* o = glb((T*)out) + (int64_t)(r0 + r) * ldo;
+    const uint32_t grow = (uint32_t)(sample0 + r0 + r);
+    for (int g = lane; g < ngrp; g += 64) {
+      float xi[4] = {0.f, 0.f, 0.f, 0.f};
+      if (m.noise) gauss4(m.seed, step, grow, (uint32_t)g, m.tag, xi);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * g + e;
+        if (c < D) st1<T>((T*)(o + c), cf * ld1<V>((const V*)row + c) + m.stdv * xi[e]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ kernels
+template <typename T, int RT>
+__global__ __launch_bounds__(256) void k_fwd(const FwdJob* __restrict__ jp, ChainCall cc,
+                                             const TickArgs* ta) {
+  constexpr int BR = 16 * RT;
+  extern __shared__ __attribute__((aligned(16))) char s[];
+  const FwdJob& j = *jp;
+  const Call k = resolve(cc, ta);
+  if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_out) {
+    VFL_GLOBAL int32_t* h = glb(j.hdr_out);
+    h[0] = k.hdr[0]; h[1] = k.hdr[1]; h[2] = k.hdr[2];
+  }
+  const int r0 = blockIdx.x * BR;
+  if (r0 >= k.rows) return;
+  const int rv = min(BR, k.rows - r0);
+  load_input<T, BR>(s, j.in, cc, k, r0, rv);
+  __syncthreads();
+  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
+  for (int l = 0; l < j.L; ++l) {
+    run_layer<T, RT>(s, j.l[l], rv);
+    __syncthreads();
+    if (j.l[l].rc.p) lds_to_rc<T, BR>(s, j.l[l].out, j.l[l].N, j.l[l].rc, r0);
+  }
+  const ChainLayer& last = j.l[j.L - 1];
+  lds_to_rows<T, BR>(s, last.out, last.N, j.z, j.ldz, r0, rv);
+  if (j.publish)
+    msg_rows<T, T, BR>(s, last.out, last.N, j.m, (uint32_t)k.group, k.row0, j.zhat, j.ldzh, j.norm,
+                       j.cfac, r0, rv);
+}
+
+template <typename T, int RT>
+__global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp, ChainCall cc,
+                                                const TickArgs* ta) {
+  constexpr int BR = 16 * RT;
+  constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS;
+  extern __shared__ __attribute__((aligned(16))) char s[];
+  const ActiveJob& j = *jp;
+  const Call k = resolve(cc, ta);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (j.hdr_chk && glb(j.hdr_chk)[0] != k.chk) atomicAdd(j.err, 1);
+    if (j.hdr_out) {
+      VFL_GLOBAL int32_t* h = glb(j.hdr_out);
+      h[0] = k.hdr[0]; h[1] = k.hdr[1]; h[2] = k.hdr[2];
+    }
+  }
+  const int r0 = blockIdx.x * BR;
+  if (r0 >= k.rows) {
+    // rows past a short group: zero delta rows, so that the weight
+    // gradient may read whole row steps
+    zero_rc<T, BR>(j.dh_rc, j.ft[j.H - 1].N, r0);
+    for (int q = 0; q + 1 < j.H; ++q) zero_rc<T, BR>(j.dt[q].rc, j.dt[q].N, r0);
+    zero_rc<T, BR>(j.dc.rc, j.dA, r0);
+    for (int q = 0; q < j.nda; ++q) zero_rc<T, BR>(j.da[q].rc, j.da[q].N, r0);
+    return;
+  }
+  const int rv = min(BR, k.rows - r0);
+
+  // A's bottom forward; the last layer fills cat[:, 0:dA)
+  load_input<T, BR>(s, j.in, cc, k, r0, rv);
+  __syncthreads();
+  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
+  for (int l = 0; l < j.LA; ++l) {
+    run_layer<T, RT>(s, j.fa[l], rv);
+    __syncthreads();
+    if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
+  }
+  // B's embedding into cat[:, dA:dA+dB), zeros up to the MFMA depth
+  {
+    const int dA = j.dA, dB = j.dB;
+    const int nch = ((dA + dB + KS - 1) / KS * KS - dA) / CE;
+    const VFL_GLOBAL T* zb = glb((const T*)j.zb);
+    for (int u = threadIdx.x; u < BR * nch; u += 256) {
+      const int r = u / nch, ch = u % nch, c = ch * CE;
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (r < rv && c < dB) v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(zb + (int64_t)(r0 + r) * j.ldzb + c), dB - c);
+      *(u32x4*)(s + j.cat.off + r * j.cat.pitch + (dA + c) * (int)sizeof(T)) = v;
+    }
+  }
+  __syncthreads();
+  if (j.cat_rc.p) lds_to_rc<T, BR>(s, j.cat, j.dA + j.dB, j.cat_rc, r0);
+  // top hidden layers
+  for (int q = 0; q < j.H; ++q) {
+    run_layer<T, RT>(s, j.ft[q], rv);
+    __syncthreads();
+    if (j.ft[q].rc.p) lds_to_rc<T, BR>(s, j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0);
+  }
+  // logit + BCE (Eq. 1): one wavefront per row; dl = sigmoid(l) - y
+  {
+    const LBuf Hb = j.ft[j.H - 1].out, Db = j.dh;
+    const int Hd = j.ft[j.H - 1].N;
+    const int hq = (Hd + KS - 1) / KS * KS / 4;   // 4-column groups to write
+    const VFL_GLOBAL float* y = glb(cc.labels) + k.in_off + r0;
+    const VFL_GLOBAL float* lw = glb(j.lw);
+    float w[2][4], gw[2][4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * (lane + 64 * h) + e;
+        w[h][e] = c < Hd ? lw[c] : 0.f;
+        gw[h][e] = 0.f;
+      }
+    const float bias = glb(j.lb)[0];
+    float gb = 0.f, ls = 0.f;
+    for (int r = wave; r < BR; r += 4) {
+      float hv[2][4];
+      float dot = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int q = lane + 64 * h;
+        if (q < hq) ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv[h]);
+        else hv[h][0] = hv[h][1] = hv[h][2] = hv[h][3] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dot += hv[h][e] * w[h][e];
+      }
+      dot = wave_sum(dot);
+      const bool ok = r < rv;
+      const float l = dot + bias;
+      const float yy = ok ? y[r] : 0.f;
+      const float ex = expf(-fabsf(l));
+      const float loss = fmaxf(l, 0.f) - yy * l + log1pf(ex);
+      const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
+      const float dl = ok ? sig - yy : 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int q = lane + 64 * h;
+        if (q < hq) {
+          float d[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            d[e] = dl * w[h][e];
+            if (j.relu_h && !(hv[h][e] > 0.f)) d[e] = 0.f;
+            gw[h][e] += dl * hv[h][e];
+          }
+          st4<T>(lp(s, Db, r, 4 * q * (int)sizeof(T)), d);
+        }
+      }
+      if (ok) { gb += dl; ls += loss; }
+    }
+    float* red = (float*)(s + j.red.off);
+    const int W = Hd + 2;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * (lane + 64 * h) + e;
+        if (c < Hd) red[wave * W + 2 + c] = gw[h][e];
+      }
+    if (lane == 0) { red[wave * W] = ls; red[wave * W + 1] = gb; }
+    __syncthreads();
+    VFL_GLOBAL float* part = glb(j.part) + (int64_t)blockIdx.x * W;
+    for (int c = threadIdx.x; c < W; c += 256)
+      part[c] = ((red[c] + red[W + c]) + red[2 * W + c]) + red[3 * W + c];
+  }
+  if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[j.H - 1].N, j.dh_rc, r0);
+  // top input-gradient chain
+  for (int q = 0; q + 1 < j.H; ++q) {
+    run_layer<T, RT>(s, j.dt[q], rv);
+    __syncthreads();
+    if (j.dt[q].rc.p) lds_to_rc<T, BR>(s, j.dt[q].out, j.dt[q].N, j.dt[q].rc, r0);
+  }
+  // concat product: A's cut delta and the gradient message for B
+  {
+    const int dA = j.dA, dAB = j.dA + j.dB;
+    const int dApad = (dA + KS - 1) / KS * KS;
+    const LBuf ob = j.dc.out, cat = j.cat, msg = j.msg;
+    const bool maskA = j.dc.mask.pitch > 0, gextra = j.gextra != 0;
+    VFL_GLOBAL T* ring = glb((T*)j.ring);
+    const int64_t ldr = j.ldring;
+    block_mm<T, RT>(s, j.dc, [&](int r, int n, const f32x4& a, const f32x4&) {
+      const bool ok = r < rv;
+      if (n + 4 <= dA) {
+        float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
+        if (maskA) ld4<T>(lp(s, cat, r, n * (int)sizeof(T)), m);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = (ok && m[i] > 0.f) ? a[i] : 0.f;
+        st4<T>(lp(s, ob, r, n * (int)sizeof(T)), v);
+        return;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = n + i;
+        const float x = ok ? a[i] : 0.f;
+        if (c < dA) {
+          const bool keep = !maskA || ld1<T>((const T*)lp(s, cat, r, 0) + c) > 0.f;
+          st1<T>((T*)lp(s, ob, r, 0) + c, keep ? x : 0.f);
+        } else if (c < dApad) {
+          st1<T>((T*)lp(s, ob, r, 0) + c, 0.f);
+        }
+        if (c >= dA && c < dAB) {
+          if (gextra) ((float*)lp(s, msg, r, 0))[c - dA] = x;
+          else if (ok) st1<T>((T*)(ring + (int64_t)(r0 + r) * ldr + (c - dA)), x);
+        }
+      }
+    });
+    __syncthreads();
+    if (j.dc.rc.p) lds_to_rc<T, BR>(s, ob, dA, j.dc.rc, r0);
+    if (gextra)
+      msg_rows<T, float, BR>(s, msg, j.dB, j.m, (uint32_t)k.group, k.row0, j.ring, j.ldring, nullptr,
+                             nullptr, r0, rv);
+  }
+  // A's input-gradient chain
+  for (int q = 0; q < j.nda; ++q) {
+    run_layer<T, RT>(s, j.da[q], rv);
+    __syncthreads();
+    if (j.da[q].rc.p) lds_to_rc<T, BR>(s, j.da[q].out, j.da[q].N, j.da[q].rc, r0);
+  }
+  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv);
+}
+
+template <typename T, int RT>
+__global__ __launch_bounds__(256) void k_bwd(const BwdJob* __restrict__ jp, ChainCall cc,
+                                             const TickArgs* ta) {
+  constexpr int BR = 16 * RT;
+  constexpr int KS = Ch<T>::KS;
+  extern __shared__ __attribute__((aligned(16))) char s[];
+  const BwdJob& j = *jp;
+  const Call k = resolve(cc, ta);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_chk && glb(j.hdr_chk)[0] != k.chk) atomicAdd(j.err, 1);
+  const int r0 = blockIdx.x * BR;
+  if (r0 >= k.rows) {
+    zero_rc<T, BR>(j.d_rc, j.D, r0);
+    for (int q = 0; q < j.nd; ++q) zero_rc<T, BR>(j.dx[q].rc, j.dx[q].N, r0);
+    return;
+  }
+  const int rv = min(BR, k.rows - r0);
+  // cut-layer backward: through the clip when the row was clipped
+  // (d(c v)/dv = c (I - u u^T) with u = v / ||v||), then the ReLU of B's
+  // last layer
+  {
+    const int D = j.D;
+    const int hq = (D + KS - 1) / KS * KS / 4;
+    for (int r = wave; r < BR; r += 4) {
+      const bool ok = r < rv;
+      const int64_t row = r0 + r;
+      const VFL_GLOBAL T* G = glb((const T*)j.g) + row * j.ldg;
+      const VFL_GLOBAL T* Z = glb((const T*)j.z) + row * j.ldz;
+      const bool clipped = ok && j.clip && glb(j.norm)[row] > j.C;
+      float dot = 0.f, inv = 0.f, cf = 1.f;
+      if (clipped) {
+        inv = 1.f / glb(j.norm)[row];
+        cf = glb(j.cfac)[row];
+        for (int c = lane; c < D; c += 64) dot += ld1<T>((const T*)(Z + c)) * inv * ld1<T>((const T*)(G + c));
+        dot = wave_sum(dot);
+      }
+      for (int q = lane; q < hq; q += 64) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int c = 4 * q + e;
+          float g = 0.f;
+          if (ok && c < D) {
+            const float z = ld1<T>((const T*)(Z + c));
+            g = ld1<T>((const T*)(G + c));
+            if (clipped) g = cf * (g - z * inv * dot);
+            if (j.relu && !(z > 0.f)) g = 0.f;
+          }
+          v[e] = g;
+        }
+        st4<T>(lp(s, j.d, r, 4 * q * (int)sizeof(T)), v);
+      }
+    }
+  }
+  __syncthreads();
+  if (j.d_rc.p) lds_to_rc<T, BR>(s, j.d, j.D, j.d_rc, r0);
+  for (int q = 0; q < j.nd; ++q) {
+    const ChainLayer& L = j.dx[q];
+    if (L.mask_src.p) {
+      rc_to_lds<T, BR>(s, L.mask, L.N, L.mask_src, r0);
+      __syncthreads();
+    }
+    run_layer<T, RT>(s, L, rv);
+    __syncthreads();
+    if (L.rc.p) lds_to_rc<T, BR>(s, L.out, L.N, L.rc, r0);
+  }
+  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv);
+}
+
+template <typename K>
+hipError_t raise_lds(K kernel) {
+  return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax);
+}
+
+}  // namespace
+
+#define VFL_CHAIN_DISPATCH(KER, e, rt, ...)                                                   \
+  do {                                                                                       \
+    if (e == BF16) {                                                                         \
+      if (rt == 1) hipLaunchKernelGGL((KER<uint16_t, 1>), __VA_ARGS__);                       \
+      else if (rt == 2) hipLaunchKernelGGL((KER<uint16_t, 2>), __VA_ARGS__);                  \
+      else if (rt == 4) hipLaunchKernelGGL((KER<uint16_t, 4>), __VA_ARGS__);                  \
+      else return hipErrorInvalidValue;                                                      \
+    } else {                                                                                 \
+      if (rt == 1) hipLaunchKernelGGL((KER<float, 1>), __VA_ARGS__);                          \
+      else if (rt == 2) hipLaunchKernelGGL((KER<float, 2>), __VA_ARGS__);                     \
+      else if (rt == 4) hipLaunchKernelGGL((KER<float, 4>), __VA_ARGS__);                     \
+      else return hipErrorInvalidValue;                                                      \
+    }                                                                                        \
+  } while (0)
+
+hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
+                      const TickArgs* ta, hipStream_t st) {
+  if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
+  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  return hipGetLastError();
+}
+
+hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
+                         const ChainCall& c, const TickArgs* ta, hipStream_t st) {
+  if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
+  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
+                      const TickArgs* ta, hipStream_t st) {
+  if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
+  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  return hipGetLastError();
+}
+
+hipError_t chain_init() {
+  const hipError_t r[] = {
+      raise_lds(k_fwd<uint16_t, 1>), raise_lds(k_fwd<uint16_t, 2>), raise_lds(k_fwd<uint16_t, 4>),
+      raise_lds(k_fwd<float, 1>), raise_lds(k_fwd<float, 2>), raise_lds(k_fwd<float, 4>),
+      raise_lds(k_active<uint16_t, 1>), raise_lds(k_active<uint16_t, 2>), raise_lds(k_active<uint16_t, 4>),
+      raise_lds(k_active<float, 1>), raise_lds(k_active<float, 2>), raise_lds(k_active<float, 4>),
+      raise_lds(k_bwd<uint16_t, 1>), raise_lds(k_bwd<uint16_t, 2>), raise_lds(k_bwd<uint16_t, 4>),
+      raise_lds(k_bwd<float, 1>), raise_lds(k_bwd<float, 2>), raise_lds(k_bwd<float, 4>)};
+  for (hipError_t x : r)
+    if (x != hipSuccess) return x;
+  return hipSuccess;
+}
+
+}  // namespace vfl

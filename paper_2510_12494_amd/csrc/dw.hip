@@ -1,0 +1,283 @@
+// Weight gradients and SGD of the split-learning step on gfx950 (k_dw,
+// k_dw_reduce; see kernels.h).
+//
+// G = D^T X contracts over the rows of the group.  Both operands are in the
+// row-chunked layout, so every MFMA fragment is one 16-byte load per lane
+// straight from global memory: lane group g (lane / 16) takes the chunk of
+// rows [8g, 8g + 8) of the step (4 rows for float32), lane % 16 the column.
+// The input X is the MFMA's A operand and the delta D its B operand, so a
+// lane accumulates four consecutive k of one output row n: partials and SGD
+// updates are 16-byte row segments.  A block owns a 64 x 64 output tile (2 x
+// 2 wavefronts of 32 x 32) and one chunk of rows, loads the fragments of
+// four MFMA steps as one group while multiplying the previous group, and
+// sums the bias gradient from the D fragments it already holds.
+//
+// Split chunks are summed by k_dw_reduce in chunk order, as are the logit
+// layer's per-block partials, so every result is deterministic.  SGD (Eq. 2)
+// updates the float32 master weights; the element-type operand copies the
+// next forward (W) and input-gradient (W^T) products read are rewritten from
+// the new weights in the same pass.
+#include "device.h"
+#include "kernels.h"
+
+namespace vfl {
+namespace {
+using namespace dev;
+
+template <typename T>
+__device__ __forceinline__ void sgd_store(const DwProb& P, int n, int k, float g, float scale) {
+  const int64_t idx = (int64_t)n * P.K + k;
+  VFL_GLOBAL float* W = glb(P.W);
+  const float w = W[idx] - scale * g;
+  W[idx] = w;
+  if (P.Wq) st1<T>((T*)(glb((T*)P.Wq) + (int64_t)n * P.ldq + k), w);
+  if (P.Wtq) st1<T>((T*)(glb((T*)P.Wtq) + (int64_t)k * P.ldt + n), w);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Rarg, float scale_arg,
+                                            const TickArgs* ta) {
+  constexpr int RR = 16 / (int)sizeof(T);   // rows per chunk
+  constexpr int KR = 4 * RR;                // rows per MFMA step
+  constexpr int PF = 4;                     // MFMA steps per load group
+  const DwJob& J = *jp;
+  int q = 0;
+#pragma unroll 1
+  while (q + 1 < J.n && (int)blockIdx.x >= J.p[q + 1].first_block) ++q;
+  const DwProb& P = J.p[q];
+  const int lb = blockIdx.x - P.first_block;
+  const int tiles_k = (P.K + 63) / 64;
+  const int tile = lb / P.splits, split = lb % P.splits;
+  const int n0 = (tile / tiles_k) * 64, k0 = (tile % tiles_k) * 64;
+  const int R = ta ? ta->rows : Rarg;
+  const float scale = ta ? ta->scale : scale_arg;
+  const int rb = split * P.rps;
+  const int re = min(R, rb + P.rps);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1, kc = lane >> 4, lr = lane & 15;
+  const VFL_GLOBAL char* Dp = glb((const char*)P.D.p);
+  const VFL_GLOBAL char* Xp = glb((const char*)P.X.p);
+  const int64_t dcp = P.D.cp, xcp = P.X.cp;
+  const int N = P.N, K = P.K;
+  int nd[2], kx[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    nd[i] = n0 + 32 * wm + 16 * i + lr;
+    kx[i] = k0 + 32 * wn + 16 * i + lr;
+  }
+  const bool do_bias = (tile % tiles_k) == 0 && wn == 0;
+
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float bsum[2] = {0.f, 0.f};
+
+  // group g: MFMA steps at rows rb + (g * PF + st) * KR.  Loads are
+  // unconditional: rps is a multiple of PF * KR, so a group never reaches
+  // into the next chunk, and the delta rows from the group's end up to the
+  // group's last step are zero (chain blocks zero them); columns are
+  // clamped, their outputs discarded.
+  const VFL_GLOBAL char* dcol[2];
+  const VFL_GLOBAL char* xcol[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    dcol[i] = Dp + (int64_t)min(nd[i], N - 1) * 16;
+    xcol[i] = Xp + (int64_t)min(kx[i], K - 1) * 16;
+  }
+  auto load = [&](int g, u32x4 (&df)[PF][2], u32x4 (&xf)[PF][2]) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) {
+      const int64_t rg = (rb + (g * PF + st) * KR) / RR + kc;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        df[st][i] = *(const VFL_GLOBAL u32x4*)(dcol[i] + rg * dcp * 16);
+        xf[st][i] = *(const VFL_GLOBAL u32x4*)(xcol[i] + rg * xcp * 16);
+      }
+    }
+  };
+  const int ngr = re > rb ? (re - rb + PF * KR - 1) / (PF * KR) : 0;
+  u32x4 dA[PF][2], xA[PF][2], dB[PF][2], xB[PF][2];
+  auto group = [&](const u32x4 (&df)[PF][2], const u32x4 (&xf)[PF][2]) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) {
+          if constexpr (sizeof(T) == 2) {
+            acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, xf[st][i]), __builtin_bit_cast(bf16x8, df[st][jn]), acc[i][jn], 0, 0, 0);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  __uint_as_float(xf[st][i][e]), __uint_as_float(df[st][jn][e]), acc[i][jn], 0, 0, 0);
+          }
+        }
+      }
+      if (do_bias) {
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (sizeof(T) == 2) {
+              bsum[jn] += __uint_as_float(df[st][jn][e] << 16) + __uint_as_float(df[st][jn][e] & 0xffff0000u);
+            } else {
+              bsum[jn] += __uint_as_float(df[st][jn][e]);
+            }
+          }
+        }
+      }
+    }
+  };
+  // two groups per iteration, ping-ponging between the A and B registers;
+  // every prefetch is unconditional (past the end it reloads the last group)
+  load(0, dA, xA);
+#pragma unroll 1
+  for (int g = 0; g < ngr; g += 2) {
+    load(min(g + 1, ngr - 1), dB, xB);
+    group(dA, xA);
+    if (g + 1 >= ngr) break;
+    load(min(g + 2, ngr - 1), dA, xA);
+    group(dB, xB);
+  }
+
+  // bias: sum the four lane groups of each column
+  if (do_bias) {
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) {
+      bsum[jn] += __shfl_xor(bsum[jn], 16, 64);
+      bsum[jn] += __shfl_xor(bsum[jn], 32, 64);
+    }
+    if (kc == 0) {
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn) {
+        const int n = nd[jn];
+        if (n >= N) continue;
+        if (P.splits == 1) glb(P.bias)[n] -= scale * bsum[jn];
+        else glb(P.partb)[(int64_t)split * N + n] = bsum[jn];
+      }
+    }
+  }
+  // weights: lane holds G[n][kb .. kb+3]
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) {
+      const int n = nd[jn];
+      const int kb = k0 + 32 * wn + 16 * i + 4 * kc;
+      if (n >= N || kb >= K) continue;
+      if (P.splits > 1) {
+        *(VFL_GLOBAL f32x4*)(glb(P.part) + ((int64_t)split * N + n) * P.kp + kb) = acc[i][jn];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (kb + e < K) sgd_store<T>(P, n, kb + e, acc[i][jn][e], scale);
+      }
+    }
+  }
+}
+
+// Blocks [0, red_blocks): one thread per 4 consecutive weights (or one
+// bias) of a split problem.  Blocks after: 4 logit columns each, the
+// partial rows split over 64 slices and summed slice by slice.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp, int Rarg,
+                                                   float scale_arg, float* loss_out,
+                                                   const TickArgs* ta, float* loss_base) {
+  const DwJob& J = *jp;
+  const int R = ta ? ta->rows : Rarg;
+  const float scale = ta ? ta->scale : scale_arg;
+  if ((int)blockIdx.x < J.red_blocks) {
+    int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    for (int q = 0; q < J.n; ++q) {
+      const DwProb& P = J.p[q];
+      if (P.splits <= 1) continue;
+      const int64_t qw = (int64_t)P.N * (P.kp / 4);
+      if (t >= qw + P.N) { t -= qw + P.N; continue; }
+      if (t < qw) {
+        const int n = (int)(t / (P.kp / 4)), kb = (int)(t % (P.kp / 4)) * 4;
+        const VFL_GLOBAL float* src = glb(P.part) + (int64_t)n * P.kp + kb;
+        const int64_t stride = (int64_t)P.N * P.kp;
+        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+        int s = 0;
+        for (; s + 8 <= P.splits; s += 8) {
+          f32x4 v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = *(const VFL_GLOBAL f32x4*)(src + (s + u) * stride);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) sum += v[u];
+        }
+        for (; s < P.splits; ++s) sum += *(const VFL_GLOBAL f32x4*)(src + s * stride);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (kb + e < P.K) sgd_store<T>(P, n, kb + e, sum[e], scale);
+      } else {
+        const int n = (int)(t - qw);
+        const VFL_GLOBAL float* pb = glb(P.partb);
+        float sum = 0.f;
+        for (int s = 0; s < P.splits; ++s) sum += pb[(int64_t)s * P.N + n];
+        glb(P.bias)[n] -= scale * sum;
+      }
+      return;
+    }
+    return;
+  }
+  // logit layer: column c of the block partials {loss, dl, dl * h}
+  __shared__ float red[64][5];
+  const int W = J.Hd + 2;
+  const int cl = threadIdx.x & 3, sl = threadIdx.x >> 2;
+  const int c = ((int)blockIdx.x - J.red_blocks) * 4 + cl;
+  const int rows = (R + J.lrows - 1) / J.lrows;
+  const VFL_GLOBAL float* lp = glb(J.lpart);
+  float acc = 0.f;
+  if (c < W) {
+    int b = sl;
+    for (; b + 3 * 64 < rows; b += 4 * 64) {
+      const float v0 = lp[(int64_t)b * W + c], v1 = lp[(int64_t)(b + 64) * W + c];
+      const float v2 = lp[(int64_t)(b + 128) * W + c], v3 = lp[(int64_t)(b + 192) * W + c];
+      acc += ((v0 + v1) + v2) + v3;
+    }
+    for (; b < rows; b += 64) acc += lp[(int64_t)b * W + c];
+  }
+  red[sl][cl] = acc;
+  __syncthreads();
+  if (sl == 0 && c < W) {
+    float tot = 0.f;
+    for (int i = 0; i < 64; ++i) tot += red[i][cl];
+    if (c == 0) {
+      float* lo = ta ? (loss_base ? loss_base + ta->loss_idx : nullptr) : loss_out;
+      if (lo) *glb(lo) = tot / (float)R;
+    } else if (c == 1) {
+      glb(J.lb)[0] -= scale * tot;
+    } else {
+      glb(J.lw)[c - 2] -= scale * tot;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, const TickArgs* ta,
+                     hipStream_t st) {
+  if (blocks < 1) return hipErrorInvalidValue;
+  if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, ta);
+  else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, ta);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
+                            float* loss_out, const TickArgs* ta, float* loss_base, hipStream_t st) {
+  if (blocks < 1) return hipErrorInvalidValue;
+  if (e == BF16)
+    hipLaunchKernelGGL(k_dw_reduce<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out,
+                       ta, loss_base);
+  else
+    hipLaunchKernelGGL(k_dw_reduce<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out, ta,
+                       loss_base);
+  return hipGetLastError();
+}
+
+}  // namespace vfl

@@ -1,6 +1,6 @@
-// Embedding tables of the categorical bottoms on gfx950: the gather that
-// builds a bottom model's input [tables of n_cat fields | dense], and the
-// sparse SGD step on the tables.
+// Sparse SGD step on the embedding tables of the categorical bottoms on
+// gfx950 (the gather of the looked-up rows is part of the chain kernels'
+// input stage).
 //
 // The sparse step sums, for every table row a batch touches, the gradient
 // rows of all samples that looked it up, and applies SGD once per touched
@@ -16,53 +16,6 @@
 
 namespace vfl {
 namespace {
-
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-template <typename T>
-__device__ __forceinline__ void st1(T* p, float v) {
-  if constexpr (sizeof(T) == 4) *p = v;
-  else *p = f2bf(v);
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void k_gather(GatherJob j) {
-  const int ne4 = j.E >> 2;                    // float4 chunks per field row
-  if (j.ta) {
-    j.R = j.ta->rows;
-    j.ids += j.ta->row0 * j.n_cat;
-    if (j.dense) j.dense = (const T*)j.dense + j.ta->row0 * j.ldx_in;
-  }
-  const int64_t n_emb = (int64_t)j.R * j.n_cat * ne4;
-  const int64_t total = n_emb + (int64_t)j.R * j.dense_in;
-  T* X = (T*)j.X;
-  const T* Dn = (const T*)j.dense;
-  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    if (i < n_emb) {
-      const int q = (int)(i % ne4);
-      const int64_t rf = i / ne4;
-      const int f = (int)(rf % j.n_cat);
-      const int r = (int)(rf / j.n_cat);
-      const int id = j.ids[(int64_t)r * j.n_cat + f];
-      const f32x4 v = *(const f32x4*)(j.T + ((int64_t)f * j.V + id) * j.E + 4 * q);
-      T* dst = X + (int64_t)r * j.ldx + f * j.E + 4 * q;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) st1<T>(dst + e, v[e]);
-    } else {
-      const int64_t k = i - n_emb;
-      const int c = (int)(k % j.dense_in);
-      const int r = (int)(k / j.dense_in);
-      X[(int64_t)r * j.ldx + j.n_cat * j.E + c] = Dn[(int64_t)r * j.ldx_in + c];
-    }
-  }
-}
 
 constexpr int kSortN = 8192;               // samples sorted per pass
 constexpr int kThreads = 512;
@@ -169,19 +122,7 @@ __global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
   }
 }
 
-int grid_for(int64_t work, int per_block, int cap) {
-  return (int)std::max<int64_t>(1, std::min<int64_t>((work + per_block - 1) / per_block, cap));
-}
-
 }  // namespace
-
-hipError_t launch_gather(Elt e, const GatherJob& j, hipStream_t st) {
-  const int64_t total = (int64_t)j.R * (j.n_cat * (j.E / 4) + j.dense_in);
-  const int blocks = grid_for(total, 256, 8192);
-  if (e == BF16) hipLaunchKernelGGL(k_gather<uint16_t>, dim3(blocks), dim3(256), 0, st, j);
-  else hipLaunchKernelGGL(k_gather<float>, dim3(blocks), dim3(256), 0, st, j);
-  return hipGetLastError();
-}
 
 hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st) {
   if (j.E > kMaxEmbDim || j.V > (1 << (32 - kRowBits))) return hipErrorInvalidValue;

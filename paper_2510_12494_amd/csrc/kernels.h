@@ -1,4 +1,30 @@
 // Internal launch interface of the gfx950 kernels (not part of the C ABI).
+//
+// One tick of the training step runs as a handful of fused kernels:
+//   k_fwd     party B: bottom forward of a row block through every layer,
+//             then the published embedding (clip + Philox noise);
+//   k_active  party A: bottom forward, concat with B's embedding, the top
+//             model, logit + BCE, and the whole input-gradient chain back
+//             through the top model and A's bottom, emitting the gradient
+//             message for B (clip + noise);
+//   k_bwd     party B: cut-layer backward of the message and the
+//             input-gradient chain through B's bottom;
+//   k_dw      every layer's weight gradient of one party (one launch),
+//             rows split into chunks; SGD fused when a layer is unsplit;
+//   k_dw_reduce  split chunks and the logit layer's block partials summed
+//             in a fixed order, SGD, weight operand copies refreshed.
+// The three chain kernels give each workgroup a block of BR = 16 * RT rows
+// and keep the block's activations and deltas in LDS from layer to layer:
+// only the tensors a later kernel reads go to HBM.  Those that the weight
+// gradient contracts over rows are written in the row-chunked layout below.
+//
+// Row-chunked ("RC") layout of a [rows x cols] matrix: element (r, c) lives
+// at ((r / RR) * cp + c) * RR + r % RR, RR = 16 bytes / element size (8 rows
+// of bf16, 4 of float32), cp = cols rounded up to 8.  Every 16-byte chunk
+// holds RR consecutive rows of one column, which is exactly an MFMA operand
+// fragment of a product that contracts over rows.  Rows of a block beyond
+// the group's row count are written as zeros, and so are the delta rows of
+// blocks past a short group's end.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -10,11 +36,15 @@ enum Elt { F32 = 0, BF16 = 1 };
 
 inline int elt_size(Elt e) { return e == F32 ? 4 : 2; }
 
+constexpr int kMaxChain = 8;          // layers per chain (bottom or top)
+constexpr int kMaxDw = 8;             // weight-gradient problems per launch
+constexpr int kMaxLogitCols = 512;    // widest last hidden layer of the top model
+constexpr int kLdsMax = 160 * 1024;   // LDS of one gfx950 workgroup
+
 // Per-tick values that a replayed graph reads from device memory; k_advance
-// writes them at the start of each stream's part of a tick.  A job whose
-// `ta` is set takes its row count (and the values listed with each job)
-// from *ta instead of its immediate fields; with ta_in set its dataset
-// input pointers are bases, offset by ta->row0 rows.
+// writes them at the start of each stream's part of a tick.  With a tick
+// record the kernels take the row count, noise step, headers and scale from
+// it and offset the dataset pointers of their call by row0 rows.
 struct TickArgs {
   int32_t rows;        // rows of the batch group
   int32_t group;       // batch-group id (noise step, header sequence)
@@ -43,137 +73,187 @@ struct AdvanceJob {
 };
 hipError_t launch_advance(const AdvanceJob& j, hipStream_t st);
 
-// C[m][n] = epilogue( sum_k A[m][k] * B[n][k] ), A = [A1 | A2] split at
-// column ksplit (A2 may be null when ksplit >= K).  Epilogue: + bias[n],
-// optional ReLU, then columns n < nsplit go to C1 (multiplied by
-// (mask[m][n] > 0) when mask is set), columns n >= nsplit to C2 at column
-// n - nsplit (float32 when c2_f32).  All matrices row-major with leading
-// dimensions in elements; rows must be 16-byte aligned.
-struct GemmNT {
-  const void* A1 = nullptr; int64_t lda1 = 0;
-  const void* A2 = nullptr; int64_t lda2 = 0; int ksplit = 1 << 30;
-  const void* B = nullptr; int64_t ldb = 0;
-  void* C1 = nullptr; int64_t ldc1 = 0;
-  void* C2 = nullptr; int64_t ldc2 = 0; int nsplit = 1 << 30; int c2_f32 = 0;
+// ------------------------------------------------------------ chain kernels
+// LDS region of a row block: byte offset in the kernel's dynamic LDS and row
+// pitch in bytes (a pitch of 0 marks an absent buffer).
+struct LBuf { int32_t off = 0, pitch = 0; };
+
+// RC-layout global matrix (null p: not written).
+struct RCMat { void* p = nullptr; int32_t cp = 0, pad = 0; };
+
+// One product of a row block with a weight operand W [N x ldw] (element
+// type, row-major, ldw a multiple of 8, columns K .. ldw-1 zero):
+// out[r][n] = sum_k in[r][k] * W[n][k], n < N, then
+//   forward:         + bias[n] (bias set), ReLU when relu;
+//   input gradient:  * (mask[r][n] > 0) when mask.pitch > 0.
+// Columns of `out` from N up to the next multiple of the MFMA depth are
+// written as zeros, as are rows beyond the group.  rc: RC copy of out.
+// mask_src (k_bwd): the mask is first loaded into `mask` from this matrix.
+struct ChainLayer {
+  const void* W = nullptr;
   const float* bias = nullptr;
-  const void* mask = nullptr; int64_t ldm = 0;
-  int relu = 0;
-  int M = 0, N = 0, K = 0;
-  // channel slot header written by block 0 (hdr_out != null) / checked by
-  // block 0 against chk_seq (mismatch -> atomic increment of *err)
-  int32_t* hdr_out = nullptr; int32_t hdr[3] = {0, 0, 0};
-  const int32_t* hdr_chk = nullptr; int32_t chk_seq = 0; int32_t* err = nullptr;
-  // tick record: M = ta->rows; ta_in: A1 += ta->row0 rows; header values
-  // and the expected sequence from *ta
-  const TickArgs* ta = nullptr; int ta_in = 0;
+  int32_t ldw = 0, N = 0, K = 0, relu = 0;
+  LBuf in, out, mask;
+  RCMat rc, mask_src;
 };
 
-// One layer's weight gradient + SGD: G[n][k] = sum over rows r of
-// D[r][n] * X[r][k], g_b[n] = sum_r D[r][n]; W -= scale * G, bias -= scale *
-// g_b, then the operand copies Wq [N x ldq] and Wtq [K x ldt] (nullable) are
-// rewritten from the new W.  X = [X1 | X2] split at column ksplit.  The rows
-// are cut into `splits` chunks of rows_per_split (a multiple of the stage
-// depth); with more than one chunk each block writes float32 partials
-// part[s][n][k] (partb[s][n]) and k_multi_reduce finishes the layer.
-struct GemmDW {
-  const void* D = nullptr; int64_t ldd = 0;
-  const void* X1 = nullptr; int64_t ldx1 = 0;
-  const void* X2 = nullptr; int64_t ldx2 = 0; int ksplit = 1 << 30;
+// Bottom-model input of a row block: [embeddings of n_cat fields | dense],
+// gathered into LDS (`buf`) and copied to `rc` (for the first layer's
+// weight gradient).  T: float32 tables [n_cat * V x E].
+struct RowInput {
+  int32_t dense_in = 0, n_cat = 0, V = 0, E = 0;
+  int32_t dense_vec = 0;              // dense rows 16-byte aligned: vector loads
+  const float* T = nullptr;
+  LBuf buf;
+  RCMat rc;
+};
+
+// Per-row clip to L2 norm C and Philox Gaussian noise of std stdv keyed by
+// (seed, step = group, global row, column / 4, tag).
+struct MsgOp {
+  int32_t clip = 0, noise = 0;
+  float C = 0.f, stdv = 0.f;
+  uint64_t seed = 0;
+  uint32_t tag = 0;
+};
+
+// Values of one chain launch (a tick record replaces rows, group, row0 and
+// the headers, and then dense / ids / labels are dataset bases).
+struct ChainCall {
+  const void* dense = nullptr;
+  int64_t ld = 0;
+  const int32_t* ids = nullptr;
+  const float* labels = nullptr;
+  int64_t row0 = 0;                   // global sample id of row 0
+  int32_t rows = 0, group = 0;
+  int32_t hdr[3] = {0, 0, 0};         // header written by block 0
+  int32_t chk = 0;                    // group expected in the header read
+};
+
+// Party B's forward of a group: input, L layers (ping-pong LDS buffers),
+// the last layer's output row-major in z, and the embedding message in
+// zhat (zhat == z when neither clip nor noise is on), with norm/cfac per
+// row when clipping; block 0 writes the slot header.
+struct FwdJob {
+  RowInput in;
+  int32_t L = 0;
+  ChainLayer l[kMaxChain];
+  void* z = nullptr; int32_t ldz = 0;
+  int32_t publish = 0;
+  MsgOp m;
+  void* zhat = nullptr; int32_t ldzh = 0;
+  float* norm = nullptr; float* cfac = nullptr;
+  int32_t* hdr_out = nullptr;
+};
+
+// Party A's step of a group: forward of A's layers fa (the last writes the
+// first dA columns of `cat`), B's embedding zb into columns [dA, dA + dB) of
+// cat, the top hidden layers ft, logit + BCE into the last hidden delta dh
+// (per-block partials {sum loss, sum dl, sum_r dl * h[r][c]} to
+// part[block]), the top input-gradient chain dt (j = H-1 .. 1), the concat
+// product dc (columns < dA: A's cut delta into dc.out, masked by cat when
+// A's last layer has a ReLU; columns >= dA: the gradient message, staged as
+// float32 in `msg` when clip/noise run, else written to ring directly), and
+// A's chain da (l = LA-1 .. 1); with tables, gx = the float32 gradient of
+// the embedding columns.
+struct ActiveJob {
+  RowInput in;
+  int32_t LA = 0;
+  ChainLayer fa[kMaxChain];
+  LBuf cat; RCMat cat_rc; int32_t dA = 0, dB = 0;
+  const void* zb = nullptr; int32_t ldzb = 0;
+  const int32_t* hdr_chk = nullptr; int32_t* err = nullptr;
+  int32_t H = 0;
+  ChainLayer ft[kMaxChain];
+  const float* lw = nullptr; const float* lb = nullptr; int32_t relu_h = 0;
+  LBuf dh; RCMat dh_rc;
+  float* part = nullptr;
+  LBuf red;
+  ChainLayer dt[kMaxChain];
+  ChainLayer dc;
+  int32_t gextra = 0;
+  MsgOp m;
+  LBuf msg;
+  void* ring = nullptr; int32_t ldring = 0;
+  int32_t* hdr_out = nullptr;
+  int32_t nda = 0;
+  ChainLayer da[kMaxChain];
+  int32_t has_gx = 0;
+  ChainLayer gx;
+  float* gxp = nullptr; int32_t ldgx = 0;
+};
+
+// Party B's backward of a group: cut-layer backward of the message g
+// (row-major) at the stashed output z (clip backward with norm/cfac when
+// clip), then the chain dx (l = L-1 .. 1), masks loaded from the stashed
+// RC activations; with tables, gx as in ActiveJob.
+struct BwdJob {
+  const void* g = nullptr; int32_t ldg = 0;
+  const void* z = nullptr; int32_t ldz = 0;
+  const float* norm = nullptr; const float* cfac = nullptr;
+  int32_t clip = 0, relu = 0, D = 0;
+  float C = 0.f;
+  LBuf d; RCMat d_rc;
+  const int32_t* hdr_chk = nullptr; int32_t* err = nullptr;
+  int32_t nd = 0;
+  ChainLayer dx[kMaxChain];
+  int32_t has_gx = 0;
+  ChainLayer gx;
+  float* gxp = nullptr; int32_t ldgx = 0;
+};
+
+// Jobs live in device memory (written once when the context is created);
+// `rt` selects 16 * rt rows per block, `lds` the dynamic LDS bytes.
+hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
+                      const TickArgs* ta, hipStream_t st);
+hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
+                         const ChainCall& c, const TickArgs* ta, hipStream_t st);
+hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
+                      const TickArgs* ta, hipStream_t st);
+// Raise the dynamic-LDS limit of every chain kernel to kLdsMax.
+hipError_t chain_init();
+
+// --------------------------------------------------------- weight gradients
+// One layer's weight gradient over the group's rows from RC operands:
+// G[n][k] = sum_r D[r][n] X[r][k], g_b[n] = sum_r D[r][n]; W -= scale * G,
+// bias -= scale * g_b, then the operand copies Wq [N x ldq] and Wtq
+// [K x ldt] (nullable) are rewritten from the new W.  Rows are cut into
+// `splits` chunks of rps rows (a multiple of 128); with more than one chunk
+// each block writes float32 partials part[s][n][kp] (kp = K rounded up to
+// 4) and partb[s][n], and k_dw_reduce finishes the layer.  Blocks
+// [first_block, first_block + tiles * splits) work on this problem.
+struct DwProb {
+  RCMat D, X;
   float* W = nullptr; float* bias = nullptr;
-  void* Wq = nullptr; int64_t ldq = 0; void* Wtq = nullptr; int64_t ldt = 0;
+  void* Wq = nullptr; void* Wtq = nullptr;
+  int32_t ldq = 0, ldt = 0;
   float* part = nullptr; float* partb = nullptr;
-  int N = 0, K = 0, splits = 1, rows_per_split = 0;
-  int x_ta = 0;                        // X1 += ta->row0 rows (dataset input)
+  int32_t N = 0, K = 0, kp = 0, splits = 1, rps = 0, first_block = 0;
 };
-constexpr int kMaxDw = 8;
-// Several layers' weight gradients over the same R rows (one launch).
-struct MultiDW {
-  GemmDW p[kMaxDw];
-  int n = 0, R = 0;
-  float scale = 0.f;
-  int first_block[kMaxDw + 1] = {0};   // filled by launch_multi_dw
-  const TickArgs* ta = nullptr;        // R = ta->rows, scale = ta->scale
+struct DwJob {
+  int32_t n = 0, blocks = 0;
+  DwProb p[kMaxDw];
+  // reduction launch: split problems' element groups, then the logit
+  // layer's columns (lblocks partial rows of Hd + 2 floats, of which the
+  // first ceil(rows / lrows) are the group's)
+  int32_t red_threads = 0, red_blocks = 0;
+  float* lpart = nullptr; int32_t Hd = 0, lrows = 0;
+  float* lw = nullptr; float* lb = nullptr;
 };
+hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, const TickArgs* ta,
+                     hipStream_t st);
+// loss_out: the group's mean loss (from the logit partials); with a tick
+// record, loss_base + ta->loss_idx instead.
+hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
+                            float* loss_out, const TickArgs* ta, float* loss_base, hipStream_t st);
 
-hipError_t launch_gemm_nt(Elt e, const GemmNT& g, hipStream_t st);
-hipError_t launch_multi_dw(Elt e, MultiDW& m, hipStream_t st);
-int dw_stage_rows(Elt e);   // rows per pipeline stage of the dW kernel
-int dw_tiles(int N, int K); // 64 x 64 output tiles of one layer
-
+// ---------------------------------------------------------------- others
 // Operand copies of one layer's float32 weight W [out x in]:
 // Wq [out x ldq] and Wtq [in x ldt] of element type e (ldq, ldt padded).
 struct CastJob {
   const float* W; void* Wq; void* Wtq; int out, in; int64_t ldq, ldt;
 };
 hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
-
-constexpr int kMaxLogitCols = 512;   // widest last hidden layer of the top model
-
-// Logit layer + BCE on the last hidden activation H [R x ldh] (width Hd):
-// l = H w + b, loss_i = BCE(l, y), dl = sigmoid(l) - y; writes
-// delta [R x ldd] = dl * w * (H > 0) (element type e).  Each block writes
-// partial sums part[blk] = {loss, sum dl, sum_r dl * H[r][0..Hd)} (Hd + 2
-// floats); k_multi_reduce reduces them in block order:
-// *loss_out = sum loss / R (loss_out may be null), w -= scale * sum dl*H,
-// b -= scale * sum dl.
-struct LogitJob {
-  const void* H; int64_t ldh; int Hd, R;
-  float* w; float* b; const float* y;
-  void* delta; int64_t ldd; int relu;
-  float* part; int blocks; float scale; float* loss_out;
-  // tick record: R, scale, y += row0, loss_out = loss_base + loss_idx
-  const TickArgs* ta; float* loss_base;
-};
-hipError_t launch_logit_bce(Elt e, const LogitJob& j, hipStream_t st);
-// Second stage of the split layers of m and (lj != null) of the logit
-// kernel's partials, in one launch.
-hipError_t launch_multi_reduce(Elt e, const MultiDW& m, const LogitJob* lj, hipStream_t st);
-
-// Segments mapping a row of a tick to its global sample id (<= 8 replicas).
-struct RowMap {
-  int n = 1;
-  int32_t start[8] = {0};
-  int64_t row0[8] = {0};
-};
-
-// Per-row clip + Gaussian noise: out[r] = c_r * v[r] + std * xi(seed, step,
-// global row, col, tag), c_r = min(1, C / ||v[r]||) when clip (else 1).
-// v is element type e (or float32 when v_f32); out is element type e.
-// norm/cfac (nullable) receive ||v[r]|| and c_r.  Block 0 writes the slot
-// header.
-struct ClipNoiseJob {
-  const void* v; int64_t ldv; int v_f32;
-  void* out; int64_t ldo;
-  float* norm; float* cfac;
-  int R, D; int clip; float C; int noise; float stdv;
-  uint64_t seed; uint32_t step; uint32_t tag; RowMap rows;
-  int32_t* hdr_out; int32_t hdr[3];
-  // tick record: R, step = group, global rows from row0, header values
-  const TickArgs* ta;
-};
-hipError_t launch_clip_noise(Elt e, const ClipNoiseJob& j, hipStream_t st);
-
-// Cut-layer backward of party B: g = message row; if clipped (n_r > C):
-// g = c_r (g - u (u . g)), u = z_r / n_r; delta = g * (z > 0 when relu).
-// Block 0 checks the slot header.
-struct CutBwdJob {
-  const void* g; int64_t ldg; const void* z; int64_t ldz;
-  const float* norm; const float* cfac; int clip; float C; int relu;
-  void* delta; int64_t ldd; int R, D;
-  const int32_t* hdr_chk; int32_t chk_seq; int32_t* err;
-  const TickArgs* ta;                  // R and the expected sequence
-};
-hipError_t launch_cut_backward(Elt e, const CutBwdJob& j, hipStream_t st);
-
-// Embedding gather + concat: X[r] = [T[f*V + ids[r][f]] for f | dense[r]]
-// (float32 tables; X and dense of element type e).
-struct GatherJob {
-  const float* T; const int32_t* ids; int n_cat, V, E;
-  const void* dense; int64_t ldx_in; int dense_in;
-  void* X; int64_t ldx; int R;
-  const TickArgs* ta;                  // R; ids and dense offset by row0 rows
-};
-hipError_t launch_gather(Elt e, const GatherJob& j, hipStream_t st);
 
 // Sparse SGD on the tables: for every row f*V + id touched by field f,
 // T[row][c] -= scale * sum over samples r with ids[r][f] == id of G[r][f*E + c]
