@@ -60,7 +60,7 @@ struct Party {
   int L = 0, din = 0, nslots = 1;
   int in[VFL_MAX_LAYERS]{}, out[VFL_MAX_LAYERS]{};
   bool relu[VFL_MAX_LAYERS]{};
-  int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
+  int kq[VFL_MAX_LAYERS]{}, kt[VFL_MAX_LAYERS]{};   // K steps of the packed copies of W, W^T
   size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{}, T = 0;
   size_t Wq[kMaxSlots][VFL_MAX_LAYERS]{}, Wtq[kMaxSlots][VFL_MAX_LAYERS]{};
   size_t x0rc[kMaxSlots]{};                     // RC copy of the bottom input
@@ -78,7 +78,7 @@ struct Top {
   int H = 0;                          // hidden layers (n_layers - 1)
   int in[VFL_MAX_LAYERS]{}, out[VFL_MAX_LAYERS]{};
   bool relu[VFL_MAX_LAYERS]{};
-  int64_t ldq[VFL_MAX_LAYERS]{}, ldt[VFL_MAX_LAYERS]{};
+  int kq[VFL_MAX_LAYERS]{}, kt[VFL_MAX_LAYERS]{};
   size_t W[VFL_MAX_LAYERS]{}, b[VFL_MAX_LAYERS]{};
   size_t Wq[VFL_MAX_LAYERS]{}, Wtq[VFL_MAX_LAYERS]{};
   size_t arc[VFL_MAX_LAYERS]{}, drc[VFL_MAX_LAYERS]{};
@@ -112,7 +112,7 @@ struct ActLds {
   LBuf in, fa[VFL_MAX_LAYERS], cat, ft[VFL_MAX_LAYERS], P[2], msg, red;
   int bytes = 0;
 };
-struct BwdLds { LBuf P[2], mask; int bytes = 0; };
+struct BwdLds { LBuf P[2], mask[VFL_MAX_LAYERS]; int bytes = 0; };
 
 struct KMeta { int rt = 1, blocks = 1, lds = 0; };
 
@@ -276,7 +276,9 @@ void plan_act_lds(const Plan& p, int BR, bool gextra, ActLds& a) {
   a.P[0] = l.take(w, es);
   a.P[1] = l.take(w, es);
   if (gextra) a.msg = l.take(p.dB, 4);
-  a.red = l.raw(4 * 4 * (p.T.out[p.T.H - 1] + 2));
+  // logit reduction scratch [wavefronts][Hd + 2], logit weights [Hd], the
+  // block's labels [BR]
+  a.red = l.raw(4 * (kChainWaves * (p.T.out[p.T.H - 1] + 2) + p.T.out[p.T.H - 1] + BR));
   a.bytes = l.off;
 }
 
@@ -285,12 +287,13 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
   l.KS = p.e == BF16 ? 32 : 16;
   l.BR = BR;
   const int es = elt_size(p.e);
-  int w = 1, wm = 0;
+  int w = 1;
   for (int i = 0; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
-  for (int i = 0; i + 1 < p.P.L; ++i) wm = std::max(wm, p.P.out[i]);
   b.P[0] = l.take(w, es);
   b.P[1] = l.take(w, es);
-  if (wm) b.mask = l.take(wm, es);
+  // one mask buffer per ReLU layer below the last: all are loaded up front
+  for (int i = 0; i + 1 < p.P.L; ++i)
+    if (p.P.relu[i]) b.mask[i] = l.take(p.P.out[i], es);
   b.bytes = l.off;
 }
 
@@ -345,6 +348,11 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   const bool gextra = o->flags & (VFL_CLIP_GRAD | VFL_NOISE_GRAD);
   Layout ly;
   auto rc_bytes = [&](int cols) { return (size_t)es * Ra * ld_of(cols); };
+  // packed MFMA operands: tiles of 16 rows up to the MFMA depth, K steps of
+  // one fragment (1 KB) each
+  const int KS = p.e == BF16 ? 32 : 16;
+  auto ksteps = [&](int K) { return (K + KS - 1) / KS; };
+  auto packed_bytes = [&](int N, int K) { return (size_t)((N + KS - 1) / KS * KS) * ksteps(K) * 64; };
 
   auto party = [&](Party& P, const vfl_bottom_spec* s, int nslots, bool passive) {
     P.spec = *s;
@@ -356,8 +364,8 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       P.in[l] = in;
       P.out[l] = s->widths[l];
       P.relu[l] = (s->relu_mask >> l) & 1u;
-      P.ldq[l] = ld_of(in);
-      P.ldt[l] = ld_of(P.out[l]);
+      P.kq[l] = ksteps(in);
+      P.kt[l] = ksteps(P.out[l]);
       P.W[l] = ly.take(sizeof(float) * (size_t)P.out[l] * in);
       P.b[l] = ly.take(sizeof(float) * (size_t)P.out[l]);
       P.drc[l] = ly.take(rc_bytes(P.out[l]));
@@ -366,8 +374,8 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     if (s->n_cat) P.T = ly.take(sizeof(float) * (size_t)s->n_cat * s->vocab * s->emb_dim);
     for (int q = 0; q < nslots; ++q) {
       for (int l = 0; l < P.L; ++l) {
-        P.Wq[q][l] = ly.take((size_t)es * P.out[l] * P.ldq[l]);
-        P.Wtq[q][l] = ly.take((size_t)es * P.in[l] * P.ldt[l]);
+        P.Wq[q][l] = ly.take(packed_bytes(P.out[l], P.in[l]));
+        P.Wtq[q][l] = ly.take(packed_bytes(P.in[l], P.out[l]));
         if (l + 1 < P.L) P.arc[q][l] = ly.take(rc_bytes(P.out[l]));
       }
       P.x0rc[q] = ly.take(rc_bytes(P.din));
@@ -399,13 +407,13 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     T.in[j] = in;
     T.out[j] = t->widths[j];
     T.relu[j] = j < T.H && ((t->relu_mask >> j) & 1u);
-    T.ldq[j] = ld_of(in);
-    T.ldt[j] = ld_of(T.out[j]);
+    T.kq[j] = ksteps(in);
+    T.kt[j] = ksteps(T.out[j]);
     T.W[j] = ly.take(sizeof(float) * (size_t)T.out[j] * in);
     T.b[j] = ly.take(sizeof(float) * (size_t)T.out[j]);
     if (j < T.H) {
-      T.Wq[j] = ly.take((size_t)es * T.out[j] * T.ldq[j]);
-      T.Wtq[j] = ly.take((size_t)es * T.in[j] * T.ldt[j]);
+      T.Wq[j] = ly.take(packed_bytes(T.out[j], T.in[j]));
+      T.Wtq[j] = ly.take(packed_bytes(T.in[j], T.out[j]));
       if (j + 1 < T.H) T.arc[j] = ly.take(rc_bytes(T.out[j]));
       T.drc[j] = ly.take(rc_bytes(T.out[j]));
     }
@@ -469,10 +477,10 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
 int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
 int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
 
-ChainLayer layer(const void* W, int64_t ldw, const float* bias, int N, int K, bool relu, LBuf in,
+ChainLayer layer(const void* W, int kst, const float* bias, int N, int K, bool relu, LBuf in,
                  LBuf out) {
   ChainLayer L;
-  L.W = W; L.ldw = (int32_t)ldw; L.bias = bias;
+  L.W = W; L.kst = kst; L.bias = bias;
   L.N = N; L.K = K; L.relu = relu ? 1 : 0;
   L.in = in; L.out = out;
   return L;
@@ -488,16 +496,16 @@ MsgOp msg_op(const vfl_opts& o, bool clip, bool noise, uint32_t tag) {
 
 // Host check of what a chain kernel touches in LDS and in a weight operand:
 // the input buffer holds K columns rounded up to the MFMA depth, the output
-// and mask buffers N columns, all inside the block's LDS, and the operand
-// rows hold K elements rounded up to a 16-byte chunk; the RC copy holds
+// and mask buffers N columns, all inside the block's LDS, and the packed
+// operand has the K steps of the product; the RC copy holds
 // rc_cols columns (N unless given).
 bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_out, int rc_cols = -1) {
-  const int es = elt_size(p.e), KS = p.e == BF16 ? 32 : 16, CE = 16 / es;
+  const int es = elt_size(p.e), KS = p.e == BF16 ? 32 : 16;
   auto inside = [&](const LBuf& b, int cols) {
     const int need = (cols + KS - 1) / KS * KS * es;
     return b.pitch >= need && b.off >= 0 && b.off + b.pitch * BR <= lds && b.off % 16 == 0 && b.pitch % 16 == 0;
   };
-  if (!L.W || L.N < 1 || L.K < 1 || L.ldw < (L.K + CE - 1) / CE * CE) return false;
+  if (!L.W || L.N < 1 || L.K < 1 || L.kst != (L.K + KS - 1) / KS) return false;
   if (!inside(L.in, L.K)) return false;
   if (lds_out && !inside(L.out, L.N)) return false;
   if (L.mask.pitch && !inside(L.mask, L.N)) return false;
@@ -552,7 +560,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     f.in.rc = rcm(c, P.x0rc[q], P.din);
     f.L = P.L;
     for (int l = 0; l < P.L; ++l) {
-      f.l[l] = layer(c->ws + P.Wq[q][l], P.ldq[l], at_f(P.b[l]), P.out[l], P.in[l], P.relu[l],
+      f.l[l] = layer(c->ws + P.Wq[q][l], P.kq[l], at_f(P.b[l]), P.out[l], P.in[l], P.relu[l],
                      p.lf.buf[l % 2], p.lf.buf[(l + 1) % 2]);
       if (l + 1 < P.L) f.l[l].rc = rcm(c, P.arc[q][l], P.out[l]);
     }
@@ -576,7 +584,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int l = 0; l < A.L; ++l) {
       const LBuf src = l == 0 ? la.in : la.fa[l - 1];
       const LBuf dst = l + 1 < A.L ? la.fa[l] : la.cat;
-      a.fa[l] = layer(c->ws + A.Wq[0][l], A.ldq[l], at_f(A.b[l]), A.out[l], A.in[l], A.relu[l], src, dst);
+      a.fa[l] = layer(c->ws + A.Wq[0][l], A.kq[l], at_f(A.b[l]), A.out[l], A.in[l], A.relu[l], src, dst);
       if (l + 1 < A.L) a.fa[l].rc = rcm(c, A.arc[0][l], A.out[l]);
     }
     a.cat = la.cat; a.cat_rc = rcm(c, p.cat_rc, p.dA + p.dB); a.dA = p.dA; a.dB = p.dB;
@@ -584,7 +592,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     a.hdr_chk = hdrp(0, q); a.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
     a.H = T.H;
     for (int j = 0; j < T.H; ++j) {
-      a.ft[j] = layer(c->ws + T.Wq[j], T.ldq[j], at_f(T.b[j]), T.out[j], T.in[j], T.relu[j],
+      a.ft[j] = layer(c->ws + T.Wq[j], T.kq[j], at_f(T.b[j]), T.out[j], T.in[j], T.relu[j],
                       j == 0 ? la.cat : la.ft[j - 1], la.ft[j]);
       if (j + 1 < T.H) a.ft[j].rc = rcm(c, T.arc[j], T.out[j]);
     }
@@ -595,14 +603,14 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int qq = 0; qq + 1 < T.H; ++qq) {
       const int j = T.H - 1 - qq;           // delta of top layer j -> layer j-1
       ChainLayer& L = a.dt[qq];
-      L = layer(c->ws + T.Wtq[j], T.ldt[j], nullptr, T.in[j], T.out[j], false, la.P[qq % 2], la.P[(qq + 1) % 2]);
+      L = layer(c->ws + T.Wtq[j], T.kt[j], nullptr, T.in[j], T.out[j], false, la.P[qq % 2], la.P[(qq + 1) % 2]);
       if (T.relu[j - 1]) L.mask = la.ft[j - 1];
       L.rc = rcm(c, T.drc[j - 1], T.out[j - 1]);
     }
     {
       const int h = T.H - 1;
       ChainLayer& L = a.dc;
-      L = layer(c->ws + T.Wtq[0], T.ldt[0], nullptr, p.dA + p.dB, T.out[0], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      L = layer(c->ws + T.Wtq[0], T.kt[0], nullptr, p.dA + p.dB, T.out[0], false, la.P[h % 2], la.P[(h + 1) % 2]);
       if (A.relu[A.L - 1]) L.mask = la.cat;
       L.rc = rcm(c, A.drc[A.L - 1], p.dA);
     }
@@ -616,14 +624,14 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       const int l = A.L - 1 - qq;           // delta of A's layer l -> layer l-1
       const int h = T.H + qq;
       ChainLayer& L = a.da[qq];
-      L = layer(c->ws + A.Wtq[0][l], A.ldt[l], nullptr, A.in[l], A.out[l], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      L = layer(c->ws + A.Wtq[0][l], A.kt[l], nullptr, A.in[l], A.out[l], false, la.P[h % 2], la.P[(h + 1) % 2]);
       if (A.relu[l - 1]) L.mask = la.fa[l - 1];
       L.rc = rcm(c, A.drc[l - 1], A.out[l - 1]);
     }
     a.has_gx = A.spec.n_cat > 0;
     if (a.has_gx) {
       const int h = T.H + A.L - 1;
-      a.gx = layer(c->ws + A.Wtq[0][0], A.ldt[0], nullptr, A.spec.n_cat * A.spec.emb_dim, A.out[0], false,
+      a.gx = layer(c->ws + A.Wtq[0][0], A.kt[0], nullptr, A.spec.n_cat * A.spec.emb_dim, A.out[0], false,
                    la.P[h % 2], LBuf());
       a.gxp = at_f(A.gx); a.ldgx = (int32_t)A.ldgx;
     }
@@ -643,16 +651,16 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int qq = 0; qq + 1 < P.L; ++qq) {
       const int l = P.L - 1 - qq;
       ChainLayer& L = b.dx[qq];
-      L = layer(c->ws + P.Wtq[q][l], P.ldt[l], nullptr, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
+      L = layer(c->ws + P.Wtq[q][l], P.kt[l], nullptr, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
       if (P.relu[l - 1]) {
-        L.mask = lb.mask;
+        L.mask = lb.mask[l - 1];
         L.mask_src = rcm(c, P.arc[q][l - 1], P.out[l - 1]);
       }
       L.rc = rcm(c, P.drc[l - 1], P.out[l - 1]);
     }
     b.has_gx = P.spec.n_cat > 0;
     if (b.has_gx) {
-      b.gx = layer(c->ws + P.Wtq[q][0], P.ldt[0], nullptr, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
+      b.gx = layer(c->ws + P.Wtq[q][0], P.kt[0], nullptr, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
                    lb.P[(P.L - 1) % 2], LBuf());
       b.gxp = at_f(P.gx); b.ldgx = (int32_t)P.ldgx;
     }
@@ -660,12 +668,12 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
 
   // weight gradients
   auto add = [&](DwJob& J, const DwMeta& m, size_t D, size_t X, int N, int K, size_t W, size_t bias,
-                 size_t Wq, int64_t ldq, size_t Wtq, int64_t ldt, size_t part, size_t partb) {
+                 size_t Wq, int kq, size_t Wtq, int kt, size_t part, size_t partb) {
     DwProb& d = J.p[J.n++];
     d.D = rcm(c, D, N);
     d.X = rcm(c, X, K);
     d.W = at_f(W); d.bias = at_f(bias);
-    d.Wq = c->ws + Wq; d.Wtq = c->ws + Wtq; d.ldq = (int32_t)ldq; d.ldt = (int32_t)ldt;
+    d.Wq = c->ws + Wq; d.Wtq = c->ws + Wtq; d.kq = kq; d.kt = kt;
     d.part = part ? at_f(part) : nullptr;
     d.partb = partb ? at_f(partb) : nullptr;
     d.N = N; d.K = K; d.kp = (K + 3) / 4 * 4;
@@ -675,10 +683,10 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
   };
   for (int j = 0; j < T.H; ++j)
     add(dwa, p.da, T.drc[j], j == 0 ? p.cat_rc : T.arc[j - 1], T.out[j], T.in[j], T.W[j], T.b[j], T.Wq[j],
-        T.ldq[j], T.Wtq[j], T.ldt[j], T.part[j], T.partb[j]);
+        T.kq[j], T.Wtq[j], T.kt[j], T.part[j], T.partb[j]);
   for (int l = 0; l < A.L; ++l)
     add(dwa, p.da, A.drc[l], l == 0 ? A.x0rc[0] : A.arc[0][l - 1], A.out[l], A.in[l], A.W[l], A.b[l],
-        A.Wq[0][l], A.ldq[l], A.Wtq[0][l], A.ldt[l], A.part[l], A.partb[l]);
+        A.Wq[0][l], A.kq[l], A.Wtq[0][l], A.kt[l], A.part[l], A.partb[l]);
   dwa.red_threads = p.da.red_threads;
   dwa.red_blocks = p.da.red_blocks;
   dwa.lpart = at_f(T.logit_part);
@@ -690,7 +698,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     DwJob& J = dwb[q];
     for (int l = 0; l < P.L; ++l)
       add(J, p.db, P.drc[l], l == 0 ? P.x0rc[q] : P.arc[q][l - 1], P.out[l], P.in[l], P.W[l], P.b[l],
-          P.Wq[q][l], P.ldq[l], P.Wtq[q][l], P.ldt[l], P.part[l], P.partb[l]);
+          P.Wq[q][l], P.kq[l], P.Wtq[q][l], P.kt[l], P.part[l], P.partb[l]);
     J.red_threads = p.db.red_threads;
     J.red_blocks = p.db.red_blocks;
   }
@@ -708,7 +716,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     if (aj[q].has_gx) ok = ok && layer_fits(p, aj[q].gx, ba, p.ka.lds, false);
     for (int l = 0; l < bj[q].nd; ++l) ok = ok && layer_fits(p, bj[q].dx[l], bb, p.kb.lds, true);
     if (bj[q].has_gx) ok = ok && layer_fits(p, bj[q].gx, bb, p.kb.lds, false);
-    ok = ok && p.la.red.off + 16 * (p.T.out[p.T.H - 1] + 2) <= p.ka.lds;
+    ok = ok && p.la.red.off + 4 * ((kChainWaves + 1) * p.T.out[p.T.H - 1] + 2 * kChainWaves + ba) <= p.ka.lds;
     if (!ok) return "internal: chain layout does not cover a layer";
   }
   return "";
@@ -864,11 +872,11 @@ vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipS
   int n = 0;
   for (int l = 0; l < P.L; ++l)
     jobs[n++] = CastJob{at<float>(c, P.W[l]), c->ws + P.Wq[slot][l], c->ws + P.Wtq[slot][l],
-                        P.out[l], P.in[l], P.ldq[l], P.ldt[l]};
+                        P.out[l], P.in[l], P.kq[l], P.kt[l]};
   if (T)
     for (int j = 0; j < T->H; ++j)
       jobs[n++] = CastJob{at<float>(c, T->W[j]), c->ws + T->Wq[j], c->ws + T->Wtq[j],
-                          T->out[j], T->in[j], T->ldq[j], T->ldt[j]};
+                          T->out[j], T->in[j], T->kq[j], T->kt[j]};
   double bytes = 0;
   for (int i = 0; i < n; ++i) bytes += (double)jobs[i].out * jobs[i].in * (4 + 2 * elt_size(c->p.e));
   TIMED(VFL_K_CAST, bytes, st, launch_cast(c->p.e, jobs, n, st));

@@ -1,11 +1,11 @@
 // Fused row-block kernels of the split-learning step on gfx950 (k_fwd,
 // k_active, k_bwd; see kernels.h for what each computes).
 //
-// A workgroup of 256 threads (4 wavefronts) owns BR = 16 * RT consecutive
-// rows of the group and runs every layer of its chain on them, the
-// activations and deltas staying in LDS.  Each layer is one MFMA product
+// A workgroup of 512 threads (8 wavefronts, two per SIMD) owns BR = 16 * RT
+// consecutive rows of the group and runs every layer of its chain on them,
+// the activations and deltas staying in LDS.  Each layer is one MFMA product
 // out[BR x N] = in[BR x K] W^T: wavefront w takes the 16-column output tiles
-// w, w+4, w+8, ... (four at a time), loads the weight fragments of its tiles
+// w, w+8, w+16, ... (two at a time), loads the weight fragments of its tiles
 // straight from global memory (L2-resident: every block reads each weight
 // once) four MFMA steps ahead, and the activation fragments from LDS;
 // v_mfma_f32_16x16x32_bf16 for bf16 operands, v_mfma_f32_16x16x4_f32 for
@@ -63,73 +63,119 @@ __device__ __forceinline__ char* lp(char* s, const LBuf& b, int r, int byte_col)
 }
 
 // ------------------------------------------------------------ block product
-// epi(r, n, acc, bias): block row r, output columns n .. n+3 (n a multiple
-// of 4; bias[i] = bias[n + i], zero without a bias or beyond N), called for
+constexpr int kNW = kChainWaves;    // wavefronts per block (two per SIMD)
+constexpr int kNT = 64 * kNW;        // threads per block
+constexpr int kNTW = 2;              // 16-column output tiles per wavefront and pass
+constexpr int kPF = 4;               // MFMA steps per weight load group
+
+// Weight-fragment registers of a chain: two load groups (ping-pong) and the
+// bias of the next pass.  Between two layers `wa` / `bn` already hold the
+// first group and the bias of the next layer's first pass (`layer` names
+// it), loaded while the previous layer finished: the next layer does not
+// start with a memory round trip.
+struct Pipe {
+  u32x4 wa[kPF][kNTW], wb[kPF][kNTW];
+  f32x4 bn[kNTW];
+  const ChainLayer* layer = nullptr;
+};
+
+// the loads of group g of a pass (tiles tile[]) of layer L into d: one
+// contiguous 1 KB fragment per tile and step of the packed operand.  Loads
+// are unconditional, clamped: tiles past the operand's last are never
+// stored and steps past the last never multiplied (a condition or a mask
+// around a load would make the compiler wait for it on the spot)
+template <typename T>
+__device__ __forceinline__ void wgroup(const ChainLayer& L, const int (&tile)[kNTW], int g,
+                                       u32x4 (&d)[kPF][kNTW]) {
+  constexpr int KS = Ch<T>::KS;
+  const int lane = threadIdx.x & 63;
+  const int ntl = (L.N + KS - 1) / KS * (KS / 16);
+  const VFL_GLOBAL u32x4* W = glb((const u32x4*)L.W) + lane;
+#pragma unroll
+  for (int j = 0; j < kNTW; ++j) {
+    const VFL_GLOBAL u32x4* wt = W + (int64_t)min(tile[j], ntl - 1) * L.kst * 64;
+#pragma unroll
+    for (int q = 0; q < kPF; ++q) d[q][j] = wt[min(g * kPF + q, L.kst - 1) * 64];
+  }
+}
+
+// bias values bias[n .. n+3] of the lane's output columns (zero past N)
+__device__ __forceinline__ void bgroup(const ChainLayer& L, const int (&tile)[kNTW], f32x4 (&b)[kNTW]) {
+  const int kc = (threadIdx.x & 63) >> 4;
+#pragma unroll
+  for (int j = 0; j < kNTW; ++j) {
+    const int n = tile[j] * 16 + 4 * kc;
+    b[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (L.bias) {
+      const VFL_GLOBAL float* bias = glb(L.bias);
+      if (n + 4 <= L.N) {
+        b[j] = *(const VFL_GLOBAL f32x4*)(bias + n);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n + i < L.N) b[j][i] = bias[n + i];
+      }
+    }
+  }
+}
+
+// the tiles of a wavefront's pass: wave + kNW * (kNTW * pass + j)
+__device__ __forceinline__ void pass_tiles(int pass, int (&tile)[kNTW]) {
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < kNTW; ++j) tile[j] = wave + kNW * (kNTW * pass + j);
+}
+
+// start the loads of the first group and bias of L's first pass into p
+template <typename T>
+__device__ __forceinline__ void prefetch(const ChainLayer* L, Pipe& p) {
+  p.layer = L;
+  if (!L) return;
+  int tile[kNTW];
+  pass_tiles(0, tile);
+  wgroup<T>(*L, tile, 0, p.wa);
+  bgroup(*L, tile, p.bn);
+}
+
+// out[r][n] = epi(r, n, sum_k in[r][k] W[n][k], bias) for the block's rows:
+// epi(r, n, acc, bias) receives block row r, output columns n .. n+3 (n a
+// multiple of 4; bias[i] = bias[n + i], zero without a bias or past N), for
 // every row of the block and every column below N rounded up to the MFMA
-// depth.  The weight fragments of PF consecutive MFMA steps are loaded as
-// one group while the previous group is multiplied, so a layer exposes the
-// load latency about once per PF steps.  Loads are unconditional and
-// fragments are used as loaded: a condition or a mask around a load makes
-// the compiler wait for it on the spot.
+// depth.  Full load groups are pipelined two per iteration (ping-pong
+// between p.wa and p.wb, so that no register copy waits for a prefetch),
+// then the remainder steps; after a wavefront's last MFMA of L it starts the
+// loads of `next` (nullable) into p.
 template <typename T, int RT, typename Epi>
-__device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Epi&& epi) {
-  constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS, NTW = 4, PF = 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe& p,
+                                         const ChainLayer* next, Epi&& epi) {
+  constexpr int KS = Ch<T>::KS, PF = kPF, NTW = kNTW;
+  const int lane = threadIdx.x & 63;
   const int kc = lane >> 4, lr = lane & 15;
   const int N = L.N, K = L.K;
   const int ntl = (N + KS - 1) / KS * (KS / 16);
   const int nks = (K + KS - 1) / KS;
-  const VFL_GLOBAL T* W = glb((const T*)L.W);
-  const VFL_GLOBAL float* bias = L.bias ? glb(L.bias) : nullptr;
-  const int64_t ldw = L.ldw;
+  const int nfull = nks / PF, rem = nks % PF;
   const LBuf in = L.in;
+  const int npass = (ntl + kNW * NTW - 1) / (kNW * NTW);
+  bool pre = p.layer == &L;
 #pragma unroll 1
-  for (int pass = 0; wave + 4 * NTW * pass < ntl; ++pass) {
+  for (int pass = 0; pass < npass; ++pass) {
     int tile[NTW];
-    bool on[NTW];
-#pragma unroll
-    for (int j = 0; j < NTW; ++j) {
-      tile[j] = wave + 4 * (NTW * pass + j);
-      on[j] = tile[j] < ntl;
-    }
+    pass_tiles(pass, tile);
     f32x4 bv[NTW];
+    if (pre) {
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) {
-      const int n = tile[j] * 16 + 4 * kc;
-      bv[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (bias && on[j]) {
-        if (n + 4 <= N) {
-          bv[j] = *(const VFL_GLOBAL f32x4*)(bias + n);
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (n + i < N) bv[j][i] = bias[n + i];
-        }
-      }
+      for (int j = 0; j < NTW; ++j) bv[j] = p.bn[j];
+    } else {
+      bgroup(L, tile, bv);
+      wgroup<T>(L, tile, 0, p.wa);
     }
+    pre = false;
     f32x4 acc[NTW][RT];
 #pragma unroll
     for (int j = 0; j < NTW; ++j)
 #pragma unroll
       for (int t = 0; t < RT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // branch-free loads from clamped addresses: a lane past N only feeds
-    // output columns the epilogue zeroes, a lane past K multiplies the zero
-    // LDS padding, and steps past the last are never multiplied
-    const VFL_GLOBAL T* wrow[NTW];
-#pragma unroll
-    for (int j = 0; j < NTW; ++j) wrow[j] = W + (int64_t)min(tile[j] * 16 + lr, N - 1) * ldw;
-    u32x4 wa[PF][NTW], wb[PF][NTW];
-    auto wload = [&](int g, u32x4 (&d)[PF][NTW]) {
-#pragma unroll
-      for (int q = 0; q < PF; ++q) {
-        const int k = (g * PF + q) * KS + kc * CE;
-        const int kk = k < K ? k : 0;
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) d[q][j] = *(const VFL_GLOBAL u32x4*)(wrow[j] + kk);
-      }
-    };
-    // one MFMA step: the weight fragments of step ks (held in w) against
-    // the LDS activation fragments of the step
     auto step = [&](int ks, const u32x4 (&w)[NTW]) {
       u32x4 xf[RT];
 #pragma unroll
@@ -151,12 +197,6 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Epi
         }
       }
     };
-    // full groups pipelined with an unconditional prefetch of the next
-    // group (the remainder group after the last full one), then the
-    // remainder steps; off tiles are multiplied too and never stored
-    // (two groups per iteration, ping-ponging between wa and wb, so that no
-    // register copy waits for a prefetch)
-    const int nfull = nks / PF, rem = nks % PF;
     auto group = [&](int g, const u32x4 (&w)[PF][NTW]) {
 #pragma unroll
       for (int q = 0; q < PF; ++q) step(g * PF + q, w[q]);
@@ -166,25 +206,27 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Epi
       for (int q = 0; q < PF - 1; ++q)
         if (q < rem) step(nfull * PF + q, w[q]);
     };
-    wload(0, wa);
     int g = 0;
 #pragma unroll 1
     for (; g + 2 <= nfull; g += 2) {
-      wload(g + 1, wb);
-      group(g, wa);
-      wload(g + 2, wa);
-      group(g + 1, wb);
+      wgroup<T>(L, tile, g + 1, p.wb);
+      group(g, p.wa);
+      wgroup<T>(L, tile, g + 2, p.wa);
+      group(g + 1, p.wb);
     }
     if (g < nfull) {
-      wload(g + 1, wb);
-      group(g, wa);
-      tail(wb);
+      wgroup<T>(L, tile, g + 1, p.wb);
+      group(g, p.wa);
+      tail(p.wb);
     } else {
-      tail(wa);
+      tail(p.wa);
     }
+    // the last pass: the next layer's loads fly during this epilogue, the
+    // barrier and whatever runs before the next product
+    if (pass + 1 == npass) prefetch<T>(next, p);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
-      if (!on[j]) continue;
+      if (tile[j] >= ntl) continue;
 #pragma unroll
       for (int t = 0; t < RT; ++t) epi(t * 16 + lr, tile[j] * 16 + 4 * kc, acc[j][t], bv[j]);
     }
@@ -193,11 +235,12 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Epi
 
 // Forward or input-gradient layer into LDS (see ChainLayer).
 template <typename T, int RT>
-__device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv) {
+__device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe& p,
+                                          const ChainLayer* next) {
   const int N = L.N;
   const bool relu = L.relu != 0, msk = L.mask.pitch > 0;
   const LBuf out = L.out, mk = L.mask;
-  block_mm<T, RT>(s, L, [&](int r, int n, const f32x4& a, const f32x4& b) {
+  block_mm<T, RT>(s, L, p, next, [&](int r, int n, const f32x4& a, const f32x4& b) {
     float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
     if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
 #pragma unroll
@@ -216,10 +259,10 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv) 
 // of gx (block rows below rv).
 template <typename T, int RT>
 __device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float* gx, int64_t ldgx,
-                                       int r0, int rv) {
+                                       int r0, int rv, Pipe& p) {
   const int N = L.N;
   VFL_GLOBAL float* gxg = glb(gx);
-  block_mm<T, RT>(s, L, [&](int r, int n, const f32x4& a, const f32x4&) {
+  block_mm<T, RT>(s, L, p, nullptr, [&](int r, int n, const f32x4& a, const f32x4&) {
     if (r >= rv) return;
     VFL_GLOBAL float* dst = gxg + (int64_t)(r0 + r) * ldgx + n;
     if (n + 4 <= N) {
@@ -241,7 +284,7 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
   const int units = (BR / RR) * ncc;
   VFL_GLOBAL char* g = glb((char*)m.p);
   const int64_t cp = m.cp;
-  for (int u = threadIdx.x; u < units; u += 256) {
+  for (int u = threadIdx.x; u < units; u += kNT) {
     const int rg = u / ncc, cc = u % ncc;
     u32x4 in[RR], out[RR];
 #pragma unroll
@@ -261,7 +304,7 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
   if (!m.p) return;
   const int ncc = (cols + RR - 1) / RR;
   VFL_GLOBAL char* g = glb((char*)m.p);
-  for (int u = threadIdx.x; u < (BR / RR) * ncc * RR; u += 256) {
+  for (int u = threadIdx.x; u < (BR / RR) * ncc * RR; u += kNT) {
     const int rg = u / (ncc * RR), c = u % (ncc * RR);
     *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * m.cp + c) * 16) = u32x4{0u, 0u, 0u, 0u};
   }
@@ -276,7 +319,7 @@ __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, cons
   const int units = (BR / RR) * ncc;
   const VFL_GLOBAL char* g = glb((const char*)m.p);
   const int64_t cp = m.cp;
-  for (int u = threadIdx.x; u < units; u += 256) {
+  for (int u = threadIdx.x; u < units; u += kNT) {
     const int rg = u / ncc, cc = u % ncc;
     u32x4 in[RR], out[RR];
     if (cc * RR < cols) {
@@ -301,7 +344,7 @@ __device__ __forceinline__ void lds_to_rows(const char* s, const LBuf& b, int co
   constexpr int CE = Ch<T>::CE;
   const int nch = (cols + CE - 1) / CE;
   VFL_GLOBAL char* d = glb((char*)dst);
-  for (int u = threadIdx.x; u < rv * nch; u += 256) {
+  for (int u = threadIdx.x; u < rv * nch; u += kNT) {
     const int r = u / nch, ch = u % nch;
     *(VFL_GLOBAL u32x4*)(d + ((int64_t)(r0 + r) * ld + ch * CE) * sizeof(T)) =
         *(const u32x4*)(s + b.off + r * b.pitch + ch * 16);
@@ -320,7 +363,7 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
   const VFL_GLOBAL T* dense = glb((const T*)cc.dense);
   const VFL_GLOBAL int32_t* ids = glb(cc.ids);
   const VFL_GLOBAL float* tab = glb(in.T);
-  for (int u = threadIdx.x; u < BR * nch; u += 256) {
+  for (int u = threadIdx.x; u < BR * nch; u += kNT) {
     const int r = u / nch, ch = u % nch, c0 = ch * CE;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (r < rv && c0 < din) {
@@ -341,7 +384,7 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
           for (int e = 0; e < 4; ++e) v[e] = __float_as_uint(x[e]);
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (uint32_t)f2bf(x[2 * e]) | ((uint32_t)f2bf(x[2 * e + 1]) << 16);
+          for (int e = 0; e < 4; ++e) v[e] = pack_bf16(x[2 * e], x[2 * e + 1]);
         }
       } else {
         float x[CE];
@@ -362,7 +405,7 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
           for (int e = 0; e < 4; ++e) v[e] = __float_as_uint(x[e]);
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (uint32_t)f2bf(x[2 * e]) | ((uint32_t)f2bf(x[2 * e + 1]) << 16);
+          for (int e = 0; e < 4; ++e) v[e] = pack_bf16(x[2 * e], x[2 * e + 1]);
         }
       }
     }
@@ -372,38 +415,53 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
 
 // Per-row clip + noise of an LDS message of D columns (element V) into
 // row-major element-T rows; norm/cfac (nullable) receive ||v|| and the clip
-// factor.  One wavefront per row; the noise is keyed by the row's sample id.
+// factor.  16 lanes per row (4 rows per wavefront at a time), each lane on
+// the 4-column groups cg, cg + 16, ...; the noise is keyed by the row's
+// sample id.
 template <typename T, typename V, int BR>
 __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, const MsgOp& m,
                                          uint32_t step, int64_t sample0, void* out, int64_t ldo,
                                          float* norm, float* cfac, int r0, int rv) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane >> 4, cg = lane & 15;
   const int ngrp = (D + 3) >> 2;
-  for (int r = wave; r < rv; r += 4) {
+  for (int rb = 0; rb < BR; rb += 4 * kNW) {
+    const int r = rb + wave * 4 + sub;
+    if (r >= rv) continue;   // uniform within the row's 16 lanes
     const char* row = s + src.off + r * src.pitch;
     float ss = 0.f;
-    for (int g = lane; g < ngrp; g += 64) {
+    for (int g = cg; g < ngrp; g += 16) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int c = 4 * g + e;
         if (c < D) { const float x = ld1<V>((const V*)row + c); ss += x * x; }
       }
     }
-    const float n = sqrtf(wave_sum(ss));
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o, 64);
+    const float n = sqrtf(ss);
     const float cf = (m.clip && n > m.C) ? m.C / n : 1.f;
-    if (lane == 0) {
+    if (cg == 0) {
       if (norm) glb(norm)[r0 + r] = n;
       if (cfac) glb(cfac)[r0 + r] = cf;
     }
     VFL_GLOBAL T* o = glb((T*)out) + (int64_t)(r0 + r) * ldo;
     const uint32_t grow = (uint32_t)(sample0 + r0 + r);
-    for (int g = lane; g < ngrp; g += 64) {
+    for (int g = cg; g < ngrp; g += 16) {
       float xi[4] = {0.f, 0.f, 0.f, 0.f};
       if (m.noise) gauss4(m.seed, step, grow, (uint32_t)g, m.tag, xi);
+      float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int c = 4 * g + e;
-        if (c < D) st1<T>((T*)(o + c), cf * ld1<V>((const V*)row + c) + m.stdv * xi[e]);
+        v[e] = c < D ? cf * ld1<V>((const V*)row + c) + m.stdv * xi[e] : 0.f;
+      }
+      if (4 * g + 4 <= D) {
+        st4<T>((T*)(o + 4 * g), v);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (4 * g + e < D) st1<T>((T*)(o + 4 * g + e), v[e]);
       }
     }
   }
@@ -411,7 +469,7 @@ __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, 
 
 // ------------------------------------------------------------------ kernels
 template <typename T, int RT>
-__global__ __launch_bounds__(256) void k_fwd(const FwdJob* __restrict__ jp, ChainCall cc,
+__global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, ChainCall cc,
                                              const TickArgs* ta) {
   constexpr int BR = 16 * RT;
   extern __shared__ __attribute__((aligned(16))) char s[];
@@ -424,11 +482,13 @@ __global__ __launch_bounds__(256) void k_fwd(const FwdJob* __restrict__ jp, Chai
   const int r0 = blockIdx.x * BR;
   if (r0 >= k.rows) return;
   const int rv = min(BR, k.rows - r0);
+  Pipe pp;
+  prefetch<T>(&j.l[0], pp);   // overlaps the input rows' loads
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
   __syncthreads();
   if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
   for (int l = 0; l < j.L; ++l) {
-    run_layer<T, RT>(s, j.l[l], rv);
+    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < j.L ? &j.l[l + 1] : nullptr);
     __syncthreads();
     if (j.l[l].rc.p) lds_to_rc<T, BR>(s, j.l[l].out, j.l[l].N, j.l[l].rc, r0);
   }
@@ -440,7 +500,7 @@ __global__ __launch_bounds__(256) void k_fwd(const FwdJob* __restrict__ jp, Chai
 }
 
 template <typename T, int RT>
-__global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp, ChainCall cc,
+__global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp, ChainCall cc,
                                                 const TickArgs* ta) {
   constexpr int BR = 16 * RT;
   constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS;
@@ -466,13 +526,36 @@ __global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp
     return;
   }
   const int rv = min(BR, k.rows - r0);
+  const int Hd = j.ft[j.H - 1].N;
+  // the labels and logit weights, fetched alongside the input rows and
+  // kept in LDS next to the logit reduction scratch
+  float* lwl = (float*)(s + j.red.off) + kNW * (Hd + 2);
+  float* yl = lwl + Hd;
+  float pw[kMaxLogitCols / kNT], py;
+  {
+    const VFL_GLOBAL float* lw = glb(j.lw);
+    const VFL_GLOBAL float* y = glb(cc.labels) + k.in_off + r0;
+#pragma unroll
+    for (int q = 0; q < kMaxLogitCols / kNT; ++q) {
+      const int i = threadIdx.x + kNT * q;
+      pw[q] = i < Hd ? lw[i] : 0.f;
+    }
+    py = (int)threadIdx.x < rv ? y[threadIdx.x] : 0.f;
+  }
+  const float lbias = glb(j.lb)[0];
+  Pipe pp;
+  prefetch<T>(&j.fa[0], pp);
 
   // A's bottom forward; the last layer fills cat[:, 0:dA)
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
+#pragma unroll
+  for (int q = 0; q < kMaxLogitCols / kNT; ++q)
+    if ((int)threadIdx.x + kNT * q < Hd) lwl[threadIdx.x + kNT * q] = pw[q];
+  if ((int)threadIdx.x < BR) yl[threadIdx.x] = py;
   __syncthreads();
   if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
   for (int l = 0; l < j.LA; ++l) {
-    run_layer<T, RT>(s, j.fa[l], rv);
+    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < j.LA ? &j.fa[l + 1] : &j.ft[0]);
     __syncthreads();
     if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
   }
@@ -481,7 +564,7 @@ __global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp
     const int dA = j.dA, dB = j.dB;
     const int nch = ((dA + dB + KS - 1) / KS * KS - dA) / CE;
     const VFL_GLOBAL T* zb = glb((const T*)j.zb);
-    for (int u = threadIdx.x; u < BR * nch; u += 256) {
+    for (int u = threadIdx.x; u < BR * nch; u += kNT) {
       const int r = u / nch, ch = u % nch, c = ch * CE;
       u32x4 v = u32x4{0u, 0u, 0u, 0u};
       if (r < rv && c < dB) v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(zb + (int64_t)(r0 + r) * j.ldzb + c), dB - c);
@@ -492,82 +575,101 @@ __global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp
   if (j.cat_rc.p) lds_to_rc<T, BR>(s, j.cat, j.dA + j.dB, j.cat_rc, r0);
   // top hidden layers
   for (int q = 0; q < j.H; ++q) {
-    run_layer<T, RT>(s, j.ft[q], rv);
+    run_layer<T, RT>(s, j.ft[q], rv, pp, q + 1 < j.H ? &j.ft[q + 1] : (j.H > 1 ? &j.dt[0] : &j.dc));
     __syncthreads();
     if (j.ft[q].rc.p) lds_to_rc<T, BR>(s, j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0);
   }
-  // logit + BCE (Eq. 1): one wavefront per row; dl = sigmoid(l) - y
+  // logit + BCE (Eq. 1), dl = sigmoid(l) - y: 16 lanes per row, 4 rows per
+  // wavefront at a time, each lane on the 4-column groups cg, cg + 16, ...
   {
     const LBuf Hb = j.ft[j.H - 1].out, Db = j.dh;
-    const int Hd = j.ft[j.H - 1].N;
     const int hq = (Hd + KS - 1) / KS * KS / 4;   // 4-column groups to write
-    const VFL_GLOBAL float* y = glb(cc.labels) + k.in_off + r0;
-    const VFL_GLOBAL float* lw = glb(j.lw);
-    float w[2][4], gw[2][4];
+    const int sub = lane >> 4, cg = lane & 15;
+    constexpr int NG = kMaxLogitCols / 64;
+    float gw[NG][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int i = 0; i < NG; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int c = 4 * (lane + 64 * h) + e;
-        w[h][e] = c < Hd ? lw[c] : 0.f;
-        gw[h][e] = 0.f;
-      }
-    const float bias = glb(j.lb)[0];
+      for (int e = 0; e < 4; ++e) gw[i][e] = 0.f;
     float gb = 0.f, ls = 0.f;
-    for (int r = wave; r < BR; r += 4) {
-      float hv[2][4];
+    for (int rb = 0; rb < BR; rb += 4 * kNW) {
+      const int r = rb + wave * 4 + sub;
+      if (r >= BR) continue;   // uniform within the row's 16 lanes
+      const bool ok = r < rv;
+      float hv[NG][4];
       float dot = 0.f;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int q = lane + 64 * h;
-        if (q < hq) ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv[h]);
-        else hv[h][0] = hv[h][1] = hv[h][2] = hv[h][3] = 0.f;
+      for (int i = 0; i < NG; ++i) {
+        const int q = cg + 16 * i;
+        if (q < hq) {
+          ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv[i]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dot += hv[h][e] * w[h][e];
+          for (int e = 0; e < 4; ++e) dot += hv[i][e] * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
+        } else {
+          hv[i][0] = hv[i][1] = hv[i][2] = hv[i][3] = 0.f;
+        }
       }
-      dot = wave_sum(dot);
-      const bool ok = r < rv;
-      const float l = dot + bias;
-      const float yy = ok ? y[r] : 0.f;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) dot += __shfl_xor(dot, o, 64);
+      const float l = dot + lbias;
+      const float yy = ok ? yl[r] : 0.f;
       const float ex = expf(-fabsf(l));
       const float loss = fmaxf(l, 0.f) - yy * l + log1pf(ex);
       const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
       const float dl = ok ? sig - yy : 0.f;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int q = lane + 64 * h;
+      for (int i = 0; i < NG; ++i) {
+        const int q = cg + 16 * i;
         if (q < hq) {
           float d[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            d[e] = dl * w[h][e];
-            if (j.relu_h && !(hv[h][e] > 0.f)) d[e] = 0.f;
-            gw[h][e] += dl * hv[h][e];
+            d[e] = dl * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
+            if (j.relu_h && !(hv[i][e] > 0.f)) d[e] = 0.f;
+            gw[i][e] += dl * hv[i][e];
           }
           st4<T>(lp(s, Db, r, 4 * q * (int)sizeof(T)), d);
         }
       }
       if (ok) { gb += dl; ls += loss; }
     }
-    float* red = (float*)(s + j.red.off);
-    const int W = Hd + 2;
+    // the four rows of a wavefront: lanes 16 and 32 apart
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int i = 0; i < NG; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int c = 4 * (lane + 64 * h) + e;
-        if (c < Hd) red[wave * W + 2 + c] = gw[h][e];
+        gw[i][e] += __shfl_xor(gw[i][e], 16, 64);
+        gw[i][e] += __shfl_xor(gw[i][e], 32, 64);
       }
+    gb += __shfl_xor(gb, 16, 64);
+    gb += __shfl_xor(gb, 32, 64);
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    float* red = (float*)(s + j.red.off);
+    const int W = Hd + 2;
+    if (sub == 0) {
+#pragma unroll
+      for (int i = 0; i < NG; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int c = 4 * (cg + 16 * i) + e;
+          if (c < Hd) red[wave * W + 2 + c] = gw[i][e];
+        }
+    }
     if (lane == 0) { red[wave * W] = ls; red[wave * W + 1] = gb; }
     __syncthreads();
     VFL_GLOBAL float* part = glb(j.part) + (int64_t)blockIdx.x * W;
-    for (int c = threadIdx.x; c < W; c += 256)
-      part[c] = ((red[c] + red[W + c]) + red[2 * W + c]) + red[3 * W + c];
+    for (int c = threadIdx.x; c < W; c += kNT) {
+      float a = 0.f;
+#pragma unroll
+      for (int w = 0; w < kNW; ++w) a += red[w * W + c];
+      part[c] = a;
+    }
   }
   if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[j.H - 1].N, j.dh_rc, r0);
   // top input-gradient chain
   for (int q = 0; q + 1 < j.H; ++q) {
-    run_layer<T, RT>(s, j.dt[q], rv);
+    run_layer<T, RT>(s, j.dt[q], rv, pp, q + 2 < j.H ? &j.dt[q + 1] : &j.dc);
     __syncthreads();
     if (j.dt[q].rc.p) lds_to_rc<T, BR>(s, j.dt[q].out, j.dt[q].N, j.dt[q].rc, r0);
   }
@@ -579,7 +681,8 @@ __global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp
     const bool maskA = j.dc.mask.pitch > 0, gextra = j.gextra != 0;
     VFL_GLOBAL T* ring = glb((T*)j.ring);
     const int64_t ldr = j.ldring;
-    block_mm<T, RT>(s, j.dc, [&](int r, int n, const f32x4& a, const f32x4&) {
+    block_mm<T, RT>(s, j.dc, pp, j.nda > 0 ? &j.da[0] : (j.has_gx ? &j.gx : nullptr),
+                    [&](int r, int n, const f32x4& a, const f32x4&) {
       const bool ok = r < rv;
       if (n + 4 <= dA) {
         float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
@@ -613,15 +716,15 @@ __global__ __launch_bounds__(256) void k_active(const ActiveJob* __restrict__ jp
   }
   // A's input-gradient chain
   for (int q = 0; q < j.nda; ++q) {
-    run_layer<T, RT>(s, j.da[q], rv);
+    run_layer<T, RT>(s, j.da[q], rv, pp, q + 1 < j.nda ? &j.da[q + 1] : (j.has_gx ? &j.gx : nullptr));
     __syncthreads();
     if (j.da[q].rc.p) lds_to_rc<T, BR>(s, j.da[q].out, j.da[q].N, j.da[q].rc, r0);
   }
-  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv);
+  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
 }
 
 template <typename T, int RT>
-__global__ __launch_bounds__(256) void k_bwd(const BwdJob* __restrict__ jp, ChainCall cc,
+__global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, ChainCall cc,
                                              const TickArgs* ta) {
   constexpr int BR = 16 * RT;
   constexpr int KS = Ch<T>::KS;
@@ -637,13 +740,23 @@ __global__ __launch_bounds__(256) void k_bwd(const BwdJob* __restrict__ jp, Chai
     return;
   }
   const int rv = min(BR, k.rows - r0);
+  Pipe pp;
+  if (j.nd > 0) prefetch<T>(&j.dx[0], pp);
+  else if (j.has_gx) prefetch<T>(&j.gx, pp);
+  // the ReLU masks of every layer of the chain, each in an LDS buffer of
+  // its own (stashed activations of this group's forward)
+  for (int q = 0; q < j.nd; ++q)
+    if (j.dx[q].mask_src.p) rc_to_lds<T, BR>(s, j.dx[q].mask, j.dx[q].N, j.dx[q].mask_src, r0);
   // cut-layer backward: through the clip when the row was clipped
   // (d(c v)/dv = c (I - u u^T) with u = v / ||v||), then the ReLU of B's
-  // last layer
+  // last layer; 16 lanes per row, 4 rows per wavefront at a time
   {
     const int D = j.D;
     const int hq = (D + KS - 1) / KS * KS / 4;
-    for (int r = wave; r < BR; r += 4) {
+    const int sub = lane >> 4, cg = lane & 15;
+    for (int rb = 0; rb < BR; rb += 4 * kNW) {
+      const int r = rb + wave * 4 + sub;
+      if (r >= BR) continue;   // uniform within the row's 16 lanes
       const bool ok = r < rv;
       const int64_t row = r0 + r;
       const VFL_GLOBAL T* G = glb((const T*)j.g) + row * j.ldg;
@@ -653,22 +766,29 @@ __global__ __launch_bounds__(256) void k_bwd(const BwdJob* __restrict__ jp, Chai
       if (clipped) {
         inv = 1.f / glb(j.norm)[row];
         cf = glb(j.cfac)[row];
-        for (int c = lane; c < D; c += 64) dot += ld1<T>((const T*)(Z + c)) * inv * ld1<T>((const T*)(G + c));
-        dot = wave_sum(dot);
+        for (int q = cg; 4 * q < D; q += 16)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * q + e < D) dot += ld1<T>((const T*)(Z + 4 * q + e)) * inv * ld1<T>((const T*)(G + 4 * q + e));
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) dot += __shfl_xor(dot, o, 64);
       }
-      for (int q = lane; q < hq; q += 64) {
-        float v[4];
+      for (int q = cg; q < hq; q += 16) {
+        float gv[4] = {0.f, 0.f, 0.f, 0.f}, zv[4] = {0.f, 0.f, 0.f, 0.f}, v[4];
+        if (ok && 4 * q + 4 <= D) {
+          ld4<T>((const T*)(G + 4 * q), gv);
+          ld4<T>((const T*)(Z + 4 * q), zv);
+        } else if (ok) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * q + e < D) { gv[e] = ld1<T>((const T*)(G + 4 * q + e)); zv[e] = ld1<T>((const T*)(Z + 4 * q + e)); }
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int c = 4 * q + e;
-          float g = 0.f;
-          if (ok && c < D) {
-            const float z = ld1<T>((const T*)(Z + c));
-            g = ld1<T>((const T*)(G + c));
-            if (clipped) g = cf * (g - z * inv * dot);
-            if (j.relu && !(z > 0.f)) g = 0.f;
-          }
-          v[e] = g;
+          float g = gv[e];
+          if (clipped) g = cf * (g - zv[e] * inv * dot);
+          if (j.relu && !(zv[e] > 0.f)) g = 0.f;
+          v[e] = (ok && 4 * q + e < D) ? g : 0.f;
         }
         st4<T>(lp(s, j.d, r, 4 * q * (int)sizeof(T)), v);
       }
@@ -678,15 +798,11 @@ __global__ __launch_bounds__(256) void k_bwd(const BwdJob* __restrict__ jp, Chai
   if (j.d_rc.p) lds_to_rc<T, BR>(s, j.d, j.D, j.d_rc, r0);
   for (int q = 0; q < j.nd; ++q) {
     const ChainLayer& L = j.dx[q];
-    if (L.mask_src.p) {
-      rc_to_lds<T, BR>(s, L.mask, L.N, L.mask_src, r0);
-      __syncthreads();
-    }
-    run_layer<T, RT>(s, L, rv);
+    run_layer<T, RT>(s, L, rv, pp, q + 1 < j.nd ? &j.dx[q + 1] : (j.has_gx ? &j.gx : nullptr));
     __syncthreads();
     if (L.rc.p) lds_to_rc<T, BR>(s, L.out, L.N, L.rc, r0);
   }
-  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv);
+  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
 }
 
 template <typename K>
@@ -714,21 +830,21 @@ hipError_t raise_lds(K kernel) {
 hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
                       const TickArgs* ta, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
   return hipGetLastError();
 }
 
 hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
                          const ChainCall& c, const TickArgs* ta, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
                       const TickArgs* ta, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(256), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
   return hipGetLastError();
 }
 

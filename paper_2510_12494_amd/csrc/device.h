@@ -13,6 +13,8 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 
 // Global-memory view of a pointer read from a job descriptor: without it
 // the compiler emits flat accesses, which wait on both the vector-memory and
@@ -25,12 +27,10 @@ __device__ __forceinline__ const VFL_GLOBAL T* glb(const T* p) { return (const V
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// float -> bf16, round to nearest even (NaN stays NaN)
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// two floats -> packed bf16 (low half first), round to nearest even: one
+// v_cvt_pk_bf16_f32 on gfx950
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
 }
 
 template <typename T>
@@ -42,7 +42,7 @@ __device__ __forceinline__ float ld1(const T* p) {
 template <typename T>
 __device__ __forceinline__ void st1(T* p, float v) {
   if constexpr (sizeof(T) == 4) *p = v;
-  else *p = f2bf(v);
+  else *p = (uint16_t)pack_bf16(v, 0.f);
 }
 
 // four consecutive elements (8 bytes of bf16 or 16 bytes of float32)
@@ -64,8 +64,8 @@ __device__ __forceinline__ void st4(void* p, const float (&v)[4]) {
     *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
   } else {
     u32x2 x;
-    x[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-    x[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    x[0] = pack_bf16(v[0], v[1]);
+    x[1] = pack_bf16(v[2], v[3]);
     *(u32x2*)p = x;
   }
 }
@@ -85,6 +85,19 @@ __device__ __forceinline__ u32x4 mask_tail(u32x4 v, int valid) {
     }
   }
   return v;
+}
+
+// Packed MFMA operand of a chain product [N x K]: stored fragment by
+// fragment, fragment (tile, ks) = rows 16*tile .. +16, columns KS*ks .. +KS
+// (KS = 4 * CE: one MFMA step), lane l holding row 16*tile + l % 16 and
+// columns KS*ks + CE*(l / 16) .. +CE in 16 bytes, fragments of a tile
+// consecutive in ks; kst = steps per tile.  A wavefront's fragment load is
+// then one contiguous 1 KB block.  Element index of (n, k):
+template <typename T>
+__device__ __forceinline__ int64_t pk_index(int n, int k, int kst) {
+  constexpr int CE = 16 / (int)sizeof(T), KS = 4 * CE;
+  const int lane = (n & 15) + 16 * ((k % KS) / CE);
+  return ((((int64_t)(n >> 4) * kst + k / KS) * 64 + lane) * CE) + k % CE;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

@@ -30,8 +30,8 @@ __device__ __forceinline__ void sgd_store(const DwProb& P, int n, int k, float g
   VFL_GLOBAL float* W = glb(P.W);
   const float w = W[idx] - scale * g;
   W[idx] = w;
-  if (P.Wq) st1<T>((T*)(glb((T*)P.Wq) + (int64_t)n * P.ldq + k), w);
-  if (P.Wtq) st1<T>((T*)(glb((T*)P.Wtq) + (int64_t)k * P.ldt + n), w);
+  if (P.Wq) st1<T>((T*)(glb((T*)P.Wq) + pk_index<T>(n, k, P.kq)), w);
+  if (P.Wtq) st1<T>((T*)(glb((T*)P.Wtq) + pk_index<T>(k, n, P.kt)), w);
 }
 
 template <typename T>

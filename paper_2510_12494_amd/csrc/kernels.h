@@ -13,8 +13,9 @@
 //             rows split into chunks; SGD fused when a layer is unsplit;
 //   k_dw_reduce  split chunks and the logit layer's block partials summed
 //             in a fixed order, SGD, weight operand copies refreshed.
-// The three chain kernels give each workgroup a block of BR = 16 * RT rows
-// and keep the block's activations and deltas in LDS from layer to layer:
+// The three chain kernels give each workgroup (kChainWaves wavefronts) a
+// block of BR = 16 * RT rows and keep the block's activations and deltas in
+// LDS from layer to layer:
 // only the tensors a later kernel reads go to HBM.  Those that the weight
 // gradient contracts over rows are written in the row-chunked layout below.
 //
@@ -40,6 +41,7 @@ constexpr int kMaxChain = 8;          // layers per chain (bottom or top)
 constexpr int kMaxDw = 8;             // weight-gradient problems per launch
 constexpr int kMaxLogitCols = 512;    // widest last hidden layer of the top model
 constexpr int kLdsMax = 160 * 1024;   // LDS of one gfx950 workgroup
+constexpr int kChainWaves = 8;        // wavefronts per chain-kernel block
 
 // Per-tick values that a replayed graph reads from device memory; k_advance
 // writes them at the start of each stream's part of a tick.  With a tick
@@ -81,8 +83,9 @@ struct LBuf { int32_t off = 0, pitch = 0; };
 // RC-layout global matrix (null p: not written).
 struct RCMat { void* p = nullptr; int32_t cp = 0, pad = 0; };
 
-// One product of a row block with a weight operand W [N x ldw] (element
-// type, row-major, ldw a multiple of 8, columns K .. ldw-1 zero):
+// One product of a row block with a weight operand W [N x K] (element type,
+// packed: see pk_index; kst = K steps of the packing, tiles up to N rounded
+// up to the MFMA depth, padding zero):
 // out[r][n] = sum_k in[r][k] * W[n][k], n < N, then
 //   forward:         + bias[n] (bias set), ReLU when relu;
 //   input gradient:  * (mask[r][n] > 0) when mask.pitch > 0.
@@ -92,7 +95,7 @@ struct RCMat { void* p = nullptr; int32_t cp = 0, pad = 0; };
 struct ChainLayer {
   const void* W = nullptr;
   const float* bias = nullptr;
-  int32_t ldw = 0, N = 0, K = 0, relu = 0;
+  int32_t kst = 0, N = 0, K = 0, relu = 0;
   LBuf in, out, mask;
   RCMat rc, mask_src;
 };
@@ -216,8 +219,9 @@ hipError_t chain_init();
 // --------------------------------------------------------- weight gradients
 // One layer's weight gradient over the group's rows from RC operands:
 // G[n][k] = sum_r D[r][n] X[r][k], g_b[n] = sum_r D[r][n]; W -= scale * G,
-// bias -= scale * g_b, then the operand copies Wq [N x ldq] and Wtq
-// [K x ldt] (nullable) are rewritten from the new W.  Rows are cut into
+// bias -= scale * g_b, then the packed operand copies Wq of W (kq steps)
+// and Wtq of W^T (kt steps; both nullable) are rewritten from the new W.
+// Rows are cut into
 // `splits` chunks of rps rows (a multiple of 128); with more than one chunk
 // each block writes float32 partials part[s][n][kp] (kp = K rounded up to
 // 4) and partb[s][n], and k_dw_reduce finishes the layer.  Blocks
@@ -226,7 +230,7 @@ struct DwProb {
   RCMat D, X;
   float* W = nullptr; float* bias = nullptr;
   void* Wq = nullptr; void* Wtq = nullptr;
-  int32_t ldq = 0, ldt = 0;
+  int32_t kq = 0, kt = 0;
   float* part = nullptr; float* partb = nullptr;
   int32_t N = 0, K = 0, kp = 0, splits = 1, rps = 0, first_block = 0;
 };
@@ -248,10 +252,11 @@ hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float sc
                             float* loss_out, const TickArgs* ta, float* loss_base, hipStream_t st);
 
 // ---------------------------------------------------------------- others
-// Operand copies of one layer's float32 weight W [out x in]:
-// Wq [out x ldq] and Wtq [in x ldt] of element type e (ldq, ldt padded).
+// Operand copies of one layer's float32 weight W [out x in], element type
+// e, packed (pk_index): Wq of W (kq = K steps over `in`), Wtq of W^T (kt =
+// steps over `out`).
 struct CastJob {
-  const float* W; void* Wq; void* Wtq; int out, in; int64_t ldq, ldt;
+  const float* W; void* Wq; void* Wtq; int out, in; int kq, kt;
 };
 hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
 

@@ -23,8 +23,8 @@ __global__ __launch_bounds__(256) void k_cast(CastJobs js) {
   for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
     const int o = (int)(i / j.in), k = (int)(i % j.in);
     const float w = j.W[i];
-    st1<T>(Wq + (int64_t)o * j.ldq + k, w);
-    st1<T>(Wt + (int64_t)k * j.ldt + o, w);
+    st1<T>(Wq + pk_index<T>(o, k, j.kq), w);
+    st1<T>(Wt + pk_index<T>(k, o, j.kt), w);
   }
 }
 
