@@ -190,7 +190,8 @@ def main():
                    "bottom_B": "-".join(map(str, [w.B.d_in] + w.B.widths)),
                    "top": "-".join(map(str, [w.top_in] + w.top.widths)), "lr": w.lr},
         "roofline": roof,
-        "kernel_classes_us_per_step_probe": {k: 1e3 * v[0] / cyc for k, v in probe.items() if v[1]},
+        "kernel_classes_us_per_step_probe": {k: 1e3 * v[0] / (cyc // V.VFL_TIMED_EVERY)
+                                             for k, v in probe.items() if v[1]},
         "graph_ticks": cyc,
         "last_loss": float(losses[0]),
     }

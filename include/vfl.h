@@ -266,7 +266,9 @@ typedef enum {
 
 /* Measurement hook: while class_mask is non-zero, every launch of a
  * selected class is bracketed by two HIP events on its own stream (this adds
- * two event records per launch and nothing else).  vfl_timing_read
+ * two event records per launch and nothing else); in vfl_run's replayed
+ * graphs, the launches of every fourth tick of the captured cycle, and
+ * vfl_timing_read then reports those of the last replay.  vfl_timing_read
  * synchronises both streams and returns, for one class, the summed kernel
  * durations in milliseconds, the number of launches and the summed
  * algorithmic work (matrix-product FLOPs for the first four classes, bytes

@@ -42,6 +42,7 @@ constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
 constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
 constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
 constexpr int kDwRows = 128;          // rows of one k_dw load group (4 MFMA steps of bf16)
+constexpr int kTimedEvery = 4;        // ticks of a captured cycle between timed ticks
 
 int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
 
@@ -126,8 +127,7 @@ struct Plan {
   size_t cat_rc = 0;
   size_t ring_g[kMaxSlots]{};
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
-  size_t ta_a = 0, ta_bf = 0, ta_bb = 0;   // tick records (graph replay)
-  size_t ctr = 0;                     // int64 tick counters of streams A and B
+  size_t tsrc = 0;                    // TickSrc of the replayed graphs
   size_t job_fwd = 0, job_act = 0, job_bwd = 0, job_dwa = 0, job_dwb = 0;
   KMeta kf, ka, kb;
   FwdLds lf;
@@ -196,6 +196,7 @@ struct vfl_ctx {
   uint32_t graph_mask[kMaxSlots]{};
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int capture_phase = -1;             // >= 0 while capturing that phase's graph
+  int capture_tick = -1;              // tick of the cycle being captured
   struct GPair { hipEvent_t e0, e1; int cls; double work; };
   std::vector<GPair> gpairs[kMaxSlots];   // created before capture
   int gused[kMaxSlots]{};                 // pairs used by the captured graph
@@ -276,9 +277,8 @@ void plan_act_lds(const Plan& p, int BR, bool gextra, ActLds& a) {
   a.P[0] = l.take(w, es);
   a.P[1] = l.take(w, es);
   if (gextra) a.msg = l.take(p.dB, 4);
-  // logit reduction scratch [wavefronts][Hd + 2], logit weights [Hd], the
-  // block's labels [BR]
-  a.red = l.raw(4 * (kChainWaves * (p.T.out[p.T.H - 1] + 2) + p.T.out[p.T.H - 1] + BR));
+  // logit weights [Hd], the block's labels, dl and loss [BR each]
+  a.red = l.raw(4 * (p.T.out[p.T.H - 1] + 3 * BR));
   a.bytes = l.off;
 }
 
@@ -436,10 +436,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   // messages and control
   for (int q = 0; q <= p.s; ++q) p.ring_g[q] = ly.take((size_t)es * R * ld_of(p.dB));
   p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
-  p.ta_a = ly.take(sizeof(TickArgs));
-  p.ta_bf = ly.take(sizeof(TickArgs));
-  p.ta_bb = ly.take(sizeof(TickArgs));
-  p.ctr = ly.take(2 * sizeof(int64_t));
+  p.tsrc = ly.take(sizeof(TickSrc));
 
   // weight gradients: row chunks, partials, block counts
   int tiles_a = 0, tiles_b = 0;
@@ -716,7 +713,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     if (aj[q].has_gx) ok = ok && layer_fits(p, aj[q].gx, ba, p.ka.lds, false);
     for (int l = 0; l < bj[q].nd; ++l) ok = ok && layer_fits(p, bj[q].dx[l], bb, p.kb.lds, true);
     if (bj[q].has_gx) ok = ok && layer_fits(p, bj[q].gx, bb, p.kb.lds, false);
-    ok = ok && p.la.red.off + 4 * ((kChainWaves + 1) * p.T.out[p.T.H - 1] + 2 * kChainWaves + ba) <= p.ka.lds;
+    ok = ok && p.la.red.off + 4 * (p.T.out[p.T.H - 1] + 3 * ba) <= p.ka.lds;
     if (!ok) return "internal: chain layout does not cover a layer";
   }
   return "";
@@ -827,7 +824,10 @@ int tbegin(vfl_ctx* c, int cls, double work, hipStream_t st) {
   if (!((T.mask >> cls) & 1u)) return -1;
   if (c->capture_phase >= 0) {
     // inside a captured graph: an event pair of its own (created before the
-    // capture), recorded as graph nodes, read after the graph's last replay
+    // capture), recorded as graph nodes, read after the graph's last replay;
+    // only every kTimedEvery-th tick of the cycle is timed (each pair adds
+    // two nodes that the host launches with every replay)
+    if (c->capture_tick % kTimedEvery != 0) return -1;
     const int ph = c->capture_phase;
     if (c->gused[ph] >= (int)c->gpairs[ph].size()) return -1;
     vfl_ctx::GPair& gp = c->gpairs[ph][c->gused[ph]];
@@ -864,9 +864,9 @@ void tend(vfl_ctx* c, int i, hipStream_t st) {
 double mm_flops(int R, int N, int K) { return 2.0 * R * (double)N * K; }
 
 // ------------------------------------------------------------ enqueue steps
-// Every enqueue function below takes an optional tick record `ta`: null when
-// the call's values are known on the host (the per-call API), the device
-// record of the stream when the work is captured into a replayed graph.
+// Every enqueue function below takes a tick reference `tr`: null (src) when
+// the call's values are known on the host (the per-call API), the tick of a
+// captured launch when the work is captured into a replayed graph.
 vfl_status enqueue_cast(vfl_ctx* c, const Party& P, int slot, const Top* T, hipStream_t st) {
   CastJob jobs[2 * VFL_MAX_LAYERS + 2];
   int n = 0;
@@ -907,17 +907,17 @@ double party_dx_flops(const Party& P, int R) {
 
 // sparse SGD of a party's tables from its float32 input gradient gx
 vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const int32_t* ids, int R, float scale,
-                             hipStream_t st, const TickArgs* ta) {
+                             hipStream_t st, TickRef tr) {
   if (!P.spec.n_cat) return VFL_OK;
   ScatterJob sj{at<float>(c, P.T), ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                at<float>(c, P.gx), P.ldgx, R, scale, ta};
+                at<float>(c, P.gx), P.ldgx, R, scale, tr};
   TIMED(VFL_K_EMB_SGD, (double)R * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
         launch_scatter_sgd(sj, st));
   return VFL_OK;
 }
 
 // one party's weight gradients + SGD (+ the logit layer and loss for A)
-vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, const TickArgs* ta,
+vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, TickRef tr,
                       hipStream_t st) {
   const Plan& p = c->p;
   const DwMeta& m = party_a ? p.da : p.db;
@@ -930,7 +930,7 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, co
   } else {
     flops += party_fwd_flops(p.P, R);
   }
-  TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, ta, st));
+  TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
   const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);
   if (blocks > 0) {
     double bytes = 0;
@@ -943,7 +943,7 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, co
     }
     if (party_a) bytes += 4.0 * p.ka.blocks * (p.T.out[p.T.H - 1] + 2);
     TIMED(VFL_K_REDUCE, bytes, st,
-          launch_dw_reduce(p.e, job, blocks, R, scale, ta ? nullptr : loss, ta, ta ? loss : nullptr, st));
+          launch_dw_reduce(p.e, job, blocks, R, scale, tr.src ? nullptr : loss, tr, tr.src ? loss : nullptr, st));
   }
   return VFL_OK;
 }
@@ -951,12 +951,12 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, co
 // ---- the phases of a tick (enqueue only; the callers keep the host state)
 
 // B's forward + publish of `st` (group st.group) into `slot`.
-vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, const TickArgs* ta) {
+vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, TickRef tr) {
   const Plan& p = c->p;
   const int32_t hdr[3] = {(int32_t)st.group, (int32_t)st.group, (int32_t)st.version};
   const ChainCall k = call_of(st, st.group, hdr, 0);
   TIMED(VFL_K_FWD, party_fwd_flops(p.P, p.R), c->sb,
-        launch_fwd(p.e, p.kf.rt, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k, ta, c->sb));
+        launch_fwd(p.e, p.kf.rt, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k, tr, c->sb));
   return VFL_OK;
 }
 
@@ -969,7 +969,7 @@ vfl_status b_publish(vfl_ctx* c, int slot) {
 // (A's batch in `st`) against embedding slot `slot`; gradient message +
 // event.
 vfl_status a_top(vfl_ctx* c, int64_t group, int slot, const SlotState& st, int32_t b_version,
-                 const TickArgs* ta, bool wait_emb = true) {
+                 TickRef tr, bool wait_emb = true) {
   const Plan& p = c->p;
   if (wait_emb) HIPCHK(hipStreamWaitEvent(c->sa, c->ev_emb[slot], 0));
   const int32_t hdr[3] = {(int32_t)group, (int32_t)(group + p.s), b_version};
@@ -980,31 +980,31 @@ vfl_status a_top(vfl_ctx* c, int64_t group, int slot, const SlotState& st, int32
   for (int j = 1; j < p.T.H; ++j) f += mm_flops(R, p.T.in[j], p.T.out[j]);
   TIMED(VFL_K_ACTIVE, f, c->sa,
         launch_active(p.e, p.ka.rt, (const ActiveJob*)(c->ws + p.job_act) + slot, p.ka.lds, p.ka.blocks, k,
-                      ta, c->sa));
+                      tr, c->sa));
   HIPCHK(hipEventRecord(c->ev_grad[slot], c->sa));
   return VFL_OK;
 }
 
 // A's and the top model's SGD for A's group (rows R).
-vfl_status a_backward(vfl_ctx* c, const SlotState& st, float* loss, const TickArgs* ta) {
+vfl_status a_backward(vfl_ctx* c, const SlotState& st, float* loss, TickRef tr) {
   const Plan& p = c->p;
-  vfl_status r = enqueue_dw(c, true, 0, st.rows, loss, ta, c->sa);
+  vfl_status r = enqueue_dw(c, true, 0, st.rows, loss, tr, c->sa);
   if (r) return r;
-  return enqueue_table_sgd(c, p.A, st.ids, st.rows, c->o.lr / (float)st.rows, c->sa, ta);
+  return enqueue_table_sgd(c, p.A, st.ids, st.rows, c->o.lr / (float)st.rows, c->sa, tr);
 }
 
 // B's delayed backward of the group stashed in `slot` + SGD on B's current
 // weights; the refreshed operand copies go to this slot, which B's next
 // forward uses.
-vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, const TickArgs* ta) {
+vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, TickRef tr) {
   const Plan& p = c->p;
   HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
   const ChainCall k = call_of(st, group, nullptr, group);
   TIMED(VFL_K_BWD, party_dx_flops(p.P, p.R), c->sb,
-        launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, ta, c->sb));
-  vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, ta, c->sb);
+        launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
+  vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, tr, c->sb);
   if (r) return r;
-  return enqueue_table_sgd(c, p.P, st.ids, st.rows, c->o.lr / (float)st.rows, c->sb, ta);
+  return enqueue_table_sgd(c, p.P, st.ids, st.rows, c->o.lr / (float)st.rows, c->sb, tr);
 }
 
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
@@ -1179,7 +1179,7 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
       if ((r = enqueue_cast(c, p.P, slot, nullptr, c->sb))) return r;
       c->b_copy_version[slot] = c->b_version;
     }
-    if ((r = b_forward(c, slot, st, nullptr))) return r;
+    if ((r = b_forward(c, slot, st, TickRef()))) return r;
     c->bslot[slot] = st;
     c->b_next_fwd = group + 1;
     return VFL_OK;
@@ -1227,7 +1227,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev) {
     if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
     c->a_copy_version = c->a_version;
   }
-  if ((r = a_top(c, group, slot, c->aslot, (int32_t)bs.version, nullptr))) return r;
+  if ((r = a_top(c, group, slot, c->aslot, (int32_t)bs.version, TickRef()))) return r;
   c->grad_group[slot] = group;
   c->grad_rows[slot] = c->aslot.rows;
   c->a_loss = loss_dev;
@@ -1241,7 +1241,7 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
   if (party == VFL_PARTY_A) {
     if (group != c->a_next || c->a_phase != 2)
       return fail(c, VFL_E_STATE, "A's backward must follow its top step");
-    vfl_status r = a_backward(c, c->aslot, c->a_loss, nullptr);
+    vfl_status r = a_backward(c, c->aslot, c->a_loss, TickRef());
     if (r) return r;
     c->a_version += 1;
     c->a_copy_version = c->a_version;
@@ -1254,7 +1254,7 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     const int slot = (int)(group % (p.s + 1));
     if (c->grad_group[slot] != group || c->bslot[slot].group != group)
       return fail(c, VFL_E_NOT_READY, "gradient of this group not published");
-    vfl_status r = b_backward(c, slot, c->bslot[slot], group, nullptr);
+    vfl_status r = b_backward(c, slot, c->bslot[slot], group, TickRef());
     if (r) return r;
     c->b_next_bwd = group + 1;
     c->b_version += 1;
@@ -1356,19 +1356,10 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
           HIPCHK(hipEventCreate(&gp.e1));
         }
       }
-      // capture cyc ticks starting at this phase; the tick records and
-      // counters make the graph independent of the absolute tick
-      TickArgs* ta_a = at<TickArgs>(c, p.ta_a);
-      TickArgs* ta_bf = at<TickArgs>(c, p.ta_bf);
-      TickArgs* ta_bb = at<TickArgs>(c, p.ta_bb);
-      int64_t* ctr = at<int64_t>(c, p.ctr);
-      AdvanceJob adv_a, adv_b;
-      adv_a.counter = ctr; adv_a.out[0] = ta_a; adv_a.kind = 0;
-      adv_b.counter = ctr + 1; adv_b.out[0] = ta_bf; adv_b.out[1] = ta_bb; adv_b.kind = 1;
-      for (AdvanceJob* aj : {&adv_a, &adv_b}) {
-        aj->n_rows = c->n_rows; aj->R = p.R; aj->s = s; aj->lr = c->o.lr;
-        aj->loss_len = loss_ring ? loss_len : 1;
-      }
+      // capture cyc ticks starting at this phase; launches refer to tick
+      // base + i of the replay, so the graph is independent of the
+      // absolute tick, and its last node advances the base by cyc
+      TickSrc* tsrc = at<TickSrc>(c, p.tsrc);
       // dataset bases: the tick records supply rows, row0 and the headers
       SlotState sa_in, sb_in;
       sa_in.rows = p.R; sa_in.dense = c->ds_a.dense; sa_in.ld = c->ds_a.ld; sa_in.ids = c->ds_a.ids;
@@ -1383,20 +1374,21 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
       for (int i = 0; i < cyc && he == hipSuccess && r == VFL_OK; ++i) {
         const int fs = (phase + i) % S1;             // slot of group t
         const int us = ((phase + i - s) % S1 + S1) % S1;   // slot of group t - s
-        he = launch_advance(adv_b, c->sb);
-        if (he == hipSuccess) he = launch_advance(adv_a, c->sa);
-        if (he != hipSuccess) break;
-        if ((r = b_forward(c, fs, sb_in, ta_bf))) break;
+        const TickRef tb{tsrc, i, 0}, ta{tsrc, i, 1}, tu{tsrc, i, 2};
+        c->capture_tick = i;
+        if ((r = b_forward(c, fs, sb_in, tb))) break;
         if ((r = b_publish(c, fs))) break;
         // the first s ticks consume groups published before this graph;
         // replays of a graph on one stream never overlap, so the publish
         // of those groups is already complete
-        if ((r = a_top(c, 0, us, sa_in, 0, ta_a, i >= s))) break;
-        if ((r = a_backward(c, sa_in, loss_ring, ta_a))) break;
-        if ((r = b_backward(c, us, sb_in, 0, ta_bb))) break;
+        if ((r = a_top(c, 0, us, sa_in, 0, ta, i >= s))) break;
+        if ((r = a_backward(c, sa_in, loss_ring, ta))) break;
+        if ((r = b_backward(c, us, sb_in, 0, tu))) break;
       }
+      c->capture_tick = -1;
       if (he == hipSuccess && r == VFL_OK) he = hipEventRecord(c->ev_join, c->sb);
       if (he == hipSuccess && r == VFL_OK) he = hipStreamWaitEvent(c->sa, c->ev_join, 0);
+      if (he == hipSuccess && r == VFL_OK) he = launch_tick_base(tsrc, cyc, c->sa);
       hipGraph_t g = nullptr;
       const hipError_t he2 = hipStreamEndCapture(c->sa, &g);
       c->capture_phase = -1;
@@ -1418,9 +1410,11 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
       c->graph_loss_len[phase] = loss_len;
       c->graph_mask[phase] = mask;
     }
-    // both counters start at t0; the graph's advance kernels read them
-    const int64_t ctr_h[2] = {t0, t0};
-    HIPCHK(hipMemcpyAsync(at<int64_t>(c, p.ctr), ctr_h, sizeof(ctr_h), hipMemcpyHostToDevice, c->sa));
+    // the replays start at tick t0 (the dataset and schedule constants with it)
+    TickSrc src;
+    src.base = t0; src.n_rows = c->n_rows; src.R = p.R; src.s = s; src.lr = c->o.lr;
+    src.loss_len = loss_ring ? loss_len : 1;
+    HIPCHK(hipMemcpyAsync(at<TickSrc>(c, p.tsrc), &src, sizeof(src), hipMemcpyHostToDevice, c->sa));
     // the graph runs both parties' work from stream A: it must follow the
     // work already enqueued on stream B
     HIPCHK(hipEventRecord(c->ev_fork, c->sb));

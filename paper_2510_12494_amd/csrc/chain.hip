@@ -44,12 +44,13 @@ struct Call {
   int32_t hdr[3];
 };
 
-__device__ __forceinline__ Call resolve(const ChainCall& c, const TickArgs* ta) {
+__device__ __forceinline__ Call resolve(const ChainCall& c, const TickRef& tr) {
   Call k;
-  if (ta) {
-    k.rows = ta->rows; k.group = ta->group; k.chk = ta->chk;
-    k.row0 = ta->row0; k.in_off = ta->row0;
-    k.hdr[0] = ta->hdr[0]; k.hdr[1] = ta->hdr[1]; k.hdr[2] = ta->hdr[2];
+  if (tr.src) {
+    const TickArgs ta = tick_args(tr);
+    k.rows = ta.rows; k.group = ta.group; k.chk = ta.chk;
+    k.row0 = ta.row0; k.in_off = ta.row0;
+    k.hdr[0] = ta.hdr[0]; k.hdr[1] = ta.hdr[1]; k.hdr[2] = ta.hdr[2];
   } else {
     k.rows = c.rows; k.group = c.group; k.chk = c.chk;
     k.row0 = c.row0; k.in_off = 0;
@@ -470,11 +471,11 @@ __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, 
 // ------------------------------------------------------------------ kernels
 template <typename T, int RT>
 __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, ChainCall cc,
-                                             const TickArgs* ta) {
+                                             TickRef tr) {
   constexpr int BR = 16 * RT;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const FwdJob& j = *jp;
-  const Call k = resolve(cc, ta);
+  const Call k = resolve(cc, tr);
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_out) {
     VFL_GLOBAL int32_t* h = glb(j.hdr_out);
     h[0] = k.hdr[0]; h[1] = k.hdr[1]; h[2] = k.hdr[2];
@@ -501,12 +502,12 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
 
 template <typename T, int RT>
 __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp, ChainCall cc,
-                                                const TickArgs* ta) {
+                                                TickRef tr) {
   constexpr int BR = 16 * RT;
   constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const ActiveJob& j = *jp;
-  const Call k = resolve(cc, ta);
+  const Call k = resolve(cc, tr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     if (j.hdr_chk && glb(j.hdr_chk)[0] != k.chk) atomicAdd(j.err, 1);
@@ -529,7 +530,7 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   const int Hd = j.ft[j.H - 1].N;
   // the labels and logit weights, fetched alongside the input rows and
   // kept in LDS next to the logit reduction scratch
-  float* lwl = (float*)(s + j.red.off) + kNW * (Hd + 2);
+  float* lwl = (float*)(s + j.red.off);
   float* yl = lwl + Hd;
   float pw[kMaxLogitCols / kNT], py;
   {
@@ -580,34 +581,24 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     if (j.ft[q].rc.p) lds_to_rc<T, BR>(s, j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0);
   }
   // logit + BCE (Eq. 1), dl = sigmoid(l) - y: 16 lanes per row, 4 rows per
-  // wavefront at a time, each lane on the 4-column groups cg, cg + 16, ...
+  // wavefront at a time, each lane on the 4-column groups cg, cg + 16, ...;
+  // the rows' dl and loss go to LDS
+  float* dlv = yl + BR;
+  float* lsv = dlv + BR;
   {
     const LBuf Hb = j.ft[j.H - 1].out, Db = j.dh;
     const int hq = (Hd + KS - 1) / KS * KS / 4;   // 4-column groups to write
     const int sub = lane >> 4, cg = lane & 15;
-    constexpr int NG = kMaxLogitCols / 64;
-    float gw[NG][4];
-#pragma unroll
-    for (int i = 0; i < NG; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) gw[i][e] = 0.f;
-    float gb = 0.f, ls = 0.f;
     for (int rb = 0; rb < BR; rb += 4 * kNW) {
       const int r = rb + wave * 4 + sub;
       if (r >= BR) continue;   // uniform within the row's 16 lanes
       const bool ok = r < rv;
-      float hv[NG][4];
       float dot = 0.f;
+      for (int q = cg; q < hq; q += 16) {
+        float hv[4];
+        ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv);
 #pragma unroll
-      for (int i = 0; i < NG; ++i) {
-        const int q = cg + 16 * i;
-        if (q < hq) {
-          ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv[i]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) dot += hv[i][e] * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
-        } else {
-          hv[i][0] = hv[i][1] = hv[i][2] = hv[i][3] = 0.f;
-        }
+        for (int e = 0; e < 4; ++e) dot += hv[e] * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
       }
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) dot += __shfl_xor(dot, o, 64);
@@ -617,53 +608,43 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
       const float loss = fmaxf(l, 0.f) - yy * l + log1pf(ex);
       const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
       const float dl = ok ? sig - yy : 0.f;
-#pragma unroll
-      for (int i = 0; i < NG; ++i) {
-        const int q = cg + 16 * i;
-        if (q < hq) {
-          float d[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            d[e] = dl * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
-            if (j.relu_h && !(hv[i][e] > 0.f)) d[e] = 0.f;
-            gw[i][e] += dl * hv[i][e];
-          }
-          st4<T>(lp(s, Db, r, 4 * q * (int)sizeof(T)), d);
-        }
-      }
-      if (ok) { gb += dl; ls += loss; }
-    }
-    // the four rows of a wavefront: lanes 16 and 32 apart
-#pragma unroll
-    for (int i = 0; i < NG; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        gw[i][e] += __shfl_xor(gw[i][e], 16, 64);
-        gw[i][e] += __shfl_xor(gw[i][e], 32, 64);
-      }
-    gb += __shfl_xor(gb, 16, 64);
-    gb += __shfl_xor(gb, 32, 64);
-    ls += __shfl_xor(ls, 16, 64);
-    ls += __shfl_xor(ls, 32, 64);
-    float* red = (float*)(s + j.red.off);
-    const int W = Hd + 2;
-    if (sub == 0) {
-#pragma unroll
-      for (int i = 0; i < NG; ++i)
+      for (int q = cg; q < hq; q += 16) {
+        float hv[4], d[4];
+        ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int c = 4 * (cg + 16 * i) + e;
-          if (c < Hd) red[wave * W + 2 + c] = gw[i][e];
+          d[e] = dl * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
+          if (j.relu_h && !(hv[e] > 0.f)) d[e] = 0.f;
         }
+        st4<T>(lp(s, Db, r, 4 * q * (int)sizeof(T)), d);
+      }
+      if (cg == 0) {
+        dlv[r] = dl;
+        lsv[r] = ok ? loss : 0.f;
+      }
     }
-    if (lane == 0) { red[wave * W] = ls; red[wave * W + 1] = gb; }
     __syncthreads();
-    VFL_GLOBAL float* part = glb(j.part) + (int64_t)blockIdx.x * W;
-    for (int c = threadIdx.x; c < W; c += kNT) {
-      float a = 0.f;
-#pragma unroll
-      for (int w = 0; w < kNW; ++w) a += red[w * W + c];
-      part[c] = a;
+    // the logit layer's weight gradient over the block's rows, sum_r dl_r
+    // h[r][c]: a float32 MFMA per 16 columns and 4 rows (every output row of
+    // the MFMA gets the same sums), wavefront w on the column tiles w, w+8, ..
+    VFL_GLOBAL float* part = glb(j.part) + (int64_t)blockIdx.x * (Hd + 2);
+    const int kc = lane >> 4, lr = lane & 15;
+    for (int t = wave; t * 16 < Hd; t += kNW) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int c = t * 16 + lr;
+#pragma unroll 4
+      for (int s4 = 0; s4 < BR / 4; ++s4) {
+        const int r = 4 * s4 + kc;
+        const float h = c < Hd ? ld1<T>((const T*)lp(s, Hb, r, 0) + c) : 0.f;
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv[r], h, acc, 0, 0, 0);
+      }
+      if (kc == 0 && c < Hd) part[2 + c] = acc[0];
+    }
+    if (threadIdx.x == 0) {
+      float ls = 0.f, gb = 0.f;
+      for (int r = 0; r < BR; ++r) { ls += lsv[r]; gb += dlv[r]; }
+      part[0] = ls;
+      part[1] = gb;
     }
   }
   if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[j.H - 1].N, j.dh_rc, r0);
@@ -725,12 +706,12 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
 
 template <typename T, int RT>
 __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, ChainCall cc,
-                                             const TickArgs* ta) {
+                                             TickRef tr) {
   constexpr int BR = 16 * RT;
   constexpr int KS = Ch<T>::KS;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const BwdJob& j = *jp;
-  const Call k = resolve(cc, ta);
+  const Call k = resolve(cc, tr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_chk && glb(j.hdr_chk)[0] != k.chk) atomicAdd(j.err, 1);
   const int r0 = blockIdx.x * BR;
@@ -828,23 +809,23 @@ hipError_t raise_lds(K kernel) {
   } while (0)
 
 hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
-                      const TickArgs* ta, hipStream_t st) {
+                      TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
   return hipGetLastError();
 }
 
 hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
-                         const ChainCall& c, const TickArgs* ta, hipStream_t st) {
+                         const ChainCall& c, TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
-                      const TickArgs* ta, hipStream_t st) {
+                      TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, ta);
+  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
   return hipGetLastError();
 }
 

@@ -36,7 +36,7 @@ __device__ __forceinline__ void sgd_store(const DwProb& P, int n, int k, float g
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Rarg, float scale_arg,
-                                            const TickArgs* ta) {
+                                            TickRef tr) {
   constexpr int RR = 16 / (int)sizeof(T);   // rows per chunk
   constexpr int KR = 4 * RR;                // rows per MFMA step
   constexpr int PF = 4;                     // MFMA steps per load group
@@ -49,8 +49,13 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
   const int tiles_k = (P.K + 63) / 64;
   const int tile = lb / P.splits, split = lb % P.splits;
   const int n0 = (tile / tiles_k) * 64, k0 = (tile % tiles_k) * 64;
-  const int R = ta ? ta->rows : Rarg;
-  const float scale = ta ? ta->scale : scale_arg;
+  int R = Rarg;
+  float scale = scale_arg;
+  if (tr.src) {
+    const TickArgs ta = tick_args(tr);
+    R = ta.rows;
+    scale = ta.scale;
+  }
   const int rb = split * P.rps;
   const int re = min(R, rb + P.rps);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -186,10 +191,16 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
 template <typename T>
 __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp, int Rarg,
                                                    float scale_arg, float* loss_out,
-                                                   const TickArgs* ta, float* loss_base) {
+                                                   TickRef tr, float* loss_base) {
   const DwJob& J = *jp;
-  const int R = ta ? ta->rows : Rarg;
-  const float scale = ta ? ta->scale : scale_arg;
+  int R = Rarg;
+  float scale = scale_arg;
+  if (tr.src) {
+    const TickArgs ta = tick_args(tr);
+    R = ta.rows;
+    scale = ta.scale;
+    loss_out = loss_base ? loss_base + ta.loss_idx : nullptr;
+  }
   if ((int)blockIdx.x < J.red_blocks) {
     int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     for (int q = 0; q < J.n; ++q) {
@@ -248,8 +259,7 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
     float tot = 0.f;
     for (int i = 0; i < 64; ++i) tot += red[i][cl];
     if (c == 0) {
-      float* lo = ta ? (loss_base ? loss_base + ta->loss_idx : nullptr) : loss_out;
-      if (lo) *glb(lo) = tot / (float)R;
+      if (loss_out) *glb(loss_out) = tot / (float)R;
     } else if (c == 1) {
       glb(J.lb)[0] -= scale * tot;
     } else {
@@ -260,22 +270,22 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
 
 }  // namespace
 
-hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, const TickArgs* ta,
+hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, TickRef tr,
                      hipStream_t st) {
   if (blocks < 1) return hipErrorInvalidValue;
-  if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, ta);
-  else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, ta);
+  if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
+  else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
   return hipGetLastError();
 }
 
 hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
-                            float* loss_out, const TickArgs* ta, float* loss_base, hipStream_t st) {
+                            float* loss_out, TickRef tr, float* loss_base, hipStream_t st) {
   if (blocks < 1) return hipErrorInvalidValue;
   if (e == BF16)
     hipLaunchKernelGGL(k_dw_reduce<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out,
-                       ta, loss_base);
+                       tr, loss_base);
   else
-    hipLaunchKernelGGL(k_dw_reduce<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out, ta,
+    hipLaunchKernelGGL(k_dw_reduce<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out, tr,
                        loss_base);
   return hipGetLastError();
 }

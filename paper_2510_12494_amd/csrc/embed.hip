@@ -31,10 +31,11 @@ __global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
   const int tid = threadIdx.x;
   const int f = blockIdx.x;
   const int E = j.E;
-  if (j.ta) {
-    j.R = j.ta->rows;
-    j.scale = j.ta->scale;
-    j.ids += j.ta->row0 * j.n_cat;
+  if (j.tr.src) {
+    const TickArgs ta = tick_args(j.tr);
+    j.R = ta.rows;
+    j.scale = ta.scale;
+    j.ids += ta.row0 * j.n_cat;
   }
   float* table = j.T + (int64_t)f * j.V * E;
 

@@ -43,10 +43,9 @@ constexpr int kMaxLogitCols = 512;    // widest last hidden layer of the top mod
 constexpr int kLdsMax = 160 * 1024;   // LDS of one gfx950 workgroup
 constexpr int kChainWaves = 8;        // wavefronts per chain-kernel block
 
-// Per-tick values that a replayed graph reads from device memory; k_advance
-// writes them at the start of each stream's part of a tick.  With a tick
-// record the kernels take the row count, noise step, headers and scale from
-// it and offset the dataset pointers of their call by row0 rows.
+// The values of one tick of the deterministic schedule over a resident
+// dataset of n_rows rows (group g covers rows [(g mod E) * R, ...), E =
+// ceil(n_rows / R), the last group of an epoch short), as a kernel uses them.
 struct TickArgs {
   int32_t rows;        // rows of the batch group
   int32_t group;       // batch-group id (noise step, header sequence)
@@ -54,26 +53,48 @@ struct TickArgs {
   int32_t hdr[3];      // channel header to write {group, tick, version}
   int32_t chk;         // group expected in the header of the slot read
   float scale;         // lr / rows
-  int32_t pad;
   int64_t loss_idx;    // index of the group's loss in the loss ring
 };
 
-// k_advance: one thread reads this stream's tick counter t, writes the
-// records of tick t of the deterministic schedule over a resident dataset
-// of n_rows rows (group g covers rows [(g mod E) * R, ...), E = ceil(n/R),
-// the last group of an epoch short) and increments the counter.
-// Party A (kind 0): out[0] = group t - s.  Party B (kind 1): out[0] =
-// group t (its forward), out[1] = group t - s (its backward).
-struct AdvanceJob {
-  int64_t* counter = nullptr;
-  TickArgs* out[2] = {nullptr, nullptr};
-  int kind = 0;
+// Replayed graphs: a captured launch refers to tick base + off, base being
+// the first tick of the current replay (written before the first replay,
+// advanced by the graph's last node).  role 0: party B publishes group t;
+// role 1: party A consumes group u = t - s; role 2: party B back-propagates
+// u.  A null src means the launch's values are given directly.
+struct TickSrc {
+  int64_t base = 0;
   int64_t n_rows = 0;
-  int R = 0, s = 0;
+  int32_t R = 0, s = 0;
   float lr = 0.f;
+  int32_t pad = 0;
   int64_t loss_len = 1;
 };
-hipError_t launch_advance(const AdvanceJob& j, hipStream_t st);
+struct TickRef {
+  const TickSrc* src = nullptr;
+  int32_t off = 0, role = 0;
+};
+
+__device__ __forceinline__ TickArgs tick_args(const TickRef& r) {
+  const TickSrc& x = *r.src;
+  const int64_t t = x.base + r.off;
+  const int64_t g = r.role == 0 ? t : t - x.s;
+  const int64_t E = (x.n_rows + x.R - 1) / x.R;
+  const int64_t start = (g % E) * x.R;
+  TickArgs a;
+  a.rows = (int32_t)(x.n_rows - start < x.R ? x.n_rows - start : x.R);
+  a.group = (int32_t)g;
+  a.row0 = start;
+  a.chk = (int32_t)g;
+  a.scale = x.lr / (float)a.rows;
+  a.loss_idx = g % x.loss_len;
+  a.hdr[0] = (int32_t)g;
+  a.hdr[1] = (int32_t)t;
+  a.hdr[2] = (int32_t)(g - x.s > 0 ? g - x.s : 0);
+  return a;
+}
+
+// the graph's last node: base += cyc
+hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st);
 
 // ------------------------------------------------------------ chain kernels
 // LDS region of a row block: byte offset in the kernel's dynamic LDS and row
@@ -120,8 +141,9 @@ struct MsgOp {
   uint32_t tag = 0;
 };
 
-// Values of one chain launch (a tick record replaces rows, group, row0 and
-// the headers, and then dense / ids / labels are dataset bases).
+// Values of one chain launch (with a tick reference its tick record replaces
+// rows, group, row0 and the headers, and then dense / ids / labels are
+// dataset bases).
 struct ChainCall {
   const void* dense = nullptr;
   int64_t ld = 0;
@@ -153,7 +175,8 @@ struct FwdJob {
 // first dA columns of `cat`), B's embedding zb into columns [dA, dA + dB) of
 // cat, the top hidden layers ft, logit + BCE into the last hidden delta dh
 // (per-block partials {sum loss, sum dl, sum_r dl * h[r][c]} to
-// part[block]), the top input-gradient chain dt (j = H-1 .. 1), the concat
+// part[block]; `red`: LDS for the logit weights, labels, dl and loss of the
+// block's rows), the top input-gradient chain dt (j = H-1 .. 1), the concat
 // product dc (columns < dA: A's cut delta into dc.out, masked by cat when
 // A's last layer has a ReLU; columns >= dA: the gradient message, staged as
 // float32 in `msg` when clip/noise run, else written to ring directly), and
@@ -208,11 +231,11 @@ struct BwdJob {
 // Jobs live in device memory (written once when the context is created);
 // `rt` selects 16 * rt rows per block, `lds` the dynamic LDS bytes.
 hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
-                      const TickArgs* ta, hipStream_t st);
+                      TickRef tr, hipStream_t st);
 hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
-                         const ChainCall& c, const TickArgs* ta, hipStream_t st);
+                         const ChainCall& c, TickRef tr, hipStream_t st);
 hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
-                      const TickArgs* ta, hipStream_t st);
+                      TickRef tr, hipStream_t st);
 // Raise the dynamic-LDS limit of every chain kernel to kLdsMax.
 hipError_t chain_init();
 
@@ -244,12 +267,12 @@ struct DwJob {
   float* lpart = nullptr; int32_t Hd = 0, lrows = 0;
   float* lw = nullptr; float* lb = nullptr;
 };
-hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, const TickArgs* ta,
+hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, TickRef tr,
                      hipStream_t st);
 // loss_out: the group's mean loss (from the logit partials); with a tick
-// record, loss_base + ta->loss_idx instead.
+// reference, loss_base + the tick's loss index instead.
 hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
-                            float* loss_out, const TickArgs* ta, float* loss_base, hipStream_t st);
+                            float* loss_out, TickRef tr, float* loss_base, hipStream_t st);
 
 // ---------------------------------------------------------------- others
 // Operand copies of one layer's float32 weight W [out x in], element type
@@ -268,7 +291,7 @@ constexpr int kMaxEmbDim = 16;
 struct ScatterJob {
   float* T; const int32_t* ids; int n_cat, V, E;
   const float* G; int64_t ldg; int R; float scale;
-  const TickArgs* ta;                  // R, scale; ids offset by row0 rows
+  TickRef tr;                          // R, scale; ids offset by row0 rows
 };
 hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st);
 

@@ -1,6 +1,6 @@
 // Small kernels of the split-learning step on gfx950: the weight operand
-// copies, the per-stream tick record of a replayed graph, and the raw
-// Philox4x32-10 words of the noise generator.
+// copies, the tick base of a replayed graph, and the raw Philox4x32-10
+// words of the noise generator.
 #include <algorithm>
 
 #include "device.h"
@@ -28,37 +28,8 @@ __global__ __launch_bounds__(256) void k_cast(CastJobs js) {
   }
 }
 
-__device__ void fill_tick(const AdvanceJob& j, TickArgs* o, int64_t g) {
-  const int64_t E = (j.n_rows + j.R - 1) / j.R;
-  const int64_t start = (g % E) * j.R;
-  const int64_t rows = j.n_rows - start < j.R ? j.n_rows - start : j.R;
-  o->rows = (int32_t)rows;
-  o->group = (int32_t)g;
-  o->row0 = start;
-  o->scale = j.lr / (float)rows;
-  o->loss_idx = g % j.loss_len;
-  o->chk = (int32_t)g;
-}
-
-__global__ void k_advance(AdvanceJob j) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const int64_t t = *j.counter;
-  *j.counter = t + 1;
-  const int64_t u = t - j.s;
-  if (j.kind == 0) {
-    // party A consumes group u and writes the header of its gradient slot
-    fill_tick(j, j.out[0], u);
-    j.out[0]->hdr[0] = (int32_t)u;
-    j.out[0]->hdr[1] = (int32_t)t;
-    j.out[0]->hdr[2] = (int32_t)(u - j.s > 0 ? u - j.s : 0);
-  } else {
-    // party B publishes group t (version max(0, t - s)) and back-propagates u
-    fill_tick(j, j.out[0], t);
-    j.out[0]->hdr[0] = (int32_t)t;
-    j.out[0]->hdr[1] = (int32_t)t;
-    j.out[0]->hdr[2] = (int32_t)(t - j.s > 0 ? t - j.s : 0);
-    fill_tick(j, j.out[1], u);
-  }
+__global__ void k_tick_base(TickSrc* src, int cyc) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) src->base += cyc;
 }
 
 __global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t step, uint32_t tag,
@@ -81,8 +52,8 @@ int grid_for(int64_t work, int per_block, int cap) {
 
 }  // namespace
 
-hipError_t launch_advance(const AdvanceJob& j, hipStream_t st) {
-  hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, st, j);
+hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st) {
+  hipLaunchKernelGGL(k_tick_base, dim3(1), dim3(64), 0, st, src, cyc);
   return hipGetLastError();
 }
 

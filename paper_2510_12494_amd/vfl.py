@@ -18,6 +18,7 @@ VFL_PARAM_W, VFL_PARAM_B, VFL_PARAM_TABLE = 0, 1, 2
 VFL_NOISE_EMB, VFL_NOISE_GRAD, VFL_CLIP_EMB, VFL_CLIP_GRAD = 1, 2, 4, 8
 VFL_MAX_LAYERS = 8
 VFL_GRAPH_CYCLES = 4
+VFL_TIMED_EVERY = 4       # vfl_run times the launches of every 4th tick of a captured cycle
 STATUS_NAMES = {0: "VFL_OK", 1: "VFL_E_INVALID", 2: "VFL_E_NOMEM", 3: "VFL_E_HIP",
                 4: "VFL_E_NOT_READY", 5: "VFL_E_STALE", 6: "VFL_E_STATE"}
 
