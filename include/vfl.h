@@ -140,7 +140,8 @@ vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b
 
 /* Create a context over a caller-owned device workspace (16-byte aligned) of
  * at least vfl_workspace_size() bytes; stream_a / stream_b are hipStream_t
- * (NULL: the null stream).  Parameters start at zero: set them with
+ * (NULL: the null stream).  They may be the same stream: both parties' work
+ * then runs in enqueue order, with no overlap.  Parameters start at zero: set them with
  * vfl_set_param before the first step. */
 vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
                       const vfl_top_spec* top, const vfl_opts* o, void* workspace,

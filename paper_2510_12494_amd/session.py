@@ -52,7 +52,8 @@ class Session:
     dataset ``data`` (numpy arrays from the seeded generators); ``rows_of(g)``
     gives the [(start, count)] replica rows of batch group g."""
 
-    def __init__(self, w, data: dict, params: dict, rows_of, device: str = "cuda:0"):
+    def __init__(self, w, data: dict, params: dict, rows_of, device: str = "cuda:0",
+                 one_stream: bool = False):
         self.w = w
         self.dev = torch.device(device)
         self.rows_of = rows_of
@@ -63,7 +64,8 @@ class Session:
         self.nbytes = V.vfl_workspace_size(self.specA, self.specB, self.specT, self.o)
         with torch.cuda.device(self.dev):
             self.sa = torch.cuda.Stream(device=self.dev)
-            self.sb = torch.cuda.Stream(device=self.dev)
+            # one_stream: both parties on one stream (no overlap between them)
+            self.sb = self.sa if one_stream else torch.cuda.Stream(device=self.dev)
         self.ws = torch.empty(self.nbytes, dtype=torch.uint8, device=self.dev)
         self.ctx = V.vfl_create(self.specA, self.specB, self.specT, self.o, self.ws.data_ptr(),
                                 self.nbytes, self.sa.cuda_stream, self.sb.cuda_stream)
