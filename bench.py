@@ -54,23 +54,74 @@ def gemm_flops_per_tick(w) -> float:
     return f
 
 
-def source_sha(path: str) -> str:
-    with open(path, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+CSRC = "paper_2510_12494_amd/csrc"
+# kernel class -> (kernel symbol, the sources its code and launch layout come from)
+KERNEL_SOURCES = {
+    "fwd": ("k_fwd<", ["chain.hip"]), "active": ("k_active<", ["chain.hip"]),
+    "bwd": ("k_bwd<", ["chain.hip"]), "dw": ("k_dw<", ["dw.hip"]),
+    "reduce": ("k_dw_reduce<", ["dw.hip"]), "cast": ("k_cast<", ["rowops.hip"]),
+    "emb_sgd": ("k_embed_sgd", ["embed.hip"]),
+}
+
+
+def source_sha(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel][1] + ["kernels.h", "device.h", "api.cpp"]:
+        with open(os.path.join(ROOT, CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_for(kernel: str, per_launch_work: float):
     """HBM traffic per launch from the committed rocprofv3 counter summary,
-    or None when there is none or the kernel source changed since."""
+    or None when there is none or the kernel's sources changed since."""
     p = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
     if not os.path.exists(p):
         return None
     with open(p) as fh:
         t = json.load(fh)
-    src = os.path.join(ROOT, t.get("source", ""))
-    if not os.path.exists(src) or source_sha(src) != t.get("source_sha"):
+    if t.get("source_sha") != source_sha(kernel):
         return None
     return t.get("bytes_per_launch")
+
+
+def _counter_rows(d: str, counter: str):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    out = []
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int) -> dict:
+    """HBM bytes per launch of one kernel class from two rocprofv3 --pmc
+    runs of this script with --copy-bytes (FETCH_SIZE, then WRITE_SIZE, KiB
+    per dispatch), each counter scaled so that the plain copy of known size
+    in the same run reads exactly its bytes."""
+    sym = KERNEL_SOURCES[kernel][0]
+    res = {"kernel": kernel, "copy_bytes": copy_bytes}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _counter_rows(d, name)
+        copy = [v for k, v in rows if "copy" in k.lower()]
+        if not copy:
+            raise SystemExit(f"{name}: no copy dispatch in {d}")
+        cal = copy_bytes / (max(copy) * 1024.0)
+        ks = [v for k, v in rows if sym in k]
+        if not ks:
+            raise SystemExit(f"{name}: no {sym} dispatch in {d}")
+        res[name] = {"dispatches": len(ks), "kib_per_dispatch": sum(ks) / len(ks),
+                     "copy_kib": max(copy), "scale": cal,
+                     "bytes_per_launch": cal * 1024.0 * sum(ks) / len(ks)}
+    res["bytes_per_launch"] = res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"]
+    res["source_sha"] = source_sha(kernel)
+    return res
 
 
 def cpu_baseline(w, data, params, seconds: float) -> dict:
@@ -135,7 +186,20 @@ def main():
     ap.add_argument("--workload", default="dense_tabular")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="first run one plain device copy of this many bytes "
+                         "(the calibration dispatch of a counter run)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="no GPU: summarise two rocprofv3 --pmc runs (FETCH_SIZE, "
+                         "WRITE_SIZE) into profiles/traffic_<kernel>.json")
+    ap.add_argument("--kernel", default="active", choices=sorted(KERNEL_SOURCES))
     args = ap.parse_args()
+    if args.traffic_summary:
+        res = traffic_summary(*args.traffic_summary, args.kernel, args.copy_bytes)
+        with open(os.path.join(ROOT, "profiles", f"traffic_{args.kernel}.json"), "w") as fh:
+            json.dump(res, fh, indent=1)
+        print(json.dumps(res))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: both parties share a single MI355X as two HIP "
@@ -148,6 +212,13 @@ def main():
     from paper_2510_12494_amd import vfl as V
     from paper_2510_12494_amd.session import Session
 
+    if args.copy_bytes:
+        n = args.copy_bytes // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     w = S.get(args.workload)
     data = S.generate(w)
     params = S.init_params(w)
