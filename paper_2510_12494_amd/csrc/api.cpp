@@ -41,7 +41,7 @@ namespace {
 constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
 constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
 constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
-constexpr int kDwRows = 128;          // rows of one k_dw load group (4 MFMA steps of bf16)
+constexpr int kDwRows = 256;          // rows of two k_dw load groups (4 MFMA steps each, bf16)
 constexpr int kTimedEvery = 4;        // ticks of a captured cycle between timed ticks
 
 int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
@@ -72,6 +72,8 @@ struct Party {
   size_t gx = 0;
   int64_t ldgx = 0;
   size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
+  int bo[VFL_MAX_LAYERS]{};                     // bias offsets (floats) in the party's bias table
+  size_t wq_end[kMaxSlots]{}, wtq_end[kMaxSlots]{};   // ends of the packed ranges
 };
 
 struct Top {
@@ -85,6 +87,8 @@ struct Top {
   size_t arc[VFL_MAX_LAYERS]{}, drc[VFL_MAX_LAYERS]{};
   size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
   size_t logit_part = 0;
+  int bo[VFL_MAX_LAYERS]{};           // hidden-layer bias offsets (floats) in A's bias table
+  size_t packed_end = 0;
 };
 
 // LDS layout of one chain kernel at BR rows per block
@@ -108,23 +112,30 @@ struct Lds {
   }
 };
 
-struct FwdLds { LBuf buf[2]; int bytes = 0; };
+struct FwdLds { LBuf buf[2], bias; int bytes = 0; };
 struct ActLds {
-  LBuf in, fa[VFL_MAX_LAYERS], cat, ft[VFL_MAX_LAYERS], P[2], msg, red;
+  LBuf in, fa[VFL_MAX_LAYERS], cat, ft[VFL_MAX_LAYERS], P[2], msg, red, bias;
   int bytes = 0;
 };
 struct BwdLds { LBuf P[2], mask[VFL_MAX_LAYERS]; int bytes = 0; };
 
 struct KMeta { int rt = 1, blocks = 1, lds = 0; };
 
-struct DwMeta { int splits = 1, rps = 0, blocks = 0, red_blocks = 0, red_threads = 0, logit_blocks = 0; };
+// Weight-gradient launch shape of a party: tile 32 (one unsplit launch,
+// k_dw32) or 64 (row chunks, k_dw + k_dw_reduce).
+struct DwMeta { int tile = 64, splits = 1, rps = 0, blocks = 0, red_blocks = 0, red_threads = 0, logit_blocks = 0; };
 
 struct Plan {
   Elt e = F32;
   int s = 0, k = 1, B = 1, R = 1, Ra = 64, dA = 0, dB = 0;
+  bool dw32 = false;                  // unsplit 32 x 32 weight gradients
   Party A, P;                         // P: party B (passive)
   Top T;
   size_t cat_rc = 0;
+  // bias tables: A's layers then the top model's hidden layers; B's layers
+  // (each row padded to 32 floats)
+  size_t bias_a = 0, bias_b = 0;
+  int nbias_a = 0, nbias_b = 0;       // floats
   size_t ring_g[kMaxSlots]{};
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
   size_t tsrc = 0;                    // TickSrc of the replayed graphs
@@ -237,7 +248,11 @@ bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
   return true;
 }
 
-int dw_tiles(int N, int K) { return ((N + 63) / 64) * ((K + 63) / 64); }
+int dw_tiles(int N, int K, int tile = 64) { return ((N + tile - 1) / tile) * ((K + tile - 1) / tile); }
+
+// Groups whose RC operand columns hold at most this many bytes (rows times
+// element size) contract all their rows in one block per 32 x 32 tile.
+constexpr int kDwUnsplitBytes = 2048;
 
 // Row chunks of a weight-gradient launch over `tiles` output tiles: aim at
 // kDwBlocks blocks, chunks a multiple of kDwRows rows (the rows of one load
@@ -259,6 +274,7 @@ void plan_fwd_lds(const Plan& p, int BR, FwdLds& f) {
   const int es = elt_size(p.e);
   f.buf[0] = l.take(w, es);
   f.buf[1] = l.take(w, es);
+  f.bias = l.raw(4 * p.nbias_b);
   f.bytes = l.off;
 }
 
@@ -278,7 +294,10 @@ void plan_act_lds(const Plan& p, int BR, bool gextra, ActLds& a) {
   a.P[1] = l.take(w, es);
   if (gextra) a.msg = l.take(p.dB, 4);
   // logit weights [Hd], the block's labels, dl and loss [BR each]
-  a.red = l.raw(4 * (p.T.out[p.T.H - 1] + 3 * BR));
+  // the block's labels, per-wavefront partials of the logit layer's
+  // weight gradient [kChainWaves][Hd rounded to 4] and of {loss, dl}
+  a.red = l.raw(4 * (BR + kChainWaves * ((p.T.out[p.T.H - 1] + 3) / 4 * 4) + 2 * kChainWaves));
+  a.bias = l.raw(4 * p.nbias_a);
   a.bytes = l.off;
 }
 
@@ -341,7 +360,39 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.k = o->replicas;
   p.B = o->batch;
   p.R = o->batch * o->replicas;
-  p.Ra = (p.R + kDwRows - 1) / kDwRows * kDwRows;   // RC rows: whole k_dw load groups
+  // weight-gradient launch shapes (they fix the RC row count Ra): small
+  // groups take the unsplit 32 x 32 weight gradient, whose four wavefronts
+  // run two groups of four row steps per iteration over rows rounded up to
+  // 1024; larger ones row chunks of rps rows (a multiple of two load
+  // groups) over 64 x 64 tiles.  Every block contracts whole chunks: the
+  // rows past the group are zero deltas.
+  {
+    auto bottom_tiles = [&](const vfl_bottom_spec* sp, int tile) {
+      int in = sp->n_cat * sp->emb_dim + sp->dense_in, n = 0;
+      for (int l = 0; l < sp->n_layers; ++l) { n += dw_tiles(sp->widths[l], in, tile); in = sp->widths[l]; }
+      return n;
+    };
+    auto top_tiles = [&](int tile) {
+      int in = a->widths[a->n_layers - 1] + b->widths[b->n_layers - 1], n = 0;
+      for (int j = 0; j + 1 < t->n_layers; ++j) { n += dw_tiles(t->widths[j], in, tile); in = t->widths[j]; }
+      return n;
+    };
+    const int Ra128 = (p.R + 127) / 128 * 128;
+    p.dw32 = (int64_t)Ra128 * elt_size(p.e) <= kDwUnsplitBytes;
+    if (p.dw32) {
+      p.Ra = (p.R + 1023) / 1024 * 1024;
+      p.da.blocks = bottom_tiles(a, 32) + top_tiles(32);
+      p.db.blocks = bottom_tiles(b, 32);
+      for (DwMeta* m : {&p.da, &p.db}) { m->tile = 32; m->splits = 1; m->rps = p.Ra; }
+    } else {
+      const int ta = bottom_tiles(a, 64) + top_tiles(64), tb = bottom_tiles(b, 64);
+      dw_split(p.R, ta, p.da);
+      dw_split(p.R, tb, p.db);
+      p.da.blocks = ta * p.da.splits;
+      p.db.blocks = tb * p.db.splits;
+      p.Ra = std::max(p.da.splits * p.da.rps, p.db.splits * p.db.rps);
+    }
+  }
   const int es = elt_size(p.e);
   const int64_t R = p.R, Ra = p.Ra;
   const bool eextra = o->flags & (VFL_CLIP_EMB | VFL_NOISE_EMB);
@@ -352,7 +403,9 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   // one fragment (1 KB) each
   const int KS = p.e == BF16 ? 32 : 16;
   auto ksteps = [&](int K) { return (K + KS - 1) / KS; };
-  auto packed_bytes = [&](int N, int K) { return (size_t)((N + KS - 1) / KS * KS) * ksteps(K) * 64; };
+  // (+ slack for the loads of a chain pass's last group, which may run up
+  // to 2 * 4 - 1 MFMA steps past the last tile)
+  auto packed_bytes = [&](int N, int K) { return (size_t)((N + KS - 1) / KS * KS) * ksteps(K) * 64 + 8192; };
 
   auto party = [&](Party& P, const vfl_bottom_spec* s, int nslots, bool passive) {
     P.spec = *s;
@@ -367,17 +420,17 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       P.kq[l] = ksteps(in);
       P.kt[l] = ksteps(P.out[l]);
       P.W[l] = ly.take(sizeof(float) * (size_t)P.out[l] * in);
-      P.b[l] = ly.take(sizeof(float) * (size_t)P.out[l]);
       P.drc[l] = ly.take(rc_bytes(P.out[l]));
       in = P.out[l];
     }
     if (s->n_cat) P.T = ly.take(sizeof(float) * (size_t)s->n_cat * s->vocab * s->emb_dim);
     for (int q = 0; q < nslots; ++q) {
-      for (int l = 0; l < P.L; ++l) {
-        P.Wq[q][l] = ly.take(packed_bytes(P.out[l], P.in[l]));
-        P.Wtq[q][l] = ly.take(packed_bytes(P.in[l], P.out[l]));
-        if (l + 1 < P.L) P.arc[q][l] = ly.take(rc_bytes(P.out[l]));
-      }
+      // the forward's packed copies, then the backward's: two ranges
+      for (int l = 0; l < P.L; ++l) P.Wq[q][l] = ly.take(packed_bytes(P.out[l], P.in[l]));
+      P.wq_end[q] = ly.off;
+      for (int l = 0; l < P.L; ++l) P.Wtq[q][l] = ly.take(packed_bytes(P.in[l], P.out[l]));
+      P.wtq_end[q] = ly.off;
+      for (int l = 0; l + 1 < P.L; ++l) P.arc[q][l] = ly.take(rc_bytes(P.out[l]));
       P.x0rc[q] = ly.take(rc_bytes(P.din));
       if (passive) {
         P.z[q] = ly.take((size_t)es * R * ld_of(P.out[P.L - 1]));
@@ -410,15 +463,29 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     T.kq[j] = ksteps(in);
     T.kt[j] = ksteps(T.out[j]);
     T.W[j] = ly.take(sizeof(float) * (size_t)T.out[j] * in);
-    T.b[j] = ly.take(sizeof(float) * (size_t)T.out[j]);
     if (j < T.H) {
-      T.Wq[j] = ly.take(packed_bytes(T.out[j], T.in[j]));
-      T.Wtq[j] = ly.take(packed_bytes(T.in[j], T.out[j]));
       if (j + 1 < T.H) T.arc[j] = ly.take(rc_bytes(T.out[j]));
       T.drc[j] = ly.take(rc_bytes(T.out[j]));
     }
     in = T.out[j];
   }
+  // the top model's packed copies, contiguous
+  for (int j = 0; j < T.H; ++j) T.Wq[j] = ly.take(packed_bytes(T.out[j], T.in[j]));
+  for (int j = 0; j < T.H; ++j) T.Wtq[j] = ly.take(packed_bytes(T.in[j], T.out[j]));
+  T.packed_end = ly.off;
+  // bias tables (rows padded to 32 floats; the padding stays zero)
+  auto pad32 = [](int n) { return (n + 31) / 32 * 32; };
+  p.nbias_a = 0;
+  for (int l = 0; l < p.A.L; ++l) { p.A.bo[l] = p.nbias_a; p.nbias_a += pad32(p.A.out[l]); }
+  for (int j = 0; j < T.H; ++j) { T.bo[j] = p.nbias_a; p.nbias_a += pad32(T.out[j]); }
+  p.bias_a = ly.take(sizeof(float) * (size_t)p.nbias_a);
+  for (int l = 0; l < p.A.L; ++l) p.A.b[l] = p.bias_a + sizeof(float) * p.A.bo[l];
+  for (int j = 0; j < T.H; ++j) T.b[j] = p.bias_a + sizeof(float) * T.bo[j];
+  T.b[T.H] = ly.take(sizeof(float));  // the logit's bias
+  p.nbias_b = 0;
+  for (int l = 0; l < p.P.L; ++l) { p.P.bo[l] = p.nbias_b; p.nbias_b += pad32(p.P.out[l]); }
+  p.bias_b = ly.take(sizeof(float) * (size_t)p.nbias_b);
+  for (int l = 0; l < p.P.L; ++l) p.P.b[l] = p.bias_b + sizeof(float) * p.P.bo[l];
   p.cat_rc = ly.take(rc_bytes(p.dA + p.dB));
 
   // chain kernels: rows per block and LDS layouts
@@ -438,15 +505,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.hdr = ly.take(sizeof(int32_t) * (2 * kMaxSlots * 4 + 4));
   p.tsrc = ly.take(sizeof(TickSrc));
 
-  // weight gradients: row chunks, partials, block counts
-  int tiles_a = 0, tiles_b = 0;
-  for (int l = 0; l < p.A.L; ++l) tiles_a += dw_tiles(p.A.out[l], p.A.in[l]);
-  for (int j = 0; j < T.H; ++j) tiles_a += dw_tiles(T.out[j], T.in[j]);
-  for (int l = 0; l < p.P.L; ++l) tiles_b += dw_tiles(p.P.out[l], p.P.in[l]);
-  dw_split(p.R, tiles_a, p.da);
-  dw_split(p.R, tiles_b, p.db);
-  p.da.blocks = tiles_a * p.da.splits;
-  p.db.blocks = tiles_b * p.db.splits;
+  // weight gradients: partials of the split problems
   auto parts = [&](const DwMeta& m, int N, int K, size_t& pw, size_t& pb, int& thr) {
     if (m.splits <= 1) return;
     const int kp = (K + 3) / 4 * 4;
@@ -474,10 +533,9 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
 int32_t* hdr_ptr(vfl_ctx* c, int which, int slot) { return at<int32_t>(c, c->p.hdr) + (which * kMaxSlots + slot) * 4; }
 int32_t* err_ptr(vfl_ctx* c) { return at<int32_t>(c, c->p.hdr) + 2 * kMaxSlots * 4; }
 
-ChainLayer layer(const void* W, int kst, const float* bias, int N, int K, bool relu, LBuf in,
-                 LBuf out) {
+ChainLayer layer(const void* W, int kst, int bl, int N, int K, bool relu, LBuf in, LBuf out) {
   ChainLayer L;
-  L.W = W; L.kst = kst; L.bias = bias;
+  L.W = W; L.kst = kst; L.bl = bl;
   L.N = N; L.K = K; L.relu = relu ? 1 : 0;
   L.in = in; L.out = out;
   return L;
@@ -503,6 +561,7 @@ bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_ou
     return b.pitch >= need && b.off >= 0 && b.off + b.pitch * BR <= lds && b.off % 16 == 0 && b.pitch % 16 == 0;
   };
   if (!L.W || L.N < 1 || L.K < 1 || L.kst != (L.K + KS - 1) / KS) return false;
+  if (L.bl >= 0 && (L.bl % 16 || L.bl + 4 * ((L.N + 31) / 32 * 32) > lds)) return false;
   if (!inside(L.in, L.K)) return false;
   if (lds_out && !inside(L.out, L.N)) return false;
   if (L.mask.pitch && !inside(L.mask, L.N)) return false;
@@ -555,9 +614,12 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     f.in.T = P.spec.n_cat ? at_f(P.T) : nullptr;
     f.in.buf = p.lf.buf[0];
     f.in.rc = rcm(c, P.x0rc[q], P.din);
+    f.bt.src = at_f(p.bias_b); f.bt.off = p.lf.bias.off; f.bt.n4 = p.nbias_b / 4;
+    f.warm.p[0] = c->ws + P.Wq[q][0];
+    f.warm.lines[0] = (int32_t)((P.wq_end[q] - P.Wq[q][0]) / 128);
     f.L = P.L;
     for (int l = 0; l < P.L; ++l) {
-      f.l[l] = layer(c->ws + P.Wq[q][l], P.kq[l], at_f(P.b[l]), P.out[l], P.in[l], P.relu[l],
+      f.l[l] = layer(c->ws + P.Wq[q][l], P.kq[l], p.lf.bias.off + 4 * P.bo[l], P.out[l], P.in[l], P.relu[l],
                      p.lf.buf[l % 2], p.lf.buf[(l + 1) % 2]);
       if (l + 1 < P.L) f.l[l].rc = rcm(c, P.arc[q][l], P.out[l]);
     }
@@ -577,11 +639,17 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     a.in.T = A.spec.n_cat ? at_f(A.T) : nullptr;
     a.in.buf = la.in;
     a.in.rc = rcm(c, A.x0rc[0], A.din);
+    a.bt.src = at_f(p.bias_a); a.bt.off = la.bias.off; a.bt.n4 = p.nbias_a / 4;
+    a.warm.p[0] = c->ws + A.Wq[0][0];
+    a.warm.lines[0] = (int32_t)((A.wtq_end[0] - A.Wq[0][0]) / 128);
+    a.warm.p[1] = c->ws + T.Wq[0];
+    a.warm.lines[1] = (int32_t)((T.packed_end - T.Wq[0]) / 128);
     a.LA = A.L;
     for (int l = 0; l < A.L; ++l) {
       const LBuf src = l == 0 ? la.in : la.fa[l - 1];
       const LBuf dst = l + 1 < A.L ? la.fa[l] : la.cat;
-      a.fa[l] = layer(c->ws + A.Wq[0][l], A.kq[l], at_f(A.b[l]), A.out[l], A.in[l], A.relu[l], src, dst);
+      a.fa[l] = layer(c->ws + A.Wq[0][l], A.kq[l], la.bias.off + 4 * A.bo[l], A.out[l], A.in[l], A.relu[l],
+                      src, dst);
       if (l + 1 < A.L) a.fa[l].rc = rcm(c, A.arc[0][l], A.out[l]);
     }
     a.cat = la.cat; a.cat_rc = rcm(c, p.cat_rc, p.dA + p.dB); a.dA = p.dA; a.dB = p.dB;
@@ -589,7 +657,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     a.hdr_chk = hdrp(0, q); a.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
     a.H = T.H;
     for (int j = 0; j < T.H; ++j) {
-      a.ft[j] = layer(c->ws + T.Wq[j], T.kq[j], at_f(T.b[j]), T.out[j], T.in[j], T.relu[j],
+      a.ft[j] = layer(c->ws + T.Wq[j], T.kq[j], la.bias.off + 4 * T.bo[j], T.out[j], T.in[j], T.relu[j],
                       j == 0 ? la.cat : la.ft[j - 1], la.ft[j]);
       if (j + 1 < T.H) a.ft[j].rc = rcm(c, T.arc[j], T.out[j]);
     }
@@ -600,14 +668,14 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int qq = 0; qq + 1 < T.H; ++qq) {
       const int j = T.H - 1 - qq;           // delta of top layer j -> layer j-1
       ChainLayer& L = a.dt[qq];
-      L = layer(c->ws + T.Wtq[j], T.kt[j], nullptr, T.in[j], T.out[j], false, la.P[qq % 2], la.P[(qq + 1) % 2]);
+      L = layer(c->ws + T.Wtq[j], T.kt[j], -1, T.in[j], T.out[j], false, la.P[qq % 2], la.P[(qq + 1) % 2]);
       if (T.relu[j - 1]) L.mask = la.ft[j - 1];
       L.rc = rcm(c, T.drc[j - 1], T.out[j - 1]);
     }
     {
       const int h = T.H - 1;
       ChainLayer& L = a.dc;
-      L = layer(c->ws + T.Wtq[0], T.kt[0], nullptr, p.dA + p.dB, T.out[0], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      L = layer(c->ws + T.Wtq[0], T.kt[0], -1, p.dA + p.dB, T.out[0], false, la.P[h % 2], la.P[(h + 1) % 2]);
       if (A.relu[A.L - 1]) L.mask = la.cat;
       L.rc = rcm(c, A.drc[A.L - 1], p.dA);
     }
@@ -621,14 +689,14 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       const int l = A.L - 1 - qq;           // delta of A's layer l -> layer l-1
       const int h = T.H + qq;
       ChainLayer& L = a.da[qq];
-      L = layer(c->ws + A.Wtq[0][l], A.kt[l], nullptr, A.in[l], A.out[l], false, la.P[h % 2], la.P[(h + 1) % 2]);
+      L = layer(c->ws + A.Wtq[0][l], A.kt[l], -1, A.in[l], A.out[l], false, la.P[h % 2], la.P[(h + 1) % 2]);
       if (A.relu[l - 1]) L.mask = la.fa[l - 1];
       L.rc = rcm(c, A.drc[l - 1], A.out[l - 1]);
     }
     a.has_gx = A.spec.n_cat > 0;
     if (a.has_gx) {
       const int h = T.H + A.L - 1;
-      a.gx = layer(c->ws + A.Wtq[0][0], A.kt[0], nullptr, A.spec.n_cat * A.spec.emb_dim, A.out[0], false,
+      a.gx = layer(c->ws + A.Wtq[0][0], A.kt[0], -1, A.spec.n_cat * A.spec.emb_dim, A.out[0], false,
                    la.P[h % 2], LBuf());
       a.gxp = at_f(A.gx); a.ldgx = (int32_t)A.ldgx;
     }
@@ -644,11 +712,13 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     b.C = o.clip_c; b.relu = P.relu[P.L - 1]; b.D = p.dB;
     b.d = lb.P[0]; b.d_rc = rcm(c, P.drc[P.L - 1], p.dB);
     b.hdr_chk = hdrp(1, q); b.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
+    b.warm.p[0] = c->ws + P.Wtq[q][0];
+    b.warm.lines[0] = (int32_t)((P.wtq_end[q] - P.Wtq[q][0]) / 128);
     b.nd = P.L - 1;
     for (int qq = 0; qq + 1 < P.L; ++qq) {
       const int l = P.L - 1 - qq;
       ChainLayer& L = b.dx[qq];
-      L = layer(c->ws + P.Wtq[q][l], P.kt[l], nullptr, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
+      L = layer(c->ws + P.Wtq[q][l], P.kt[l], -1, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
       if (P.relu[l - 1]) {
         L.mask = lb.mask[l - 1];
         L.mask_src = rcm(c, P.arc[q][l - 1], P.out[l - 1]);
@@ -657,7 +727,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     }
     b.has_gx = P.spec.n_cat > 0;
     if (b.has_gx) {
-      b.gx = layer(c->ws + P.Wtq[q][0], P.kt[0], nullptr, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
+      b.gx = layer(c->ws + P.Wtq[q][0], P.kt[0], -1, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
                    lb.P[(P.L - 1) % 2], LBuf());
       b.gxp = at_f(P.gx); b.ldgx = (int32_t)P.ldgx;
     }
@@ -676,7 +746,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     d.N = N; d.K = K; d.kp = (K + 3) / 4 * 4;
     d.splits = m.splits; d.rps = m.rps;
     d.first_block = J.blocks;
-    J.blocks += dw_tiles(N, K) * m.splits;
+    J.blocks += dw_tiles(N, K, m.tile) * m.splits;
   };
   for (int j = 0; j < T.H; ++j)
     add(dwa, p.da, T.drc[j], j == 0 ? p.cat_rc : T.arc[j - 1], T.out[j], T.in[j], T.W[j], T.b[j], T.Wq[j],
@@ -684,6 +754,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
   for (int l = 0; l < A.L; ++l)
     add(dwa, p.da, A.drc[l], l == 0 ? A.x0rc[0] : A.arc[0][l - 1], A.out[l], A.in[l], A.W[l], A.b[l],
         A.Wq[0][l], A.kq[l], A.Wtq[0][l], A.kt[l], A.part[l], A.partb[l]);
+  dwa.rows_pad = p.Ra;
   dwa.red_threads = p.da.red_threads;
   dwa.red_blocks = p.da.red_blocks;
   dwa.lpart = at_f(T.logit_part);
@@ -696,6 +767,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int l = 0; l < P.L; ++l)
       add(J, p.db, P.drc[l], l == 0 ? P.x0rc[q] : P.arc[q][l - 1], P.out[l], P.in[l], P.W[l], P.b[l],
           P.Wq[q][l], P.kq[l], P.Wtq[q][l], P.kt[l], P.part[l], P.partb[l]);
+    J.rows_pad = p.Ra;
     J.red_threads = p.db.red_threads;
     J.red_blocks = p.db.red_blocks;
   }
@@ -713,7 +785,8 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     if (aj[q].has_gx) ok = ok && layer_fits(p, aj[q].gx, ba, p.ka.lds, false);
     for (int l = 0; l < bj[q].nd; ++l) ok = ok && layer_fits(p, bj[q].dx[l], bb, p.kb.lds, true);
     if (bj[q].has_gx) ok = ok && layer_fits(p, bj[q].gx, bb, p.kb.lds, false);
-    ok = ok && p.la.red.off + 4 * (p.T.out[p.T.H - 1] + 3 * ba) <= p.ka.lds;
+    ok = ok && p.la.red.off + 4 * (ba + kChainWaves * ((p.T.out[p.T.H - 1] + 3) / 4 * 4) + 2 * kChainWaves) <=
+                   p.ka.lds;
     if (!ok) return "internal: chain layout does not cover a layer";
   }
   return "";
@@ -929,6 +1002,13 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, Ti
     flops += party_fwd_flops(p.A, R);
   } else {
     flops += party_fwd_flops(p.P, R);
+  }
+  if (m.tile == 32) {
+    // one launch: products, SGD, copy refresh and (A) the logit reduction
+    TIMED(VFL_K_DW, flops, st,
+          launch_dw32(p.e, job, m.blocks + (party_a ? m.logit_blocks : 0), R, scale, tr.src ? nullptr : loss, tr,
+                      tr.src ? loss : nullptr, st));
+    return VFL_OK;
   }
   TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
   const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);

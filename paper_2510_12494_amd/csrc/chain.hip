@@ -6,8 +6,10 @@
 // the activations and deltas staying in LDS.  Each layer is one MFMA product
 // out[BR x N] = in[BR x K] W^T: wavefront w takes the 16-column output tiles
 // w, w+8, w+16, ... (two at a time), loads the weight fragments of its tiles
-// straight from global memory (L2-resident: every block reads each weight
-// once) four MFMA steps ahead, and the activation fragments from LDS;
+// straight from global memory (L2-resident: the workgroups of an XCD fetch
+// the kernel's weights into its L2 at the start) two groups of four MFMA
+// steps ahead, across layer boundaries, and the activation fragments from
+// LDS; biases come from an LDS table filled at the start;
 // v_mfma_f32_16x16x32_bf16 for bf16 operands, v_mfma_f32_16x16x4_f32 for
 // float32, float32 accumulation.  The weight fragment is the MFMA's A
 // operand, so a lane ends up with four consecutive output columns of one row.
@@ -63,127 +65,200 @@ __device__ __forceinline__ char* lp(char* s, const LBuf& b, int r, int byte_col)
   return s + b.off + r * b.pitch + byte_col;
 }
 
+// eight consecutive elements of an LDS row (16 bytes of bf16, 32 of float32)
+template <typename T>
+__device__ __forceinline__ void ld8(const char* p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 4) {
+    const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 16);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { v[e] = a[e]; v[4 + e] = b[e]; }
+  } else {
+    const u32x4 x = *(const u32x4*)p;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = __uint_as_float(x[e] << 16);
+      v[2 * e + 1] = __uint_as_float(x[e] & 0xffff0000u);
+    }
+  }
+}
+template <typename T>
+__device__ __forceinline__ void st8(char* p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 4) {
+    *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
+    *(f32x4*)(p + 16) = f32x4{v[4], v[5], v[6], v[7]};
+  } else {
+    *(u32x4*)p = u32x4{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])};
+  }
+}
+
 // ------------------------------------------------------------ block product
 constexpr int kNW = kChainWaves;    // wavefronts per block (two per SIMD)
 constexpr int kNT = 64 * kNW;        // threads per block
 constexpr int kNTW = 2;              // 16-column output tiles per wavefront and pass
 constexpr int kPF = 4;               // MFMA steps per weight load group
+constexpr int kLogitChunks = kMaxLogitCols / 256;   // 4-column chunks per lane in the logit stage
 
-// Weight-fragment registers of a chain: two load groups (ping-pong) and the
-// bias of the next pass.  Between two layers `wa` / `bn` already hold the
-// first group and the bias of the next layer's first pass (`layer` names
-// it), loaded while the previous layer finished: the next layer does not
-// start with a memory round trip.
+// Weight-fragment registers of a chain: two load groups of kPF MFMA steps
+// (ping-pong).  The groups of a chain's products form one stream: when a
+// wavefront has issued the loads of a pass's last group, the next two loads
+// it issues are groups 0 and 1 of the next pass or of the next product, so
+// a product starts with both of its first groups already in flight.  A
+// pass has an even number of groups (steps past K are skipped), so every
+// pass starts in `wa`.
 struct Pipe {
   u32x4 wa[kPF][kNTW], wb[kPF][kNTW];
-  f32x4 bn[kNTW];
-  const ChainLayer* layer = nullptr;
 };
 
-// the loads of group g of a pass (tiles tile[]) of layer L into d: one
-// contiguous 1 KB fragment per tile and step of the packed operand.  Loads
-// are unconditional, clamped: tiles past the operand's last are never
-// stored and steps past the last never multiplied (a condition or a mask
-// around a load would make the compiler wait for it on the spot)
-template <typename T>
-__device__ __forceinline__ void wgroup(const ChainLayer& L, const int (&tile)[kNTW], int g,
-                                       u32x4 (&d)[kPF][kNTW]) {
-  constexpr int KS = Ch<T>::KS;
-  const int lane = threadIdx.x & 63;
-  const int ntl = (L.N + KS - 1) / KS * (KS / 16);
-  const VFL_GLOBAL u32x4* W = glb((const u32x4*)L.W) + lane;
-#pragma unroll
-  for (int j = 0; j < kNTW; ++j) {
-    const VFL_GLOBAL u32x4* wt = W + (int64_t)min(tile[j], ntl - 1) * L.kst * 64;
-#pragma unroll
-    for (int q = 0; q < kPF; ++q) d[q][j] = wt[min(g * kPF + q, L.kst - 1) * 64];
-  }
+// A pointer or value the compiler must keep in scalar registers (it is
+// uniform, but derived through selects the compiler may place in vector
+// registers, and a field loaded through a vector-register pointer is a
+// vector-memory load whose wait drains every load in flight).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// A job descriptor read through the constant address space: the jobs are
+// written once, before any launch, so their fields may come through the
+// scalar cache (scalar loads, counted apart from the vector loads in flight)
+// even after the kernel's own stores.
+#define VFL_CONST __attribute__((address_space(4)))
+template <typename X>
+__device__ __forceinline__ const VFL_CONST X& cst(const X& x) {
+  return *(const VFL_CONST X*)&x;
 }
 
-// bias values bias[n .. n+3] of the lane's output columns (zero past N)
-__device__ __forceinline__ void bgroup(const ChainLayer& L, const int (&tile)[kNTW], f32x4 (&b)[kNTW]) {
-  const int kc = (threadIdx.x & 63) >> 4;
+// 16-column tiles of a product of N output columns (up to the MFMA depth)
+template <typename T>
+__device__ __forceinline__ int tiles_of(int N) {
+  constexpr int KS = Ch<T>::KS;
+  return (N + KS - 1) / KS * (KS / 16);
+}
+
+// the loads of group g of a pass (tiles tile[]) of an operand W with kst
+// K steps and ntl tiles into d: one contiguous 1 KB fragment per tile and
+// step of the packed operand.  Loads are unconditional: tiles past the
+// operand's last are clamped to it (never used), steps past K read on into
+// the next tile or the operand's slack (never used either; a conditional
+// load would make the compiler wait for it on the spot).  The address is a
+// uniform base per tile plus the lane's 16 bytes plus an immediate.
+__device__ __forceinline__ void wgroup(const void* Wp, int kst, int ntl, const int (&tile)[kNTW], int g,
+                                       u32x4 (&d)[kPF][kNTW]) {
+  const uint32_t lo = (threadIdx.x & 63) * 16;
 #pragma unroll
   for (int j = 0; j < kNTW; ++j) {
-    const int n = tile[j] * 16 + 4 * kc;
-    b[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (L.bias) {
-      const VFL_GLOBAL float* bias = glb(L.bias);
-      if (n + 4 <= L.N) {
-        b[j] = *(const VFL_GLOBAL f32x4*)(bias + n);
-      } else {
+    const VFL_GLOBAL char* base =
+        glb((const char*)Wp) + ((int64_t)min(tile[j], ntl - 1) * kst + g * kPF) * 1024;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (n + i < L.N) b[j][i] = bias[n + i];
-      }
-    }
+    for (int q = 0; q < kPF; ++q) d[q][j] = *(const VFL_GLOBAL u32x4*)(base + lo + q * 1024);
   }
 }
 
 // the tiles of a wavefront's pass: wave + kNW * (kNTW * pass + j)
 __device__ __forceinline__ void pass_tiles(int pass, int (&tile)[kNTW]) {
-  const int wave = threadIdx.x >> 6;
+  const int wave = uniform((int)(threadIdx.x >> 6));
 #pragma unroll
   for (int j = 0; j < kNTW; ++j) tile[j] = wave + kNW * (kNTW * pass + j);
 }
 
-// start the loads of the first group and bias of L's first pass into p
+// start the loads of groups 0 and 1 of L's first pass
 template <typename T>
 __device__ __forceinline__ void prefetch(const ChainLayer* L, Pipe& p) {
-  p.layer = L;
-  if (!L) return;
   int tile[kNTW];
   pass_tiles(0, tile);
-  wgroup<T>(*L, tile, 0, p.wa);
-  bgroup(*L, tile, p.bn);
+  const VFL_CONST ChainLayer& C = cst(*(const ChainLayer*)uniform_ptr(L));
+  const void* W = uniform_ptr(C.W);
+  const int kst = uniform(C.kst), ntl = uniform(tiles_of<T>(C.N));
+  wgroup(W, kst, ntl, tile, 0, p.wa);
+  wgroup(W, kst, ntl, tile, 1, p.wb);
+}
+
+// Copy of a chain kernel's bias table into LDS (see BiasTab).
+__device__ __forceinline__ void copy_bias(char* s, const BiasTab& b) {
+  const VFL_GLOBAL f32x4* src = glb((const f32x4*)b.src);
+  for (int i = threadIdx.x; i < b.n4; i += kNT) *(f32x4*)(s + b.off + 16 * i) = src[i];
+}
+
+// One 4-byte load per 128-byte line of this workgroup's slice of the
+// kernel's weight ranges (slice = workgroup / 8 mod 32: the workgroups of
+// one XCD share its L2), returned so that the caller can consume the values
+// where it waits for its inputs anyway.  Up to 2 lines per thread and
+// range; addresses are clamped into the range, so the loads are
+// unconditional.
+__device__ __forceinline__ uint32_t warm_l2(const WarmSet& w, const void* dummy) {
+  const int slice = (blockIdx.x >> 3) & 31;
+  uint32_t x = 0u;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int lines = w.lines[r];
+    const int per = (lines + 31) >> 5;
+    const int c0 = slice * per, c1 = min(lines, c0 + per);
+    const VFL_GLOBAL uint32_t* base = glb((const uint32_t*)(lines > 0 ? w.p[r] : dummy));
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int c = c0 + (int)threadIdx.x + k * kNT;
+      x ^= base[(int64_t)(c < c1 ? c : 0) * 32];
+    }
+  }
+  return x;
 }
 
 // out[r][n] = epi(r, n, sum_k in[r][k] W[n][k], bias) for the block's rows:
 // epi(r, n, acc, bias) receives block row r, output columns n .. n+3 (n a
-// multiple of 4; bias[i] = bias[n + i], zero without a bias or past N), for
-// every row of the block and every column below N rounded up to the MFMA
-// depth.  Full load groups are pipelined two per iteration (ping-pong
-// between p.wa and p.wb, so that no register copy waits for a prefetch),
-// then the remainder steps; after a wavefront's last MFMA of L it starts the
-// loads of `next` (nullable) into p.
+// multiple of 4; bias[i] = bias[n + i] from the LDS table, zero without a
+// bias or past N), for every row of the block and every column below N
+// rounded up to the MFMA depth.  On entry p holds groups 0 and 1 of L's
+// first pass; on return, groups 0 and 1 of `next`'s (nullable).
 template <typename T, int RT, typename Epi>
 __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe& p,
                                          const ChainLayer* next, Epi&& epi) {
-  constexpr int KS = Ch<T>::KS, PF = kPF, NTW = kNTW;
+  constexpr int PF = kPF, NTW = kNTW;
   const int lane = threadIdx.x & 63;
   const int kc = lane >> 4, lr = lane & 15;
-  const int N = L.N, K = L.K;
-  const int ntl = (N + KS - 1) / KS * (KS / 16);
-  const int nks = (K + KS - 1) / KS;
-  const int nfull = nks / PF, rem = nks % PF;
-  const LBuf in = L.in;
+  const VFL_CONST ChainLayer& C = cst(L);
+  const void* W = uniform_ptr(C.W);
+  const int ntl = uniform(tiles_of<T>(C.N));
+  const int nks = uniform(C.kst);
+  const int ng = ((nks + PF - 1) / PF + 1) & ~1;
+  const int bl = uniform(C.bl);
+  LBuf in;
+  in.off = C.in.off;
+  in.pitch = C.in.pitch;
   const int npass = (ntl + kNW * NTW - 1) / (kNW * NTW);
-  bool pre = p.layer == &L;
+  // the next product's operand; past the chain's end the loads repeat this
+  // product's (never used: every refill issues the same loads, so the
+  // compiler's wait counts stay exact)
+  next = (const ChainLayer*)uniform_ptr(next);
+  const VFL_CONST ChainLayer& CN = cst(next ? *next : L);
+  const void* nW = uniform_ptr(CN.W);
+  const int nkst = uniform(CN.kst), nntl = uniform(tiles_of<T>(CN.N));
 #pragma unroll 1
   for (int pass = 0; pass < npass; ++pass) {
-    int tile[NTW];
+    int tile[NTW], ntile[NTW];
     pass_tiles(pass, tile);
-    f32x4 bv[NTW];
-    if (pre) {
-#pragma unroll
-      for (int j = 0; j < NTW; ++j) bv[j] = p.bn[j];
-    } else {
-      bgroup(L, tile, bv);
-      wgroup<T>(L, tile, 0, p.wa);
-    }
-    pre = false;
+    // where the loads go once this pass's groups are all issued: the next
+    // pass, or the next product's first
+    const bool more = pass + 1 < npass;
+    pass_tiles(more ? pass + 1 : 0, ntile);
+    const void* rW = more ? W : nW;
+    const int rkst = more ? nks : nkst, rntl = more ? ntl : nntl;
     f32x4 acc[NTW][RT];
 #pragma unroll
     for (int j = 0; j < NTW; ++j)
 #pragma unroll
       for (int t = 0; t < RT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     auto step = [&](int ks, const u32x4 (&w)[NTW]) {
+      if (ks >= nks) return;
       u32x4 xf[RT];
 #pragma unroll
       for (int t = 0; t < RT; ++t)
         xf[t] = *(const u32x4*)(s + in.off + (t * 16 + lr) * in.pitch + (ks * 4 + kc) * 16);
 #pragma unroll
       for (int j = 0; j < NTW; ++j) {
+        if (tile[j] >= ntl) continue;
 #pragma unroll
         for (int t = 0; t < RT; ++t) {
           if constexpr (sizeof(T) == 2) {
@@ -202,34 +277,28 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
 #pragma unroll
       for (int q = 0; q < PF; ++q) step(g * PF + q, w[q]);
     };
-    auto tail = [&](const u32x4 (&w)[PF][NTW]) {
+    // group g of this pass into w, or group g - ng of the next pass/product
+    auto refill = [&](int g, u32x4 (&w)[PF][NTW]) {
+      const bool cur = g < ng;
+      int tt[NTW];
 #pragma unroll
-      for (int q = 0; q < PF - 1; ++q)
-        if (q < rem) step(nfull * PF + q, w[q]);
+      for (int j = 0; j < NTW; ++j) tt[j] = cur ? tile[j] : ntile[j];
+      wgroup(cur ? W : rW, cur ? nks : rkst, cur ? ntl : rntl, tt, cur ? g : g - ng, w);
     };
-    int g = 0;
 #pragma unroll 1
-    for (; g + 2 <= nfull; g += 2) {
-      wgroup<T>(L, tile, g + 1, p.wb);
+    for (int g = 0; g < ng; g += 2) {
       group(g, p.wa);
-      wgroup<T>(L, tile, g + 2, p.wa);
+      refill(g + 2, p.wa);
       group(g + 1, p.wb);
+      refill(g + 3, p.wb);
     }
-    if (g < nfull) {
-      wgroup<T>(L, tile, g + 1, p.wb);
-      group(g, p.wa);
-      tail(p.wb);
-    } else {
-      tail(p.wa);
-    }
-    // the last pass: the next layer's loads fly during this epilogue, the
-    // barrier and whatever runs before the next product
-    if (pass + 1 == npass) prefetch<T>(next, p);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       if (tile[j] >= ntl) continue;
+      const int n = tile[j] * 16 + 4 * kc;
+      const f32x4 bv = bl >= 0 ? *(const f32x4*)(s + bl + 4 * n) : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < RT; ++t) epi(t * 16 + lr, tile[j] * 16 + 4 * kc, acc[j][t], bv[j]);
+      for (int t = 0; t < RT; ++t) epi(t * 16 + lr, n, acc[j][t], bv);
     }
   }
 }
@@ -285,7 +354,13 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
   const int units = (BR / RR) * ncc;
   VFL_GLOBAL char* g = glb((char*)m.p);
   const int64_t cp = m.cp;
-  for (int u = threadIdx.x; u < units; u += kNT) {
+  // wavefront w takes the units [w * per, (w + 1) * per): the transposes
+  // are spread over every SIMD, and a wavefront's stores stay contiguous
+  const int per = (units + kNW - 1) / kNW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int i = lane; i < per; i += 64) {
+    const int u = wave * per + i;
+    if (u >= units) break;
     const int rg = u / ncc, cc = u % ncc;
     u32x4 in[RR], out[RR];
 #pragma unroll
@@ -320,7 +395,11 @@ __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, cons
   const int units = (BR / RR) * ncc;
   const VFL_GLOBAL char* g = glb((const char*)m.p);
   const int64_t cp = m.cp;
-  for (int u = threadIdx.x; u < units; u += kNT) {
+  const int per = (units + kNW - 1) / kNW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int i = lane; i < per; i += 64) {
+    const int u = wave * per + i;
+    if (u >= units) break;
     const int rg = u / ncc, cc = u % ncc;
     u32x4 in[RR], out[RR];
     if (cc * RR < cols) {
@@ -475,6 +554,7 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
   constexpr int BR = 16 * RT;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const FwdJob& j = *jp;
+  const int nL = cst(j).L;
   const Call k = resolve(cc, tr);
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_out) {
     VFL_GLOBAL int32_t* h = glb(j.hdr_out);
@@ -485,15 +565,18 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
   const int rv = min(BR, k.rows - r0);
   Pipe pp;
   prefetch<T>(&j.l[0], pp);   // overlaps the input rows' loads
+  const uint32_t wx = warm_l2(j.warm, jp);
+  copy_bias(s, j.bt);
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
   __syncthreads();
+  asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
   if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
-  for (int l = 0; l < j.L; ++l) {
-    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < j.L ? &j.l[l + 1] : nullptr);
+  for (int l = 0; l < nL; ++l) {
+    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < nL ? &j.l[l + 1] : nullptr);
     __syncthreads();
     if (j.l[l].rc.p) lds_to_rc<T, BR>(s, j.l[l].out, j.l[l].N, j.l[l].rc, r0);
   }
-  const ChainLayer& last = j.l[j.L - 1];
+  const ChainLayer& last = j.l[nL - 1];
   lds_to_rows<T, BR>(s, last.out, last.N, j.z, j.ldz, r0, rv);
   if (j.publish)
     msg_rows<T, T, BR>(s, last.out, last.N, j.m, (uint32_t)k.group, k.row0, j.zhat, j.ldzh, j.norm,
@@ -507,6 +590,10 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   constexpr int CE = Ch<T>::CE, KS = Ch<T>::KS;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const ActiveJob& j = *jp;
+  const int LA = cst(j).LA;
+  const int H = cst(j).H;
+  const int nda = cst(j).nda;
+  const int has_gx = cst(j).has_gx;
   const Call k = resolve(cc, tr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -520,43 +607,47 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   if (r0 >= k.rows) {
     // rows past a short group: zero delta rows, so that the weight
     // gradient may read whole row steps
-    zero_rc<T, BR>(j.dh_rc, j.ft[j.H - 1].N, r0);
-    for (int q = 0; q + 1 < j.H; ++q) zero_rc<T, BR>(j.dt[q].rc, j.dt[q].N, r0);
+    zero_rc<T, BR>(j.dh_rc, j.ft[H - 1].N, r0);
+    for (int q = 0; q + 1 < H; ++q) zero_rc<T, BR>(j.dt[q].rc, j.dt[q].N, r0);
     zero_rc<T, BR>(j.dc.rc, j.dA, r0);
-    for (int q = 0; q < j.nda; ++q) zero_rc<T, BR>(j.da[q].rc, j.da[q].N, r0);
+    for (int q = 0; q < nda; ++q) zero_rc<T, BR>(j.da[q].rc, j.da[q].N, r0);
     return;
   }
   const int rv = min(BR, k.rows - r0);
-  const int Hd = j.ft[j.H - 1].N;
-  // the labels and logit weights, fetched alongside the input rows and
-  // kept in LDS next to the logit reduction scratch
-  float* lwl = (float*)(s + j.red.off);
-  float* yl = lwl + Hd;
-  float pw[kMaxLogitCols / kNT], py;
+  const int Hd = j.ft[H - 1].N;
+  // the labels (to LDS with the inputs) and the logit weights of the lane's
+  // columns in the logit stage (columns 256 i + 4 lane .. +4, kept in
+  // registers); loads clamped, so all are unconditional
+  float* yl = (float*)(s + j.red.off);
+  float py;
+  float lwr[kLogitChunks][4];
   {
     const VFL_GLOBAL float* lw = glb(j.lw);
     const VFL_GLOBAL float* y = glb(cc.labels) + k.in_off + r0;
 #pragma unroll
-    for (int q = 0; q < kMaxLogitCols / kNT; ++q) {
-      const int i = threadIdx.x + kNT * q;
-      pw[q] = i < Hd ? lw[i] : 0.f;
-    }
-    py = (int)threadIdx.x < rv ? y[threadIdx.x] : 0.f;
+    for (int i = 0; i < kLogitChunks; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 256 * i + 4 * lane + e;
+        const float v = lw[min(c, Hd - 1)];
+        lwr[i][e] = c < Hd ? v : 0.f;
+      }
+    py = y[min((int)threadIdx.x, rv - 1)];
   }
   const float lbias = glb(j.lb)[0];
   Pipe pp;
   prefetch<T>(&j.fa[0], pp);
+  const uint32_t wx = warm_l2(j.warm, jp);
+  copy_bias(s, j.bt);
 
   // A's bottom forward; the last layer fills cat[:, 0:dA)
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
-#pragma unroll
-  for (int q = 0; q < kMaxLogitCols / kNT; ++q)
-    if ((int)threadIdx.x + kNT * q < Hd) lwl[threadIdx.x + kNT * q] = pw[q];
-  if ((int)threadIdx.x < BR) yl[threadIdx.x] = py;
+  if ((int)threadIdx.x < BR) yl[threadIdx.x] = (int)threadIdx.x < rv ? py : 0.f;
   __syncthreads();
+  asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
   if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
-  for (int l = 0; l < j.LA; ++l) {
-    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < j.LA ? &j.fa[l + 1] : &j.ft[0]);
+  for (int l = 0; l < LA; ++l) {
+    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < LA ? &j.fa[l + 1] : &j.ft[0]);
     __syncthreads();
     if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
   }
@@ -575,82 +666,98 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   __syncthreads();
   if (j.cat_rc.p) lds_to_rc<T, BR>(s, j.cat, j.dA + j.dB, j.cat_rc, r0);
   // top hidden layers
-  for (int q = 0; q < j.H; ++q) {
-    run_layer<T, RT>(s, j.ft[q], rv, pp, q + 1 < j.H ? &j.ft[q + 1] : (j.H > 1 ? &j.dt[0] : &j.dc));
+  for (int q = 0; q < H; ++q) {
+    run_layer<T, RT>(s, j.ft[q], rv, pp, q + 1 < H ? &j.ft[q + 1] : (H > 1 ? &j.dt[0] : &j.dc));
     __syncthreads();
     if (j.ft[q].rc.p) lds_to_rc<T, BR>(s, j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0);
   }
-  // logit + BCE (Eq. 1), dl = sigmoid(l) - y: 16 lanes per row, 4 rows per
-  // wavefront at a time, each lane on the 4-column groups cg, cg + 16, ...;
-  // the rows' dl and loss go to LDS
-  float* dlv = yl + BR;
-  float* lsv = dlv + BR;
+  // logit + BCE (Eq. 1), dl = sigmoid(l) - y: a wavefront per row (its
+  // BR / 8 rows one after the other), lane on the columns 256 i + 4 lane
+  // .. +4; the last hidden delta dl * w (ReLU-masked) goes to LDS.  The
+  // logit layer's weight gradient sum_r dl_r h[r][c], the loss and dl
+  // accumulate per wavefront in registers and are then summed over the
+  // wavefronts in order.  The loss only reports progress: its exp and log
+  // are the hardware's.
   {
-    const LBuf Hb = j.ft[j.H - 1].out, Db = j.dh;
-    const int hq = (Hd + KS - 1) / KS * KS / 4;   // 4-column groups to write
-    const int sub = lane >> 4, cg = lane & 15;
-    for (int rb = 0; rb < BR; rb += 4 * kNW) {
-      const int r = rb + wave * 4 + sub;
-      if (r >= BR) continue;   // uniform within the row's 16 lanes
+    const LBuf Hb = j.ft[H - 1].out, Db = j.dh;
+    constexpr int KS = Ch<T>::KS, RW = BR / kNW;
+    const int Hw = (Hd + KS - 1) / KS * KS;     // LDS width of h and dh
+    const int Hd4 = (Hd + 3) / 4 * 4;
+    float* wpart = yl + BR;                     // [kNW][Hd4]
+    float* wl = wpart + kNW * Hd4;              // [kNW][2]
+    float g[kLogitChunks][4];
+#pragma unroll
+    for (int i = 0; i < kLogitChunks; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) g[i][e] = 0.f;
+    float lsum = 0.f, dsum = 0.f;
+    const bool relu_h = j.relu_h != 0;
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      const int r = wave * RW + rr;
       const bool ok = r < rv;
+      float h[kLogitChunks][4];
       float dot = 0.f;
-      for (int q = cg; q < hq; q += 16) {
-        float hv[4];
-        ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dot += hv[e] * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
+      for (int i = 0; i < kLogitChunks; ++i) {
+        const int c0 = 256 * i + 4 * lane;
+        if (c0 < Hw) ld4<T>(lp(s, Hb, r, c0 * (int)sizeof(T)), h[i]);
+        else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) h[i][e] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dot += h[i][e] * lwr[i][e];
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) dot += __shfl_xor(dot, o, 64);
+      dot = wave_sum(dot);
       const float l = dot + lbias;
-      const float yy = ok ? yl[r] : 0.f;
-      const float ex = expf(-fabsf(l));
-      const float loss = fmaxf(l, 0.f) - yy * l + log1pf(ex);
-      const float sig = l >= 0.f ? 1.f / (1.f + ex) : ex / (1.f + ex);
+      const float yy = yl[r];
+      const float ex = __expf(-fabsf(l));
+      const float inv = __frcp_rn(1.f + ex);
+      const float sig = l >= 0.f ? inv : ex * inv;
       const float dl = ok ? sig - yy : 0.f;
-      for (int q = cg; q < hq; q += 16) {
-        float hv[4], d[4];
-        ld4<T>(lp(s, Hb, r, 4 * q * (int)sizeof(T)), hv);
+      if (ok) lsum += fmaxf(l, 0.f) - yy * l + __logf(1.f + ex);
+      dsum += dl;
+#pragma unroll
+      for (int i = 0; i < kLogitChunks; ++i) {
+        const int c0 = 256 * i + 4 * lane;
+        float d[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          d[e] = dl * (4 * q + e < Hd ? lwl[4 * q + e] : 0.f);
-          if (j.relu_h && !(hv[e] > 0.f)) d[e] = 0.f;
+          d[e] = dl * lwr[i][e];
+          if (relu_h && !(h[i][e] > 0.f)) d[e] = 0.f;
+          g[i][e] += dl * h[i][e];
         }
-        st4<T>(lp(s, Db, r, 4 * q * (int)sizeof(T)), d);
+        if (c0 < Hw) st4<T>(lp(s, Db, r, c0 * (int)sizeof(T)), d);
       }
-      if (cg == 0) {
-        dlv[r] = dl;
-        lsv[r] = ok ? loss : 0.f;
-      }
+    }
+#pragma unroll
+    for (int i = 0; i < kLogitChunks; ++i) {
+      const int c0 = 256 * i + 4 * lane;
+      if (c0 < Hd4) *(f32x4*)(wpart + wave * Hd4 + c0) = f32x4{g[i][0], g[i][1], g[i][2], g[i][3]};
+    }
+    if (lane == 0) {
+      wl[2 * wave] = lsum;
+      wl[2 * wave + 1] = dsum;
     }
     __syncthreads();
-    // the logit layer's weight gradient over the block's rows, sum_r dl_r
-    // h[r][c]: a float32 MFMA per 16 columns and 4 rows (every output row of
-    // the MFMA gets the same sums), wavefront w on the column tiles w, w+8, ..
     VFL_GLOBAL float* part = glb(j.part) + (int64_t)blockIdx.x * (Hd + 2);
-    const int kc = lane >> 4, lr = lane & 15;
-    for (int t = wave; t * 16 < Hd; t += kNW) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int c = t * 16 + lr;
-#pragma unroll 4
-      for (int s4 = 0; s4 < BR / 4; ++s4) {
-        const int r = 4 * s4 + kc;
-        const float h = c < Hd ? ld1<T>((const T*)lp(s, Hb, r, 0) + c) : 0.f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv[r], h, acc, 0, 0, 0);
+    for (int c = threadIdx.x; c < Hd + 2; c += kNT) {
+      float t = 0.f;
+      if (c < 2) {
+#pragma unroll
+        for (int w = 0; w < kNW; ++w) t += wl[2 * w + c];
+      } else {
+#pragma unroll
+        for (int w = 0; w < kNW; ++w) t += wpart[w * Hd4 + c - 2];
       }
-      if (kc == 0 && c < Hd) part[2 + c] = acc[0];
-    }
-    if (threadIdx.x == 0) {
-      float ls = 0.f, gb = 0.f;
-      for (int r = 0; r < BR; ++r) { ls += lsv[r]; gb += dlv[r]; }
-      part[0] = ls;
-      part[1] = gb;
+      part[c] = t;
     }
   }
-  if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[j.H - 1].N, j.dh_rc, r0);
+  if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[H - 1].N, j.dh_rc, r0);
   // top input-gradient chain
-  for (int q = 0; q + 1 < j.H; ++q) {
-    run_layer<T, RT>(s, j.dt[q], rv, pp, q + 2 < j.H ? &j.dt[q + 1] : &j.dc);
+  for (int q = 0; q + 1 < H; ++q) {
+    run_layer<T, RT>(s, j.dt[q], rv, pp, q + 2 < H ? &j.dt[q + 1] : &j.dc);
     __syncthreads();
     if (j.dt[q].rc.p) lds_to_rc<T, BR>(s, j.dt[q].out, j.dt[q].N, j.dt[q].rc, r0);
   }
@@ -662,7 +769,7 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     const bool maskA = j.dc.mask.pitch > 0, gextra = j.gextra != 0;
     VFL_GLOBAL T* ring = glb((T*)j.ring);
     const int64_t ldr = j.ldring;
-    block_mm<T, RT>(s, j.dc, pp, j.nda > 0 ? &j.da[0] : (j.has_gx ? &j.gx : nullptr),
+    block_mm<T, RT>(s, j.dc, pp, nda > 0 ? &j.da[0] : (has_gx ? &j.gx : nullptr),
                     [&](int r, int n, const f32x4& a, const f32x4&) {
       const bool ok = r < rv;
       if (n + 4 <= dA) {
@@ -696,12 +803,12 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
                              nullptr, r0, rv);
   }
   // A's input-gradient chain
-  for (int q = 0; q < j.nda; ++q) {
-    run_layer<T, RT>(s, j.da[q], rv, pp, q + 1 < j.nda ? &j.da[q + 1] : (j.has_gx ? &j.gx : nullptr));
+  for (int q = 0; q < nda; ++q) {
+    run_layer<T, RT>(s, j.da[q], rv, pp, q + 1 < nda ? &j.da[q + 1] : (has_gx ? &j.gx : nullptr));
     __syncthreads();
     if (j.da[q].rc.p) lds_to_rc<T, BR>(s, j.da[q].out, j.da[q].N, j.da[q].rc, r0);
   }
-  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
+  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
 }
 
 template <typename T, int RT>
@@ -711,22 +818,24 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
   constexpr int KS = Ch<T>::KS;
   extern __shared__ __attribute__((aligned(16))) char s[];
   const BwdJob& j = *jp;
+  const int nd = cst(j).nd;
+  const int has_gx = cst(j).has_gx;
   const Call k = resolve(cc, tr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x == 0 && threadIdx.x == 0 && j.hdr_chk && glb(j.hdr_chk)[0] != k.chk) atomicAdd(j.err, 1);
   const int r0 = blockIdx.x * BR;
   if (r0 >= k.rows) {
     zero_rc<T, BR>(j.d_rc, j.D, r0);
-    for (int q = 0; q < j.nd; ++q) zero_rc<T, BR>(j.dx[q].rc, j.dx[q].N, r0);
+    for (int q = 0; q < nd; ++q) zero_rc<T, BR>(j.dx[q].rc, j.dx[q].N, r0);
     return;
   }
   const int rv = min(BR, k.rows - r0);
   Pipe pp;
-  if (j.nd > 0) prefetch<T>(&j.dx[0], pp);
-  else if (j.has_gx) prefetch<T>(&j.gx, pp);
+  if (nd > 0 || has_gx) prefetch<T>(nd > 0 ? &j.dx[0] : &j.gx, pp);
+  const uint32_t wx = warm_l2(j.warm, jp);
   // the ReLU masks of every layer of the chain, each in an LDS buffer of
   // its own (stashed activations of this group's forward)
-  for (int q = 0; q < j.nd; ++q)
+  for (int q = 0; q < nd; ++q)
     if (j.dx[q].mask_src.p) rc_to_lds<T, BR>(s, j.dx[q].mask, j.dx[q].N, j.dx[q].mask_src, r0);
   // cut-layer backward: through the clip when the row was clipped
   // (d(c v)/dv = c (I - u u^T) with u = v / ||v||), then the ReLU of B's
@@ -776,14 +885,15 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
     }
   }
   __syncthreads();
+  asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
   if (j.d_rc.p) lds_to_rc<T, BR>(s, j.d, j.D, j.d_rc, r0);
-  for (int q = 0; q < j.nd; ++q) {
+  for (int q = 0; q < nd; ++q) {
     const ChainLayer& L = j.dx[q];
-    run_layer<T, RT>(s, L, rv, pp, q + 1 < j.nd ? &j.dx[q + 1] : (j.has_gx ? &j.gx : nullptr));
+    run_layer<T, RT>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr));
     __syncthreads();
     if (L.rc.p) lds_to_rc<T, BR>(s, L.out, L.N, L.rc, r0);
   }
-  if (j.has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
+  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
 }
 
 template <typename K>

@@ -24,14 +24,34 @@ namespace vfl {
 namespace {
 using namespace dev;
 
+// SGD of the master weights W[n][kb .. kb+3] (those below K) with the
+// gradient g, and the new values into the packed operand copies.  The four
+// master values are loaded first, unconditionally (clamped), so that their
+// loads are in flight together.
 template <typename T>
-__device__ __forceinline__ void sgd_store(const DwProb& P, int n, int k, float g, float scale) {
-  const int64_t idx = (int64_t)n * P.K + k;
-  VFL_GLOBAL float* W = glb(P.W);
-  const float w = W[idx] - scale * g;
-  W[idx] = w;
-  if (P.Wq) st1<T>((T*)(glb((T*)P.Wq) + pk_index<T>(n, k, P.kq)), w);
-  if (P.Wtq) st1<T>((T*)(glb((T*)P.Wtq) + pk_index<T>(k, n, P.kt)), w);
+__device__ __forceinline__ void sgd_load4(const DwProb& P, int n, int kb, float (&w)[4]) {
+  const int K = P.K;
+  const VFL_GLOBAL float* W = glb(P.W) + (int64_t)min(n, P.N - 1) * K;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) w[e] = W[min(kb + e, K - 1)];
+}
+template <typename T>
+__device__ __forceinline__ void sgd_store4(const DwProb& P, int n, int kb, const float (&w)[4], const f32x4& g,
+                                           float scale) {
+  const int K = P.K;
+  VFL_GLOBAL float* W = glb(P.W) + (int64_t)n * K;
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = w[e] - scale * g[e];   // unconditional: keeps the loads unsunk
+  if (n >= P.N) return;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int k = kb + e;
+    if (k >= K) continue;
+    W[k] = v[e];
+    if (P.Wq) st1<T>((T*)(glb((T*)P.Wq) + pk_index<T>(n, k, P.kq)), v[e]);
+    if (P.Wtq) st1<T>((T*)(glb((T*)P.Wtq) + pk_index<T>(k, n, P.kt)), v[e]);
+  }
 }
 
 template <typename T>
@@ -49,16 +69,11 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
   const int tiles_k = (P.K + 63) / 64;
   const int tile = lb / P.splits, split = lb % P.splits;
   const int n0 = (tile / tiles_k) * 64, k0 = (tile % tiles_k) * 64;
-  int R = Rarg;
   float scale = scale_arg;
-  if (tr.src) {
-    const TickArgs ta = tick_args(tr);
-    R = ta.rows;
-    scale = ta.scale;
-  }
+  if (tr.src) scale = tick_args(tr).scale;
+  (void)Rarg;   // every chunk is contracted whole: the group's row count is not needed
   const int rb = split * P.rps;
-  const int re = min(R, rb + P.rps);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int wm = wave >> 1, wn = wave & 1, kc = lane >> 4, lr = lane & 15;
   const VFL_GLOBAL char* Dp = glb((const char*)P.D.p);
   const VFL_GLOBAL char* Xp = glb((const char*)P.X.p);
@@ -102,7 +117,9 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
       }
     }
   };
-  const int ngr = re > rb ? (re - rb + PF * KR - 1) / (PF * KR) : 0;
+  // every chunk is contracted whole (rps rows, a multiple of two load
+  // groups; the delta rows past the group are zero)
+  const int ngr = P.rps / (PF * KR);
   u32x4 dA[PF][2], xA[PF][2], dB[PF][2], xB[PF][2];
   auto group = [&](const u32x4 (&df)[PF][2], const u32x4 (&xf)[PF][2]) {
 #pragma unroll
@@ -137,16 +154,23 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
       }
     }
   };
-  // two groups per iteration, ping-ponging between the A and B registers;
-  // every prefetch is unconditional (past the end it reloads the last group)
+  // two groups in flight at the top of every iteration (A: group g, B:
+  // group g + 1), each refilled as soon as its MFMAs have read it; every
+  // load is unconditional (past the end it reloads the last group), and
+  // the first iteration is peeled, so that the loop is entered with the
+  // loads in flight exactly as at its back edge (exact wait counts)
   load(0, dA, xA);
+  load(min(1, ngr - 1), dB, xB);
+  group(dA, xA);
+  load(min(2, ngr - 1), dA, xA);
+  group(dB, xB);
+  load(min(3, ngr - 1), dB, xB);
 #pragma unroll 1
-  for (int g = 0; g < ngr; g += 2) {
-    load(min(g + 1, ngr - 1), dB, xB);
+  for (int g = 2; g < ngr; g += 2) {
     group(dA, xA);
-    if (g + 1 >= ngr) break;
     load(min(g + 2, ngr - 1), dA, xA);
     group(dB, xB);
+    load(min(g + 3, ngr - 1), dB, xB);
   }
 
   // bias: sum the four lane groups of each column
@@ -167,21 +191,225 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
     }
   }
   // weights: lane holds G[n][kb .. kb+3]
+  if (P.splits > 1) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i) {
 #pragma unroll
-    for (int jn = 0; jn < 2; ++jn) {
-      const int n = nd[jn];
-      const int kb = k0 + 32 * wn + 16 * i + 4 * kc;
-      if (n >= N || kb >= K) continue;
-      if (P.splits > 1) {
+      for (int jn = 0; jn < 2; ++jn) {
+        const int n = nd[jn];
+        const int kb = k0 + 32 * wn + 16 * i + 4 * kc;
+        if (n >= N || kb >= K) continue;
         *(VFL_GLOBAL f32x4*)(glb(P.part) + ((int64_t)split * N + n) * P.kp + kb) = acc[i][jn];
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (kb + e < K) sgd_store<T>(P, n, kb + e, acc[i][jn][e], scale);
       }
     }
+  } else {
+    // every master value first (one wait), then the updates
+    float w[2][2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn) sgd_load4<T>(P, nd[jn], k0 + 32 * wn + 16 * i + 4 * kc, w[i][jn]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn)
+        sgd_store4<T>(P, nd[jn], k0 + 32 * wn + 16 * i + 4 * kc, w[i][jn], acc[i][jn], scale);
+  }
+}
+
+// The logit layer's block partials {loss, dl, dl * h} (one row of Hd + 2
+// floats per chain block): columns 4 lb .. 4 lb + 3, the rows split over 64
+// slices and summed slice by slice; then SGD of the logit weights and bias
+// and the group's mean loss.
+__device__ __forceinline__ void logit_reduce(const DwJob& J, int lb, int R, float scale, float* loss_out) {
+  __shared__ float red[64][5];
+  const int W = J.Hd + 2;
+  const int cl = threadIdx.x & 3, sl = threadIdx.x >> 2;
+  const int c = lb * 4 + cl;
+  const int rows = (R + J.lrows - 1) / J.lrows;
+  const VFL_GLOBAL float* lp = glb(J.lpart);
+  float acc = 0.f;
+  if (c < W) {
+    int b = sl;
+    for (; b + 3 * 64 < rows; b += 4 * 64) {
+      const float v0 = lp[(int64_t)b * W + c], v1 = lp[(int64_t)(b + 64) * W + c];
+      const float v2 = lp[(int64_t)(b + 128) * W + c], v3 = lp[(int64_t)(b + 192) * W + c];
+      acc += ((v0 + v1) + v2) + v3;
+    }
+    for (; b < rows; b += 64) acc += lp[(int64_t)b * W + c];
+  }
+  red[sl][cl] = acc;
+  __syncthreads();
+  if (sl == 0 && c < W) {
+    float tot = 0.f;
+    for (int i = 0; i < 64; ++i) tot += red[i][cl];
+    if (c == 0) {
+      if (loss_out) *glb(loss_out) = tot / (float)R;
+    } else if (c == 1) {
+      glb(J.lb)[0] -= scale * tot;
+    } else {
+      glb(J.lw)[c - 2] -= scale * tot;
+    }
+  }
+}
+
+// Unsplit weight gradient over 32 x 32 output tiles, for groups small
+// enough that one block can contract all their rows: the block's four
+// wavefronts take interleaved MFMA row steps (wavefront w: steps w, w + 4,
+// ...) and accumulate the whole tile each; the four sums meet in LDS and
+// are added in wavefront order; the SGD of the tile's master weights (and
+// bias, for the tiles of the first 32 inputs) and the operand-copy refresh
+// follow in the same block, so no reduction launch is needed.  Blocks past
+// the tiles reduce the logit layer's partials.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dw32(const DwJob* __restrict__ jp, int Rarg, float scale_arg,
+                                              float* loss_out, TickRef tr, float* loss_base) {
+  constexpr int RR = 16 / (int)sizeof(T);   // rows per chunk
+  constexpr int KR = 4 * RR;                // rows per MFMA step
+  constexpr int PF = 4;                     // MFMA steps per load group
+  const DwJob& J = *jp;
+  int R = Rarg;
+  float scale = scale_arg;
+  if (tr.src) {
+    const TickArgs ta = tick_args(tr);
+    R = ta.rows;
+    scale = ta.scale;
+    loss_out = loss_base ? loss_base + ta.loss_idx : nullptr;
+  }
+  if ((int)blockIdx.x >= J.blocks) {
+    logit_reduce(J, (int)blockIdx.x - J.blocks, R, scale, loss_out);
+    return;
+  }
+  int q = 0;
+#pragma unroll 1
+  while (q + 1 < J.n && (int)blockIdx.x >= J.p[q + 1].first_block) ++q;
+  const DwProb& P = J.p[q];
+  const int N = P.N, K = P.K;
+  const int tiles_k = (K + 31) / 32;
+  const int lb = blockIdx.x - P.first_block;
+  const int n0 = (lb / tiles_k) * 32, k0 = (lb % tiles_k) * 32;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int kc = lane >> 4, lr = lane & 15;
+  const bool do_bias = k0 == 0;
+
+  const VFL_GLOBAL char* dcol[2];
+  const VFL_GLOBAL char* xcol[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    dcol[i] = glb((const char*)P.D.p) + (int64_t)min(n0 + 16 * i + lr, N - 1) * 16;
+    xcol[i] = glb((const char*)P.X.p) + (int64_t)min(k0 + 16 * i + lr, K - 1) * 16;
+  }
+  const int64_t dcp = P.D.cp, xcp = P.X.cp;
+  // every wavefront takes the same number of row steps, covering all the
+  // RC rows (a multiple of 1024; the delta rows past the group are zero):
+  // an even number of load groups, no step conditional
+  const int nsw = J.rows_pad / KR / 4;                      // steps per wavefront
+  const int ngr = nsw / PF;                                 // load groups
+  // loads of group g (past the last group they repeat its last step:
+  // unconditional, never used)
+  auto load = [&](int g, u32x4 (&df)[PF][2], u32x4 (&xf)[PF][2]) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) {
+      const int sw = min(g * PF + st, nsw - 1);
+      const int64_t rg = (int64_t)(wave + 4 * sw) * (KR / RR) + kc;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        df[st][i] = *(const VFL_GLOBAL u32x4*)(dcol[i] + rg * dcp * 16);
+        xf[st][i] = *(const VFL_GLOBAL u32x4*)(xcol[i] + rg * xcp * 16);
+      }
+    }
+  };
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float bsum[2] = {0.f, 0.f};
+  auto group = [&](const u32x4 (&df)[PF][2], const u32x4 (&xf)[PF][2]) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) {
+          if constexpr (sizeof(T) == 2) {
+            acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, xf[st][i]), __builtin_bit_cast(bf16x8, df[st][jn]), acc[i][jn], 0, 0, 0);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  __uint_as_float(xf[st][i][e]), __uint_as_float(df[st][jn][e]), acc[i][jn], 0, 0, 0);
+          }
+        }
+      }
+      if (do_bias) {
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (sizeof(T) == 2) {
+              bsum[jn] += __uint_as_float(df[st][jn][e] << 16) + __uint_as_float(df[st][jn][e] & 0xffff0000u);
+            } else {
+              bsum[jn] += __uint_as_float(df[st][jn][e]);
+            }
+          }
+        }
+      }
+    }
+  };
+  // two groups in flight at the top of every iteration (A: group g, B:
+  // group g + 1); each is refilled as soon as its MFMAs have read it
+  // (the first iteration is peeled, so that the loop is entered with the
+  // loads in flight exactly as at its back edge: the compiler's wait
+  // counts stay exact)
+  u32x4 dA[PF][2], xA[PF][2], dB[PF][2], xB[PF][2];
+  load(0, dA, xA);
+  load(1, dB, xB);
+  group(dA, xA);
+  load(2, dA, xA);
+  group(dB, xB);
+  load(3, dB, xB);
+#pragma unroll 1
+  for (int g = 2; g < ngr; g += 2) {
+    group(dA, xA);
+    load(g + 2, dA, xA);
+    group(dB, xB);
+    load(g + 3, dB, xB);
+  }
+
+  // the SGD operands (their loads overlap the LDS reduction): thread t
+  // updates W[n0 + t / 8][k0 + 4 (t % 8) .. +4] and, t < 32, bias[n0 + t]
+  const int tn = threadIdx.x >> 3, tk = 4 * (threadIdx.x & 7);
+  float w[4];
+  sgd_load4<T>(P, n0 + tn, k0 + tk, w);
+  const float b0 = glb(P.bias)[min(n0 + (int)(threadIdx.x & 31), N - 1)];
+  // the wavefronts' tiles, added in wavefront order (rows padded to 9
+  // float4: the 16 lanes of a column group hit distinct banks)
+  __shared__ f32x4 red[4][32][9];
+  __shared__ float rb[4][32];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) red[wave][16 * jn + lr][4 * i + kc] = acc[i][jn];
+  if (do_bias) {
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) {
+      bsum[jn] += __shfl_xor(bsum[jn], 16, 64);
+      bsum[jn] += __shfl_xor(bsum[jn], 32, 64);
+    }
+    if (kc == 0) {
+      rb[wave][lr] = bsum[0];
+      rb[wave][16 + lr] = bsum[1];
+    }
+  }
+  __syncthreads();
+  const f32x4 g = ((red[0][tn][tk / 4] + red[1][tn][tk / 4]) + red[2][tn][tk / 4]) + red[3][tn][tk / 4];
+  sgd_store4<T>(P, n0 + tn, k0 + tk, w, g, scale);
+  if (do_bias && threadIdx.x < 32) {
+    const int n = n0 + threadIdx.x;
+    const float gb = ((rb[0][threadIdx.x] + rb[1][threadIdx.x]) + rb[2][threadIdx.x]) + rb[3][threadIdx.x];
+    if (n < N) glb(P.bias)[n] = b0 - scale * gb;
   }
 }
 
@@ -212,6 +440,8 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
         const int n = (int)(t / (P.kp / 4)), kb = (int)(t % (P.kp / 4)) * 4;
         const VFL_GLOBAL float* src = glb(P.part) + (int64_t)n * P.kp + kb;
         const int64_t stride = (int64_t)P.N * P.kp;
+        float w[4];
+        sgd_load4<T>(P, n, kb, w);
         f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
         int s = 0;
         for (; s + 8 <= P.splits; s += 8) {
@@ -222,50 +452,22 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
           for (int u = 0; u < 8; ++u) sum += v[u];
         }
         for (; s < P.splits; ++s) sum += *(const VFL_GLOBAL f32x4*)(src + s * stride);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (kb + e < P.K) sgd_store<T>(P, n, kb + e, sum[e], scale);
+        sgd_store4<T>(P, n, kb, w, sum, scale);
       } else {
         const int n = (int)(t - qw);
         const VFL_GLOBAL float* pb = glb(P.partb);
+        VFL_GLOBAL float* bias = glb(P.bias) + n;
+        const float b0 = *bias;
         float sum = 0.f;
+#pragma unroll 8
         for (int s = 0; s < P.splits; ++s) sum += pb[(int64_t)s * P.N + n];
-        glb(P.bias)[n] -= scale * sum;
+        *bias = b0 - scale * sum;
       }
       return;
     }
     return;
   }
-  // logit layer: column c of the block partials {loss, dl, dl * h}
-  __shared__ float red[64][5];
-  const int W = J.Hd + 2;
-  const int cl = threadIdx.x & 3, sl = threadIdx.x >> 2;
-  const int c = ((int)blockIdx.x - J.red_blocks) * 4 + cl;
-  const int rows = (R + J.lrows - 1) / J.lrows;
-  const VFL_GLOBAL float* lp = glb(J.lpart);
-  float acc = 0.f;
-  if (c < W) {
-    int b = sl;
-    for (; b + 3 * 64 < rows; b += 4 * 64) {
-      const float v0 = lp[(int64_t)b * W + c], v1 = lp[(int64_t)(b + 64) * W + c];
-      const float v2 = lp[(int64_t)(b + 128) * W + c], v3 = lp[(int64_t)(b + 192) * W + c];
-      acc += ((v0 + v1) + v2) + v3;
-    }
-    for (; b < rows; b += 64) acc += lp[(int64_t)b * W + c];
-  }
-  red[sl][cl] = acc;
-  __syncthreads();
-  if (sl == 0 && c < W) {
-    float tot = 0.f;
-    for (int i = 0; i < 64; ++i) tot += red[i][cl];
-    if (c == 0) {
-      if (loss_out) *glb(loss_out) = tot / (float)R;
-    } else if (c == 1) {
-      glb(J.lb)[0] -= scale * tot;
-    } else {
-      glb(J.lw)[c - 2] -= scale * tot;
-    }
-  }
+  logit_reduce(J, (int)blockIdx.x - J.red_blocks, R, scale, loss_out);
 }
 
 }  // namespace
@@ -275,6 +477,16 @@ hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, Ti
   if (blocks < 1) return hipErrorInvalidValue;
   if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
   else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw32(Elt e, const DwJob* job, int blocks, int R, float scale, float* loss_out,
+                      TickRef tr, float* loss_base, hipStream_t st) {
+  if (blocks < 1) return hipErrorInvalidValue;
+  if (e == BF16)
+    hipLaunchKernelGGL(k_dw32<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out, tr, loss_base);
+  else
+    hipLaunchKernelGGL(k_dw32<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, loss_out, tr, loss_base);
   return hipGetLastError();
 }
 

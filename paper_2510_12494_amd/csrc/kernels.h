@@ -113,12 +113,30 @@ struct RCMat { void* p = nullptr; int32_t cp = 0, pad = 0; };
 // Columns of `out` from N up to the next multiple of the MFMA depth are
 // written as zeros, as are rows beyond the group.  rc: RC copy of out.
 // mask_src (k_bwd): the mask is first loaded into `mask` from this matrix.
+// bl: byte offset of the layer's bias row in the kernel's LDS bias table
+// (-1: no bias).
 struct ChainLayer {
   const void* W = nullptr;
-  const float* bias = nullptr;
   int32_t kst = 0, N = 0, K = 0, relu = 0;
+  int32_t bl = -1;
   LBuf in, out, mask;
   RCMat rc, mask_src;
+};
+
+// The biases a chain kernel adds: one contiguous float32 array in global
+// memory (the masters of consecutive layers, each row padded to a multiple
+// of 32 floats), copied to LDS at byte offset `off` when the kernel starts.
+struct BiasTab {
+  const float* src = nullptr;
+  int32_t off = 0, n4 = 0;            // n4: float4 count
+};
+
+// The packed weight copies a chain kernel reads: up to two ranges of
+// 128-byte lines, fetched into L2 when the kernel starts (the workgroups of
+// one XCD each fetch a slice).
+struct WarmSet {
+  const void* p[2] = {nullptr, nullptr};
+  int32_t lines[2] = {0, 0};
 };
 
 // Bottom-model input of a row block: [embeddings of n_cat fields | dense],
@@ -161,6 +179,8 @@ struct ChainCall {
 // row when clipping; block 0 writes the slot header.
 struct FwdJob {
   RowInput in;
+  BiasTab bt;
+  WarmSet warm;
   int32_t L = 0;
   ChainLayer l[kMaxChain];
   void* z = nullptr; int32_t ldz = 0;
@@ -184,6 +204,8 @@ struct FwdJob {
 // the embedding columns.
 struct ActiveJob {
   RowInput in;
+  BiasTab bt;
+  WarmSet warm;
   int32_t LA = 0;
   ChainLayer fa[kMaxChain];
   LBuf cat; RCMat cat_rc; int32_t dA = 0, dB = 0;
@@ -214,6 +236,8 @@ struct ActiveJob {
 // clip), then the chain dx (l = L-1 .. 1), masks loaded from the stashed
 // RC activations; with tables, gx as in ActiveJob.
 struct BwdJob {
+  BiasTab bt;
+  WarmSet warm;
   const void* g = nullptr; int32_t ldg = 0;
   const void* z = nullptr; int32_t ldz = 0;
   const float* norm = nullptr; const float* cfac = nullptr;
@@ -264,11 +288,18 @@ struct DwJob {
   // layer's columns (lblocks partial rows of Hd + 2 floats, of which the
   // first ceil(rows / lrows) are the group's)
   int32_t red_threads = 0, red_blocks = 0;
+  int32_t rows_pad = 0;               // RC rows (k_dw32: its row steps cover them all)
   float* lpart = nullptr; int32_t Hd = 0, lrows = 0;
   float* lw = nullptr; float* lb = nullptr;
 };
 hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, TickRef tr,
                      hipStream_t st);
+// Unsplit problems over 32 x 32 tiles (every problem's splits == 1, tiles
+// counted with 32-wide tiles; `blocks` = job->blocks + the logit blocks):
+// products, SGD and copy refresh in one launch, the logit reduction in the
+// blocks past job->blocks (loss_out / loss_base as for k_dw_reduce).
+hipError_t launch_dw32(Elt e, const DwJob* job, int blocks, int R, float scale, float* loss_out,
+                       TickRef tr, float* loss_base, hipStream_t st);
 // loss_out: the group's mean loss (from the logit partials); with a tick
 // reference, loss_base + the tick's loss index instead.
 hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
