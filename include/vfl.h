@@ -37,7 +37,9 @@
  * vfl_get_param, vfl_get_message, vfl_check, vfl_get_trace and vfl_destroy.
  *
  * Errors.  Every call returns a vfl_status; nothing else crosses the ABI.
- * vfl_last_error() gives a text for the last failure on a context.
+ * vfl_last_error() gives a text for the last failure on a context; with a
+ * NULL context, the text of the calling thread's last vfl_workspace_size or
+ * vfl_create failure (empty after a success).
  */
 #ifndef VFL_H
 #define VFL_H
@@ -279,6 +281,9 @@ vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t class_mask);
 vfl_status vfl_timing_read(vfl_ctx* c, int32_t kernel_class, double* ms, int64_t* launches,
                            double* work);
 
+/* Text of the last failure on c (owned by the context, valid until its next
+ * call); c == NULL: the calling thread's last vfl_workspace_size/vfl_create
+ * failure (thread-local storage, valid until that thread's next such call). */
 const char* vfl_last_error(const vfl_ctx* c);
 
 /* Synchronise both streams and release the context's events and host state.

@@ -221,8 +221,17 @@ namespace {
 template <typename T>
 T* at(vfl_ctx* c, size_t off) { return (T*)(c->ws + off); }
 
+// Failures of calls that have no context yet (vfl_workspace_size, vfl_create)
+// keep their text per host thread; vfl_last_error(NULL) returns it.
+thread_local std::string t_create_err;
+
 vfl_status fail(vfl_ctx* c, vfl_status st, const std::string& msg) {
   if (c) c->err = msg;
+  return st;
+}
+
+vfl_status fail_create(vfl_status st, const std::string& msg) {
+  t_create_err = msg;
   return st;
 }
 
@@ -554,7 +563,10 @@ MsgOp msg_op(const vfl_opts& o, bool clip, bool noise, uint32_t tag) {
 // and mask buffers N columns, all inside the block's LDS, and the packed
 // operand has the K steps of the product; the RC copy holds
 // rc_cols columns (N unless given).
-bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_out, int rc_cols = -1) {
+// rc_cols / out_cols: the columns the RC copy / the LDS output hold when
+// fewer than N (the concat product keeps only A's columns of both).
+bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_out, int rc_cols = -1,
+                int out_cols = -1) {
   const int es = elt_size(p.e), KS = p.e == BF16 ? 32 : 16;
   auto inside = [&](const LBuf& b, int cols) {
     const int need = (cols + KS - 1) / KS * KS * es;
@@ -563,7 +575,7 @@ bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_ou
   if (!L.W || L.N < 1 || L.K < 1 || L.kst != (L.K + KS - 1) / KS) return false;
   if (L.bl >= 0 && (L.bl % 16 || L.bl + 4 * ((L.N + 31) / 32 * 32) > lds)) return false;
   if (!inside(L.in, L.K)) return false;
-  if (lds_out && !inside(L.out, L.N)) return false;
+  if (lds_out && !inside(L.out, out_cols < 0 ? L.N : out_cols)) return false;
   if (L.mask.pitch && !inside(L.mask, L.N)) return false;
   if (L.rc.p && L.rc.cp < ((rc_cols < 0 ? L.N : rc_cols) + 7) / 8 * 8) return false;
   return true;
@@ -780,7 +792,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     for (int l = 0; l < aj[q].LA; ++l) ok = ok && layer_fits(p, aj[q].fa[l], ba, p.ka.lds, true);
     for (int j = 0; j < aj[q].H; ++j) ok = ok && layer_fits(p, aj[q].ft[j], ba, p.ka.lds, true);
     for (int j = 0; j + 1 < aj[q].H; ++j) ok = ok && layer_fits(p, aj[q].dt[j], ba, p.ka.lds, true);
-    ok = ok && layer_fits(p, aj[q].dc, ba, p.ka.lds, true, p.dA);   // RC copy: A's columns only
+    ok = ok && layer_fits(p, aj[q].dc, ba, p.ka.lds, true, p.dA, p.dA);   // A's columns only
     for (int l = 0; l < aj[q].nda; ++l) ok = ok && layer_fits(p, aj[q].da[l], ba, p.ka.lds, true);
     if (aj[q].has_gx) ok = ok && layer_fits(p, aj[q].gx, ba, p.ka.lds, false);
     for (int l = 0; l < bj[q].nd; ++l) ok = ok && layer_fits(p, bj[q].dx[l], bb, p.kb.lds, true);
@@ -1157,12 +1169,15 @@ extern "C" {
 
 vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
                               const vfl_top_spec* top, const vfl_opts* o, size_t* bytes) {
-  if (!bytes) return VFL_E_INVALID;
+  if (!bytes) return fail_create(VFL_E_INVALID, "null bytes");
   Plan p;
-  if (!build_plan(a, b, top, o, p).empty()) return VFL_E_INVALID;
+  std::string why = build_plan(a, b, top, o, p);
+  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
   // the kernels' layouts are checked here already (against a nominal base)
   Jobs J;
-  if (!build_jobs(p, *o, (char*)(uintptr_t)4096, J).empty()) return VFL_E_INVALID;
+  why = build_jobs(p, *o, (char*)(uintptr_t)4096, J);
+  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
+  t_create_err.clear();
   *bytes = p.total;
   return VFL_OK;
 }
@@ -1170,13 +1185,16 @@ vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b
 vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* top,
                       const vfl_opts* o, void* workspace, size_t bytes, void* stream_a,
                       void* stream_b, vfl_ctx** out) {
-  if (!out) return VFL_E_INVALID;
+  if (!out) return fail_create(VFL_E_INVALID, "null out");
   *out = nullptr;
   vfl_ctx* c = new vfl_ctx();
   std::string why = build_plan(a, b, top, o, c->p);
-  if (!why.empty()) { delete c; return VFL_E_INVALID; }
-  if (!workspace || ((uintptr_t)workspace) % 256) { delete c; return VFL_E_INVALID; }
-  if (bytes < c->p.total) { delete c; return VFL_E_NOMEM; }
+  if (!why.empty()) { delete c; return fail_create(VFL_E_INVALID, why); }
+  if (!workspace || ((uintptr_t)workspace) % 256) {
+    delete c;
+    return fail_create(VFL_E_INVALID, "workspace null or not 256-byte aligned");
+  }
+  if (bytes < c->p.total) { delete c; return fail_create(VFL_E_NOMEM, "workspace too small"); }
   c->o = *o;
   c->ws = (char*)workspace;
   c->sa = (hipStream_t)stream_a;
@@ -1197,13 +1215,15 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
   if (e == hipSuccess) e = hipStreamSynchronize(c->sa);
   if (e != hipSuccess) {
     vfl_destroy(c);
-    return VFL_E_HIP;
+    return fail_create(VFL_E_HIP, std::string("context set-up: ") + hipGetErrorString(e));
   }
   const vfl_status js = write_jobs(c);
   if (js != VFL_OK) {
+    const std::string msg = c->err;
     vfl_destroy(c);
-    return js;
+    return fail_create(js, msg);
   }
+  t_create_err.clear();
   *out = c;
   return VFL_OK;
 }
@@ -1633,7 +1653,7 @@ vfl_status vfl_timing_read(vfl_ctx* c, int32_t cls, double* ms, int64_t* launche
   return VFL_OK;
 }
 
-const char* vfl_last_error(const vfl_ctx* c) { return c ? c->err.c_str() : "null context"; }
+const char* vfl_last_error(const vfl_ctx* c) { return c ? c->err.c_str() : t_create_err.c_str(); }
 
 vfl_status vfl_destroy(vfl_ctx* c) {
   if (!c) return VFL_E_INVALID;

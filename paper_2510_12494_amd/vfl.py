@@ -106,10 +106,10 @@ _lib = _load()
 
 def _chk(st: int, where: str, ctx=None):
     if st != VFL_OK:
-        text = ""
-        if ctx:
-            raw = _lib.vfl_last_error(ctx)
-            text = raw.decode() if raw else ""
+        # without a context the text is the calling thread's last
+        # vfl_workspace_size / vfl_create failure
+        raw = _lib.vfl_last_error(ctx)
+        text = raw.decode() if raw else ""
         raise VflError(st, where, text)
 
 

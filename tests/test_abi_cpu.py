@@ -87,3 +87,55 @@ def test_invalid_configurations_are_rejected(V, bad):
     with pytest.raises(V.VflError) as e:
         V.vfl_workspace_size(a, b, t, o)
     assert e.value.status == V.VFL_E_INVALID
+
+
+def test_create_failures_report_their_reason(V):
+    """A rejected configuration leaves its reason in vfl_last_error(NULL)."""
+    from paper_2510_12494_amd.session import bottom_spec, top_spec, opts
+    w = S.get("dense_tabular")
+    a, b, t, o = bottom_spec(w.A), bottom_spec(w.B), top_spec(w.top), opts(w)
+    o.staleness = 5
+    with pytest.raises(V.VflError) as e:
+        V.vfl_workspace_size(a, b, t, o)
+    assert "staleness" in str(e.value)
+    o.staleness = 2
+    assert V.vfl_workspace_size(a, b, t, o) > 0
+    assert V.vfl_last_error(None) == ""
+
+
+def _random_shape(rng, dtype):
+    from vfl_synth.workloads import Workload, PartySpec, TopSpec
+    def widths(n, last_mult):
+        ws = [int(rng.integers(1, 300)) for _ in range(n)]
+        ws[-1] = int(rng.integers(1, 40)) * last_mult
+        return ws
+    cat = bool(rng.integers(0, 2))
+    A = PartySpec(dense=int(rng.integers(1, 90)), widths=widths(int(rng.integers(1, 4)), 8))
+    B = PartySpec(dense=int(rng.integers(0 if cat else 1, 90)), widths=widths(int(rng.integers(1, 4)), 1),
+                  n_cat=int(rng.integers(1, 4)) if cat else 0, vocab=50, emb_dim=4 * int(rng.integers(1, 5)))
+    top = TopSpec(widths=[int(rng.integers(1, 300)) for _ in range(int(rng.integers(1, 3)))] + [1])
+    extra = bool(rng.integers(0, 2))
+    return Workload(name="shape", n_rows=1000, dtype=dtype, A=A, B=B, top=top,
+                    batch=int(rng.integers(1, 3000)), staleness=int(rng.integers(0, 5)),
+                    replicas=int(rng.integers(1, 5)), lr=0.01, clip=1.0 if extra else 0.0,
+                    sigma=0.5 if extra else 0.0, clip_emb=extra, clip_grad=extra, noise_emb=extra,
+                    noise_grad=extra)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_host_plan_covers_random_shapes(V, dtype):
+    """The host plan checks every chain layer's LDS and RC layout against
+    what the kernels touch; any shape within the documented limits must
+    pass (a failure here is an internal layout error, reported by text)."""
+    import numpy as np
+    from paper_2510_12494_amd.session import bottom_spec, top_spec, opts
+    rng = np.random.default_rng(7 if dtype == "f32" else 8)
+    for _ in range(300):
+        w = _random_shape(rng, dtype)
+        try:
+            n = V.vfl_workspace_size(bottom_spec(w.A), bottom_spec(w.B), top_spec(w.top), opts(w))
+        except V.VflError as e:
+            # only the LDS capacity may refuse a shape within the limits
+            assert "exceed the LDS" in str(e), (w, str(e))
+            continue
+        assert n > 0
