@@ -71,6 +71,7 @@ struct Party {
   size_t norm[kMaxSlots]{}, cfac[kMaxSlots]{};
   size_t gx = 0;
   int64_t ldgx = 0;
+  size_t idt[kMaxSlots]{};                      // field-major id copies (tables)
   size_t part[VFL_MAX_LAYERS]{}, partb[VFL_MAX_LAYERS]{};
   int bo[VFL_MAX_LAYERS]{};                     // bias offsets (floats) in the party's bias table
   size_t wq_end[kMaxSlots]{}, wtq_end[kMaxSlots]{};   // ends of the packed ranges
@@ -453,6 +454,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     if (s->n_cat) {
       P.ldgx = ld_of(s->n_cat * s->emb_dim);
       P.gx = ly.take(sizeof(float) * R * P.ldgx);
+      for (int q = 0; q < nslots; ++q) P.idt[q] = ly.take(sizeof(int32_t) * R * s->n_cat);
     }
   };
 
@@ -624,6 +626,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     f.in.dense_in = P.spec.dense_in; f.in.n_cat = P.spec.n_cat; f.in.V = P.spec.vocab; f.in.E = P.spec.emb_dim;
     f.in.dense_vec = P.spec.n_cat == 0;
     f.in.T = P.spec.n_cat ? at_f(P.T) : nullptr;
+    f.in.idt = P.spec.n_cat ? (int32_t*)(ws + P.idt[q]) : nullptr; f.in.ldi = p.R;
     f.in.buf = p.lf.buf[0];
     f.in.rc = rcm(c, P.x0rc[q], P.din);
     f.bt.src = at_f(p.bias_b); f.bt.off = p.lf.bias.off; f.bt.n4 = p.nbias_b / 4;
@@ -649,6 +652,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     a.in.dense_in = A.spec.dense_in; a.in.n_cat = A.spec.n_cat; a.in.V = A.spec.vocab; a.in.E = A.spec.emb_dim;
     a.in.dense_vec = A.spec.n_cat == 0;
     a.in.T = A.spec.n_cat ? at_f(A.T) : nullptr;
+    a.in.idt = A.spec.n_cat ? (int32_t*)(ws + A.idt[0]) : nullptr; a.in.ldi = p.R;
     a.in.buf = la.in;
     a.in.rc = rcm(c, A.x0rc[0], A.din);
     a.bt.src = at_f(p.bias_a); a.bt.off = la.bias.off; a.bt.n4 = p.nbias_a / 4;
@@ -991,11 +995,11 @@ double party_dx_flops(const Party& P, int R) {
 }
 
 // sparse SGD of a party's tables from its float32 input gradient gx
-vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, const int32_t* ids, int R, float scale,
-                             hipStream_t st, TickRef tr) {
+vfl_status enqueue_table_sgd(vfl_ctx* c, const Party& P, int slot, int R, float scale, hipStream_t st,
+                             TickRef tr) {
   if (!P.spec.n_cat) return VFL_OK;
-  ScatterJob sj{at<float>(c, P.T), ids, P.spec.n_cat, P.spec.vocab, P.spec.emb_dim,
-                at<float>(c, P.gx), P.ldgx, R, scale, tr};
+  ScatterJob sj{at<float>(c, P.T), at<int32_t>(c, P.idt[slot]), c->p.R, P.spec.n_cat, P.spec.vocab,
+                P.spec.emb_dim, at<float>(c, P.gx), P.ldgx, R, scale, tr};
   TIMED(VFL_K_EMB_SGD, (double)R * P.spec.n_cat * 4.0 * (1 + P.spec.emb_dim), st,
         launch_scatter_sgd(sj, st));
   return VFL_OK;
@@ -1082,7 +1086,7 @@ vfl_status a_backward(vfl_ctx* c, const SlotState& st, float* loss, TickRef tr) 
   const Plan& p = c->p;
   vfl_status r = enqueue_dw(c, true, 0, st.rows, loss, tr, c->sa);
   if (r) return r;
-  return enqueue_table_sgd(c, p.A, st.ids, st.rows, c->o.lr / (float)st.rows, c->sa, tr);
+  return enqueue_table_sgd(c, p.A, 0, st.rows, c->o.lr / (float)st.rows, c->sa, tr);
 }
 
 // B's delayed backward of the group stashed in `slot` + SGD on B's current
@@ -1096,7 +1100,7 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
         launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
   vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, tr, c->sb);
   if (r) return r;
-  return enqueue_table_sgd(c, p.P, st.ids, st.rows, c->o.lr / (float)st.rows, c->sb, tr);
+  return enqueue_table_sgd(c, p.P, slot, st.rows, c->o.lr / (float)st.rows, c->sb, tr);
 }
 
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {

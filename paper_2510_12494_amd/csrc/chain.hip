@@ -443,6 +443,15 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
   const VFL_GLOBAL T* dense = glb((const T*)cc.dense);
   const VFL_GLOBAL int32_t* ids = glb(cc.ids);
   const VFL_GLOBAL float* tab = glb(in.T);
+  if (in.idt) {
+    // field-major copy of the block's ids (read contiguously)
+    VFL_GLOBAL int32_t* idt = glb(in.idt);
+    const VFL_GLOBAL int32_t* src = ids + (k.in_off + r0) * in.n_cat;
+    for (int u = threadIdx.x; u < rv * in.n_cat; u += kNT) {
+      const int r = u / in.n_cat, f = u - r * in.n_cat;
+      idt[(int64_t)f * in.ldi + r0 + r] = src[u];
+    }
+  }
   for (int u = threadIdx.x; u < BR * nch; u += kNT) {
     const int r = u / nch, ch = u % nch, c0 = ch * CE;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};

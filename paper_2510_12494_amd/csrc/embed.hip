@@ -2,122 +2,252 @@
 // gfx950 (the gather of the looked-up rows is part of the chain kernels'
 // input stage).
 //
-// The sparse step sums, for every table row a batch touches, the gradient
-// rows of all samples that looked it up, and applies SGD once per touched
-// row.  One workgroup owns one field: it sorts the (id, row) keys of up to
-// 8192 samples in LDS (bitonic network over unique 32-bit keys, so the order
-// is deterministic), walks the sorted keys in 16-key pieces per thread,
-// and combines the pieces of each id in sample order; the table row is then
-// updated with a single rounding.  Fields own disjoint table rows, so the
-// workgroups never write the same address.
+// The sparse step (Eq. 2 restricted to the table rows a batch touches) sums,
+// for every touched table row, the gradient rows of all samples that looked
+// it up, and applies SGD once per touched row.
+//
+// Work split: workgroup (field f, part p) owns the ids of field f with
+// id mod P == p (P = 16), so no two workgroups ever write the same table row and the
+// hot ids of a Zipf field (small ids) land in different parts.  Per pass of
+// up to 8192 samples a workgroup
+//   1. collects its (id / P, row) keys into LDS from the field's row of the
+//      field-major id copy (a block scan of per-thread match counts places
+//      them; the keys are unique, so their order does not matter),
+//   2. sorts them (bitonic network over 2, 8 or 32 keys per thread held in
+//      registers, so the order is deterministic: by id, then by sample),
+//   3. stages the gradient rows of the sorted keys and the table rows of
+//      their ids in LDS, 512 positions at a time (every global load of a
+//      stage issued before the first is waited for), and forms segmented
+//      sums per id with a fixed-shape scan: 64 scanners per 4-column chunk
+//      each reduce 8 consecutive positions, an exclusive segmented scan
+//      combines the scanners (lanes in order, then wavefronts in order),
+//      and each scanner walks its positions again, storing the updated
+//      table row where its id's segment ends.
+// The summation order depends only on the sorted positions, so two runs
+// give bitwise the same tables.
 #include <algorithm>
 
+#include "device.h"
 #include "kernels.h"
 
 namespace vfl {
 namespace {
+using namespace dev;
 
-constexpr int kSortN = 8192;               // samples sorted per pass
-constexpr int kThreads = 512;
-constexpr int kPer = kSortN / kThreads;    // sorted keys walked per thread
-constexpr int kRowBits = 13;               // kSortN == 1 << kRowBits
+constexpr int kThreads = 256;
+constexpr int kRowBits = 13;
+constexpr int kPass = 1 << kRowBits;           // samples per pass
+constexpr uint32_t kRowMask = kPass - 1;
+constexpr int kStage = 512;                    // sorted positions staged at a time
+constexpr int kScanners = kThreads / 4;        // per 4-column chunk
+constexpr int kSpan = kStage / kScanners;      // positions per scanner
+constexpr int kRowsPerThread = kPass / kThreads;     // rows a thread tests per pass
+constexpr int kParts = 16;                     // id parts per field (id mod kParts)
+constexpr int kStageLoads = kStage * 4 / kThreads;   // (gradient, table) pairs per thread and stage
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
-__global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
-  __shared__ uint32_t keys[kSortN];
-  __shared__ float facc[kThreads][kMaxEmbDim], lacc[kThreads][kMaxEmbDim];
-  __shared__ uint32_t fid[kThreads], lid[kThreads];
-  __shared__ uint8_t single[kThreads];
-  const int tid = threadIdx.x;
-  const int f = blockIdx.x;
-  const int E = j.E;
-  if (j.tr.src) {
-    const TickArgs ta = tick_args(j.tr);
-    j.R = ta.rows;
-    j.scale = ta.scale;
-    j.ids += ta.row0 * j.n_cat;
-  }
-  float* table = j.T + (int64_t)f * j.V * E;
+// segmented-scan operator on (head seen, value): a later head restarts the sum
+__device__ __forceinline__ void seg_combine(bool& F, f32x4& V, bool f2, const f32x4& v2) {
+  V = f2 ? v2 : V + v2;
+  F = F || f2;
+}
 
-  auto apply = [&](uint32_t id, const float (&s)[kMaxEmbDim]) {
-    float* row = table + (int64_t)id * E;
-    for (int e = 0; e < E; ++e) row[e] -= j.scale * s[e];
-  };
+__device__ __forceinline__ f32x4 shfl_up4(const f32x4& v, int d) {
+  f32x4 r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = __shfl_up(v[e], d, 64);
+  return r;
+}
 
-  for (int c0 = 0; c0 < j.R; c0 += kSortN) {
-    const int n = min(kSortN, j.R - c0);
-    for (int i = tid; i < kSortN; i += kThreads)
-      keys[i] = i < n ? ((uint32_t)j.ids[(int64_t)(c0 + i) * j.n_cat + f] << kRowBits) | (uint32_t)i
-                      : kNone;
-    __syncthreads();
-    for (int k = 2; k <= kSortN; k <<= 1) {
-      for (int h = k >> 1; h > 0; h >>= 1) {
-        for (int i = tid; i < kSortN; i += kThreads) {
-          const int l = i ^ h;
-          if (l > i) {
-            const uint32_t a = keys[i], b = keys[l];
-            const bool up = (i & k) == 0;
-            if (up ? (a > b) : (a < b)) { keys[i] = b; keys[l] = a; }
-          }
+// Bitonic sort of a[0, n) (n <= kThreads * KPT) into ascending order over
+// N = kThreads * KPT slots, a[n, N) padded with kNone.  Thread t holds the
+// slots [t * KPT, t * KPT + KPT) in registers: compare-exchange distances
+// below KPT stay in the thread, those below 64 * KPT go through wavefront
+// shuffles, and only the longer ones through LDS.  Ends with a[0, N)
+// written back and a barrier.
+template <int KPT>
+__device__ __forceinline__ void bitonic(uint32_t* a, int n) {
+  constexpr int N = kThreads * KPT;
+  const int t = threadIdx.x;
+  uint32_t x[KPT];
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) x[e] = t * KPT + e < n ? a[t * KPT + e] : kNone;
+  for (int k = 2; k <= N; k <<= 1) {
+    for (int h = k >> 1; h >= KPT; h >>= 1) {
+      // bit k of a slot index lies in t * KPT (k > h >= KPT)
+      const bool asc = ((t * KPT) & k) == 0;
+      const bool lower = ((t * KPT) & h) == 0;
+      const bool keep_min = asc == lower;
+      if (h < 64 * KPT) {
+        const int m = h / KPT;
+#pragma unroll
+        for (int e = 0; e < KPT; ++e) {
+          const uint32_t o = (uint32_t)__shfl_xor((int)x[e], m, 64);
+          x[e] = keep_min ? min(x[e], o) : max(x[e], o);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < KPT; ++e) a[t * KPT + e] = x[e];
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < KPT; ++e) {
+          const uint32_t o = a[(t * KPT + e) ^ h];
+          x[e] = keep_min ? min(x[e], o) : max(x[e], o);
         }
         __syncthreads();
       }
     }
-    // walk this thread's sorted keys; pieces strictly inside are complete ids
-    uint32_t cur = kNone, first = kNone;
-    float acc[kMaxEmbDim];
-    for (int e = 0; e < kMaxEmbDim; ++e) acc[e] = 0.f;
-    int pieces = 0;
-    for (int p = 0; p < kPer; ++p) {
-      const uint32_t key = keys[tid * kPer + p];
-      if (key == kNone) break;
-      const uint32_t id = key >> kRowBits;
-      const int r = (int)(key & (kSortN - 1));
-      if (id != cur) {
-        if (cur != kNone) {
-          if (pieces == 1) {
-            for (int e = 0; e < E; ++e) facc[tid][e] = acc[e];
-          } else {
-            apply(cur, acc);
-          }
-        }
-        if (pieces == 0) first = id;
-        cur = id;
-        ++pieces;
-        for (int e = 0; e < E; ++e) acc[e] = 0.f;
-      }
-      const float* g = j.G + (int64_t)(c0 + r) * j.ldg + f * E;
-      for (int e = 0; e < E; ++e) acc[e] += g[e];
-    }
-    fid[tid] = first;
-    lid[tid] = cur;
-    single[tid] = pieces == 1;
-    if (pieces >= 1) {
-      if (pieces == 1) {
-        for (int e = 0; e < E; ++e) facc[tid][e] = acc[e];
-      } else {
-        for (int e = 0; e < E; ++e) lacc[tid][e] = acc[e];
+    // distances below KPT: inside the thread
+#pragma unroll
+    for (int h = KPT / 2; h >= 1; h >>= 1) {
+      if (h >= k) continue;
+#pragma unroll
+      for (int e = 0; e < KPT; ++e) {
+        if (e & h) continue;
+        const bool asc = ((t * KPT + e) & k) == 0;
+        const uint32_t lo = min(x[e], x[e + h]), hi = max(x[e], x[e + h]);
+        x[e] = asc ? lo : hi;
+        x[e + h] = asc ? hi : lo;
       }
     }
+  }
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) a[t * KPT + e] = x[e];
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
+  __shared__ uint32_t keys[kPass];
+  __shared__ f32x4 gs[kStage][4], ts[kStage][4];
+  __shared__ f32x4 wv[kThreads / 64][4];
+  __shared__ int wf[kThreads / 64][4];
+  __shared__ int wcnt[kThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int f = blockIdx.x / kParts, part = blockIdx.x % kParts;
+  int R = j.R;
+  float scale = j.scale;
+  if (j.tr.src) {
+    const TickArgs ta = tick_args(j.tr);
+    R = ta.rows;
+    scale = ta.scale;
+  }
+  const int EC = j.E / 4;                       // 4-column chunks per table row
+  const VFL_GLOBAL int32_t* ids = glb(j.idt) + (int64_t)f * j.ldi;
+  const VFL_GLOBAL f32x4* G = glb((const f32x4*)j.G);
+  const int64_t ldg4 = j.ldg / 4;
+  VFL_GLOBAL f32x4* Tf = glb((f32x4*)(j.T + (int64_t)f * j.V * j.E));
+  const int q = tid >> 2, ch = tid & 3;         // scanner, chunk
+
+  for (int c0 = 0; c0 < R; c0 += kPass) {
+    const int n = min(kPass, R - c0);
+    // 1. this part's keys: every thread tests kPass / kThreads rows (strided,
+    // so each load instruction of a wavefront is contiguous), then a block
+    // scan of the per-thread counts places them
+    uint32_t idv[kRowsPerThread];
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) idv[i] = (uint32_t)ids[c0 + min(i * kThreads + tid, n - 1)];
+    uint32_t take = 0u;
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+      const bool tk = i * kThreads + tid < n && (idv[i] & (kParts - 1)) == (uint32_t)part;
+      take |= (uint32_t)tk << i;
+      c += tk;
+    }
+    int incl = c;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(incl, d, 64);
+      if (lane >= d) incl += v;
+    }
+    if (lane == 63) wcnt[wave] = incl;
     __syncthreads();
-    // an id's pieces lie in consecutive threads; its first piece's owner sums
-    // them in thread (= sample) order and applies the update once
-    float tot[kMaxEmbDim];
-    auto gather_from = [&](uint32_t id, int t0) {
-      for (int t = t0; t < kThreads && fid[t] == id; ++t) {
-        for (int e = 0; e < E; ++e) tot[e] += facc[t][e];
-        if (!single[t]) break;
-      }
-    };
-    if (fid[tid] != kNone && (tid == 0 || lid[tid - 1] != fid[tid])) {
-      for (int e = 0; e < E; ++e) tot[e] = facc[tid][e];
-      if (single[tid]) gather_from(fid[tid], tid + 1);
-      apply(fid[tid], tot);
+    int pos = incl - c, total = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+      const int x = wcnt[w];
+      pos += w < wave ? x : 0;
+      total += x;
     }
-    if (lid[tid] != kNone && !single[tid]) {
-      for (int e = 0; e < E; ++e) tot[e] = lacc[tid][e];
-      gather_from(lid[tid], tid + 1);
-      apply(lid[tid], tot);
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i)
+      if ((take >> i) & 1u) keys[pos++] = ((idv[i] / kParts) << kRowBits) | (uint32_t)(i * kThreads + tid);
+    __syncthreads();
+    const int np = total;
+    // 2. sort keys[0, np) ascending (padding kNone sorts last)
+    if (np <= 2 * kThreads) bitonic<2>(keys, np);
+    else if (np <= 8 * kThreads) bitonic<8>(keys, np);
+    else bitonic<32>(keys, np);
+    // 3. segmented sums, kStage sorted positions at a time
+    f32x4 carry = f32x4{0.f, 0.f, 0.f, 0.f};    // the open segment entering the stage
+    for (int s0 = 0; s0 < np; s0 += kStage) {
+      const int ns = min(kStage, np - s0);
+      {
+        // loads clamped into range, so all are unconditional and in flight
+        // together; chunks past E repeat the last one (never stored back)
+        f32x4 gv[kStageLoads], tv[kStageLoads];
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+          const int i = min(u * kThreads + tid, ns * 4 - 1);
+          const int c = min(i & 3, EC - 1);
+          const uint32_t key = keys[s0 + (i >> 2)];
+          gv[u] = G[(int64_t)(c0 + (key & kRowMask)) * ldg4 + f * EC + c];
+          tv[u] = Tf[(int64_t)((key >> kRowBits) * (uint32_t)kParts + (uint32_t)part) * EC + c];
+        }
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+          const int i = u * kThreads + tid;
+          if (i < ns * 4) { gs[i >> 2][i & 3] = gv[u]; ts[i >> 2][i & 3] = tv[u]; }
+        }
+      }
+      __syncthreads();
+      auto head = [&](int a) { return a == 0 || (keys[a] >> kRowBits) != (keys[a - 1] >> kRowBits); };
+      const int p0 = q * kSpan, p1 = min(p0 + kSpan, ns);
+      // (a) the scanner's aggregate
+      bool F = false;
+      f32x4 V = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int i = p0; i < p1; ++i) seg_combine(F, V, head(s0 + i), gs[i][ch]);
+      // (b) inclusive scan over the 16 scanners of the wavefront (lanes 4 apart)
+      bool Fi = F;
+      f32x4 Vi = V;
+#pragma unroll
+      for (int d = 1; d < 16; d <<= 1) {
+        const f32x4 vu = shfl_up4(Vi, 4 * d);
+        const bool fu = __shfl_up((int)Fi, 4 * d, 64) != 0;
+        if ((lane >> 2) >= d) {
+          // (fu, vu) comes first: (fu, vu) then (Fi, Vi)
+          Vi = Fi ? Vi : vu + Vi;
+          Fi = Fi || fu;
+        }
+      }
+      if ((lane >> 2) == 15) { wv[wave][ch] = Vi; wf[wave][ch] = Fi; }
+      // exclusive prefix within the wavefront
+      f32x4 Ve = shfl_up4(Vi, 4);
+      bool Fe = __shfl_up((int)Fi, 4, 64) != 0;
+      if ((lane >> 2) == 0) { Ve = f32x4{0.f, 0.f, 0.f, 0.f}; Fe = false; }
+      __syncthreads();
+      // carry-in: stage carry, then the earlier wavefronts in order, then
+      // the earlier scanners of this wavefront
+      bool Fc = false;
+      f32x4 Vc = carry;
+      for (int w = 0; w < wave; ++w) seg_combine(Fc, Vc, wf[w][ch] != 0, wv[w][ch]);
+      seg_combine(Fc, Vc, Fe, Ve);
+      // (c) walk again; update where a segment ends
+      f32x4 run = Vc;
+      for (int i = p0; i < p1; ++i) {
+        const int a = s0 + i;
+        const f32x4 g = gs[i][ch];
+        run = head(a) ? g : run + g;
+        const bool last = a + 1 == np || (keys[a + 1] >> kRowBits) != (keys[a] >> kRowBits);
+        if (last && ch < EC) {
+          const uint32_t id = (keys[a] >> kRowBits) * (uint32_t)kParts + (uint32_t)part;
+          Tf[(int64_t)id * EC + ch] = ts[i][ch] - scale * run;
+        }
+      }
+      // the open segment after the whole stage
+      bool Ft = false;
+      for (int w = 0; w < kThreads / 64; ++w) seg_combine(Ft, carry, wf[w][ch] != 0, wv[w][ch]);
+      __syncthreads();
     }
     __syncthreads();
   }
@@ -126,8 +256,8 @@ __global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
 }  // namespace
 
 hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st) {
-  if (j.E > kMaxEmbDim || j.V > (1 << (32 - kRowBits))) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_embed_sgd, dim3(j.n_cat), dim3(kThreads), 0, st, j);
+  if (j.E > kMaxEmbDim || j.E % 4 || j.ldg % 4 || j.V > (1 << (32 - kRowBits))) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed_sgd, dim3(j.n_cat * kParts), dim3(kThreads), 0, st, j);
   return hipGetLastError();
 }
 

@@ -141,11 +141,14 @@ struct WarmSet {
 
 // Bottom-model input of a row block: [embeddings of n_cat fields | dense],
 // gathered into LDS (`buf`) and copied to `rc` (for the first layer's
-// weight gradient).  T: float32 tables [n_cat * V x E].
+// weight gradient).  T: float32 tables [n_cat * V x E]; idt (with tables):
+// field-major copy of the group's ids, idt[f * ldi + tick row], for the
+// sparse table step.
 struct RowInput {
   int32_t dense_in = 0, n_cat = 0, V = 0, E = 0;
   int32_t dense_vec = 0;              // dense rows 16-byte aligned: vector loads
   const float* T = nullptr;
+  int32_t* idt = nullptr; int32_t ldi = 0;
   LBuf buf;
   RCMat rc;
 };
@@ -315,14 +318,15 @@ struct CastJob {
 hipError_t launch_cast(Elt e, const CastJob* jobs, int n_jobs, hipStream_t st);
 
 // Sparse SGD on the tables: for every row f*V + id touched by field f,
-// T[row][c] -= scale * sum over samples r with ids[r][f] == id of G[r][f*E + c]
-// (one rounding per touched row; deterministic).  E <= kMaxEmbDim,
-// V <= 2^19.
+// T[row][c] -= scale * sum over samples r with idt[f][r] == id of G[r][f*E + c]
+// (one rounding per touched row and pass of 8192 samples; deterministic).
+// idt: the field-major id copy the chain kernel's gather wrote
+// (idt[f * ldi + r]).  E <= kMaxEmbDim and a multiple of 4, V <= 2^19.
 constexpr int kMaxEmbDim = 16;
 struct ScatterJob {
-  float* T; const int32_t* ids; int n_cat, V, E;
+  float* T; const int32_t* idt; int64_t ldi; int n_cat, V, E;
   const float* G; int64_t ldg; int R; float scale;
-  TickRef tr;                          // R, scale; ids offset by row0 rows
+  TickRef tr;                          // R, scale
 };
 hipError_t launch_scatter_sgd(const ScatterJob& j, hipStream_t st);
 
