@@ -258,7 +258,17 @@ bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
   return true;
 }
 
-int dw_tiles(int N, int K, int tile = 64) { return ((N + tile - 1) / tile) * ((K + tile - 1) / tile); }
+// output tiles of a weight gradient [N x K]: square tiles of 32 or 64, or
+// 256 x 128 (tile == 256, the large-tile kernel)
+int dw_tiles(int N, int K, int tile = 64) {
+  if (tile == 256) return ((N + 255) / 256) * ((K + 127) / 128);
+  return ((N + tile - 1) / tile) * ((K + tile - 1) / tile);
+}
+
+// Parties whose weight gradient per tick reaches this many FLOPs (bf16)
+// take the large-tile kernel (one 96 KB-LDS block per CU, so at most one
+// block per CU is planned).
+constexpr double kDwtMinFlops = 4e9;
 
 // Groups whose RC operand columns hold at most this many bytes (rows times
 // element size) contract all their rows in one block per 32 x 32 tile.
@@ -269,7 +279,9 @@ constexpr int kDwUnsplitBytes = 2048;
 // group of the kernel).
 void dw_split(int R, int tiles, DwMeta& m) {
   const int max_splits = std::max(1, (R + kDwRows - 1) / kDwRows);
-  const int s = std::min(max_splits, std::max(1, (kDwBlocks + tiles - 1) / tiles));
+  // the large-tile kernel runs one block per CU: never more than kDwBlocks
+  const int want = m.tile == 256 ? kDwBlocks / tiles : (kDwBlocks + tiles - 1) / tiles;
+  const int s = std::min(max_splits, std::max(1, want));
   m.rps = ((R + s - 1) / s + kDwRows - 1) / kDwRows * kDwRows;
   m.splits = (R + m.rps - 1) / m.rps;
 }
@@ -395,7 +407,21 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       p.db.blocks = bottom_tiles(b, 32);
       for (DwMeta* m : {&p.da, &p.db}) { m->tile = 32; m->splits = 1; m->rps = p.Ra; }
     } else {
-      const int ta = bottom_tiles(a, 64) + top_tiles(64), tb = bottom_tiles(b, 64);
+      // MACs per row of each party's weight gradients
+      auto bottom_macs = [&](const vfl_bottom_spec* sp) {
+        double in = sp->n_cat * sp->emb_dim + sp->dense_in, n = 0;
+        for (int l = 0; l < sp->n_layers; ++l) { n += in * sp->widths[l]; in = sp->widths[l]; }
+        return n;
+      };
+      double top_macs = 0;
+      {
+        double in = a->widths[a->n_layers - 1] + b->widths[b->n_layers - 1];
+        for (int j = 0; j + 1 < t->n_layers; ++j) { top_macs += in * t->widths[j]; in = t->widths[j]; }
+      }
+      const bool bf = o->dtype == VFL_BF16;
+      p.da.tile = bf && 2.0 * p.R * (bottom_macs(a) + top_macs) >= kDwtMinFlops ? 256 : 64;
+      p.db.tile = bf && 2.0 * p.R * bottom_macs(b) >= kDwtMinFlops ? 256 : 64;
+      const int ta = bottom_tiles(a, p.da.tile) + top_tiles(p.da.tile), tb = bottom_tiles(b, p.db.tile);
       dw_split(p.R, ta, p.da);
       dw_split(p.R, tb, p.db);
       p.da.blocks = ta * p.da.splits;
@@ -1026,7 +1052,8 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, Ti
                       tr.src ? loss : nullptr, st));
     return VFL_OK;
   }
-  TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
+  if (m.tile == 256) TIMED(VFL_K_DW, flops, st, launch_dwt(job, m.blocks, scale, tr, st));
+  else TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
   const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);
   if (blocks > 0) {
     double bytes = 0;

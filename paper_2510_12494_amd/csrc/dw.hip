@@ -217,6 +217,190 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
   }
 }
 
+// Large-tile weight gradient for bf16 operands and long groups: a block of
+// 256 threads owns a kDwtN x kDwtK (256 x 128) output tile and one row
+// chunk.  Rows go through LDS in stages of 64 (8 row groups of 16-byte
+// chunks, the D columns of the tile then its X columns, as laid out in
+// global memory, so every load instruction of a wavefront is contiguous);
+// the next stage's loads are in flight while the current stage is
+// multiplied, and one barrier per stage separates the two LDS buffers.
+// Wavefront (wn, wk) of the 2 x 2 grid computes 128 x 64 of the tile with
+// v_mfma_f32_32x32x16_bf16: X fragments as the A operand (32 inputs x 16
+// rows), D fragments as the B operand (16 rows x 32 outputs), so a lane
+// accumulates four runs of four consecutive inputs k of one output n.
+// The bias gradient is summed from the D fragments of the wavefronts with
+// wk == 0 in the tiles at k0 == 0.  Partials and the unsplit SGD are as in
+// k_dw (same DwProb fields; tiles counted 256 x 128).
+constexpr int kDwtN = 256, kDwtK = 128;
+constexpr int kDwtStageRows = 64;
+constexpr int kDwtGroups = kDwtStageRows / 8;                     // row groups per stage
+constexpr int kDwtChunks = kDwtGroups * (kDwtN + kDwtK);          // 16-byte chunks per stage
+constexpr int kDwtLoads = kDwtChunks / 256;                       // per thread and stage
+constexpr int kDwtPad = 4;   // chunks of padding per LDS row group (the two half-wavefronts of a
+                             // fragment read then start on different banks)
+
+__global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp, float scale_arg, TickRef tr) {
+  typedef __attribute__((ext_vector_type(16))) float f32x16;
+  constexpr int WN = kDwtN / 2, NB = WN / 32, KB = 2;
+  __shared__ u32x4 lds[2][kDwtGroups][kDwtN + kDwtK + kDwtPad];
+  const DwJob& J = *jp;
+  int q = 0;
+#pragma unroll 1
+  while (q + 1 < J.n && (int)blockIdx.x >= J.p[q + 1].first_block) ++q;
+  const DwProb& P = J.p[q];
+  const int lb = blockIdx.x - P.first_block;
+  const int tiles_k = (P.K + kDwtK - 1) / kDwtK;
+  const int tile = lb / P.splits, split = lb % P.splits;
+  const int n0 = (tile / tiles_k) * kDwtN, k0 = (tile % tiles_k) * kDwtK;
+  float scale = scale_arg;
+  if (tr.src) scale = tick_args(tr).scale;
+  const int rb = split * P.rps;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wn = wave >> 1, wk = wave & 1;
+  const int N = P.N, K = P.K;
+  const bool do_bias = k0 == 0 && wk == 0;
+  const VFL_GLOBAL char* Dp = glb((const char*)P.D.p);
+  const VFL_GLOBAL char* Xp = glb((const char*)P.X.p);
+  const int64_t dcp = P.D.cp, xcp = P.X.cp;
+
+  // this thread's chunks of a stage: chunk c = i * 256 + t -> row group
+  // c / (N + K tile), column j; columns clamped into the operands (their
+  // outputs are discarded)
+  int64_t coff[kDwtLoads];
+  bool isd[kDwtLoads];
+  int rgi[kDwtLoads];
+#pragma unroll
+  for (int i = 0; i < kDwtLoads; ++i) {
+    const int c = i * 256 + t;
+    const int rg = c / (kDwtN + kDwtK), j = c % (kDwtN + kDwtK);
+    rgi[i] = rg;
+    isd[i] = j < kDwtN;
+    coff[i] = isd[i] ? (int64_t)min(n0 + j, N - 1) * 16 : (int64_t)min(k0 + j - kDwtN, K - 1) * 16;
+  }
+  u32x4 stg[kDwtLoads];
+  auto gload = [&](int st) {
+    const int64_t rg0 = (int64_t)(rb + st * kDwtStageRows) / 8;
+#pragma unroll
+    for (int i = 0; i < kDwtLoads; ++i) {
+      const int64_t rg = rg0 + rgi[i];
+      const VFL_GLOBAL char* a = isd[i] ? Dp + rg * dcp * 16 + coff[i] : Xp + rg * xcp * 16 + coff[i];
+      stg[i] = *(const VFL_GLOBAL u32x4*)a;
+    }
+  };
+  auto lstore = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < kDwtLoads; ++i) {
+      const int c = i * 256 + t;
+      lds[b][rgi[i]][c - rgi[i] * (kDwtN + kDwtK)] = stg[i];
+    }
+  };
+
+  f32x16 acc[KB][NB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[kb][nb][e] = 0.f;
+  float bsum[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) bsum[nb] = 0.f;
+
+  const int half = lane >> 5, col = lane & 31;
+  const bf16x2 kOnes2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  // one 16-row step: the fragments of step ks + 1 are read before the
+  // products of step ks are issued, so LDS latency hides behind the MFMAs
+  auto frags = [&](int b, int ks, u32x4 (&xa)[KB], u32x4 (&db)[NB]) {
+    const u32x4* row = &lds[b][2 * ks + half][0];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) xa[kb] = row[kDwtN + wk * 64 + kb * 32 + col];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) db[nb] = row[wn * WN + nb * 32 + col];
+  };
+  auto mma = [&](const u32x4 (&xa)[KB], const u32x4 (&db)[NB]) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[kb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, xa[kb]), __builtin_bit_cast(bf16x8, db[nb]), acc[kb][nb], 0, 0, 0);
+    // bias sums in every wavefront (no branch between the steps), kept only
+    // where do_bias: one v_dot2_f32_bf16 against (1, 1) per two rows
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 v = __builtin_bit_cast(bf16x8, db[nb]);
+      bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), kOnes2, bsum[nb], false);
+      bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), kOnes2, bsum[nb], false);
+      bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 4, 5), kOnes2, bsum[nb], false);
+      bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), kOnes2, bsum[nb], false);
+    }
+  };
+  auto compute = [&](int b) {
+    constexpr int NKS = kDwtStageRows / 16;
+    u32x4 xa0[KB], db0[NB], xa1[KB], db1[NB];
+    frags(b, 0, xa0, db0);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks += 2) {
+      frags(b, ks + 1, xa1, db1);
+      mma(xa0, db0);
+      if (ks + 2 < NKS) frags(b, ks + 2, xa0, db0);
+      mma(xa1, db1);
+    }
+  };
+
+  // stages: the chunk is contracted whole (rps rows, a multiple of the
+  // stage; the delta rows past the group are zero).  The last iteration
+  // reloads the last stage (unconditional loads, never used).
+  const int nst = P.rps / kDwtStageRows;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+#pragma unroll 1
+  for (int st = 0; st < nst; ++st) {
+    gload(min(st + 1, nst - 1));
+    compute(st & 1);
+    lstore((st + 1) & 1);
+    __syncthreads();
+  }
+
+  if (do_bias) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) bsum[nb] += __shfl_xor(bsum[nb], 32, 64);
+    if (half == 0) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int n = n0 + wn * WN + nb * 32 + col;
+        if (n >= N) continue;
+        if (P.splits == 1) glb(P.bias)[n] -= scale * bsum[nb];
+        else glb(P.partb)[(int64_t)split * N + n] = bsum[nb];
+      }
+    }
+  }
+  // lane: output n = n0 + wn * WN + nb * 32 + col, inputs
+  // k = k0 + wk * 64 + kb * 32 + 8 j + 4 half + (0 .. 3) in acc[kb][nb][4 j ..]
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int n = n0 + wn * WN + nb * 32 + col;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kk = k0 + wk * 64 + kb * 32 + 8 * j + 4 * half;
+        const f32x4 g = f32x4{acc[kb][nb][4 * j], acc[kb][nb][4 * j + 1], acc[kb][nb][4 * j + 2],
+                              acc[kb][nb][4 * j + 3]};
+        if (P.splits > 1) {
+          if (n < N && kk < K) *(VFL_GLOBAL f32x4*)(glb(P.part) + ((int64_t)split * N + n) * P.kp + kk) = g;
+        } else {
+          float w[4];
+          sgd_load4<uint16_t>(P, n, kk, w);
+          sgd_store4<uint16_t>(P, n, kk, w, g, scale);
+        }
+      }
+    }
+  }
+}
+
 // The logit layer's block partials {loss, dl, dl * h} (one row of Hd + 2
 // floats per chain block): columns 4 lb .. 4 lb + 3, the rows split over 64
 // slices and summed slice by slice; then SGD of the logit weights and bias
@@ -477,6 +661,12 @@ hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, Ti
   if (blocks < 1) return hipErrorInvalidValue;
   if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
   else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
+  return hipGetLastError();
+}
+
+hipError_t launch_dwt(const DwJob* job, int blocks, float scale, TickRef tr, hipStream_t st) {
+  if (blocks < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_dwt, dim3(blocks), dim3(256), 0, st, job, scale, tr);
   return hipGetLastError();
 }
 
