@@ -310,16 +310,18 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
   const int N = L.N;
   const bool relu = L.relu != 0, msk = L.mask.pitch > 0;
   const LBuf out = L.out, mk = L.mask;
+  // branch-free: every condition is a select (a short-circuit test here
+  // compiles to one exec-mask branch per element)
   block_mm<T, RT>(s, L, p, next, [&](int r, int n, const f32x4& a, const f32x4& b) {
     float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
     if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
+    const bool rok = r < rv;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float x = a[i] + b[i];
-      if (relu) x = fmaxf(x, 0.f);
-      if (!(m[i] > 0.f)) x = 0.f;
-      if (n + i >= N || r >= rv) x = 0.f;
-      v[i] = x;
+      const float x0 = a[i] + b[i];
+      const float x = relu ? fmaxf(x0, 0.f) : x0;
+      const bool keep = rok & (n + i < N) & (m[i] > 0.f);
+      v[i] = keep ? x : 0.f;
     }
     st4<T>(lp(s, out, r, n * (int)sizeof(T)), v);
   });
