@@ -55,12 +55,12 @@ def gemm_flops_per_tick(w) -> float:
 
 
 CSRC = "paper_2510_12494_amd/csrc"
-# kernel class -> (kernel symbol, the sources its code and launch layout come from)
+# kernel class -> (kernel symbols, the sources its code and launch layout come from)
 KERNEL_SOURCES = {
-    "fwd": ("k_fwd<", ["chain.hip"]), "active": ("k_active<", ["chain.hip"]),
-    "bwd": ("k_bwd<", ["chain.hip"]), "dw": ("k_dw<", ["dw.hip"]),
-    "reduce": ("k_dw_reduce<", ["dw.hip"]), "cast": ("k_cast<", ["rowops.hip"]),
-    "emb_sgd": ("k_embed_sgd", ["embed.hip"]),
+    "fwd": (("k_fwd<",), ["chain.hip"]), "active": (("k_active<",), ["chain.hip"]),
+    "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dwt(", "k_dw32<"), ["dw.hip"]),
+    "reduce": (("k_dw_reduce<",), ["dw.hip"]), "cast": (("k_cast<",), ["rowops.hip"]),
+    "emb_sgd": (("k_embed_sgd",), ["embed.hip"]),
 }
 
 
@@ -105,7 +105,7 @@ def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int
     runs of this script with --copy-bytes (FETCH_SIZE, then WRITE_SIZE, KiB
     per dispatch), each counter scaled so that the plain copy of known size
     in the same run reads exactly its bytes."""
-    sym = KERNEL_SOURCES[kernel][0]
+    syms = KERNEL_SOURCES[kernel][0]
     res = {"kernel": kernel, "copy_bytes": copy_bytes}
     for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _counter_rows(d, name)
@@ -113,9 +113,9 @@ def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int
         if not copy:
             raise SystemExit(f"{name}: no copy dispatch in {d}")
         cal = copy_bytes / (max(copy) * 1024.0)
-        ks = [v for k, v in rows if sym in k]
+        ks = [v for k, v in rows if any(sym in k for sym in syms)]
         if not ks:
-            raise SystemExit(f"{name}: no {sym} dispatch in {d}")
+            raise SystemExit(f"{name}: no {'/'.join(syms)} dispatch in {d}")
         res[name] = {"dispatches": len(ks), "kib_per_dispatch": sum(ks) / len(ks),
                      "copy_kib": max(copy), "scale": cal,
                      "bytes_per_launch": cal * 1024.0 * sum(ks) / len(ks)}
