@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 PEAK = {"bf16": 2.5e15, "f32": 157.3e12}     # dense MFMA FLOP/s (MI355X spec)
 HBM_PEAK = 8.0e12                            # bytes/s
 METRIC = "training samples/sec (both parties fwd+bwd+update) on 1 MI355X; MFMA util %"
-GEMM_CLASSES = ("fwd", "active", "bwd", "dw")
+GEMM_CLASSES = ("fwd", "active", "bwd", "dw", "gemm")
 
 
 def gemm_flops_per_tick(w) -> float:
@@ -60,7 +60,7 @@ KERNEL_SOURCES = {
     "fwd": (("k_fwd<",), ["chain.hip"]), "active": (("k_active<",), ["chain.hip"]),
     "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dwt(", "k_dw32<"), ["dw.hip"]),
     "reduce": (("k_dw_reduce<",), ["dw.hip"]), "cast": (("k_cast<",), ["rowops.hip"]),
-    "emb_sgd": (("k_embed_sgd",), ["embed.hip"]),
+    "emb_sgd": (("k_embed_sgd",), ["embed.hip"]), "gemm": (("k_gemm",), ["gemm.hip"]),
 }
 
 

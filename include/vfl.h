@@ -264,7 +264,8 @@ typedef enum {
   VFL_K_REDUCE = 4,     /* split-partial and logit reductions + SGD */
   VFL_K_CAST = 5,       /* weight operand copies */
   VFL_K_EMB_SGD = 6,    /* sorted sparse SGD of the tables */
-  VFL_K_COUNT = 7
+  VFL_K_GEMM = 7,       /* layer products of party B's wide layers (input gradient) */
+  VFL_K_COUNT = 8
 } vfl_kernel_class;
 
 /* Measurement hook: while class_mask is non-zero, every launch of a

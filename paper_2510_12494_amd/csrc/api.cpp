@@ -39,6 +39,7 @@ using namespace vfl;
 namespace {
 
 constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
+constexpr int kGemmMinWidth = 512;    // B's first-layer width from which its input gradient is a layer product
 constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
 constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
 constexpr int kDwRows = 256;          // rows of two k_dw load groups (4 MFMA steps each, bf16)
@@ -141,6 +142,11 @@ struct Plan {
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
   size_t tsrc = 0;                    // TickSrc of the replayed graphs
   size_t job_fwd = 0, job_act = 0, job_bwd = 0, job_dwa = 0, job_dwb = 0;
+  // party B's layer-1 input gradient as a layer product (wide first layer):
+  // the chain stops at layer 2 and writes its last delta row-major to d1rm
+  bool bgemm = false;
+  size_t d1rm = 0, job_bgemm = 0;
+  int bgemm_blocks = 0;
   KMeta kf, ka, kb;
   FwdLds lf;
   ActLds la;
@@ -328,12 +334,15 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
   l.KS = p.e == BF16 ? 32 : 16;
   l.BR = BR;
   const int es = elt_size(p.e);
+  // the chain's deltas: every layer's output, or (layer product below)
+  // those of layers 1 .. L-1
+  const int lo = p.bgemm ? 1 : 0;
   int w = 1;
-  for (int i = 0; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
+  for (int i = lo; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
   b.P[0] = l.take(w, es);
   b.P[1] = l.take(w, es);
-  // one mask buffer per ReLU layer below the last: all are loaded up front
-  for (int i = 0; i + 1 < p.P.L; ++i)
+  // one mask buffer per ReLU layer the chain crosses: all are loaded up front
+  for (int i = lo; i + 1 < p.P.L; ++i)
     if (p.P.relu[i]) b.mask[i] = l.take(p.P.out[i], es);
   b.bytes = l.off;
 }
@@ -488,6 +497,11 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   party(p.P, b, p.s + 1, true);
   p.dA = p.A.out[p.A.L - 1];
   p.dB = p.P.out[p.P.L - 1];
+  // B's first layer at least kGemmMinWidth wide (its deltas would crowd the
+  // chain's LDS), no tables, bf16: layer 1's input gradient is a layer
+  // product over the whole group
+  p.bgemm = p.e == BF16 && p.P.L >= 2 && p.P.spec.n_cat == 0 && p.P.out[0] >= kGemmMinWidth;
+  if (p.bgemm) p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
 
   Top& T = p.T;
   T.spec = *t;
@@ -563,6 +577,10 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.job_bwd = ly.take(sizeof(BwdJob) * (p.s + 1));
   p.job_dwa = ly.take(sizeof(DwJob));
   p.job_dwb = ly.take(sizeof(DwJob) * (p.s + 1));
+  if (p.bgemm) {
+    p.job_bgemm = ly.take(sizeof(GemmJob) * (p.s + 1));
+    p.bgemm_blocks = gemm_tiles(p.Ra, p.P.out[0]);
+  }
   p.total = (ly.off + 255) / 256 * 256;
   return "";
 }
@@ -615,6 +633,7 @@ struct Jobs {
   std::vector<BwdJob> bj;
   std::vector<DwJob> dwb;
   DwJob dwa;
+  std::vector<GemmJob> bg;            // party B's layer-1 input gradient per slot (bgemm)
 };
 
 // The job descriptors of every slot for a workspace at `ws` (host only;
@@ -633,6 +652,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
   J.bj.assign(S1, BwdJob());
   J.dwb.assign(S1, DwJob());
   J.dwa = DwJob();
+  J.bg.assign(S1, GemmJob());
   std::vector<FwdJob>& fj = J.fj;
   std::vector<ActiveJob>& aj = J.aj;
   std::vector<BwdJob>& bj = J.bj;
@@ -756,8 +776,8 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     b.hdr_chk = hdrp(1, q); b.err = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4;
     b.warm.p[0] = c->ws + P.Wtq[q][0];
     b.warm.lines[0] = (int32_t)((P.wtq_end[q] - P.Wtq[q][0]) / 128);
-    b.nd = P.L - 1;
-    for (int qq = 0; qq + 1 < P.L; ++qq) {
+    b.nd = P.L - 1 - (p.bgemm ? 1 : 0);
+    for (int qq = 0; qq < b.nd; ++qq) {
       const int l = P.L - 1 - qq;
       ChainLayer& L = b.dx[qq];
       L = layer(c->ws + P.Wtq[q][l], P.kt[l], -1, P.in[l], P.out[l], false, lb.P[qq % 2], lb.P[(qq + 1) % 2]);
@@ -772,6 +792,19 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       b.gx = layer(c->ws + P.Wtq[q][0], P.kt[0], -1, P.spec.n_cat * P.spec.emb_dim, P.out[0], false,
                    lb.P[(P.L - 1) % 2], LBuf());
       b.gxp = at_f(P.gx); b.ldgx = (int32_t)P.ldgx;
+    }
+    if (p.bgemm) {
+      // layer 1's input gradient over the group: the chain's last delta
+      // (row-major) times the stashed W1, masked by the stashed layer-0 output
+      b.drm = ws + p.d1rm; b.lddrm = (int32_t)ld_of(P.out[1]);
+      GemmJob& g = J.bg[q];
+      g.A = ws + p.d1rm; g.lda = ld_of(P.out[1]);
+      g.W = c->ws + P.Wtq[q][1]; g.kst = P.kt[1];
+      g.N = P.out[0]; g.K = P.out[1];
+      if (P.relu[0]) g.mask_rc = rcm(c, P.arc[q][0], P.out[0]);
+      g.out_rc = rcm(c, P.drc[0], P.out[0]);
+      g.tiles_n = (g.N + 127) / 128; g.tiles_m = (p.Ra + 255) / 256;
+      g.rows_pad = p.Ra;
     }
   }
 
@@ -852,6 +885,7 @@ vfl_status write_jobs(vfl_ctx* c) {
   HIPCHK(hipMemcpy(c->ws + p.job_bwd, bj.data(), sizeof(BwdJob) * S1, hipMemcpyHostToDevice));
   HIPCHK(hipMemcpy(c->ws + p.job_dwa, &dwa, sizeof(DwJob), hipMemcpyHostToDevice));
   HIPCHK(hipMemcpy(c->ws + p.job_dwb, dwb.data(), sizeof(DwJob) * S1, hipMemcpyHostToDevice));
+  if (p.bgemm) HIPCHK(hipMemcpy(c->ws + p.job_bgemm, J.bg.data(), sizeof(GemmJob) * S1, hipMemcpyHostToDevice));
   return VFL_OK;
 }
 
@@ -1123,8 +1157,12 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
   const Plan& p = c->p;
   HIPCHK(hipStreamWaitEvent(c->sb, c->ev_grad[slot], 0));
   const ChainCall k = call_of(st, group, nullptr, group);
-  TIMED(VFL_K_BWD, party_dx_flops(p.P, p.R), c->sb,
+  const double gf = p.bgemm ? mm_flops(p.R, p.P.out[0], p.P.out[1]) : 0.0;
+  TIMED(VFL_K_BWD, party_dx_flops(p.P, p.R) - gf, c->sb,
         launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
+  if (p.bgemm)
+    TIMED(VFL_K_GEMM, gf, c->sb,
+          launch_gemm((const GemmJob*)(c->ws + p.job_bgemm) + slot, p.bgemm_blocks, nullptr, 0, st.rows, tr, c->sb));
   vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, tr, c->sb);
   if (r) return r;
   return enqueue_table_sgd(c, p.P, slot, st.rows, c->o.lr / (float)st.rows, c->sb, tr);

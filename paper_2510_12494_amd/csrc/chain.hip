@@ -905,6 +905,12 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
     if (L.rc.p) lds_to_rc<T, BR>(s, L.out, L.N, L.rc, r0);
   }
   if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
+  if (j.drm) {
+    // the last delta of the chain, row-major, for the layer product below it
+    const LBuf last = nd > 0 ? j.dx[nd - 1].out : j.d;
+    const int w = nd > 0 ? j.dx[nd - 1].N : j.D;
+    lds_to_rows<T, BR>(s, last, w, j.drm, j.lddrm, r0, rv);
+  }
 }
 
 template <typename K>
@@ -960,7 +966,7 @@ hipError_t chain_init() {
       raise_lds(k_bwd<float, 1>), raise_lds(k_bwd<float, 2>), raise_lds(k_bwd<float, 4>)};
   for (hipError_t x : r)
     if (x != hipSuccess) return x;
-  return hipSuccess;
+  return gemm_init();
 }
 
 }  // namespace vfl

@@ -236,8 +236,10 @@ struct ActiveJob {
 
 // Party B's backward of a group: cut-layer backward of the message g
 // (row-major) at the stashed output z (clip backward with norm/cfac when
-// clip), then the chain dx (l = L-1 .. 1), masks loaded from the stashed
-// RC activations; with tables, gx as in ActiveJob.
+// clip), then the chain dx (l = L-1 .. 1, or down to 2 when layer 1's input
+// gradient is a layer product: then the last delta also goes row-major to
+// drm), masks loaded from the stashed RC activations; with tables, gx as in
+// ActiveJob.
 struct BwdJob {
   BiasTab bt;
   WarmSet warm;
@@ -253,6 +255,7 @@ struct BwdJob {
   int32_t has_gx = 0;
   ChainLayer gx;
   float* gxp = nullptr; int32_t ldgx = 0;
+  void* drm = nullptr; int32_t lddrm = 0;
 };
 
 // Jobs live in device memory (written once when the context is created);
@@ -310,6 +313,30 @@ hipError_t launch_dw32(Elt e, const DwJob* job, int blocks, int R, float scale, 
 // reference, loss_base + the tick's loss index instead.
 hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float scale,
                             float* loss_out, TickRef tr, float* loss_base, hipStream_t st);
+
+// ---------------------------------------------------------- layer products
+// One wide bottom layer over the rows of a group (bf16):
+// out[r][n] = sum_k A[r][k] W[n][k] (+ bias[n], ReLU when relu) or
+// (* (mask[r][n] > 0), mask_rc set), for r < rows; out_rc receives the RC
+// copy (rows from the group's end up to rows_pad zero), out_rm (nullable,
+// N a multiple of 8) the row-major copy, ldo elements per row.  A: row-major,
+// lda elements per row, zero from K up to the next multiple of 8; W packed
+// (pk_index, kst 32-k steps).  in_rc (nullable): RC copy of A's K columns.
+// Blocks: gemm_tiles(rows_pad, N): tiles_m x tiles_n tiles of 256 x 128
+// outputs, rounded up to a multiple of 8 (one contiguous range per XCD).
+struct GemmJob {
+  const void* A = nullptr; int64_t lda = 0;     // workspace operand (a launch may pass its own)
+  const void* W = nullptr; int32_t kst = 0;
+  int32_t N = 0, K = 0, relu = 0;
+  const float* bias = nullptr;
+  RCMat out_rc, mask_rc, in_rc;
+  void* out_rm = nullptr; int64_t ldo = 0;
+  int32_t tiles_n = 0, tiles_m = 0, rows_pad = 0;
+};
+int gemm_tiles(int rows, int N);
+hipError_t gemm_init();
+hipError_t launch_gemm(const GemmJob* job, int blocks, const void* A, int64_t lda, int rows, TickRef tr,
+                       hipStream_t st);
 
 // ---------------------------------------------------------------- others
 // Operand copies of one layer's float32 weight W [out x in], element type

@@ -218,3 +218,24 @@ def test_table_sgd_segments(zipf_a, vocab):
     _check_ints(run, o, recs)
     _check_losses(run, recs, 1e-4)
     _check_params(run, recs, w, per_tick=True)
+
+
+@pytest.mark.parametrize("widths,s,k,clip", [([520, 40], 1, 2, True), ([600, 264, 24], 2, 1, False)])
+def test_wide_first_layer_product(widths, s, k, clip):
+    """Party B's first layer at least 512 wide (bf16): layer 1's input
+    gradient runs as a layer product over the whole group after the chain;
+    odd widths (partial 128-output and 256-row tiles), a ragged last group,
+    and with two layers the cut-layer delta itself feeds the product."""
+    w = Workload(name="wide", n_rows=1401, dtype="bf16",
+                 A=PartySpec(dense=24, widths=[32, 16]), B=PartySpec(dense=33, widths=widths),
+                 top=TopSpec(widths=[20, 1]), batch=300, staleness=s, replicas=k, lr=0.5,
+                 clip=1.0 if clip else 0.0, sigma=0.5 if clip else 0.0, clip_emb=clip,
+                 clip_grad=clip, noise_emb=clip, noise_grad=clip, labels="teacher",
+                 data_seed=71, init_seed=72, noise_seed=73)
+    n_groups = (w.n_rows + w.rows_per_tick - 1) // w.rows_per_tick
+    run = H.Run(w, w.n_rows, n_groups)
+    o, recs = run.oracle("bf16")
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
