@@ -348,30 +348,33 @@ __device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float
 }
 
 // ------------------------------------------------------------ data movement
-// LDS rows -> RC global matrix (block rows at tick rows r0 ..)
+// LDS rows -> RC global matrix (block rows at tick rows r0 ..): one lane per
+// output chunk (RR rows of one column), built from RR element reads of the
+// LDS rows, so every lane of the block works and consecutive lanes store
+// consecutive chunks of a row group.  Columns up to the next multiple of RR
+// (zero in LDS) are written too.
 template <typename T, int BR>
 __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE;
-  const int ncc = (cols + RR - 1) / RR;
-  const int units = (BR / RR) * ncc;
+  const int cw = (cols + RR - 1) / RR * RR;
   VFL_GLOBAL char* g = glb((char*)m.p);
   const int64_t cp = m.cp;
-  // wavefront w takes the units [w * per, (w + 1) * per): the transposes
-  // are spread over every SIMD, and a wavefront's stores stay contiguous
-  const int per = (units + kNW - 1) / kNW;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int i = lane; i < per; i += 64) {
-    const int u = wave * per + i;
-    if (u >= units) break;
-    const int rg = u / ncc, cc = u % ncc;
-    u32x4 in[RR], out[RR];
+  for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
+    const int rg = u / cw, c = u - rg * cw;
+    const char* src = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
+    u32x4 v;
+    if constexpr (RR == 8) {
 #pragma unroll
-    for (int i = 0; i < RR; ++i) in[i] = *(const u32x4*)(s + b.off + (rg * RR + i) * b.pitch + cc * 16);
-    if constexpr (RR == 8) transpose8x8_u16(in, out);
-    else transpose4x4_u32(in, out);
-    const int64_t base = ((int64_t)(r0 / RR + rg) * cp + (int64_t)cc * RR) * 16;
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t lo = *(const uint16_t*)(src + (2 * w) * b.pitch);
+        const uint32_t hi = *(const uint16_t*)(src + (2 * w + 1) * b.pitch);
+        v[w] = lo | (hi << 16);
+      }
+    } else {
 #pragma unroll
-    for (int j = 0; j < RR; ++j) *(VFL_GLOBAL u32x4*)(g + base + j * 16) = out[j];
+      for (int w = 0; w < 4; ++w) v[w] = *(const uint32_t*)(src + w * b.pitch);
+    }
+    *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16) = v;
   }
 }
 
@@ -389,33 +392,29 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
 }
 
 // RC global matrix -> LDS rows (columns below cols; zeros up to the MFMA
-// depth)
+// depth): one lane per chunk (RR rows of one column), one 16-byte load and
+// RR element writes
 template <typename T, int BR>
 __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE, KS = Ch<T>::KS;
-  const int ncc = (cols + KS - 1) / KS * 4;   // chunks up to the MFMA depth
-  const int units = (BR / RR) * ncc;
+  const int cw = (cols + KS - 1) / KS * KS;   // columns up to the MFMA depth
   const VFL_GLOBAL char* g = glb((const char*)m.p);
   const int64_t cp = m.cp;
-  const int per = (units + kNW - 1) / kNW;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int i = lane; i < per; i += 64) {
-    const int u = wave * per + i;
-    if (u >= units) break;
-    const int rg = u / ncc, cc = u % ncc;
-    u32x4 in[RR], out[RR];
-    if (cc * RR < cols) {
-      const int64_t base = ((int64_t)(r0 / RR + rg) * cp + (int64_t)cc * RR) * 16;
+  for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
+    const int rg = u / cw, c = u - rg * cw;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (c < cols) v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+    char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
+    if constexpr (RR == 8) {
 #pragma unroll
-      for (int j = 0; j < RR; ++j) out[j] = *(const VFL_GLOBAL u32x4*)(g + base + j * 16);
-      if constexpr (RR == 8) transpose8x8_u16(out, in);
-      else transpose4x4_u32(out, in);
+      for (int w = 0; w < 4; ++w) {
+        *(uint16_t*)(dst + (2 * w) * b.pitch) = (uint16_t)(v[w] & 0xffffu);
+        *(uint16_t*)(dst + (2 * w + 1) * b.pitch) = (uint16_t)(v[w] >> 16);
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < RR; ++i) in[i] = u32x4{0u, 0u, 0u, 0u};
+      for (int w = 0; w < 4; ++w) *(uint32_t*)(dst + w * b.pitch) = v[w];
     }
-#pragma unroll
-    for (int i = 0; i < RR; ++i) *(u32x4*)(s + b.off + (rg * RR + i) * b.pitch + cc * 16) = in[i];
   }
 }
 
