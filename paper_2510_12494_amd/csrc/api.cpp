@@ -112,6 +112,16 @@ struct Lds {
     off += (bytes + 15) / 16 * 16;
     return b;
   }
+  // two buffers that are never live at the same time: one region as large
+  // as the larger, each with its own pitch
+  void take_shared(LBuf& a, int wa, int ea, LBuf& b, int wb, int eb) {
+    const int o = off;
+    a = take(wa, ea);
+    const int ea_end = off;
+    off = o;
+    b = take(wb, eb);
+    off = std::max(off, ea_end);
+  }
 };
 
 struct FwdLds { LBuf buf[2], bias; int bytes = 0; };
@@ -297,11 +307,13 @@ void plan_fwd_lds(const Plan& p, int BR, FwdLds& f) {
   Lds l;
   l.KS = p.e == BF16 ? 32 : 16;
   l.BR = BR;
-  int w = p.P.din;
-  for (int i = 0; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
+  // layer l reads buf[l % 2] and writes buf[(l + 1) % 2]; the input is in
+  // buf[0]: each buffer is as wide as the widest tensor it holds
+  int w[2] = {p.P.din, 1};
+  for (int i = 0; i < p.P.L; ++i) w[(i + 1) % 2] = std::max(w[(i + 1) % 2], p.P.out[i]);
   const int es = elt_size(p.e);
-  f.buf[0] = l.take(w, es);
-  f.buf[1] = l.take(w, es);
+  f.buf[0] = l.take(w[0], es);
+  f.buf[1] = l.take(w[1], es);
   f.bias = l.raw(4 * p.nbias_b);
   f.bytes = l.off;
 }
@@ -311,16 +323,21 @@ void plan_act_lds(const Plan& p, int BR, bool gextra, ActLds& a) {
   l.KS = p.e == BF16 ? 32 : 16;
   l.BR = BR;
   const int es = elt_size(p.e);
-  a.in = l.take(p.A.din, es);
   for (int i = 0; i + 1 < p.A.L; ++i) a.fa[i] = l.take(p.A.out[i], es);
   a.cat = l.take(p.dA + p.dB, es);
-  for (int j = 0; j < p.T.H; ++j) a.ft[j] = l.take(p.T.out[j], es);
+  for (int j = 0; j + 1 < p.T.H; ++j) a.ft[j] = l.take(p.T.out[j], es);
   int w = 1;
   for (int j = 0; j < p.T.H; ++j) w = std::max(w, p.T.out[j]);
   for (int i = 0; i < p.A.L; ++i) w = std::max(w, p.A.out[i]);
   a.P[0] = l.take(w, es);
-  a.P[1] = l.take(w, es);
-  if (gextra) a.msg = l.take(p.dB, 4);
+  // buffers never live at the same time share LDS: the input (read by A's
+  // first layer only) with P[1] (first written after the logit stage), and
+  // the last top hidden output (dead once the logit stage has formed dh)
+  // with the float32 gradient-message staging (written by the concat
+  // product)
+  l.take_shared(a.in, p.A.din, es, a.P[1], w, es);
+  if (gextra) l.take_shared(a.ft[p.T.H - 1], p.T.out[p.T.H - 1], es, a.msg, p.dB, 4);
+  else a.ft[p.T.H - 1] = l.take(p.T.out[p.T.H - 1], es);
   // logit weights [Hd], the block's labels, dl and loss [BR each]
   // the block's labels, per-wavefront partials of the logit layer's
   // weight gradient [kChainWaves][Hd rounded to 4] and of {loss, dl}
@@ -337,10 +354,12 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
   // the chain's deltas: every layer's output, or (layer product below)
   // those of layers 1 .. L-1
   const int lo = p.bgemm ? 1 : 0;
-  int w = 1;
-  for (int i = lo; i < p.P.L; ++i) w = std::max(w, p.P.out[i]);
-  b.P[0] = l.take(w, es);
-  b.P[1] = l.take(w, es);
+  // the cut delta (layer L-1's output) is in P[0], the delta of layer i's
+  // output in P[(L-1-i) % 2]; the table input gradient reads layer 0's
+  int w[2] = {1, 1};
+  for (int i = lo; i < p.P.L; ++i) w[(p.P.L - 1 - i) % 2] = std::max(w[(p.P.L - 1 - i) % 2], p.P.out[i]);
+  b.P[0] = l.take(w[0], es);
+  b.P[1] = l.take(w[1], es);
   // one mask buffer per ReLU layer the chain crosses: all are loaded up front
   for (int i = lo; i + 1 < p.P.L; ++i)
     if (p.P.relu[i]) b.mask[i] = l.take(p.P.out[i], es);
@@ -351,7 +370,7 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
 // that still gives kMinBlocks blocks (16 when nothing gives that many).
 template <typename F>
 bool pick_rt(int R, KMeta& m, F&& bytes_at) {
-  for (int rt : {4, 2, 1}) {
+  for (int rt : {4, 3, 2, 1}) {
     const int BR = 16 * rt;
     const int blocks = (R + BR - 1) / BR;
     const int lds = bytes_at(BR);
@@ -664,6 +683,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     RCMat m;
     m.p = ws + off;
     m.cp = (int32_t)ld_of(cols);
+    m.rows = p.Ra;
     return m;
   };
   for (int q = 0; q < S1; ++q) {

@@ -2,7 +2,7 @@
 // k_active, k_bwd; see kernels.h for what each computes).
 //
 // A workgroup of 512 threads (8 wavefronts, two per SIMD) owns BR = 16 * RT
-// consecutive rows of the group and runs every layer of its chain on them,
+// (RT = 1 .. 4) consecutive rows of the group and runs every layer of its chain on them,
 // the activations and deltas staying in LDS.  Each layer is one MFMA product
 // out[BR x N] = in[BR x K] W^T: wavefront w takes the 16-column output tiles
 // w, w+8, w+16, ... (two at a time), loads the weight fragments of its tiles
@@ -359,7 +359,8 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
   const int cw = (cols + RR - 1) / RR * RR;
   VFL_GLOBAL char* g = glb((char*)m.p);
   const int64_t cp = m.cp;
-  for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
+  const int nrg = m.rows > 0 ? min(BR / RR, (m.rows - r0) / RR) : BR / RR;   // row groups inside m
+  for (int u = threadIdx.x; u < nrg * cw; u += kNT) {
     const int rg = u / cw, c = u - rg * cw;
     const char* src = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
     u32x4 v;
@@ -385,7 +386,8 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
   if (!m.p) return;
   const int ncc = (cols + RR - 1) / RR;
   VFL_GLOBAL char* g = glb((char*)m.p);
-  for (int u = threadIdx.x; u < (BR / RR) * ncc * RR; u += kNT) {
+  const int nrg = m.rows > 0 ? min(BR / RR, (m.rows - r0) / RR) : BR / RR;   // row groups inside m
+  for (int u = threadIdx.x; u < nrg * ncc * RR; u += kNT) {
     const int rg = u / (ncc * RR), c = u % (ncc * RR);
     *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * m.cp + c) * 16) = u32x4{0u, 0u, 0u, 0u};
   }
@@ -403,7 +405,8 @@ __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, cons
   for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
     const int rg = u / cw, c = u - rg * cw;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (c < cols) v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+    const bool in_m = m.rows == 0 || r0 + rg * RR < m.rows;
+    if (c < cols && in_m) v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
     char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
     if constexpr (RR == 8) {
 #pragma unroll
@@ -924,11 +927,13 @@ hipError_t raise_lds(K kernel) {
     if (e == BF16) {                                                                         \
       if (rt == 1) hipLaunchKernelGGL((KER<uint16_t, 1>), __VA_ARGS__);                       \
       else if (rt == 2) hipLaunchKernelGGL((KER<uint16_t, 2>), __VA_ARGS__);                  \
+      else if (rt == 3) hipLaunchKernelGGL((KER<uint16_t, 3>), __VA_ARGS__);                  \
       else if (rt == 4) hipLaunchKernelGGL((KER<uint16_t, 4>), __VA_ARGS__);                  \
       else return hipErrorInvalidValue;                                                      \
     } else {                                                                                 \
       if (rt == 1) hipLaunchKernelGGL((KER<float, 1>), __VA_ARGS__);                          \
       else if (rt == 2) hipLaunchKernelGGL((KER<float, 2>), __VA_ARGS__);                     \
+      else if (rt == 3) hipLaunchKernelGGL((KER<float, 3>), __VA_ARGS__);                     \
       else if (rt == 4) hipLaunchKernelGGL((KER<float, 4>), __VA_ARGS__);                     \
       else return hipErrorInvalidValue;                                                      \
     }                                                                                        \
@@ -959,10 +964,13 @@ hipError_t chain_init() {
   const hipError_t r[] = {
       raise_lds(k_fwd<uint16_t, 1>), raise_lds(k_fwd<uint16_t, 2>), raise_lds(k_fwd<uint16_t, 4>),
       raise_lds(k_fwd<float, 1>), raise_lds(k_fwd<float, 2>), raise_lds(k_fwd<float, 4>),
+      raise_lds(k_fwd<uint16_t, 3>), raise_lds(k_fwd<float, 3>),
       raise_lds(k_active<uint16_t, 1>), raise_lds(k_active<uint16_t, 2>), raise_lds(k_active<uint16_t, 4>),
       raise_lds(k_active<float, 1>), raise_lds(k_active<float, 2>), raise_lds(k_active<float, 4>),
+      raise_lds(k_active<uint16_t, 3>), raise_lds(k_active<float, 3>),
       raise_lds(k_bwd<uint16_t, 1>), raise_lds(k_bwd<uint16_t, 2>), raise_lds(k_bwd<uint16_t, 4>),
-      raise_lds(k_bwd<float, 1>), raise_lds(k_bwd<float, 2>), raise_lds(k_bwd<float, 4>)};
+      raise_lds(k_bwd<float, 1>), raise_lds(k_bwd<float, 2>), raise_lds(k_bwd<float, 4>),
+      raise_lds(k_bwd<uint16_t, 3>), raise_lds(k_bwd<float, 3>)};
   for (hipError_t x : r)
     if (x != hipSuccess) return x;
   return gemm_init();

@@ -101,8 +101,9 @@ hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st);
 // pitch in bytes (a pitch of 0 marks an absent buffer).
 struct LBuf { int32_t off = 0, pitch = 0; };
 
-// RC-layout global matrix (null p: not written).
-struct RCMat { void* p = nullptr; int32_t cp = 0, pad = 0; };
+// RC-layout global matrix (null p: not written); rows: the rows it holds
+// (a chain block's rows past it are not written; 0: unbounded).
+struct RCMat { void* p = nullptr; int32_t cp = 0, rows = 0; };
 
 // One product of a row block with a weight operand W [N x K] (element type,
 // packed: see pk_index; kst = K steps of the packing, tiles up to N rounded
