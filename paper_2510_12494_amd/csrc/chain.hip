@@ -141,19 +141,17 @@ __device__ __forceinline__ int tiles_of(int N) {
 // the loads of group g of a pass (tiles tile[]) of an operand W with kst
 // K steps and ntl tiles into d: one contiguous 1 KB fragment per tile and
 // step of the packed operand.  Loads are unconditional: tiles past the
-// operand's last are clamped to it (never used), steps past K read on into
-// the next tile or the operand's slack (never used either; a conditional
-// load would make the compiler wait for it on the spot).  The address is a
-// uniform base per tile plus the lane's 16 bytes plus an immediate.
+// operand's last are clamped to it, steps past K to its last step (never
+// used; re-reading lines already fetched keeps them off the L2, and a
+// conditional load would make the compiler wait for it on the spot).
 __device__ __forceinline__ void wgroup(const void* Wp, int kst, int ntl, const int (&tile)[kNTW], int g,
                                        u32x4 (&d)[kPF][kNTW]) {
   const uint32_t lo = (threadIdx.x & 63) * 16;
 #pragma unroll
   for (int j = 0; j < kNTW; ++j) {
-    const VFL_GLOBAL char* base =
-        glb((const char*)Wp) + ((int64_t)min(tile[j], ntl - 1) * kst + g * kPF) * 1024;
+    const VFL_GLOBAL char* base = glb((const char*)Wp) + (int64_t)min(tile[j], ntl - 1) * kst * 1024 + lo;
 #pragma unroll
-    for (int q = 0; q < kPF; ++q) d[q][j] = *(const VFL_GLOBAL u32x4*)(base + lo + q * 1024);
+    for (int q = 0; q < kPF; ++q) d[q][j] = *(const VFL_GLOBAL u32x4*)(base + (int64_t)min(g * kPF + q, kst - 1) * 1024);
   }
 }
 
