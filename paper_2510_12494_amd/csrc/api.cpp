@@ -733,6 +733,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       a.fa[l] = layer(c->ws + A.Wq[0][l], A.kq[l], la.bias.off + 4 * A.bo[l], A.out[l], A.in[l], A.relu[l],
                       src, dst);
       if (l + 1 < A.L) a.fa[l].rc = rcm(c, A.arc[0][l], A.out[l]);
+      else a.fa[l].nopad = 1;   // B's embedding is already in cat past dA
     }
     a.cat = la.cat; a.cat_rc = rcm(c, p.cat_rc, p.dA + p.dB); a.dA = p.dA; a.dB = p.dB;
     a.zb = c->ws + P.zhat[q]; a.ldzb = (int32_t)ld_of(p.dB);

@@ -306,7 +306,7 @@ template <typename T, int RT>
 __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe& p,
                                           const ChainLayer* next) {
   const int N = L.N;
-  const bool relu = L.relu != 0, msk = L.mask.pitch > 0;
+  const bool relu = L.relu != 0, msk = L.mask.pitch > 0, nopad = L.nopad != 0;
   const LBuf out = L.out, mk = L.mask;
   // branch-free: every condition is a select (a short-circuit test here
   // compiles to one exec-mask branch per element)
@@ -321,7 +321,9 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
       const bool keep = rok & (n + i < N) & (m[i] > 0.f);
       v[i] = keep ? x : 0.f;
     }
-    st4<T>(lp(s, out, r, n * (int)sizeof(T)), v);
+    // n is a multiple of 4 and a nopad N of 8: the four columns are all
+    // below N or all past it
+    if (!nopad || n < N) st4<T>(lp(s, out, r, n * (int)sizeof(T)), v);
   });
 }
 
@@ -651,18 +653,11 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   const uint32_t wx = warm_l2(j.warm, jp);
   copy_bias(s, j.bt);
 
-  // A's bottom forward; the last layer fills cat[:, 0:dA)
+  // A's bottom input, and B's embedding into cat[:, dA:dA+dB) with zeros up
+  // to the MFMA depth (published before this launch; A's last layer fills
+  // cat[:, 0:dA) and leaves these columns alone)
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
   if ((int)threadIdx.x < BR) yl[threadIdx.x] = (int)threadIdx.x < rv ? py : 0.f;
-  __syncthreads();
-  asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
-  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
-  for (int l = 0; l < LA; ++l) {
-    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < LA ? &j.fa[l + 1] : &j.ft[0]);
-    __syncthreads();
-    if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
-  }
-  // B's embedding into cat[:, dA:dA+dB), zeros up to the MFMA depth
   {
     const int dA = j.dA, dB = j.dB;
     const int nch = ((dA + dB + KS - 1) / KS * KS - dA) / CE;
@@ -675,6 +670,13 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     }
   }
   __syncthreads();
+  asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
+  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
+  for (int l = 0; l < LA; ++l) {
+    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < LA ? &j.fa[l + 1] : &j.ft[0]);
+    __syncthreads();
+    if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
+  }
   if (j.cat_rc.p) lds_to_rc<T, BR>(s, j.cat, j.dA + j.dB, j.cat_rc, r0);
   // top hidden layers
   for (int q = 0; q < H; ++q) {

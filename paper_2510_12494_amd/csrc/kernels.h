@@ -115,11 +115,12 @@ struct RCMat { void* p = nullptr; int32_t cp = 0, rows = 0; };
 // written as zeros, as are rows beyond the group.  rc: RC copy of out.
 // mask_src (k_bwd): the mask is first loaded into `mask` from this matrix.
 // bl: byte offset of the layer's bias row in the kernel's LDS bias table
-// (-1: no bias).
+// (-1: no bias).  nopad: columns from N on are left as they are (another
+// tensor shares the LDS rows there).
 struct ChainLayer {
   const void* W = nullptr;
   int32_t kst = 0, N = 0, K = 0, relu = 0;
-  int32_t bl = -1;
+  int32_t bl = -1, nopad = 0;
   LBuf in, out, mask;
   RCMat rc, mask_src;
 };
