@@ -17,7 +17,7 @@
 //      registers, so the order is deterministic: by id, then by sample),
 //   3. stages the gradient rows of the sorted keys and the table rows of
 //      their ids in LDS, 512 positions at a time (every global load of a
-//      stage issued before the first is waited for), and forms segmented
+//      stage issued together, while the previous stage is scanned), and forms segmented
 //      sums per id with a fixed-shape scan: 64 scanners per 4-column chunk
 //      each reduce 8 consecutive positions, an exclusive segmented scan
 //      combines the scanners (lanes in order, then wavefronts in order),
@@ -178,29 +178,32 @@ __global__ __launch_bounds__(kThreads) void k_embed_sgd(ScatterJob j) {
     if (np <= 2 * kThreads) bitonic<2>(keys, np);
     else if (np <= 8 * kThreads) bitonic<8>(keys, np);
     else bitonic<32>(keys, np);
-    // 3. segmented sums, kStage sorted positions at a time
+    // 3. segmented sums, kStage sorted positions at a time; the gradient and
+    // table rows of the next stage are loaded while this one is scanned
     f32x4 carry = f32x4{0.f, 0.f, 0.f, 0.f};    // the open segment entering the stage
+    f32x4 gv[kStageLoads], tv[kStageLoads];
+    // loads clamped into range, so all are unconditional and in flight
+    // together; chunks past E repeat the last one (never stored back)
+    auto issue = [&](int s0) {
+#pragma unroll
+      for (int u = 0; u < kStageLoads; ++u) {
+        const int i = min(s0 * 4 + u * kThreads + tid, np * 4 - 1);
+        const int c = min(i & 3, EC - 1);
+        const uint32_t key = keys[i >> 2];
+        gv[u] = G[(int64_t)(c0 + (key & kRowMask)) * ldg4 + f * EC + c];
+        tv[u] = Tf[(int64_t)((key >> kRowBits) * (uint32_t)kParts + (uint32_t)part) * EC + c];
+      }
+    };
+    if (np > 0) issue(0);
     for (int s0 = 0; s0 < np; s0 += kStage) {
       const int ns = min(kStage, np - s0);
-      {
-        // loads clamped into range, so all are unconditional and in flight
-        // together; chunks past E repeat the last one (never stored back)
-        f32x4 gv[kStageLoads], tv[kStageLoads];
 #pragma unroll
-        for (int u = 0; u < kStageLoads; ++u) {
-          const int i = min(u * kThreads + tid, ns * 4 - 1);
-          const int c = min(i & 3, EC - 1);
-          const uint32_t key = keys[s0 + (i >> 2)];
-          gv[u] = G[(int64_t)(c0 + (key & kRowMask)) * ldg4 + f * EC + c];
-          tv[u] = Tf[(int64_t)((key >> kRowBits) * (uint32_t)kParts + (uint32_t)part) * EC + c];
-        }
-#pragma unroll
-        for (int u = 0; u < kStageLoads; ++u) {
-          const int i = u * kThreads + tid;
-          if (i < ns * 4) { gs[i >> 2][i & 3] = gv[u]; ts[i >> 2][i & 3] = tv[u]; }
-        }
+      for (int u = 0; u < kStageLoads; ++u) {
+        const int i = u * kThreads + tid;
+        if (i < ns * 4) { gs[i >> 2][i & 3] = gv[u]; ts[i >> 2][i & 3] = tv[u]; }
       }
       __syncthreads();
+      issue(s0 + kStage);   // past the last stage: clamped repeats, never stored
       auto head = [&](int a) { return a == 0 || (keys[a] >> kRowBits) != (keys[a - 1] >> kRowBits); };
       const int p0 = q * kSpan, p1 = min(p0 + kSpan, ns);
       // (a) the scanner's aggregate
