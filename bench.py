@@ -136,9 +136,12 @@ def cpu_baseline(w, data, params, seconds: float) -> dict:
         threads = len(os.sched_getaffinity(0))
     R = w.rows_per_tick
     rows_of = lambda g: S.group_rows(w, g)
-    t0 = time.perf_counter()
+    # size the sample from a 4-group run after a 1-group warm-up (one group
+    # alone is dominated by set-up and the s-tick lead-in)
     PubSubOracle(w, params, "f64").run(data, 1, rows_of, keep_messages=False)
-    per_group = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    PubSubOracle(w, params, "f64").run(data, 4, rows_of, keep_messages=False)
+    per_group = (time.perf_counter() - t0) / 4
     groups = int(max(1, min(4096, seconds / max(per_group, 1e-6))))
     o = PubSubOracle(w, params, "f64")
     t0 = time.perf_counter()
