@@ -1,30 +1,27 @@
-// Layer products of the wide bottom layers on gfx950 (k_gemm; see
+// Input-gradient products of wide bottom layers on gfx950 (k_gemm; see
 // kernels.h for the job).
 //
-// out[r][n] = sum_k A[r][k] W[n][k] for the rows of a group, bf16 operands
-// and float32 accumulation, then
-//   forward:         + bias[n], ReLU when relu;
-//   input gradient:  * (mask[r][n] > 0) from an RC matrix (the ReLU
-//                    derivative of the layer's stashed output).
-// A is row-major (a dataset slice or a previous product's row-major output),
-// W the packed operand copy the chain kernels read (pk_index: 16 x 32
-// fragments).  A block of 256 threads owns a 256-row x 128-column output
-// tile; K goes through LDS in stages of 64 (the A rows and the W fragments of
-// the stage, 48 KB, double-buffered), one barrier per stage.  Wavefront
-// (wm, wn) of the 2 x 2 grid computes 128 x 64 of the tile with
-// v_mfma_f32_32x32x16_bf16: A fragments (32 rows x 16 k) as the A operand,
-// W fragments (16 k x 32 outputs) as the B operand, so a lane ends up with
-// one output column n and four runs of four consecutive rows.
+// out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k] for the rows of a
+// group, bf16 operands and float32 accumulation: the delta of a layer's
+// output (A, row-major) times the layer's stashed weight copy (W, the packed
+// transpose the chain kernels read: pk_index, 16 x 32 fragments), masked by
+// the ReLU derivative of the layer below (its stashed output, RC layout),
+// written in the RC layout the weight gradient reads.  A block of 256
+// threads owns a 256-row x 128-column output tile; K goes through LDS in
+// stages of 64 (the A rows and the W fragments of the stage, 48 KB,
+// double-buffered), one barrier per stage.  Wavefront (wm, wn) of the 2 x 2
+// grid computes 128 x 64 of the tile with v_mfma_f32_32x32x16_bf16: A
+// fragments (32 rows x 16 k) as the A operand, W fragments (16 k x 32
+// outputs) as the B operand, so a lane ends up with one output column n and
+// four runs of four consecutive rows.  The tiles are dealt to the XCDs in
+// contiguous ranges, so the column tiles that share an A row slab meet in
+// one L2.
 //
 // Epilogue: the runs of lanes l and l + 32 are exchanged so that each lane
-// holds two whole 8-row chunks of its column, which go to the RC output
-// (and meet the RC mask chunk at the same place); the row-major output goes
-// through LDS (each wavefront transposes its 128 x 64 sub-tile) so that the
-// global stores are contiguous rows.  Rows past the group are written as
-// zeros in the RC outputs (the weight gradient reads whole row chunks).
-// With in_rc set, the stage's A rows are also written to that RC matrix
-// (the weight-gradient operand of the first layer), each n-tile block taking
-// the stages s with s mod tiles_n == its n-tile.
+// holds two whole 8-row chunks of its column, which meet the RC mask chunk
+// at the same place (all mask chunks are loaded together first) and go to
+// the RC output.  Rows past the group are written as zeros (the weight
+// gradient reads whole row chunks).
 #include "device.h"
 #include "kernels.h"
 
@@ -38,7 +35,6 @@ constexpr int kSC = kSK / 8;                   // 16-byte chunks per row and sta
 constexpr int kPitch = kSC + 1;                // LDS chunks per row (+1: banks)
 constexpr int kStageChunks = (kTM + kTN) * kPitch;   // one stage buffer, in chunks
 constexpr int kWN = kTN / 2, kNB = kWN / 32;   // wavefront outputs, 32-wide blocks of them
-constexpr int kOutPitch = kWN + 8;             // row-major transpose rows (bf16)
 constexpr int kGemmLds = 2 * kStageChunks * 16;
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -82,14 +78,6 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
       const int64_t g = m0 / 8 + rg;
       if (n >= N || g >= rg_end) continue;
       *(VFL_GLOBAL u32x4*)(glb((char*)J.out_rc.p) + (g * J.out_rc.cp + n) * 16) = u32x4{0u, 0u, 0u, 0u};
-    }
-    if (J.in_rc.p && tile_n == 0) {
-      for (int c = t; c < kTM / 8 * K; c += 256) {
-        const int rg = c / K, k = c % K;
-        const int64_t g = m0 / 8 + rg;
-        if (g >= rg_end) continue;
-        *(VFL_GLOBAL u32x4*)(glb((char*)J.in_rc.p) + (g * J.in_rc.cp + k) * 16) = u32x4{0u, 0u, 0u, 0u};
-      }
     }
     return;
   }
@@ -162,34 +150,6 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8, af[mb]), __builtin_bit_cast(bf16x8, bf[nb]), acc[mb][nb], 0, 0, 0);
   };
-  // the stage's A rows to the RC copy (8 x 8 transposes; rows past the group zero)
-  auto in_rc = [&](int b, int s) {
-    const u32x4* S = L + b * kStageChunks;
-    const int rg = t >> 3, kc = t & 7;         // 32 row groups x 8 k chunks
-    const int kbase = s * kSK + 8 * kc;
-    if (kbase >= K) return;
-    u32x4 in[8], out[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) in[i] = S[(rg * 8 + i) * kPitch + kc];
-    transpose8x8_u16(in, out);
-    const int64_t g = m0 / 8 + rg;
-    if (g >= rg_end) return;
-    VFL_GLOBAL char* dst = glb((char*)J.in_rc.p) + (g * J.in_rc.cp + kbase) * 16;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      u32x4 v = out[j];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // rows 2w, 2w + 1 of the chunk: zero those past the group
-        const int r = m0 + rg * 8 + 2 * w;
-        uint32_t m = r < rows ? 0xffffu : 0u;
-        m |= r + 1 < rows ? 0xffff0000u : 0u;
-        v[w] &= m;
-      }
-      if (kbase + j < K) *(VFL_GLOBAL u32x4*)(dst + j * 16) = v;
-    }
-  };
-
   gload(0);
   lstore(0);
   __syncthreads();
@@ -197,7 +157,6 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
   for (int s = 0; s < nst; ++s) {
     const int b = s & 1;
     gload(min(s + 1, nst - 1));
-    if (J.in_rc.p && s % J.tiles_n == tile_n) in_rc(b, s);
     u32x4 a0[4], b0[kNB], a1[4], b1[kNB];
     frags(b, 0, a0, b0);
 #pragma unroll
@@ -216,9 +175,6 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
   // m0 + wm * 128 + mb * 32 + 8 g + 4 half + (0 .. 3) in acc[mb][nb][4 g ..]
   // (the last barrier of the loop follows every stage read, so the LDS
   // now holds each wavefront's private transpose tile)
-  const bool has_rm = J.out_rm != nullptr;
-  char* T = smem + wave * (128 * kOutPitch * 2);
-  const float* biasp = J.bias;
   // the mask chunks (if any) all in flight before the first is used:
   // chunk (mb, nb, p) = 8-row group 2 p + half of MFMA tile (mb, nb)
   u32x4 mk[4][kNB][2];
@@ -240,17 +196,14 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
   for (int nb = 0; nb < kNB; ++nb) {
     const int n = n0 + wn * kWN + nb * 32 + col;
     const bool nok = n < N;
-    const float bv = biasp ? glb(biasp)[min(n, N - 1)] : 0.f;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       const int rl = wm * 128 + mb * 32;           // block row of the MFMA tile
       float v[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float x0 = acc[mb][nb][e] + bv;
-        const float x = J.relu ? fmaxf(x0, 0.f) : x0;
         const int r = m0 + rl + 8 * (e >> 2) + 4 * half + (e & 3);
-        v[e] = (r < rows && nok) ? x : 0.f;
+        v[e] = (r < rows && nok) ? acc[mb][nb][e] : 0.f;
       }
       // 8-row groups g = 0..3 of the MFMA tile: half 0 holds rows 0..3 of
       // each, half 1 rows 4..7.  After one exchange per pair (2p, 2p + 1),
@@ -285,27 +238,6 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmJob* __restrict__ jp, co
                               pack_bf16(o[6], o[7])};
         *(VFL_GLOBAL u32x4*)(glb((char*)J.out_rc.p) + (rg * J.out_rc.cp + n) * 16) = q;
       }
-      if (has_rm) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int rr = mb * 32 + 8 * (e >> 2) + 4 * half + (e & 3);   // row of the wavefront tile
-          *(uint16_t*)(T + (rr * kOutPitch + nb * 32 + col) * 2) = (uint16_t)pack_bf16(v[e], 0.f);
-        }
-      }
-    }
-  }
-  if (has_rm) {
-    // the wavefront's 128 x 64 tile back in 16-byte row pieces (its own
-    // LDS writes are in order before its reads); rows of the group only,
-    // N a multiple of 8
-    VFL_GLOBAL char* O = glb((char*)J.out_rm);
-    const int r0 = m0 + wm * 128, c0 = n0 + wn * kWN;
-#pragma unroll 4
-    for (int i = 0; i < 128 * kWN / 8 / 64; ++i) {
-      const int c = i * 64 + lane, rr = c / (kWN / 8), ch = c % (kWN / 8);
-      const u32x4 x = *(const u32x4*)(T + (rr * kOutPitch + ch * 8) * 2);
-      if (r0 + rr < rows && c0 + ch * 8 < N)
-        *(VFL_GLOBAL u32x4*)(O + ((int64_t)(r0 + rr) * J.ldo + c0 + ch * 8) * 2) = x;
     }
   }
 }

@@ -317,22 +317,18 @@ hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float sc
                             float* loss_out, TickRef tr, float* loss_base, hipStream_t st);
 
 // ---------------------------------------------------------- layer products
-// One wide bottom layer over the rows of a group (bf16):
-// out[r][n] = sum_k A[r][k] W[n][k] (+ bias[n], ReLU when relu) or
-// (* (mask[r][n] > 0), mask_rc set), for r < rows; out_rc receives the RC
-// copy (rows from the group's end up to rows_pad zero), out_rm (nullable,
-// N a multiple of 8) the row-major copy, ldo elements per row.  A: row-major,
-// lda elements per row, zero from K up to the next multiple of 8; W packed
-// (pk_index, kst 32-k steps).  in_rc (nullable): RC copy of A's K columns.
-// Blocks: gemm_tiles(rows_pad, N): tiles_m x tiles_n tiles of 256 x 128
-// outputs, rounded up to a multiple of 8 (one contiguous range per XCD).
+// The input gradient of one wide bottom layer over the rows of a group
+// (bf16): out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k] for r < rows
+// (mask_rc null: no mask), into out_rc (rows from the group's end up to
+// rows_pad zero).  A: row-major, lda elements per row, zero from K up to
+// the next multiple of 8; W packed (pk_index, kst 32-k steps).  Blocks:
+// gemm_tiles(rows_pad, N): tiles_m x tiles_n tiles of 256 x 128 outputs,
+// rounded up to a multiple of 8 (one contiguous range per XCD).
 struct GemmJob {
   const void* A = nullptr; int64_t lda = 0;     // workspace operand (a launch may pass its own)
   const void* W = nullptr; int32_t kst = 0;
-  int32_t N = 0, K = 0, relu = 0;
-  const float* bias = nullptr;
-  RCMat out_rc, mask_rc, in_rc;
-  void* out_rm = nullptr; int64_t ldo = 0;
+  int32_t N = 0, K = 0;
+  RCMat out_rc, mask_rc;
   int32_t tiles_n = 0, tiles_m = 0, rows_pad = 0;
 };
 int gemm_tiles(int rows, int N);
