@@ -510,7 +510,24 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
 // row-major element-T rows; norm/cfac (nullable) receive ||v|| and the clip
 // factor.  16 lanes per row (4 rows per wavefront at a time), each lane on
 // the 4-column groups cg, cg + 16, ...; the noise is keyed by the row's
-// sample id.
+// sample id, two groups' Philox blocks at a time (independent instruction
+// streams, so one lane keeps the VALU busy).
+template <typename V>
+__device__ __forceinline__ void msg_ld4(const char* row, int g, int D, float (&x)[4]) {
+  ld4<V>(row + 4 * g * (int)sizeof(V), x);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = 4 * g + e < D ? x[e] : 0.f;   // columns past D may hold anything
+}
+template <typename T>
+__device__ __forceinline__ void msg_st4(VFL_GLOBAL T* o, int g, int D, const float (&v)[4]) {
+  if (4 * g + 4 <= D) {
+    st4<T>((T*)(o + 4 * g), v);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (4 * g + e < D) st1<T>((T*)(o + 4 * g + e), v[e]);
+  }
+}
 template <typename T, typename V, int BR>
 __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, const MsgOp& m,
                                          uint32_t step, int64_t sample0, void* out, int64_t ldo,
@@ -524,11 +541,10 @@ __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, 
     const char* row = s + src.off + r * src.pitch;
     float ss = 0.f;
     for (int g = cg; g < ngrp; g += 16) {
+      float x[4];
+      msg_ld4<V>(row, g, D, x);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int c = 4 * g + e;
-        if (c < D) { const float x = ld1<V>((const V*)row + c); ss += x * x; }
-      }
+      for (int e = 0; e < 4; ++e) ss += x[e] * x[e];
     }
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o, 64);
@@ -540,22 +556,23 @@ __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, 
     }
     VFL_GLOBAL T* o = glb((T*)out) + (int64_t)(r0 + r) * ldo;
     const uint32_t grow = (uint32_t)(sample0 + r0 + r);
-    for (int g = cg; g < ngrp; g += 16) {
-      float xi[4] = {0.f, 0.f, 0.f, 0.f};
-      if (m.noise) gauss4(m.seed, step, grow, (uint32_t)g, m.tag, xi);
-      float v[4];
+    for (int g = cg; g < ngrp; g += 32) {
+      // groups g and g + 16 (the second past the row: computed, never stored)
+      float xa[4] = {0.f, 0.f, 0.f, 0.f}, xb[4] = {0.f, 0.f, 0.f, 0.f};
+      if (m.noise) {
+        gauss4(m.seed, step, grow, (uint32_t)g, m.tag, xa);
+        gauss4(m.seed, step, grow, (uint32_t)(g + 16), m.tag, xb);
+      }
+      float va[4], vb[4];
+      msg_ld4<V>(row, g, D, va);
+      msg_ld4<V>(row, min(g + 16, ngrp - 1), D, vb);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int c = 4 * g + e;
-        v[e] = c < D ? cf * ld1<V>((const V*)row + c) + m.stdv * xi[e] : 0.f;
+        va[e] = 4 * g + e < D ? cf * va[e] + m.stdv * xa[e] : 0.f;
+        vb[e] = cf * vb[e] + m.stdv * xb[e];
       }
-      if (4 * g + 4 <= D) {
-        st4<T>((T*)(o + 4 * g), v);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (4 * g + e < D) st1<T>((T*)(o + 4 * g + e), v[e]);
-      }
+      msg_st4<T>(o, g, D, va);
+      if (g + 16 < ngrp) msg_st4<T>(o, g + 16, D, vb);
     }
   }
 }
@@ -705,12 +722,7 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
       for (int e = 0; e < 4; ++e) g[i][e] = 0.f;
     float lsum = 0.f, dsum = 0.f;
     const bool relu_h = j.relu_h != 0;
-#pragma unroll
-    for (int rr = 0; rr < RW; ++rr) {
-      const int r = wave * RW + rr;
-      const bool ok = r < rv;
-      float h[kLogitChunks][4];
-      float dot = 0.f;
+    auto load_h = [&](int r, float (&h)[kLogitChunks][4]) {
 #pragma unroll
       for (int i = 0; i < kLogitChunks; ++i) {
         const int c0 = 256 * i + 4 * lane;
@@ -719,11 +731,33 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
 #pragma unroll
           for (int e = 0; e < 4; ++e) h[i][e] = 0.f;
         }
+      }
+    };
+    // the logits of the wavefront's rows: partial dots first, then their
+    // wavefront reductions side by side (independent shuffle chains)
+    float dots[RW];
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      float h[kLogitChunks][4];
+      load_h(wave * RW + rr, h);
+      float dot = 0.f;
+#pragma unroll
+      for (int i = 0; i < kLogitChunks; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) dot += h[i][e] * lwr[i][e];
-      }
-      dot = wave_sum(dot);
-      const float l = dot + lbias;
+      dots[rr] = dot;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr) dots[rr] += __shfl_xor(dots[rr], o, 64);
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      const int r = wave * RW + rr;
+      const bool ok = r < rv;
+      float h[kLogitChunks][4];
+      load_h(r, h);
+      const float l = dots[rr] + lbias;
       const float yy = yl[r];
       const float ex = __expf(-fabsf(l));
       const float inv = __frcp_rn(1.f + ex);

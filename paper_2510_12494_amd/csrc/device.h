@@ -124,7 +124,10 @@ __device__ __forceinline__ float word_uniform(uint32_t w) {  // (0, 1], exact
 }
 
 // four standard normals for columns 4q .. 4q+3 of (step, row, tag):
-// Box-Muller on the word pairs (0, 1) and (2, 3) of one Philox block
+// Box-Muller on the word pairs (0, 1) and (2, 3) of one Philox block, with
+// the hardware's single-instruction transcendentals: -2 ln u = -2 ln 2 *
+// log2 u (v_log_f32), v_sqrt_f32, and v_sin_f32 / v_cos_f32, whose argument
+// is in revolutions, so sin(2 pi u) is one instruction
 __device__ __forceinline__ void gauss4(uint64_t seed, uint32_t step, uint32_t row, uint32_t q,
                                        uint32_t tag, float (&n)[4]) {
   uint32_t c[4] = {step, row, q, tag};
@@ -132,11 +135,9 @@ __device__ __forceinline__ void gauss4(uint64_t seed, uint32_t step, uint32_t ro
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const float ua = word_uniform(c[2 * p]), ub = word_uniform(c[2 * p + 1]);
-    const float rad = sqrtf(-2.f * logf(ua));
-    float s, co;
-    sincospif(2.f * ub, &s, &co);
-    n[2 * p] = rad * co;
-    n[2 * p + 1] = rad * s;
+    const float rad = __builtin_amdgcn_sqrtf(-1.3862943611198906f * __builtin_amdgcn_logf(ua));
+    n[2 * p] = rad * __builtin_amdgcn_cosf(ub);
+    n[2 * p + 1] = rad * __builtin_amdgcn_sinf(ub);
   }
 }
 
