@@ -109,6 +109,19 @@ struct Pipe {
   u32x4 wa[kPF][kNTW], wb[kPF][kNTW];
 };
 
+// The RC copy of a stage's LDS output (lds_to_rc of b's first cols columns
+// into m at block row r0; m.p null: none), left for the next product to
+// issue.  On gfx950 stores count in the same in-order counter as loads, so
+// a wait for any load issued after a store also waits for the store's
+// write to complete; the next product issues the copy after its last
+// weight loads, where nothing waits on them until the product after it.
+struct RcPend {
+  LBuf b;
+  int cols = 0;
+  RCMat m;
+  int r0 = 0;
+};
+
 // A pointer or value the compiler must keep in scalar registers (it is
 // uniform, but derived through selects the compiler may place in vector
 // registers, and a field loaded through a vector-register pointer is a
@@ -209,10 +222,15 @@ __device__ __forceinline__ uint32_t warm_l2(const WarmSet& w, const void* dummy)
 // multiple of 4; bias[i] = bias[n + i] from the LDS table, zero without a
 // bias or past N), for every row of the block and every column below N
 // rounded up to the MFMA depth.  On entry p holds groups 0 and 1 of L's
-// first pass; on return, groups 0 and 1 of `next`'s (nullable).
+// first pass; on return, groups 0 and 1 of `next`'s (nullable).  The
+// pending RC copy (whose LDS rows this product does not write) is issued
+// in the last pass once every weight load of the pass is out.
+template <typename T, int BR>
+__device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0);
+
 template <typename T, int RT, typename Epi>
 __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe& p,
-                                         const ChainLayer* next, Epi&& epi) {
+                                         const ChainLayer* next, const RcPend& pend, Epi&& epi) {
   constexpr int PF = kPF, NTW = kNTW;
   const int lane = threadIdx.x & 63;
   const int kc = lane >> 4, lr = lane & 15;
@@ -290,6 +308,7 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
       group(g + 1, p.wb);
       refill(g + 3, p.wb);
     }
+    if (!more && pend.m.p) lds_to_rc<T, 16 * RT>(s, pend.b, pend.cols, pend.m, pend.r0);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       if (tile[j] >= ntl) continue;
@@ -304,13 +323,13 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
 // Forward or input-gradient layer into LDS (see ChainLayer).
 template <typename T, int RT>
 __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe& p,
-                                          const ChainLayer* next) {
+                                          const ChainLayer* next, const RcPend& pend) {
   const int N = L.N;
   const bool relu = L.relu != 0, msk = L.mask.pitch > 0, nopad = L.nopad != 0;
   const LBuf out = L.out, mk = L.mask;
   // branch-free: every condition is a select (a short-circuit test here
   // compiles to one exec-mask branch per element)
-  block_mm<T, RT>(s, L, p, next, [&](int r, int n, const f32x4& a, const f32x4& b) {
+  block_mm<T, RT>(s, L, p, next, pend, [&](int r, int n, const f32x4& a, const f32x4& b) {
     float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
     if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
     const bool rok = r < rv;
@@ -331,10 +350,10 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
 // of gx (block rows below rv).
 template <typename T, int RT>
 __device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float* gx, int64_t ldgx,
-                                       int r0, int rv, Pipe& p) {
+                                       int r0, int rv, Pipe& p, const RcPend& pend) {
   const int N = L.N;
   VFL_GLOBAL float* gxg = glb(gx);
-  block_mm<T, RT>(s, L, p, nullptr, [&](int r, int n, const f32x4& a, const f32x4&) {
+  block_mm<T, RT>(s, L, p, nullptr, pend, [&](int r, int n, const f32x4& a, const f32x4&) {
     if (r >= rv) return;
     VFL_GLOBAL float* dst = gxg + (int64_t)(r0 + r) * ldgx + n;
     if (n + 4 <= N) {
@@ -600,12 +619,14 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
   load_input<T, BR>(s, j.in, cc, k, r0, rv);
   __syncthreads();
   asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
-  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
+  // each stage's RC copy goes out during the next product
+  RcPend pend{j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0};
   for (int l = 0; l < nL; ++l) {
-    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < nL ? &j.l[l + 1] : nullptr);
+    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < nL ? &j.l[l + 1] : nullptr, pend);
     __syncthreads();
-    if (j.l[l].rc.p) lds_to_rc<T, BR>(s, j.l[l].out, j.l[l].N, j.l[l].rc, r0);
+    pend = RcPend{j.l[l].out, j.l[l].N, j.l[l].rc, r0};
   }
+  if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
   const ChainLayer& last = j.l[nL - 1];
   lds_to_rows<T, BR>(s, last.out, last.N, j.z, j.ldz, r0, rv);
   if (j.publish)
@@ -688,19 +709,22 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   }
   __syncthreads();
   asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
-  if (j.in.rc.p) lds_to_rc<T, BR>(s, j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0);
+  // each stage's RC copy goes out during the next product (A's last
+  // layer writes cat, copied whole)
+  RcPend pend{j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0};
   for (int l = 0; l < LA; ++l) {
-    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < LA ? &j.fa[l + 1] : &j.ft[0]);
+    run_layer<T, RT>(s, j.fa[l], rv, pp, l + 1 < LA ? &j.fa[l + 1] : &j.ft[0], pend);
     __syncthreads();
-    if (j.fa[l].rc.p) lds_to_rc<T, BR>(s, j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0);
+    pend = l + 1 < LA ? RcPend{j.fa[l].out, j.fa[l].N, j.fa[l].rc, r0} : RcPend{j.cat, j.dA + j.dB, j.cat_rc, r0};
   }
-  if (j.cat_rc.p) lds_to_rc<T, BR>(s, j.cat, j.dA + j.dB, j.cat_rc, r0);
   // top hidden layers
   for (int q = 0; q < H; ++q) {
-    run_layer<T, RT>(s, j.ft[q], rv, pp, q + 1 < H ? &j.ft[q + 1] : (H > 1 ? &j.dt[0] : &j.dc));
+    run_layer<T, RT>(s, j.ft[q], rv, pp, q + 1 < H ? &j.ft[q + 1] : (H > 1 ? &j.dt[0] : &j.dc), pend);
     __syncthreads();
-    if (j.ft[q].rc.p) lds_to_rc<T, BR>(s, j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0);
+    pend = RcPend{j.ft[q].out, j.ft[q].N, j.ft[q].rc, r0};
   }
+  // the logit stage reads the last hidden output, not a product's input
+  if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
   // logit + BCE (Eq. 1), dl = sigmoid(l) - y: a wavefront per row (its
   // BR / 8 rows one after the other), lane on the columns 256 i + 4 lane
   // .. +4; the last hidden delta dl * w (ReLU-masked) goes to LDS.  The
@@ -801,12 +825,12 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
       part[c] = t;
     }
   }
-  if (j.dh_rc.p) lds_to_rc<T, BR>(s, j.dh, j.ft[H - 1].N, j.dh_rc, r0);
+  pend = RcPend{j.dh, j.ft[H - 1].N, j.dh_rc, r0};
   // top input-gradient chain
   for (int q = 0; q + 1 < H; ++q) {
-    run_layer<T, RT>(s, j.dt[q], rv, pp, q + 2 < H ? &j.dt[q + 1] : &j.dc);
+    run_layer<T, RT>(s, j.dt[q], rv, pp, q + 2 < H ? &j.dt[q + 1] : &j.dc, pend);
     __syncthreads();
-    if (j.dt[q].rc.p) lds_to_rc<T, BR>(s, j.dt[q].out, j.dt[q].N, j.dt[q].rc, r0);
+    pend = RcPend{j.dt[q].out, j.dt[q].N, j.dt[q].rc, r0};
   }
   // concat product: A's cut delta and the gradient message for B
   {
@@ -816,7 +840,7 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     const bool maskA = j.dc.mask.pitch > 0, gextra = j.gextra != 0;
     VFL_GLOBAL T* ring = glb((T*)j.ring);
     const int64_t ldr = j.ldring;
-    block_mm<T, RT>(s, j.dc, pp, nda > 0 ? &j.da[0] : (has_gx ? &j.gx : nullptr),
+    block_mm<T, RT>(s, j.dc, pp, nda > 0 ? &j.da[0] : (has_gx ? &j.gx : nullptr), pend,
                     [&](int r, int n, const f32x4& a, const f32x4&) {
       const bool ok = r < rv;
       if (n + 4 <= dA) {
@@ -844,18 +868,19 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
       }
     });
     __syncthreads();
-    if (j.dc.rc.p) lds_to_rc<T, BR>(s, ob, dA, j.dc.rc, r0);
+    pend = RcPend{ob, dA, j.dc.rc, r0};
     if (gextra)
       msg_rows<T, float, BR>(s, msg, j.dB, j.m, (uint32_t)k.group, k.row0, j.ring, j.ldring, nullptr,
                              nullptr, r0, rv);
   }
   // A's input-gradient chain
   for (int q = 0; q < nda; ++q) {
-    run_layer<T, RT>(s, j.da[q], rv, pp, q + 1 < nda ? &j.da[q + 1] : (has_gx ? &j.gx : nullptr));
+    run_layer<T, RT>(s, j.da[q], rv, pp, q + 1 < nda ? &j.da[q + 1] : (has_gx ? &j.gx : nullptr), pend);
     __syncthreads();
-    if (j.da[q].rc.p) lds_to_rc<T, BR>(s, j.da[q].out, j.da[q].N, j.da[q].rc, r0);
+    pend = RcPend{j.da[q].out, j.da[q].N, j.da[q].rc, r0};
   }
-  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
+  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp, pend);
+  else if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
 }
 
 template <typename T, int RT>
@@ -933,14 +958,16 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
   }
   __syncthreads();
   asm volatile("" ::"v"(wx));   // the L2 fetches have landed with the inputs
-  if (j.d_rc.p) lds_to_rc<T, BR>(s, j.d, j.D, j.d_rc, r0);
+  // each stage's RC copy goes out during the next product
+  RcPend pend{j.d, j.D, j.d_rc, r0};
   for (int q = 0; q < nd; ++q) {
     const ChainLayer& L = j.dx[q];
-    run_layer<T, RT>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr));
+    run_layer<T, RT>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr), pend);
     __syncthreads();
-    if (L.rc.p) lds_to_rc<T, BR>(s, L.out, L.N, L.rc, r0);
+    pend = RcPend{L.out, L.N, L.rc, r0};
   }
-  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp);
+  if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp, pend);
+  else if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
   if (j.drm) {
     // the last delta of the chain, row-major, for the layer product below it
     const LBuf last = nd > 0 ? j.dx[nd - 1].out : j.d;

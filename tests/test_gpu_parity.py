@@ -239,3 +239,24 @@ def test_wide_first_layer_product(widths, s, k, clip):
     _check_losses(run, recs, 1e-3)
     _check_messages(run, recs, w)
     _check_params(run, recs, w, per_tick=True)
+
+
+def test_shared_lds_buffers_deep_top():
+    """The active kernel shares LDS between buffers that are never live
+    together (its input with the second delta buffer, the last top hidden
+    output with the gradient-message staging): two hidden top layers (the
+    delta chain then writes the second buffer and reads the first hidden
+    layer's mask), clip and noise on both messages, two A layers, and groups
+    large enough for 32-row blocks."""
+    w = Workload(name="deep_top", n_rows=3 * 8192 + 1000, dtype="bf16",
+                 A=PartySpec(dense=40, widths=[72, 32]), B=PartySpec(dense=24, widths=[48, 24]),
+                 top=TopSpec(widths=[64, 40, 1]), batch=8192, staleness=1, replicas=1, lr=0.2,
+                 clip=1.0, sigma=0.5, clip_emb=True, clip_grad=True, noise_emb=True,
+                 noise_grad=True, labels="teacher", data_seed=61, init_seed=62, noise_seed=63)
+    n_groups = 4
+    run = H.Run(w, w.n_rows, n_groups)
+    o, recs = run.oracle("bf16")
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
