@@ -242,6 +242,32 @@ vfl_status vfl_get_trace(vfl_ctx* c, int64_t* buf, size_t cap_rows, size_t* rows
  * staleness s and n_groups groups (no context, no GPU). */
 vfl_status vfl_schedule_tick(int64_t t, int32_t s, int64_t n_groups, int64_t out[7]);
 
+/* Checkpoint and resume.  The state of a context is what the next tick
+ * depends on: both parties' parameters (float32 masters, tables, B's
+ * per-slot stashed weight copies), the contents and headers of the
+ * publisher/subscriber channel slots (Section 4.1: the embedding ring, the
+ * gradient ring and B's stashed activations, masks and clip factors of the
+ * groups in flight), the versions and next groups of both parties, and the
+ * integer schedule trace.  The image is a host buffer of vfl_state_size()
+ * bytes (the size grows with the trace: ask again right before
+ * vfl_get_state).  vfl_get_state synchronises both streams and copies the
+ * whole workspace to the image; VFL_E_STATE while party A is inside a
+ * group's step (after vfl_bottom_forward(A) and before its
+ * vfl_bottom_backward), VFL_E_INVALID if bytes is too small.
+ * vfl_set_state synchronises both streams, restores the image into this
+ * context (the same one, or a fresh one created with the same specs,
+ * dtype, batch, staleness and replicas on any workspace; the hyper-
+ * parameters lr, clip, sigma, seed and flags are this context's), and
+ * leaves every channel event complete; VFL_E_INVALID for a foreign,
+ * truncated or mismatched image (the context is then unchanged).  A
+ * restored run continues exactly as the original from the tick after the
+ * image: its results are bitwise those of the uninterrupted run.  Batch
+ * pointers of the slots are not part of the image (only the forward that
+ * filled a slot reads them). */
+vfl_status vfl_state_size(const vfl_ctx* c, size_t* bytes);
+vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes);
+vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes);
+
 /* Synchronise both streams and report the device-side channel checks: the
  * number of times a consumer found a slot header whose group differs from
  * the one it expected (0 when the channel is race-free). */

@@ -1189,6 +1189,48 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
   return enqueue_table_sgd(c, p.P, slot, st.rows, c->o.lr / (float)st.rows, c->sb, tr);
 }
 
+// ---- checkpoint / resume: host channel state + the whole workspace
+
+// Fixed header of a state image, followed by the workspace bytes and the
+// schedule trace (int64).  Slot inputs are not kept: a slot's batch
+// pointers are read only by the forward that filled it.
+struct StateHead {
+  char magic[8];
+  uint32_t format, n_slots;
+  uint64_t layout, ws_bytes, trace_len;
+  int64_t b_next_fwd, b_next_bwd, b_version, b_pub_next, a_next, a_version, a_copy_version;
+  int64_t b_copy_version[kMaxSlots], grad_group[kMaxSlots], grad_rows[kMaxSlots];
+  int64_t slot_group[kMaxSlots], slot_version[kMaxSlots], slot_row0[kMaxSlots], slot_rows[kMaxSlots],
+      slot_published[kMaxSlots];
+};
+constexpr char kStateMagic[8] = {'V', 'F', 'L', 'S', 'T', 'A', 'T', 'E'};
+constexpr uint32_t kStateFormat = 1;
+
+// FNV-1a over everything that fixes the workspace layout: element type,
+// batch, staleness, replicas and both bottom specs and the top spec.
+uint64_t layout_signature(const vfl_ctx* c) {
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&](int64_t v) {
+    for (int i = 0; i < 8; ++i) {
+      h ^= (uint64_t)((v >> (8 * i)) & 0xff);
+      h *= 1099511628211ull;
+    }
+  };
+  const Plan& p = c->p;
+  mix(p.e); mix(p.B); mix(p.s); mix(p.k); mix((int64_t)p.total);
+  for (const vfl_bottom_spec* b : {&p.A.spec, &p.P.spec}) {
+    mix(b->dense_in); mix(b->n_cat); mix(b->vocab); mix(b->emb_dim); mix(b->n_layers); mix(b->relu_mask);
+    for (int l = 0; l < b->n_layers; ++l) mix(b->widths[l]);
+  }
+  mix(p.T.spec.n_layers); mix(p.T.spec.relu_mask);
+  for (int j = 0; j < p.T.spec.n_layers; ++j) mix(p.T.spec.widths[j]);
+  return h;
+}
+
+size_t state_bytes(const vfl_ctx* c) {
+  return sizeof(StateHead) + c->p.total + sizeof(int64_t) * c->trace.size();
+}
+
 vfl_status param_loc(vfl_ctx* c, vfl_party party, int layer, int kind, size_t& off, size_t& bytes) {
   const Plan& p = c->p;
   if (party == VFL_PARTY_A || party == VFL_PARTY_B) {
@@ -1740,6 +1782,92 @@ vfl_status vfl_timing_read(vfl_ctx* c, int32_t cls, double* ms, int64_t* launche
   T.ms[cls] = 0.0;
   T.wk[cls] = 0.0;
   T.n[cls] = 0;
+  return VFL_OK;
+}
+
+vfl_status vfl_state_size(const vfl_ctx* c, size_t* bytes) {
+  if (!c || !bytes) return VFL_E_INVALID;
+  *bytes = state_bytes(c);
+  return VFL_OK;
+}
+
+vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes) {
+  if (!c || !host_buf) return VFL_E_INVALID;
+  if (c->a_phase != 0) return fail(c, VFL_E_STATE, "A is inside a group's step (forward or top step pending)");
+  if (c->capture_phase >= 0) return fail(c, VFL_E_STATE, "graph capture in progress");
+  if (bytes < state_bytes(c)) return fail(c, VFL_E_INVALID, "buffer smaller than vfl_state_size()");
+  const Plan& p = c->p;
+  StateHead h;
+  std::memset(&h, 0, sizeof(h));
+  std::memcpy(h.magic, kStateMagic, sizeof(h.magic));
+  h.format = kStateFormat;
+  h.n_slots = (uint32_t)(p.s + 1);
+  h.layout = layout_signature(c);
+  h.ws_bytes = p.total;
+  h.trace_len = c->trace.size();
+  h.b_next_fwd = c->b_next_fwd; h.b_next_bwd = c->b_next_bwd; h.b_version = c->b_version;
+  h.b_pub_next = c->b_pub_next; h.a_next = c->a_next; h.a_version = c->a_version;
+  h.a_copy_version = c->a_copy_version;
+  for (int q = 0; q < kMaxSlots; ++q) {
+    h.b_copy_version[q] = c->b_copy_version[q];
+    h.grad_group[q] = c->grad_group[q];
+    h.grad_rows[q] = c->grad_rows[q];
+    const SlotState& st = c->bslot[q];
+    h.slot_group[q] = st.group; h.slot_version[q] = st.version; h.slot_row0[q] = st.row0;
+    h.slot_rows[q] = st.rows; h.slot_published[q] = st.published;
+  }
+  char* out = (char*)host_buf;
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  std::memcpy(out, &h, sizeof(h));
+  HIPCHK(hipMemcpy(out + sizeof(h), c->ws, p.total, hipMemcpyDeviceToHost));
+  if (!c->trace.empty())
+    std::memcpy(out + sizeof(h) + p.total, c->trace.data(), sizeof(int64_t) * c->trace.size());
+  return VFL_OK;
+}
+
+vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes) {
+  if (!c || !host_buf) return VFL_E_INVALID;
+  if (c->capture_phase >= 0) return fail(c, VFL_E_STATE, "graph capture in progress");
+  const Plan& p = c->p;
+  StateHead h;
+  if (bytes < sizeof(h)) return fail(c, VFL_E_INVALID, "state image too short");
+  std::memcpy(&h, host_buf, sizeof(h));
+  if (std::memcmp(h.magic, kStateMagic, sizeof(h.magic)) || h.format != kStateFormat)
+    return fail(c, VFL_E_INVALID, "not a state image of this library");
+  if (h.layout != layout_signature(c) || h.ws_bytes != p.total || h.n_slots != (uint32_t)(p.s + 1))
+    return fail(c, VFL_E_INVALID, "state image of another configuration");
+  if (h.trace_len % 7 || bytes < sizeof(h) + h.ws_bytes + sizeof(int64_t) * h.trace_len)
+    return fail(c, VFL_E_INVALID, "state image truncated");
+  const char* in = (const char*)host_buf;
+  HIPCHK(hipStreamSynchronize(c->sa));
+  HIPCHK(hipStreamSynchronize(c->sb));
+  HIPCHK(hipMemcpy(c->ws, in + sizeof(h), p.total, hipMemcpyHostToDevice));
+  // the image's job descriptors point into the workspace it was taken from
+  const vfl_status js = write_jobs(c);
+  if (js != VFL_OK) return js;
+  c->b_next_fwd = h.b_next_fwd; c->b_next_bwd = h.b_next_bwd; c->b_version = h.b_version;
+  c->b_pub_next = h.b_pub_next; c->a_next = h.a_next; c->a_version = h.a_version;
+  c->a_copy_version = h.a_copy_version;
+  c->a_phase = 0;
+  c->aslot = SlotState();
+  c->a_loss = nullptr;
+  for (int q = 0; q < kMaxSlots; ++q) {
+    c->b_copy_version[q] = h.b_copy_version[q];
+    c->grad_group[q] = h.grad_group[q];
+    c->grad_rows[q] = (int)h.grad_rows[q];
+    SlotState st;
+    st.group = h.slot_group[q]; st.version = h.slot_version[q]; st.row0 = h.slot_row0[q];
+    st.rows = (int)h.slot_rows[q]; st.published = h.slot_published[q] != 0;
+    c->bslot[q] = st;
+  }
+  c->trace.assign((const int64_t*)(in + sizeof(h) + h.ws_bytes),
+                  (const int64_t*)(in + sizeof(h) + h.ws_bytes) + h.trace_len);
+  // the channel events: everything they guarded is in place
+  for (int q = 0; q <= p.s; ++q) {
+    HIPCHK(hipEventRecord(c->ev_emb[q], c->sb));
+    HIPCHK(hipEventRecord(c->ev_grad[q], c->sa));
+  }
   return VFL_OK;
 }
 

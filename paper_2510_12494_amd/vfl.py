@@ -8,6 +8,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvfl.so")
 
@@ -26,7 +28,7 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
-           "vfl_last_error", "vfl_destroy")
+           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_last_error", "vfl_destroy")
 KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm")
 
 
@@ -90,6 +92,9 @@ def _load():
         "vfl_timing_read": [P, I32, C.POINTER(C.c_double), C.POINTER(I64), C.POINTER(C.c_double)],
         "vfl_bind_dataset": [P, C.POINTER(vfl_dataset), C.POINTER(vfl_dataset), I64],
         "vfl_run": [P, I64, I64, P, I64],
+        "vfl_state_size": [P, C.POINTER(SZ)],
+        "vfl_get_state": [P, P, SZ],
+        "vfl_set_state": [P, P, SZ],
         "vfl_destroy": [P],
     }
     for name, args in sig.items():
@@ -220,6 +225,24 @@ def vfl_bind_dataset(ctx, a: vfl_dataset, b: vfl_dataset, n_rows: int):
 
 def vfl_run(ctx, t0: int, n: int, loss_ptr: int = 0, loss_len: int = 0):
     _chk(_lib.vfl_run(ctx, t0, n, C.c_void_p(loss_ptr or None), loss_len), "vfl_run", ctx)
+
+
+def vfl_state_size(ctx) -> int:
+    n = C.c_size_t(0)
+    _chk(_lib.vfl_state_size(ctx, C.byref(n)), "vfl_state_size", ctx)
+    return n.value
+
+
+def vfl_get_state(ctx) -> np.ndarray:
+    """The context's state image (uint8 host array of vfl_state_size bytes)."""
+    buf = np.empty(vfl_state_size(ctx), dtype=np.uint8)
+    _chk(_lib.vfl_get_state(ctx, buf.ctypes.data, buf.nbytes), "vfl_get_state", ctx)
+    return buf
+
+
+def vfl_set_state(ctx, image: np.ndarray):
+    a = np.ascontiguousarray(image, dtype=np.uint8)
+    _chk(_lib.vfl_set_state(ctx, a.ctypes.data, a.nbytes), "vfl_set_state", ctx)
 
 
 def vfl_last_error(ctx) -> str:
