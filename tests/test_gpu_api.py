@@ -69,12 +69,14 @@ def test_protocol_errors():
         s.close()
 
 
-def test_individual_calls_equal_vfl_step():
+@pytest.mark.parametrize("name", ["dense_tabular", "ctr", "private", "hetero"])
+def test_individual_calls_equal_vfl_step(name):
     """Driving the phases one call at a time in the schedule's order gives
-    bitwise the same parameters as vfl_step."""
+    bitwise the same parameters as vfl_step: tables (ctr), clip and noise
+    (private), B's wide-layer product (hetero)."""
     from paper_2510_12494_amd import vfl as V
-    w, s1, p = _session(groups=5)
-    w, s2, _ = _session(groups=5)
+    w, s1, p = _session(name, groups=5)
+    w, s2, _ = _session(name, groups=5)
     shapes = {k: v.shape for k, v in p.items()}
     try:
         for t in range(5 + w.staleness):
