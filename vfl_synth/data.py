@@ -74,8 +74,8 @@ def generate(w: Workload, n_rows: int | None = None) -> dict:
             ids = np.empty((n, spec.n_cat), np.int32)
             for c, lo, hi in _chunks(n):
                 u = _rng(w.data_seed, c, pid, 1).random((hi - lo, spec.n_cat))
-                ids[lo:hi] = np.minimum(np.searchsorted(cdf, u, side="right"),
-                                        spec.vocab - 1)
+                k = np.minimum(np.searchsorted(cdf, u, side="right"), spec.vocab - 1)
+                ids[lo:hi] = (k + w.id_shift) % spec.vocab
             out[key] = ids
     out["y"] = _labels(w, out, n)
     return out

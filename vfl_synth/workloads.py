@@ -84,6 +84,7 @@ class Workload:
     labels: str = "teacher"  # "logistic" | "teacher" | "bernoulli"
     label_p: float = 0.25
     zipf_a: float = 1.1
+    id_shift: int = 0        # ids (k + id_shift) mod vocab: moves the hot ids
     data_seed: int = 0
     init_seed: int = 0
     noise_seed: int = 0
