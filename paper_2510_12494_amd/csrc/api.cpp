@@ -42,7 +42,8 @@ constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
 constexpr int kGemmMinWidth = 512;    // B's first-layer width from which its input gradient is a layer product
 constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
 constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
-constexpr int kDwRows = 256;          // rows of two k_dw load groups (4 MFMA steps each, bf16)
+constexpr int kDwRows = 256;          // rows of two k_dw load groups (4 MFMA steps each) in bf16;
+                                      // float32 chunks hold half the rows: 128
 constexpr int kTimedEvery = 4;        // ticks of a captured cycle between timed ticks
 
 int64_t ld_of(int w) { return ((int64_t)w + 7) / 8 * 8; }  // 16-byte rows for both types
@@ -290,15 +291,15 @@ constexpr double kDwtMinFlops = 4e9;
 // element size) contract all their rows in one block per 32 x 32 tile.
 constexpr int kDwUnsplitBytes = 2048;
 
-// Row chunks of a weight-gradient launch over `tiles` output tiles: aim at
-// kDwBlocks blocks, chunks a multiple of kDwRows rows (the rows of one load
-// group of the kernel).
-void dw_split(int R, int tiles, DwMeta& m) {
-  const int max_splits = std::max(1, (R + kDwRows - 1) / kDwRows);
-  // the large-tile kernel runs one block per CU: never more than kDwBlocks
-  const int want = m.tile == 256 ? kDwBlocks / tiles : (kDwBlocks + tiles - 1) / tiles;
-  const int s = std::min(max_splits, std::max(1, want));
-  m.rps = ((R + s - 1) / s + kDwRows - 1) / kDwRows * kDwRows;
+// Row chunks of a weight-gradient launch over `tiles` output tiles: at
+// most kDwBlocks blocks (one round on the CUs: a few blocks past it would
+// double the launch), chunks a multiple of two load groups (kDwRows rows
+// in bf16, half that in float32).
+void dw_split(int R, int tiles, bool bf16, DwMeta& m) {
+  const int gran = bf16 ? kDwRows : kDwRows / 2;
+  const int max_splits = std::max(1, (R + gran - 1) / gran);
+  const int s = std::min(max_splits, std::max(1, kDwBlocks / tiles));
+  m.rps = ((R + s - 1) / s + gran - 1) / gran * gran;
   m.splits = (R + m.rps - 1) / m.rps;
 }
 
@@ -450,8 +451,8 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       p.da.tile = bf && 2.0 * p.R * (bottom_macs(a) + top_macs) >= kDwtMinFlops ? 256 : 64;
       p.db.tile = bf && 2.0 * p.R * bottom_macs(b) >= kDwtMinFlops ? 256 : 64;
       const int ta = bottom_tiles(a, p.da.tile) + top_tiles(p.da.tile), tb = bottom_tiles(b, p.db.tile);
-      dw_split(p.R, ta, p.da);
-      dw_split(p.R, tb, p.db);
+      dw_split(p.R, ta, bf, p.da);
+      dw_split(p.R, tb, bf, p.db);
       p.da.blocks = ta * p.da.splits;
       p.db.blocks = tb * p.db.splits;
       p.Ra = std::max(p.da.splits * p.da.rps, p.db.splits * p.db.rps);
