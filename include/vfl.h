@@ -76,7 +76,9 @@ enum {
   VFL_NOISE_EMB = 1,    /* add Gaussian noise to the published embedding */
   VFL_NOISE_GRAD = 2,   /* add Gaussian noise to the returned gradient */
   VFL_CLIP_EMB = 4,     /* clip each embedding row to L2 norm clip_c */
-  VFL_CLIP_GRAD = 8     /* clip each gradient row to L2 norm clip_c */
+  VFL_CLIP_GRAD = 8,    /* clip each gradient row to L2 norm clip_c */
+  VFL_FIFO_DISCARD = 16 /* a full channel discards its oldest group (see
+                           vfl_bottom_forward) instead of VFL_E_STALE */
 };
 
 #define VFL_MAX_LAYERS 8
@@ -163,8 +165,13 @@ vfl_status vfl_get_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kin
  * Party B: uses B's current parameters (the version is recorded), stashes
  * the weights and activations in the group's slot (group mod (s+1)); at most
  * s+1 groups may be in flight (published and not yet back-propagated), else
- * VFL_E_STALE.  Party A: group must be the next group A consumes.
- * per_replica: n_replicas (1..k) back-to-back batches. */
+ * VFL_E_STALE.  With VFL_FIFO_DISCARD the channel instead discards its
+ * oldest group (the buffer mechanism of Section 4.2): its embedding when A
+ * has not taken it yet (A then skips that group), else its gradient; either
+ * way B drops the group without an update and reuses its slot
+ * (VFL_E_STALE remains when A is inside that group's step).  Party A: group
+ * must be the next group A consumes.  per_replica: n_replicas (1..k)
+ * back-to-back batches. */
 vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group,
                               const vfl_batch* per_replica, int32_t n_replicas);
 
@@ -187,11 +194,23 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev);
  * goes to B's current parameters and increments B's version. */
 vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group);
 
+/* Waiting deadline (Section 4.2): party A gives up on `group`, the next
+ * group it would consume, before its forward (host-decided, for instance
+ * after a deadline on the embedding's event).  A moves on to group + 1; B's
+ * backward of the group (vfl_bottom_backward or the tick's vfl_step) then
+ * releases its slot without an update and without waiting for a gradient.
+ * Retraining the group's rows is the caller's: feed them again under a
+ * later group id.  VFL_E_STATE if group is not A's next group or A is inside
+ * a step.  vfl_run refuses to start while a discarded group awaits B's
+ * backward; vfl_get_state likewise. */
+vfl_status vfl_discard(vfl_ctx* c, int64_t group);
+
 /* One tick t of the deterministic schedule: when n_b > 0, B's forward and
  * publish of group t; when n_a > 0, A's forward, top step and backward of
  * group u = t - s, then B's backward of u.  (b: group t's batches, a: group
  * u's batches with labels.)  With this schedule B's forward of group g uses
- * version max(0, g - s) and the update from group u is delayed by min(u, s). */
+ * version max(0, g - s) and the update from group u is delayed by min(u, s).
+ * A group u discarded by vfl_discard skips A's phases; B releases it. */
 vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a,
                     const vfl_batch* b, int32_t n_b, float* loss_dev);
 

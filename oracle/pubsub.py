@@ -228,13 +228,21 @@ class PubSubOracle:
 
     # -------------------------------------------------------------- loop
     def run(self, data: dict, n_groups: int, group_rows, snapshot=None,
-            keep_messages=True, keep_grads=False):
+            keep_messages=True, keep_grads=False, discard=None):
         """Run n_groups batch groups (n_groups + s ticks).
 
         group_rows(g) -> [(start, count)] per replica.  ``snapshot(t)`` says
-        whether to copy the parameters after tick t.  Returns a list of
-        per-tick dicts.
+        whether to copy the parameters after tick t.  ``discard`` maps a
+        group to the channel entry dropped for it (Section 4.2: the buffer
+        mechanism drops the oldest embedding or gradient of a full channel,
+        the waiting deadline a batch whose embedding came too late):
+        "emb" -- A never uses the group's embedding, so neither A nor B
+        updates on it; "grad" -- A takes its step (and publishes the
+        gradient), B drops the gradient and makes no update.  A dropped
+        group leaves B's version where it was.  Returns a list of per-tick
+        dicts.
         """
+        discard = discard or {}
         recs = []
         s = self.s
         for t in range(n_groups + s):
@@ -251,14 +259,16 @@ class PubSubOracle:
             u = t - s
             if 0 <= u < n_groups:
                 bwd = u
-                loss, gm, gA = self.active_step(u, t, data, group_rows(u))
-                gB = self.passive_backward(u, t)
-                rec["loss"] = loss
                 rec["bwd_slot"] = u % (s + 1)
-                if keep_messages:
-                    rec["gtilde"] = gm["g"]
-                rec["grad_header"] = (gm["seq"], gm["tick"], gm["version"])
-                if keep_grads:
+                drop = discard.get(u)
+                if drop != "emb":
+                    loss, gm, gA = self.active_step(u, t, data, group_rows(u))
+                    rec["loss"] = loss
+                    if keep_messages:
+                        rec["gtilde"] = gm["g"]
+                    rec["grad_header"] = (gm["seq"], gm["tick"], gm["version"])
+                gB = self.passive_backward(u, t) if drop is None else {}
+                if keep_grads and drop is None:
                     rec["grads"] = {**gA, **gB}
             rec["fwd_group"], rec["bwd_group"] = fwd, bwd
             self.trace.append((t, fwd, rec.get("fwd_slot", -1), rec.get("fwd_version", -1),

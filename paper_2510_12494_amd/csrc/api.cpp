@@ -212,6 +212,12 @@ struct vfl_ctx {
   int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
   SlotState aslot;
   float* a_loss = nullptr;
+  // discarded groups (Section 4.2's buffer and waiting-deadline
+  // mechanisms), each until B's backward of it releases its slot without
+  // an update; grad: A had consumed the group (B must wait for A's
+  // gradient event before reusing the slot)
+  struct Drop { int64_t group; bool grad; };
+  std::vector<Drop> drops;
   std::vector<int64_t> trace;
   std::string err;
   // resident dataset + captured graphs (one per phase t mod (s+1))
@@ -1190,6 +1196,36 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
   return enqueue_table_sgd(c, p.P, slot, st.rows, c->o.lr / (float)st.rows, c->sb, tr);
 }
 
+// Discard of group g (A will not, or no longer, use it): noted until B's
+// backward of g releases the slot.
+void note_drop(vfl_ctx* c, int64_t g, bool grad) { c->drops.push_back(vfl_ctx::Drop{g, grad}); }
+
+// B's backward of a discarded group: the slot is released, nothing is
+// updated (B's version stays); returns false when g was not discarded.
+bool release_drop(vfl_ctx* c, int64_t g, vfl_status& r) {
+  for (size_t i = 0; i < c->drops.size(); ++i) {
+    if (c->drops[i].group != g) continue;
+    const bool grad = c->drops[i].grad;
+    c->drops.erase(c->drops.begin() + (long)i);
+    r = VFL_OK;
+    if (grad) {
+      // A read the embedding slot: B's next forward into it follows A's
+      // gradient event, as after an ordinary backward
+      const hipError_t e = hipStreamWaitEvent(c->sb, c->ev_grad[g % (c->p.s + 1)], 0);
+      if (e != hipSuccess) r = fail(c, VFL_E_HIP, std::string("hipStreamWaitEvent: ") + hipGetErrorString(e));
+    }
+    c->b_next_bwd = g + 1;
+    return true;
+  }
+  return false;
+}
+
+bool dropped(const vfl_ctx* c, int64_t g) {
+  for (const auto& d : c->drops)
+    if (d.group == g) return true;
+  return false;
+}
+
 // ---- checkpoint / resume: host channel state + the whole workspace
 
 // Fixed header of a state image, followed by the workspace bytes and the
@@ -1399,8 +1435,23 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
   if (party == VFL_PARTY_B) {
     if (group != c->b_next_fwd || c->b_pub_next != group)
       return fail(c, VFL_E_STATE, "B's forward must take the next group after publishing the last");
-    if (group - c->b_next_bwd > p.s)
-      return fail(c, VFL_E_STALE, "more than s+1 groups in flight");
+    if (group - c->b_next_bwd > p.s) {
+      // a full channel: with FIFO discard the oldest group in flight goes
+      // (its embedding if A has not taken it, else its gradient)
+      const int64_t g0 = c->b_next_bwd;
+      if (!(c->o.flags & VFL_FIFO_DISCARD) || group - g0 != p.s + 1 || c->bslot[g0 % (p.s + 1)].group != g0)
+        return fail(c, VFL_E_STALE, "more than s+1 groups in flight");
+      if (!dropped(c, g0)) {
+        if (c->a_next == g0 && c->a_phase != 0)
+          return fail(c, VFL_E_STALE, "the oldest group is inside A's step");
+        const bool consumed = c->a_next > g0;
+        if (!consumed) c->a_next = g0 + 1;
+        note_drop(c, g0, consumed);
+      }
+      vfl_status rr = VFL_OK;
+      (void)release_drop(c, g0, rr);
+      if (rr) return rr;
+    }
     const int slot = (int)(group % (p.s + 1));
     SlotState st;
     vfl_status r = take_batches(c, p.P, br, n, false, st);
@@ -1485,6 +1536,10 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
   if (party == VFL_PARTY_B) {
     if (group != c->b_next_bwd) return fail(c, VFL_E_STATE, "B back-propagates groups in order");
     const int slot = (int)(group % (p.s + 1));
+    if (c->bslot[slot].group == group) {
+      vfl_status rr = VFL_OK;
+      if (release_drop(c, group, rr)) return rr;
+    }
     if (c->grad_group[slot] != group || c->bslot[slot].group != group)
       return fail(c, VFL_E_NOT_READY, "gradient of this group not published");
     vfl_status r = b_backward(c, slot, c->bslot[slot], group, TickRef());
@@ -1495,6 +1550,16 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     return VFL_OK;
   }
   return fail(c, VFL_E_INVALID, "bad party");
+}
+
+vfl_status vfl_discard(vfl_ctx* c, int64_t group) {
+  if (!c) return VFL_E_INVALID;
+  if (group != c->a_next || c->a_phase != 0)
+    return fail(c, VFL_E_STATE, "A discards the next group it would consume, before its forward");
+  if (group < c->b_next_bwd || dropped(c, group)) return fail(c, VFL_E_STATE, "group already released");
+  note_drop(c, group, false);
+  c->a_next = group + 1;
+  return VFL_OK;
 }
 
 vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a, const vfl_batch* b,
@@ -1511,9 +1576,12 @@ vfl_status vfl_step(vfl_ctx* c, int64_t t, const vfl_batch* a, int32_t n_a, cons
   if (n_a > 0) {
     const int64_t u = t - s;
     if (u < 0) return fail(c, VFL_E_STATE, "no group to consume before tick s");
-    if ((r = vfl_bottom_forward(c, VFL_PARTY_A, u, a, n_a))) return r;
-    if ((r = vfl_top_step(c, u, loss_dev))) return r;
-    if ((r = vfl_bottom_backward(c, VFL_PARTY_A, u))) return r;
+    // a group discarded by vfl_discard: no A step, B releases its slot
+    if (!(dropped(c, u) && c->a_next > u)) {
+      if ((r = vfl_bottom_forward(c, VFL_PARTY_A, u, a, n_a))) return r;
+      if ((r = vfl_top_step(c, u, loss_dev))) return r;
+      if ((r = vfl_bottom_backward(c, VFL_PARTY_A, u))) return r;
+    }
     if ((r = vfl_bottom_backward(c, VFL_PARTY_B, u))) return r;
     row[4] = u; row[5] = u % (s + 1); row[6] = c->b_version;
   }
@@ -1563,6 +1631,7 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
   if (t0 < S1 || c->b_next_fwd != t0 || c->b_pub_next != t0 || c->b_next_bwd != t0 - s ||
       c->a_next != t0 - s || c->a_phase != 0)
     return fail(c, VFL_E_STATE, "vfl_run continues a run of ticks 0 .. t0-1 with t0 >= s+1");
+  if (!c->drops.empty()) return fail(c, VFL_E_STATE, "discarded groups in flight: run those ticks with vfl_step");
   if (c->b_copy_version[t0 % S1] != c->b_version || c->a_copy_version != c->a_version)
     return fail(c, VFL_E_STATE, "operand copies not current; run vfl_step first");
   const int cyc = VFL_GRAPH_CYCLES * S1;
@@ -1796,6 +1865,7 @@ vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes) {
   if (!c || !host_buf) return VFL_E_INVALID;
   if (c->a_phase != 0) return fail(c, VFL_E_STATE, "A is inside a group's step (forward or top step pending)");
   if (c->capture_phase >= 0) return fail(c, VFL_E_STATE, "graph capture in progress");
+  if (!c->drops.empty()) return fail(c, VFL_E_STATE, "discarded groups not yet released by B");
   if (bytes < state_bytes(c)) return fail(c, VFL_E_INVALID, "buffer smaller than vfl_state_size()");
   const Plan& p = c->p;
   StateHead h;
@@ -1853,6 +1923,7 @@ vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes) {
   c->a_phase = 0;
   c->aslot = SlotState();
   c->a_loss = nullptr;
+  c->drops.clear();
   for (int q = 0; q < kMaxSlots; ++q) {
     c->b_copy_version[q] = h.b_copy_version[q];
     c->grad_group[q] = h.grad_group[q];

@@ -18,6 +18,7 @@ VFL_F32, VFL_BF16 = 0, 1
 VFL_PARTY_A, VFL_PARTY_B, VFL_TOP = 0, 1, 2
 VFL_PARAM_W, VFL_PARAM_B, VFL_PARAM_TABLE = 0, 1, 2
 VFL_NOISE_EMB, VFL_NOISE_GRAD, VFL_CLIP_EMB, VFL_CLIP_GRAD = 1, 2, 4, 8
+VFL_FIFO_DISCARD = 16
 VFL_MAX_LAYERS = 8
 VFL_GRAPH_CYCLES = 4
 VFL_TIMED_EVERY = 4       # vfl_run times the launches of every 4th tick of a captured cycle
@@ -28,7 +29,8 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
-           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_last_error", "vfl_destroy")
+           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_last_error",
+           "vfl_destroy")
 KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm")
 
 
@@ -93,6 +95,7 @@ def _load():
         "vfl_bind_dataset": [P, C.POINTER(vfl_dataset), C.POINTER(vfl_dataset), I64],
         "vfl_run": [P, I64, I64, P, I64],
         "vfl_state_size": [P, C.POINTER(SZ)],
+        "vfl_discard": [P, I64],
         "vfl_get_state": [P, P, SZ],
         "vfl_set_state": [P, P, SZ],
         "vfl_destroy": [P],
@@ -225,6 +228,10 @@ def vfl_bind_dataset(ctx, a: vfl_dataset, b: vfl_dataset, n_rows: int):
 
 def vfl_run(ctx, t0: int, n: int, loss_ptr: int = 0, loss_len: int = 0):
     _chk(_lib.vfl_run(ctx, t0, n, C.c_void_p(loss_ptr or None), loss_len), "vfl_run", ctx)
+
+
+def vfl_discard(ctx, group: int):
+    _chk(_lib.vfl_discard(ctx, group), "vfl_discard", ctx)
 
 
 def vfl_state_size(ctx) -> int:

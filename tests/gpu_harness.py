@@ -67,7 +67,7 @@ class Run:
     of the epoch, e.g. its ragged tail)."""
 
     def __init__(self, w, n_rows, n_groups, g0=0, data=None, params=None, snap=None,
-                 messages=True):
+                 messages=True, discard=None):
         from paper_2510_12494_amd.session import Session
         from paper_2510_12494_amd import vfl as V
         self.w, self.n_rows, self.n_groups, self.g0 = w, n_rows, n_groups, g0
@@ -78,14 +78,32 @@ class Run:
         shapes = {k: v.shape for k, v in self.p0.items()}
         self.snaps, self.msgs = {}, {}
         s = w.staleness
+        # discard: {group u: kind}; "emb" -- A gives up on u (vfl_discard)
+        # before tick u + s; "emb_fifo" / "grad" -- tick u + s runs B's
+        # forward and publish only / everything but B's backward of u, so
+        # that B's next forward finds s + 2 groups in flight and the FIFO
+        # channel drops u's embedding / gradient
+        self.discard = dict(discard or {})
         try:
             for t in range(n_groups + s):
-                sess.step(t, n_groups)
+                u = t - s
+                kind = self.discard.get(u) if 0 <= u < n_groups else None
+                if kind == "emb":
+                    V.vfl_discard(sess.ctx, u)
+                if kind in ("emb_fifo", "grad"):
+                    if t < n_groups:
+                        V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_B, t, sess.batches("B", t))
+                        V.vfl_publish(sess.ctx, t)
+                    if kind == "grad":
+                        V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_A, u, sess.batches("A", u))
+                        V.vfl_top_step(sess.ctx, u, sess.loss.data_ptr() + 4 * (u % sess.loss.numel()))
+                        V.vfl_bottom_backward(sess.ctx, V.VFL_PARTY_A, u)
+                else:
+                    sess.step(t, n_groups)
                 if messages:
                     if t < n_groups:
                         self.msgs[("e", t)] = sess.message(0, t)
-                    u = t - s
-                    if 0 <= u < n_groups:
+                    if 0 <= u < n_groups and kind not in ("emb", "emb_fifo"):
                         self.msgs[("g", u)] = sess.message(1, u)
                 if snap is None or snap(t):
                     self.snaps[t] = sess.params(shapes)
@@ -98,6 +116,7 @@ class Run:
 
     def oracle(self, precision, snap=None):
         o = PubSubOracle(self.w, self.p0, precision)
+        drop = {u: ("grad" if k == "grad" else "emb") for u, k in self.discard.items()}
         recs = o.run(self.data, self.n_groups, self.rows_of,
-                     snapshot=(lambda t: True) if snap is None else snap)
+                     snapshot=(lambda t: True) if snap is None else snap, discard=drop)
         return o, recs

@@ -122,3 +122,49 @@ def test_deterministic_and_overlap_independent(name):
             s.close()
     for k in outs[0]:
         assert np.array_equal(outs[0][k], outs[1][k]), k
+
+
+def test_discard_protocol():
+    """vfl_discard takes only A's next group, between A's steps; without
+    VFL_FIFO_DISCARD a full channel stays VFL_E_STALE; graph replay and
+    state images wait until B has released a discarded group."""
+    from paper_2510_12494_amd import vfl as V
+    w, sess, p = _session(groups=8)
+    s = w.staleness
+    try:
+        for t in range(s + 1):
+            sess.step(t, 8)
+        u = 1                                   # A's next group
+        for bad in (u + 1, u - 1):
+            with pytest.raises(V.VflError) as e:
+                V.vfl_discard(sess.ctx, bad)
+            assert e.value.status == V.VFL_E_STATE
+        V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_A, u, sess.batches("A", u))
+        with pytest.raises(V.VflError) as e:
+            V.vfl_discard(sess.ctx, u)              # A inside its step
+        assert e.value.status == V.VFL_E_STATE
+        V.vfl_top_step(sess.ctx, u, 0)
+        V.vfl_bottom_backward(sess.ctx, V.VFL_PARTY_A, u)
+        V.vfl_bottom_backward(sess.ctx, V.VFL_PARTY_B, u)
+        V.vfl_discard(sess.ctx, u + 1)          # the deadline path
+        sess.bind()
+        with pytest.raises(V.VflError) as e:
+            sess.run(s + 1, 12)
+        assert e.value.status == V.VFL_E_STATE
+        with pytest.raises(V.VflError) as e:
+            V.vfl_get_state(sess.ctx)
+        assert e.value.status == V.VFL_E_STATE
+        # B: forward and publish s + 1 groups ahead, then one more: stale
+        for g in range(s + 1, 2 * s + 3):
+            if g <= u + 1 + s:
+                V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_B, g, sess.batches("B", g))
+                V.vfl_publish(sess.ctx, g)
+        g = u + 2 + s
+        with pytest.raises(V.VflError) as e:
+            V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_B, g, sess.batches("B", g))
+        assert e.value.status == V.VFL_E_STALE
+        # B's backward releases the discarded group, then the forward goes on
+        V.vfl_bottom_backward(sess.ctx, V.VFL_PARTY_B, u + 1)
+        V.vfl_bottom_forward(sess.ctx, V.VFL_PARTY_B, g, sess.batches("B", g))
+    finally:
+        sess.close()

@@ -261,3 +261,41 @@ def test_shared_lds_buffers_deep_top():
     _check_losses(run, recs, 1e-3)
     _check_messages(run, recs, w)
     _check_params(run, recs, w, per_tick=True)
+
+
+@pytest.mark.parametrize("dtype,s,discard", [
+    ("bf16", 2, {1: "emb", 3: "grad", 5: "emb_fifo"}),
+    ("f32", 1, {0: "grad", 3: "emb", 5: "emb_fifo"}),
+])
+def test_channel_discards(dtype, s, discard):
+    """The buffer and waiting-deadline mechanisms (Section 4.2): groups whose
+    embedding is dropped (A gives up on the group, or a full FIFO channel
+    drops it before A takes it) and groups whose gradient is dropped (a full
+    channel after A's step).  Per-tick parameters, the losses of the groups
+    A stepped on and every message against the oracle run with the same
+    drops; a dropped group never advances B's version (checked through the
+    parameters and the slot headers of later forwards)."""
+    tables = dtype == "f32"
+    w = Workload(name="drops", n_rows=9 * 600, dtype=dtype,
+                 A=PartySpec(dense=24, n_cat=2 if tables else 0, vocab=50, emb_dim=8, widths=[32, 16]),
+                 B=PartySpec(dense=16, widths=[24, 16]), top=TopSpec(widths=[20, 1]),
+                 batch=300, staleness=s, replicas=2, lr=0.5, clip=1.0, sigma=0.5, clip_emb=True,
+                 clip_grad=True, noise_emb=True, noise_grad=True, fifo_discard=True,
+                 labels="teacher", data_seed=91, init_seed=92, noise_seed=93)
+    n_groups = 9
+    run = H.Run(w, w.n_rows, n_groups, discard=discard)
+    o, recs = run.oracle(_prec(w))
+    assert run.mismatches == 0
+    for r in recs:
+        if "emb_header" in r:
+            assert run.msgs[("e", r["fwd_group"])][1] == r["emb_header"]
+        if "grad_header" in r:
+            assert run.msgs[("g", r["bwd_group"])][1] == r["grad_header"]
+    stepped = [r["bwd_group"] for r in recs if "loss" in r]
+    assert sorted(set(range(n_groups)) - set(stepped)) == sorted(
+        u for u, k in discard.items() if k in ("emb", "emb_fifo"))
+    ref = np.array([r["loss"] for r in recs if "loss" in r])
+    got = np.array([run.losses[u] for u in stepped])
+    np.testing.assert_allclose(got, ref, rtol=1e-3 if dtype == "bf16" else 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)

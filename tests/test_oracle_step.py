@@ -137,6 +137,38 @@ def test_equals_history_formulation(s, k):
         assert _relerr(o.p[key] - d0, v - d0) < 1e-10, key
 
 
+@pytest.mark.parametrize("s,discard", [(0, {1: "emb", 3: "grad"}),
+                                       (2, {0: "grad", 2: "emb", 3: "emb", 6: "grad"})])
+def test_discards_equal_history_formulation(s, discard):
+    """Dropped embeddings and gradients (Section 4.2): the oracle's ring,
+    stash and version counter against the history formulation, where B's
+    forward of group u takes the version counted from the groups applied
+    before it; with clip, noise and tables."""
+    w = _mk(A=PartySpec(dense=3, n_cat=2, vocab=7, emb_dim=2, widths=[6, 3]),
+            B=PartySpec(dense=4, n_cat=1, vocab=5, emb_dim=3, widths=[5, 4]),
+            top=TopSpec(widths=[5, 1]), staleness=s, replicas=2, batch=6,
+            n_rows=12 * 8, lr=0.5, clip=0.7, sigma=0.3, clip_emb=True,
+            clip_grad=True, noise_emb=True, noise_grad=True, zipf_a=0.8)
+    n_groups = 8
+    o, recs, d, p = _run(w, n_groups, discard=discard)
+    losses, final = run_history(w, p, d, n_groups, lambda g: S.group_rows(w, g), discard=discard)
+    got = [r["loss"] for r in recs if "loss" in r]
+    np.testing.assert_allclose(got, losses, rtol=1e-13)
+    for key, v in final.items():
+        assert _relerr(o.p[key], v) < 1e-12, key
+    # B's version: one step per group it did not drop; A skipped the
+    # dropped embeddings only
+    assert o.vB == n_groups - len(discard)
+    assert len(got) == n_groups - sum(1 for k in discard.values() if k == "emb")
+    # a dropped group leaves B untouched over its tick, and a dropped
+    # embedding leaves A untouched too
+    vb = [r for r in o.trace if r[4] >= 0]
+    for row in vb:
+        u = row[4]
+        applied = sum(1 for g in range(u + 1) if g not in discard)
+        assert row[6] == applied, row
+
+
 def test_synchronous_equals_centralized_sgd():
     """s = 0, k = 1, no clip or noise: one tick is one SGD step of the
     centralized network g([f_A(x_A) | f_B(x_B)]) on the batch mean BCE."""

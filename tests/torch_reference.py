@@ -11,6 +11,11 @@ message is the per-row gradient w.r.t. the published embedding, optionally
 clipped and noised; B's gradient is the vector-Jacobian product of its
 embedding at the delayed version with that message / R; every party takes
 one SGD step (Eq. 2).
+
+Dropped channel entries (Section 4.2): for a group whose embedding is
+dropped nothing is computed; for one whose gradient is dropped A and the top
+model step and B does not.  B's version for the forward of group u is then
+the number of B updates applied by the groups g < u - s.
 """
 import numpy as np
 import torch
@@ -43,8 +48,10 @@ def _clip(v, C):
     return v * c
 
 
-def run_history(w, params, data, n_groups, rows_of):
-    """Returns (losses per group, final parameters as float64 numpy dict)."""
+def run_history(w, params, data, n_groups, rows_of, discard=None):
+    """Returns (losses per group that A stepped on, final parameters as a
+    float64 numpy dict); discard: {group: "emb" | "grad"}."""
+    discard = discard or {}
     s = w.staleness
     std = w.sigma * (w.clip if w.clip > 0 else 1.0)
     cur = {k: _t(v) for k, v in params.items()}
@@ -52,9 +59,12 @@ def run_history(w, params, data, n_groups, rows_of):
     versions = [{k: cur[k].clone() for k in b_keys}]
     losses = []
     for u in range(n_groups):
+        if discard.get(u) == "emb":
+            continue
         rows = np.concatenate([np.arange(a, a + c) for a, c in rows_of(u)])
         R = len(rows)
-        PB = {k: versions[max(0, u - s)][k].clone().requires_grad_(True) for k in b_keys}
+        v_fwd = sum(1 for g in range(max(0, u - s)) if g not in discard)
+        PB = {k: versions[v_fwd][k].clone().requires_grad_(True) for k in b_keys}
         PA = {k: v.clone().requires_grad_(True) for k, v in cur.items() if not k.startswith("B.")}
         xb = data["xb"][rows] if data["xb"] is not None else None
         idb = data["idb"][rows] if data["idb"] is not None else None
@@ -86,6 +96,9 @@ def run_history(w, params, data, n_groups, rows_of):
         with torch.no_grad():
             for k, g in zip(names, grads[:-1]):
                 cur[k] = cur[k] - w.lr * g
+            if discard.get(u) == "grad":
+                losses.append(float(loss.detach()))
+                continue
             nv = {}
             for k, g in zip(b_keys, gB):
                 nv[k] = versions[-1][k] - w.lr * (g if g is not None else 0.0)

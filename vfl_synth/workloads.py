@@ -81,6 +81,7 @@ class Workload:
     noise_grad: bool = False
     clip_emb: bool = False
     clip_grad: bool = False
+    fifo_discard: bool = False   # a full channel drops its oldest group
     labels: str = "teacher"  # "logistic" | "teacher" | "bernoulli"
     label_p: float = 0.25
     zipf_a: float = 1.1
