@@ -126,7 +126,8 @@ def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int
 
 def cpu_baseline(w, data, params, seconds: float) -> dict:
     """The oracle (float64 numpy) on this host over the same resident dataset,
-    for about ``seconds`` of CPU work: one probe group sizes the sample."""
+    for about ``seconds`` of CPU work: a probe run sizes the sample, and a
+    sample that ends well short of ``seconds`` is run again, longer."""
     import vfl_synth as S
     from oracle import PubSubOracle
     try:
@@ -136,17 +137,19 @@ def cpu_baseline(w, data, params, seconds: float) -> dict:
         threads = len(os.sched_getaffinity(0))
     R = w.rows_per_tick
     rows_of = lambda g: S.group_rows(w, g)
-    # size the sample from a 4-group run after a 1-group warm-up (one group
-    # alone is dominated by set-up and the s-tick lead-in)
+    # size the sample from a 16-group run after a 1-group warm-up (a few
+    # groups are dominated by set-up and the s-tick lead-in); a run under
+    # half of the target is repeated with the groups scaled to the target
     PubSubOracle(w, params, "f64").run(data, 1, rows_of, keep_messages=False)
-    t0 = time.perf_counter()
-    PubSubOracle(w, params, "f64").run(data, 4, rows_of, keep_messages=False)
-    per_group = (time.perf_counter() - t0) / 4
-    groups = int(max(1, min(4096, seconds / max(per_group, 1e-6))))
-    o = PubSubOracle(w, params, "f64")
-    t0 = time.perf_counter()
-    o.run(data, groups, rows_of, keep_messages=False)
-    dt = time.perf_counter() - t0
+    groups, dt = 16, 0.0
+    for _ in range(3):
+        o = PubSubOracle(w, params, "f64")
+        t0 = time.perf_counter()
+        o.run(data, groups, rows_of, keep_messages=False)
+        dt = time.perf_counter() - t0
+        if dt >= 0.5 * seconds or groups >= 8192:
+            break
+        groups = int(max(groups + 1, min(8192, groups * seconds / max(dt, 1e-6))))
     return {"value": groups * R / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {groups} batch groups of {R} rows of the same dataset "
                       f"({groups + w.staleness} ticks incl. the s={w.staleness} lead-in), "
