@@ -299,3 +299,29 @@ def test_channel_discards(dtype, s, discard):
     np.testing.assert_allclose(got, ref, rtol=1e-3 if dtype == "bf16" else 1e-4)
     _check_messages(run, recs, w)
     _check_params(run, recs, w, per_tick=True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_limits_of_the_interface(dtype):
+    """The largest staleness (s = 4: five channel slots) and replica count
+    (k = 8), B's bottom at the 8-layer limit, A's bottom and the top's hidden
+    layers at the 8-problem limit of one weight-gradient launch (3 + 5),
+    linear layers mixed with ReLU ones (the masks of the input-gradient
+    chains skip them), the largest embedding width (16) and a ragged last
+    group of 3 rows."""
+    w = Workload(name="limits", n_rows=9 * 400 + 3, dtype=dtype,
+                 A=PartySpec(dense=11, n_cat=2, vocab=29, emb_dim=16, widths=[36, 20, 16],
+                             relu=[True, False, True]),
+                 B=PartySpec(dense=9, widths=[24, 18, 30, 12, 26, 16, 20, 10],
+                             relu=[True, True, False, True, True, False, True, True]),
+                 top=TopSpec(widths=[28, 14, 22, 9, 17, 1], relu=[True, False, True, True, False]),
+                 batch=50, staleness=4, replicas=8, lr=0.3, clip=1.0, sigma=0.5,
+                 clip_emb=True, clip_grad=True, noise_emb=True, noise_grad=True,
+                 labels="bernoulli", label_p=0.45, data_seed=101, init_seed=102, noise_seed=103)
+    n_groups = (w.n_rows + w.rows_per_tick - 1) // w.rows_per_tick
+    run = H.Run(w, w.n_rows, n_groups)
+    o, recs = run.oracle(_prec(w))
+    _check_ints(run, o, recs)
+    _check_losses(run, recs, 1e-3 if dtype == "bf16" else 1e-4)
+    _check_messages(run, recs, w)
+    _check_params(run, recs, w, per_tick=True)
