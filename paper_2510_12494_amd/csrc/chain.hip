@@ -775,12 +775,14 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     for (int o = 32; o > 0; o >>= 1)
 #pragma unroll
       for (int rr = 0; rr < RW; ++rr) dots[rr] += __shfl_xor(dots[rr], o, 64);
+    // the loss terms and dl of every row first: their exp / reciprocal /
+    // log chains are independent, while the stage below alternates LDS
+    // reads and writes the compiler must keep in order (they may alias)
+    float dls[RW];
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
       const int r = wave * RW + rr;
       const bool ok = r < rv;
-      float h[kLogitChunks][4];
-      load_h(r, h);
       const float l = dots[rr] + lbias;
       const float yy = yl[r];
       const float ex = __expf(-fabsf(l));
@@ -789,6 +791,14 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
       const float dl = ok ? sig - yy : 0.f;
       if (ok) lsum += fmaxf(l, 0.f) - yy * l + __logf(1.f + ex);
       dsum += dl;
+      dls[rr] = dl;
+    }
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      const int r = wave * RW + rr;
+      const float dl = dls[rr];
+      float h[kLogitChunks][4];
+      load_h(r, h);
 #pragma unroll
       for (int i = 0; i < kLogitChunks; ++i) {
         const int c0 = 256 * i + 4 * lane;
