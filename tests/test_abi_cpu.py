@@ -139,3 +139,20 @@ def test_host_plan_covers_random_shapes(V, dtype):
             assert "exceed the LDS" in str(e), (w, str(e))
             continue
         assert n > 0
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: importing the binding where libvfl.so is missing raises
+    (checked in a child interpreter on a copy of the package without the
+    library)."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = os.path.join(ROOT, "paper_2510_12494_amd")
+    dst = tmp_path / "paper_2510_12494_amd"
+    shutil.copytree(pkg, dst, ignore=shutil.ignore_patterns("*.so", "*.so.tmp", "__pycache__", "csrc"))
+    assert not list(dst.glob("*.so"))
+    code = "import paper_2510_12494_amd.vfl"
+    r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "no fallback" in r.stderr
