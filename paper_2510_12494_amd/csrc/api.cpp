@@ -1435,27 +1435,30 @@ vfl_status vfl_bottom_forward(vfl_ctx* c, vfl_party party, int64_t group, const 
   if (party == VFL_PARTY_B) {
     if (group != c->b_next_fwd || c->b_pub_next != group)
       return fail(c, VFL_E_STATE, "B's forward must take the next group after publishing the last");
-    if (group - c->b_next_bwd > p.s) {
-      // a full channel: with FIFO discard the oldest group in flight goes
-      // (its embedding if A has not taken it, else its gradient)
-      const int64_t g0 = c->b_next_bwd;
+    // a full channel: with FIFO discard the oldest group in flight goes
+    // (its embedding if A has not taken it, else its gradient), once the
+    // call is known to be valid
+    const int64_t g0 = c->b_next_bwd;
+    const bool full = group - g0 > p.s;
+    if (full) {
       if (!(c->o.flags & VFL_FIFO_DISCARD) || group - g0 != p.s + 1 || c->bslot[g0 % (p.s + 1)].group != g0)
         return fail(c, VFL_E_STALE, "more than s+1 groups in flight");
-      if (!dropped(c, g0)) {
-        if (c->a_next == g0 && c->a_phase != 0)
-          return fail(c, VFL_E_STALE, "the oldest group is inside A's step");
-        const bool consumed = c->a_next > g0;
-        if (!consumed) c->a_next = g0 + 1;
-        note_drop(c, g0, consumed);
-      }
-      vfl_status rr = VFL_OK;
-      (void)release_drop(c, g0, rr);
-      if (rr) return rr;
+      if (!dropped(c, g0) && c->a_next == g0 && c->a_phase != 0)
+        return fail(c, VFL_E_STALE, "the oldest group is inside A's step");
     }
     const int slot = (int)(group % (p.s + 1));
     SlotState st;
     vfl_status r = take_batches(c, p.P, br, n, false, st);
     if (r) return r;
+    if (full) {
+      if (!dropped(c, g0)) {
+        const bool consumed = c->a_next > g0;
+        if (!consumed) c->a_next = g0 + 1;
+        note_drop(c, g0, consumed);
+      }
+      (void)release_drop(c, g0, r);
+      if (r) return r;
+    }
     st.group = group;
     st.version = c->b_version;
     st.published = false;
