@@ -287,6 +287,37 @@ vfl_status vfl_state_size(const vfl_ctx* c, size_t* bytes);
 vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes);
 vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes);
 
+/* Planner of the system-planning phase (Section 4.4, Algorithm 2; host
+ * only, no context).  A party's profile: per-iteration forward and backward
+ * delays T = coef * B^exp * w / C of its bottom (Eqs. 7-8) and, for party A,
+ * of the top model (Eq. 9; zero coefficients for party B), its total cores
+ * C, its candidate worker counts [w_min, w_max] and its memory model
+ * M(B) = mem_base + mem_coef * B^chi per worker against mem_cap
+ * (mem_coef <= 0: no memory bound). */
+typedef struct {
+  double lambda, gamma, phi, beta;
+  double lambda_top, gamma_top, phi_top, beta_top;
+  double cores;
+  int32_t w_min, w_max;
+  double mem_base, mem_coef, mem_cap;
+} vfl_plan_party;
+
+/* The exchange: embedding and gradient bytes per batch row (E and G of a
+ * batch of B rows are B times these), the bandwidth B_b in bytes per
+ * second, and the memory exponent chi. */
+typedef struct {
+  double emb_bytes_per_row, grad_bytes_per_row, bandwidth, chi;
+} vfl_plan_link;
+
+/* The (w_a, w_p, B) that minimises max(T_A, T_P) + (E + G) / B_b over the
+ * candidate batch sizes batches[0 .. n_batches) that both memory models
+ * allow and every worker count in the two ranges (Algorithm 2's
+ * enumeration; ties keep the first in batch, w_a, w_p order).  out =
+ * {w_a, w_p, B}; *cost (may be NULL) the minimum.  VFL_E_INVALID for bad
+ * profiles or when no candidate is feasible. */
+vfl_status vfl_plan(const vfl_plan_party* a, const vfl_plan_party* p, const vfl_plan_link* link,
+                    const int32_t* batches, int32_t n_batches, int32_t out[3], double* cost);
+
 /* Synchronise both streams and report the device-side channel checks: the
  * number of times a consumer found a slot header whose group differs from
  * the one it expected (0 when the channel is race-free). */

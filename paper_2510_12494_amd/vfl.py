@@ -29,9 +29,22 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
-           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_last_error",
-           "vfl_destroy")
+           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan",
+           "vfl_last_error", "vfl_destroy")
 KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm")
+
+
+class vfl_plan_party(C.Structure):
+    _fields_ = [("lambda_", C.c_double), ("gamma", C.c_double), ("phi", C.c_double),
+                ("beta", C.c_double), ("lambda_top", C.c_double), ("gamma_top", C.c_double),
+                ("phi_top", C.c_double), ("beta_top", C.c_double), ("cores", C.c_double),
+                ("w_min", C.c_int32), ("w_max", C.c_int32), ("mem_base", C.c_double),
+                ("mem_coef", C.c_double), ("mem_cap", C.c_double)]
+
+
+class vfl_plan_link(C.Structure):
+    _fields_ = [("emb_bytes_per_row", C.c_double), ("grad_bytes_per_row", C.c_double),
+                ("bandwidth", C.c_double), ("chi", C.c_double)]
 
 
 class vfl_bottom_spec(C.Structure):
@@ -96,6 +109,8 @@ def _load():
         "vfl_run": [P, I64, I64, P, I64],
         "vfl_state_size": [P, C.POINTER(SZ)],
         "vfl_discard": [P, I64],
+        "vfl_plan": [C.POINTER(vfl_plan_party), C.POINTER(vfl_plan_party), C.POINTER(vfl_plan_link),
+                     C.POINTER(I32), I32, C.POINTER(I32), C.POINTER(C.c_double)],
         "vfl_get_state": [P, P, SZ],
         "vfl_set_state": [P, P, SZ],
         "vfl_destroy": [P],
@@ -228,6 +243,16 @@ def vfl_bind_dataset(ctx, a: vfl_dataset, b: vfl_dataset, n_rows: int):
 
 def vfl_run(ctx, t0: int, n: int, loss_ptr: int = 0, loss_len: int = 0):
     _chk(_lib.vfl_run(ctx, t0, n, C.c_void_p(loss_ptr or None), loss_len), "vfl_run", ctx)
+
+
+def vfl_plan(a: vfl_plan_party, p: vfl_plan_party, link: vfl_plan_link, batches):
+    """Returns ((w_a, w_p, B), cost)."""
+    arr = (C.c_int32 * len(batches))(*batches)
+    out = (C.c_int32 * 3)()
+    cost = C.c_double(0.0)
+    _chk(_lib.vfl_plan(C.byref(a), C.byref(p), C.byref(link), arr, len(batches), out, C.byref(cost)),
+         "vfl_plan")
+    return (out[0], out[1], out[2]), cost.value
 
 
 def vfl_discard(ctx, group: int):
