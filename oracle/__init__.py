@@ -21,5 +21,5 @@ Parity status: every function here is pinned by a CPU test in ``tests/``
 noise multiplier to a privacy budget, which the paper gives only up to an
 unspecified constant (Eq. 25): parity unpinned, and not implemented.
 """
-from .pubsub import PubSubOracle  # noqa: F401
+from .pubsub import PubSubOracle, ROUNDING_POINTS  # noqa: F401
 from . import layers, philox, rounding, schedule  # noqa: F401

@@ -26,10 +26,32 @@ Appendix) on a deterministic tick schedule (``oracle/schedule.py``):
 
 Readings of points the paper leaves open are listed where they are used.
 Precision: ``precision='f64'`` computes everything in float64.  ``'bf16'`` and
-``'f32'`` additionally round to that storage type exactly where the GPU path
-stores a value (inputs to every matrix product, layer outputs, exchanged
-messages, back-propagated deltas) and keep float32 master parameters; the
-arithmetic in between stays float64.
+``'f32'`` additionally round to that storage type at the points named in
+``ROUNDING_POINTS`` and keep float32 master parameters; the arithmetic in
+between stays float64.  The points are where the values a later product or
+the other party reads are stored:
+
+  input         a bottom model's input row (dense features and the looked-up
+                embedding rows);
+  weight        the weight operand of every bottom and hidden top layer
+                (the float32 master, rounded); the logit layer reads its
+                float32 master weight unrounded;
+  act.bottom    every bottom layer's output;
+  act.top       every hidden top layer's output;
+  delta.bottom  the gradient at the pre-activation of bottom layers below the
+                cut layer;
+  delta.top     the gradient at the pre-activation of hidden top layers;
+  delta.cut_a   the gradient at A's cut-layer pre-activation;
+  delta.cut_b   the gradient at B's cut-layer pre-activation (after the clip
+                Jacobian);
+  msg.emb       the published embedding when it is clipped or noised (else
+                the cut layer's stored output is the message);
+  msg.grad      the returned gradient message;
+  master        the float32 master parameters after every update.
+
+Deltas are gradients of the *sum* of the per-row losses of a group (the 1/R
+of the mean loss is applied in the SGD step), so their rounding does not
+depend on the group's size.  ``points`` selects a subset (default: all).
 """
 from __future__ import annotations
 
@@ -39,18 +61,23 @@ from . import layers as L
 from .philox import gaussian, TAG_EMB, TAG_GRAD
 from .rounding import ROUNDERS, round_f32, identity
 
+ROUNDING_POINTS = ("input", "weight", "act.bottom", "act.top", "delta.bottom", "delta.top",
+                   "delta.cut_a", "delta.cut_b", "msg.emb", "msg.grad", "master")
+
 
 class PubSubOracle:
     """State: float64 master parameters of A, B and the top model; ring of
     s + 1 embedding and gradient slots with headers; B's weight stash and
     activation cache per slot; B's update count (its parameter version)."""
 
-    def __init__(self, w, params: dict, precision: str = "f64"):
+    def __init__(self, w, params: dict, precision: str = "f64", points=None):
         self.w = w
         self.s = int(w.staleness)
         self.prec = precision
         self.rnd = ROUNDERS[precision]
-        self.rnd_master = identity if precision == "f64" else round_f32
+        self.points = frozenset(ROUNDING_POINTS if points is None else points)
+        assert self.points <= set(ROUNDING_POINTS), self.points
+        self.rnd_master = identity if precision == "f64" or "master" not in self.points else round_f32
         self.p = {k: np.asarray(v, dtype=np.float64).copy() for k, v in params.items()}
         self.nA, self.nB = len(w.A.widths), len(w.B.widths)
         self.nT = len(w.top.widths)
@@ -62,10 +89,19 @@ class PubSubOracle:
         self.noise_std = w.sigma * (w.clip if w.clip > 0 else 1.0)
 
     # ----------------------------------------------------------- helpers
+    def _q(self, point: str, x):
+        """Storage rounding at a named point (identity when the point is off
+        or the precision is float64)."""
+        return self.rnd(x) if point in self.points else identity(x)
+
     def _weights(self, party: str, n: int):
         """Matrix-product operands: the current master weights rounded to the
         storage type (bf16 copies on the GPU)."""
-        return [self.rnd(self.p[f"{party}.W{l}"]) for l in range(n)]
+        return [self._q("weight", self.p[f"{party}.W{l}"]) for l in range(n)]
+
+    def _logit_weight(self):
+        """The logit layer's weight row: its float32 master, unrounded."""
+        return self.p[f"top.W{self.nT - 1}"][0]
 
     def _bottom_input(self, party: str, spec, data: dict, rows: np.ndarray):
         xs = []
@@ -76,14 +112,14 @@ class PubSubOracle:
         if spec.dense:
             xs.append(data["xa" if party == "A" else "xb"][rows].astype(np.float64))
         x = np.concatenate(xs, axis=1) if len(xs) > 1 else xs[0]
-        return self.rnd(x), ids
+        return self._q("input", x), ids
 
     def _bottom_forward(self, spec, Wq, bias, x):
         acts = [x]
         a = x
         for l in range(len(Wq)):
             p = L.linear(a, Wq[l], bias[l])
-            a = self.rnd(L.relu(p) if spec.relu[l] else p)
+            a = self._q("act.bottom", L.relu(p) if spec.relu[l] else p)
             acts.append(a)
         return acts
 
@@ -98,7 +134,7 @@ class PubSubOracle:
             if l > 0:
                 gin = delta @ Wq[l]
                 m = L.relu_mask(acts[l]) if spec.relu[l - 1] else 1.0
-                delta = self.rnd(gin * m)
+                delta = self._q("delta.bottom", gin * m)
             elif spec.n_cat:
                 gx = delta @ Wq[0]
                 ne = spec.n_cat * spec.emb_dim
@@ -136,7 +172,7 @@ class PubSubOracle:
                 v, n, c = z, None, None
             if w.noise_emb:
                 v = v + self.noise_std * gaussian(w.noise_seed, g, rows, z.shape[1], TAG_EMB)
-            zhat = self.rnd(v) if (w.clip_emb or w.noise_emb) else z
+            zhat = self._q("msg.emb", v) if (w.clip_emb or w.noise_emb) else z
             parts.append(dict(rows=rows, ids=ids, acts=acts, n=n, c=c, zhat=zhat))
         self.S[slot] = dict(group=g, version=self.vB, Wq=Wq, parts=parts)
         self.E[slot] = dict(seq=g, tick=t, version=self.vB,
@@ -154,7 +190,7 @@ class PubSubOracle:
         bA = [self.p[f"A.b{l}"] for l in range(self.nA)]
         WqT = self._weights("top", self.nT - 1)
         bT = [self.p[f"top.b{l}"] for l in range(self.nT - 1)]
-        w_out = self.p[f"top.W{self.nT - 1}"][0]          # logit weights, float
+        w_out = self._logit_weight()
         b_out = self.p[f"top.b{self.nT - 1}"][0]
         dA = w.A.d_out
         grads = {}
@@ -170,7 +206,7 @@ class PubSubOracle:
             h = [np.concatenate([acts[-1], zb], axis=1)]
             for j in range(self.nT - 1):
                 p = L.linear(h[-1], WqT[j], bT[j])
-                h.append(self.rnd(L.relu(p) if w.top.relu[j] else p))
+                h.append(self._q("act.top", L.relu(p) if w.top.relu[j] else p))
             logit = h[-1] @ w_out + b_out
             y = data["y"][rows].astype(np.float64)
             loss_sum += L.bce_with_logits(logit, y).sum()
@@ -180,13 +216,13 @@ class PubSubOracle:
             gin = dl[:, None] * w_out[None, :]
             for j in range(self.nT - 2, -1, -1):
                 m = L.relu_mask(h[j + 1]) if w.top.relu[j] else 1.0
-                delta = self.rnd(gin * m)
+                delta = self._q("delta.top", gin * m)
                 g[f"top.W{j}"] = delta.T @ h[j]
                 g[f"top.b{j}"] = delta.sum(axis=0)
                 gin = delta @ WqT[j]
             gA, GB = gin[:, :dA], gin[:, dA:]
             mA = L.relu_mask(acts[-1]) if w.A.relu[-1] else 1.0
-            self._add(g, self._bottom_backward(w.A, WqA, acts, self.rnd(gA * mA), ids, "A"))
+            self._add(g, self._bottom_backward(w.A, WqA, acts, self._q("delta.cut_a", gA * mA), ids, "A"))
             self._add(grads, g)
             # gradient message: per-row gradient w.r.t. the published
             # embedding (no 1/R), optionally clipped and noised
@@ -196,7 +232,7 @@ class PubSubOracle:
                 v = GB
             if w.noise_grad:
                 v = v + self.noise_std * gaussian(w.noise_seed, u, rows, v.shape[1], TAG_GRAD)
-            msgs.append(self.rnd(v))
+            msgs.append(self._q("msg.grad", v))
         R = sum(c for _, c in replicas)
         self._sgd(grads, R)
         self.G[slot] = dict(seq=u, tick=t, version=ent["version"], g=np.concatenate(msgs))
@@ -220,7 +256,7 @@ class PubSubOracle:
             if w.clip_emb:
                 dz = L.clip_rows_backward(dz, z, q["n"], q["c"], w.clip)
             m = L.relu_mask(z) if w.B.relu[-1] else 1.0
-            delta = self.rnd(dz * m)
+            delta = self._q("delta.cut_b", dz * m)
             self._add(grads, self._bottom_backward(w.B, st["Wq"], q["acts"], delta, q["ids"], "B"))
         self._sgd(grads, R)
         self.vB += 1
