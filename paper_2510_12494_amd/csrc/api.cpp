@@ -1635,6 +1635,12 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
       c->a_next != t0 - s || c->a_phase != 0)
     return fail(c, VFL_E_STATE, "vfl_run continues a run of ticks 0 .. t0-1 with t0 >= s+1");
   if (!c->drops.empty()) return fail(c, VFL_E_STATE, "discarded groups in flight: run those ticks with vfl_step");
+  // the replays derive B's version for group g as max(0, g - s - vofs); the
+  // groups in flight must already follow that (s + 1 ticks after a drop)
+  const int64_t vofs = (t0 - s) - c->b_version;
+  for (int64_t g = t0 - s; g < t0; ++g)
+    if (c->bslot[g % S1].group != g || c->bslot[g % S1].version != std::max<int64_t>(0, g - s - vofs))
+      return fail(c, VFL_E_STATE, "groups in flight predate a discard: run s+1 ticks with vfl_step first");
   if (c->b_copy_version[t0 % S1] != c->b_version || c->a_copy_version != c->a_version)
     return fail(c, VFL_E_STATE, "operand copies not current; run vfl_step first");
   const int cyc = VFL_GRAPH_CYCLES * S1;
@@ -1718,6 +1724,7 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
     // the replays start at tick t0 (the dataset and schedule constants with it)
     TickSrc src;
     src.base = t0; src.n_rows = c->n_rows; src.R = p.R; src.s = s; src.lr = c->o.lr;
+    src.vofs = (int32_t)vofs;
     src.loss_len = loss_ring ? loss_len : 1;
     HIPCHK(hipMemcpyAsync(at<TickSrc>(c, p.tsrc), &src, sizeof(src), hipMemcpyHostToDevice, c->sa));
     // the graph runs both parties' work from stream A: it must follow the

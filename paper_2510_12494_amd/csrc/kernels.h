@@ -60,13 +60,15 @@ struct TickArgs {
 // the first tick of the current replay (written before the first replay,
 // advanced by the graph's last node).  role 0: party B publishes group t;
 // role 1: party A consumes group u = t - s; role 2: party B back-propagates
-// u.  A null src means the launch's values are given directly.
+// u.  A null src means the launch's values are given directly.  B's forward
+// of group g used version max(0, g - s - vofs): vofs counts the groups
+// dropped before the replays (each leaves B's version one step behind).
 struct TickSrc {
   int64_t base = 0;
   int64_t n_rows = 0;
   int32_t R = 0, s = 0;
   float lr = 0.f;
-  int32_t pad = 0;
+  int32_t vofs = 0;
   int64_t loss_len = 1;
 };
 struct TickRef {
@@ -89,7 +91,7 @@ __device__ __forceinline__ TickArgs tick_args(const TickRef& r) {
   a.loss_idx = g % x.loss_len;
   a.hdr[0] = (int32_t)g;
   a.hdr[1] = (int32_t)t;
-  a.hdr[2] = (int32_t)(g - x.s > 0 ? g - x.s : 0);
+  a.hdr[2] = (int32_t)(g - x.s - x.vofs > 0 ? g - x.s - x.vofs : 0);
   return a;
 }
 
