@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 PEAK = {"bf16": 2.5e15, "f32": 157.3e12}     # dense MFMA FLOP/s (MI355X spec)
 HBM_PEAK = 8.0e12                            # bytes/s
 METRIC = "training samples/sec (both parties fwd+bwd+update) on 1 MI355X; MFMA util %"
-GEMM_CLASSES = ("fwd", "active", "bwd", "dw", "gemm")
+GEMM_CLASSES = ("fwd", "active", "bwd", "dw", "gemm", "dwt")
 
 
 def gemm_flops_per_tick(w) -> float:
@@ -58,7 +58,8 @@ CSRC = "paper_2510_12494_amd/csrc"
 # kernel class -> (kernel symbols, the sources its code and launch layout come from)
 KERNEL_SOURCES = {
     "fwd": (("k_fwd<",), ["chain.hip"]), "active": (("k_active<",), ["chain.hip"]),
-    "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dwt(", "k_dw32<"), ["dw.hip"]),
+    "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dw32<"), ["dw.hip"]),
+    "dwt": (("k_dwt(",), ["dw.hip"]),
     "reduce": (("k_dw_reduce<",), ["dw.hip"]), "cast": (("k_cast<",), ["rowops.hip"]),
     "emb_sgd": (("k_embed_sgd",), ["embed.hip"]), "gemm": (("k_gemm",), ["gemm.hip"]),
 }
@@ -124,25 +125,36 @@ def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int
     return res
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, data, params, seconds: float) -> dict:
     """The oracle (float64 numpy) on this host over the same resident dataset,
     for about ``seconds`` of CPU work: a probe run sizes the sample, and a
     sample that ends well short of ``seconds`` is run again, longer."""
     import vfl_synth as S
     from oracle import PubSubOracle
+    affinity = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        threads = affinity
     R = w.rows_per_tick
     rows_of = lambda g: S.group_rows(w, g)
-    # size the sample from a 16-group run after a 1-group warm-up (a few
-    # groups are dominated by set-up and the s-tick lead-in); a run under
-    # half of the target is repeated with the groups scaled to the target
+    # size the sample from a 1-group run after a 1-group warm-up; a run
+    # under half of the target is repeated with the groups scaled to it
     PubSubOracle(w, params, "f64").run(data, 1, rows_of, keep_messages=False)
-    groups, dt = 16, 0.0
-    for _ in range(3):
+    groups, dt = 1, 0.0
+    for _ in range(4):
         o = PubSubOracle(w, params, "f64")
         t0 = time.perf_counter()
         o.run(data, groups, rows_of, keep_messages=False)
@@ -153,7 +165,8 @@ def cpu_baseline(w, data, params, seconds: float) -> dict:
     return {"value": groups * R / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {groups} batch groups of {R} rows of the same dataset "
                       f"({groups + w.staleness} ticks incl. the s={w.staleness} lead-in), "
-                      f"float64 numpy, {dt:.1f} s"}
+                      f"float64 numpy, {dt:.1f} s",
+            "affinity_cores": affinity, "blas_threads": int(threads), "cpu_model": cpu_model()}
 
 
 def serial_probe(w, data, params, epoch, ticks: int = 24) -> dict:
@@ -189,7 +202,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2400)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="dense_tabular")
+    ap.add_argument("--workload", default="hetero")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -243,8 +256,8 @@ def main():
     sess.bind()
     cyc = V.VFL_GRAPH_CYCLES * (w.staleness + 1)
     V.vfl_timing_enable(sess.ctx, 1 << dom_i)
-    sess.run(t, cyc)                       # captures the graph timed region replays
-    t += cyc
+    sess.run(t, args.steps)                # captures the graphs the timed region replays
+    t += args.steps
     V.vfl_timing_read(sess.ctx, dom_i)
 
     torch.cuda.synchronize()

@@ -77,11 +77,15 @@ enum {
   VFL_NOISE_GRAD = 2,   /* add Gaussian noise to the returned gradient */
   VFL_CLIP_EMB = 4,     /* clip each embedding row to L2 norm clip_c */
   VFL_CLIP_GRAD = 8,    /* clip each gradient row to L2 norm clip_c */
-  VFL_FIFO_DISCARD = 16 /* a full channel discards its oldest group (see
+  VFL_FIFO_DISCARD = 16,/* a full channel discards its oldest group (see
                            vfl_bottom_forward) instead of VFL_E_STALE */
+  VFL_LOSS_MSE = 32     /* regression: the top model's output is a prediction
+                           and the loss the mean squared error over the
+                           group's rows (labels are real-valued targets)
+                           instead of the binary cross-entropy of Eq. (1) */
 };
 
-#define VFL_MAX_LAYERS 8
+#define VFL_MAX_LAYERS 16
 #define VFL_MAX_REPLICAS 8
 #define VFL_MAX_STALENESS 4   /* channel capacity p = q = 5 slots */
 
@@ -97,8 +101,9 @@ typedef struct {
 } vfl_bottom_spec;
 
 /* The top model on [z_A | z_B]: n_layers >= 2 fully connected layers, the
- * last of width 1 (the logit, linear); bit j of relu_mask puts a ReLU after
- * hidden layer j. */
+ * last of width 1 (the logit, or with VFL_LOSS_MSE the prediction; linear);
+ * bit j of relu_mask puts a ReLU after hidden layer j.  Party A's layers and
+ * the top model's hidden layers together number at most VFL_MAX_LAYERS. */
 typedef struct {
   int32_t n_layers;
   int32_t widths[VFL_MAX_LAYERS];
@@ -232,13 +237,16 @@ vfl_status vfl_bind_dataset(vfl_ctx* c, const vfl_dataset* a, const vfl_dataset*
  * Group g covers rows [(g mod E) * R, ...) with E = ceil(n_rows / R) groups
  * per epoch (the last group of an epoch is short; its rows are split into
  * replicas of `batch` rows like any group), which are exactly the batches a
- * caller of vfl_step would pass.  The ticks replay a captured HIP graph of
- * several ticks per phase t mod (s+1); a small kernel at the start of each
- * party's part of a tick derives the tick's rows, noise step and channel
- * headers from a device-side tick counter, so the host launches one graph
- * per graph length (VFL_GRAPH_CYCLES * (s+1) ticks; the remainder runs as
- * vfl_step).  Steady state only: t0 >= s+1 and ticks 0 .. t0-1 already run
- * (VFL_E_STATE otherwise).  loss_ring (device float [loss_len], nullable)
+ * caller of vfl_step would pass.  The ticks replay captured HIP graphs: one
+ * of VFL_GRAPH_CYCLES * (s+1) ticks per phase t mod (s+1), launched n / that
+ * many times, and one of the remaining ticks (captured per phase and
+ * length).  Every launch derives its tick's rows, noise step and channel
+ * headers from a device-side tick record that the graph's last node
+ * advances, so the host launches whole graphs only.  Steady state only: t0
+ * >= s+1, ticks 0 .. t0-1 already run, no discarded group awaiting B's
+ * backward and, after a discard, s+1 further ticks run with vfl_step (the
+ * groups in flight then carry the versions the replays derive);
+ * VFL_E_STATE otherwise.  loss_ring (device float [loss_len], nullable)
  * receives group u's mean loss at index u mod loss_len. */
 #define VFL_GRAPH_CYCLES 4
 vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t loss_len);
@@ -341,7 +349,8 @@ typedef enum {
   VFL_K_CAST = 5,       /* weight operand copies */
   VFL_K_EMB_SGD = 6,    /* sorted sparse SGD of the tables */
   VFL_K_GEMM = 7,       /* layer products of party B's wide layers (input gradient) */
-  VFL_K_COUNT = 8
+  VFL_K_DWT = 8,        /* large-tile bf16 weight-gradient products (partials + SGD) */
+  VFL_K_COUNT = 9
 } vfl_kernel_class;
 
 /* Measurement hook: while class_mask is non-zero, every launch of a
@@ -351,7 +360,8 @@ typedef enum {
  * vfl_timing_read then reports those of the last replay.  vfl_timing_read
  * synchronises both streams and returns, for one class, the summed kernel
  * durations in milliseconds, the number of launches and the summed
- * algorithmic work (matrix-product FLOPs for the first four classes, bytes
+ * algorithmic work (matrix-product FLOPs for VFL_K_FWD .. VFL_K_DW, VFL_K_GEMM
+ * and VFL_K_DWT, bytes
  * that the kernel must move at minimum for the others); then it resets that class.
  * Enabling with mask 0 stops recording. */
 vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t class_mask);

@@ -6,7 +6,9 @@ Test infrastructure only (see ``oracle/__init__.py``).
   y = x W^T + b, W stored [out, in], optionally followed by ReLU (the paper's
   bottom and top models are MLPs, Section 5 "Models").
 * The loss is the binary cross-entropy of Eq. (1) on the top model's logit,
-  averaged over the rows it is given.
+  averaged over the rows it is given; for the regression tasks (Section 5,
+  "Datasets" and "Evaluation Metrics") the mean squared error of the top
+  model's output.
 * Categorical inputs look up rows of per-field embedding tables; the bottom
   model's input is the concatenation of the looked-up rows (field order) and
   the dense features.
@@ -57,6 +59,19 @@ def bce_with_logits(logit, y):
 def bce_dlogit(logit, y):
     """d/dl of the per-row loss: sigmoid(l) - y."""
     return sigmoid(logit) - y
+
+
+def mse(pred, y):
+    """Squared error of a regression output per row, (pred - y)^2; its mean
+    over the rows is the regression loss (scored as RMSE, Section 5
+    "Evaluation Metrics")."""
+    d = np.asarray(pred, dtype=np.float64) - y
+    return d * d
+
+
+def mse_dpred(pred, y):
+    """d/dpred of the per-row squared error: 2 (pred - y)."""
+    return 2.0 * (np.asarray(pred, dtype=np.float64) - y)
 
 
 def clip_rows(v, C):

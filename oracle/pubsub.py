@@ -11,7 +11,8 @@ Appendix) on a deterministic tick schedule (``oracle/schedule.py``):
    publishes the result to the embedding channel of group t;
 2. subscriber phase, active party A, group u = t - s: each replica fetches
    its rows of the published embedding, computes z_A = f_A(x_A), the top
-   model on [z_A | z_B] and the loss of Eq. (1), the gradients of A's and
+   model on [z_A | z_B] and the loss of Eq. (1) (the mean squared error for
+   a regression workload), the gradients of A's and
    the top's parameters and the per-row gradient with respect to the
    published embedding, which (optionally clipped and noised) it publishes
    to the gradient channel of group u;
@@ -209,8 +210,12 @@ class PubSubOracle:
                 h.append(self._q("act.top", L.relu(p) if w.top.relu[j] else p))
             logit = h[-1] @ w_out + b_out
             y = data["y"][rows].astype(np.float64)
-            loss_sum += L.bce_with_logits(logit, y).sum()
-            dl = L.bce_dlogit(logit, y)                    # per row, unscaled
+            if w.loss == "mse":
+                loss_sum += L.mse(logit, y).sum()
+                dl = L.mse_dpred(logit, y)                 # per row, unscaled
+            else:
+                loss_sum += L.bce_with_logits(logit, y).sum()
+                dl = L.bce_dlogit(logit, y)                # per row, unscaled
             g = {f"top.W{self.nT - 1}": (dl @ h[-1])[None, :],
                  f"top.b{self.nT - 1}": np.array([dl.sum()])}
             gin = dl[:, None] * w_out[None, :]

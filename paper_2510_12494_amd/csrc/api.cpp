@@ -224,20 +224,24 @@ struct vfl_ctx {
   bool bound = false;
   vfl_dataset ds_a{}, ds_b{};
   int64_t n_rows = 0;
-  hipGraph_t graph[kMaxSlots]{};
-  hipGraphExec_t gexec[kMaxSlots]{};
-  float* graph_loss[kMaxSlots]{};
-  int64_t graph_loss_len[kMaxSlots]{};
-  uint32_t graph_mask[kMaxSlots]{};
+  // graph i < kMaxSlots: VFL_GRAPH_CYCLES * (s+1) ticks from phase i;
+  // graph kMaxSlots + i: a shorter remainder from phase i
+  static constexpr int kGraphs = 2 * kMaxSlots;
+  hipGraph_t graph[kGraphs]{};
+  hipGraphExec_t gexec[kGraphs]{};
+  float* graph_loss[kGraphs]{};
+  int64_t graph_loss_len[kGraphs]{};
+  uint32_t graph_mask[kGraphs]{};
+  int graph_len[kGraphs]{};
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  int capture_phase = -1;             // >= 0 while capturing that phase's graph
+  int capture_phase = -1;             // >= 0 while capturing that graph (its index)
   int capture_tick = -1;              // tick of the cycle being captured
   struct GPair { hipEvent_t e0, e1; int cls; double work; };
-  std::vector<GPair> gpairs[kMaxSlots];   // created before capture
-  int gused[kMaxSlots]{};                 // pairs used by the captured graph
+  std::vector<GPair> gpairs[kGraphs];     // created before capture
+  int gused[kGraphs]{};                   // pairs used by the captured graph
   hipError_t tm_err = hipSuccess;         // first failed event record in a capture
   std::string tm_err_what;
-  int last_phase = -1;                // phase of the graph replayed last
+  int last_phase = -1;                // the graph replayed last
 };
 
 namespace {
@@ -403,13 +407,15 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   if ((o->flags & (VFL_CLIP_EMB | VFL_CLIP_GRAD)) && !(o->clip_c > 0.f)) return "clip needs clip_c > 0";
   if ((o->flags & (VFL_NOISE_EMB | VFL_NOISE_GRAD)) && !(o->sigma >= 0.f)) return "sigma must be >= 0";
   if (!check_bottom(a, why) || !check_bottom(b, why)) return why;
-  if (!t || t->n_layers < 2 || t->n_layers > VFL_MAX_LAYERS) return "top needs 2..8 layers (>= 1 hidden + logit)";
+  if (!t || t->n_layers < 2 || t->n_layers > VFL_MAX_LAYERS)
+    return "top needs 2.." + std::to_string(VFL_MAX_LAYERS) + " layers (>= 1 hidden + output)";
   if (t->widths[t->n_layers - 1] != 1) return "last top layer must have width 1";
   for (int j = 0; j + 1 < t->n_layers; ++j)
     if (t->widths[j] < 1 || t->widths[j] > 65536) return "bad top width";
   if (t->widths[t->n_layers - 2] > kMaxLogitCols) return "last hidden top width must be <= 512";
   if (a->widths[a->n_layers - 1] % 8) return "party A's embedding width must be a multiple of 8";
-  if (a->n_layers + t->n_layers - 1 > kMaxDw) return "party A + top hidden layers must be <= 8";
+  if (a->n_layers + t->n_layers - 1 > kMaxDw)
+    return "party A's + the top's hidden layers must be <= " + std::to_string(kMaxDw);
   if ((int64_t)o->batch * o->replicas > (1 << 28)) return "rows per tick too large";
 
   p.e = o->dtype == VFL_BF16 ? BF16 : F32;
@@ -752,6 +758,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       if (j + 1 < T.H) a.ft[j].rc = rcm(c, T.arc[j], T.out[j]);
     }
     a.lw = at_f(T.W[T.H]); a.lb = at_f(T.b[T.H]); a.relu_h = T.relu[T.H - 1];
+    a.mse = (o.flags & VFL_LOSS_MSE) != 0;
     a.dh = la.P[0]; a.dh_rc = rcm(c, T.drc[T.H - 1], T.out[T.H - 1]);
     a.part = at_f(T.logit_part);
     a.red = la.red;
@@ -1114,7 +1121,7 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, Ti
                       tr.src ? loss : nullptr, st));
     return VFL_OK;
   }
-  if (m.tile == 256) TIMED(VFL_K_DW, flops, st, launch_dwt(job, m.blocks, scale, tr, st));
+  if (m.tile == 256) TIMED(VFL_K_DWT, flops, st, launch_dwt(job, m.blocks, scale, tr, st));
   else TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
   const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);
   if (blocks > 0) {
@@ -1330,6 +1337,87 @@ int dataset_batches(vfl_ctx* c, int party, int64_t g, vfl_batch* out) {
     b.row0 = st.row0 + o;
   }
   return n;
+}
+
+// Graph gi of `len` ticks whose first tick has phase `phase` (t mod (s+1)),
+// captured once for a loss ring and timing mask; launches refer to tick
+// base + i of the replay, so the graph is independent of the absolute tick,
+// and its last node advances the base by len.
+vfl_status ensure_graph(vfl_ctx* c, int gi, int phase, int len, float* loss_ring, int64_t loss_len) {
+  const Plan& p = c->p;
+  const int s = p.s, S1 = s + 1;
+  const uint32_t mask = c->tm.mask;
+  const bool stale = c->gexec[gi] &&
+      (c->graph_loss[gi] != loss_ring || c->graph_loss_len[gi] != loss_len || c->graph_mask[gi] != mask ||
+       c->graph_len[gi] != len);
+  if (stale) {
+    (void)hipGraphExecDestroy(c->gexec[gi]);
+    (void)hipGraphDestroy(c->graph[gi]);
+    c->gexec[gi] = nullptr;
+    c->graph[gi] = nullptr;
+  }
+  if (c->gexec[gi]) return VFL_OK;
+  c->gused[gi] = 0;
+  if (mask && c->gpairs[gi].empty()) {
+    constexpr int kGraphPairs = 1024;
+    c->gpairs[gi].resize(kGraphPairs);
+    for (auto& gp : c->gpairs[gi]) {
+      HIPCHK(hipEventCreate(&gp.e0));
+      HIPCHK(hipEventCreate(&gp.e1));
+    }
+  }
+  TickSrc* tsrc = at<TickSrc>(c, p.tsrc);
+  // dataset bases: the tick records supply rows, row0 and the headers
+  SlotState sa_in, sb_in;
+  sa_in.rows = p.R; sa_in.dense = c->ds_a.dense; sa_in.ld = c->ds_a.ld; sa_in.ids = c->ds_a.ids;
+  sa_in.labels = c->ds_a.labels;
+  sb_in.rows = p.R; sb_in.dense = c->ds_b.dense; sb_in.ld = c->ds_b.ld; sb_in.ids = c->ds_b.ids;
+  c->tm_err = hipSuccess;
+  HIPCHK(hipStreamBeginCapture(c->sa, hipStreamCaptureModeThreadLocal));
+  c->capture_phase = gi;
+  vfl_status r = VFL_OK;
+  hipError_t he = hipEventRecord(c->ev_fork, c->sa);
+  if (he == hipSuccess) he = hipStreamWaitEvent(c->sb, c->ev_fork, 0);
+  for (int i = 0; i < len && he == hipSuccess && r == VFL_OK; ++i) {
+    const int fs = (phase + i) % S1;                   // slot of group t
+    const int us = ((phase + i - s) % S1 + S1) % S1;   // slot of group t - s
+    const TickRef tb{tsrc, i, 0}, ta{tsrc, i, 1}, tu{tsrc, i, 2};
+    c->capture_tick = i;
+    if ((r = b_forward(c, fs, sb_in, tb))) break;
+    if ((r = b_publish(c, fs))) break;
+    // the first s ticks consume groups published before this graph;
+    // replays on one stream never overlap, so the publish of those groups
+    // is already complete
+    if ((r = a_top(c, 0, us, sa_in, 0, ta, i >= s))) break;
+    if ((r = a_backward(c, sa_in, loss_ring, ta))) break;
+    if ((r = b_backward(c, us, sb_in, 0, tu))) break;
+  }
+  c->capture_tick = -1;
+  if (he == hipSuccess && r == VFL_OK) he = hipEventRecord(c->ev_join, c->sb);
+  if (he == hipSuccess && r == VFL_OK) he = hipStreamWaitEvent(c->sa, c->ev_join, 0);
+  if (he == hipSuccess && r == VFL_OK) he = launch_tick_base(tsrc, len, c->sa);
+  hipGraph_t g = nullptr;
+  const hipError_t he2 = hipStreamEndCapture(c->sa, &g);
+  c->capture_phase = -1;
+  if (r) { if (g) (void)hipGraphDestroy(g); return r; }
+  if (he != hipSuccess || he2 != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    return fail(c, VFL_E_HIP, std::string("graph capture: ") + hipGetErrorString(he != hipSuccess ? he : he2));
+  }
+  if (c->tm_err != hipSuccess) {
+    const hipError_t te = c->tm_err;
+    c->tm_err = hipSuccess;
+    (void)hipGraphDestroy(g);
+    return fail(c, VFL_E_HIP, std::string("timing event record in graph capture: ") + c->tm_err_what +
+                           ": " + hipGetErrorString(te));
+  }
+  c->graph[gi] = g;
+  HIPCHK(hipGraphInstantiate(&c->gexec[gi], g, nullptr, nullptr, 0));
+  c->graph_loss[gi] = loss_ring;
+  c->graph_loss_len[gi] = loss_len;
+  c->graph_mask[gi] = mask;
+  c->graph_len[gi] = len;
+  return VFL_OK;
 }
 
 }  // namespace
@@ -1610,7 +1698,7 @@ vfl_status vfl_bind_dataset(vfl_ctx* c, const vfl_dataset* a, const vfl_dataset*
   }
   if (!a->labels) return fail(c, VFL_E_INVALID, "dataset labels missing");
   // captured graphs point at the previous binding
-  for (int q = 0; q < kMaxSlots; ++q) {
+  for (int q = 0; q < vfl_ctx::kGraphs; ++q) {
     if (c->gexec[q]) (void)hipGraphExecDestroy(c->gexec[q]);
     if (c->graph[q]) (void)hipGraphDestroy(c->graph[q]);
     c->gexec[q] = nullptr;
@@ -1645,127 +1733,53 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
     return fail(c, VFL_E_STATE, "operand copies not current; run vfl_step first");
   const int cyc = VFL_GRAPH_CYCLES * S1;
   const int64_t reps = n / cyc;
+  const int rem = (int)(n % cyc);
+  if (n == 0) return VFL_OK;
+  const int phase = (int)(t0 % S1);   // every graph starts at a multiple of s+1 ticks from t0
   if (reps > 0) {
-    const int phase = (int)(t0 % S1);
-    const uint32_t mask = c->tm.mask;
-    const bool stale = c->gexec[phase] &&
-        (c->graph_loss[phase] != loss_ring || c->graph_loss_len[phase] != loss_len ||
-         c->graph_mask[phase] != mask);
-    if (stale) {
-      (void)hipGraphExecDestroy(c->gexec[phase]);
-      (void)hipGraphDestroy(c->graph[phase]);
-      c->gexec[phase] = nullptr;
-      c->graph[phase] = nullptr;
-    }
-    if (!c->gexec[phase]) {
-      c->gused[phase] = 0;
-      if (mask && c->gpairs[phase].empty()) {
-        constexpr int kGraphPairs = 1024;
-        c->gpairs[phase].resize(kGraphPairs);
-        for (auto& gp : c->gpairs[phase]) {
-          HIPCHK(hipEventCreate(&gp.e0));
-          HIPCHK(hipEventCreate(&gp.e1));
-        }
-      }
-      // capture cyc ticks starting at this phase; launches refer to tick
-      // base + i of the replay, so the graph is independent of the
-      // absolute tick, and its last node advances the base by cyc
-      TickSrc* tsrc = at<TickSrc>(c, p.tsrc);
-      // dataset bases: the tick records supply rows, row0 and the headers
-      SlotState sa_in, sb_in;
-      sa_in.rows = p.R; sa_in.dense = c->ds_a.dense; sa_in.ld = c->ds_a.ld; sa_in.ids = c->ds_a.ids;
-      sa_in.labels = c->ds_a.labels;
-      sb_in.rows = p.R; sb_in.dense = c->ds_b.dense; sb_in.ld = c->ds_b.ld; sb_in.ids = c->ds_b.ids;
-      c->tm_err = hipSuccess;
-      HIPCHK(hipStreamBeginCapture(c->sa, hipStreamCaptureModeThreadLocal));
-      c->capture_phase = phase;
-      vfl_status r = VFL_OK;
-      hipError_t he = hipEventRecord(c->ev_fork, c->sa);
-      if (he == hipSuccess) he = hipStreamWaitEvent(c->sb, c->ev_fork, 0);
-      for (int i = 0; i < cyc && he == hipSuccess && r == VFL_OK; ++i) {
-        const int fs = (phase + i) % S1;             // slot of group t
-        const int us = ((phase + i - s) % S1 + S1) % S1;   // slot of group t - s
-        const TickRef tb{tsrc, i, 0}, ta{tsrc, i, 1}, tu{tsrc, i, 2};
-        c->capture_tick = i;
-        if ((r = b_forward(c, fs, sb_in, tb))) break;
-        if ((r = b_publish(c, fs))) break;
-        // the first s ticks consume groups published before this graph;
-        // replays of a graph on one stream never overlap, so the publish
-        // of those groups is already complete
-        if ((r = a_top(c, 0, us, sa_in, 0, ta, i >= s))) break;
-        if ((r = a_backward(c, sa_in, loss_ring, ta))) break;
-        if ((r = b_backward(c, us, sb_in, 0, tu))) break;
-      }
-      c->capture_tick = -1;
-      if (he == hipSuccess && r == VFL_OK) he = hipEventRecord(c->ev_join, c->sb);
-      if (he == hipSuccess && r == VFL_OK) he = hipStreamWaitEvent(c->sa, c->ev_join, 0);
-      if (he == hipSuccess && r == VFL_OK) he = launch_tick_base(tsrc, cyc, c->sa);
-      hipGraph_t g = nullptr;
-      const hipError_t he2 = hipStreamEndCapture(c->sa, &g);
-      c->capture_phase = -1;
-      if (r) { if (g) (void)hipGraphDestroy(g); return r; }
-      if (he != hipSuccess || he2 != hipSuccess) {
-        if (g) (void)hipGraphDestroy(g);
-        return fail(c, VFL_E_HIP, std::string("graph capture: ") + hipGetErrorString(he != hipSuccess ? he : he2));
-      }
-      if (c->tm_err != hipSuccess) {
-        const hipError_t te = c->tm_err;
-        c->tm_err = hipSuccess;
-        (void)hipGraphDestroy(g);
-        return fail(c, VFL_E_HIP, std::string("timing event record in graph capture: ") + c->tm_err_what +
-                               ": " + hipGetErrorString(te));
-      }
-      c->graph[phase] = g;
-      HIPCHK(hipGraphInstantiate(&c->gexec[phase], g, nullptr, nullptr, 0));
-      c->graph_loss[phase] = loss_ring;
-      c->graph_loss_len[phase] = loss_len;
-      c->graph_mask[phase] = mask;
-    }
-    // the replays start at tick t0 (the dataset and schedule constants with it)
-    TickSrc src;
-    src.base = t0; src.n_rows = c->n_rows; src.R = p.R; src.s = s; src.lr = c->o.lr;
-    src.vofs = (int32_t)vofs;
-    src.loss_len = loss_ring ? loss_len : 1;
-    HIPCHK(hipMemcpyAsync(at<TickSrc>(c, p.tsrc), &src, sizeof(src), hipMemcpyHostToDevice, c->sa));
-    // the graph runs both parties' work from stream A: it must follow the
-    // work already enqueued on stream B
-    HIPCHK(hipEventRecord(c->ev_fork, c->sb));
-    HIPCHK(hipStreamWaitEvent(c->sa, c->ev_fork, 0));
-    for (int64_t k = 0; k < reps; ++k) HIPCHK(hipGraphLaunch(c->gexec[phase], c->sa));
-    // later work on stream B must follow the graph
-    HIPCHK(hipEventRecord(c->ev_join, c->sa));
-    HIPCHK(hipStreamWaitEvent(c->sb, c->ev_join, 0));
-    c->last_phase = phase;
-    // host state as if the ticks had been enqueued one by one
-    for (int64_t t = t0; t < t0 + reps * cyc; ++t) {
-      const int64_t u = t - s;
-      const int fs = (int)(t % S1), us = (int)(u % S1);
-      int64_t row[7] = {t, t, fs, c->b_version, u, us, -1};
-      SlotState st = dataset_slot(c, 1, t);
-      st.version = c->b_version;
-      st.published = true;
-      c->bslot[fs] = st;
-      c->grad_group[us] = u;
-      c->grad_rows[us] = c->bslot[us].rows;
-      c->a_version += 1;
-      c->b_version += 1;
-      c->b_copy_version[us] = c->b_version;
-      row[6] = c->b_version;
-      c->trace.insert(c->trace.end(), row, row + 7);
-    }
-    c->a_copy_version = c->a_version;
-    c->b_next_fwd = c->b_pub_next = t0 + reps * cyc;
-    c->b_next_bwd = c->a_next = t0 + reps * cyc - s;
-  }
-  // the remainder tick by tick
-  for (int64_t t = t0 + reps * cyc; t < t0 + n; ++t) {
-    vfl_batch ab[VFL_MAX_REPLICAS], bb[VFL_MAX_REPLICAS];
-    const int na = dataset_batches(c, 0, t - s, ab);
-    const int nb = dataset_batches(c, 1, t, bb);
-    float* lp = loss_ring ? loss_ring + ((t - s) % loss_len) : nullptr;
-    vfl_status r = vfl_step(c, t, ab, na, bb, nb, lp);
+    vfl_status r = ensure_graph(c, phase, phase, cyc, loss_ring, loss_len);
     if (r) return r;
   }
+  if (rem > 0) {
+    vfl_status r = ensure_graph(c, kMaxSlots + phase, phase, rem, loss_ring, loss_len);
+    if (r) return r;
+  }
+  // the replays start at tick t0 (the dataset and schedule constants with it)
+  TickSrc src;
+  src.base = t0; src.n_rows = c->n_rows; src.R = p.R; src.s = s; src.lr = c->o.lr;
+  src.vofs = (int32_t)vofs;
+  src.loss_len = loss_ring ? loss_len : 1;
+  HIPCHK(hipMemcpyAsync(at<TickSrc>(c, p.tsrc), &src, sizeof(src), hipMemcpyHostToDevice, c->sa));
+  // the graphs run both parties' work from stream A: they must follow the
+  // work already enqueued on stream B
+  HIPCHK(hipEventRecord(c->ev_fork, c->sb));
+  HIPCHK(hipStreamWaitEvent(c->sa, c->ev_fork, 0));
+  for (int64_t k = 0; k < reps; ++k) HIPCHK(hipGraphLaunch(c->gexec[phase], c->sa));
+  if (rem > 0) HIPCHK(hipGraphLaunch(c->gexec[kMaxSlots + phase], c->sa));
+  // later work on stream B must follow the graphs
+  HIPCHK(hipEventRecord(c->ev_join, c->sa));
+  HIPCHK(hipStreamWaitEvent(c->sb, c->ev_join, 0));
+  c->last_phase = rem > 0 ? kMaxSlots + phase : phase;
+  // host state as if the ticks had been enqueued one by one
+  for (int64_t t = t0; t < t0 + n; ++t) {
+    const int64_t u = t - s;
+    const int fs = (int)(t % S1), us = (int)(u % S1);
+    int64_t row[7] = {t, t, fs, c->b_version, u, us, -1};
+    SlotState st = dataset_slot(c, 1, t);
+    st.version = c->b_version;
+    st.published = true;
+    c->bslot[fs] = st;
+    c->grad_group[us] = u;
+    c->grad_rows[us] = c->bslot[us].rows;
+    c->a_version += 1;
+    c->b_version += 1;
+    c->b_copy_version[us] = c->b_version;
+    row[6] = c->b_version;
+    c->trace.insert(c->trace.end(), row, row + 7);
+  }
+  c->a_copy_version = c->a_version;
+  c->b_next_fwd = c->b_pub_next = t0 + n;
+  c->b_next_bwd = c->a_next = t0 + n - s;
   return VFL_OK;
 }
 
@@ -1970,6 +1984,8 @@ vfl_status vfl_destroy(vfl_ctx* c) {
   for (int q = 0; q < kMaxSlots; ++q) {
     if (c->ev_emb[q]) (void)hipEventDestroy(c->ev_emb[q]);
     if (c->ev_grad[q]) (void)hipEventDestroy(c->ev_grad[q]);
+  }
+  for (int q = 0; q < vfl_ctx::kGraphs; ++q) {
     if (c->gexec[q]) (void)hipGraphExecDestroy(c->gexec[q]);
     if (c->graph[q]) (void)hipGraphDestroy(c->graph[q]);
     for (auto& gp : c->gpairs[q]) {

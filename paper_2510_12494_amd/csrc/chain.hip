@@ -725,7 +725,8 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   }
   // the logit stage reads the last hidden output, not a product's input
   if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
-  // logit + BCE (Eq. 1), dl = sigmoid(l) - y: a wavefront per row (its
+  // logit + BCE (Eq. 1), dl = sigmoid(l) - y, or for regression the
+  // squared error and dl = 2 (l - y): a wavefront per row (its
   // BR / 8 rows one after the other), lane on the columns 256 i + 4 lane
   // .. +4; the last hidden delta dl * w (ReLU-masked) goes to LDS.  The
   // logit layer's weight gradient sum_r dl_r h[r][c], the loss and dl
@@ -779,19 +780,33 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     // log chains are independent, while the stage below alternates LDS
     // reads and writes the compiler must keep in order (they may alias)
     float dls[RW];
+    if (cst(j).mse) {
+      // regression: squared error (l - y)^2, dl = 2 (l - y)
 #pragma unroll
-    for (int rr = 0; rr < RW; ++rr) {
-      const int r = wave * RW + rr;
-      const bool ok = r < rv;
-      const float l = dots[rr] + lbias;
-      const float yy = yl[r];
-      const float ex = __expf(-fabsf(l));
-      const float inv = __frcp_rn(1.f + ex);
-      const float sig = l >= 0.f ? inv : ex * inv;
-      const float dl = ok ? sig - yy : 0.f;
-      if (ok) lsum += fmaxf(l, 0.f) - yy * l + __logf(1.f + ex);
-      dsum += dl;
-      dls[rr] = dl;
+      for (int rr = 0; rr < RW; ++rr) {
+        const int r = wave * RW + rr;
+        const bool ok = r < rv;
+        const float e = dots[rr] + lbias - yl[r];
+        const float dl = ok ? 2.f * e : 0.f;
+        if (ok) lsum += e * e;
+        dsum += dl;
+        dls[rr] = dl;
+      }
+    } else {
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr) {
+        const int r = wave * RW + rr;
+        const bool ok = r < rv;
+        const float l = dots[rr] + lbias;
+        const float yy = yl[r];
+        const float ex = __expf(-fabsf(l));
+        const float inv = __frcp_rn(1.f + ex);
+        const float sig = l >= 0.f ? inv : ex * inv;
+        const float dl = ok ? sig - yy : 0.f;
+        if (ok) lsum += fmaxf(l, 0.f) - yy * l + __logf(1.f + ex);
+        dsum += dl;
+        dls[rr] = dl;
+      }
     }
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {

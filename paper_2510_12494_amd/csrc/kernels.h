@@ -37,8 +37,8 @@ enum Elt { F32 = 0, BF16 = 1 };
 
 inline int elt_size(Elt e) { return e == F32 ? 4 : 2; }
 
-constexpr int kMaxChain = 8;          // layers per chain (bottom or top)
-constexpr int kMaxDw = 8;             // weight-gradient problems per launch
+constexpr int kMaxChain = 16;         // layers per chain (bottom or top)
+constexpr int kMaxDw = 16;            // weight-gradient problems per launch
 constexpr int kMaxLogitCols = 512;    // widest last hidden layer of the top model
 constexpr int kLdsMax = 160 * 1024;   // LDS of one gfx950 workgroup
 constexpr int kChainWaves = 8;        // wavefronts per chain-kernel block
@@ -200,7 +200,8 @@ struct FwdJob {
 
 // Party A's step of a group: forward of A's layers fa (the last writes the
 // first dA columns of `cat`), B's embedding zb into columns [dA, dA + dB) of
-// cat, the top hidden layers ft, logit + BCE into the last hidden delta dh
+// cat, the top hidden layers ft, logit + BCE (mse: output + squared error)
+// into the last hidden delta dh
 // (per-block partials {sum loss, sum dl, sum_r dl * h[r][c]} to
 // part[block]; `red`: LDS for the logit weights, labels, dl and loss of the
 // block's rows), the top input-gradient chain dt (j = H-1 .. 1), the concat
@@ -221,6 +222,7 @@ struct ActiveJob {
   int32_t H = 0;
   ChainLayer ft[kMaxChain];
   const float* lw = nullptr; const float* lb = nullptr; int32_t relu_h = 0;
+  int32_t mse = 0;                    // squared-error loss on the output (else BCE)
   LBuf dh; RCMat dh_rc;
   float* part = nullptr;
   LBuf red;

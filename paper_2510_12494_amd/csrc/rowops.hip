@@ -12,7 +12,7 @@ namespace {
 using namespace dev;
 
 // ------------------------------------------------------------ weight copies
-struct CastJobs { CastJob j[2 * 8 + 2]; int n; };
+struct CastJobs { CastJob j[2 * kMaxChain + 2]; int n; };
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_cast(CastJobs js) {

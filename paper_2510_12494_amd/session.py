@@ -44,7 +44,8 @@ def opts(w) -> V.vfl_opts:
     o.seed = w.noise_seed
     o.flags = ((V.VFL_NOISE_EMB if w.noise_emb else 0) | (V.VFL_NOISE_GRAD if w.noise_grad else 0)
                | (V.VFL_CLIP_EMB if w.clip_emb else 0) | (V.VFL_CLIP_GRAD if w.clip_grad else 0)
-               | (V.VFL_FIFO_DISCARD if getattr(w, "fifo_discard", False) else 0))
+               | (V.VFL_FIFO_DISCARD if getattr(w, "fifo_discard", False) else 0)
+               | (V.VFL_LOSS_MSE if getattr(w, "loss", "bce") == "mse" else 0))
     return o
 
 

@@ -18,8 +18,8 @@ VFL_F32, VFL_BF16 = 0, 1
 VFL_PARTY_A, VFL_PARTY_B, VFL_TOP = 0, 1, 2
 VFL_PARAM_W, VFL_PARAM_B, VFL_PARAM_TABLE = 0, 1, 2
 VFL_NOISE_EMB, VFL_NOISE_GRAD, VFL_CLIP_EMB, VFL_CLIP_GRAD = 1, 2, 4, 8
-VFL_FIFO_DISCARD = 16
-VFL_MAX_LAYERS = 8
+VFL_FIFO_DISCARD, VFL_LOSS_MSE = 16, 32
+VFL_MAX_LAYERS = 16
 VFL_GRAPH_CYCLES = 4
 VFL_TIMED_EVERY = 4       # vfl_run times the launches of every 4th tick of a captured cycle
 STATUS_NAMES = {0: "VFL_OK", 1: "VFL_E_INVALID", 2: "VFL_E_NOMEM", 3: "VFL_E_HIP",
@@ -31,7 +31,7 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
            "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan",
            "vfl_last_error", "vfl_destroy")
-KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm")
+KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt")
 
 
 class vfl_plan_party(C.Structure):

@@ -32,11 +32,19 @@ import vfl_synth as S
 from oracle import PubSubOracle
 
 F32_TOL = 1e-4
-BF16_TOL = 2e-2          # theta, against both the bf16 emulation and float64
-BF16_DELTA_TOL = 2e-2    # delta-theta against the bf16 emulation
-BF16_LOSS = 1e-3         # per-group mean loss, relative
+# bf16 workloads.  The stated bound is 2e-2 on parameters against float64;
+# against the bf16 emulation (which rounds where the GPU stores) the GPU
+# differs by float32 accumulation order, which moves a few values across a
+# bf16 rounding boundary or a ReLU kink, and those differences grow over
+# the run.  Measured worst cases: theta 3e-7, loss 1.2e-6, delta-theta 5.6e-3
+# over 100 groups (the bf16 effect itself, emulation vs float64, is 1.8e-2
+# there and 5-7e-2 on the k = 2..4 workloads).
+BF16_TOL = 2e-2          # theta against float64 (the stated bound)
+BF16_THETA_EMU = 1e-4    # theta against the bf16 emulation
+BF16_DELTA_TOL = 1e-2    # delta-theta against the bf16 emulation (+ float32 ulps per update)
+BF16_LOSS = 1e-4         # per-group mean loss, relative
 BF16_MSG_ELEM = 2.0 ** -6  # message elements: |gpu - ref| <= this * max|ref| ...
-BF16_MSG_FRAC = 2e-3       # ... on all but this fraction
+BF16_MSG_FRAC = 5e-3       # ... on all but this fraction
 BF16_MSG_L2 = 2e-2         # global relative L2 error of a message
 
 # achieved errors: {(test, quantity): (worst value, bound)}

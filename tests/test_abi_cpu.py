@@ -63,7 +63,7 @@ def test_workspace_size_for_every_workload(V):
 
 
 @pytest.mark.parametrize("bad", ["staleness", "top_logit", "a_width", "no_hidden", "replicas",
-                                 "emb_dim", "clip"])
+                                 "emb_dim", "clip", "layers", "a_plus_top"])
 def test_invalid_configurations_are_rejected(V, bad):
     from paper_2510_12494_amd.session import bottom_spec, top_spec, opts
     w = S.get("dense_tabular")
@@ -84,6 +84,17 @@ def test_invalid_configurations_are_rejected(V, bad):
     elif bad == "clip":
         o.flags = V.VFL_CLIP_EMB
         o.clip_c = 0.0
+    elif bad == "layers":
+        b.n_layers = V.VFL_MAX_LAYERS + 1
+    elif bad == "a_plus_top":
+        # A's layers and the top's hidden layers share one weight-gradient launch
+        a.n_layers = 10
+        for i in range(10):
+            a.widths[i] = 16
+        t.n_layers = 8
+        for i in range(7):
+            t.widths[i] = 16
+        t.widths[7] = 1
     with pytest.raises(V.VflError) as e:
         V.vfl_workspace_size(a, b, t, o)
     assert e.value.status == V.VFL_E_INVALID
@@ -110,8 +121,10 @@ def _random_shape(rng, dtype):
         ws[-1] = int(rng.integers(1, 40)) * last_mult
         return ws
     cat = bool(rng.integers(0, 2))
-    A = PartySpec(dense=int(rng.integers(1, 90)), widths=widths(int(rng.integers(1, 4)), 8))
-    B = PartySpec(dense=int(rng.integers(0 if cat else 1, 90)), widths=widths(int(rng.integers(1, 4)), 1),
+    deep = bool(rng.integers(0, 4) == 0)        # a quarter of the shapes up to 12 layers deep
+    nl = lambda: int(rng.integers(1, 13 if deep else 4))
+    A = PartySpec(dense=int(rng.integers(1, 90)), widths=widths(nl(), 8))
+    B = PartySpec(dense=int(rng.integers(0 if cat else 1, 90)), widths=widths(nl(), 1),
                   n_cat=int(rng.integers(1, 4)) if cat else 0, vocab=50, emb_dim=4 * int(rng.integers(1, 5)))
     top = TopSpec(widths=[int(rng.integers(1, 300)) for _ in range(int(rng.integers(1, 3)))] + [1])
     extra = bool(rng.integers(0, 2))

@@ -25,7 +25,7 @@ def _prec(w):
 
 
 def _tol(w):
-    return H.BF16_TOL if w.dtype == "bf16" else H.F32_TOL
+    return H.BF16_THETA_EMU if w.dtype == "bf16" else H.F32_TOL
 
 
 def _dtol(w):
@@ -185,6 +185,45 @@ def test_large_workloads_100_groups(name, batch):
     last = 100 + w.staleness - 1
     snap = lambda t: t in (10, 50, last)
     run = H.Run(w, n, 100, snap=snap)
+    _full_check(run, w)
+
+
+def test_regression_ten_layer_bottoms():
+    """The regression workload (ten-layer bottoms, squared-error head, bf16,
+    s=2, k=2) at its real tick shape over 6 groups."""
+    w = S.get("regression")
+    run = H.Run(w, 6 * w.rows_per_tick, 6)
+    _full_check(run, w)
+
+
+@pytest.mark.timeout(900)
+def test_regression_100_groups():
+    """The regression workload over 100 batch groups at a smaller replica
+    batch (R = 2048 rows per tick): parameters at groups 10, 50 and 100
+    against the bf16 emulation, and theta against the float64 oracle."""
+    w = S.get("regression").replace(batch=1024)
+    n = 100 * w.rows_per_tick
+    last = 100 + w.staleness - 1
+    snap = lambda t: t in (10, 50, last)
+    run = H.Run(w, n, 100, snap=snap)
+    _full_check(run, w)
+
+
+@pytest.mark.parametrize("s,k", [(0, 1), (3, 2)])
+def test_ten_layer_odd_widths_f32(s, k):
+    """Ten-layer bottoms at odd widths with linear layers among the ReLU
+    ones, a two-layer top with the squared-error head, float32: every tick
+    against the float64 oracle."""
+    relu = [True, False, True, True, True, False, True, True, True, True]
+    w = Workload(name="deep", n_rows=7 * 130 + 9, dtype="f32",
+                 A=PartySpec(dense=19, widths=[40, 33, 24, 17, 40, 9, 28, 31, 12, 8], relu=relu),
+                 B=PartySpec(dense=13, n_cat=2, vocab=23, emb_dim=4,
+                             widths=[29, 36, 17, 22, 40, 13, 27, 18, 33, 20], relu=relu[::-1]),
+                 top=TopSpec(widths=[21, 11, 1]), batch=130 // k, staleness=s, replicas=k,
+                 lr=0.01, labels="regression", loss="mse", data_seed=111, init_seed=112,
+                 noise_seed=113)
+    n_groups = (w.n_rows + w.rows_per_tick - 1) // w.rows_per_tick
+    run = H.Run(w, w.n_rows, n_groups)
     _full_check(run, w)
 
 
@@ -349,17 +388,19 @@ def test_channel_discards(dtype, s, discard):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_limits_of_the_interface(dtype):
     """The largest staleness (s = 4: five channel slots) and replica count
-    (k = 8), B's bottom at the 8-layer limit, A's bottom and the top's hidden
-    layers at the 8-problem limit of one weight-gradient launch (3 + 5),
-    linear layers mixed with ReLU ones (the masks of the input-gradient
-    chains skip them), the largest embedding width (16) and a ragged last
-    group of 3 rows."""
+    (k = 8), B's bottom at the 16-layer limit, A's bottom and the top's
+    hidden layers at the 16-problem limit of one weight-gradient launch
+    (3 + 13), linear layers mixed with ReLU ones (the masks of the
+    input-gradient chains skip them), the largest embedding width (16) and
+    a ragged last group of 3 rows."""
     w = Workload(name="limits", n_rows=9 * 400 + 3, dtype=dtype,
                  A=PartySpec(dense=11, n_cat=2, vocab=29, emb_dim=16, widths=[36, 20, 16],
                              relu=[True, False, True]),
-                 B=PartySpec(dense=9, widths=[24, 18, 30, 12, 26, 16, 20, 10],
-                             relu=[True, True, False, True, True, False, True, True]),
-                 top=TopSpec(widths=[28, 14, 22, 9, 17, 1], relu=[True, False, True, True, False]),
+                 B=PartySpec(dense=9, widths=[24, 18, 30, 12, 26, 16, 20, 10, 14, 22, 9, 17, 25, 11, 19, 10],
+                             relu=[True, True, False, True, True, False, True, True] * 2),
+                 top=TopSpec(widths=[28, 14, 22, 9, 17, 12, 20, 15, 11, 18, 13, 16, 10, 1],
+                             relu=[True, False, True, True, False, True, True, False, True, True,
+                                   True, False, True]),
                  batch=50, staleness=4, replicas=8, lr=0.3, clip=1.0, sigma=0.5,
                  clip_emb=True, clip_grad=True, noise_emb=True, noise_grad=True,
                  labels="bernoulli", label_p=0.45, data_seed=101, init_seed=102, noise_seed=103)

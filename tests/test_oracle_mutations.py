@@ -16,7 +16,7 @@ def _fails(fn, *a):
 
 def test_dropped_clip_jacobian_is_caught(monkeypatch):
     monkeypatch.setattr(L, "clip_rows_backward", lambda g, v, n, c, C: g)
-    _fails(T.test_finite_differences_whole_step)
+    _fails(T.test_finite_differences_whole_step, "bce")
 
 
 def test_wrong_sign_in_dlogit_is_caught(monkeypatch):
@@ -33,20 +33,20 @@ def test_backward_at_current_weights_is_caught(monkeypatch):
         self.S[u % (self.s + 1)]["Wq"] = self._weights("B", self.nB)
         return orig(self, u, t)
     monkeypatch.setattr(PS.PubSubOracle, "passive_backward", current)
-    _fails(T.test_equals_history_formulation, 2, 2)
+    _fails(T.test_equals_history_formulation, 2, 2, "bce")
 
 
 def test_swapped_embedding_fields_is_caught(monkeypatch):
     orig = L.embedding_grad
     monkeypatch.setattr(L, "embedding_grad",
                         lambda g, ids, vocab, shape: orig(g, ids[:, ::-1], vocab, shape))
-    _fails(T.test_finite_differences_whole_step)
+    _fails(T.test_finite_differences_whole_step, "bce")
 
 
 def test_noise_on_wrong_tag_is_caught(monkeypatch):
     orig = PS.gaussian
     monkeypatch.setattr(PS, "gaussian", lambda seed, step, rows, n, tag: orig(seed, step, rows, n, 0))
-    _fails(T.test_equals_history_formulation, 1, 1)
+    _fails(T.test_equals_history_formulation, 1, 1, "bce")
 
 
 def test_mean_instead_of_row_weighted_mean_is_caught(monkeypatch):
@@ -57,4 +57,16 @@ def test_mean_instead_of_row_weighted_mean_is_caught(monkeypatch):
     def unweighted(self, grads_sum, n_rows):
         return orig(self, grads_sum, self.w.batch * self.w.replicas)
     monkeypatch.setattr(PS.PubSubOracle, "_sgd", unweighted)
-    _fails(T.test_equals_history_formulation, 1, 1)
+    _fails(T.test_equals_history_formulation, 1, 1, "bce")
+
+
+def test_squared_error_without_its_factor_two_is_caught(monkeypatch):
+    monkeypatch.setattr(L, "mse_dpred", lambda p, y: p - y)
+    _fails(T.test_closed_form_linear_regression)
+
+
+def test_regression_trained_on_bce_is_caught(monkeypatch):
+    """The regression head taking the BCE branch (the loss flag ignored)."""
+    monkeypatch.setattr(L, "mse", L.bce_with_logits)
+    monkeypatch.setattr(L, "mse_dpred", L.bce_dlogit)
+    _fails(T.test_equals_history_formulation, 2, 2, "mse")

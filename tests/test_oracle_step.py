@@ -74,16 +74,51 @@ def test_closed_form_logistic_regression():
     assert abs(recs[0]["loss"] - loss) < 1e-13
 
 
+def test_closed_form_linear_regression():
+    """Linear one-layer bottoms and a linear output with the squared error:
+    the prediction is l = u . [Z_A | Z_B] + c and, with r = 2 (l - y),
+    dL/du = [Z_A | Z_B]^T r / R, dL/dW_X = u_X (r^T X_X) / R,
+    dL/db_X = u_X sum(r) / R, dL/dc = sum(r) / R (the least-squares
+    gradient); the loss is the mean of (l - y)^2."""
+    w = _mk(A=PartySpec(dense=3, widths=[2], relu=[False]),
+            B=PartySpec(dense=4, widths=[3], relu=[False]),
+            top=TopSpec(widths=[1]), batch=25, n_rows=25, lr=0.3, labels="regression",
+            loss="mse")
+    o, recs, d, p = _run(w, 1, keep_grads=True)
+    R = 25
+    XA, XB, y = d["xa"].astype(float), d["xb"].astype(float), d["y"].astype(float)
+    assert len(np.unique(y)) == R          # real-valued targets
+    ZA = XA @ p["A.W0"].T.astype(float) + p["A.b0"]
+    ZB = XB @ p["B.W0"].T.astype(float) + p["B.b0"]
+    u = p["top.W0"][0].astype(float)
+    c = float(p["top.b0"][0])
+    l = np.concatenate([ZA, ZB], 1) @ u + c
+    r = 2.0 * (l - y)
+    uA, uB = u[:2], u[2:]
+    want = {"top.W0": np.concatenate([ZA, ZB], 1).T @ r / R,
+            "top.b0": np.array([r.sum() / R]),
+            "A.W0": np.outer(uA, r @ XA) / R, "A.b0": uA * r.sum() / R,
+            "B.W0": np.outer(uB, r @ XB) / R, "B.b0": uB * r.sum() / R}
+    g = recs[0]["grads"]
+    for k, v in want.items():
+        np.testing.assert_allclose(g[k].reshape(v.shape) / R, v, rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(o.p[k].reshape(v.shape),
+                                   p[k].astype(float).reshape(v.shape) - w.lr * v, rtol=1e-12)
+    assert abs(recs[0]["loss"] - np.mean((l - y) ** 2)) < 1e-13
+
+
 # ------------------------------------------------------ finite differences
-def _fd_workload():
+def _fd_workload(loss="bce"):
     return _mk(A=PartySpec(dense=3, n_cat=2, vocab=7, emb_dim=2, widths=[4, 3]),
                B=PartySpec(dense=2, n_cat=2, vocab=7, emb_dim=2, widths=[4, 2]),
                top=TopSpec(widths=[3, 1]), n_rows=5, batch=5, clip=0.3,
-               clip_emb=True, noise_emb=True, sigma=0.5, zipf_a=0.5)
+               clip_emb=True, noise_emb=True, sigma=0.5, zipf_a=0.5,
+               loss=loss, labels="regression" if loss == "mse" else "bernoulli")
 
 
-def test_finite_differences_whole_step():
-    w = _fd_workload()
+@pytest.mark.parametrize("loss", ["bce", "mse"])
+def test_finite_differences_whole_step(loss):
+    w = _fd_workload(loss)
     d = S.generate(w)
     p0 = S.init_params(w)
 
@@ -116,16 +151,19 @@ def test_finite_differences_whole_step():
 
 
 # ------------------------------------------- independent torch formulation
-@pytest.mark.parametrize("s,k", [(0, 1), (1, 1), (2, 2), (3, 1), (4, 4)])
-def test_equals_history_formulation(s, k):
+@pytest.mark.parametrize("s,k,loss", [(0, 1, "bce"), (1, 1, "bce"), (2, 2, "bce"), (3, 1, "bce"),
+                                      (4, 4, "bce"), (2, 2, "mse")])
+def test_equals_history_formulation(s, k, loss):
     """Ring + stash oracle == full-version-history torch autograd, with the
     private workload's clip and noise on both messages and embedding tables
-    on both parties; k replicas == one batch of k * B rows."""
+    on both parties; k replicas == one batch of k * B rows; BCE and the
+    squared error of a regression output."""
     w = _mk(A=PartySpec(dense=3, n_cat=2, vocab=7, emb_dim=2, widths=[6, 3]),
             B=PartySpec(dense=4, n_cat=1, vocab=5, emb_dim=3, widths=[5, 4]),
             top=TopSpec(widths=[5, 1]), staleness=s, replicas=k, batch=12 // k,
-            n_rows=12 * 7 - 5, lr=0.5, clip=0.7, sigma=0.3, clip_emb=True,
-            clip_grad=True, noise_emb=True, noise_grad=True, zipf_a=0.8)
+            n_rows=12 * 7 - 5, lr=0.5 if loss == "bce" else 0.05, clip=0.7, sigma=0.3,
+            clip_emb=True, clip_grad=True, noise_emb=True, noise_grad=True, zipf_a=0.8,
+            loss=loss, labels="regression" if loss == "mse" else "bernoulli")
     n_groups = 9          # wraps the 7-group epoch; its last group is short
     o, recs, d, p = _run(w, n_groups)
     losses, final = run_history(w, p, d, n_groups, lambda g: S.group_rows(w, g))
@@ -231,3 +269,21 @@ def test_bf16_mode_stores_bf16_and_stays_close():
         assert np.array_equal(ob.p[k].astype(np.float32).astype(np.float64), ob.p[k])
         d0 = p[k].astype(np.float64)
         assert _relerr(ob.p[k] - d0, of.p[k] - d0) < 5e-2
+
+
+def test_ten_layer_bottoms_equal_history_formulation():
+    """The paper's bottom model depth (a ten-layer MLP, Section 5 "Models")
+    with linear layers between ReLU ones, the squared-error head, s = 3,
+    k = 2: the oracle's chains against the autograd formulation."""
+    relu = [True, False, True, True, True, False, True, True, True, True]
+    w = _mk(A=PartySpec(dense=5, widths=[6, 5, 7, 4, 6, 5, 6, 4, 5, 8], relu=relu),
+            B=PartySpec(dense=4, widths=[5, 6, 4, 7, 5, 6, 5, 4, 6, 3], relu=relu[::-1]),
+            top=TopSpec(widths=[4, 3, 1]), staleness=3, replicas=2, batch=6, n_rows=12 * 6 - 1,
+            lr=0.05, labels="regression", loss="mse")
+    o, recs, d, p = _run(w, 8)
+    losses, final = run_history(w, p, d, 8, lambda g: S.group_rows(w, g))
+    np.testing.assert_allclose([r["loss"] for r in recs if "loss" in r], losses, rtol=1e-13)
+    for key, v in final.items():
+        assert _relerr(o.p[key], v) < 1e-12, key
+        d0 = p[key].astype(np.float64)
+        assert _relerr(o.p[key] - d0, v - d0) < 1e-9, key

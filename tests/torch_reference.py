@@ -156,7 +156,10 @@ def run_history(w, params, data, n_groups, rows_of, discard=None, rnd=None, poin
             else:
                 h = h @ PA[f"top.W{j}"].T + PA[f"top.b{j}"]     # logit: float32 master weight
         y = _t(data["y"][rows])
-        loss_sum = torch.nn.functional.binary_cross_entropy_with_logits(h[:, 0], y, reduction="sum")
+        if getattr(w, "loss", "bce") == "mse":
+            loss_sum = ((h[:, 0] - y) ** 2).sum()
+        else:
+            loss_sum = torch.nn.functional.binary_cross_entropy_with_logits(h[:, 0], y, reduction="sum")
         names = list(PA)
         grads = torch.autograd.grad(loss_sum, [PA[k] for k in names] + [zhat])
         gmsg = grads[-1]                            # per-row gradient

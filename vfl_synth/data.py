@@ -55,7 +55,7 @@ def generate(w: Workload, n_rows: int | None = None) -> dict:
     Keys: ``xa``, ``xb`` float32 [n, dense] (bf16-exact values when
     ``w.dtype == 'bf16'``, None when a party has no dense features), ``ida``,
     ``idb`` int32 [n, n_cat] (None without categorical fields), ``y`` float32
-    [n] in {0, 1}.
+    [n] in {0, 1} (real-valued targets for ``labels == 'regression'``).
     """
     n = w.n_rows if n_rows is None else int(n_rows)
     out = {"xa": None, "xb": None, "ida": None, "idb": None}
@@ -98,9 +98,10 @@ def _labels(w: Workload, d: dict, n: int) -> np.ndarray:
             p = 1.0 / (1.0 + np.exp(-(x @ v)))
             y[lo:hi] = _rng(w.data_seed, c, 9, 3).random(hi - lo) < p
         return y
-    if w.labels == "teacher":
+    if w.labels in ("teacher", "regression"):
         # random 2-layer teacher dim -> 32 -> 1 (ReLU, zero biases,
-        # weights ~ N(0, 1/fan_in)); label = teacher output above its median
+        # weights ~ N(0, 1/fan_in)); label = teacher output above its
+        # median, or (regression) the teacher output itself
         r = _rng(w.data_seed, 7, 1)
         w1 = r.standard_normal((32, dim)) / np.sqrt(dim)
         w2 = r.standard_normal(32) / np.sqrt(32)
@@ -108,6 +109,8 @@ def _labels(w: Workload, d: dict, n: int) -> np.ndarray:
         for c, lo, hi in _chunks(n):
             x = np.concatenate([a[lo:hi].astype(np.float64) for a in xs], axis=1)
             t[lo:hi] = np.maximum(x @ w1.T, 0.0) @ w2
+        if w.labels == "regression":
+            return t.astype(np.float32)
         return (t > np.median(t)).astype(np.float32)
     raise ValueError(w.labels)
 

@@ -82,7 +82,8 @@ class Workload:
     clip_emb: bool = False
     clip_grad: bool = False
     fifo_discard: bool = False   # a full channel drops its oldest group
-    labels: str = "teacher"  # "logistic" | "teacher" | "bernoulli"
+    labels: str = "teacher"  # "logistic" | "teacher" | "bernoulli" | "regression"
+    loss: str = "bce"        # "bce" (Eq. 1 on a logit) | "mse" (squared error on a prediction)
     label_p: float = 0.25
     zipf_a: float = 1.1
     id_shift: int = 0        # ids (k + id_shift) mod vocab: moves the hot ids
@@ -181,7 +182,21 @@ def private() -> Workload:
               noise_emb=True, noise_grad=True)
 
 
-ALL = {f.__name__: f for f in (tiny_sync, dense_tabular, ctr, hetero, private)}
+def regression() -> Workload:
+    """Regression with ten-layer MLP bottoms (the paper's bottom model,
+    Section 5 "Models"; its regression sets are scored by RMSE): 1M rows,
+    140 + 140 bf16 features (the width of a blog-feedback-like table), a
+    continuous target from a random teacher; each bottom nine 256-wide ReLU
+    layers and a 64-wide cut layer, top 128->64->1 with a linear output and
+    the mean squared error; batch 4096, s=2, k=2."""
+    return _w(6, name="regression", n_rows=1_000_000, dtype="bf16",
+              A=PartySpec(dense=140, widths=[256] * 9 + [64]),
+              B=PartySpec(dense=140, widths=[256] * 9 + [64]),
+              top=TopSpec(widths=[64, 1]),
+              batch=4096, staleness=2, replicas=2, lr=0.001, labels="regression", loss="mse")
+
+
+ALL = {f.__name__: f for f in (tiny_sync, dense_tabular, ctr, hetero, private, regression)}
 
 
 def get(name: str) -> Workload:
