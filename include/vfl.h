@@ -171,7 +171,7 @@ vfl_status vfl_get_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kin
  * the weights and activations in the group's slot (group mod (s+1)); at most
  * s+1 groups may be in flight (published and not yet back-propagated), else
  * VFL_E_STALE.  With VFL_FIFO_DISCARD the channel instead discards its
- * oldest group (the buffer mechanism of Section 4.2): its embedding when A
+ * oldest group (the buffer mechanism of Section 4.1 "System Design"): its embedding when A
  * has not taken it yet (A then skips that group), else its gradient; either
  * way B drops the group without an update and reuses its slot
  * (VFL_E_STALE remains when A is inside that group's step).  Party A: group
@@ -199,7 +199,7 @@ vfl_status vfl_top_step(vfl_ctx* c, int64_t group, float* loss_dev);
  * goes to B's current parameters and increments B's version. */
 vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group);
 
-/* Waiting deadline (Section 4.2): party A gives up on `group`, the next
+/* Waiting deadline (Section 4.1 "System Design"): party A gives up on `group`, the next
  * group it would consume, before its forward (host-decided, for instance
  * after a deadline on the embedding's event).  A moves on to group + 1; B's
  * backward of the group (vfl_bottom_backward or the tick's vfl_step) then
@@ -295,7 +295,7 @@ vfl_status vfl_state_size(const vfl_ctx* c, size_t* bytes);
 vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes);
 vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes);
 
-/* Planner of the system-planning phase (Section 4.4, Algorithm 2; host
+/* Planner of the system-planning phase (Section 4.3 "System Planning Phase", Algorithm 2; host
  * only, no context).  A party's profile: per-iteration forward and backward
  * delays T = coef * B^exp * w / C of its bottom (Eqs. 7-8) and, for party A,
  * of the top model (Eq. 9; zero coefficients for party B), its total cores
@@ -325,6 +325,15 @@ typedef struct {
  * profiles or when no candidate is feasible. */
 vfl_status vfl_plan(const vfl_plan_party* a, const vfl_plan_party* p, const vfl_plan_link* link,
                     const int32_t* batches, int32_t n_batches, int32_t out[3], double* cost);
+
+/* Fit one delay term T = coef * B^exp of Eqs. 7-9 to n measured pairs
+ * (batch[i], seconds[i]) of a batch-size sweep (host only): exp and
+ * log(coef) minimise sum_i (log T_i - log coef - exp * log B_i)^2, the way
+ * the constants of the Appendix's Table 7 come from measured delays.
+ * VFL_E_INVALID for n < 2, a non-positive or non-finite value, or fewer than
+ * two distinct batch sizes. */
+vfl_status vfl_fit_delay(const double* batch, const double* seconds, int32_t n, double* coef,
+                         double* expo);
 
 /* Synchronise both streams and report the device-side channel checks: the
  * number of times a consumer found a slot header whose group differs from

@@ -1,4 +1,4 @@
-"""Plain exhaustive search of the system-planning phase (Section 4.4,
+"""Plain exhaustive search of the system-planning phase (Section 4.3 "System Planning Phase",
 Algorithm 2).  Test infrastructure only (see ``oracle/__init__.py``).
 
 A party's per-iteration computation delay is the sum of power laws in the
@@ -46,3 +46,18 @@ def plan(a: dict, p: dict, link: dict, batches):
                 if o < best:
                     best, arg = o, (wa, wp, B)
     return None if arg is None else (arg, best)
+
+
+def fit_power_law(batches, seconds):
+    """One delay term of Eqs. 7-9, T = coef * B**exp, fitted to measured
+    (B, T) pairs of a batch-size sweep by least squares on log T against
+    log B (normal equations of the straight line); returns (coef, exp)."""
+    xs = [math.log(b) for b in batches]
+    ys = [math.log(t) for t in seconds]
+    n = len(xs)
+    sx, sy = sum(xs), sum(ys)
+    sxx = sum(x * x for x in xs)
+    sxy = sum(x * y for x, y in zip(xs, ys))
+    expo = (n * sxy - sx * sy) / (n * sxx - sx * sx)
+    coef = math.exp((sy - expo * sx) / n)
+    return coef, expo

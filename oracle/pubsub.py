@@ -274,7 +274,7 @@ class PubSubOracle:
 
         group_rows(g) -> [(start, count)] per replica.  ``snapshot(t)`` says
         whether to copy the parameters after tick t.  ``discard`` maps a
-        group to the channel entry dropped for it (Section 4.2: the buffer
+        group to the channel entry dropped for it (Section 4.1 "System Design": the buffer
         mechanism drops the oldest embedding or gradient of a full channel,
         the waiting deadline a batch whose embedding came too late):
         "emb" -- A never uses the group's embedding, so neither A nor B

@@ -212,7 +212,7 @@ struct vfl_ctx {
   int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
   SlotState aslot;
   float* a_loss = nullptr;
-  // discarded groups (Section 4.2's buffer and waiting-deadline
+  // discarded groups (Section 4.1 "System Design": the buffer and waiting-deadline
   // mechanisms), each until B's backward of it releases its slot without
   // an update; grad: A had consumed the group (B must wait for A's
   // gradient event before reusing the slot)

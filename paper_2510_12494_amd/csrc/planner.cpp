@@ -1,4 +1,4 @@
-// Configuration planner of the system-planning phase (Section 4.4,
+// Configuration planner of the system-planning phase (Section 4.3 "System Planning Phase",
 // Algorithm 2): host code only.
 //
 // Per candidate (workers w_a of party A, workers w_p of party B, batch size
@@ -13,6 +13,10 @@
 // feasible.  Algorithm 2 fills its table over every feasible (w_a, w_p, B),
 // so the search below is that enumeration: batch sizes in the caller's
 // order, then w_a, then w_p, keeping the first strict minimum.
+//
+// The delay constants are fitted from measured times over a batch-size
+// sweep (the Appendix's Table 7 lists the paper's): vfl_fit_delay fits one
+// power law coef * B^exp by least squares in log space.
 #include <cmath>
 #include <limits>
 
@@ -68,6 +72,31 @@ vfl_status vfl_plan(const vfl_plan_party* a, const vfl_plan_party* p, const vfl_
   if (!(best < std::numeric_limits<double>::infinity())) return VFL_E_INVALID;   // nothing feasible
   out[0] = arg[0]; out[1] = arg[1]; out[2] = arg[2];
   if (cost) *cost = best;
+  return VFL_OK;
+}
+
+vfl_status vfl_fit_delay(const double* batch, const double* seconds, int32_t n, double* coef,
+                         double* expo) {
+  if (!batch || !seconds || !coef || !expo || n < 2) return VFL_E_INVALID;
+  // ordinary least squares of log T on log B (centred sums)
+  double mx = 0.0, my = 0.0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!(batch[i] > 0.0) || !(seconds[i] > 0.0) || !std::isfinite(batch[i]) || !std::isfinite(seconds[i]))
+      return VFL_E_INVALID;
+    mx += std::log(batch[i]);
+    my += std::log(seconds[i]);
+  }
+  mx /= n;
+  my /= n;
+  double sxx = 0.0, sxy = 0.0;
+  for (int32_t i = 0; i < n; ++i) {
+    const double dx = std::log(batch[i]) - mx;
+    sxx += dx * dx;
+    sxy += dx * (std::log(seconds[i]) - my);
+  }
+  if (!(sxx > 0.0)) return VFL_E_INVALID;   // a single distinct batch size
+  *expo = sxy / sxx;
+  *coef = std::exp(my - *expo * mx);
   return VFL_OK;
 }
 

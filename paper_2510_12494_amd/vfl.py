@@ -29,7 +29,7 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
-           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan",
+           "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan", "vfl_fit_delay",
            "vfl_last_error", "vfl_destroy")
 KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt")
 
@@ -111,6 +111,8 @@ def _load():
         "vfl_discard": [P, I64],
         "vfl_plan": [C.POINTER(vfl_plan_party), C.POINTER(vfl_plan_party), C.POINTER(vfl_plan_link),
                      C.POINTER(I32), I32, C.POINTER(I32), C.POINTER(C.c_double)],
+        "vfl_fit_delay": [C.POINTER(C.c_double), C.POINTER(C.c_double), I32, C.POINTER(C.c_double),
+                          C.POINTER(C.c_double)],
         "vfl_get_state": [P, P, SZ],
         "vfl_set_state": [P, P, SZ],
         "vfl_destroy": [P],
@@ -253,6 +255,16 @@ def vfl_plan(a: vfl_plan_party, p: vfl_plan_party, link: vfl_plan_link, batches)
     _chk(_lib.vfl_plan(C.byref(a), C.byref(p), C.byref(link), arr, len(batches), out, C.byref(cost)),
          "vfl_plan")
     return (out[0], out[1], out[2]), cost.value
+
+
+def vfl_fit_delay(batches, seconds):
+    """Returns (coef, exp) of T = coef * B**exp fitted to the measured pairs."""
+    n = len(batches)
+    xb = (C.c_double * n)(*batches)
+    xt = (C.c_double * n)(*seconds)
+    coef, expo = C.c_double(0.0), C.c_double(0.0)
+    _chk(_lib.vfl_fit_delay(xb, xt, n, C.byref(coef), C.byref(expo)), "vfl_fit_delay")
+    return coef.value, expo.value
 
 
 def vfl_discard(ctx, group: int):

@@ -27,11 +27,11 @@ def pytest_terminal_summary(terminalreporter):
         return
     tr = terminalreporter
     tr.section("achieved parity errors (worst value / bound)")
-    for (test, q), (v, b) in sorted(H.ERRORS.items()):
-        tr.write_line(f"{test:60s} {q:22s} {v:10.3e} / {b:9.2e}")
+    for (test, q), (v, b, where) in sorted(H.ERRORS.items()):
+        tr.write_line(f"{test:60s} {q:22s} {v:10.3e} / {b:9.2e}  {where}")
     out = os.environ.get("PARITY_ERRORS_JSON")
     if out:
         import json
         with open(out, "w") as fh:
-            json.dump([{"test": t, "quantity": q, "value": v, "bound": b}
-                       for (t, q), (v, b) in sorted(H.ERRORS.items())], fh, indent=1)
+            json.dump([{"test": t, "quantity": q, "value": v, "bound": b, "where": wh}
+                       for (t, q), (v, b, wh) in sorted(H.ERRORS.items())], fh, indent=1)

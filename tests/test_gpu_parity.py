@@ -51,8 +51,8 @@ def _check_messages(run, recs, w):
         for key, tag, grp in (("zhat", "e", "fwd_group"), ("gtilde", "g", "bwd_group")):
             if key in r:
                 ok, f, e = H.message_ok(run.msgs[(tag, r[grp])][0], r[key], tol_elem, frac, l2)
-                H.record(f"{key} bad frac", f, frac)
-                H.record(f"{key} rel L2", e, l2)
+                H.record(f"{key} bad frac", f, frac, f"t{r['tick']}")
+                H.record(f"{key} rel L2", e, l2, f"t{r['tick']}")
                 assert ok, (key, r["tick"], f, e)
 
 
@@ -81,25 +81,26 @@ def _check_params(run, recs, w, per_tick, f64_recs=None):
             g = run.snaps[t][k]
             p0 = run.p0[k].astype(np.float64)
             e = H.rel_inf(g, v)
-            H.record("theta rel", e, tol)
+            H.record("theta rel", e, tol, f"{k} t{t}")
             assert e <= tol, (k, t, e)
             ok, err, bound = H.delta_ok(g, v, p0, dtol, n_upd)
-            H.record("dtheta err/bound", err / bound if bound > 0 else 0.0, 1.0)
+            H.record("dtheta err/bound", err / bound if bound > 0 else 0.0, 1.0, f"{k} t{t}")
             d_ref = np.max(np.abs(v - p0))
             if d_ref > 0:
-                H.record("dtheta rel", err / d_ref, dtol)
+                H.record("dtheta rel", err / d_ref, dtol,
+                         f"{k} t{t} max|dtheta| {d_ref:.2e} ulp {H.ulp32(v):.1e} x {n_upd}")
             assert ok, (k, t, err, bound)
             if t in by_tick64 and "params" in by_tick64[t]:
                 v64 = by_tick64[t]["params"][k]
                 e64 = H.rel_inf(g, v64)
-                H.record("theta rel vs f64", e64, H.BF16_TOL)
+                H.record("theta rel vs f64", e64, H.BF16_TOL, f"{k} t{t}")
                 assert e64 <= H.BF16_TOL, (k, t, e64)
                 d64 = np.max(np.abs(v64 - p0))
                 if d64 > 0:
                     H.record("dtheta rel vs f64 (info)", np.max(np.abs((g - p0) - (v64 - p0))) / d64,
-                             float("inf"))
+                             float("inf"), f"{k} t{t}")
                     H.record("emulation dtheta gap to f64 (info)",
-                             np.max(np.abs((v - p0) - (v64 - p0))) / d64, float("inf"))
+                             np.max(np.abs((v - p0) - (v64 - p0))) / d64, float("inf"), f"{k} t{t}")
 
 
 def _full_check(run, w, per_tick=True, f64=True):
@@ -241,7 +242,7 @@ def test_gradient_probe(name):
         ok, err, bound = H.delta_ok(run.final[k], v, run.p0[k].astype(np.float64), dtol, 1)
         d_ref = np.max(np.abs(v - run.p0[k]))
         if d_ref > 0:
-            H.record("grad rel (lr 1)", err / d_ref, dtol)
+            H.record("grad rel (lr 1)", err / d_ref, dtol, f"{k} max|grad| {d_ref:.2e}")
         assert ok, (k, err, bound)
 
 
@@ -342,7 +343,7 @@ def test_shared_lds_buffers_deep_top():
     ("f32", 1, {0: "grad", 3: "emb", 5: "emb_fifo"}),
 ])
 def test_channel_discards(dtype, s, discard):
-    """The buffer and waiting-deadline mechanisms (Section 4.2): groups whose
+    """The buffer and waiting-deadline mechanisms (Section 4.1 "System Design"): groups whose
     embedding is dropped (A gives up on the group, or a full FIFO channel
     drops it before A takes it) and groups whose gradient is dropped (a full
     channel after A's step).  Per-tick parameters, the losses of the groups

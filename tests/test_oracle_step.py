@@ -178,7 +178,7 @@ def test_equals_history_formulation(s, k, loss):
 @pytest.mark.parametrize("s,discard", [(0, {1: "emb", 3: "grad"}),
                                        (2, {0: "grad", 2: "emb", 3: "emb", 6: "grad"})])
 def test_discards_equal_history_formulation(s, discard):
-    """Dropped embeddings and gradients (Section 4.2): the oracle's ring,
+    """Dropped embeddings and gradients (Section 4.1 "System Design"): the oracle's ring,
     stash and version counter against the history formulation, where B's
     forward of group u takes the version counted from the groups applied
     before it; with clip, noise and tables."""

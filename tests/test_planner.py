@@ -1,4 +1,4 @@
-"""The planner of the system-planning phase (Section 4.4, Algorithm 2):
+"""The planner of the system-planning phase (Section 4.3 "System Planning Phase", Algorithm 2):
 the oracle's exhaustive search pinned by closed forms, the memory bound,
 scaling and symmetry properties, and the library's vfl_plan against the
 oracle on random profiles (host only, no GPU)."""
@@ -114,3 +114,53 @@ def test_library_equals_oracle():
         arg, cost = V.vfl_plan(_lib_party(V, a), _lib_party(V, p), lv, batches)
         assert arg == tuple(int(x) for x in ref[0])
         assert cost == pytest.approx(ref[1], rel=1e-12)
+
+
+# ---------------------------------------------------- delay-model fitting
+def test_fit_recovers_exact_power_laws():
+    """Times that follow coef * B**exp exactly (positive, zero and negative
+    exponents, as in the Appendix's Table 7) give back coef and exp."""
+    B = [16, 32, 64, 128, 256, 512, 1024]
+    for coef, expo in [(0.018, -0.8015), (0.010, -1.0071), (3.5e-6, 1.0), (2.0e-4, 0.0),
+                       (7.0e-9, 1.37)]:
+        T = [coef * b ** expo for b in B]
+        c, e = OP.fit_power_law(B, T)
+        assert c == pytest.approx(coef, rel=1e-12) and e == pytest.approx(expo, abs=1e-12)
+
+
+def test_fit_two_points_is_the_secant():
+    """Two points: the exponent is the slope log(T2/T1) / log(B2/B1) and the
+    line passes through both."""
+    c, e = OP.fit_power_law([100.0, 400.0], [2.0, 5.0])
+    assert e == pytest.approx(math.log(2.5) / math.log(4.0), rel=1e-14)
+    assert c * 100.0 ** e == pytest.approx(2.0, rel=1e-13)
+
+
+def test_fit_minimises_the_log_residuals():
+    """Noisy times: the fitted line has zero mean log residual and residuals
+    orthogonal to log B (the normal equations), and moving either constant
+    raises the squared residual."""
+    rng = np.random.default_rng(3)
+    B = np.array([16, 32, 64, 128, 256, 512, 1024], float)
+    T = 0.02 * B ** -0.7 * np.exp(rng.normal(0, 0.1, B.size))
+    c, e = OP.fit_power_law(B, T)
+    r = np.log(T) - np.log(c) - e * np.log(B)
+    assert abs(r.sum()) < 1e-12 and abs((r * np.log(B)).sum()) < 1e-11
+    sse = lambda cc, ee: float(((np.log(T) - np.log(cc) - ee * np.log(B)) ** 2).sum())
+    for dc, de in [(1.01, 0), (0.99, 0), (1, 0.01), (1, -0.01)]:
+        assert sse(c * dc, e + de) > sse(c, e)
+
+
+def test_library_fit_equals_oracle():
+    from paper_2510_12494_amd import vfl as V
+    rng = np.random.default_rng(11)
+    for _ in range(50):
+        n = int(rng.integers(2, 12))
+        B = np.sort(rng.choice(np.arange(1, 40000), n, replace=False)).astype(float)
+        T = np.exp(rng.normal(-8, 2)) * B ** rng.normal(0, 1) * np.exp(rng.normal(0, 0.2, n))
+        c1, e1 = OP.fit_power_law(B, T)
+        c2, e2 = V.vfl_fit_delay(list(B), list(T))
+        assert c2 == pytest.approx(c1, rel=1e-9) and e2 == pytest.approx(e1, rel=1e-9, abs=1e-12)
+    for bad in ([1.0], [2.0, 2.0], [0.0, 3.0]):
+        with pytest.raises(V.VflError):
+            V.vfl_fit_delay(bad, [1.0] * len(bad))

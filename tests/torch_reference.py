@@ -12,7 +12,7 @@ clipped and noised; B's gradient is the vector-Jacobian product of its
 embedding at the delayed version with that message / R; every party takes
 one SGD step (Eq. 2).
 
-Dropped channel entries (Section 4.2): for a group whose embedding is
+Dropped channel entries (Section 4.1 "System Design"): for a group whose embedding is
 dropped nothing is computed; for one whose gradient is dropped A and the top
 model step and B does not.  B's version for the forward of group u is then
 the number of B updates applied by the groups g < u - s.
