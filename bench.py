@@ -61,7 +61,7 @@ KERNEL_SOURCES = {
     "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dw32<"), ["dw.hip"]),
     "dwt": (("k_dwt(",), ["dw.hip"]),
     "reduce": (("k_dw_reduce<",), ["dw.hip"]), "cast": (("k_cast<",), ["rowops.hip"]),
-    "emb_sgd": (("k_embed_sgd",), ["embed.hip"]), "gemm": (("k_gemm",), ["gemm.hip"]),
+    "emb_sgd": (("k_embed_sgd",), ["embed.hip"]), "gemm": (("k_lin(",), ["lin.hip"]),
 }
 
 

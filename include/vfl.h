@@ -359,9 +359,7 @@ typedef enum {
   VFL_K_EMB_SGD = 6,    /* sorted sparse SGD of the tables */
   VFL_K_GEMM = 7,       /* layer products of party B's wide layers (input gradient) */
   VFL_K_DWT = 8,        /* large-tile bf16 weight-gradient products (partials + SGD) */
-  VFL_K_LINF = 9,       /* layer products of party B's wide layers (forward) */
-  VFL_K_RC = 10,        /* row-chunked copy of party B's wide input */
-  VFL_K_COUNT = 11
+  VFL_K_COUNT = 9
 } vfl_kernel_class;
 
 /* Measurement hook: while class_mask is non-zero, every launch of a
@@ -371,8 +369,8 @@ typedef enum {
  * vfl_timing_read then reports those of the last replay.  vfl_timing_read
  * synchronises both streams and returns, for one class, the summed kernel
  * durations in milliseconds, the number of launches and the summed
- * algorithmic work (matrix-product FLOPs for VFL_K_FWD .. VFL_K_DW, VFL_K_GEMM,
- * VFL_K_DWT and VFL_K_LINF, bytes
+ * algorithmic work (matrix-product FLOPs for VFL_K_FWD .. VFL_K_DW, VFL_K_GEMM
+ * and VFL_K_DWT, bytes
  * that the kernel must move at minimum for the others); then it resets that class.
  * Enabling with mask 0 stops recording. */
 vfl_status vfl_timing_enable(vfl_ctx* c, uint32_t class_mask);

@@ -8,8 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libvfl.so")
-SOURCES = ["chain.hip", "dw.hip", "gemm.hip", "lin.hip", "rowops.hip", "embed.hip", "api.cpp", "schedule.cpp",
-           "planner.cpp"]
+SOURCES = ["chain.hip", "dw.hip", "lin.hip", "rowops.hip", "embed.hip", "api.cpp", "schedule.cpp", "planner.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -153,18 +153,12 @@ struct Plan {
   size_t hdr = 0;                     // int32 [2][kMaxSlots][4] + error counter
   size_t tsrc = 0;                    // TickSrc of the replayed graphs
   size_t job_fwd = 0, job_act = 0, job_bwd = 0, job_dwa = 0, job_dwb = 0;
-  // party B's wide layers (first layer at least kGemmMinWidth wide, bf16,
-  // no tables): every layer but the last runs as a large-tile layer product
-  // that writes its output row-major to arm[l] (the next product's input)
-  // and, below layer L-2, in the RC layout; the chain kernel runs layer L-1
-  // from arm[L-2] and publishes.  Layer 1's input gradient is a layer
-  // product too: the backward chain stops at layer 2 and writes its last
-  // delta row-major to d1rm.  LinJob [slot][L]: the forward products of
-  // layers 0 .. L-2, then the input gradient at index L-1.
+  // party B's layer-1 input gradient as a large-tile layer product (wide
+  // first layer): the backward chain stops at layer 2 and writes its last
+  // delta row-major to d1rm; LinJob per slot
   bool bgemm = false;
   size_t d1rm = 0, job_lin = 0;
-  size_t arm[VFL_MAX_LAYERS]{};
-  int lin_blocks_fwd[VFL_MAX_LAYERS]{}, lin_blocks_dx = 0;
+  int lin_blocks_dx = 0;
   KMeta kf, ka, kb;
   FwdLds lf;
   ActLds la;
@@ -326,14 +320,9 @@ void plan_fwd_lds(const Plan& p, int BR, FwdLds& f) {
   l.KS = p.e == BF16 ? 32 : 16;
   l.BR = BR;
   // layer l reads buf[l % 2] and writes buf[(l + 1) % 2]; the input is in
-  // buf[0]: each buffer is as wide as the widest tensor it holds (wide
-  // layers: the chain runs the last layer only, from layer L-2's output)
+  // buf[0]: each buffer is as wide as the widest tensor it holds
   int w[2] = {p.P.din, 1};
   for (int i = 0; i < p.P.L; ++i) w[(i + 1) % 2] = std::max(w[(i + 1) % 2], p.P.out[i]);
-  if (p.bgemm) {
-    w[0] = p.P.out[p.P.L - 2];
-    w[1] = p.P.out[p.P.L - 1];
-  }
   const int es = elt_size(p.e);
   f.buf[0] = l.take(w[0], es);
   f.buf[1] = l.take(w[1], es);
@@ -545,10 +534,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   // chain's LDS), no tables, bf16: layer 1's input gradient is a layer
   // product over the whole group
   p.bgemm = p.e == BF16 && p.P.L >= 2 && p.P.spec.n_cat == 0 && p.P.out[0] >= kGemmMinWidth;
-  if (p.bgemm) {
-    p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
-    for (int l = 0; l + 1 < p.P.L; ++l) p.arm[l] = ly.take((size_t)es * R * ld_of(p.P.out[l]));
-  }
+  if (p.bgemm) p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
 
   Top& T = p.T;
   T.spec = *t;
@@ -625,8 +611,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.job_dwa = ly.take(sizeof(DwJob));
   p.job_dwb = ly.take(sizeof(DwJob) * (p.s + 1));
   if (p.bgemm) {
-    p.job_lin = ly.take(sizeof(LinJob) * (p.s + 1) * p.P.L);
-    for (int l = 0; l + 1 < p.P.L; ++l) p.lin_blocks_fwd[l] = lin_blocks(p.Ra, p.P.out[l]);
+    p.job_lin = ly.take(sizeof(LinJob) * (p.s + 1));
     p.lin_blocks_dx = lin_blocks(p.Ra, p.P.out[0]);
   }
   p.total = (ly.off + 255) / 256 * 256;
@@ -681,7 +666,7 @@ struct Jobs {
   std::vector<BwdJob> bj;
   std::vector<DwJob> dwb;
   DwJob dwa;
-  std::vector<LinJob> lin;            // party B's wide-layer products [slot][L] (bgemm)
+  std::vector<LinJob> lin;            // party B's layer-1 input gradient per slot (bgemm)
 };
 
 // The job descriptors of every slot for a workspace at `ws` (host only;
@@ -700,7 +685,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
   J.bj.assign(S1, BwdJob());
   J.dwb.assign(S1, DwJob());
   J.dwa = DwJob();
-  J.lin.assign(p.bgemm ? S1 * P.L : 0, LinJob());
+  J.lin.assign(p.bgemm ? S1 : 0, LinJob());
   std::vector<FwdJob>& fj = J.fj;
   std::vector<ActiveJob>& aj = J.aj;
   std::vector<BwdJob>& bj = J.bj;
@@ -740,34 +725,6 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     f.norm = P.norm[q] ? at_f(P.norm[q]) : nullptr;
     f.cfac = P.cfac[q] ? at_f(P.cfac[q]) : nullptr;
     f.hdr_out = hdrp(0, q);
-    if (p.bgemm) {
-      // wide layers: the chain runs layer L-1 from layer L-2's row-major
-      // output (the tick's rows in the workspace) and writes its RC copy
-      const int lc = P.L - 1;
-      f.in = RowInput();
-      f.in.dense_in = P.out[lc - 1];
-      f.in.dense_vec = 1;
-      f.in.tick_rows = 1;
-      f.in.buf = p.lf.buf[0];
-      f.in.rc = rcm(c, P.arc[q][lc - 1], P.out[lc - 1]);
-      f.warm.p[0] = c->ws + P.Wq[q][lc];
-      f.warm.lines[0] = (int32_t)((P.wq_end[q] - P.Wq[q][lc]) / 128);
-      f.L = 1;
-      f.l[0] = layer(c->ws + P.Wq[q][lc], P.kq[lc], p.lf.bias.off + 4 * P.bo[lc], P.out[lc], P.in[lc],
-                     P.relu[lc], p.lf.buf[0], p.lf.buf[1]);
-      for (int l = 0; l < lc; ++l) {
-        LinJob& g = J.lin[q * P.L + l];
-        g.A = l == 0 ? nullptr : ws + p.arm[l - 1];
-        g.lda = l == 0 ? 0 : ld_of(P.out[l - 1]);
-        g.W = c->ws + P.Wq[q][l]; g.kst = P.kq[l];
-        g.N = P.out[l]; g.K = P.in[l];
-        g.bias = at_f(P.b[l]); g.relu = P.relu[l];
-        g.out_rm = ws + p.arm[l]; g.ldo = (int32_t)ld_of(P.out[l]);
-        if (l + 1 < lc) g.out_rc = rcm(c, P.arc[q][l], P.out[l]);
-        g.tiles_n = (g.N + 255) / 256; g.tiles_m = (p.Ra + 255) / 256;
-        g.rows_pad = p.Ra;
-      }
-    }
 
     // party A's step against embedding slot q
     ActiveJob& a = aj[q];
@@ -876,7 +833,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       // layer 1's input gradient over the group: the chain's last delta
       // (row-major) times the stashed W1, masked by the stashed layer-0 output
       b.drm = ws + p.d1rm; b.lddrm = (int32_t)ld_of(P.out[1]);
-      LinJob& g = J.lin[q * P.L + P.L - 1];
+      LinJob& g = J.lin[q];
       g.A = ws + p.d1rm; g.lda = ld_of(P.out[1]);
       g.W = c->ws + P.Wtq[q][1]; g.kst = P.kt[1];
       g.N = P.out[0]; g.K = P.out[1];
@@ -1189,29 +1146,9 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, Ti
 // B's forward + publish of `st` (group st.group) into `slot`.
 vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, TickRef tr) {
   const Plan& p = c->p;
-  const Party& P = p.P;
   const int32_t hdr[3] = {(int32_t)st.group, (int32_t)st.group, (int32_t)st.version};
-  ChainCall k = call_of(st, st.group, hdr, 0);
-  double chain_flops = party_fwd_flops(P, p.R);
-  if (p.bgemm) {
-    // wide layers: the input's RC copy (first layer's weight gradient), the
-    // products of layers 0 .. L-2, then the chain from layer L-2's output
-    RCMat x0;
-    x0.p = c->ws + P.x0rc[slot]; x0.cp = (int32_t)ld_of(P.din); x0.rows = p.Ra;
-    TIMED(VFL_K_RC, 4.0 * (double)p.R * x0.cp, c->sb,
-          launch_rows_rc(st.dense, st.ld, P.din, x0, st.rows, p.Ra, tr, c->sb));
-    const LinJob* lj = (const LinJob*)(c->ws + p.job_lin) + slot * P.L;
-    for (int l = 0; l + 1 < P.L; ++l) {
-      const double f = mm_flops(p.R, P.out[l], P.in[l]);
-      TIMED(VFL_K_LINF, f, c->sb,
-            launch_lin(lj + l, p.lin_blocks_fwd[l], l == 0 ? st.dense : nullptr, l == 0 ? st.ld : 0, st.rows, tr,
-                       c->sb));
-      chain_flops -= f;
-    }
-    k.dense = c->ws + p.arm[P.L - 2];
-    k.ld = ld_of(P.out[P.L - 2]);
-  }
-  TIMED(VFL_K_FWD, chain_flops, c->sb,
+  const ChainCall k = call_of(st, st.group, hdr, 0);
+  TIMED(VFL_K_FWD, party_fwd_flops(p.P, p.R), c->sb,
         launch_fwd(p.e, p.kf.rt, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k, tr, c->sb));
   return VFL_OK;
 }
@@ -1261,8 +1198,7 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
         launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
   if (p.bgemm)
     TIMED(VFL_K_GEMM, gf, c->sb,
-          launch_lin((const LinJob*)(c->ws + p.job_lin) + slot * p.P.L + p.P.L - 1, p.lin_blocks_dx, nullptr, 0,
-                     st.rows, tr, c->sb));
+          launch_lin((const LinJob*)(c->ws + p.job_lin) + slot, p.lin_blocks_dx, st.rows, tr, c->sb));
   vfl_status r = enqueue_dw(c, false, slot, st.rows, nullptr, tr, c->sb);
   if (r) return r;
   return enqueue_table_sgd(c, p.P, slot, st.rows, c->o.lr / (float)st.rows, c->sb, tr);

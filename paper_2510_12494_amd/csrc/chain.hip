@@ -475,12 +475,11 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
       idt[(int64_t)f * in.ldi + r0 + r] = src[u];
     }
   }
-  const int64_t in_off = in.tick_rows ? 0 : k.in_off;
   for (int u = threadIdx.x; u < BR * nch; u += kNT) {
     const int r = u / nch, ch = u % nch, c0 = ch * CE;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (r < rv && c0 < din) {
-      const int64_t row = in_off + r0 + r;
+      const int64_t row = k.in_off + r0 + r;
       if (c0 >= ne && in.dense_vec && (ne % CE) == 0) {
         v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (c0 - ne)), din - c0);
       } else if (c0 + CE <= ne && (in.E % CE) == 0) {
@@ -1060,8 +1059,7 @@ hipError_t chain_init() {
       raise_lds(k_bwd<uint16_t, 3>), raise_lds(k_bwd<float, 3>)};
   for (hipError_t x : r)
     if (x != hipSuccess) return x;
-  const hipError_t g = gemm_init();
-  return g != hipSuccess ? g : lin_init();
+  return lin_init();
 }
 
 }  // namespace vfl

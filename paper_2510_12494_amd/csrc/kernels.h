@@ -151,8 +151,6 @@ struct WarmSet {
 struct RowInput {
   int32_t dense_in = 0, n_cat = 0, V = 0, E = 0;
   int32_t dense_vec = 0;              // dense rows 16-byte aligned: vector loads
-  int32_t tick_rows = 0;              // dense holds the tick's rows (a workspace buffer),
-                                      // not a dataset base
   const float* T = nullptr;
   int32_t* idt = nullptr; int32_t ldi = 0;
   LBuf buf;
@@ -323,53 +321,24 @@ hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float sc
                             float* loss_out, TickRef tr, float* loss_base, hipStream_t st);
 
 // ---------------------------------------------------------- layer products
-// The input gradient of one wide bottom layer over the rows of a group
-// (bf16): out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k] for r < rows
-// (mask_rc null: no mask), into out_rc (rows from the group's end up to
-// rows_pad zero).  A: row-major, lda elements per row, zero from K up to
-// the next multiple of 8; W packed (pk_index, kst 32-k steps).  Blocks:
-// gemm_tiles(rows_pad, N): tiles_m x tiles_n tiles of 256 x 128 outputs,
-// rounded up to a multiple of 8 (one contiguous range per XCD).
-struct GemmJob {
-  const void* A = nullptr; int64_t lda = 0;     // workspace operand (a launch may pass its own)
-  const void* W = nullptr; int32_t kst = 0;
-  int32_t N = 0, K = 0;
-  RCMat out_rc, mask_rc;
-  int32_t tiles_n = 0, tiles_m = 0, rows_pad = 0;
-};
-int gemm_tiles(int rows, int N);
-hipError_t gemm_init();
-hipError_t launch_gemm(const GemmJob* job, int blocks, const void* A, int64_t lda, int rows, TickRef tr,
-                       hipStream_t st);
-
-// The products of party B's wide bottom layers (bf16), large tiles:
-//   forward (bias set):  out[r][n] = relu?(sum_k A[r][k] W[n][k] + bias[n]),
-//                        to out_rm (row-major, ldo) and/or out_rc;
-//   input gradient:      out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k]
-//                        (mask_rc null: no mask), to out_rc.
+// The input gradient of a wide bottom layer of party B over the rows of a
+// group (bf16), in large tiles:
+//   out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k]   (mask_rc null: no mask)
+// for r < rows, into out_rc (rows from the group's end up to rows_pad zero).
 // A: row-major bf16, lda elements per row (a multiple of 8; finite values
 // from K up to lda); W: packed [N x K] (pk_index, kst 32-k steps, zero past
-// K).  RC rows of the output from the group's end up to rows_pad are
-// written as zeros.  Blocks: lin_blocks(rows_pad, N): 256 x 256 output
-// tiles rounded up to a multiple of the 8 XCDs.
+// K).  Blocks: lin_blocks(rows_pad, N): 256 x 256 output tiles rounded up
+// to a multiple of the 8 XCDs.
 struct LinJob {
-  const void* A = nullptr; int64_t lda = 0;     // workspace operand (a launch may pass its own)
+  const void* A = nullptr; int64_t lda = 0;
   const void* W = nullptr; int32_t kst = 0;
   int32_t N = 0, K = 0;
-  const float* bias = nullptr; int32_t relu = 0;
-  void* out_rm = nullptr; int32_t ldo = 0;
   RCMat out_rc, mask_rc;
   int32_t tiles_n = 0, tiles_m = 0, rows_pad = 0;
 };
 int lin_blocks(int rows_pad, int N);
 hipError_t lin_init();
-// RC copy `out` (cp >= K) of a row-major bf16 input [rows x K] (A and tr as
-// for launch_lin's A operand); rows from `rows` up to rows_pad and columns
-// from K are zeros.
-hipError_t launch_rows_rc(const void* A, int64_t lda, int K, RCMat out, int rows, int rows_pad, TickRef tr,
-                          hipStream_t st);
-hipError_t launch_lin(const LinJob* job, int blocks, const void* A, int64_t lda, int rows, TickRef tr,
-                      hipStream_t st);
+hipError_t launch_lin(const LinJob* job, int blocks, int rows, TickRef tr, hipStream_t st);
 
 // ---------------------------------------------------------------- others
 // Operand copies of one layer's float32 weight W [out x in], element type

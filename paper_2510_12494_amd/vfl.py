@@ -31,7 +31,7 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
            "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan", "vfl_fit_delay",
            "vfl_last_error", "vfl_destroy")
-KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt", "linf", "rc")
+KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt")
 
 
 class vfl_plan_party(C.Structure):
