@@ -286,10 +286,9 @@ bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
   return true;
 }
 
-// output tiles of a weight gradient [N x K]: square tiles of 32 or 64, or
-// 256 x 128 (tile == 256, the large-tile kernel)
+// output tiles of a weight gradient [N x K]: square tiles of 32, 64 or 256
+// (tile == 256: the large-tile kernel)
 int dw_tiles(int N, int K, int tile = 64) {
-  if (tile == 256) return ((N + 255) / 256) * ((K + 127) / 128);
   return ((N + tile - 1) / tile) * ((K + tile - 1) / tile);
 }
 
@@ -312,6 +311,12 @@ void dw_split(int R, int tiles, bool bf16, DwMeta& m) {
   const int s = std::min(max_splits, std::max(1, kDwBlocks / tiles));
   m.rps = ((R + s - 1) / s + gran - 1) / gran * gran;
   m.splits = (R + m.rps - 1) / m.rps;
+  if (m.tile == 256 && m.splits < 2) {
+    // the large-tile kernel writes partials only: two chunks of a multiple
+    // of its 32-row stage
+    m.rps = ((R + 1) / 2 + 31) / 32 * 32;
+    m.splits = 2;
+  }
 }
 
 // LDS layouts at BR rows per block (bytes in .bytes)
@@ -1122,7 +1127,7 @@ vfl_status enqueue_dw(vfl_ctx* c, bool party_a, int slot, int R, float* loss, Ti
                       tr.src ? loss : nullptr, st));
     return VFL_OK;
   }
-  if (m.tile == 256) TIMED(VFL_K_DWT, flops, st, launch_dwt(job, m.blocks, scale, tr, st));
+  if (m.tile == 256) TIMED(VFL_K_DWT, flops, st, launch_dwt(job, m.blocks, st));
   else TIMED(VFL_K_DW, flops, st, launch_dw(p.e, job, m.blocks, R, scale, tr, st));
   const int blocks = m.red_blocks + (party_a ? m.logit_blocks : 0);
   if (blocks > 0) {

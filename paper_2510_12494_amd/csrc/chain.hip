@@ -1059,7 +1059,8 @@ hipError_t chain_init() {
       raise_lds(k_bwd<uint16_t, 3>), raise_lds(k_bwd<float, 3>)};
   for (hipError_t x : r)
     if (x != hipSuccess) return x;
-  return lin_init();
+  const hipError_t d = dwt_init();
+  return d != hipSuccess ? d : lin_init();
 }
 
 }  // namespace vfl

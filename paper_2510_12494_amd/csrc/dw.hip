@@ -218,31 +218,44 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
 }
 
 // Large-tile weight gradient for bf16 operands and long groups: a block of
-// 256 threads owns a kDwtN x kDwtK (256 x 128) output tile and one row
-// chunk.  Rows go through LDS in stages of 64 (8 row groups of 16-byte
-// chunks, the D columns of the tile then its X columns, as laid out in
-// global memory, so every load instruction of a wavefront is contiguous);
-// the next stage's loads are in flight while the current stage is
-// multiplied, and one barrier per stage separates the two LDS buffers.
-// Wavefront (wn, wk) of the 2 x 2 grid computes 128 x 64 of the tile with
-// v_mfma_f32_32x32x16_bf16: X fragments as the A operand (32 inputs x 16
-// rows), D fragments as the B operand (16 rows x 32 outputs), so a lane
-// accumulates four runs of four consecutive inputs k of one output n.
-// The bias gradient is summed from the D fragments of the wavefronts with
-// wk == 0 in the tiles at k0 == 0.  Partials and the unsplit SGD are as in
-// k_dw (same DwProb fields; tiles counted 256 x 128).
-constexpr int kDwtN = 256, kDwtK = 128;
-constexpr int kDwtStageRows = 64;
-constexpr int kDwtGroups = kDwtStageRows / 8;                     // row groups per stage
-constexpr int kDwtChunks = kDwtGroups * (kDwtN + kDwtK);          // 16-byte chunks per stage
-constexpr int kDwtLoads = kDwtChunks / 256;                       // per thread and stage
-constexpr int kDwtPad = 4;   // chunks of padding per LDS row group (the two half-wavefronts of a
-                             // fragment read then start on different banks)
+// 256 threads owns a kDwtN x kDwtK (256 x 256) output tile of one problem
+// and one row chunk.  Rows go through LDS in stages of 32 (four 32 KB
+// buffers, three stages in flight, one barrier per stage), copied from
+// global memory straight into LDS (global_load_lds_dwordx4) in the order
+// the matrix cores read them: one 1 KB block per 32 x 16 operand fragment of
+// v_mfma_f32_32x32x16_bf16, which in the row-chunked layout is 32
+// consecutive chunks (columns) of one 8-row group for each half-wavefront.
+// Waves 0 and 1 copy the X fragments (32-input slabs 0-3 and 4-7), waves 2
+// and 3 the D fragments.  Wavefront (wn, wk) of the 2 x 2 grid computes 128
+// outputs x 128 inputs: X fragments as the A operand (32 inputs x 16 rows),
+// D fragments as the B operand (16 rows x 32 outputs), so a lane
+// accumulates four runs of four consecutive inputs k of one output n; per
+// 16-row step 4 X and 4 D fragments feed 16 MFMAs, with the next step's
+// fragment reads issued between them.  The bias gradient is summed from the
+// D fragments of the wavefronts with wk == 0 in the tiles at k0 == 0 (one
+// v_dot2_f32_bf16 against (1, 1) per two rows).  The row chunks always
+// write float32 partials (as k_dw's split problems; tiles counted 256 x
+// 256): k_dw_reduce sums them and makes the SGD step.
+constexpr int kDwtN = 256, kDwtK = 256;
+constexpr int kDwtStageRows = 32;
+constexpr int kDwtFrag = 1024;                              // one 32 x 16 bf16 fragment
+constexpr int kDwtStageBytes = 2 * (kDwtN / 32) * 2 * kDwtFrag;   // 16 X + 16 D fragments
+constexpr int kDwtBufs = 4;                                 // three stages in flight
+constexpr int kDwtLds = kDwtBufs * kDwtStageBytes;
 
-__global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp, float scale_arg, TickRef tr) {
+typedef __attribute__((address_space(3))) void lds_void;
+
+// wait until at most n (0, 8 or 16) of this wave's vector-memory operations
+// are outstanding (expcnt and lgkmcnt unconstrained)
+__device__ __forceinline__ void wait_vm(int n) {
+  if (n >= 16) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4));
+  else if (n >= 8) __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4) | 8);
+  else __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4));
+}
+
+__global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp) {
   typedef __attribute__((ext_vector_type(16))) float f32x16;
-  constexpr int WN = kDwtN / 2, NB = WN / 32, KB = 2;
-  __shared__ u32x4 lds[2][kDwtGroups][kDwtN + kDwtK + kDwtPad];
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
   const DwJob& J = *jp;
   int q = 0;
 #pragma unroll 1
@@ -252,83 +265,64 @@ __global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp, float
   const int tiles_k = (P.K + kDwtK - 1) / kDwtK;
   const int tile = lb / P.splits, split = lb % P.splits;
   const int n0 = (tile / tiles_k) * kDwtN, k0 = (tile % tiles_k) * kDwtK;
-  float scale = scale_arg;
-  if (tr.src) scale = tick_args(tr).scale;
-  const int rb = split * P.rps;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wn = wave >> 1, wk = wave & 1;
+  const int col = lane & 31, hi = lane >> 5;
   const int N = P.N, K = P.K;
   const bool do_bias = k0 == 0 && wk == 0;
-  const VFL_GLOBAL char* Dp = glb((const char*)P.D.p);
-  const VFL_GLOBAL char* Xp = glb((const char*)P.X.p);
-  const int64_t dcp = P.D.cp, xcp = P.X.cp;
 
-  // this thread's chunks of a stage: chunk c = i * 256 + t -> row group
-  // c / (N + K tile), column j; columns clamped into the operands (their
-  // outputs are discarded)
-  int64_t coff[kDwtLoads];
-  bool isd[kDwtLoads];
-  int rgi[kDwtLoads];
+  // the lane's source column of the four slabs this wave copies (clamped
+  // into the operand: those outputs are discarded); the chunk of 16-row
+  // step k16 of stage s is 8-row group rb / 8 + 4 s + 2 k16 + hi
+  const bool copies_x = wave < 2;
+  const int wq = copies_x ? wave : wave - 2;
+  const VFL_GLOBAL char* base = glb((const char*)(copies_x ? P.X.p : P.D.p));
+  const int64_t unit = (int64_t)(copies_x ? P.X.cp : P.D.cp) * 16;   // bytes per 8-row group
+  const int lim = copies_x ? K - 1 : N - 1;
+  const int c0 = copies_x ? k0 : n0;
+  const VFL_GLOBAL char* src[4];
 #pragma unroll
-  for (int i = 0; i < kDwtLoads; ++i) {
-    const int c = i * 256 + t;
-    const int rg = c / (kDwtN + kDwtK), j = c % (kDwtN + kDwtK);
-    rgi[i] = rg;
-    isd[i] = j < kDwtN;
-    coff[i] = isd[i] ? (int64_t)min(n0 + j, N - 1) * 16 : (int64_t)min(k0 + j - kDwtN, K - 1) * 16;
-  }
-  u32x4 stg[kDwtLoads];
-  auto gload = [&](int st) {
-    const int64_t rg0 = (int64_t)(rb + st * kDwtStageRows) / 8;
+  for (int s4 = 0; s4 < 4; ++s4) src[s4] = base + (int64_t)min(c0 + 32 * (4 * wq + s4) + col, lim) * 16;
+  const int64_t rg0 = (int64_t)split * P.rps / 8;
+  auto issue = [&](int s) {
+    char* dst = smem + (s % kDwtBufs) * kDwtStageBytes + (copies_x ? 0 : kDwtStageBytes / 2) + wq * 8 * kDwtFrag;
 #pragma unroll
-    for (int i = 0; i < kDwtLoads; ++i) {
-      const int64_t rg = rg0 + rgi[i];
-      const VFL_GLOBAL char* a = isd[i] ? Dp + rg * dcp * 16 + coff[i] : Xp + rg * xcp * 16 + coff[i];
-      stg[i] = *(const VFL_GLOBAL u32x4*)a;
-    }
-  };
-  auto lstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < kDwtLoads; ++i) {
-      const int c = i * 256 + t;
-      lds[b][rgi[i]][c - rgi[i] * (kDwtN + kDwtK)] = stg[i];
+    for (int i = 0; i < 8; ++i) {
+      const int s4 = i >> 1, k16 = i & 1;
+      __builtin_amdgcn_global_load_lds((VFL_GLOBAL void*)(src[s4] + (rg0 + 4 * s + 2 * k16 + hi) * unit),
+                                       (lds_void*)(dst + i * kDwtFrag), 16, 0, 0);
     }
   };
 
-  f32x16 acc[KB][NB];
+  f32x16 acc[4][4];
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb)
+  for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[kb][nb][e] = 0.f;
-  float bsum[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) bsum[nb] = 0.f;
-
-  const int half = lane >> 5, col = lane & 31;
+  float bsum[4] = {0.f, 0.f, 0.f, 0.f};
   const bf16x2 kOnes2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);
-  // one 16-row step: the fragments of step ks + 1 are read before the
-  // products of step ks are issued, so LDS latency hides behind the MFMAs
-  auto frags = [&](int b, int ks, u32x4 (&xa)[KB], u32x4 (&db)[NB]) {
-    const u32x4* row = &lds[b][2 * ks + half][0];
+
+  auto frags = [&](const char* S, int k16, u32x4 (&xa)[4], u32x4 (&db)[4]) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) xa[kb] = row[kDwtN + wk * 64 + kb * 32 + col];
+    for (int kb = 0; kb < 4; ++kb) xa[kb] = *(const u32x4*)(S + ((4 * wk + kb) * 2 + k16) * kDwtFrag + lane * 16);
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) db[nb] = row[wn * WN + nb * 32 + col];
+    for (int nb = 0; nb < 4; ++nb)
+      db[nb] = *(const u32x4*)(S + kDwtStageBytes / 2 + ((4 * wn + nb) * 2 + k16) * kDwtFrag + lane * 16);
   };
-  auto mma = [&](const u32x4 (&xa)[KB], const u32x4 (&db)[NB]) {
+  auto mma = [&](const u32x4 (&xa)[4], const u32x4 (&db)[4]) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+      for (int nb = 0; nb < 4; ++nb)
         acc[kb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8, xa[kb]), __builtin_bit_cast(bf16x8, db[nb]), acc[kb][nb], 0, 0, 0);
-    // bias sums in every wavefront (no branch between the steps), kept only
-    // where do_bias: one v_dot2_f32_bf16 against (1, 1) per two rows
+  };
+  auto bias_sums = [&](const u32x4 (&db)[4]) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < 4; ++nb) {
       const bf16x8 v = __builtin_bit_cast(bf16x8, db[nb]);
       bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), kOnes2, bsum[nb], false);
       bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), kOnes2, bsum[nb], false);
@@ -336,68 +330,68 @@ __global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp, float
       bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), kOnes2, bsum[nb], false);
     }
   };
-  auto compute = [&](int b) {
-    constexpr int NKS = kDwtStageRows / 16;
-    u32x4 xa0[KB], db0[NB], xa1[KB], db1[NB];
-    frags(b, 0, xa0, db0);
+  auto interleave = [] {
 #pragma unroll
-    for (int ks = 0; ks < NKS; ks += 2) {
-      frags(b, ks + 1, xa1, db1);
-      mma(xa0, db0);
-      if (ks + 2 < NKS) frags(b, ks + 2, xa0, db0);
-      mma(xa1, db1);
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
   };
 
-  // stages: the chunk is contracted whole (rps rows, a multiple of the
-  // stage; the delta rows past the group are zero).  The last iteration
-  // reloads the last stage (unconditional loads, never used).
+  // the chunk is contracted whole (rps rows, a multiple of the stage; the
+  // delta rows past the group are zero)
   const int nst = P.rps / kDwtStageRows;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  for (int s = 0; s < kDwtBufs - 1 && s < nst; ++s) issue(s);
 #pragma unroll 1
-  for (int st = 0; st < nst; ++st) {
-    gload(min(st + 1, nst - 1));
-    compute(st & 1);
-    lstore((st + 1) & 1);
-    __syncthreads();
+  for (int s = 0; s < nst; ++s) {
+    // this wave's copies of stage s have landed; after the (unfenced)
+    // barrier every wave's have, and every wave is done with stage s - 1
+    wait_vm(8 * min(kDwtBufs - 2, nst - 1 - s));
+    __builtin_amdgcn_s_barrier();
+    if (s + kDwtBufs - 1 < nst) issue(s + kDwtBufs - 1);
+    const char* S = smem + (s % kDwtBufs) * kDwtStageBytes;
+    u32x4 xa0[4], db0[4], xa1[4], db1[4];
+    frags(S, 0, xa0, db0);
+    frags(S, 1, xa1, db1);
+    mma(xa0, db0);
+    interleave();
+    mma(xa1, db1);
+    if (do_bias) {
+      bias_sums(db0);
+      bias_sums(db1);
+    }
   }
 
   if (do_bias) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) bsum[nb] += __shfl_xor(bsum[nb], 32, 64);
-    if (half == 0) {
+    for (int nb = 0; nb < 4; ++nb) bsum[nb] += __shfl_xor(bsum[nb], 32, 64);
+    if (hi == 0) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int n = n0 + wn * WN + nb * 32 + col;
-        if (n >= N) continue;
-        if (P.splits == 1) glb(P.bias)[n] -= scale * bsum[nb];
-        else glb(P.partb)[(int64_t)split * N + n] = bsum[nb];
+      for (int nb = 0; nb < 4; ++nb) {
+        const int n = n0 + 128 * wn + 32 * nb + col;
+        if (n < N) glb(P.partb)[(int64_t)split * N + n] = bsum[nb];
       }
     }
   }
-  // lane: output n = n0 + wn * WN + nb * 32 + col, inputs
-  // k = k0 + wk * 64 + kb * 32 + 8 j + 4 half + (0 .. 3) in acc[kb][nb][4 j ..]
+  // lane: output n = n0 + 128 wn + 32 nb + col, inputs
+  // k = k0 + 128 wk + 32 kb + 8 g + 4 hi + (0 .. 3) in acc[kb][nb][4 g ..]
+  // (the plan gives this kernel at least two row chunks: the SGD is the
+  // reduction's)
+  VFL_GLOBAL float* part = glb(P.part) + (int64_t)split * N * P.kp;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int n = n0 + wn * WN + nb * 32 + col;
+  for (int nb = 0; nb < 4; ++nb) {
+    const int n = n0 + 128 * wn + 32 * nb + col;
+    if (n >= N) continue;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kk = k0 + wk * 64 + kb * 32 + 8 * j + 4 * half;
-        const f32x4 g = f32x4{acc[kb][nb][4 * j], acc[kb][nb][4 * j + 1], acc[kb][nb][4 * j + 2],
-                              acc[kb][nb][4 * j + 3]};
-        if (P.splits > 1) {
-          if (n < N && kk < K) *(VFL_GLOBAL f32x4*)(glb(P.part) + ((int64_t)split * N + n) * P.kp + kk) = g;
-        } else {
-          float w[4];
-          sgd_load4<uint16_t>(P, n, kk, w);
-          sgd_store4<uint16_t>(P, n, kk, w, g, scale);
-        }
+      for (int g = 0; g < 4; ++g) {
+        const int kk = k0 + 128 * wk + 32 * kb + 8 * g + 4 * hi;
+        if (kk < K)
+          *(VFL_GLOBAL f32x4*)(part + (int64_t)n * P.kp + kk) =
+              f32x4{acc[kb][nb][4 * g], acc[kb][nb][4 * g + 1], acc[kb][nb][4 * g + 2], acc[kb][nb][4 * g + 3]};
       }
-    }
   }
 }
 
@@ -664,9 +658,13 @@ hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, Ti
   return hipGetLastError();
 }
 
-hipError_t launch_dwt(const DwJob* job, int blocks, float scale, TickRef tr, hipStream_t st) {
+hipError_t dwt_init() {
+  return hipFuncSetAttribute((const void*)k_dwt, hipFuncAttributeMaxDynamicSharedMemorySize, kDwtLds);
+}
+
+hipError_t launch_dwt(const DwJob* job, int blocks, hipStream_t st) {
   if (blocks < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_dwt, dim3(blocks), dim3(256), 0, st, job, scale, tr);
+  hipLaunchKernelGGL(k_dwt, dim3(blocks), dim3(256), kDwtLds, st, job);
   return hipGetLastError();
 }
 

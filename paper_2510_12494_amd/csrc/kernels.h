@@ -306,9 +306,11 @@ struct DwJob {
 };
 hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, TickRef tr,
                      hipStream_t st);
-// bf16 problems over 256 x 128 tiles (tiles counted with that shape; rps a
-// multiple of 64), the same partial / SGD contract as launch_dw.
-hipError_t launch_dwt(const DwJob* job, int blocks, float scale, TickRef tr, hipStream_t st);
+// bf16 problems over 256 x 256 tiles (tiles counted with that shape; rps a
+// multiple of 32, at least two chunks per problem): float32 partials only,
+// which k_dw_reduce sums (with the SGD step).
+hipError_t dwt_init();
+hipError_t launch_dwt(const DwJob* job, int blocks, hipStream_t st);
 // Unsplit problems over 32 x 32 tiles (every problem's splits == 1, tiles
 // counted with 32-wide tiles; `blocks` = job->blocks + the logit blocks):
 // products, SGD and copy refresh in one launch, the logit reduction in the
