@@ -159,6 +159,8 @@ struct Plan {
   bool bgemm = false;
   size_t d1rm = 0, job_lin = 0;
   int lin_blocks_dx = 0;
+  size_t mbits[kMaxSlots]{};          // layer 0's ReLU bits per slot [out0 x ldb]
+  int ldb = 0;
   KMeta kf, ka, kb;
   FwdLds lf;
   ActLds la;
@@ -539,7 +541,13 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   // chain's LDS), no tables, bf16: layer 1's input gradient is a layer
   // product over the whole group
   p.bgemm = p.e == BF16 && p.P.L >= 2 && p.P.spec.n_cat == 0 && p.P.out[0] >= kGemmMinWidth;
-  if (p.bgemm) p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
+  if (p.bgemm) {
+    p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
+    if (p.P.relu[0]) {
+      p.ldb = (int)((Ra / 8 + 31) / 32 * 32);
+      for (int q = 0; q <= p.s; ++q) p.mbits[q] = ly.take((size_t)p.P.out[0] * p.ldb);
+    }
+  }
 
   Top& T = p.T;
   T.spec = *t;
@@ -723,6 +731,11 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
                      p.lf.buf[l % 2], p.lf.buf[(l + 1) % 2]);
       if (l + 1 < P.L) f.l[l].rc = rcm(c, P.arc[q][l], P.out[l]);
     }
+    if (p.bgemm && P.relu[0]) {
+      // layer 0's ReLU bits for the wide input-gradient product
+      f.l[0].rc.bits = (uint8_t*)(ws + p.mbits[q]);
+      f.l[0].rc.ldb = p.ldb;
+    }
     f.z = c->ws + P.z[q]; f.ldz = (int32_t)ld_of(p.dB);
     f.publish = eextra;
     f.m = msg_op(o, o.flags & VFL_CLIP_EMB, o.flags & VFL_NOISE_EMB, 0);
@@ -842,7 +855,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       g.A = ws + p.d1rm; g.lda = ld_of(P.out[1]);
       g.W = c->ws + P.Wtq[q][1]; g.kst = P.kt[1];
       g.N = P.out[0]; g.K = P.out[1];
-      if (P.relu[0]) g.mask_rc = rcm(c, P.arc[q][0], P.out[0]);
+      if (P.relu[0]) { g.mbits = (const uint8_t*)(ws + p.mbits[q]); g.ldb = p.ldb; }
       g.out_rc = rcm(c, P.drc[0], P.out[0]);
       g.tiles_n = (g.N + 255) / 256; g.tiles_m = (p.Ra + 255) / 256;
       g.rows_pad = p.Ra;

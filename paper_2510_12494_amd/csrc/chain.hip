@@ -395,6 +395,20 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
       for (int w = 0; w < 4; ++w) v[w] = *(const uint32_t*)(src + w * b.pitch);
     }
     *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16) = v;
+    if constexpr (RR == 8) {
+      if (m.bits && c < cols) {
+        // the chunk's positive rows, one bit each (ReLU outputs: a row is
+        // positive when its sign bit is clear and it is not zero)
+        uint32_t byte = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t lo = v[w] & 0xffffu, hi = v[w] >> 16;
+          byte |= (uint32_t)(lo != 0 && !(lo & 0x8000u)) << (2 * w);
+          byte |= (uint32_t)(hi != 0 && !(hi & 0x8000u)) << (2 * w + 1);
+        }
+        glb(m.bits)[(int64_t)c * m.ldb + r0 / RR + rg] = (uint8_t)byte;
+      }
+    }
   }
 }
 

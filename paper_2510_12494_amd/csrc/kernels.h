@@ -104,8 +104,14 @@ hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st);
 struct LBuf { int32_t off = 0, pitch = 0; };
 
 // RC-layout global matrix (null p: not written); rows: the rows it holds
-// (a chain block's rows past it are not written; 0: unbounded).
-struct RCMat { void* p = nullptr; int32_t cp = 0, rows = 0; };
+// (a chain block's rows past it are not written; 0: unbounded).  bits (bf16
+// chain copies only; null: none): a byte per 8-row chunk as well, bit i set
+// when row i of the chunk is positive, at bits[column * ldb + row / 8] (the
+// ReLU derivative of a layer for the wide input-gradient product).
+struct RCMat {
+  void* p = nullptr; int32_t cp = 0, rows = 0;
+  uint8_t* bits = nullptr; int32_t ldb = 0;
+};
 
 // One product of a row block with a weight operand W [N x K] (element type,
 // packed: see pk_index; kst = K steps of the packing, tiles up to N rounded
@@ -325,8 +331,9 @@ hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float sc
 // ---------------------------------------------------------- layer products
 // The input gradient of a wide bottom layer of party B over the rows of a
 // group (bf16), in large tiles:
-//   out[r][n] = (mask[r][n] > 0) * sum_k A[r][k] W[n][k]   (mask_rc null: no mask)
-// for r < rows, into out_rc (rows from the group's end up to rows_pad zero).
+//   out[r][n] = mask(r, n) * sum_k A[r][k] W[n][k]
+// for r < rows, into out_rc (rows from the group's end up to rows_pad zero);
+// mask(r, n) = bit r mod 8 of mbits[n * ldb + r / 8] (mbits null: 1).
 // A: row-major bf16, lda elements per row (a multiple of 8; finite values
 // from K up to lda); W: packed [N x K] (pk_index, kst 32-k steps, zero past
 // K).  Blocks: lin_blocks(rows_pad, N): 256 x 256 output tiles rounded up
@@ -335,7 +342,8 @@ struct LinJob {
   const void* A = nullptr; int64_t lda = 0;
   const void* W = nullptr; int32_t kst = 0;
   int32_t N = 0, K = 0;
-  RCMat out_rc, mask_rc;
+  RCMat out_rc;
+  const uint8_t* mbits = nullptr; int32_t ldb = 0;
   int32_t tiles_n = 0, tiles_m = 0, rows_pad = 0;
 };
 int lin_blocks(int rows_pad, int N);

@@ -23,8 +23,9 @@
 // Epilogue: a lane holds one output column and four runs of four rows of
 // each 32 x 32 MFMA tile.  The tile goes through LDS as bf16, column by
 // column (8-byte writes of four rows); each thread then owns one column and
-// writes its 8-row chunks, masked by the RC mask: every store is a full
-// 16-byte chunk and a store instruction writes 64 consecutive chunks.  Rows
+// writes its 8-row chunks, masked by the bit mask of the layer below (a byte
+// per chunk): every store is a full 16-byte chunk and a store instruction
+// writes 64 consecutive chunks.  Rows
 // past the group are written as zeros, up to the padded row count.
 #include "device.h"
 #include "kernels.h"
@@ -220,28 +221,28 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
   __syncthreads();
   // 2. the RC output: thread t owns tile column t and walks its 8-row
   //    chunks, so that each store instruction writes 64 consecutive chunks
-  //    of one row group (masked by the RC mask for the input gradient)
-  const bool masked = J.mask_rc.p != nullptr;
-  if (rc_out && n0 + t < N) {
+  //    of one row group; the mask bytes of the column's chunks (the ReLU
+  //    derivative of the layer below) are loaded up front
+  if (n0 + t < N) {
     const int n = n0 + t;
     VFL_GLOBAL u32x4* dst = (VFL_GLOBAL u32x4*)glb((char*)J.out_rc.p) + n;
-    const VFL_GLOBAL u32x4* msk = masked ? (const VFL_GLOBAL u32x4*)glb((const char*)J.mask_rc.p) + n : nullptr;
     const int ng = (int)min((int64_t)kBM / 8, rg_end - m0 / 8);   // row groups inside the padded rows
+    uint32_t mb[kBM / 32];
+#pragma unroll
+    for (int i = 0; i < kBM / 32; ++i) mb[i] = ~0u;
+    if (J.mbits) {
+      const VFL_GLOBAL uint32_t* bp = (const VFL_GLOBAL uint32_t*)(glb(J.mbits) + (int64_t)n * J.ldb + m0 / 8);
+#pragma unroll
+      for (int i = 0; i < kBM / 32; ++i) mb[i] = bp[i];
+    }
 #pragma unroll 4
     for (int rg = 0; rg < ng; ++rg) {
       const int64_t g = m0 / 8 + rg;
       u32x4 q = mask_tail<uint16_t>(*(const u32x4*)(smem + out_slot(t, rg)), rows - (m0 + 8 * rg));
-      if (masked) {
-        const u32x4 m = msk[g * J.mask_rc.cp];
+      const uint32_t byte = mb[rg >> 2] >> (8 * (rg & 3));
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          // the ReLU derivative of the layer below: keep the elements whose
-          // mask value is positive
-          const uint32_t lo = __uint_as_float(m[w] << 16) > 0.f ? 0x0000ffffu : 0u;
-          const uint32_t hm = __uint_as_float(m[w] & 0xffff0000u) > 0.f ? 0xffff0000u : 0u;
-          q[w] &= lo | hm;
-        }
-      }
+      for (int w = 0; w < 4; ++w)
+        q[w] &= ((byte >> (2 * w)) & 1u ? 0x0000ffffu : 0u) | ((byte >> (2 * w + 1)) & 1u ? 0xffff0000u : 0u);
       dst[g * J.out_rc.cp] = q;
     }
   }
