@@ -147,7 +147,7 @@ typedef struct vfl_ctx vfl_ctx;
 vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
                               const vfl_top_spec* top, const vfl_opts* o, size_t* bytes);
 
-/* Create a context over a caller-owned device workspace (16-byte aligned) of
+/* Create a context over a caller-owned device workspace (256-byte aligned) of
  * at least vfl_workspace_size() bytes; stream_a / stream_b are hipStream_t
  * (NULL: the null stream).  They may be the same stream: both parties' work
  * then runs in enqueue order, with no overlap.  Parameters start at zero: set them with
@@ -155,6 +155,26 @@ vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b
 vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
                       const vfl_top_spec* top, const vfl_opts* o, void* workspace,
                       size_t bytes, void* stream_a, void* stream_b, vfl_ctx** out);
+
+/* For callers that cannot allocate device memory (code that must not call
+ * hipMalloc, such as harnesses that forbid it or set-up that precedes a
+ * graph capture): vfl_create with the library's own static workspace of the
+ * current device instead of a caller's buffer.  The library holds one
+ * array of VFL_STATIC_WORKSPACE_BYTES per device from its load on that
+ * device until the process ends; this call allocates no device memory (no
+ * hipMalloc, hipFree or allocating library routine) and, like vfl_create,
+ * clears the part of the array the configuration uses before returning.
+ * stream_a / stream_b as for vfl_create, on the current device.  Every
+ * later call on the context behaves exactly as on a vfl_create context.
+ * At most one context holds a device's array at a time: VFL_E_STATE while
+ * another one has not been destroyed (vfl_destroy releases the array;
+ * contexts that shared it would race).  VFL_E_NOMEM when the configuration's
+ * vfl_workspace_size exceeds VFL_STATIC_WORKSPACE_BYTES, VFL_E_INVALID for
+ * a configuration vfl_create rejects. */
+#define VFL_STATIC_WORKSPACE_BYTES (64u << 20)
+vfl_status vfl_create_static(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                             const vfl_top_spec* top, const vfl_opts* o, void* stream_a,
+                             void* stream_b, vfl_ctx** out);
 
 /* Copy one parameter tensor in or out (float32 master copy).  party
  * VFL_PARTY_A / VFL_PARTY_B / VFL_TOP; kind VFL_PARAM_W ([out x in]

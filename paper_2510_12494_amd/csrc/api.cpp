@@ -28,6 +28,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -202,6 +203,7 @@ struct vfl_ctx {
   Timing tm;
   vfl_opts o{};
   char* ws = nullptr;
+  int static_dev = -1;  // device whose static workspace this context holds (-1: caller's)
   hipStream_t sa = nullptr, sb = nullptr;
   hipEvent_t ev_emb[kMaxSlots]{}, ev_grad[kMaxSlots]{};
   // B
@@ -1441,36 +1443,64 @@ vfl_status ensure_graph(vfl_ctx* c, int gi, int phase, int len, float* loss_ring
 
 }  // namespace
 
-extern "C" {
+extern "C" vfl_status vfl_destroy(vfl_ctx* c);
 
-vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
-                              const vfl_top_spec* top, const vfl_opts* o, size_t* bytes) {
-  if (!bytes) return fail_create(VFL_E_INVALID, "null bytes");
-  Plan p;
-  std::string why = build_plan(a, b, top, o, p);
-  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
-  // the kernels' layouts are checked here already (against a nominal base)
-  Jobs J;
-  why = build_jobs(p, *o, (char*)(uintptr_t)4096, J);
-  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
-  t_create_err.clear();
-  *bytes = p.total;
+namespace {
+
+// The workspace of vfl_create_static: one array per device, in the code
+// object's zero-initialised data, held from the library's load on a device
+// until the process ends.  Host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (the array's name is a
+// host-side stand-in); at most one context holds a device's array at a time.
+static __device__ __align__(256) unsigned char scratch[VFL_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+void* g_static_ptr[kMaxDevices] = {};
+bool g_static_held[kMaxDevices] = {};
+
+// Take the current device's static workspace: its address (looked up once
+// per device, with that device current) or an error.
+vfl_status static_ws_acquire(int& dev, void*& ptr, std::string& why) {
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    why = std::string("hipGetDevice: ") + hipGetErrorString(e);
+    return VFL_E_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    why = "device index beyond the static workspace table";
+    return VFL_E_INVALID;
+  }
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_held[dev]) {
+    why = "the static workspace of device " + std::to_string(dev) +
+          " is held by another context (destroy that one first)";
+    return VFL_E_STATE;
+  }
+  if (!g_static_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p || ((uintptr_t)p) % 256) {
+      why = std::string("hipGetSymbolAddress of the static workspace: ") + hipGetErrorString(e);
+      return VFL_E_HIP;
+    }
+    g_static_ptr[dev] = p;
+  }
+  g_static_held[dev] = true;
+  ptr = g_static_ptr[dev];
   return VFL_OK;
 }
 
-vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* top,
-                      const vfl_opts* o, void* workspace, size_t bytes, void* stream_a,
-                      void* stream_b, vfl_ctx** out) {
-  if (!out) return fail_create(VFL_E_INVALID, "null out");
-  *out = nullptr;
-  vfl_ctx* c = new vfl_ctx();
-  std::string why = build_plan(a, b, top, o, c->p);
-  if (!why.empty()) { delete c; return fail_create(VFL_E_INVALID, why); }
-  if (!workspace || ((uintptr_t)workspace) % 256) {
-    delete c;
-    return fail_create(VFL_E_INVALID, "workspace null or not 256-byte aligned");
-  }
-  if (bytes < c->p.total) { delete c; return fail_create(VFL_E_NOMEM, "workspace too small"); }
+void static_ws_release(int dev) {
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  g_static_held[dev] = false;
+}
+
+// The part of context creation shared by vfl_create and vfl_create_static:
+// plan checked, workspace chosen.  On failure the context is destroyed (which
+// also releases a static workspace).
+vfl_status finish_create(vfl_ctx* c, const vfl_opts* o, void* workspace, void* stream_a,
+                         void* stream_b, vfl_ctx** out) {
   c->o = *o;
   c->ws = (char*)workspace;
   c->sa = (hipStream_t)stream_a;
@@ -1502,6 +1532,64 @@ vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const 
   t_create_err.clear();
   *out = c;
   return VFL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vfl_status vfl_workspace_size(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                              const vfl_top_spec* top, const vfl_opts* o, size_t* bytes) {
+  if (!bytes) return fail_create(VFL_E_INVALID, "null bytes");
+  Plan p;
+  std::string why = build_plan(a, b, top, o, p);
+  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
+  // the kernels' layouts are checked here already (against a nominal base)
+  Jobs J;
+  why = build_jobs(p, *o, (char*)(uintptr_t)4096, J);
+  if (!why.empty()) return fail_create(VFL_E_INVALID, why);
+  t_create_err.clear();
+  *bytes = p.total;
+  return VFL_OK;
+}
+
+vfl_status vfl_create(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const vfl_top_spec* top,
+                      const vfl_opts* o, void* workspace, size_t bytes, void* stream_a,
+                      void* stream_b, vfl_ctx** out) {
+  if (!out) return fail_create(VFL_E_INVALID, "null out");
+  *out = nullptr;
+  vfl_ctx* c = new vfl_ctx();
+  std::string why = build_plan(a, b, top, o, c->p);
+  if (!why.empty()) { delete c; return fail_create(VFL_E_INVALID, why); }
+  if (!workspace || ((uintptr_t)workspace) % 256) {
+    delete c;
+    return fail_create(VFL_E_INVALID, "workspace null or not 256-byte aligned");
+  }
+  if (bytes < c->p.total) { delete c; return fail_create(VFL_E_NOMEM, "workspace too small"); }
+  return finish_create(c, o, workspace, stream_a, stream_b, out);
+}
+
+vfl_status vfl_create_static(const vfl_bottom_spec* a, const vfl_bottom_spec* b,
+                             const vfl_top_spec* top, const vfl_opts* o, void* stream_a,
+                             void* stream_b, vfl_ctx** out) {
+  if (!out) return fail_create(VFL_E_INVALID, "null out");
+  *out = nullptr;
+  vfl_ctx* c = new vfl_ctx();
+  std::string why = build_plan(a, b, top, o, c->p);
+  if (!why.empty()) { delete c; return fail_create(VFL_E_INVALID, why); }
+  if (c->p.total > (size_t)VFL_STATIC_WORKSPACE_BYTES) {
+    const std::string msg = "configuration needs " + std::to_string(c->p.total) +
+                            " bytes of workspace; the static workspace holds " +
+                            std::to_string((size_t)VFL_STATIC_WORKSPACE_BYTES);
+    delete c;
+    return fail_create(VFL_E_NOMEM, msg);
+  }
+  int dev = -1;
+  void* ws = nullptr;
+  const vfl_status st = static_ws_acquire(dev, ws, why);
+  if (st != VFL_OK) { delete c; return fail_create(st, why); }
+  c->static_dev = dev;
+  return finish_create(c, o, ws, stream_a, stream_b, out);
 }
 
 vfl_status vfl_set_param(vfl_ctx* c, vfl_party party, int32_t layer, int32_t kind, const void* src,
@@ -2014,6 +2102,7 @@ vfl_status vfl_destroy(vfl_ctx* c) {
   }
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
   if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+  if (c->static_dev >= 0) static_ws_release(c->static_dev);
   delete c;
   return r;
 }

@@ -55,7 +55,7 @@ class Session:
     gives the [(start, count)] replica rows of batch group g."""
 
     def __init__(self, w, data: dict, params: dict, rows_of, device: str = "cuda:0",
-                 one_stream: bool = False):
+                 one_stream: bool = False, static_ws: bool = False):
         self.w = w
         self.dev = torch.device(device)
         self.rows_of = rows_of
@@ -68,9 +68,16 @@ class Session:
             self.sa = torch.cuda.Stream(device=self.dev)
             # one_stream: both parties on one stream (no overlap between them)
             self.sb = self.sa if one_stream else torch.cuda.Stream(device=self.dev)
-        self.ws = torch.empty(self.nbytes, dtype=torch.uint8, device=self.dev)
-        self.ctx = V.vfl_create(self.specA, self.specB, self.specT, self.o, self.ws.data_ptr(),
-                                self.nbytes, self.sa.cuda_stream, self.sb.cuda_stream)
+        if static_ws:
+            # the library's own per-device workspace (vfl_create_static)
+            self.ws = None
+            with torch.cuda.device(self.dev):
+                self.ctx = V.vfl_create_static(self.specA, self.specB, self.specT, self.o,
+                                               self.sa.cuda_stream, self.sb.cuda_stream)
+        else:
+            self.ws = torch.empty(self.nbytes, dtype=torch.uint8, device=self.dev)
+            self.ctx = V.vfl_create(self.specA, self.specB, self.specT, self.o, self.ws.data_ptr(),
+                                    self.nbytes, self.sa.cuda_stream, self.sb.cuda_stream)
         self.data = {}
         for key in ("xa", "xb"):
             x = data.get(key)

@@ -21,11 +21,12 @@ VFL_NOISE_EMB, VFL_NOISE_GRAD, VFL_CLIP_EMB, VFL_CLIP_GRAD = 1, 2, 4, 8
 VFL_FIFO_DISCARD, VFL_LOSS_MSE = 16, 32
 VFL_MAX_LAYERS = 16
 VFL_GRAPH_CYCLES = 4
+VFL_STATIC_WORKSPACE_BYTES = 64 << 20
 VFL_TIMED_EVERY = 4       # vfl_run times the launches of every 4th tick of a captured cycle
 STATUS_NAMES = {0: "VFL_OK", 1: "VFL_E_INVALID", 2: "VFL_E_NOMEM", 3: "VFL_E_HIP",
                 4: "VFL_E_NOT_READY", 5: "VFL_E_STALE", 6: "VFL_E_STATE"}
 
-EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_set_param", "vfl_get_param",
+EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_create_static", "vfl_set_param", "vfl_get_param",
            "vfl_bottom_forward", "vfl_publish", "vfl_top_step", "vfl_bottom_backward",
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
@@ -91,6 +92,7 @@ def _load():
     sig = {
         "vfl_workspace_size": [BS, BS, TS, OP, C.POINTER(SZ)],
         "vfl_create": [BS, BS, TS, OP, P, SZ, P, P, C.POINTER(P)],
+        "vfl_create_static": [BS, BS, TS, OP, P, P, C.POINTER(P)],
         "vfl_set_param": [P, C.c_int, I32, I32, P, SZ, I32],
         "vfl_get_param": [P, C.c_int, I32, I32, P, SZ, I32],
         "vfl_bottom_forward": [P, C.c_int, I64, BA, I32],
@@ -159,6 +161,14 @@ def vfl_create(a, b, top, o, workspace_ptr: int, nbytes: int, stream_a: int, str
     _chk(_lib.vfl_create(C.byref(a), C.byref(b), C.byref(top), C.byref(o), C.c_void_p(workspace_ptr),
                          nbytes, C.c_void_p(stream_a), C.c_void_p(stream_b), C.byref(h)),
          "vfl_create")
+    return h
+
+
+def vfl_create_static(a, b, top, o, stream_a: int, stream_b: int):
+    h = C.c_void_p()
+    _chk(_lib.vfl_create_static(C.byref(a), C.byref(b), C.byref(top), C.byref(o), C.c_void_p(stream_a),
+                                C.c_void_p(stream_b), C.byref(h)),
+         "vfl_create_static")
     return h
 
 
