@@ -289,6 +289,38 @@ vfl_status vfl_get_trace(vfl_ctx* c, int64_t* buf, size_t cap_rows, size_t* rows
  * staleness s and n_groups groups (no context, no GPU). */
 vfl_status vfl_schedule_tick(int64_t t, int32_t s, int64_t n_groups, int64_t out[7]);
 
+/* Semi-asynchronous replicas (Section 4.1 "Intra-party Semi-asynchronous
+ * Mechanism", Eq. 5; the aggregation step of Algorithm 1).  Each of a
+ * party's n workers is its own context (k = 1, the worker's batch of
+ * `batch` rows per group, its own parameters and local SGD); every
+ * Delta T_t units the party's parameter server averages the workers'
+ * parameters and broadcasts the result.  A unit is an epoch in Algorithm 1
+ * (or any fixed number of ticks); after unit t (t = 1, 2, ...) the caller
+ * averages when t mod vfl_sync_interval(dt0, t) == 0.  With one unit per
+ * tick and Delta T = 1 the replicas stay equal to one context of k = n
+ * replicas (gradient averaging), up to float32 rounding.
+ *
+ * vfl_sync_interval (pure host): *dt = Delta T_t of Eq. 5, the ceiling of
+ * dt0/2 * tanh(2t/dt0 - 2) + dt0/2, in [1, dt0] (dt0 >= 1, t >= 0).
+ *
+ * vfl_replica_average: enqueue the average of the float32 master
+ * parameters of `parties` (bit VFL_PARTY_A: A's bottom layers, its table
+ * and the top model; bit VFL_PARTY_B: B's bottom layers and table) over the
+ * n contexts ctxs[0 .. n-1] (1 <= n <= 16, distinct, one configuration, on
+ * the current device), weighted by the rows each context's party applied
+ * since its previous average (the weights sum to 1; a context that applied
+ * none gets weight 0), and write it to every context.  Ordered after the
+ * work already enqueued on each context's stream of that party (A: stream_a,
+ * B: stream_b) and before their later work; it then rewrites the operand
+ * copies of the averaged weights (A's current copies; B's copies in the
+ * slot of its next forward, while the slots of groups in flight keep the
+ * weights their forward used, as B's delayed backward needs).  Versions and
+ * the schedule do not change.  VFL_E_STATE when party A of a context is
+ * inside a group's step or no context applied rows since the last average;
+ * VFL_E_INVALID for bad arguments. */
+vfl_status vfl_sync_interval(int32_t dt0, int64_t t, int32_t* dt);
+vfl_status vfl_replica_average(vfl_ctx* const* ctxs, int32_t n, uint32_t parties);
+
 /* Checkpoint and resume.  The state of a context is what the next tick
  * depends on: both parties' parameters (float32 masters, tables, B's
  * per-slot stashed weight copies), the contents and headers of the
@@ -379,7 +411,8 @@ typedef enum {
   VFL_K_EMB_SGD = 6,    /* sorted sparse SGD of the tables */
   VFL_K_GEMM = 7,       /* layer products of party B's wide layers (input gradient) */
   VFL_K_DWT = 8,        /* large-tile bf16 weight-gradient products (partials + SGD) */
-  VFL_K_COUNT = 9
+  VFL_K_AVG = 9,        /* replica parameter averaging (vfl_replica_average) */
+  VFL_K_COUNT = 10
 } vfl_kernel_class;
 
 /* Measurement hook: while class_mask is non-zero, every launch of a

@@ -268,6 +268,41 @@ class PubSubOracle:
         return grads
 
     # -------------------------------------------------------------- loop
+    def tick(self, t: int, data: dict, n_groups: int, group_rows, keep_messages=True,
+             keep_grads=False, drop=None):
+        """Tick t of the schedule: B publishes group t (t < n_groups); A takes
+        group u = t - s and B back-propagates it (0 <= u < n_groups), unless
+        ``drop`` ("emb" or "grad", see ``run``) discards group u.  Returns the
+        tick's record."""
+        s = self.s
+        rec = dict(tick=t)
+        fwd = bwd = -1
+        if t < n_groups:
+            fwd = t
+            rec["fwd_version"] = self.vB
+            ent = self.publish(t, t, data, group_rows(t))
+            rec["fwd_slot"] = t % (s + 1)
+            if keep_messages:
+                rec["zhat"] = ent["zhat"]
+            rec["emb_header"] = (ent["seq"], ent["tick"], ent["version"])
+        u = t - s
+        if 0 <= u < n_groups:
+            bwd = u
+            rec["bwd_slot"] = u % (s + 1)
+            if drop != "emb":
+                loss, gm, gA = self.active_step(u, t, data, group_rows(u))
+                rec["loss"] = loss
+                if keep_messages:
+                    rec["gtilde"] = gm["g"]
+                rec["grad_header"] = (gm["seq"], gm["tick"], gm["version"])
+            gB = self.passive_backward(u, t) if drop is None else {}
+            if keep_grads and drop is None:
+                rec["grads"] = {**gA, **gB}
+        rec["fwd_group"], rec["bwd_group"] = fwd, bwd
+        self.trace.append((t, fwd, rec.get("fwd_slot", -1), rec.get("fwd_version", -1),
+                           bwd, rec.get("bwd_slot", -1), self.vB if bwd >= 0 else -1))
+        return rec
+
     def run(self, data: dict, n_groups: int, group_rows, snapshot=None,
             keep_messages=True, keep_grads=False, discard=None):
         """Run n_groups batch groups (n_groups + s ticks).
@@ -285,35 +320,9 @@ class PubSubOracle:
         """
         discard = discard or {}
         recs = []
-        s = self.s
-        for t in range(n_groups + s):
-            rec = dict(tick=t)
-            fwd = bwd = -1
-            if t < n_groups:
-                fwd = t
-                rec["fwd_version"] = self.vB
-                ent = self.publish(t, t, data, group_rows(t))
-                rec["fwd_slot"] = t % (s + 1)
-                if keep_messages:
-                    rec["zhat"] = ent["zhat"]
-                rec["emb_header"] = (ent["seq"], ent["tick"], ent["version"])
-            u = t - s
-            if 0 <= u < n_groups:
-                bwd = u
-                rec["bwd_slot"] = u % (s + 1)
-                drop = discard.get(u)
-                if drop != "emb":
-                    loss, gm, gA = self.active_step(u, t, data, group_rows(u))
-                    rec["loss"] = loss
-                    if keep_messages:
-                        rec["gtilde"] = gm["g"]
-                    rec["grad_header"] = (gm["seq"], gm["tick"], gm["version"])
-                gB = self.passive_backward(u, t) if drop is None else {}
-                if keep_grads and drop is None:
-                    rec["grads"] = {**gA, **gB}
-            rec["fwd_group"], rec["bwd_group"] = fwd, bwd
-            self.trace.append((t, fwd, rec.get("fwd_slot", -1), rec.get("fwd_version", -1),
-                               bwd, rec.get("bwd_slot", -1), self.vB if bwd >= 0 else -1))
+        for t in range(n_groups + self.s):
+            rec = self.tick(t, data, n_groups, group_rows, keep_messages, keep_grads,
+                            discard.get(t - self.s))
             if snapshot is not None and snapshot(t):
                 rec["params"] = {k: v.copy() for k, v in self.p.items()}
             recs.append(rec)

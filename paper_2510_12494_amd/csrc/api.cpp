@@ -217,6 +217,10 @@ struct vfl_ctx {
   int a_phase = 0;                    // 0 forward, 1 top step, 2 backward
   SlotState aslot;
   float* a_loss = nullptr;
+  // rows each party has applied since its last replica average (the
+  // average's weights)
+  int64_t a_rows_avg = 0, b_rows_avg = 0;
+  hipEvent_t ev_avg = nullptr;
   // discarded groups (Section 4.1 "System Design": the buffer and waiting-deadline
   // mechanisms), each until B's backward of it releases its slot without
   // an update; grad: A had consumed the group (B must wait for A's
@@ -273,6 +277,13 @@ vfl_status fail_create(vfl_status st, const std::string& msg) {
     hipError_t e_ = (expr);                                                              \
     if (e_ != hipSuccess)                                                                \
       return fail(c, VFL_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
+  } while (0)
+
+#define HIPCHK0(ctx, expr)                                                               \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail((ctx), VFL_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));  \
   } while (0)
 
 bool check_bottom(const vfl_bottom_spec* s, std::string& why) {
@@ -1264,12 +1275,13 @@ struct StateHead {
   uint32_t format, n_slots;
   uint64_t layout, ws_bytes, trace_len;
   int64_t b_next_fwd, b_next_bwd, b_version, b_pub_next, a_next, a_version, a_copy_version;
+  int64_t a_rows_avg, b_rows_avg;
   int64_t b_copy_version[kMaxSlots], grad_group[kMaxSlots], grad_rows[kMaxSlots];
   int64_t slot_group[kMaxSlots], slot_version[kMaxSlots], slot_row0[kMaxSlots], slot_rows[kMaxSlots],
       slot_published[kMaxSlots];
 };
 constexpr char kStateMagic[8] = {'V', 'F', 'L', 'S', 'T', 'A', 'T', 'E'};
-constexpr uint32_t kStateFormat = 1;
+constexpr uint32_t kStateFormat = 2;
 
 // FNV-1a over everything that fixes the workspace layout: element type,
 // batch, staleness, replicas and both bottom specs and the top spec.
@@ -1372,6 +1384,8 @@ vfl_status ensure_graph(vfl_ctx* c, int gi, int phase, int len, float* loss_ring
       (c->graph_loss[gi] != loss_ring || c->graph_loss_len[gi] != loss_len || c->graph_mask[gi] != mask ||
        c->graph_len[gi] != len);
   if (stale) {
+    // an earlier replay of it may still run
+    HIPCHK(hipStreamSynchronize(c->sa));
     (void)hipGraphExecDestroy(c->gexec[gi]);
     (void)hipGraphDestroy(c->graph[gi]);
     c->gexec[gi] = nullptr;
@@ -1516,6 +1530,7 @@ vfl_status finish_create(vfl_ctx* c, const vfl_opts* o, void* workspace, void* s
   }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_avg, hipEventDisableTiming);
   // parameters, headers and the error counter start at zero
   if (e == hipSuccess) e = hipMemsetAsync(c->ws, 0, c->p.total, c->sa);
   if (e == hipSuccess) e = hipStreamSynchronize(c->sa);
@@ -1726,6 +1741,7 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     vfl_status r = a_backward(c, c->aslot, c->a_loss, TickRef());
     if (r) return r;
     c->a_version += 1;
+    c->a_rows_avg += c->aslot.rows;
     c->a_copy_version = c->a_version;
     c->a_next = group + 1;
     c->a_phase = 0;
@@ -1744,6 +1760,7 @@ vfl_status vfl_bottom_backward(vfl_ctx* c, vfl_party party, int64_t group) {
     if (r) return r;
     c->b_next_bwd = group + 1;
     c->b_version += 1;
+    c->b_rows_avg += c->bslot[slot].rows;
     c->b_copy_version[slot] = c->b_version;
     return VFL_OK;
   }
@@ -1880,6 +1897,8 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
     c->grad_rows[us] = c->bslot[us].rows;
     c->a_version += 1;
     c->b_version += 1;
+    c->a_rows_avg += c->grad_rows[us];
+    c->b_rows_avg += c->grad_rows[us];
     c->b_copy_version[us] = c->b_version;
     row[6] = c->b_version;
     c->trace.insert(c->trace.end(), row, row + 7);
@@ -1887,6 +1906,105 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
   c->a_copy_version = c->a_version;
   c->b_next_fwd = c->b_pub_next = t0 + n;
   c->b_next_bwd = c->a_next = t0 + n - s;
+  return VFL_OK;
+}
+
+vfl_status vfl_replica_average(vfl_ctx* const* ctxs, int32_t n, uint32_t parties) {
+  if (!ctxs || n < 1 || n > kMaxAvgSets || !parties || (parties & ~3u)) return VFL_E_INVALID;
+  vfl_ctx* c0 = ctxs[0];
+  if (!c0) return VFL_E_INVALID;
+  int dev = -1;
+  HIPCHK0(c0, hipGetDevice(&dev));
+  for (int i = 0; i < n; ++i) {
+    vfl_ctx* c = ctxs[i];
+    if (!c) return fail(c0, VFL_E_INVALID, "null context");
+    for (int j = 0; j < i; ++j)
+      if (ctxs[j] == c) return fail(c0, VFL_E_INVALID, "a context appears twice");
+    if (layout_signature(c) != layout_signature(c0))
+      return fail(c0, VFL_E_INVALID, "contexts of different configurations");
+    if (c->capture_phase >= 0) return fail(c0, VFL_E_STATE, "graph capture in progress");
+    if ((parties & 1u) && c->a_phase != 0)
+      return fail(c0, VFL_E_STATE, "party A of a context is inside a group's step");
+    hipPointerAttribute_t pa;
+    HIPCHK0(c0, hipPointerGetAttributes(&pa, c->ws));
+    if (pa.device != dev) return fail(c0, VFL_E_INVALID, "contexts must live on the current device");
+  }
+  const Plan& p = c0->p;
+  for (int party = 0; party < 2; ++party) {
+    if (!(parties & (1u << party))) continue;
+    // weights: rows applied since the last average
+    int64_t tot = 0;
+    for (int i = 0; i < n; ++i) tot += party == 0 ? ctxs[i]->a_rows_avg : ctxs[i]->b_rows_avg;
+    if (tot <= 0) return fail(c0, VFL_E_STATE, "no rows applied since the last average");
+    AvgJob j;
+    j.n = n;
+    for (int i = 0; i < n; ++i) {
+      const int64_t r = party == 0 ? ctxs[i]->a_rows_avg : ctxs[i]->b_rows_avg;
+      j.w[i] = (float)((double)r / (double)tot);
+      j.base[i] = ctxs[i]->ws;
+    }
+    // the party's float32 masters: bottom layers, table, and for A the top
+    const Party& P = party == 0 ? p.A : p.P;
+    auto seg = [&](size_t off, int64_t cnt) {
+      j.off[j.nseg] = (int64_t)off;
+      j.cnt[j.nseg] = cnt;
+      j.first[j.nseg + 1] = j.first[j.nseg] + (cnt + 3) / 4;
+      ++j.nseg;
+    };
+    j.first[0] = 0;
+    for (int l = 0; l < P.L; ++l) {
+      seg(P.W[l], (int64_t)P.out[l] * P.in[l]);
+      seg(P.b[l], P.out[l]);
+    }
+    if (P.spec.n_cat) seg(P.T, (int64_t)P.spec.n_cat * P.spec.vocab * P.spec.emb_dim);
+    if (party == 0)
+      for (int l = 0; l <= p.T.H; ++l) {
+        seg(p.T.W[l], (int64_t)p.T.out[l] * p.T.in[l]);
+        seg(p.T.b[l], p.T.out[l]);
+      }
+    // ordered after every context's pending work on the party's stream;
+    // the contexts' later work on it after the average
+    auto pst = [&](vfl_ctx* c) { return party == 0 ? c->sa : c->sb; };
+    hipStream_t st0 = pst(c0);
+    for (int i = 1; i < n; ++i) {
+      HIPCHK0(c0, hipEventRecord(ctxs[i]->ev_avg, pst(ctxs[i])));
+      HIPCHK0(c0, hipStreamWaitEvent(st0, ctxs[i]->ev_avg, 0));
+    }
+    {
+      vfl_ctx* c = c0;
+      double bytes = 0;
+      for (int q = 0; q < j.nseg; ++q) bytes += 8.0 * n * (double)j.cnt[q];
+      TIMED(VFL_K_AVG, bytes, st0, launch_avg(j, st0));
+    }
+    HIPCHK0(c0, hipEventRecord(c0->ev_avg, st0));
+    for (int i = 0; i < n; ++i) {
+      vfl_ctx* c = ctxs[i];
+      if (i > 0) HIPCHK0(c0, hipStreamWaitEvent(pst(c), c0->ev_avg, 0));
+      // operand copies of the averaged weights: A's current copies; B's
+      // copies in the slot of its next forward when that slot is free (the
+      // slots of groups in flight keep the weights their forward used)
+      vfl_status r;
+      if (party == 0) {
+        if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+        c->a_copy_version = c->a_version;
+        c->a_rows_avg = 0;
+      } else {
+        const int S1 = p.s + 1;
+        for (int q = 0; q < S1; ++q) {
+          bool busy = false;
+          for (int64_t g = c->b_next_bwd; g < c->b_next_fwd; ++g) busy |= (int)(g % S1) == q;
+          if (busy) continue;
+          if (q == (int)(c->b_next_fwd % S1)) {
+            if ((r = enqueue_cast(c, p.P, q, nullptr, c->sb))) return r;
+            c->b_copy_version[q] = c->b_version;
+          } else {
+            c->b_copy_version[q] = -1;
+          }
+        }
+        c->b_rows_avg = 0;
+      }
+    }
+  }
   return VFL_OK;
 }
 
@@ -2010,6 +2128,7 @@ vfl_status vfl_get_state(vfl_ctx* c, void* host_buf, size_t bytes) {
   h.b_next_fwd = c->b_next_fwd; h.b_next_bwd = c->b_next_bwd; h.b_version = c->b_version;
   h.b_pub_next = c->b_pub_next; h.a_next = c->a_next; h.a_version = c->a_version;
   h.a_copy_version = c->a_copy_version;
+  h.a_rows_avg = c->a_rows_avg; h.b_rows_avg = c->b_rows_avg;
   for (int q = 0; q < kMaxSlots; ++q) {
     h.b_copy_version[q] = c->b_copy_version[q];
     h.grad_group[q] = c->grad_group[q];
@@ -2051,6 +2170,7 @@ vfl_status vfl_set_state(vfl_ctx* c, const void* host_buf, size_t bytes) {
   c->b_next_fwd = h.b_next_fwd; c->b_next_bwd = h.b_next_bwd; c->b_version = h.b_version;
   c->b_pub_next = h.b_pub_next; c->a_next = h.a_next; c->a_version = h.a_version;
   c->a_copy_version = h.a_copy_version;
+  c->a_rows_avg = h.a_rows_avg; c->b_rows_avg = h.b_rows_avg;
   c->a_phase = 0;
   c->aslot = SlotState();
   c->a_loss = nullptr;
@@ -2102,6 +2222,7 @@ vfl_status vfl_destroy(vfl_ctx* c) {
   }
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
   if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+  if (c->ev_avg) (void)hipEventDestroy(c->ev_avg);
   if (c->static_dev >= 0) static_ws_release(c->static_dev);
   delete c;
   return r;

@@ -350,6 +350,22 @@ int lin_blocks(int rows_pad, int N);
 hipError_t lin_init();
 hipError_t launch_lin(const LinJob* job, int blocks, int rows, TickRef tr, hipStream_t st);
 
+// ------------------------------------------------------- replica averaging
+// In place over n parameter sets of the same layout (base[i]: a context's
+// workspace): every float32 element x of the segments becomes
+// sum_i w[i] * x_i (accumulated in the order i = 0 .. n-1), written back to
+// every set.  Segment s: cnt[s] floats at byte offset off[s] (16-byte
+// aligned); first[s] = float4 units before segment s (first[nseg] = total).
+constexpr int kMaxAvgSets = 16;
+constexpr int kMaxAvgSegs = 2 * kMaxChain + 4;    // A: its layers, the top layers, the logit layer, a table
+struct AvgJob {
+  int32_t n = 0, nseg = 0;
+  float w[kMaxAvgSets];
+  char* base[kMaxAvgSets];
+  int64_t off[kMaxAvgSegs], cnt[kMaxAvgSegs], first[kMaxAvgSegs + 1];
+};
+hipError_t launch_avg(const AvgJob& j, hipStream_t st);
+
 // ---------------------------------------------------------------- others
 // Operand copies of one layer's float32 weight W [out x in], element type
 // e, packed (pk_index): Wq of W (kq = K steps over `in`), Wtq of W^T (kt =

@@ -1,6 +1,6 @@
 // Small kernels of the split-learning step on gfx950: the weight operand
-// copies, the tick base of a replayed graph, and the raw Philox4x32-10
-// words of the noise generator.
+// copies, the replicas' parameter averaging, the tick base of a replayed
+// graph, and the raw Philox4x32-10 words of the noise generator.
 #include <algorithm>
 
 #include "device.h"
@@ -46,6 +46,43 @@ __global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t st
   }
 }
 
+// ------------------------------------------------------- replica averaging
+// One thread per float4 unit of the segment list (a scalar tail where a
+// segment's length is not a multiple of 4): reads the unit from every set,
+// forms the weighted sum in a fixed order and writes it to every set.
+__global__ __launch_bounds__(256) void k_avg(AvgJob j) {
+  const int64_t total = j.first[j.nseg];
+  for (int64_t u = blockIdx.x * 256 + threadIdx.x; u < total; u += (int64_t)gridDim.x * 256) {
+    int lo = 0, hi = j.nseg - 1;                  // last segment with first <= u
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (j.first[mid] <= u) lo = mid;
+      else hi = mid - 1;
+    }
+    const int64_t e = (u - j.first[lo]) * 4;      // first float of the unit
+    const int64_t cnt = j.cnt[lo];
+    const int64_t off = j.off[lo] + e * 4;
+    if (e + 4 <= cnt) {
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int i = 0; i < j.n; ++i) {
+        const float4 v = *(const float4*)(j.base[i] + off);
+        const float w = j.w[i];
+        acc.x = fmaf(w, v.x, acc.x);
+        acc.y = fmaf(w, v.y, acc.y);
+        acc.z = fmaf(w, v.z, acc.z);
+        acc.w = fmaf(w, v.w, acc.w);
+      }
+      for (int i = 0; i < j.n; ++i) *(float4*)(j.base[i] + off) = acc;
+    } else {
+      for (int64_t q = 0; q < cnt - e; ++q) {
+        float acc = 0.f;
+        for (int i = 0; i < j.n; ++i) acc = fmaf(j.w[i], ((const float*)(j.base[i] + off))[q], acc);
+        for (int i = 0; i < j.n; ++i) ((float*)(j.base[i] + off))[q] = acc;
+      }
+    }
+  }
+}
+
 int grid_for(int64_t work, int per_block, int cap) {
   return (int)std::max<int64_t>(1, std::min<int64_t>((work + per_block - 1) / per_block, cap));
 }
@@ -62,6 +99,14 @@ hipError_t launch_philox_words(uint64_t seed, uint32_t step, uint32_t tag, uint3
   const int64_t total = (int64_t)rows * groups;
   hipLaunchKernelGGL(k_philox_words, dim3(grid_for(total, 256, 4096)), dim3(256), 0, st, seed,
                      step, tag, row0, rows, groups, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_avg(const AvgJob& j, hipStream_t st) {
+  if (j.n < 1 || j.n > kMaxAvgSets || j.nseg < 1 || j.nseg > kMaxAvgSegs) return hipErrorInvalidValue;
+  const int64_t total = j.first[j.nseg];
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_avg, dim3(grid_for(total, 256, 2048)), dim3(256), 0, st, j);
   return hipGetLastError();
 }
 

@@ -31,8 +31,9 @@ EXPORTS = ("vfl_workspace_size", "vfl_create", "vfl_create_static", "vfl_set_par
            "vfl_step", "vfl_get_message", "vfl_get_trace", "vfl_schedule_tick", "vfl_check",
            "vfl_philox", "vfl_timing_enable", "vfl_timing_read", "vfl_bind_dataset", "vfl_run",
            "vfl_state_size", "vfl_get_state", "vfl_set_state", "vfl_discard", "vfl_plan", "vfl_fit_delay",
+           "vfl_sync_interval", "vfl_replica_average",
            "vfl_last_error", "vfl_destroy")
-KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt")
+KERNEL_CLASSES = ("fwd", "active", "bwd", "dw", "reduce", "cast", "emb_sgd", "gemm", "dwt", "avg")
 
 
 class vfl_plan_party(C.Structure):
@@ -103,6 +104,8 @@ def _load():
         "vfl_get_message": [P, I32, I64, P, SZ, C.POINTER(I32)],
         "vfl_get_trace": [P, C.POINTER(I64), SZ, C.POINTER(SZ)],
         "vfl_schedule_tick": [I64, I32, I64, C.POINTER(I64)],
+        "vfl_sync_interval": [I32, I64, C.POINTER(I32)],
+        "vfl_replica_average": [C.POINTER(P), I32, U32],
         "vfl_check": [P, C.POINTER(U32)],
         "vfl_philox": [U64, U32, U32, U32, I32, I32, P, P],
         "vfl_timing_enable": [P, U32],
@@ -224,6 +227,17 @@ def vfl_schedule_tick(t: int, s: int, n_groups: int):
     out = (C.c_int64 * 7)()
     _chk(_lib.vfl_schedule_tick(t, s, n_groups, out), "vfl_schedule_tick")
     return tuple(out)
+
+
+def vfl_sync_interval(dt0: int, t: int) -> int:
+    v = C.c_int32(0)
+    _chk(_lib.vfl_sync_interval(dt0, t, C.byref(v)), "vfl_sync_interval")
+    return v.value
+
+
+def vfl_replica_average(ctxs, parties: int):
+    arr = (C.c_void_p * len(ctxs))(*[h.value if isinstance(h, C.c_void_p) else h for h in ctxs])
+    _chk(_lib.vfl_replica_average(arr, len(ctxs), parties), "vfl_replica_average", ctxs[0] if ctxs else None)
 
 
 def vfl_check(ctx) -> int:
