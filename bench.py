@@ -61,6 +61,7 @@ KERNEL_SOURCES = {
     "bwd": (("k_bwd<",), ["chain.hip"]), "dw": (("k_dw<", "k_dw32<"), ["dw.hip"]),
     "dwt": (("k_dwt(",), ["dw.hip"]),
     "reduce": (("k_dw_reduce<",), ["dw.hip"]), "cast": (("k_cast<",), ["rowops.hip"]),
+    "avg": (("k_avg(",), ["rowops.hip"]),
     "emb_sgd": (("k_embed_sgd",), ["embed.hip"]), "gemm": (("k_lin(",), ["lin.hip"]),
 }
 
@@ -197,6 +198,75 @@ def serial_probe(w, data, params, epoch, ticks: int = 24) -> dict:
     return out
 
 
+def semi_async(args, w, data, params) -> dict:
+    """The workload as k semi-asynchronous workers (one context each, over a
+    contiguous 1/k of the rows; Section 4.1, Eq. 5): every worker runs `unit`
+    ticks by graph replay, then both parties are averaged when Algorithm 1's
+    test holds for unit t.  Returns the JSON line's fields."""
+    import torch
+    import vfl_synth as S
+    from paper_2510_12494_amd import vfl as V
+    from paper_2510_12494_amd.session import Session
+    k, s, U = w.replicas, w.staleness, args.unit
+    wr = w.replace(replicas=1)
+    n = data["y"].shape[0] // k
+    shards = [{key: (None if v is None else v[r * n:(r + 1) * n]) for key, v in data.items()}
+              for r in range(k)]
+    sess = [Session(wr, shards[r], params, lambda g: S.group_rows(wr, g, n)) for r in range(k)]
+    both = (1 << V.VFL_PARTY_A) | (1 << V.VFL_PARTY_B)
+    n_avg = [0]
+
+    def advance(t, stop, graph):
+        # ticks t .. stop-1, averaging after every unit that Eq. 5 selects
+        while t < stop:
+            end = min(stop, (t // U + 1) * U)
+            for ss in sess:
+                if graph:
+                    ss.run(t, end - t)
+                else:
+                    for tt in range(t, end):
+                        ss.step(tt)
+            t = end
+            if t % U == 0 and t > s and (t // U) % V.vfl_sync_interval(args.dt0, t // U) == 0:
+                V.vfl_replica_average([ss.ctx for ss in sess], both)
+                n_avg[0] += 1
+        return t
+
+    try:
+        warm = max(args.warmup, 2 * (s + 1))
+        t = advance(0, warm, False)
+        for ss in sess:
+            ss.bind()
+        avg_i = V.KERNEL_CLASSES.index("avg")
+        V.vfl_timing_enable(sess[0].ctx, 1 << avg_i)
+        t = advance(t, t + args.steps, True)          # captures the replayed graphs
+        V.vfl_timing_read(sess[0].ctx, avg_i)
+        torch.cuda.synchronize()
+        n_avg[0] = 0
+        t0 = time.perf_counter()
+        t = advance(t, t + args.steps, True)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        ms, launches, work = V.vfl_timing_read(sess[0].ctx, avg_i)
+        V.vfl_timing_enable(sess[0].ctx, 0)
+    finally:
+        for ss in sess:
+            ss.close()
+    avg_s = ms / 1e3 / max(launches, 1)
+    per_launch = work / max(launches, 1)
+    achieved = per_launch / avg_s if avg_s > 0 else 0.0
+    return {
+        "value": args.steps * w.rows_per_tick / dt, "ms_per_step": dt / args.steps * 1e3,
+        "warmup": warm,
+        "semi_async": {"workers": k, "rows_per_worker_tick": w.batch, "dt0": args.dt0,
+                       "unit_ticks": U, "averages_in_timed_region": n_avg[0]},
+        "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": None,
+                     "kernel": "avg", "launches": launches, "avg_us": avg_s * 1e6,
+                     "work_per_launch": per_launch},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -212,6 +282,11 @@ def main():
                     help="no GPU: summarise two rocprofv3 --pmc runs (FETCH_SIZE, "
                          "WRITE_SIZE) into profiles/traffic_<kernel>.json")
     ap.add_argument("--kernel", default="active", choices=sorted(KERNEL_SOURCES))
+    ap.add_argument("--semi-async", action="store_true",
+                    help="run the workload as k semi-asynchronous workers averaged on the "
+                         "schedule of Eq. 5 (roofline: the averaging kernel)")
+    ap.add_argument("--dt0", type=int, default=5, help="initial interval of Eq. 5")
+    ap.add_argument("--unit", type=int, default=1, help="ticks per unit t of Eq. 5")
     args = ap.parse_args()
     if args.traffic_summary:
         res = traffic_summary(*args.traffic_summary, args.kernel, args.copy_bytes)
@@ -241,6 +316,22 @@ def main():
     w = S.get(args.workload)
     data = S.generate(w)
     params = S.init_params(w)
+    if args.semi_async:
+        res = semi_async(args, w, data, params)
+        out = {
+            "metric": METRIC, "value": res["value"], "unit": "samples/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": res["warmup"], "ms_per_step": res["ms_per_step"],
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": w.dtype, "data": "synthetic (seeded, resident in HBM)",
+            "mfma_util_pct": 100.0 * gemm_flops_per_tick(w) / (res["ms_per_step"] / 1e3) / PEAK[w.dtype],
+            "config": {"workload": w.name, "mode": "semi-asynchronous workers",
+                       **res["semi_async"], "staleness": w.staleness},
+            "roofline": res["roofline"],
+        }
+        if not args.no_cpu_baseline:
+            out["cpu_baseline"] = cpu_baseline(w, data, params, args.cpu_seconds)
+        print(json.dumps(out), flush=True)
+        return
     epoch = w.ticks_per_epoch()
     probe = serial_probe(w, data, params, epoch)
     dom = max(probe, key=lambda k: probe[k][0])

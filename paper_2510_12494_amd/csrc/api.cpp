@@ -1873,7 +1873,7 @@ vfl_status vfl_run(vfl_ctx* c, int64_t t0, int64_t n, float* loss_ring, int64_t 
   src.base = t0; src.n_rows = c->n_rows; src.R = p.R; src.s = s; src.lr = c->o.lr;
   src.vofs = (int32_t)vofs;
   src.loss_len = loss_ring ? loss_len : 1;
-  HIPCHK(hipMemcpyAsync(at<TickSrc>(c, p.tsrc), &src, sizeof(src), hipMemcpyHostToDevice, c->sa));
+  HIPCHK(launch_tick_set(at<TickSrc>(c, p.tsrc), src, c->sa));
   // the graphs run both parties' work from stream A: they must follow the
   // work already enqueued on stream B
   HIPCHK(hipEventRecord(c->ev_fork, c->sb));
@@ -1930,28 +1930,30 @@ vfl_status vfl_replica_average(vfl_ctx* const* ctxs, int32_t n, uint32_t parties
     if (pa.device != dev) return fail(c0, VFL_E_INVALID, "contexts must live on the current device");
   }
   const Plan& p = c0->p;
+  // one launch for the selected parties; weights per party: the rows each
+  // context applied since that party's last average
+  AvgJob j;
+  j.n = n;
+  j.first[0] = 0;
+  for (int i = 0; i < n; ++i) j.base[i] = ctxs[i]->ws;
   for (int party = 0; party < 2; ++party) {
     if (!(parties & (1u << party))) continue;
-    // weights: rows applied since the last average
     int64_t tot = 0;
     for (int i = 0; i < n; ++i) tot += party == 0 ? ctxs[i]->a_rows_avg : ctxs[i]->b_rows_avg;
     if (tot <= 0) return fail(c0, VFL_E_STATE, "no rows applied since the last average");
-    AvgJob j;
-    j.n = n;
     for (int i = 0; i < n; ++i) {
       const int64_t r = party == 0 ? ctxs[i]->a_rows_avg : ctxs[i]->b_rows_avg;
-      j.w[i] = (float)((double)r / (double)tot);
-      j.base[i] = ctxs[i]->ws;
+      j.w[party][i] = (float)((double)r / (double)tot);
     }
     // the party's float32 masters: bottom layers, table, and for A the top
     const Party& P = party == 0 ? p.A : p.P;
     auto seg = [&](size_t off, int64_t cnt) {
       j.off[j.nseg] = (int64_t)off;
       j.cnt[j.nseg] = cnt;
+      j.wsel[j.nseg] = (uint8_t)party;
       j.first[j.nseg + 1] = j.first[j.nseg] + (cnt + 3) / 4;
       ++j.nseg;
     };
-    j.first[0] = 0;
     for (int l = 0; l < P.L; ++l) {
       seg(P.W[l], (int64_t)P.out[l] * P.in[l]);
       seg(P.b[l], P.out[l]);
@@ -1962,47 +1964,62 @@ vfl_status vfl_replica_average(vfl_ctx* const* ctxs, int32_t n, uint32_t parties
         seg(p.T.W[l], (int64_t)p.T.out[l] * p.T.in[l]);
         seg(p.T.b[l], p.T.out[l]);
       }
-    // ordered after every context's pending work on the party's stream;
-    // the contexts' later work on it after the average
-    auto pst = [&](vfl_ctx* c) { return party == 0 ? c->sa : c->sb; };
-    hipStream_t st0 = pst(c0);
-    for (int i = 1; i < n; ++i) {
-      HIPCHK0(c0, hipEventRecord(ctxs[i]->ev_avg, pst(ctxs[i])));
+  }
+  // ordered after every context's pending work on the selected parties'
+  // streams, and their later work after the average
+  const bool pa = parties & 1u, pb = parties & 2u;
+  hipStream_t st0 = pa ? c0->sa : c0->sb;
+  auto streams = [&](vfl_ctx* c, hipStream_t out[2]) {
+    int m = 0;
+    if (pa) out[m++] = c->sa;
+    if (pb && !(pa && c->sb == c->sa)) out[m++] = c->sb;
+    return m;
+  };
+  for (int i = 0; i < n; ++i) {
+    hipStream_t q[2];
+    const int m = streams(ctxs[i], q);
+    for (int k = 0; k < m; ++k) {
+      if (q[k] == st0) continue;
+      HIPCHK0(c0, hipEventRecord(ctxs[i]->ev_avg, q[k]));
       HIPCHK0(c0, hipStreamWaitEvent(st0, ctxs[i]->ev_avg, 0));
     }
-    {
-      vfl_ctx* c = c0;
-      double bytes = 0;
-      for (int q = 0; q < j.nseg; ++q) bytes += 8.0 * n * (double)j.cnt[q];
-      TIMED(VFL_K_AVG, bytes, st0, launch_avg(j, st0));
+  }
+  {
+    vfl_ctx* c = c0;
+    double bytes = 0;
+    for (int q = 0; q < j.nseg; ++q) bytes += 8.0 * n * (double)j.cnt[q];
+    TIMED(VFL_K_AVG, bytes, st0, launch_avg(j, st0));
+  }
+  HIPCHK0(c0, hipEventRecord(c0->ev_avg, st0));
+  for (int i = 0; i < n; ++i) {
+    vfl_ctx* c = ctxs[i];
+    hipStream_t q[2];
+    const int m = streams(c, q);
+    for (int k = 0; k < m; ++k)
+      if (q[k] != st0) HIPCHK0(c0, hipStreamWaitEvent(q[k], c0->ev_avg, 0));
+    // operand copies of the averaged weights: A's current copies; B's
+    // copies in the slot of its next forward when that slot is free (the
+    // slots of groups in flight keep the weights their forward used)
+    vfl_status r;
+    if (pa) {
+      if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
+      c->a_copy_version = c->a_version;
+      c->a_rows_avg = 0;
     }
-    HIPCHK0(c0, hipEventRecord(c0->ev_avg, st0));
-    for (int i = 0; i < n; ++i) {
-      vfl_ctx* c = ctxs[i];
-      if (i > 0) HIPCHK0(c0, hipStreamWaitEvent(pst(c), c0->ev_avg, 0));
-      // operand copies of the averaged weights: A's current copies; B's
-      // copies in the slot of its next forward when that slot is free (the
-      // slots of groups in flight keep the weights their forward used)
-      vfl_status r;
-      if (party == 0) {
-        if ((r = enqueue_cast(c, p.A, 0, &p.T, c->sa))) return r;
-        c->a_copy_version = c->a_version;
-        c->a_rows_avg = 0;
-      } else {
-        const int S1 = p.s + 1;
-        for (int q = 0; q < S1; ++q) {
-          bool busy = false;
-          for (int64_t g = c->b_next_bwd; g < c->b_next_fwd; ++g) busy |= (int)(g % S1) == q;
-          if (busy) continue;
-          if (q == (int)(c->b_next_fwd % S1)) {
-            if ((r = enqueue_cast(c, p.P, q, nullptr, c->sb))) return r;
-            c->b_copy_version[q] = c->b_version;
-          } else {
-            c->b_copy_version[q] = -1;
-          }
+    if (pb) {
+      const int S1 = p.s + 1;
+      for (int qs = 0; qs < S1; ++qs) {
+        bool busy = false;
+        for (int64_t g = c->b_next_bwd; g < c->b_next_fwd; ++g) busy |= (int)(g % S1) == qs;
+        if (busy) continue;
+        if (qs == (int)(c->b_next_fwd % S1)) {
+          if ((r = enqueue_cast(c, p.P, qs, nullptr, c->sb))) return r;
+          c->b_copy_version[qs] = c->b_version;
+        } else {
+          c->b_copy_version[qs] = -1;
         }
-        c->b_rows_avg = 0;
       }
+      c->b_rows_avg = 0;
     }
   }
   return VFL_OK;

@@ -97,6 +97,8 @@ __device__ __forceinline__ TickArgs tick_args(const TickRef& r) {
 
 // the graph's last node: base += cyc
 hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st);
+// the record a run of replays starts from (a one-thread kernel: no copy)
+hipError_t launch_tick_set(TickSrc* dst, const TickSrc& v, hipStream_t st);
 
 // ------------------------------------------------------------ chain kernels
 // LDS region of a row block: byte offset in the kernel's dynamic LDS and row
@@ -353,16 +355,18 @@ hipError_t launch_lin(const LinJob* job, int blocks, int rows, TickRef tr, hipSt
 // ------------------------------------------------------- replica averaging
 // In place over n parameter sets of the same layout (base[i]: a context's
 // workspace): every float32 element x of the segments becomes
-// sum_i w[i] * x_i (accumulated in the order i = 0 .. n-1), written back to
-// every set.  Segment s: cnt[s] floats at byte offset off[s] (16-byte
-// aligned); first[s] = float4 units before segment s (first[nseg] = total).
+// sum_i w[ws][i] * x_i (accumulated in the order i = 0 .. n-1; ws = the
+// segment's weight set), written back to every set.  Segment s: cnt[s]
+// floats at byte offset off[s] (16-byte aligned), weight set wsel[s];
+// first[s] = float4 units before segment s (first[nseg] = total).
 constexpr int kMaxAvgSets = 16;
-constexpr int kMaxAvgSegs = 2 * kMaxChain + 4;    // A: its layers, the top layers, the logit layer, a table
+constexpr int kMaxAvgSegs = 2 * (2 * kMaxChain + 4);   // both parties' layers, the top, tables
 struct AvgJob {
   int32_t n = 0, nseg = 0;
-  float w[kMaxAvgSets];
+  float w[2][kMaxAvgSets];
   char* base[kMaxAvgSets];
   int64_t off[kMaxAvgSegs], cnt[kMaxAvgSegs], first[kMaxAvgSegs + 1];
+  uint8_t wsel[kMaxAvgSegs];
 };
 hipError_t launch_avg(const AvgJob& j, hipStream_t st);
 

@@ -32,6 +32,10 @@ __global__ void k_tick_base(TickSrc* src, int cyc) {
   if (threadIdx.x == 0 && blockIdx.x == 0) src->base += cyc;
 }
 
+__global__ void k_tick_set(TickSrc* dst, TickSrc v) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *dst = v;
+}
+
 __global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t step, uint32_t tag,
                                                       uint32_t row0, int rows, int groups,
                                                       uint32_t* out) {
@@ -48,8 +52,9 @@ __global__ __launch_bounds__(256) void k_philox_words(uint64_t seed, uint32_t st
 
 // ------------------------------------------------------- replica averaging
 // One thread per float4 unit of the segment list (a scalar tail where a
-// segment's length is not a multiple of 4): reads the unit from every set,
+// segment's length is not a multiple of 4): loads the unit from all N sets,
 // forms the weighted sum in a fixed order and writes it to every set.
+template <int N>
 __global__ __launch_bounds__(256) void k_avg(AvgJob j) {
   const int64_t total = j.first[j.nseg];
   for (int64_t u = blockIdx.x * 256 + threadIdx.x; u < total; u += (int64_t)gridDim.x * 256) {
@@ -62,25 +67,36 @@ __global__ __launch_bounds__(256) void k_avg(AvgJob j) {
     const int64_t e = (u - j.first[lo]) * 4;      // first float of the unit
     const int64_t cnt = j.cnt[lo];
     const int64_t off = j.off[lo] + e * 4;
+    const float* w = j.w[j.wsel[lo]];
     if (e + 4 <= cnt) {
+      float4 v[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) v[i] = *(const float4*)(j.base[i] + off);
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int i = 0; i < j.n; ++i) {
-        const float4 v = *(const float4*)(j.base[i] + off);
-        const float w = j.w[i];
-        acc.x = fmaf(w, v.x, acc.x);
-        acc.y = fmaf(w, v.y, acc.y);
-        acc.z = fmaf(w, v.z, acc.z);
-        acc.w = fmaf(w, v.w, acc.w);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        acc.x = fmaf(w[i], v[i].x, acc.x);
+        acc.y = fmaf(w[i], v[i].y, acc.y);
+        acc.z = fmaf(w[i], v[i].z, acc.z);
+        acc.w = fmaf(w[i], v[i].w, acc.w);
       }
-      for (int i = 0; i < j.n; ++i) *(float4*)(j.base[i] + off) = acc;
+#pragma unroll
+      for (int i = 0; i < N; ++i) *(float4*)(j.base[i] + off) = acc;
     } else {
       for (int64_t q = 0; q < cnt - e; ++q) {
         float acc = 0.f;
-        for (int i = 0; i < j.n; ++i) acc = fmaf(j.w[i], ((const float*)(j.base[i] + off))[q], acc);
-        for (int i = 0; i < j.n; ++i) ((float*)(j.base[i] + off))[q] = acc;
+#pragma unroll
+        for (int i = 0; i < N; ++i) acc = fmaf(w[i], ((const float*)(j.base[i] + off))[q], acc);
+#pragma unroll
+        for (int i = 0; i < N; ++i) ((float*)(j.base[i] + off))[q] = acc;
       }
     }
   }
+}
+
+template <int N>
+void launch_avg_n(const AvgJob& j, int grid, hipStream_t st) {
+  hipLaunchKernelGGL(k_avg<N>, dim3(grid), dim3(256), 0, st, j);
 }
 
 int grid_for(int64_t work, int per_block, int cap) {
@@ -91,6 +107,11 @@ int grid_for(int64_t work, int per_block, int cap) {
 
 hipError_t launch_tick_base(TickSrc* src, int cyc, hipStream_t st) {
   hipLaunchKernelGGL(k_tick_base, dim3(1), dim3(64), 0, st, src, cyc);
+  return hipGetLastError();
+}
+
+hipError_t launch_tick_set(TickSrc* dst, const TickSrc& v, hipStream_t st) {
+  hipLaunchKernelGGL(k_tick_set, dim3(1), dim3(64), 0, st, dst, v);
   return hipGetLastError();
 }
 
@@ -106,7 +127,25 @@ hipError_t launch_avg(const AvgJob& j, hipStream_t st) {
   if (j.n < 1 || j.n > kMaxAvgSets || j.nseg < 1 || j.nseg > kMaxAvgSegs) return hipErrorInvalidValue;
   const int64_t total = j.first[j.nseg];
   if (total == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_avg, dim3(grid_for(total, 256, 2048)), dim3(256), 0, st, j);
+  const int g = grid_for(total, 256, 4096);
+  switch (j.n) {
+    case 1: launch_avg_n<1>(j, g, st); break;
+    case 2: launch_avg_n<2>(j, g, st); break;
+    case 3: launch_avg_n<3>(j, g, st); break;
+    case 4: launch_avg_n<4>(j, g, st); break;
+    case 5: launch_avg_n<5>(j, g, st); break;
+    case 6: launch_avg_n<6>(j, g, st); break;
+    case 7: launch_avg_n<7>(j, g, st); break;
+    case 8: launch_avg_n<8>(j, g, st); break;
+    case 9: launch_avg_n<9>(j, g, st); break;
+    case 10: launch_avg_n<10>(j, g, st); break;
+    case 11: launch_avg_n<11>(j, g, st); break;
+    case 12: launch_avg_n<12>(j, g, st); break;
+    case 13: launch_avg_n<13>(j, g, st); break;
+    case 14: launch_avg_n<14>(j, g, st); break;
+    case 15: launch_avg_n<15>(j, g, st); break;
+    default: launch_avg_n<16>(j, g, st); break;
+  }
   return hipGetLastError();
 }
 
