@@ -54,6 +54,28 @@ __device__ __forceinline__ void sgd_store4(const DwProb& P, int n, int kb, const
   }
 }
 
+// The problem, output tile and row chunk of this block (tile_w: the square
+// tile width).  Workgroups are dealt to the 8 XCDs round-robin (block b on
+// XCD b mod 8); XCD x takes the contiguous range [x * per, (x + 1) * per)
+// of the job's work items, ordered problem by problem and chunk by chunk
+// with the chunk's tiles innermost, so that the tiles reading the same rows
+// of the same operands run at the same time on one XCD and share its L2.
+// False for the blocks that round the grid up to a multiple of 8.
+__device__ __forceinline__ bool dw_item(const DwJob& J, int tile_w, int& q, int& tile, int& split) {
+  const int per = (J.blocks + 7) / 8;
+  const int v = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (v >= J.blocks) return false;
+  q = 0;
+#pragma unroll 1
+  while (q + 1 < J.n && v >= J.p[q + 1].first_block) ++q;
+  const DwProb& P = J.p[q];
+  const int tiles = ((P.N + tile_w - 1) / tile_w) * ((P.K + tile_w - 1) / tile_w);
+  const int lb = v - P.first_block;
+  split = lb / tiles;
+  tile = lb % tiles;
+  return true;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Rarg, float scale_arg,
                                             TickRef tr) {
@@ -61,13 +83,10 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
   constexpr int KR = 4 * RR;                // rows per MFMA step
   constexpr int PF = 4;                     // MFMA steps per load group
   const DwJob& J = *jp;
-  int q = 0;
-#pragma unroll 1
-  while (q + 1 < J.n && (int)blockIdx.x >= J.p[q + 1].first_block) ++q;
+  int q, tile, split;
+  if (!dw_item(J, 64, q, tile, split)) return;
   const DwProb& P = J.p[q];
-  const int lb = blockIdx.x - P.first_block;
   const int tiles_k = (P.K + 63) / 64;
-  const int tile = lb / P.splits, split = lb % P.splits;
   const int n0 = (tile / tiles_k) * 64, k0 = (tile % tiles_k) * 64;
   float scale = scale_arg;
   if (tr.src) scale = tick_args(tr).scale;
@@ -257,13 +276,10 @@ __global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp) {
   typedef __attribute__((ext_vector_type(16))) float f32x16;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const DwJob& J = *jp;
-  int q = 0;
-#pragma unroll 1
-  while (q + 1 < J.n && (int)blockIdx.x >= J.p[q + 1].first_block) ++q;
+  int q, tile, split;
+  if (!dw_item(J, kDwtK, q, tile, split)) return;
   const DwProb& P = J.p[q];
-  const int lb = blockIdx.x - P.first_block;
   const int tiles_k = (P.K + kDwtK - 1) / kDwtK;
-  const int tile = lb / P.splits, split = lb % P.splits;
   const int n0 = (tile / tiles_k) * kDwtN, k0 = (tile % tiles_k) * kDwtK;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -653,8 +669,9 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
 hipError_t launch_dw(Elt e, const DwJob* job, int blocks, int R, float scale, TickRef tr,
                      hipStream_t st) {
   if (blocks < 1) return hipErrorInvalidValue;
-  if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
-  else hipLaunchKernelGGL(k_dw<float>, dim3(blocks), dim3(256), 0, st, job, R, scale, tr);
+  const int grid = (blocks + 7) / 8 * 8;       // see dw_item
+  if (e == BF16) hipLaunchKernelGGL(k_dw<uint16_t>, dim3(grid), dim3(256), 0, st, job, R, scale, tr);
+  else hipLaunchKernelGGL(k_dw<float>, dim3(grid), dim3(256), 0, st, job, R, scale, tr);
   return hipGetLastError();
 }
 
@@ -664,7 +681,7 @@ hipError_t dwt_init() {
 
 hipError_t launch_dwt(const DwJob* job, int blocks, hipStream_t st) {
   if (blocks < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_dwt, dim3(blocks), dim3(256), kDwtLds, st, job);
+  hipLaunchKernelGGL(k_dwt, dim3((blocks + 7) / 8 * 8), dim3(256), kDwtLds, st, job);   // see dw_item
   return hipGetLastError();
 }
 
