@@ -238,8 +238,8 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
 
 // Large-tile weight gradient for bf16 operands and long groups: a block of
 // 256 threads owns a kDwtN x kDwtK (256 x 256) output tile of one problem
-// and one row chunk.  Rows go through LDS in stages of 32 (four 32 KB
-// buffers, three stages in flight, one barrier per stage), copied from
+// and one row chunk.  Rows go through LDS in stages of 32 (five 32 KB
+// buffers, one barrier per stage), copied from
 // global memory straight into LDS (global_load_lds_dwordx4) in the order
 // the matrix cores read them: one 1 KB block per 32 x 16 operand fragment of
 // v_mfma_f32_32x32x16_bf16, which in the row-chunked layout is 32
@@ -249,9 +249,9 @@ __global__ __launch_bounds__(256) void k_dw(const DwJob* __restrict__ jp, int Ra
 // outputs x 128 inputs: X fragments as the A operand (32 inputs x 16 rows),
 // D fragments as the B operand (16 rows x 32 outputs), so a lane
 // accumulates four runs of four consecutive inputs k of one output n; per
-// 16-row step 4 X and 4 D fragments feed 16 MFMAs, with the next step's
-// fragment reads issued between them.  The bias gradient is summed from the
-// D fragments of the wavefronts with wk == 0 in the tiles at k0 == 0 (one
+// 16-row step 4 X and 4 D fragments feed 16 MFMAs, and the next stage's
+// fragment reads are issued between the two steps of a stage.  The bias
+// gradient is summed from the D fragments of the wavefronts with wk == 0 in the tiles at k0 == 0 (one
 // v_dot2_f32_bf16 against (1, 1) per two rows).  The row chunks always
 // write float32 partials (as k_dw's split problems; tiles counted 256 x
 // 256): k_dw_reduce sums them and makes the SGD step.
@@ -259,15 +259,16 @@ constexpr int kDwtN = 256, kDwtK = 256;
 constexpr int kDwtStageRows = 32;
 constexpr int kDwtFrag = 1024;                              // one 32 x 16 bf16 fragment
 constexpr int kDwtStageBytes = 2 * (kDwtN / 32) * 2 * kDwtFrag;   // 16 X + 16 D fragments
-constexpr int kDwtBufs = 4;                                 // three stages in flight
+constexpr int kDwtBufs = 5;                                 // up to four stages in flight
 constexpr int kDwtLds = kDwtBufs * kDwtStageBytes;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// wait until at most n (0, 8 or 16) of this wave's vector-memory operations
+// wait until at most n (0, 8, 16 or 24) of this wave's vector-memory operations
 // are outstanding (expcnt and lgkmcnt unconstrained)
 __device__ __forceinline__ void wait_vm(int n) {
-  if (n >= 16) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4));
+  if (n >= 24) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4) | 8);
+  else if (n >= 16) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4));
   else if (n >= 8) __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4) | 8);
   else __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4));
 }
@@ -346,38 +347,58 @@ __global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp) {
       bsum[nb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), kOnes2, bsum[nb], false);
     }
   };
-  auto interleave = [] {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  };
 
   // the chunk is contracted whole (rps rows, a multiple of the stage; the
-  // delta rows past the group are zero)
+  // delta rows past the group are zero).  Software pipeline: the fragment
+  // reads of stage s + 1 are issued between the two halves of the products
+  // of stage s (two register sets), after the barrier that makes stage s + 1
+  // visible; that
+  // barrier also retires the buffer of stage s - 1, which then takes the
+  // copies of stage s + kDwtBufs - 1.
+  struct Frags { u32x4 xa0[4], db0[4], xa1[4], db1[4]; };
   const int nst = P.rps / kDwtStageRows;
-  for (int s = 0; s < kDwtBufs - 1 && s < nst; ++s) issue(s);
-#pragma unroll 1
-  for (int s = 0; s < nst; ++s) {
-    // this wave's copies of stage s have landed; after the (unfenced)
-    // barrier every wave's have, and every wave is done with stage s - 1
-    wait_vm(8 * min(kDwtBufs - 2, nst - 1 - s));
-    __builtin_amdgcn_s_barrier();
-    if (s + kDwtBufs - 1 < nst) issue(s + kDwtBufs - 1);
+  auto read_stage = [&](int s, Frags& f) {
     const char* S = smem + (s % kDwtBufs) * kDwtStageBytes;
-    u32x4 xa0[4], db0[4], xa1[4], db1[4];
-    frags(S, 0, xa0, db0);
-    frags(S, 1, xa1, db1);
-    mma(xa0, db0);
-    interleave();
-    mma(xa1, db1);
-    if (do_bias) {
-      bias_sums(db0);
-      bias_sums(db1);
+    frags(S, 0, f.xa0, f.db0);
+    frags(S, 1, f.xa1, f.db1);
+  };
+  auto step = [&](int s, const Frags& x, Frags& y) {
+    if (s + 1 < nst) {
+      // this wave's copies of stage s + 1 have landed (later stages may be
+      // in flight); after the unfenced barrier every wave's have
+      wait_vm(8 * min(kDwtBufs - 3, nst - 2 - s));
+      __builtin_amdgcn_s_barrier();
+      if (s + kDwtBufs - 1 < nst) issue(s + kDwtBufs - 1);
     }
+    // the next stage's reads go between the two halves of this stage's
+    // products: the wait for x (read a step earlier) comes before the first
+    // half, and nothing waits for y until the next step (after the last
+    // stage a harmless re-read of it, so that y is always written and the
+    // two register sets are never both live across a step).  The scheduling
+    // barriers keep the compiler from sinking each read to its first use.
+    __builtin_amdgcn_sched_barrier(0);
+    mma(x.xa0, x.db0);
+    __builtin_amdgcn_sched_barrier(0);
+    read_stage(min(s + 1, nst - 1), y);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(x.xa1, x.db1);
+    if (do_bias) {
+      bias_sums(x.db0);
+      bias_sums(x.db1);
+    }
+  };
+  for (int s = 0; s < kDwtBufs - 1 && s < nst; ++s) issue(s);
+  Frags fa, fb;
+  wait_vm(8 * min(kDwtBufs - 2, nst - 1));
+  __builtin_amdgcn_s_barrier();
+  read_stage(0, fa);
+  int s = 0;
+#pragma unroll 1
+  for (; s + 1 < nst; s += 2) {
+    step(s, fa, fb);
+    step(s + 1, fb, fa);
   }
+  if (s < nst) step(s, fa, fb);
 
   if (do_bias) {
 #pragma unroll

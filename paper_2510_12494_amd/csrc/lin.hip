@@ -4,8 +4,7 @@
 // in the RC layout the weight gradient reads.
 //
 // A block of 256 threads owns a 256-row x 256-output tile; K goes through
-// LDS in stages of 32 (four 32 KB buffers, three stages in flight, one
-// barrier per stage).  Each stage is copied from global memory straight
+// LDS in stages of 32 (five 32 KB buffers, one barrier per stage).  Each stage is copied from global memory straight
 // into LDS (global_load_lds_dwordx4: no registers, no LDS store
 // instructions) in the order the matrix cores read it: one 1 KB block per
 // 32 x 16 operand fragment of v_mfma_f32_32x32x16_bf16, lane l's 16 bytes
@@ -15,8 +14,9 @@
 // 4-7), waves 2 and 3 the W fragments (gathered from the packed weight
 // copy, whose 16 x 32 fragments hold the same 16-byte chunks in another
 // order).  Wavefront (wm, wn) of the 2 x 2 grid computes 128 x 128 of the
-// tile: per 16-deep step 4 A and 4 W fragments feed 16 MFMAs, with the
-// next step's fragment reads issued between them.  The tiles are dealt to
+// tile: per 16-deep step 4 A and 4 W fragments feed 16 MFMAs, and the next
+// stage's fragment reads are issued between the two steps of a stage.  The
+// tiles are dealt to
 // the XCDs in contiguous ranges, so the output tiles that share an A row
 // slab meet in one L2.
 //
@@ -39,7 +39,7 @@ constexpr int kFragBytes = 1024;                        // one 32 x 16 bf16 oper
 constexpr int kAFrags = kBM / 32 * (kBK / 16);          // A fragments per stage (16)
 constexpr int kWFrags = kBN / 32 * (kBK / 16);          // W fragments per stage (16)
 constexpr int kStageBytes = (kAFrags + kWFrags) * kFragBytes;   // 32 KB
-constexpr int kStages = 4;                              // buffers; 3 stages in flight
+constexpr int kStages = 5;                              // buffers: up to 4 stages in flight
 // epilogue staging: the tile column by column, kOutPitch bytes per column,
 // its 8-row chunks swizzled (see out_slot) so that both the lanes' 8-byte
 // writes and the threads' 16-byte reads spread over the LDS banks
@@ -57,10 +57,11 @@ __device__ __forceinline__ void dma16(const VFL_GLOBAL char* g, char* lds) {
   __builtin_amdgcn_global_load_lds((VFL_GLOBAL void*)g, (lds_t*)lds, 16, 0, 0);
 }
 
-// wait until at most n (0, 8 or 16) of this wave's vector-memory operations
+// wait until at most n (0, 8, 16 or 24) of this wave's vector-memory operations
 // are outstanding (expcnt and lgkmcnt unconstrained)
 __device__ __forceinline__ void wait_vm(int n) {
-  if (n >= 16) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4));
+  if (n >= 24) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4) | 8);
+  else if (n >= 16) __builtin_amdgcn_s_waitcnt((1 << 14) | (15 << 8) | (7 << 4));
   else if (n >= 8) __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4) | 8);
   else __builtin_amdgcn_s_waitcnt((15 << 8) | (7 << 4));
 }
@@ -166,37 +167,52 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8, a[mb]), __builtin_bit_cast(bf16x8, w[nb]), acc[mb][nb], 0, 0, 0);
   };
-  // scheduling of one step: its 16 products with the next step's 8
-  // fragment reads issued between the first 8
-  auto interleave = [] {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  };
 
-  // three stages in flight; the buffer a stage is copied into was last read
-  // two barriers earlier
-  for (int s = 0; s < kStages - 1 && s < nst; ++s) issue(s);
-#pragma unroll 1
-  for (int s = 0; s < nst; ++s) {
-    // this wave's copies of stage s have landed (the later stages in flight
-    // may not have); after the barrier every wave's have, and every wave
-    // is done reading the buffer of stage s - 1
-    wait_vm(8 * min(kStages - 2, nst - 1 - s));
-    // a bare barrier: a fenced one would make every wave wait for all of
-    // its copies in flight, the later stages' included
-    __builtin_amdgcn_s_barrier();
-    if (s + kStages - 1 < nst) issue(s + kStages - 1);
+  // Software pipeline: the fragment reads of stage s + 1 are issued between
+  // the two halves of stage s's products (two register sets), after the
+  // barrier that makes stage s + 1 visible; that barrier also retires the
+  // buffer of stage s - 1, which then takes the copies of stage
+  // s + kStages - 1.  (Bare barriers: a fenced one would make every wave
+  // wait for all of its copies in flight, the later stages' included.)
+  struct Frags { u32x4 a0[4], w0[4], a1[4], w1[4]; };
+  auto read_stage = [&](int s, Frags& f) {
     const char* S = smem + (s % kStages) * kStageBytes;
-    u32x4 a0[4], w0[4], a1[4], w1[4];
-    frags(S, 0, a0, w0);
-    frags(S, 1, a1, w1);
-    mma(a0, w0);
-    interleave();
-    mma(a1, w1);
+    frags(S, 0, f.a0, f.w0);
+    frags(S, 1, f.a1, f.w1);
+  };
+  auto run_stage = [&](int s, const Frags& x, Frags& y) {
+    if (s + 1 < nst) {
+      // this wave's copies of stage s + 1 have landed (later stages may be
+      // in flight); after the barrier every wave's have
+      wait_vm(8 * min(kStages - 3, nst - 2 - s));
+      __builtin_amdgcn_s_barrier();
+      if (s + kStages - 1 < nst) issue(s + kStages - 1);
+    }
+    // the wait for x (read a step earlier) comes before the first half;
+    // nothing waits for y until the next step (after the last stage a
+    // harmless re-read of it, so that y is always written and the two
+    // register sets are never both live across a step).  The scheduling
+    // barriers keep the compiler from sinking each read to its first use.
+    __builtin_amdgcn_sched_barrier(0);
+    mma(x.a0, x.w0);
+    __builtin_amdgcn_sched_barrier(0);
+    read_stage(min(s + 1, nst - 1), y);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(x.a1, x.w1);
+  };
+  for (int s = 0; s < kStages - 1 && s < nst; ++s) issue(s);
+  Frags fa, fb;
+  wait_vm(8 * min(kStages - 2, nst - 1));
+  __builtin_amdgcn_s_barrier();
+  read_stage(0, fa);
+  {
+    int s = 0;
+#pragma unroll 1
+    for (; s + 1 < nst; s += 2) {
+      run_stage(s, fa, fb);
+      run_stage(s + 1, fb, fa);
+    }
+    if (s < nst) run_stage(s, fa, fb);
   }
 
   // ------------------------------------------------------------ epilogue
@@ -235,8 +251,11 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
 #pragma unroll
       for (int i = 0; i < kBM / 32; ++i) mb[i] = bp[i];
     }
-#pragma unroll 4
-    for (int rg = 0; rg < ng; ++rg) {
+    // fully unrolled: the mask words stay in registers (a runtime index
+    // would put them in scratch memory)
+#pragma unroll
+    for (int rg = 0; rg < kBM / 8; ++rg) {
+      if (rg >= ng) break;
       const int64_t g = m0 / 8 + rg;
       u32x4 q = mask_tail<uint16_t>(*(const u32x4*)(smem + out_slot(t, rg)), rows - (m0 + 8 * rg));
       const uint32_t byte = mb[rg >> 2] >> (8 * (rg & 3));
