@@ -420,7 +420,12 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
                        const vfl_opts* o, Plan& p) {
   std::string why;
   if (!o) return "null opts";
-  if (o->dtype != VFL_F32 && o->dtype != VFL_BF16) return "dtype must be VFL_F32 or VFL_BF16";
+  // the caller's dtype as the integer it is (a C caller may pass any value;
+  // loading it as the enum type would not be defined for other values)
+  int32_t dtype = 0;
+  static_assert(sizeof(o->dtype) == sizeof(dtype), "vfl_dtype is an int");
+  std::memcpy(&dtype, &o->dtype, sizeof(dtype));
+  if (dtype != VFL_F32 && dtype != VFL_BF16) return "dtype must be VFL_F32 or VFL_BF16";
   if (o->batch < 1) return "batch must be >= 1";
   if (o->staleness < 0 || o->staleness > VFL_MAX_STALENESS) return "staleness out of [0, 4]";
   if (o->replicas < 1 || o->replicas > VFL_MAX_REPLICAS) return "replicas out of [1, 8]";
@@ -439,7 +444,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     return "party A's + the top's hidden layers must be <= " + std::to_string(kMaxDw);
   if ((int64_t)o->batch * o->replicas > (1 << 28)) return "rows per tick too large";
 
-  p.e = o->dtype == VFL_BF16 ? BF16 : F32;
+  p.e = dtype == VFL_BF16 ? BF16 : F32;
   p.s = o->staleness;
   p.k = o->replicas;
   p.B = o->batch;
@@ -480,7 +485,7 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
         double in = a->widths[a->n_layers - 1] + b->widths[b->n_layers - 1];
         for (int j = 0; j + 1 < t->n_layers; ++j) { top_macs += in * t->widths[j]; in = t->widths[j]; }
       }
-      const bool bf = o->dtype == VFL_BF16;
+      const bool bf = dtype == VFL_BF16;
       p.da.tile = bf && 2.0 * p.R * (bottom_macs(a) + top_macs) >= kDwtMinFlops ? 256 : 64;
       p.db.tile = bf && 2.0 * p.R * bottom_macs(b) >= kDwtMinFlops ? 256 : 64;
       const int ta = bottom_tiles(a, p.da.tile) + top_tiles(p.da.tile), tb = bottom_tiles(b, p.db.tile);
