@@ -74,15 +74,16 @@ def source_sha(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(kernel: str, per_launch_work: float):
-    """HBM traffic per launch from the committed rocprofv3 counter summary,
-    or None when there is none or the kernel's sources changed since."""
+def traffic_for(kernel: str, workload: str):
+    """HBM traffic per launch from the committed rocprofv3 counter summary
+    of this kernel class on this workload, or None when there is none or the
+    kernel's sources changed since."""
     p = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
     if not os.path.exists(p):
         return None
     with open(p) as fh:
         t = json.load(fh)
-    if t.get("source_sha") != source_sha(kernel):
+    if t.get("source_sha") != source_sha(kernel) or t.get("workload") != workload:
         return None
     return t.get("bytes_per_launch")
 
@@ -102,13 +103,13 @@ def _counter_rows(d: str, counter: str):
     return out
 
 
-def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int) -> dict:
+def traffic_summary(fetch_dir: str, write_dir: str, kernel: str, copy_bytes: int, workload: str) -> dict:
     """HBM bytes per launch of one kernel class from two rocprofv3 --pmc
     runs of this script with --copy-bytes (FETCH_SIZE, then WRITE_SIZE, KiB
     per dispatch), each counter scaled so that the plain copy of known size
     in the same run reads exactly its bytes."""
     syms = KERNEL_SOURCES[kernel][0]
-    res = {"kernel": kernel, "copy_bytes": copy_bytes}
+    res = {"kernel": kernel, "workload": workload, "copy_bytes": copy_bytes}
     for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _counter_rows(d, name)
         copy = [v for k, v in rows if "copy" in k.lower()]
@@ -289,7 +290,7 @@ def main():
     ap.add_argument("--unit", type=int, default=1, help="ticks per unit t of Eq. 5")
     args = ap.parse_args()
     if args.traffic_summary:
-        res = traffic_summary(*args.traffic_summary, args.kernel, args.copy_bytes)
+        res = traffic_summary(*args.traffic_summary, args.kernel, args.copy_bytes, args.workload)
         with open(os.path.join(ROOT, "profiles", f"traffic_{args.kernel}.json"), "w") as fh:
             json.dump(res, fh, indent=1)
         print(json.dumps(res))
@@ -378,7 +379,7 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_for(dom, per_launch)
+    roof["traffic"] = traffic_for(dom, w.name)
     roof["kernel"] = dom
     roof["launches"] = launches
     roof["avg_us"] = avg_s * 1e6
