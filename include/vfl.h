@@ -387,10 +387,14 @@ vfl_status vfl_plan(const vfl_plan_party* a, const vfl_plan_party* p, const vfl_
 vfl_status vfl_fit_delay(const double* batch, const double* seconds, int32_t n, double* coef,
                          double* expo);
 
-/* Synchronise both streams and report the device-side channel checks: the
- * number of times a consumer found a slot header whose group differs from
- * the one it expected (0 when the channel is race-free). */
-vfl_status vfl_check(vfl_ctx* c, uint32_t* header_mismatches);
+/* Synchronise both streams and report the device-side checks since the
+ * context was created: the number of times a consumer found a slot header
+ * whose group differs from the one it expected (0 when the channel is
+ * race-free), and (bad_ids, may be NULL) the number of categorical ids
+ * outside [0, vocab) that the forwards read.  Such an id is used as the
+ * nearest valid one (0 or vocab - 1), so no access leaves its field's
+ * table; it is counted once per forward that takes its row. */
+vfl_status vfl_check(vfl_ctx* c, uint32_t* header_mismatches, uint32_t* bad_ids);
 
 /* Raw Philox4x32-10 words of the noise generator (enqueued on `stream`,
  * a hipStream_t): out_dev[(r * groups + q) * 4 + i] = word i for counter

@@ -738,6 +738,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     f.in.dense_vec = P.spec.n_cat == 0;
     f.in.T = P.spec.n_cat ? at_f(P.T) : nullptr;
     f.in.idt = P.spec.n_cat ? (int32_t*)(ws + P.idt[q]) : nullptr; f.in.ldi = p.R;
+    f.in.bad_ids = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4 + 1;
     f.in.buf = p.lf.buf[0];
     f.in.rc = rcm(c, P.x0rc[q], P.din);
     f.bt.src = at_f(p.bias_b); f.bt.off = p.lf.bias.off; f.bt.n4 = p.nbias_b / 4;
@@ -769,6 +770,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     a.in.dense_vec = A.spec.n_cat == 0;
     a.in.T = A.spec.n_cat ? at_f(A.T) : nullptr;
     a.in.idt = A.spec.n_cat ? (int32_t*)(ws + A.idt[0]) : nullptr; a.in.ldi = p.R;
+    a.in.bad_ids = (int32_t*)(ws + p.hdr) + 2 * kMaxSlots * 4 + 1;
     a.in.buf = la.in;
     a.in.rc = rcm(c, A.x0rc[0], A.din);
     a.bt.src = at_f(p.bias_a); a.bt.off = la.bias.off; a.bt.n4 = p.nbias_a / 4;
@@ -2067,13 +2069,14 @@ vfl_status vfl_get_trace(vfl_ctx* c, int64_t* buf, size_t cap_rows, size_t* rows
   return VFL_OK;
 }
 
-vfl_status vfl_check(vfl_ctx* c, uint32_t* mismatches) {
+vfl_status vfl_check(vfl_ctx* c, uint32_t* mismatches, uint32_t* bad_ids) {
   if (!c || !mismatches) return VFL_E_INVALID;
   HIPCHK(hipStreamSynchronize(c->sa));
   HIPCHK(hipStreamSynchronize(c->sb));
-  int32_t v = 0;
-  HIPCHK(hipMemcpy(&v, err_ptr(c), sizeof(v), hipMemcpyDeviceToHost));
-  *mismatches = (uint32_t)v;
+  int32_t v[2] = {0, 0};
+  HIPCHK(hipMemcpy(v, err_ptr(c), sizeof(v), hipMemcpyDeviceToHost));
+  *mismatches = (uint32_t)v[0];
+  if (bad_ids) *bad_ids = (uint32_t)v[1];
   return VFL_OK;
 }
 

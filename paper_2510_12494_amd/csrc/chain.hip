@@ -468,6 +468,9 @@ __device__ __forceinline__ void lds_to_rows(const char* s, const LBuf& b, int co
   }
 }
 
+// an embedding id clamped into [0, V)
+__device__ __forceinline__ int32_t clamp_id(int32_t id, int32_t V) { return min(max(id, 0), V - 1); }
+
 // Bottom input [embeddings | dense] of the block into LDS (zeros beyond the
 // input width up to the MFMA depth and for rows below the group).
 template <typename T, int BR>
@@ -486,7 +489,12 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
     const VFL_GLOBAL int32_t* src = ids + (k.in_off + r0) * in.n_cat;
     for (int u = threadIdx.x; u < rv * in.n_cat; u += kNT) {
       const int r = u / in.n_cat, f = u - r * in.n_cat;
-      idt[(int64_t)f * in.ldi + r0 + r] = src[u];
+      int32_t id = src[u];
+      if ((uint32_t)id >= (uint32_t)in.V) {
+        if (in.bad_ids) atomicAdd(in.bad_ids, 1);
+        id = id < 0 ? 0 : in.V - 1;
+      }
+      idt[(int64_t)f * in.ldi + r0 + r] = id;
     }
   }
   for (int u = threadIdx.x; u < BR * nch; u += kNT) {
@@ -498,7 +506,7 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
         v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (c0 - ne)), din - c0);
       } else if (c0 + CE <= ne && (in.E % CE) == 0) {
         const int f = c0 / in.E, o = c0 % in.E;
-        const VFL_GLOBAL float* src = tab + ((int64_t)f * in.V + ids[row * in.n_cat + f]) * in.E + o;
+        const VFL_GLOBAL float* src = tab + ((int64_t)f * in.V + clamp_id(ids[row * in.n_cat + f], in.V)) * in.E + o;
         float x[CE];
 #pragma unroll
         for (int q = 0; q < CE / 4; ++q) {
@@ -520,7 +528,7 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
           float val = 0.f;
           if (c < ne) {
             const int f = c / in.E;
-            val = tab[((int64_t)f * in.V + ids[row * in.n_cat + f]) * in.E + (c % in.E)];
+            val = tab[((int64_t)f * in.V + clamp_id(ids[row * in.n_cat + f], in.V)) * in.E + (c % in.E)];
           } else if (c < din) {
             val = ld1<T>((const T*)(dense + row * cc.ld + (c - ne)));
           }

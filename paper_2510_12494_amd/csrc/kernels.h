@@ -154,13 +154,16 @@ struct WarmSet {
 // Bottom-model input of a row block: [embeddings of n_cat fields | dense],
 // gathered into LDS (`buf`) and copied to `rc` (for the first layer's
 // weight gradient).  T: float32 tables [n_cat * V x E]; idt (with tables):
-// field-major copy of the group's ids, idt[f * ldi + tick row], for the
-// sparse table step.
+// field-major copy of the group's ids (clamped into [0, V)),
+// idt[f * ldi + tick row], for the sparse table step.
 struct RowInput {
   int32_t dense_in = 0, n_cat = 0, V = 0, E = 0;
   int32_t dense_vec = 0;              // dense rows 16-byte aligned: vector loads
   const float* T = nullptr;
   int32_t* idt = nullptr; int32_t ldi = 0;
+  // ids outside [0, V) are clamped into it (so no access leaves the
+  // field's table) and counted here once per copy into idt
+  int32_t* bad_ids = nullptr;
   LBuf buf;
   RCMat rc;
 };

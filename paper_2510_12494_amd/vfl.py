@@ -106,7 +106,7 @@ def _load():
         "vfl_schedule_tick": [I64, I32, I64, C.POINTER(I64)],
         "vfl_sync_interval": [I32, I64, C.POINTER(I32)],
         "vfl_replica_average": [C.POINTER(P), I32, U32],
-        "vfl_check": [P, C.POINTER(U32)],
+        "vfl_check": [P, C.POINTER(U32), C.POINTER(U32)],
         "vfl_philox": [U64, U32, U32, U32, I32, I32, P, P],
         "vfl_timing_enable": [P, U32],
         "vfl_timing_read": [P, I32, C.POINTER(C.c_double), C.POINTER(I64), C.POINTER(C.c_double)],
@@ -240,10 +240,11 @@ def vfl_replica_average(ctxs, parties: int):
     _chk(_lib.vfl_replica_average(arr, len(ctxs), parties), "vfl_replica_average", ctxs[0] if ctxs else None)
 
 
-def vfl_check(ctx) -> int:
-    v = C.c_uint32(0)
-    _chk(_lib.vfl_check(ctx, C.byref(v)), "vfl_check", ctx)
-    return v.value
+def vfl_check(ctx):
+    """(header mismatches, out-of-range ids read) since the context's creation."""
+    v, b = C.c_uint32(0), C.c_uint32(0)
+    _chk(_lib.vfl_check(ctx, C.byref(v), C.byref(b)), "vfl_check", ctx)
+    return v.value, b.value
 
 
 def vfl_philox(seed: int, step: int, tag: int, row0: int, rows: int, groups: int, out_ptr: int,

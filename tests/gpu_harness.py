@@ -142,7 +142,7 @@ class Run:
                     self.snaps[t] = sess.params(shapes)
             self.final = sess.params(shapes)
             self.losses = sess.losses(range(n_groups))
-            self.mismatches = V.vfl_check(sess.ctx)
+            self.mismatches, self.bad_ids = V.vfl_check(sess.ctx)
             self.trace = V.vfl_get_trace(sess.ctx)
         finally:
             sess.close()

@@ -58,7 +58,7 @@ def test_protocol_errors():
         V.vfl_bottom_backward(s.ctx, V.VFL_PARTY_B, 0)
         V.vfl_bottom_forward(s.ctx, V.VFL_PARTY_B, 2, s.batches("B", 2))
         V.vfl_publish(s.ctx, 2)
-        assert V.vfl_check(s.ctx) == 0
+        assert V.vfl_check(s.ctx) == (0, 0)
         # misaligned dense rows are rejected
         b = s.batches("B", 3)
         b[0].dense += 2

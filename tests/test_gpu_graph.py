@@ -65,7 +65,7 @@ def test_graph_run_equals_per_call_steps(name, extra_rows):
         groups = range(ticks - w.staleness)
         assert np.array_equal(s1.losses(groups), s2.losses(groups))
         assert V.vfl_get_trace(s1.ctx) == V.vfl_get_trace(s2.ctx)
-        assert V.vfl_check(s1.ctx) == 0 and V.vfl_check(s2.ctx) == 0
+        assert V.vfl_check(s1.ctx) == (0, 0) and V.vfl_check(s2.ctx) == (0, 0)
         # the per-call path continues seamlessly after a graph run
         for t in range(ticks, ticks + 2):
             s1.step(t, epoch=epoch)
@@ -138,7 +138,7 @@ def test_graph_run_after_a_discard():
             assert s1.message(0, g)[1] == s2.message(0, g)[1]
         for g in range(ticks - 2 * s - 1, ticks - s):
             assert s1.message(1, g)[1] == s2.message(1, g)[1]
-        assert V.vfl_check(s1.ctx) == 0 and V.vfl_check(s2.ctx) == 0
+        assert V.vfl_check(s1.ctx) == (0, 0) and V.vfl_check(s2.ctx) == (0, 0)
     finally:
         s1.close()
         s2.close()

@@ -7,6 +7,7 @@ import pytest
 
 import vfl_synth as S
 from vfl_synth.workloads import Workload, PartySpec, TopSpec
+from oracle import PubSubOracle
 from oracle.philox import philox4x32_10
 import gpu_harness as H
 
@@ -33,7 +34,7 @@ def _dtol(w):
 
 
 def _check_ints(run, o, recs):
-    assert run.mismatches == 0
+    assert run.mismatches == 0 and run.bad_ids == 0
     assert run.trace == [tuple(r) for r in o.trace]
     for r in recs:
         if "emb_header" in r:
@@ -309,6 +310,40 @@ def test_table_sgd_segments(zipf_a, vocab, shift):
     _check_params(run, recs, w, per_tick=True)
 
 
+def test_out_of_range_ids_are_clamped_and_counted():
+    """Categorical ids outside [0, vocab) (negative and past the vocabulary,
+    on both parties) are read as the nearest valid id and counted: the run
+    equals the oracle on the clamped ids, and vfl_check counts each bad id
+    once per forward that takes its row (every row here is in exactly one
+    group, read by one forward of each party)."""
+    w = Workload(name="badids", n_rows=3000, dtype="f32",
+                 A=PartySpec(dense=5, n_cat=2, vocab=40, emb_dim=8, widths=[24, 16]),
+                 B=PartySpec(dense=0, n_cat=3, vocab=30, emb_dim=4, widths=[20, 8]),
+                 top=TopSpec(widths=[12, 1]), batch=500, staleness=1, replicas=2, lr=0.5,
+                 labels="bernoulli", label_p=0.4, data_seed=85, init_seed=86, noise_seed=87)
+    d = S.generate(w)
+    rng = np.random.default_rng(5)
+    bad = 0
+    clamped = dict(d)
+    for key, V in (("ida", w.A.vocab), ("idb", w.B.vocab)):
+        ids = d[key].copy()
+        m = rng.random(ids.shape) < 0.02
+        n = int(m.sum())
+        ids[m] = np.where(rng.random(n) < 0.5, -rng.integers(1, 1000, n), V + rng.integers(0, 1000, n))
+        d[key] = ids.astype(np.int32)
+        clamped[key] = np.clip(ids, 0, V - 1).astype(np.int32)
+        bad += n
+    assert bad > 50
+    n_groups = w.n_rows // w.rows_per_tick
+    run = H.Run(w, w.n_rows, n_groups, data=d, messages=False)
+    assert run.mismatches == 0 and run.bad_ids == bad
+    o = PubSubOracle(w, run.p0, "f64")
+    o.run(clamped, n_groups, run.rows_of, keep_messages=False)
+    worst = max(H.rel_inf(run.final[k], v) for k, v in o.p.items())
+    H.record("theta rel", worst, H.F32_TOL)
+    assert worst <= H.F32_TOL
+
+
 @pytest.mark.parametrize("widths,s,k,clip", [([520, 40], 1, 2, True), ([600, 264, 24], 2, 1, False)])
 def test_wide_first_layer_product(widths, s, k, clip):
     """Party B's first layer at least 512 wide (bf16): layer 1's input
@@ -365,7 +400,7 @@ def test_channel_discards(dtype, s, discard):
     n_groups = 9
     run = H.Run(w, w.n_rows, n_groups, discard=discard)
     o, recs = run.oracle(_prec(w))
-    assert run.mismatches == 0
+    assert run.mismatches == 0 and run.bad_ids == 0
     for r in recs:
         if "emb_header" in r:
             assert run.msgs[("e", r["fwd_group"])][1] == r["emb_header"]

@@ -34,7 +34,7 @@ def _same(sa, sb, shapes, groups, trace=True):
     assert np.array_equal(sa.losses(groups), sb.losses(groups))
     if trace:
         assert V.vfl_get_trace(sa.ctx) == V.vfl_get_trace(sb.ctx)
-    assert V.vfl_check(sa.ctx) == 0 and V.vfl_check(sb.ctx) == 0
+    assert V.vfl_check(sa.ctx) == (0, 0) and V.vfl_check(sb.ctx) == (0, 0)
 
 
 @pytest.mark.parametrize("name", ["ctr", "private", "tiny_sync", "hetero"])
