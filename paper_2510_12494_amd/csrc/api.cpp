@@ -160,8 +160,8 @@ struct Plan {
   bool bgemm = false;
   size_t d1rm = 0, job_lin = 0;
   int lin_blocks_dx = 0;
-  size_t mbits[kMaxSlots]{};          // layer 0's ReLU bits per slot [out0 x ldb]
-  int ldb = 0;
+  size_t mbits[kMaxSlots][VFL_MAX_LAYERS]{};   // B's ReLU bits per slot and layer [Ra / 8 x ldb[l]] (0: none)
+  int ldb[VFL_MAX_LAYERS]{};                  // their row pitch (bytes: the layer width rounded up to 64)
   KMeta kf, ka, kb;
   FwdLds lf;
   ActLds la;
@@ -559,12 +559,16 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   // chain's LDS), no tables, bf16: layer 1's input gradient is a layer
   // product over the whole group
   p.bgemm = p.e == BF16 && p.P.L >= 2 && p.P.spec.n_cat == 0 && p.P.out[0] >= kGemmMinWidth;
-  if (p.bgemm) {
-    p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
-    if (p.P.relu[0]) {
-      p.ldb = (int)((Ra / 8 + 31) / 32 * 32);
-      for (int q = 0; q <= p.s; ++q) p.mbits[q] = ly.take((size_t)p.P.out[0] * p.ldb);
-    }
+  if (p.bgemm) p.d1rm = ly.take((size_t)es * R * ld_of(p.P.out[1]));
+  // bf16: B's forward records one bit per activation of every ReLU layer
+  // below the cut layer, which B's delayed backward (and the wide layer's
+  // input-gradient product) read as the ReLU derivative instead of the
+  // stashed activations
+  if (p.e == BF16) {
+    for (int l = 0; l + 1 < p.P.L; ++l) p.ldb[l] = (p.P.out[l] + 63) / 64 * 64;
+    for (int q = 0; q <= p.s; ++q)
+      for (int l = 0; l + 1 < p.P.L; ++l)
+        if (p.P.relu[l]) p.mbits[q][l] = ly.take((size_t)(Ra / 8) * p.ldb[l]);
   }
 
   Top& T = p.T;
@@ -750,11 +754,11 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
                      p.lf.buf[l % 2], p.lf.buf[(l + 1) % 2]);
       if (l + 1 < P.L) f.l[l].rc = rcm(c, P.arc[q][l], P.out[l]);
     }
-    if (p.bgemm && P.relu[0]) {
-      // layer 0's ReLU bits for the wide input-gradient product
-      f.l[0].rc.bits = (uint8_t*)(ws + p.mbits[q]);
-      f.l[0].rc.ldb = p.ldb;
-    }
+    for (int l = 0; l + 1 < P.L; ++l)
+      if (p.mbits[q][l]) {
+        f.l[l].rc.bits = (uint8_t*)(ws + p.mbits[q][l]);
+        f.l[l].rc.ldb = p.ldb[l];
+      }
     f.z = c->ws + P.z[q]; f.ldz = (int32_t)ld_of(p.dB);
     f.publish = eextra;
     f.m = msg_op(o, o.flags & VFL_CLIP_EMB, o.flags & VFL_NOISE_EMB, 0);
@@ -858,6 +862,10 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       if (P.relu[l - 1]) {
         L.mask = lb.mask[l - 1];
         L.mask_src = rcm(c, P.arc[q][l - 1], P.out[l - 1]);
+        if (p.mbits[q][l - 1]) {
+          L.mask_src.bits = (uint8_t*)(ws + p.mbits[q][l - 1]);
+          L.mask_src.ldb = p.ldb[l - 1];
+        }
       }
       L.rc = rcm(c, P.drc[l - 1], P.out[l - 1]);
     }
@@ -875,7 +883,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       g.A = ws + p.d1rm; g.lda = ld_of(P.out[1]);
       g.W = c->ws + P.Wtq[q][1]; g.kst = P.kt[1];
       g.N = P.out[0]; g.K = P.out[1];
-      if (P.relu[0]) { g.mbits = (const uint8_t*)(ws + p.mbits[q]); g.ldb = p.ldb; }
+      if (P.relu[0]) { g.mbits = (const uint8_t*)(ws + p.mbits[q][0]); g.ldb = p.ldb[0]; }
       g.out_rc = rcm(c, P.drc[0], P.out[0]);
       g.tiles_n = (g.N + 255) / 256; g.tiles_m = (p.Ra + 255) / 256;
       g.rows_pad = p.Ra;

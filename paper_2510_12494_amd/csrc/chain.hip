@@ -406,7 +406,7 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
           byte |= (uint32_t)(lo != 0 && !(lo & 0x8000u)) << (2 * w);
           byte |= (uint32_t)(hi != 0 && !(hi & 0x8000u)) << (2 * w + 1);
         }
-        glb(m.bits)[(int64_t)c * m.ldb + r0 / RR + rg] = (uint8_t)byte;
+        glb(m.bits)[(int64_t)(r0 / RR + rg) * m.ldb + c] = (uint8_t)byte;
       }
     }
   }
@@ -428,18 +428,35 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
 
 // RC global matrix -> LDS rows (columns below cols; zeros up to the MFMA
 // depth): one lane per chunk (RR rows of one column), one 16-byte load and
-// RR element writes
+// RR element writes; from the matrix's ReLU bits instead (a byte per chunk)
+// when it has them
 template <typename T, int BR>
 __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE, KS = Ch<T>::KS;
   const int cw = (cols + KS - 1) / KS * KS;   // columns up to the MFMA depth
   const VFL_GLOBAL char* g = glb((const char*)m.p);
   const int64_t cp = m.cp;
+  const VFL_GLOBAL uint8_t* bits = glb((const uint8_t*)m.bits);
   for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
     const int rg = u / cw, c = u - rg * cw;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     const bool in_m = m.rows == 0 || r0 + rg * RR < m.rows;
-    if (c < cols && in_m) v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+    if constexpr (RR == 8) {
+      if (bits) {
+        // the chunk's ReLU bits: bit i set for a positive row i (written
+        // as a bf16 one, which the mask test reads as positive)
+        if (c < cols && in_m) {
+          const uint32_t byte = bits[(int64_t)(r0 / RR + rg) * m.ldb + c];
+#pragma unroll
+          for (int w = 0; w < 4; ++w)
+            v[w] = ((byte >> (2 * w)) & 1u ? 0x3f80u : 0u) | ((byte >> (2 * w + 1)) & 1u ? 0x3f800000u : 0u);
+        }
+      } else if (c < cols && in_m) {
+        v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+      }
+    } else if (c < cols && in_m) {
+      v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+    }
     char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
     if constexpr (RR == 8) {
 #pragma unroll

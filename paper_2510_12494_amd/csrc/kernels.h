@@ -108,8 +108,9 @@ struct LBuf { int32_t off = 0, pitch = 0; };
 // RC-layout global matrix (null p: not written); rows: the rows it holds
 // (a chain block's rows past it are not written; 0: unbounded).  bits (bf16
 // chain copies only; null: none): a byte per 8-row chunk as well, bit i set
-// when row i of the chunk is positive, at bits[column * ldb + row / 8] (the
-// ReLU derivative of a layer for the wide input-gradient product).
+// when row i of the chunk is positive, at bits[(row / 8) * ldb + column] (the
+// ReLU derivative of a layer, for B's backward and the wide input-gradient
+// product; as a mask source, a set bits pointer is read instead of p).
 struct RCMat {
   void* p = nullptr; int32_t cp = 0, rows = 0;
   uint8_t* bits = nullptr; int32_t ldb = 0;
@@ -255,8 +256,8 @@ struct ActiveJob {
 // (row-major) at the stashed output z (clip backward with norm/cfac when
 // clip), then the chain dx (l = L-1 .. 1, or down to 2 when layer 1's input
 // gradient is a layer product: then the last delta also goes row-major to
-// drm), masks loaded from the stashed RC activations; with tables, gx as in
-// ActiveJob.
+// drm), masks loaded from the stashed ReLU bits (bf16) or RC activations;
+// with tables, gx as in ActiveJob.
 struct BwdJob {
   BiasTab bt;
   WarmSet warm;
@@ -338,7 +339,7 @@ hipError_t launch_dw_reduce(Elt e, const DwJob* job, int blocks, int R, float sc
 // group (bf16), in large tiles:
 //   out[r][n] = mask(r, n) * sum_k A[r][k] W[n][k]
 // for r < rows, into out_rc (rows from the group's end up to rows_pad zero);
-// mask(r, n) = bit r mod 8 of mbits[n * ldb + r / 8] (mbits null: 1).
+// mask(r, n) = bit r mod 8 of mbits[(r / 8) * ldb + n] (mbits null: 1).
 // A: row-major bf16, lda elements per row (a multiple of 8; finite values
 // from K up to lda); W: packed [N x K] (pk_index, kst 32-k steps, zero past
 // K).  Blocks: lin_blocks(rows_pad, N): 256 x 256 output tiles rounded up

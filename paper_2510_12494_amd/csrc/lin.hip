@@ -44,7 +44,10 @@ constexpr int kStages = 5;                              // buffers: up to 4 stag
 // its 8-row chunks swizzled (see out_slot) so that both the lanes' 8-byte
 // writes and the threads' 16-byte reads spread over the LDS banks
 constexpr int kOutPitch = kBM * 2 + 32;
-constexpr int kLinLds = kBN * kOutPitch > kStages * kStageBytes ? kBN * kOutPitch : kStages * kStageBytes;
+// then the tile's mask bytes: kBM / 8 row groups of kBN bytes
+constexpr int kBitsOff = kBN * kOutPitch;
+constexpr int kEpiLds = kBitsOff + kBM / 8 * kBN;
+constexpr int kLinLds = kEpiLds > kStages * kStageBytes ? kEpiLds : kStages * kStageBytes;
 
 // byte offset of rows 8 rg .. 8 rg + 7 of tile column c in the staging
 __device__ __forceinline__ int out_slot(int c, int rg) { return c * kOutPitch + 16 * (rg ^ ((c >> 3) & 31)); }
@@ -234,11 +237,23 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
             u32x2{pack_bf16(x[4 * g], x[4 * g + 1]), pack_bf16(x[4 * g + 2], x[4 * g + 3])};
       }
   }
+  //    and the tile's mask bytes (the ReLU derivative of the layer below:
+  //    row-group-major, so each row group's 256 bytes are one contiguous
+  //    run) go to LDS beside it, 16 bytes per thread and load
+  if (J.mbits) {
+    const VFL_GLOBAL uint8_t* bp = glb(J.mbits);
+    for (int u = t; u < kBM / 8 * (kBN / 16); u += 256) {
+      const int g = u / (kBN / 16), ch = u % (kBN / 16);
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (m0 / 8 + g < rg_end && n0 + 16 * ch + 16 <= J.ldb)
+        v = *(const VFL_GLOBAL u32x4*)(bp + (int64_t)(m0 / 8 + g) * J.ldb + n0 + 16 * ch);
+      *(u32x4*)(smem + kBitsOff + g * kBN + 16 * ch) = v;
+    }
+  }
   __syncthreads();
   // 2. the RC output: thread t owns tile column t and walks its 8-row
   //    chunks, so that each store instruction writes 64 consecutive chunks
-  //    of one row group; the mask bytes of the column's chunks (the ReLU
-  //    derivative of the layer below) are loaded up front
+  //    of one row group
   if (n0 + t < N) {
     const int n = n0 + t;
     VFL_GLOBAL u32x4* dst = (VFL_GLOBAL u32x4*)glb((char*)J.out_rc.p) + n;
@@ -247,9 +262,13 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
 #pragma unroll
     for (int i = 0; i < kBM / 32; ++i) mb[i] = ~0u;
     if (J.mbits) {
-      const VFL_GLOBAL uint32_t* bp = (const VFL_GLOBAL uint32_t*)(glb(J.mbits) + (int64_t)n * J.ldb + m0 / 8);
 #pragma unroll
-      for (int i = 0; i < kBM / 32; ++i) mb[i] = bp[i];
+      for (int i = 0; i < kBM / 32; ++i) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) w |= (uint32_t)*(const uint8_t*)(smem + kBitsOff + (4 * i + b) * kBN + t) << (8 * b);
+        mb[i] = w;
+      }
     }
     // fully unrolled: the mask words stay in registers (a runtime index
     // would put them in scratch memory)
