@@ -628,6 +628,8 @@ __global__ __launch_bounds__(256) void k_dw32(const DwJob* __restrict__ jp, int 
   }
 }
 
+constexpr int kRedBatch = 16;   // split partials loaded at once per thread
+
 // Blocks [0, red_blocks): one thread per 4 consecutive weights (or one
 // bias) of a split problem.  Blocks after: 4 logit columns each, the
 // partial rows split over 64 slices and summed slice by slice.
@@ -657,16 +659,19 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
         const int64_t stride = (int64_t)P.N * P.kp;
         float w[4];
         sgd_load4<T>(P, n, kb, w);
+        // the splits in batches of kRedBatch whose loads are all in flight
+        // before the first add (addresses past the last split repeat it;
+        // those values are not added), summed in split order
         f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-        int s = 0;
-        for (; s + 8 <= P.splits; s += 8) {
-          f32x4 v[8];
+        for (int s = 0; s < P.splits; s += kRedBatch) {
+          f32x4 v[kRedBatch];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = *(const VFL_GLOBAL f32x4*)(src + (s + u) * stride);
+          for (int u = 0; u < kRedBatch; ++u)
+            v[u] = *(const VFL_GLOBAL f32x4*)(src + (int64_t)min(s + u, P.splits - 1) * stride);
 #pragma unroll
-          for (int u = 0; u < 8; ++u) sum += v[u];
+          for (int u = 0; u < kRedBatch; ++u)
+            if (s + u < P.splits) sum += v[u];
         }
-        for (; s < P.splits; ++s) sum += *(const VFL_GLOBAL f32x4*)(src + s * stride);
         sgd_store4<T>(P, n, kb, w, sum, scale);
       } else {
         const int n = (int)(t - qw);
@@ -674,8 +679,14 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
         VFL_GLOBAL float* bias = glb(P.bias) + n;
         const float b0 = *bias;
         float sum = 0.f;
-#pragma unroll 8
-        for (int s = 0; s < P.splits; ++s) sum += pb[(int64_t)s * P.N + n];
+        for (int s = 0; s < P.splits; s += kRedBatch) {
+          float v[kRedBatch];
+#pragma unroll
+          for (int u = 0; u < kRedBatch; ++u) v[u] = pb[(int64_t)min(s + u, P.splits - 1) * P.N + n];
+#pragma unroll
+          for (int u = 0; u < kRedBatch; ++u)
+            if (s + u < P.splits) sum += v[u];
+        }
         *bias = b0 - scale * sum;
       }
       return;
