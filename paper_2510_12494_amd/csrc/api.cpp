@@ -43,6 +43,7 @@ constexpr int kMaxSlots = VFL_MAX_STALENESS + 1;
 constexpr int kGemmMinWidth = 512;    // B's first-layer width from which its input gradient is a layer product
 constexpr int kMinBlocks = 256;       // row blocks a chain launch aims at (one per CU)
 constexpr int kDwBlocks = 256;        // weight-gradient blocks a launch aims at
+constexpr double kRcStreamBytes = 32e6;  // RC copies above this size use streaming stores
 constexpr int kDwRows = 256;          // rows of two k_dw load groups (4 MFMA steps each) in bf16;
                                       // float32 chunks hold half the rows: 128
 constexpr int kTimedEvery = 4;        // ticks of a captured cycle between timed ticks
@@ -733,6 +734,10 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     m.p = ws + off;
     m.cp = (int32_t)ld_of(cols);
     m.rows = p.Ra;
+    // a copy larger than the L2s is written with the streaming hint: its
+    // reader (the weight gradient, several launches later) finds it in HBM
+    // either way
+    m.nt = (double)p.Ra * m.cp * (p.e == BF16 ? 2 : 4) > kRcStreamBytes;
     return m;
   };
   for (int q = 0; q < S1; ++q) {

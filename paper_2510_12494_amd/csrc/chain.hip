@@ -225,10 +225,12 @@ __device__ __forceinline__ uint32_t warm_l2(const WarmSet& w, const void* dummy)
 // first pass; on return, groups 0 and 1 of `next`'s (nullable).  The
 // pending RC copy (whose LDS rows this product does not write) is issued
 // in the last pass once every weight load of the pass is out.
+template <typename T, int BR, bool NT>
+__device__ __forceinline__ void lds_to_rc_(const char* s, const LBuf& b, int cols, const RCMat& m, int r0);
 template <typename T, int BR>
-__device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0);
+__device__ __forceinline__ void lds_to_rc_hint(const char* s, const LBuf& b, int cols, const RCMat& m, int r0);
 
-template <typename T, int RT, typename Epi>
+template <typename T, int RT, typename Epi, bool HINT = false>
 __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe& p,
                                          const ChainLayer* next, const RcPend& pend, Epi&& epi) {
   constexpr int PF = kPF, NTW = kNTW;
@@ -308,7 +310,10 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
       group(g + 1, p.wb);
       refill(g + 3, p.wb);
     }
-    if (!more && pend.m.p) lds_to_rc<T, 16 * RT>(s, pend.b, pend.cols, pend.m, pend.r0);
+    if (!more && pend.m.p) {
+      if constexpr (HINT) lds_to_rc_hint<T, 16 * RT>(s, pend.b, pend.cols, pend.m, pend.r0);
+      else lds_to_rc_<T, 16 * RT, false>(s, pend.b, pend.cols, pend.m, pend.r0);
+    }
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       if (tile[j] >= ntl) continue;
@@ -321,7 +326,7 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
 }
 
 // Forward or input-gradient layer into LDS (see ChainLayer).
-template <typename T, int RT>
+template <typename T, int RT, bool HINT = false>
 __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe& p,
                                           const ChainLayer* next, const RcPend& pend) {
   const int N = L.N;
@@ -329,7 +334,7 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
   const LBuf out = L.out, mk = L.mask;
   // branch-free: every condition is a select (a short-circuit test here
   // compiles to one exec-mask branch per element)
-  block_mm<T, RT>(s, L, p, next, pend, [&](int r, int n, const f32x4& a, const f32x4& b) {
+  auto epi = [&](int r, int n, const f32x4& a, const f32x4& b) {
     float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
     if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
     const bool rok = r < rv;
@@ -343,7 +348,8 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
     // n is a multiple of 4 and a nopad N of 8: the four columns are all
     // below N or all past it
     if (!nopad || n < N) st4<T>(lp(s, out, r, n * (int)sizeof(T)), v);
-  });
+  };
+  block_mm<T, RT, decltype(epi)&, HINT>(s, L, p, next, pend, epi);
 }
 
 // Input gradient of the embedding columns of a bottom input: float32 rows
@@ -372,8 +378,8 @@ __device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float
 // LDS rows, so every lane of the block works and consecutive lanes store
 // consecutive chunks of a row group.  Columns up to the next multiple of RR
 // (zero in LDS) are written too.
-template <typename T, int BR>
-__device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+template <typename T, int BR, bool NT>
+__device__ __forceinline__ void lds_to_rc_(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE;
   const int cw = (cols + RR - 1) / RR * RR;
   VFL_GLOBAL char* g = glb((char*)m.p);
@@ -394,7 +400,9 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
 #pragma unroll
       for (int w = 0; w < 4; ++w) v[w] = *(const uint32_t*)(src + w * b.pitch);
     }
-    *(VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16) = v;
+    VFL_GLOBAL u32x4* dst = (VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+    if constexpr (NT) __builtin_nontemporal_store(v, dst);
+    else *dst = v;
     if constexpr (RR == 8) {
       if (m.bits && c < cols) {
         // the chunk's positive rows, one bit each (ReLU outputs: a row is
@@ -410,6 +418,20 @@ __device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols
       }
     }
   }
+}
+
+template <typename T, int BR>
+__device__ __forceinline__ void lds_to_rc(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+  lds_to_rc_<T, BR, false>(s, b, cols, m, r0);
+}
+
+// the same with the streaming hint when m.nt (matrices too large for the
+// L2; the two loops are kept apart so that the hint survives), for B's
+// forward, whose copies are its largest output
+template <typename T, int BR>
+__device__ __forceinline__ void lds_to_rc_hint(const char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+  if (m.nt) lds_to_rc_<T, BR, true>(s, b, cols, m, r0);
+  else lds_to_rc_<T, BR, false>(s, b, cols, m, r0);
 }
 
 // zero rows r0 .. r0+BR-1 of an RC global matrix (columns below cols)
@@ -661,11 +683,11 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
   // each stage's RC copy goes out during the next product
   RcPend pend{j.in.buf, j.in.n_cat * j.in.E + j.in.dense_in, j.in.rc, r0};
   for (int l = 0; l < nL; ++l) {
-    run_layer<T, RT>(s, j.l[l], rv, pp, l + 1 < nL ? &j.l[l + 1] : nullptr, pend);
+    run_layer<T, RT, true>(s, j.l[l], rv, pp, l + 1 < nL ? &j.l[l + 1] : nullptr, pend);
     __syncthreads();
     pend = RcPend{j.l[l].out, j.l[l].N, j.l[l].rc, r0};
   }
-  if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
+  if (pend.m.p) lds_to_rc_hint<T, BR>(s, pend.b, pend.cols, pend.m, r0);
   const ChainLayer& last = j.l[nL - 1];
   lds_to_rows<T, BR>(s, last.out, last.N, j.z, j.ldz, r0, rv);
   if (j.publish)
@@ -1026,12 +1048,12 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
   RcPend pend{j.d, j.D, j.d_rc, r0};
   for (int q = 0; q < nd; ++q) {
     const ChainLayer& L = j.dx[q];
-    run_layer<T, RT>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr), pend);
+    run_layer<T, RT, true>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr), pend);
     __syncthreads();
     pend = RcPend{L.out, L.N, L.rc, r0};
   }
   if (has_gx) run_gx<T, RT>(s, j.gx, j.gxp, j.ldgx, r0, rv, pp, pend);
-  else if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
+  else if (pend.m.p) lds_to_rc_hint<T, BR>(s, pend.b, pend.cols, pend.m, r0);
   if (j.drm) {
     // the last delta of the chain, row-major, for the layer product below it
     const LBuf last = nd > 0 ? j.dx[nd - 1].out : j.d;

@@ -114,6 +114,7 @@ struct LBuf { int32_t off = 0, pitch = 0; };
 struct RCMat {
   void* p = nullptr; int32_t cp = 0, rows = 0;
   uint8_t* bits = nullptr; int32_t ldb = 0;
+  int32_t nt = 0;      // store with the non-temporal hint (matrices too large for the L2)
 };
 
 // One product of a row block with a weight operand W [N x K] (element type,

@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256) void k_lin(const LinJob* __restrict__ jp, int 
 #pragma unroll
       for (int w = 0; w < 4; ++w)
         q[w] &= ((byte >> (2 * w)) & 1u ? 0x0000ffffu : 0u) | ((byte >> (2 * w + 1)) & 1u ? 0xffff0000u : 0u);
-      dst[g * J.out_rc.cp] = q;
+      __builtin_nontemporal_store(q, dst + g * J.out_rc.cp);   // read back by the next launch from HBM
     }
   }
 }
