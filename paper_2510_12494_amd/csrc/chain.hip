@@ -542,7 +542,8 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
     if (r < rv && c0 < din) {
       const int64_t row = k.in_off + r0 + r;
       if (c0 >= ne && in.dense_vec && (ne % CE) == 0) {
-        v = mask_tail<T>(*(const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (c0 - ne)), din - c0);
+        v = mask_tail<T>(__builtin_nontemporal_load((const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (c0 - ne))),
+                         din - c0);
       } else if (c0 + CE <= ne && (in.E % CE) == 0) {
         const int f = c0 / in.E, o = c0 % in.E;
         const VFL_GLOBAL float* src = tab + ((int64_t)f * in.V + clamp_id(ids[row * in.n_cat + f], in.V)) * in.E + o;
