@@ -138,7 +138,7 @@ struct KMeta { int rt = 1, blocks = 1, lds = 0; };
 
 // Weight-gradient launch shape of a party: tile 32 (one unsplit launch,
 // k_dw32) or 64 (row chunks, k_dw + k_dw_reduce).
-struct DwMeta { int tile = 64, splits = 1, rps = 0, blocks = 0, red_blocks = 0, red_threads = 0, logit_blocks = 0; };
+struct DwMeta { int tile = 64, splits = 1, rps = 0, blocks = 0, red_blocks = 0, logit_blocks = 0; };
 
 struct Plan {
   Elt e = F32;
@@ -626,18 +626,17 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.tsrc = ly.take(sizeof(TickSrc));
 
   // weight gradients: partials of the split problems
-  auto parts = [&](const DwMeta& m, int N, int K, size_t& pw, size_t& pb, int& thr) {
+  auto parts = [&](DwMeta& m, int N, int K, size_t& pw, size_t& pb) {
     if (m.splits <= 1) return;
     const int kp = (K + 3) / 4 * 4;
     pw = ly.take(sizeof(float) * (size_t)m.splits * N * kp);
     pb = ly.take(sizeof(float) * (size_t)m.splits * N);
-    thr += N * (kp / 4) + N;
+    m.red_blocks += (N + 7) / 8 * ((kp + kRedK - 1) / kRedK) + (N + 255) / 256;   // k_dw_reduce's tiles, biases
   };
-  for (int l = 0; l < p.A.L; ++l) parts(p.da, p.A.out[l], p.A.in[l], p.A.part[l], p.A.partb[l], p.da.red_threads);
-  for (int j = 0; j < T.H; ++j) parts(p.da, T.out[j], T.in[j], T.part[j], T.partb[j], p.da.red_threads);
-  for (int l = 0; l < p.P.L; ++l) parts(p.db, p.P.out[l], p.P.in[l], p.P.part[l], p.P.partb[l], p.db.red_threads);
-  p.da.red_blocks = (p.da.red_threads + 255) / 256;
-  p.db.red_blocks = (p.db.red_threads + 255) / 256;
+  p.da.red_blocks = p.db.red_blocks = 0;
+  for (int l = 0; l < p.A.L; ++l) parts(p.da, p.A.out[l], p.A.in[l], p.A.part[l], p.A.partb[l]);
+  for (int j = 0; j < T.H; ++j) parts(p.da, T.out[j], T.in[j], T.part[j], T.partb[j]);
+  for (int l = 0; l < p.P.L; ++l) parts(p.db, p.P.out[l], p.P.in[l], p.P.part[l], p.P.partb[l]);
   p.da.logit_blocks = (T.out[T.H - 1] + 2 + 3) / 4;
 
   // device job descriptors
@@ -917,7 +916,6 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
     add(dwa, p.da, A.drc[l], l == 0 ? A.x0rc[0] : A.arc[0][l - 1], A.out[l], A.in[l], A.W[l], A.b[l],
         A.Wq[0][l], A.kq[l], A.Wtq[0][l], A.kt[l], A.part[l], A.partb[l]);
   dwa.rows_pad = p.Ra;
-  dwa.red_threads = p.da.red_threads;
   dwa.red_blocks = p.da.red_blocks;
   dwa.lpart = at_f(T.logit_part);
   dwa.Hd = T.out[T.H - 1];
@@ -930,7 +928,6 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       add(J, p.db, P.drc[l], l == 0 ? P.x0rc[q] : P.arc[q][l - 1], P.out[l], P.in[l], P.W[l], P.b[l],
           P.Wq[q][l], P.kq[l], P.Wtq[q][l], P.kt[l], P.part[l], P.partb[l]);
     J.rows_pad = p.Ra;
-    J.red_threads = p.db.red_threads;
     J.red_blocks = p.db.red_blocks;
   }
   if (dwa.blocks != p.da.blocks || dwb[0].blocks != p.db.blocks)

@@ -630,9 +630,116 @@ __global__ __launch_bounds__(256) void k_dw32(const DwJob* __restrict__ jp, int 
 
 constexpr int kRedBatch = 16;   // split partials loaded at once per thread
 
-// Blocks [0, red_blocks): one thread per 4 consecutive weights (or one
-// bias) of a split problem.  Blocks after: 4 logit columns each, the
-// partial rows split over 64 slices and summed slice by slice.
+// Sum of the split partials s = 0 .. splits-1 at src + s * stride, in split
+// order, the loads of a batch of kRedBatch all in flight before its first
+// add (addresses past the last split repeat it; those values are not added).
+__device__ __forceinline__ f32x4 split_sum4(const VFL_GLOBAL float* src, int64_t stride, int splits) {
+  f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < splits; s += kRedBatch) {
+    f32x4 v[kRedBatch];
+#pragma unroll
+    for (int u = 0; u < kRedBatch; ++u) v[u] = *(const VFL_GLOBAL f32x4*)(src + (int64_t)min(s + u, splits - 1) * stride);
+#pragma unroll
+    for (int u = 0; u < kRedBatch; ++u)
+      if (s + u < splits) sum += v[u];
+  }
+  return sum;
+}
+__device__ __forceinline__ float split_sum1(const VFL_GLOBAL float* src, int64_t stride, int splits) {
+  float sum = 0.f;
+  for (int s = 0; s < splits; s += kRedBatch) {
+    float v[kRedBatch];
+#pragma unroll
+    for (int u = 0; u < kRedBatch; ++u) v[u] = src[(int64_t)min(s + u, splits - 1) * stride];
+#pragma unroll
+    for (int u = 0; u < kRedBatch; ++u)
+      if (s + u < splits) sum += v[u];
+  }
+  return sum;
+}
+
+// One reduction tile of a split problem: rows n0 .. n0+7 and columns k0 ..
+// k0+kRedK-1 of W (thread t: row n0 + t / 32, columns k0 + 4 (t % 32) ..
+// +4).  The summed gradient makes the SGD step of the float32 masters; the
+// new values (zero past N and K) go through LDS so that both packed operand
+// copies are written as whole 16-byte chunks: CE consecutive inputs of one
+// output for Wq, CE consecutive outputs of one input for Wtq (pk_index keeps
+// such a run contiguous).
+template <typename T>
+__device__ __forceinline__ void reduce_tile(const DwProb& P, int n0, int k0, float scale) {
+  constexpr int CE = 16 / (int)sizeof(T), KS = 4 * CE;
+  constexpr int kPitch = kRedK + 16 / (int)sizeof(T);     // elements per LDS row (padded by 16 bytes)
+  __shared__ __attribute__((aligned(16))) T tile[8 * kPitch];
+  const int N = P.N, K = P.K, kp = P.kp;
+  const int nr = threadIdx.x >> 5, kb = k0 + 4 * (threadIdx.x & 31);
+  const int n = n0 + nr;
+  const bool nok = n < N;
+  // lanes past the problem's rows or inputs load nothing (narrow problems
+  // leave half of a tile's lanes idle)
+  f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (nok && kb < kp) g = split_sum4(glb(P.part) + (int64_t)n * kp + kb, (int64_t)N * kp, P.splits);
+  VFL_GLOBAL float* W = glb(P.W) + (int64_t)min(n, N - 1) * K;
+  const bool vec = (K & 3) == 0 && kb + 4 <= K;          // whole, 16-byte aligned float4 of W
+  float w[4];
+  if (vec) {
+    const f32x4 x = *(const VFL_GLOBAL f32x4*)(W + kb);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = x[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = W[min(kb + e, K - 1)];
+  }
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = (nok && kb + e < K) ? w[e] - scale * g[e] : 0.f;
+  if (nok) {
+    if (vec) {
+      *(VFL_GLOBAL f32x4*)(W + kb) = f32x4{v[0], v[1], v[2], v[3]};
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (kb + e < K) W[kb + e] = v[e];
+    }
+  }
+  if (!P.Wq && !P.Wtq) return;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) st1<T>(&tile[nr * kPitch + 4 * (threadIdx.x & 31) + e], v[e]);
+  __syncthreads();
+  if (P.Wq) {
+    // chunk i: row i / (kRedK / CE), inputs k0 + CE (i % (kRedK / CE)) ..
+    constexpr int per_row = kRedK / CE;
+    for (int i = threadIdx.x; i < 8 * per_row; i += 256) {
+      const int r = i / per_row, k = k0 + CE * (i % per_row);
+      if (k < P.kq * KS)
+        *(VFL_GLOBAL u32x4*)(glb((T*)P.Wq) + pk_index<T>(n0 + r, k, P.kq)) =
+            *(const u32x4*)&tile[r * kPitch + (k - k0)];
+    }
+  }
+  if (P.Wtq) {
+    // chunk i: input k0 + i / (8 / CE), outputs n0 + CE (i % (8 / CE)) ..
+    constexpr int per_k = 8 / CE;
+    const int krows = (K + 15) / 16 * 16;                 // rows of the transposed copy's tiles
+    for (int i = threadIdx.x; i < kRedK * per_k; i += 256) {
+      const int kk = i / per_k, h = i % per_k, k = k0 + kk, ns = n0 + CE * h;
+      if (k < krows && ns < P.kt * KS) {
+        u32x4 c;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if constexpr (sizeof(T) == 4) {
+            c[w] = __float_as_uint(tile[(CE * h + w) * kPitch + kk]);
+          } else {
+            c[w] = (uint32_t)tile[(2 * w) * kPitch + kk] | ((uint32_t)tile[(2 * w + 1) * kPitch + kk] << 16);
+          }
+        }
+        *(VFL_GLOBAL u32x4*)(glb((T*)P.Wtq) + pk_index<T>(k, ns, P.kt)) = c;
+      }
+    }
+  }
+}
+
+// Blocks [0, red_blocks): per split problem, one block per reduction tile
+// (8 outputs x kRedK inputs), then one per 256 biases.  Blocks after: 4 logit columns
+// each, the partial rows split over 64 slices and summed slice by slice.
 template <typename T>
 __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp, int Rarg,
                                                    float scale_arg, float* loss_out,
@@ -647,47 +754,21 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const DwJob* __restrict__ jp,
     loss_out = loss_base ? loss_base + ta.loss_idx : nullptr;
   }
   if ((int)blockIdx.x < J.red_blocks) {
-    int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    int b = blockIdx.x;
     for (int q = 0; q < J.n; ++q) {
       const DwProb& P = J.p[q];
       if (P.splits <= 1) continue;
-      const int64_t qw = (int64_t)P.N * (P.kp / 4);
-      if (t >= qw + P.N) { t -= qw + P.N; continue; }
-      if (t < qw) {
-        const int n = (int)(t / (P.kp / 4)), kb = (int)(t % (P.kp / 4)) * 4;
-        const VFL_GLOBAL float* src = glb(P.part) + (int64_t)n * P.kp + kb;
-        const int64_t stride = (int64_t)P.N * P.kp;
-        float w[4];
-        sgd_load4<T>(P, n, kb, w);
-        // the splits in batches of kRedBatch whose loads are all in flight
-        // before the first add (addresses past the last split repeat it;
-        // those values are not added), summed in split order
-        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < P.splits; s += kRedBatch) {
-          f32x4 v[kRedBatch];
-#pragma unroll
-          for (int u = 0; u < kRedBatch; ++u)
-            v[u] = *(const VFL_GLOBAL f32x4*)(src + (int64_t)min(s + u, P.splits - 1) * stride);
-#pragma unroll
-          for (int u = 0; u < kRedBatch; ++u)
-            if (s + u < P.splits) sum += v[u];
-        }
-        sgd_store4<T>(P, n, kb, w, sum, scale);
+      const int tk = (P.kp + kRedK - 1) / kRedK, tiles = (P.N + 7) / 8 * tk, nbb = (P.N + 255) / 256;
+      if (b >= tiles + nbb) { b -= tiles + nbb; continue; }
+      if (b < tiles) {
+        reduce_tile<T>(P, b / tk * 8, b % tk * kRedK, scale);
       } else {
-        const int n = (int)(t - qw);
-        const VFL_GLOBAL float* pb = glb(P.partb);
-        VFL_GLOBAL float* bias = glb(P.bias) + n;
-        const float b0 = *bias;
-        float sum = 0.f;
-        for (int s = 0; s < P.splits; s += kRedBatch) {
-          float v[kRedBatch];
-#pragma unroll
-          for (int u = 0; u < kRedBatch; ++u) v[u] = pb[(int64_t)min(s + u, P.splits - 1) * P.N + n];
-#pragma unroll
-          for (int u = 0; u < kRedBatch; ++u)
-            if (s + u < P.splits) sum += v[u];
+        const int nb = (b - tiles) * 256 + threadIdx.x;
+        if (nb < P.N) {
+          VFL_GLOBAL float* bias = glb(P.bias) + nb;
+          const float b0 = *bias;
+          *bias = b0 - scale * split_sum1(glb(P.partb) + nb, P.N, P.splits);
         }
-        *bias = b0 - scale * sum;
       }
       return;
     }

@@ -298,6 +298,7 @@ hipError_t chain_init();
 // each block writes float32 partials part[s][n][kp] (kp = K rounded up to
 // 4) and partb[s][n], and k_dw_reduce finishes the layer.  Blocks
 // [first_block, first_block + tiles * splits) work on this problem.
+constexpr int kRedK = 128;   // inputs per reduction tile (k_dw_reduce)
 struct DwProb {
   RCMat D, X;
   float* W = nullptr; float* bias = nullptr;
@@ -309,10 +310,12 @@ struct DwProb {
 struct DwJob {
   int32_t n = 0, blocks = 0;
   DwProb p[kMaxDw];
-  // reduction launch: split problems' element groups, then the logit
-  // layer's columns (lblocks partial rows of Hd + 2 floats, of which the
-  // first ceil(rows / lrows) are the group's)
-  int32_t red_threads = 0, red_blocks = 0;
+  // reduction launch: split problems' tiles (8 outputs x kRedK inputs)
+  // and bias blocks (256 each), problem by problem, then the logit layer's
+  // columns (lblocks partial
+  // rows of Hd + 2 floats, of which the first ceil(rows / lrows) are the
+  // group's)
+  int32_t red_blocks = 0;
   int32_t rows_pad = 0;               // RC rows (k_dw32: its row steps cover them all)
   float* lpart = nullptr; int32_t Hd = 0, lrows = 0;
   float* lw = nullptr; float* lb = nullptr;
