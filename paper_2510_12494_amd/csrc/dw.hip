@@ -414,21 +414,37 @@ __global__ __launch_bounds__(256) void k_dwt(const DwJob* __restrict__ jp) {
   // lane: output n = n0 + 128 wn + 32 nb + col, inputs
   // k = k0 + 128 wk + 32 kb + 8 g + 4 hi + (0 .. 3) in acc[kb][nb][4 g ..]
   // (the plan gives this kernel at least two row chunks: the SGD is the
-  // reduction's)
+  // reduction's).  The partials go out through LDS (the stage buffers are
+  // free by now): per wavefront and round, its 64 outputs of two blocks nb
+  // as rows of 128 inputs (padded by 4 floats: the 16 lanes of a quarter
+  // wavefront write distinct banks), read back a row per 32 lanes, so that
+  // each store instruction writes two runs of 512 consecutive bytes.
+  constexpr int kEpiPitch = kDwtK / 2 + 4;
+  static_assert(4 * 64 * kEpiPitch * 4 <= kDwtLds, "epilogue staging exceeds the stage buffers");
   VFL_GLOBAL float* part = glb(P.part) + (int64_t)split * N * P.kp;
+  float* E = (float*)(smem + wave * 64 * kEpiPitch * 4);
+  __syncthreads();   // every wavefront is done with the stage buffers
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    const int n = n0 + 128 * wn + 32 * nb + col;
-    if (n >= N) continue;
+  for (int r = 0; r < 2; ++r) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int nbi = 0; nbi < 2; ++nbi)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int kk = k0 + 128 * wk + 32 * kb + 8 * g + 4 * hi;
-        if (kk < K)
-          *(VFL_GLOBAL f32x4*)(part + (int64_t)n * P.kp + kk) =
-              f32x4{acc[kb][nb][4 * g], acc[kb][nb][4 * g + 1], acc[kb][nb][4 * g + 2], acc[kb][nb][4 * g + 3]};
-      }
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *(f32x4*)(E + (32 * nbi + col) * kEpiPitch + 32 * kb + 8 * g + 4 * hi) =
+              f32x4{acc[kb][2 * r + nbi][4 * g], acc[kb][2 * r + nbi][4 * g + 1], acc[kb][2 * r + nbi][4 * g + 2],
+                    acc[kb][2 * r + nbi][4 * g + 3]};
+    __syncthreads();
+    const int kk = k0 + 128 * wk + 4 * col;
+#pragma unroll 4
+    for (int it = 0; it < 32; ++it) {
+      const int row = 2 * it + hi;
+      const f32x4 v = *(const f32x4*)(E + row * kEpiPitch + 4 * col);
+      const int n = n0 + 128 * wn + 64 * r + row;
+      if (n < N && kk < K) *(VFL_GLOBAL f32x4*)(part + (int64_t)n * P.kp + kk) = v;
+    }
+    __syncthreads();
   }
 }
 
