@@ -647,7 +647,11 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
   p.job_dwb = ly.take(sizeof(DwJob) * (p.s + 1));
   if (p.bgemm) {
     p.job_lin = ly.take(sizeof(LinJob) * (p.s + 1));
-    p.lin_blocks_dx = lin_blocks(p.Ra, p.P.out[0]);
+    // row tiles up to the tick's rows only: the padded rows past them are
+    // zero from the workspace's creation and no launch writes them, and a
+    // 256-row tile more per XCD (Ra = 34048 at hetero) cost a third round
+    // of blocks on the CUs
+    p.lin_blocks_dx = lin_blocks(p.R, p.P.out[0]);
   }
   p.total = (ly.off + 255) / 256 * 256;
   return "";
@@ -889,7 +893,7 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
       g.N = P.out[0]; g.K = P.out[1];
       if (P.relu[0]) { g.mbits = (const uint8_t*)(ws + p.mbits[q][0]); g.ldb = p.ldb[0]; }
       g.out_rc = rcm(c, P.drc[0], P.out[0]);
-      g.tiles_n = (g.N + 255) / 256; g.tiles_m = (p.Ra + 255) / 256;
+      g.tiles_n = (g.N + 255) / 256; g.tiles_m = (p.R + 255) / 256;
       g.rows_pad = p.Ra;
     }
   }
