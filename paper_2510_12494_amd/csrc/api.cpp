@@ -317,16 +317,28 @@ constexpr double kDwtMinFlops = 4e9;
 // element size) contract all their rows in one block per 32 x 32 tile.
 constexpr int kDwUnsplitBytes = 2048;
 
+// Chunks of at least this many rows may be cut at any 32-row stage.
+constexpr int kDwtFineRows = 1024;
+
 // Row chunks of a weight-gradient launch over `tiles` output tiles: at
 // most kDwBlocks blocks (one round on the CUs: a few blocks past it would
 // double the launch), chunks a multiple of two load groups (kDwRows rows
 // in bf16, half that in float32).
 void dw_split(int R, int tiles, bool bf16, DwMeta& m) {
-  const int gran = bf16 ? kDwRows : kDwRows / 2;
-  const int max_splits = std::max(1, (R + gran - 1) / gran);
-  const int s = std::min(max_splits, std::max(1, kDwBlocks / tiles));
-  m.rps = ((R + s - 1) / s + gran - 1) / gran * gran;
-  m.splits = (R + m.rps - 1) / m.rps;
+  auto split = [&](int gran) {
+    const int max_splits = std::max(1, (R + gran - 1) / gran);
+    const int s = std::min(max_splits, std::max(1, kDwBlocks / tiles));
+    m.rps = ((R + s - 1) / s + gran - 1) / gran * gran;
+    m.splits = (R + m.rps - 1) / m.rps;
+  };
+  split(bf16 ? kDwRows : kDwRows / 2);
+  if (m.tile == 256 && m.rps >= kDwtFineRows) {
+    // long chunks of the large-tile kernel need only whole 32-row stages:
+    // the finer granularity lets them fill the CUs (hetero's B: 14 chunks of
+    // 2368 rows, 252 blocks, instead of 13 of 2560, 234 blocks); short ones
+    // keep the coarser chunks, whose fewer partials shorten the reduction
+    split(32);
+  }
   if (m.tile == 256 && m.splits < 2) {
     // the large-tile kernel writes partials only: two chunks of a multiple
     // of its 32-row stage
