@@ -449,46 +449,123 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
 }
 
 // RC global matrix -> LDS rows (columns below cols; zeros up to the MFMA
-// depth): one lane per chunk (RR rows of one column), one 16-byte load and
-// RR element writes; from the matrix's ReLU bits instead (a byte per chunk)
-// when it has them
+// depth): one lane per chunk (RR rows of one column), one 16-byte load (or
+// a byte of the matrix's ReLU bits when it has them) and RR element writes.
+// Past one chunk per lane, the loads of NB units per lane are issued
+// before their first use (one round trip to HBM per NB units, not per
+// unit), and bits go a lane per 4 chunks (one 4-byte load, an 8-byte write
+// per row).  Blocks with at most one chunk per lane keep the one-chunk
+// loop (narrow masks: there the batched form was slower beside the other
+// party's kernels).
 template <typename T, int BR>
 __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE, KS = Ch<T>::KS;
+  constexpr int NB = 4;                       // units whose loads are in flight together
   const int cw = (cols + KS - 1) / KS * KS;   // columns up to the MFMA depth
   const VFL_GLOBAL char* g = glb((const char*)m.p);
   const int64_t cp = m.cp;
   const VFL_GLOBAL uint8_t* bits = glb((const uint8_t*)m.bits);
-  for (int u = threadIdx.x; u < (BR / RR) * cw; u += kNT) {
-    const int rg = u / cw, c = u - rg * cw;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    const bool in_m = m.rows == 0 || r0 + rg * RR < m.rows;
-    if constexpr (RR == 8) {
-      if (bits) {
-        // the chunk's ReLU bits: bit i set for a positive row i (written
-        // as a bf16 one, which the mask test reads as positive)
-        if (c < cols && in_m) {
-          const uint32_t byte = bits[(int64_t)(r0 / RR + rg) * m.ldb + c];
+  const int rg_last = m.rows > 0 ? max(m.rows / RR - 1, 0) : (1 << 30);
+  const int units = (BR / RR) * cw;
+  if constexpr (RR == 8) {
+    if (bits && units > kNT) {
+      // the ReLU bits: a lane takes 4 columns of a row group (one 4-byte
+      // load, byte j = column c + j, bit i = row i), written as bf16 ones
+      // (which the mask test reads as positive), 8 bytes per LDS row
+      const int nc4 = cw / 4, nu = (BR / RR) * nc4;
+      for (int u0 = threadIdx.x; u0 < nu; u0 += NB * kNT) {
+        uint32_t wv[NB];
 #pragma unroll
-          for (int w = 0; w < 4; ++w)
-            v[w] = ((byte >> (2 * w)) & 1u ? 0x3f80u : 0u) | ((byte >> (2 * w + 1)) & 1u ? 0x3f800000u : 0u);
+        for (int i = 0; i < NB; ++i) {
+          const int u = min(u0 + i * kNT, nu - 1);
+          const int rg = u / nc4, c = 4 * (u - rg * nc4);
+          wv[i] = *(const VFL_GLOBAL uint32_t*)(bits + (int64_t)min(r0 / RR + rg, rg_last) * m.ldb + c);
         }
-      } else if (c < cols && in_m) {
-        v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int u = u0 + i * kNT;
+          if (u >= nu) continue;
+          const int rg = u / nc4, c = 4 * (u - rg * nc4);
+          const bool in_m = m.rows == 0 || r0 + rg * RR < m.rows;
+          uint32_t w = in_m ? wv[i] : 0u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (c + j >= cols) w &= ~(0xffu << (8 * j));
+          char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
+#pragma unroll
+          for (int r = 0; r < 8; ++r) {
+            uint2 q;
+            q.x = ((w >> r) & 1u ? 0x3f80u : 0u) | ((w >> (8 + r)) & 1u ? 0x3f800000u : 0u);
+            q.y = ((w >> (16 + r)) & 1u ? 0x3f80u : 0u) | ((w >> (24 + r)) & 1u ? 0x3f800000u : 0u);
+            *(uint2*)(dst + r * b.pitch) = q;
+          }
+        }
       }
-    } else if (c < cols && in_m) {
-      v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+      return;
     }
-    char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
-    if constexpr (RR == 8) {
+  }
+  if (units <= kNT) {
+    // at most one chunk per lane: a chunk of RC data or of bits each
+    const int u = threadIdx.x;
+    if (u < units) {
+      const int rg = u / cw, c = u - rg * cw;
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (c < cols && (m.rows == 0 || r0 + rg * RR < m.rows)) {
+        if constexpr (RR == 8) {
+          if (bits) {
+            const uint32_t byte = bits[(int64_t)(r0 / RR + rg) * m.ldb + c];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        *(uint16_t*)(dst + (2 * w) * b.pitch) = (uint16_t)(v[w] & 0xffffu);
-        *(uint16_t*)(dst + (2 * w + 1) * b.pitch) = (uint16_t)(v[w] >> 16);
+            for (int w = 0; w < 4; ++w)
+              v[w] = ((byte >> (2 * w)) & 1u ? 0x3f80u : 0u) | ((byte >> (2 * w + 1)) & 1u ? 0x3f800000u : 0u);
+          } else {
+            v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+          }
+        } else {
+          v = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)(r0 / RR + rg) * cp + c) * 16);
+        }
       }
-    } else {
+      char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
+      if constexpr (RR == 8) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) *(uint32_t*)(dst + w * b.pitch) = v[w];
+        for (int w = 0; w < 4; ++w) {
+          *(uint16_t*)(dst + (2 * w) * b.pitch) = (uint16_t)(v[w] & 0xffffu);
+          *(uint16_t*)(dst + (2 * w + 1) * b.pitch) = (uint16_t)(v[w] >> 16);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) *(uint32_t*)(dst + w * b.pitch) = v[w];
+      }
+    }
+    return;
+  }
+  // the RC chunks, several per lane: batches of NB 16-byte loads
+  const int nu = units;
+  for (int u0 = threadIdx.x; u0 < nu; u0 += NB * kNT) {
+    u32x4 v[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int u = min(u0 + i * kNT, nu - 1);
+      const int rg = u / cw, c = min(u - rg * cw, cols - 1);
+      v[i] = *(const VFL_GLOBAL u32x4*)(g + ((int64_t)min(r0 / RR + rg, rg_last) * cp + c) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int u = u0 + i * kNT;
+      if (u >= nu) continue;
+      const int rg = u / cw, c = u - rg * cw;
+      const bool ok = c < cols && (m.rows == 0 || r0 + rg * RR < m.rows);
+      const u32x4 x = ok ? v[i] : u32x4{0u, 0u, 0u, 0u};
+      char* dst = s + b.off + rg * RR * b.pitch + c * (int)sizeof(T);
+      if constexpr (RR == 8) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          *(uint16_t*)(dst + (2 * w) * b.pitch) = (uint16_t)(x[w] & 0xffffu);
+          *(uint16_t*)(dst + (2 * w + 1) * b.pitch) = (uint16_t)(x[w] >> 16);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) *(uint32_t*)(dst + w * b.pitch) = x[w];
+      }
     }
   }
 }
@@ -535,6 +612,35 @@ __device__ __forceinline__ void load_input(char* s, const RowInput& in, const Ch
       }
       idt[(int64_t)f * in.ldi + r0 + r] = id;
     }
+  }
+  if (ne == 0 && in.dense_vec && BR * nch > kNT) {
+    // dense rows only, several chunks per lane: NB chunks per lane in
+    // flight before the first LDS write (one round trip to HBM per NB
+    // chunks; NB grows with the rows per block, so that narrow blocks keep
+    // their register count); chunks past the rows or the width load a valid
+    // chunk of the block's first row and store zero.  (With one chunk per
+    // lane the loop below issues each lane's only load at once anyway.)
+    constexpr int NB = BR / 8 < 8 ? BR / 8 : 8;
+    const int nu = BR * nch;
+    for (int u0 = threadIdx.x; u0 < nu; u0 += NB * kNT) {
+      u32x4 v[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int u = u0 + i * kNT, r = u / nch, c0 = (u % nch) * CE;
+        const bool ok = u < nu && r < rv && c0 < din;
+        const int64_t row = k.in_off + r0 + (ok ? r : 0);
+        v[i] = __builtin_nontemporal_load((const VFL_GLOBAL u32x4*)(dense + row * cc.ld + (ok ? c0 : 0)));
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int u = u0 + i * kNT, r = u / nch, ch = u % nch, c0 = ch * CE;
+        if (u >= nu) continue;
+        const bool ok = r < rv && c0 < din;
+        *(u32x4*)(s + in.buf.off + r * in.buf.pitch + ch * 16) =
+            ok ? mask_tail<T>(v[i], din - c0) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    return;
   }
   for (int u = threadIdx.x; u < BR * nch; u += kNT) {
     const int r = u / nch, ch = u % nch, c0 = ch * CE;
