@@ -627,6 +627,30 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
     return "party A's and the top model's widths exceed the LDS of one workgroup";
   if (!pick_rt(p.R, p.kb, [&](int BR) { BwdLds x; plan_bwd_lds(p, BR, x); return x.bytes; }))
     return "party B's widths exceed the LDS of one workgroup";
+  {
+    // B's backward starts every block with its loads (ReLU masks, gradient
+    // message, stashed output): 32-row blocks when two of them fit one CU's
+    // LDS and the larger pick would not, so that one block's loads overlap
+    // the other's products.  Only where B's stream carries most of the
+    // tick's work (its bottom has over twice the per-row MACs of A's bottom
+    // and the top model): two backward blocks per CU leave no room beside
+    // them for A's kernels, which would otherwise be the longer stream.
+    auto macs = [](const Party& q) {
+      double m = 0;
+      for (int l = 0; l < q.L; ++l) m += (double)q.in[l] * q.out[l];
+      return m;
+    };
+    double macs_a = macs(p.A);
+    for (int j = 0; j < T.H; ++j) macs_a += (double)T.in[j] * T.out[j];
+    BwdLds two, cur;
+    plan_bwd_lds(p, 32, two);
+    plan_bwd_lds(p, 16 * p.kb.rt, cur);
+    if (p.kb.rt > 2 && 2 * two.bytes <= kLdsMax && 2 * cur.bytes > kLdsMax && macs(p.P) > 2 * macs_a) {
+      p.kb.rt = 2;
+      p.kb.blocks = (p.R + 31) / 32;
+      p.kb.lds = two.bytes;
+    }
+  }
   plan_fwd_lds(p, 16 * p.kf.rt, p.lf);
   plan_act_lds(p, 16 * p.ka.rt, gextra, p.la);
   plan_bwd_lds(p, 16 * p.kb.rt, p.lb);
