@@ -274,6 +274,9 @@ def main():
     ap.add_argument("--steps", type=int, default=2400)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="hetero")
+    ap.add_argument("--id-stride", type=int, default=1,
+                    help="categorical ids k * stride mod vocab (a stride coprime with the vocabulary "
+                         "scatters the frequent ids, as hashed ids would)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -315,6 +318,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     w = S.get(args.workload)
+    if args.id_stride != 1:
+        w = w.replace(id_stride=args.id_stride)
     data = S.generate(w)
     params = S.init_params(w)
     if args.semi_async:
@@ -396,7 +401,8 @@ def main():
                    "replicas": w.replicas, "staleness": w.staleness,
                    "bottom_A": "-".join(map(str, [w.A.d_in] + w.A.widths)),
                    "bottom_B": "-".join(map(str, [w.B.d_in] + w.B.widths)),
-                   "top": "-".join(map(str, [w.top_in] + w.top.widths)), "lr": w.lr},
+                   "top": "-".join(map(str, [w.top_in] + w.top.widths)), "lr": w.lr,
+                   **({"id_stride": w.id_stride} if w.id_stride != 1 else {})},
         "roofline": roof,
         "kernel_classes_us_per_step_serial": {k: 1e3 * v[0] for k, v in probe.items() if v[1]},
         "graph_ticks": cyc,

@@ -289,20 +289,23 @@ def test_odd_shapes(dtype, s, k, clip):
     _full_check(run, w)
 
 
-@pytest.mark.parametrize("zipf_a,vocab,shift", [(30.0, 5, 0), (1.1, 3000, 0), (30.0, 40, 17)])
-def test_table_sgd_segments(zipf_a, vocab, shift):
+@pytest.mark.parametrize("zipf_a,vocab,shift,stride", [(30.0, 5, 0, 1), (1.1, 3000, 0, 1), (30.0, 40, 17, 1),
+                                                      (1.1, 3000, 0, 1009)])
+def test_table_sgd_segments(zipf_a, vocab, shift, stride):
     """Sparse table SGD at its extremes: 10,000 rows per tick (two passes of
     the per-field key collection), and either (zipf_a = 30) every sample of
     a field on one id, below 16 (a hot-id workgroup's sum over all rows) or
     at 17 (one id part: the 32-keys-per-thread sort and a segment spanning
     every staged block of both passes, while most parts stay empty), or a
-    spread of ids with repeats across parts and hot ids."""
+    spread of ids with repeats across parts and hot ids, also with the Zipf
+    ranks scattered over the ids (stride 1009, as hashed ids would be: the
+    frequent ids are no longer the low ones the hot-id workgroups take).""" 
     w = Workload(name="tables", n_rows=20000, dtype="f32",
                  A=PartySpec(dense=7, n_cat=2, vocab=vocab, emb_dim=16, widths=[24, 16]),
                  B=PartySpec(dense=0, n_cat=3, vocab=vocab, emb_dim=8, widths=[20, 8]),
                  top=TopSpec(widths=[12, 1]), batch=5000, staleness=1, replicas=2, lr=0.5,
-                 labels="bernoulli", label_p=0.4, zipf_a=zipf_a, id_shift=shift, data_seed=81,
-                 init_seed=82, noise_seed=83)
+                 labels="bernoulli", label_p=0.4, zipf_a=zipf_a, id_shift=shift, id_stride=stride,
+                 data_seed=81, init_seed=82, noise_seed=83)
     run = H.Run(w, w.n_rows, 2)
     o, recs = run.oracle("f64")
     _check_ints(run, o, recs)

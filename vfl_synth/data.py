@@ -75,7 +75,7 @@ def generate(w: Workload, n_rows: int | None = None) -> dict:
             for c, lo, hi in _chunks(n):
                 u = _rng(w.data_seed, c, pid, 1).random((hi - lo, spec.n_cat))
                 k = np.minimum(np.searchsorted(cdf, u, side="right"), spec.vocab - 1)
-                ids[lo:hi] = (k + w.id_shift) % spec.vocab
+                ids[lo:hi] = (k.astype(np.int64) * w.id_stride + w.id_shift) % spec.vocab
             out[key] = ids
     out["y"] = _labels(w, out, n)
     return out

@@ -86,7 +86,8 @@ class Workload:
     loss: str = "bce"        # "bce" (Eq. 1 on a logit) | "mse" (squared error on a prediction)
     label_p: float = 0.25
     zipf_a: float = 1.1
-    id_shift: int = 0        # ids (k + id_shift) mod vocab: moves the hot ids
+    id_shift: int = 0        # ids (k * id_stride + id_shift) mod vocab: moves the hot ids
+    id_stride: int = 1       # coprime with vocab: scatters the Zipf ranks over the ids (hashed ids)
     data_seed: int = 0
     init_seed: int = 0
     noise_seed: int = 0
