@@ -134,7 +134,8 @@ struct ActLds {
 };
 struct BwdLds { LBuf P[2], mask[VFL_MAX_LAYERS]; int bytes = 0; };
 
-struct KMeta { int rt = 1, blocks = 1, lds = 0; };
+struct KMeta { int rt = 1, blocks = 1, lds = 0, pf = kChainPFNarrow; };
+constexpr size_t kPFWideElts = 256 * 1024;   // chain weights taking the deeper load groups
 
 // Weight-gradient launch shape of a party: tile 32 (one unsplit launch,
 // k_dw32) or 64 (row chunks, k_dw + k_dw_reduce).
@@ -650,6 +651,25 @@ std::string build_plan(const vfl_bottom_spec* a, const vfl_bottom_spec* b, const
       p.kb.blocks = (p.R + 31) / 32;
       p.kb.lds = two.bytes;
     }
+  }
+  {
+    // deeper weight load groups for bf16 chains whose weights are large
+    // (hetero's B, ten 256-wide layers): there they keep the L2 stream busy,
+    // while small chains run faster with the shallower groups (the forward
+    // of 64 -> 256 -> 128 at 16384 rows: 36 -> 26 us).  B's backward takes
+    // the deeper groups only through more than three such layers: hetero's
+    // three-layer backward runs faster with the shallow ones (42 -> 40 us),
+    // the ten-layer one of 256-wide layers slower (tick 265 -> 278 us).
+    auto welts = [](const Party& P) {
+      size_t n = 0;
+      for (int l = 0; l < P.L; ++l) n += (size_t)P.in[l] * P.out[l];
+      return n;
+    };
+    size_t wa = welts(p.A);
+    for (int j = 0; j < p.T.H; ++j) wa += (size_t)p.T.in[j] * p.T.out[j];
+    if (p.e == BF16 && welts(p.P) >= kPFWideElts) p.kf.pf = kChainPFWide;
+    if (p.e == BF16 && wa >= kPFWideElts) p.ka.pf = kChainPFWide;
+    if (p.e == BF16 && welts(p.P) >= kPFWideElts && p.P.L > 3) p.kb.pf = kChainPFWide;
   }
   plan_fwd_lds(p, 16 * p.kf.rt, p.lf);
   plan_act_lds(p, 16 * p.ka.rt, gextra, p.la);
@@ -1237,7 +1257,8 @@ vfl_status b_forward(vfl_ctx* c, int slot, const SlotState& st, TickRef tr) {
   const int32_t hdr[3] = {(int32_t)st.group, (int32_t)st.group, (int32_t)st.version};
   const ChainCall k = call_of(st, st.group, hdr, 0);
   TIMED(VFL_K_FWD, party_fwd_flops(p.P, p.R), c->sb,
-        launch_fwd(p.e, p.kf.rt, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k, tr, c->sb));
+        launch_fwd(p.e, p.kf.rt, p.kf.pf, (const FwdJob*)(c->ws + p.job_fwd) + slot, p.kf.lds, p.kf.blocks, k,
+                   tr, c->sb));
   return VFL_OK;
 }
 
@@ -1260,7 +1281,7 @@ vfl_status a_top(vfl_ctx* c, int64_t group, int slot, const SlotState& st, int32
   for (int j = 0; j < p.T.H; ++j) f += mm_flops(R, p.T.out[j], p.T.in[j]);
   for (int j = 1; j < p.T.H; ++j) f += mm_flops(R, p.T.in[j], p.T.out[j]);
   TIMED(VFL_K_ACTIVE, f, c->sa,
-        launch_active(p.e, p.ka.rt, (const ActiveJob*)(c->ws + p.job_act) + slot, p.ka.lds, p.ka.blocks, k,
+        launch_active(p.e, p.ka.rt, p.ka.pf, (const ActiveJob*)(c->ws + p.job_act) + slot, p.ka.lds, p.ka.blocks, k,
                       tr, c->sa));
   HIPCHK(hipEventRecord(c->ev_grad[slot], c->sa));
   return VFL_OK;
@@ -1283,7 +1304,7 @@ vfl_status b_backward(vfl_ctx* c, int slot, const SlotState& st, int64_t group, 
   const ChainCall k = call_of(st, group, nullptr, group);
   const double gf = p.bgemm ? mm_flops(p.R, p.P.out[0], p.P.out[1]) : 0.0;
   TIMED(VFL_K_BWD, party_dx_flops(p.P, p.R) - gf, c->sb,
-        launch_bwd(p.e, p.kb.rt, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
+        launch_bwd(p.e, p.kb.rt, p.kb.pf, (const BwdJob*)(c->ws + p.job_bwd) + slot, p.kb.lds, p.kb.blocks, k, tr, c->sb));
   if (p.bgemm)
     TIMED(VFL_K_GEMM, gf, c->sb,
           launch_lin((const LinJob*)(c->ws + p.job_lin) + slot, p.lin_blocks_dx, st.rows, tr, c->sb));

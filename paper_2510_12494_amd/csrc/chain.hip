@@ -95,18 +95,20 @@ __device__ __forceinline__ void st8(char* p, const float (&v)[8]) {
 constexpr int kNW = kChainWaves;    // wavefronts per block (two per SIMD)
 constexpr int kNT = 64 * kNW;        // threads per block
 constexpr int kNTW = 2;              // 16-column output tiles per wavefront and pass
-constexpr int kPF = 4;               // MFMA steps per weight load group
+constexpr int kPFNarrow = kChainPFNarrow;   // MFMA steps per weight load group
+constexpr int kPFWide = kChainPFWide;
 constexpr int kLogitChunks = kMaxLogitCols / 256;   // 4-column chunks per lane in the logit stage
 
-// Weight-fragment registers of a chain: two load groups of kPF MFMA steps
+// Weight-fragment registers of a chain: two load groups of PF MFMA steps
 // (ping-pong).  The groups of a chain's products form one stream: when a
 // wavefront has issued the loads of a pass's last group, the next two loads
 // it issues are groups 0 and 1 of the next pass or of the next product, so
 // a product starts with both of its first groups already in flight.  A
 // pass has an even number of groups (steps past K are skipped), so every
 // pass starts in `wa`.
+template <int PF>
 struct Pipe {
-  u32x4 wa[kPF][kNTW], wb[kPF][kNTW];
+  u32x4 wa[PF][kNTW], wb[PF][kNTW];
 };
 
 // The RC copy of a stage's LDS output (lds_to_rc of b's first cols columns
@@ -157,14 +159,15 @@ __device__ __forceinline__ int tiles_of(int N) {
 // operand's last are clamped to it, steps past K to its last step (never
 // used; re-reading lines already fetched keeps them off the L2, and a
 // conditional load would make the compiler wait for it on the spot).
+template <int PF>
 __device__ __forceinline__ void wgroup(const void* Wp, int kst, int ntl, const int (&tile)[kNTW], int g,
-                                       u32x4 (&d)[kPF][kNTW]) {
+                                       u32x4 (&d)[PF][kNTW]) {
   const uint32_t lo = (threadIdx.x & 63) * 16;
 #pragma unroll
   for (int j = 0; j < kNTW; ++j) {
     const VFL_GLOBAL char* base = glb((const char*)Wp) + (int64_t)min(tile[j], ntl - 1) * kst * 1024 + lo;
 #pragma unroll
-    for (int q = 0; q < kPF; ++q) d[q][j] = *(const VFL_GLOBAL u32x4*)(base + (int64_t)min(g * kPF + q, kst - 1) * 1024);
+    for (int q = 0; q < PF; ++q) d[q][j] = *(const VFL_GLOBAL u32x4*)(base + (int64_t)min(g * PF + q, kst - 1) * 1024);
   }
 }
 
@@ -176,8 +179,8 @@ __device__ __forceinline__ void pass_tiles(int pass, int (&tile)[kNTW]) {
 }
 
 // start the loads of groups 0 and 1 of L's first pass
-template <typename T>
-__device__ __forceinline__ void prefetch(const ChainLayer* L, Pipe& p) {
+template <typename T, int PF>
+__device__ __forceinline__ void prefetch(const ChainLayer* L, Pipe<PF>& p) {
   int tile[kNTW];
   pass_tiles(0, tile);
   const VFL_CONST ChainLayer& C = cst(*(const ChainLayer*)uniform_ptr(L));
@@ -230,10 +233,10 @@ __device__ __forceinline__ void lds_to_rc_(const char* s, const LBuf& b, int col
 template <typename T, int BR>
 __device__ __forceinline__ void lds_to_rc_hint(const char* s, const LBuf& b, int cols, const RCMat& m, int r0);
 
-template <typename T, int RT, typename Epi, bool HINT = false>
-__device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe& p,
+template <typename T, int RT, typename Epi, bool HINT = false, int PF>
+__device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pipe<PF>& p,
                                          const ChainLayer* next, const RcPend& pend, Epi&& epi) {
-  constexpr int PF = kPF, NTW = kNTW;
+  constexpr int NTW = kNTW;
   const int lane = threadIdx.x & 63;
   const int kc = lane >> 4, lr = lane & 15;
   const VFL_CONST ChainLayer& C = cst(L);
@@ -326,8 +329,8 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
 }
 
 // Forward or input-gradient layer into LDS (see ChainLayer).
-template <typename T, int RT, bool HINT = false>
-__device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe& p,
+template <typename T, int RT, bool HINT = false, int PF>
+__device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe<PF>& p,
                                           const ChainLayer* next, const RcPend& pend) {
   const int N = L.N;
   const bool relu = L.relu != 0, msk = L.mask.pitch > 0, nopad = L.nopad != 0;
@@ -354,9 +357,9 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
 
 // Input gradient of the embedding columns of a bottom input: float32 rows
 // of gx (block rows below rv).
-template <typename T, int RT>
+template <typename T, int RT, int PF>
 __device__ __forceinline__ void run_gx(const char* s, const ChainLayer& L, float* gx, int64_t ldgx,
-                                       int r0, int rv, Pipe& p, const RcPend& pend) {
+                                       int r0, int rv, Pipe<PF>& p, const RcPend& pend) {
   const int N = L.N;
   VFL_GLOBAL float* gxg = glb(gx);
   block_mm<T, RT>(s, L, p, nullptr, pend, [&](int r, int n, const f32x4& a, const f32x4&) {
@@ -765,7 +768,7 @@ __device__ __forceinline__ void msg_rows(const char* s, const LBuf& src, int D, 
 }
 
 // ------------------------------------------------------------------ kernels
-template <typename T, int RT>
+template <typename T, int RT, int PF>
 __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, ChainCall cc,
                                              TickRef tr) {
   constexpr int BR = 16 * RT;
@@ -780,7 +783,7 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
   const int r0 = blockIdx.x * BR;
   if (r0 >= k.rows) return;
   const int rv = min(BR, k.rows - r0);
-  Pipe pp;
+  Pipe<PF> pp;
   prefetch<T>(&j.l[0], pp);   // overlaps the input rows' loads
   const uint32_t wx = warm_l2(j.warm, jp);
   copy_bias(s, j.bt);
@@ -802,7 +805,7 @@ __global__ __launch_bounds__(kNT) void k_fwd(const FwdJob* __restrict__ jp, Chai
                        j.cfac, r0, rv);
 }
 
-template <typename T, int RT>
+template <typename T, int RT, int PF>
 __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp, ChainCall cc,
                                                 TickRef tr) {
   constexpr int BR = 16 * RT;
@@ -854,8 +857,8 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
     py = y[min((int)threadIdx.x, rv - 1)];
   }
   const float lbias = glb(j.lb)[0];
-  Pipe pp;
-  prefetch<T>(&j.fa[0], pp);
+  Pipe<PF> pp;
+  prefetch<T, PF>(&j.fa[0], pp);
   const uint32_t wx = warm_l2(j.warm, jp);
   copy_bias(s, j.bt);
 
@@ -1076,7 +1079,7 @@ __global__ __launch_bounds__(kNT) void k_active(const ActiveJob* __restrict__ jp
   else if (pend.m.p) lds_to_rc<T, BR>(s, pend.b, pend.cols, pend.m, r0);
 }
 
-template <typename T, int RT>
+template <typename T, int RT, int PF>
 __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, ChainCall cc,
                                              TickRef tr) {
   constexpr int BR = 16 * RT;
@@ -1095,8 +1098,8 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
     return;
   }
   const int rv = min(BR, k.rows - r0);
-  Pipe pp;
-  if (nd > 0 || has_gx) prefetch<T>(nd > 0 ? &j.dx[0] : &j.gx, pp);
+  Pipe<PF> pp;
+  if (nd > 0 || has_gx) prefetch<T, PF>(nd > 0 ? &j.dx[0] : &j.gx, pp);
   const uint32_t wx = warm_l2(j.warm, jp);
   // the ReLU masks of every layer of the chain, each in an LDS buffer of
   // its own (stashed activations of this group's forward)
@@ -1176,55 +1179,66 @@ hipError_t raise_lds(K kernel) {
 
 }  // namespace
 
-#define VFL_CHAIN_DISPATCH(KER, e, rt, ...)                                                   \
+
+#define VFL_PF_RT(K, T, PF, rt, ...)                                                            \
   do {                                                                                       \
-    if (e == BF16) {                                                                         \
-      if (rt == 1) hipLaunchKernelGGL((KER<uint16_t, 1>), __VA_ARGS__);                       \
-      else if (rt == 2) hipLaunchKernelGGL((KER<uint16_t, 2>), __VA_ARGS__);                  \
-      else if (rt == 3) hipLaunchKernelGGL((KER<uint16_t, 3>), __VA_ARGS__);                  \
-      else if (rt == 4) hipLaunchKernelGGL((KER<uint16_t, 4>), __VA_ARGS__);                  \
-      else return hipErrorInvalidValue;                                                      \
-    } else {                                                                                 \
-      if (rt == 1) hipLaunchKernelGGL((KER<float, 1>), __VA_ARGS__);                          \
-      else if (rt == 2) hipLaunchKernelGGL((KER<float, 2>), __VA_ARGS__);                     \
-      else if (rt == 3) hipLaunchKernelGGL((KER<float, 3>), __VA_ARGS__);                     \
-      else if (rt == 4) hipLaunchKernelGGL((KER<float, 4>), __VA_ARGS__);                     \
-      else return hipErrorInvalidValue;                                                      \
-    }                                                                                        \
+    if (rt == 1) hipLaunchKernelGGL((K<T, 1, PF>), __VA_ARGS__);                          \
+    else if (rt == 2) hipLaunchKernelGGL((K<T, 2, PF>), __VA_ARGS__);                     \
+    else if (rt == 3) hipLaunchKernelGGL((K<T, 3, PF>), __VA_ARGS__);                     \
+    else if (rt == 4) hipLaunchKernelGGL((K<T, 4, PF>), __VA_ARGS__);                     \
+    else return hipErrorInvalidValue;                                                        \
   } while (0)
 
-hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
+hipError_t launch_fwd(Elt e, int rt, int pf, const FwdJob* job, int lds, int blocks, const ChainCall& c,
                       TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_fwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  if (pf == kPFWide && e == BF16) VFL_PF_RT(k_fwd, uint16_t, kPFWide, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow && e == BF16) VFL_PF_RT(k_fwd, uint16_t, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow) VFL_PF_RT(k_fwd, float, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
+hipError_t launch_active(Elt e, int rt, int pf, const ActiveJob* job, int lds, int blocks,
                          const ChainCall& c, TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_active, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  if (pf == kPFWide && e == BF16) VFL_PF_RT(k_active, uint16_t, kPFWide, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow && e == BF16) VFL_PF_RT(k_active, uint16_t, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow) VFL_PF_RT(k_active, float, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
+hipError_t launch_bwd(Elt e, int rt, int pf, const BwdJob* job, int lds, int blocks, const ChainCall& c,
                       TickRef tr, hipStream_t st) {
   if (lds > kLdsMax || blocks < 1) return hipErrorInvalidValue;
-  VFL_CHAIN_DISPATCH(k_bwd, e, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  if (pf == kPFWide && e == BF16) VFL_PF_RT(k_bwd, uint16_t, kPFWide, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow && e == BF16) VFL_PF_RT(k_bwd, uint16_t, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else if (pf == kPFNarrow) VFL_PF_RT(k_bwd, float, kPFNarrow, rt, dim3(blocks), dim3(kNT), lds, st, job, c, tr);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t chain_init() {
   const hipError_t r[] = {
-      raise_lds(k_fwd<uint16_t, 1>), raise_lds(k_fwd<uint16_t, 2>), raise_lds(k_fwd<uint16_t, 4>),
-      raise_lds(k_fwd<float, 1>), raise_lds(k_fwd<float, 2>), raise_lds(k_fwd<float, 4>),
-      raise_lds(k_fwd<uint16_t, 3>), raise_lds(k_fwd<float, 3>),
-      raise_lds(k_active<uint16_t, 1>), raise_lds(k_active<uint16_t, 2>), raise_lds(k_active<uint16_t, 4>),
-      raise_lds(k_active<float, 1>), raise_lds(k_active<float, 2>), raise_lds(k_active<float, 4>),
-      raise_lds(k_active<uint16_t, 3>), raise_lds(k_active<float, 3>),
-      raise_lds(k_bwd<uint16_t, 1>), raise_lds(k_bwd<uint16_t, 2>), raise_lds(k_bwd<uint16_t, 4>),
-      raise_lds(k_bwd<float, 1>), raise_lds(k_bwd<float, 2>), raise_lds(k_bwd<float, 4>),
-      raise_lds(k_bwd<uint16_t, 3>), raise_lds(k_bwd<float, 3>)};
+      raise_lds(k_fwd<uint16_t, 1, kPFNarrow>), raise_lds(k_fwd<uint16_t, 2, kPFNarrow>),
+      raise_lds(k_fwd<uint16_t, 3, kPFNarrow>), raise_lds(k_fwd<uint16_t, 4, kPFNarrow>),
+      raise_lds(k_fwd<uint16_t, 1, kPFWide>), raise_lds(k_fwd<uint16_t, 2, kPFWide>),
+      raise_lds(k_fwd<uint16_t, 3, kPFWide>), raise_lds(k_fwd<uint16_t, 4, kPFWide>),
+      raise_lds(k_fwd<float, 1, kPFNarrow>), raise_lds(k_fwd<float, 2, kPFNarrow>),
+      raise_lds(k_fwd<float, 3, kPFNarrow>), raise_lds(k_fwd<float, 4, kPFNarrow>),
+      raise_lds(k_active<uint16_t, 1, kPFNarrow>), raise_lds(k_active<uint16_t, 2, kPFNarrow>),
+      raise_lds(k_active<uint16_t, 3, kPFNarrow>), raise_lds(k_active<uint16_t, 4, kPFNarrow>),
+      raise_lds(k_active<uint16_t, 1, kPFWide>), raise_lds(k_active<uint16_t, 2, kPFWide>),
+      raise_lds(k_active<uint16_t, 3, kPFWide>), raise_lds(k_active<uint16_t, 4, kPFWide>),
+      raise_lds(k_active<float, 1, kPFNarrow>), raise_lds(k_active<float, 2, kPFNarrow>),
+      raise_lds(k_active<float, 3, kPFNarrow>), raise_lds(k_active<float, 4, kPFNarrow>),
+      raise_lds(k_bwd<uint16_t, 1, kPFNarrow>), raise_lds(k_bwd<uint16_t, 2, kPFNarrow>),
+      raise_lds(k_bwd<uint16_t, 3, kPFNarrow>), raise_lds(k_bwd<uint16_t, 4, kPFNarrow>),
+      raise_lds(k_bwd<uint16_t, 1, kPFWide>), raise_lds(k_bwd<uint16_t, 2, kPFWide>),
+      raise_lds(k_bwd<uint16_t, 3, kPFWide>), raise_lds(k_bwd<uint16_t, 4, kPFWide>),
+      raise_lds(k_bwd<float, 1, kPFNarrow>), raise_lds(k_bwd<float, 2, kPFNarrow>),
+      raise_lds(k_bwd<float, 3, kPFNarrow>), raise_lds(k_bwd<float, 4, kPFNarrow>)};
   for (hipError_t x : r)
     if (x != hipSuccess) return x;
   const hipError_t d = dwt_init();

@@ -42,6 +42,8 @@ constexpr int kMaxDw = 16;            // weight-gradient problems per launch
 constexpr int kMaxLogitCols = 512;    // widest last hidden layer of the top model
 constexpr int kLdsMax = 160 * 1024;   // LDS of one gfx950 workgroup
 constexpr int kChainWaves = 8;        // wavefronts per chain-kernel block
+constexpr int kChainPFNarrow = 2;     // MFMA steps per chain weight load group
+constexpr int kChainPFWide = 4;       // the same for bf16 chains with large weights
 
 // The values of one tick of the deterministic schedule over a resident
 // dataset of n_rows rows (group g covers rows [(g mod E) * R, ...), E =
@@ -279,11 +281,13 @@ struct BwdJob {
 
 // Jobs live in device memory (written once when the context is created);
 // `rt` selects 16 * rt rows per block, `lds` the dynamic LDS bytes.
-hipError_t launch_fwd(Elt e, int rt, const FwdJob* job, int lds, int blocks, const ChainCall& c,
+// pf: MFMA steps per weight load group of the chain kernel,
+// kChainPFNarrow, or kChainPFWide for bf16
+hipError_t launch_fwd(Elt e, int rt, int pf, const FwdJob* job, int lds, int blocks, const ChainCall& c,
                       TickRef tr, hipStream_t st);
-hipError_t launch_active(Elt e, int rt, const ActiveJob* job, int lds, int blocks,
+hipError_t launch_active(Elt e, int rt, int pf, const ActiveJob* job, int lds, int blocks,
                          const ChainCall& c, TickRef tr, hipStream_t st);
-hipError_t launch_bwd(Elt e, int rt, const BwdJob* job, int lds, int blocks, const ChainCall& c,
+hipError_t launch_bwd(Elt e, int rt, int pf, const BwdJob* job, int lds, int blocks, const ChainCall& c,
                       TickRef tr, hipStream_t st);
 // Raise the dynamic-LDS limit of every chain kernel to kLdsMax.
 hipError_t chain_init();

@@ -10,9 +10,9 @@ namespace vfl {
 static hipError_t no_gpu() { return hipErrorNotSupported; }
 hipError_t launch_tick_base(TickSrc*, int, hipStream_t) { return no_gpu(); }
 hipError_t launch_tick_set(TickSrc*, const TickSrc&, hipStream_t) { return no_gpu(); }
-hipError_t launch_fwd(Elt, int, const FwdJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
-hipError_t launch_active(Elt, int, const ActiveJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
-hipError_t launch_bwd(Elt, int, const BwdJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
+hipError_t launch_fwd(Elt, int, int, const FwdJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
+hipError_t launch_active(Elt, int, int, const ActiveJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
+hipError_t launch_bwd(Elt, int, int, const BwdJob*, int, int, const ChainCall&, TickRef, hipStream_t) { return no_gpu(); }
 hipError_t chain_init() { return no_gpu(); }
 hipError_t launch_dw(Elt, const DwJob*, int, int, float, TickRef, hipStream_t) { return no_gpu(); }
 hipError_t dwt_init() { return no_gpu(); }
