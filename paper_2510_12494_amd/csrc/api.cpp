@@ -412,8 +412,8 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
   b.bytes = l.off;
 }
 
-// Rows per block: the largest of 64, 32, 16 whose layout fits the LDS and
-// that still gives kMinBlocks blocks (16 when nothing gives that many).
+// Rows per block: the largest of 64, 48, 32, 16 whose layout fits the LDS
+// and that still gives kMinBlocks blocks (16 when nothing gives that many).
 template <typename F>
 bool pick_rt(int R, KMeta& m, F&& bytes_at) {
   for (int rt : {4, 3, 2, 1}) {
