@@ -406,9 +406,19 @@ void plan_bwd_lds(const Plan& p, int BR, BwdLds& b) {
   for (int i = lo; i < p.P.L; ++i) w[(p.P.L - 1 - i) % 2] = std::max(w[(p.P.L - 1 - i) % 2], p.P.out[i]);
   b.P[0] = l.take(w[0], es);
   b.P[1] = l.take(w[1], es);
-  // one mask buffer per ReLU layer the chain crosses: all are loaded up front
-  for (int i = lo; i + 1 < p.P.L; ++i)
-    if (p.P.relu[i]) b.mask[i] = l.take(p.P.out[i], es);
+  // one mask buffer per ReLU layer the chain crosses: all are loaded up
+  // front; bf16 keeps the bits B's forward recorded (a byte per 8 rows and
+  // column), float32 the stashed activations
+  for (int i = lo; i + 1 < p.P.L; ++i) {
+    if (!p.P.relu[i]) continue;
+    if (p.e == BF16) {
+      const int pitch = p.ldb[i] + 16;
+      b.mask[i] = l.raw(BR / 8 * pitch);
+      b.mask[i].pitch = pitch;
+    } else {
+      b.mask[i] = l.take(p.P.out[i], es);
+    }
+  }
   b.bytes = l.off;
 }
 
@@ -750,7 +760,16 @@ bool layer_fits(const Plan& p, const ChainLayer& L, int BR, int lds, bool lds_ou
   if (L.bl >= 0 && (L.bl % 16 || L.bl + 4 * ((L.N + 31) / 32 * 32) > lds)) return false;
   if (!inside(L.in, L.K)) return false;
   if (lds_out && !inside(L.out, out_cols < 0 ? L.N : out_cols)) return false;
-  if (L.mask.pitch && !inside(L.mask, L.N)) return false;
+  if (L.mask.pitch && L.mask_bits) {
+    // a byte per 8 rows and column, copied 16 columns at a time
+    const int nb = (L.N + 15) / 16 * 16;
+    if (BR % 8 || L.mask.off < 0 || L.mask.off % 16 || L.mask.pitch % 16 || L.mask.pitch < nb ||
+        L.mask.off + L.mask.pitch * (BR / 8) > lds || !L.mask_src.bits || L.mask_src.ldb < nb ||
+        L.mask_src.ldb % 16)
+      return false;
+  } else if (L.mask.pitch && !inside(L.mask, L.N)) {
+    return false;
+  }
   if (L.rc.p && L.rc.cp < ((rc_cols < 0 ? L.N : rc_cols) + 7) / 8 * 8) return false;
   return true;
 }
@@ -929,7 +948,10 @@ std::string build_jobs(const Plan& p, const vfl_opts& o, char* ws, Jobs& J) {
         if (p.mbits[q][l - 1]) {
           L.mask_src.bits = (uint8_t*)(ws + p.mbits[q][l - 1]);
           L.mask_src.ldb = p.ldb[l - 1];
+          L.mask_bits = 1;
         }
+        // bf16 backward kernels read masks only in the byte form
+        if ((p.e == BF16) != (L.mask_bits != 0)) return "party B's backward: bf16 masks without ReLU bits";
       }
       L.rc = rcm(c, P.drc[l - 1], P.out[l - 1]);
     }

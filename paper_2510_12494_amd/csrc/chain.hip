@@ -329,7 +329,8 @@ __device__ __forceinline__ void block_mm(const char* s, const ChainLayer& L, Pip
 }
 
 // Forward or input-gradient layer into LDS (see ChainLayer).
-template <typename T, int RT, bool HINT = false, int PF>
+// MB: the mask (when there is one) is the byte form of the ReLU bits
+template <typename T, int RT, bool HINT = false, int PF, bool MB = false>
 __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, Pipe<PF>& p,
                                           const ChainLayer* next, const RcPend& pend) {
   const int N = L.N;
@@ -339,7 +340,16 @@ __device__ __forceinline__ void run_layer(char* s, const ChainLayer& L, int rv, 
   // compiles to one exec-mask branch per element)
   auto epi = [&](int r, int n, const f32x4& a, const f32x4& b) {
     float m[4] = {1.f, 1.f, 1.f, 1.f}, v[4];
-    if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
+    if constexpr (MB) {
+      if (msk) {
+        // the 4 columns' bytes of r's row group in one word
+        const uint32_t w = *(const uint32_t*)(s + mk.off + (r >> 3) * mk.pitch + n);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m[i] = (w >> (8 * i + (r & 7))) & 1u ? 1.f : 0.f;
+      }
+    } else {
+      if (msk) ld4<T>(lp(s, mk, r, n * (int)sizeof(T)), m);
+    }
     const bool rok = r < rv;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -460,6 +470,22 @@ __device__ __forceinline__ void zero_rc(const RCMat& m, int cols, int r0) {
 // per row).  Blocks with at most one chunk per lane keep the one-chunk
 // loop (narrow masks: there the batched form was slower beside the other
 // party's kernels).
+// The ReLU bits of a block's BR rows as they are (a byte per 8 rows and
+// column) into b: BR / 8 rows of b.pitch bytes, 16 bytes per lane and load,
+// columns up to cols rounded to 16 (within m.ldb).  Row groups past m.rows
+// repeat its last (their rows are past the tick's and never kept).
+template <int BR>
+__device__ __forceinline__ void bits_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
+  const int nc = (cols + 15) / 16;
+  const int rg_last = m.rows > 0 ? max(m.rows / 8 - 1, 0) : (1 << 30);
+  const VFL_GLOBAL uint8_t* bits = glb((const uint8_t*)m.bits);
+  for (int u = threadIdx.x; u < (BR / 8) * nc; u += kNT) {
+    const int rg = u / nc, c = 16 * (u - rg * nc);
+    const u32x4 v = __builtin_nontemporal_load((const VFL_GLOBAL u32x4*)(bits + (int64_t)min(r0 / 8 + rg, rg_last) * m.ldb + c));
+    *(u32x4*)(s + b.off + rg * b.pitch + c) = v;
+  }
+}
+
 template <typename T, int BR>
 __device__ __forceinline__ void rc_to_lds(char* s, const LBuf& b, int cols, const RCMat& m, int r0) {
   constexpr int RR = Ch<T>::CE, KS = Ch<T>::KS;
@@ -1102,9 +1128,13 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
   if (nd > 0 || has_gx) prefetch<T, PF>(nd > 0 ? &j.dx[0] : &j.gx, pp);
   const uint32_t wx = warm_l2(j.warm, jp);
   // the ReLU masks of every layer of the chain, each in an LDS buffer of
-  // its own (stashed activations of this group's forward)
+  // its own (bf16: the ReLU bits of this group's forward as bytes; float32:
+  // its stashed activations)
   for (int q = 0; q < nd; ++q)
-    if (j.dx[q].mask_src.p) rc_to_lds<T, BR>(s, j.dx[q].mask, j.dx[q].N, j.dx[q].mask_src, r0);
+    if (j.dx[q].mask_src.p) {
+      if constexpr (sizeof(T) == 2) bits_to_lds<BR>(s, j.dx[q].mask, j.dx[q].N, j.dx[q].mask_src, r0);
+      else rc_to_lds<T, BR>(s, j.dx[q].mask, j.dx[q].N, j.dx[q].mask_src, r0);
+    }
   // cut-layer backward: through the clip when the row was clipped
   // (d(c v)/dv = c (I - u u^T) with u = v / ||v||), then the ReLU of B's
   // last layer; 16 lanes per row, 4 rows per wavefront at a time
@@ -1158,7 +1188,8 @@ __global__ __launch_bounds__(kNT) void k_bwd(const BwdJob* __restrict__ jp, Chai
   RcPend pend{j.d, j.D, j.d_rc, r0};
   for (int q = 0; q < nd; ++q) {
     const ChainLayer& L = j.dx[q];
-    run_layer<T, RT, true>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr), pend);
+    run_layer<T, RT, true, PF, sizeof(T) == 2>(s, L, rv, pp, q + 1 < nd ? &j.dx[q + 1] : (has_gx ? &j.gx : nullptr),
+                                               pend);
     __syncthreads();
     pend = RcPend{L.out, L.N, L.rc, r0};
   }

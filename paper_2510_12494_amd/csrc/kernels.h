@@ -135,6 +135,10 @@ struct ChainLayer {
   const void* W = nullptr;
   int32_t kst = 0, N = 0, K = 0, relu = 0;
   int32_t bl = -1, nopad = 0;
+  // mask_bits: `mask` holds a byte per 8 rows and column (bit r % 8 of byte
+  // (r / 8) * pitch + column: the ReLU bits as B's forward records them),
+  // else one element per row and column (kept where positive)
+  int32_t mask_bits = 0;
   LBuf in, out, mask;
   RCMat rc, mask_src;
 };
